@@ -1,0 +1,204 @@
+"""WaveRNN oracle -- test infrastructure only.
+
+ctypes wrapper around ``wavernn_oracle.c``: a plain scalar CPU implementation of
+the WaveRNN sampling step (Eq. 2 and the dual softmax of Sec. 2, the masked
+input matrix I*, the coarse-then-fine order of the Fig. 1 caption).  Only the
+tests, ``__graft_entry__.smoke()`` and ``bench.py``'s CPU-baseline leg may use
+it.  It shares no code with the GPU library and never imports it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "wavernn_oracle.c")
+_BUILD = os.path.join(_HERE, "_build")
+_LIB_PATH = os.path.join(_BUILD, "liborc.so")
+_lib = None
+
+N_CLASSES = 256
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, no fp contraction, no fast-math)."""
+    os.makedirs(_BUILD, exist_ok=True)
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < max(
+        os.path.getmtime(_SRC), os.path.getmtime(os.path.join(_HERE, "wavernn_oracle.h"))
+    ):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared", "-std=c11",
+             "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class _Model(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int32), ("Dc", ctypes.c_int32), ("frame_len", ctypes.c_int32),
+                ("B", ctypes.c_int32), ("Dx", ctypes.c_int32)] + [
+        (n, ctypes.POINTER(ctypes.c_float))
+        for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")]
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        _lib = load(build())
+    return _lib
+
+
+def load(path: str):
+    """Load an oracle build (tests load planted-mistake builds this way)."""
+    L = ctypes.CDLL(path)
+    f32, i32, i64, u64 = ctypes.c_float, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+    vp = ctypes.c_void_p
+    for name in ("orc_exp", "orc_sigmoid", "orc_tanh"):
+        getattr(L, name).restype = f32
+        getattr(L, name).argtypes = [f32]
+    L.orc_scale.restype = f32
+    L.orc_scale.argtypes = [ctypes.c_int]
+    L.orc_philox4x64_10.restype = None
+    L.orc_philox4x64_10.argtypes = [vp, vp, vp]
+    L.orc_uniforms.restype = None
+    L.orc_uniforms.argtypes = [u64, u64, i64, ctypes.POINTER(f32), ctypes.POINTER(f32)]
+    L.orc_draw.restype = ctypes.c_int
+    L.orc_draw.argtypes = [vp, ctypes.c_int, f32]
+    L.orc_run.restype = ctypes.c_int
+    L.orc_run.argtypes = [ctypes.POINTER(_Model), i32, i64, i64, vp, i64, u64, vp, vp, vp, vp, vp,
+                          vp, vp, vp]
+    return L
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def exp(y: float) -> float:
+    return lib().orc_exp(y)
+
+
+def sigmoid(x: float) -> float:
+    return lib().orc_sigmoid(x)
+
+
+def tanh(x: float) -> float:
+    return lib().orc_tanh(x)
+
+
+def scale(v: int) -> float:
+    return lib().orc_scale(v)
+
+
+def philox4x64_10(ctr, key):
+    c = np.asarray(ctr, dtype=np.uint64).copy()
+    k = np.asarray(key, dtype=np.uint64).copy()
+    out = np.zeros(4, dtype=np.uint64)
+    lib().orc_philox4x64_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def uniforms(seed: int, stream: int, t: int):
+    uc, uf = ctypes.c_float(), ctypes.c_float()
+    lib().orc_uniforms(seed, stream, t, ctypes.byref(uc), ctypes.byref(uf))
+    return uc.value, uf.value
+
+
+def draw(z, u: float) -> int:
+    z = np.ascontiguousarray(z, dtype=np.float32)
+    return lib().orc_draw(_p(z), len(z), u)
+
+
+def bf16_round(a: np.ndarray) -> np.ndarray:
+    """fp32 -> nearest bf16 value (ties to even), returned widened to fp32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    bits = a.view(np.uint32).astype(np.uint64)
+    bias = ((bits >> 16) & 1) + 0x7FFF
+    r = ((bits + bias) >> 16) << 16
+    nan = np.isnan(a)
+    out = r.astype(np.uint32).view(np.float32).copy()
+    out[nan] = a[nan]
+    return out
+
+
+@dataclass
+class Weights:
+    """fp32 weights (row-major, gate order u, r, e) as the oracle reads them."""
+    H: int
+    R: np.ndarray
+    I: np.ndarray
+    b: np.ndarray
+    O1: np.ndarray
+    b1: np.ndarray
+    O2: np.ndarray
+    b2: np.ndarray
+    O3: np.ndarray
+    b3: np.ndarray
+    O4: np.ndarray
+    b4: np.ndarray
+    Wc: np.ndarray | None = None
+    Wx: np.ndarray | None = None
+    frame_len: int = 120
+    B: int = 1
+
+    @staticmethod
+    def from_dict(d: dict, bf16: bool = False) -> "Weights":
+        keys = ("R", "I", "b", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4", "Wc", "Wx")
+        kw = {}
+        for k in keys:
+            v = d.get(k)
+            if v is None:
+                kw[k] = None
+                continue
+            v = np.ascontiguousarray(v, dtype=np.float32)
+            kw[k] = bf16_round(v) if bf16 else v.copy()
+        return Weights(H=int(d["H"]), frame_len=int(d.get("frame_len", 120)), B=int(d.get("B", 1)), **kw)
+
+
+def _model(w: Weights):
+    f = ctypes.POINTER(ctypes.c_float)
+
+    def fp(a):
+        return ctypes.cast(a.ctypes.data, f) if a is not None else ctypes.cast(None, f)
+
+    m = _Model()
+    m.H = w.H
+    m.Dc = 0 if w.Wc is None else w.Wc.shape[1]
+    m.Dx = 0 if w.Wx is None else w.Wx.shape[1]
+    m.frame_len = w.frame_len
+    m.B = w.B
+    for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4"):
+        setattr(m, n, fp(getattr(w, n)))
+    return m
+
+
+def run(w: Weights, S: int, T: int, feat=None, seed: int = 1, target=None, h0=None, c0=None, f0=None,
+        t0: int = 0, logits: bool = False, nll: bool = False) -> dict:
+    """Sample (target None) or teacher-force S utterances of T samples.
+
+    Returns dict(out [S][T] uint16, h [S*B][H], c, f [S*B] uint8, zc, zf [S][T][256], nll [S][T])."""
+    L = lib()
+    B = w.B
+    H = w.H
+    h = np.zeros((S * B, H), np.float32) if h0 is None else np.ascontiguousarray(h0, np.float32).copy()
+    c = np.full(S * B, 128, np.uint8) if c0 is None else np.ascontiguousarray(c0, np.uint8).copy()
+    f = np.zeros(S * B, np.uint8) if f0 is None else np.ascontiguousarray(f0, np.uint8).copy()
+    out = np.zeros((S, T), np.uint16)
+    n_frames = 0
+    if feat is not None:
+        feat = np.ascontiguousarray(feat, np.float32)
+        n_frames = feat.shape[1]
+    tgt = None if target is None else np.ascontiguousarray(target, np.uint16)
+    zc = np.zeros((S, T, N_CLASSES), np.float32) if logits else None
+    zf = np.zeros((S, T, N_CLASSES), np.float32) if logits else None
+    nl = np.zeros((S, T), np.float64) if nll else None
+    m = _model(w)
+    rc = L.orc_run(ctypes.byref(m), S, T, t0, _p(feat), n_frames, seed, _p(tgt), _p(h), _p(c), _p(f), _p(out),
+                   _p(zc), _p(zf), _p(nl))
+    if rc != 0:
+        raise ValueError("oracle rejected the inputs")
+    return dict(out=out, h=h, c=c, f=f, zc=zc, zf=zf, nll=nl)

@@ -1,0 +1,305 @@
+/*
+ * WaveRNN oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, scalar CPU implementation of the WaveRNN sampling step of
+ * "Efficient Neural Audio Synthesis" (Kalchbrenner et al., 2018), used to check
+ * the GPU library.  Only the tests, the smoke check and the benchmark's CPU
+ * baseline may load it; the GPU library neither links nor calls it, and it shares
+ * no code with the GPU library.
+ *
+ * What it computes (per stream, per step t):
+ *   x_t = [c_{t-1}, f_{t-1}, c_t], each byte scaled from [0,255] to [-1,1]   (Sec. 2, text after Eq. 2)
+ *   u = sigma(R_u h + I*_u x + b_u),  r = sigma(R_r h + I*_r x + b_r)        (Eq. 2)
+ *   e = tanh(r o (R_e h) + I*_e x + b_e),  h' = u o h + (1-u) o e            (Eq. 2)
+ *   y_c, y_f = split(h');  P(c) = softmax(O2 relu(O1 y_c + b1) + b2)         (Eq. 2)
+ *                          P(f) = softmax(O4 relu(O3 y_f + b3) + b4)
+ *   I* is masked: c_t reaches only the fine half of u, r, e                  (Sec. 2, text after Eq. 2)
+ *   gates of the coarse half are evaluated first, c_t is sampled, then the
+ *   fine half is evaluated and f_t is sampled                                (Fig. 1 caption)
+ *
+ * Precision: weights and activations are fp32 (weights may carry values rounded
+ * to bf16 by the caller); the paper keeps activations and arithmetic in 32-bit
+ * float (Sec. 3.3).  Readings of the paper fixed here (the paper is silent):
+ *   - every dot product is a chain of fused multiply-adds in increasing index
+ *     order starting from +0;
+ *   - one bias per gate, added outside the reset product; biases on O1..O4;
+ *   - exp is evaluated by Cody-Waite range reduction and a degree-7 Taylor
+ *     polynomial (Cody & Waite, 1980), sigma(x) = 1/(1+exp(-x)),
+ *     tanh(x) = sign(x)(1-q)/(1+q) with q = exp(-2|x|);
+ *   - a class is drawn by inverse CDF: k* = #{k : C_k <= U*C_255} over the
+ *     running sums C_k of exp(z_k - max z), clamped to the last class with
+ *     nonzero weight;
+ *   - uniforms come from Philox4x64-10 (Salmon et al., SC'11) with key
+ *     (seed, 0) and counter (t, stream, 0, 0); U = (word >> 40) * 2^-24,
+ *     word 0 for the coarse draw and word 1 for the fine draw;
+ *   - initial state h = 0, c_{-1} = 128, f_{-1} = 0 unless given;
+ *   - conditioning: a feature frame of Dc values per frame_len samples enters
+ *     every gate pre-activation through W_cond (3H x Dc);
+ *   - Subscale (Sec. 4, Eq. 4) in lockstep: B lanes, lane s at row i makes
+ *     sample n = B*i + s from its own state; its context is the Dx/2 samples
+ *     before n, each as (c, f) scaled, zero when the sample is not yet made at
+ *     the start of row i, entering the gates through W_ctx (3H x Dx).
+ *
+ * Build: cc -O2 -ffp-contract=off -fPIC -shared (no fast-math; fmaf only where written).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "wavernn_oracle.h"
+
+/* ------------------------------------------------------------------------- */
+/* Elementary functions (reading: Cody-Waite + Taylor, see header comment)    */
+/* ------------------------------------------------------------------------- */
+
+static float g_ln2_hi, g_ln2_lo, g_log2e, g_inv_fact[8];
+static int g_consts_ready = 0;
+
+/* ln 2 split into a 15-significant-bit head (so k*ln2_hi is exact for |k| < 512)
+ * and a tail, both derived here from the double-precision value of ln 2;
+ * Taylor coefficients 1/i! rounded to fp32. */
+static void init_consts(void) {
+  if (g_consts_ready) return;
+  double ln2 = log(2.0);
+  int e;
+  double m = frexp(ln2, &e);                   /* ln2 = m * 2^e, m in [0.5,1) */
+  double head = ldexp(floor(ldexp(m, 15)), e - 15);
+  g_ln2_hi = (float)head;
+  g_ln2_lo = (float)(ln2 - head);
+  g_log2e = (float)(1.0 / ln2);
+  double f = 1.0;
+  for (int i = 0; i < 8; ++i) {
+    if (i > 0) f *= i;
+    g_inv_fact[i] = (float)(1.0 / f);
+  }
+  g_consts_ready = 1;
+}
+
+float orc_exp(float y) {
+  init_consts();
+  if (y != y) return y;
+  if (y < -86.0f) return 0.0f;           /* result would be below 2^-124 */
+  if (y > 88.0f) return INFINITY;
+  float k = rintf(y * g_log2e);          /* nearest integer, ties to even */
+  float r = fmaf(-k, g_ln2_hi, y);
+  r = fmaf(-k, g_ln2_lo, r);
+  float p = g_inv_fact[7];
+  for (int i = 6; i >= 0; --i) p = fmaf(p, r, g_inv_fact[i]);
+  int ki = (int)k;                       /* in [-124, 127] */
+  uint32_t bits = (uint32_t)(ki + 127) << 23;
+  float two_k;
+  memcpy(&two_k, &bits, 4);
+  return p * two_k;
+}
+
+float orc_sigmoid(float x) { return 1.0f / (1.0f + orc_exp(-x)); }
+
+float orc_tanh(float x) {
+  float a = fabsf(x);
+  float q = orc_exp(-2.0f * a);
+  float t = (1.0f - q) / (1.0f + q);
+  return copysignf(t, x);
+}
+
+static float relu(float v) { return v > 0.0f ? v : 0.0f; }
+
+/* Byte -> [-1, 1]: (2v - 255) / 255, correctly rounded (Sec. 2: scalars in
+ * [0,255] scaled to [-1,1]). */
+float orc_scale(int v) { return (float)(2 * v - 255) / 255.0f; }
+
+/* Dot product as an fma chain in increasing index order from +0. */
+static float dot(const float* w, const float* x, int n) {
+  float acc = 0.0f;
+  for (int j = 0; j < n; ++j) acc = fmaf(w[j], x[j], acc);
+  return acc;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11)                          */
+/* ------------------------------------------------------------------------- */
+
+static void mulhilo64(uint64_t a, uint64_t b, uint64_t* hi, uint64_t* lo) {
+  unsigned __int128 p = (unsigned __int128)a * b;
+  *hi = (uint64_t)(p >> 64);
+  *lo = (uint64_t)p;
+}
+
+void orc_philox4x64_10(const uint64_t ctr_in[4], const uint64_t key_in[2], uint64_t out[4]) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ULL, M1 = 0xCA5A826395121157ULL;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ULL, W1 = 0xBB67AE8584CAA73BULL;
+  uint64_t c[4] = {ctr_in[0], ctr_in[1], ctr_in[2], ctr_in[3]};
+  uint64_t k0 = key_in[0], k1 = key_in[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) { k0 += W0; k1 += W1; }
+    uint64_t hi0, lo0, hi1, lo1;
+    mulhilo64(M0, c[0], &hi0, &lo0);
+    mulhilo64(M1, c[2], &hi1, &lo1);
+    uint64_t n0 = hi1 ^ c[1] ^ k0, n1 = lo1, n2 = hi0 ^ c[3] ^ k1, n3 = lo0;
+    c[0] = n0; c[1] = n1; c[2] = n2; c[3] = n3;
+  }
+  memcpy(out, c, sizeof c);
+}
+
+void orc_uniforms(uint64_t seed, uint64_t stream, int64_t t, float* uc, float* uf) {
+  uint64_t ctr[4] = {(uint64_t)t, stream, 0, 0}, key[2] = {seed, 0}, w[4];
+  orc_philox4x64_10(ctr, key, w);
+  *uc = (float)(w[0] >> 40) * (1.0f / 16777216.0f);
+  *uf = (float)(w[1] >> 40) * (1.0f / 16777216.0f);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Softmax sampling (Eq. 2 softmax; inverse CDF reading)                       */
+/* ------------------------------------------------------------------------- */
+
+int orc_draw(const float* z, int n, float u) {
+  float m = z[0];
+  for (int k = 1; k < n; ++k) if (z[k] > m) m = z[k];
+  float w[ORC_MAX_CLASSES], c[ORC_MAX_CLASSES];
+  float run = 0.0f;
+  for (int k = 0; k < n; ++k) {
+    w[k] = orc_exp(z[k] - m);
+    run = run + w[k];
+    c[k] = run;
+  }
+  float thr = u * c[n - 1];
+  int count = 0;
+  for (int k = 0; k < n; ++k) count += (c[k] <= thr);
+  if (count == n) {
+    count = n - 1;
+    while (count > 0 && !(w[count] > 0.0f)) --count;
+  }
+  return count;
+}
+
+/* -log softmax(z)[k] in double from fp32 logits (plain definition). */
+static double neg_log_prob(const float* z, int n, int k) {
+  double m = z[0];
+  for (int j = 1; j < n; ++j) if (z[j] > m) m = z[j];
+  double s = 0.0;
+  for (int j = 0; j < n; ++j) s += exp((double)z[j] - m);
+  return -(((double)z[k] - m) - log(s));
+}
+
+/* ------------------------------------------------------------------------- */
+/* The recurrent step                                                         */
+/* ------------------------------------------------------------------------- */
+
+/* Additive gate term that does not depend on h or x: bias + conditioning
+ * (+ subscale context).  add[g*H + i] for gate g in {u, r, e}. */
+static void gate_additive(const orc_model* m, const float* feat_frame, const float* ctx, float* add) {
+  const int H = m->H;
+  for (int row = 0; row < 3 * H; ++row) {
+    float a = m->b[row];
+    if (m->Dc > 0) a = dot(m->Wc + (size_t)row * m->Dc, feat_frame, m->Dc) + m->b[row];
+    if (m->Dx > 0) a = a + dot(m->Wx + (size_t)row * m->Dx, ctx, m->Dx);
+    add[row] = a;
+  }
+}
+
+/* Gates for units i in [lo, hi): Eq. 2 with the masked input matrix.
+ * x has three entries; for the coarse half (i < H/2) the third is ignored. */
+static void gru_units(const orc_model* m, const float* G, const float* add, const float* x,
+                      const float* h_prev, float* h_new, int lo, int hi) {
+  const int H = m->H, Hh = H / 2;
+  for (int i = lo; i < hi; ++i) {
+    float ix[3];
+    for (int g = 0; g < 3; ++g) {
+      const float* Ig = m->I + ((size_t)g * H + i) * 3;
+      ix[g] = dot(Ig, x, i < Hh ? 2 : 3);
+    }
+    float au = G[0 * H + i] + (ix[0] + add[0 * H + i]);
+    float ar = G[1 * H + i] + (ix[1] + add[1 * H + i]);
+    float u = orc_sigmoid(au);
+    float r = orc_sigmoid(ar);
+    float e = orc_tanh(fmaf(r, G[2 * H + i], ix[2] + add[2 * H + i]));
+    h_new[i] = fmaf(u, h_prev[i], (1.0f - u) * e);
+  }
+}
+
+/* One output head: z = Ob relu(Oa y + ba) + bb (Eq. 2). */
+static void head(const orc_model* m, const float* Oa, const float* ba, const float* Ob, const float* bb,
+                 const float* y, float* z) {
+  const int Hh = m->H / 2;
+  float hid[ORC_MAX_HIDDEN / 2];
+  for (int k = 0; k < Hh; ++k) hid[k] = relu(dot(Oa + (size_t)k * Hh, y, Hh) + ba[k]);
+  for (int v = 0; v < ORC_MAX_CLASSES; ++v) z[v] = dot(Ob + (size_t)v * Hh, hid, Hh) + bb[v];
+}
+
+/* Context of subscale lane s at row i: (c, f) of samples n-1, n-2, ... scaled;
+ * zero where the sample does not yet exist at the start of row i. */
+static void subscale_context(const orc_model* m, const uint16_t* seq, int64_t n, int64_t row_start, float* ctx) {
+  const int L = m->Dx / 2;
+  for (int j = 0; j < L; ++j) {
+    int64_t q = n - 1 - j;
+    if (q >= 0 && q < row_start) {
+      ctx[2 * j] = orc_scale(seq[q] >> 8);
+      ctx[2 * j + 1] = orc_scale(seq[q] & 255);
+    } else {
+      ctx[2 * j] = 0.0f;
+      ctx[2 * j + 1] = 0.0f;
+    }
+  }
+}
+
+int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* feat, int64_t n_frames,
+            uint64_t seed, const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, uint16_t* out,
+            float* zc_out, float* zf_out, double* nll_out) {
+  const int H = m->H, Hh = H / 2, B = m->B > 0 ? m->B : 1;
+  if (H <= 0 || (H & 1) || H > ORC_MAX_HIDDEN || S <= 0 || T < 0) return -1;
+  if (B > 1 && (T % B != 0 || t0 != 0)) return -1;
+  if (m->Dc > 0 && (m->frame_len <= 0 || feat == NULL)) return -1;
+  if (m->Dx > 0 && (B == 1 || m->Dx % 2 != 0)) return -1;
+  if (target == NULL && out == NULL) return -1;
+  if (T == 0) return 0;
+  float* G = (float*)malloc(sizeof(float) * 3 * H);
+  float* add = (float*)malloc(sizeof(float) * 3 * H);
+  float* hn = (float*)malloc(sizeof(float) * H);
+  float* ctx = (float*)malloc(sizeof(float) * (m->Dx > 0 ? m->Dx : 1));
+  float zc[ORC_MAX_CLASSES], zf[ORC_MAX_CLASSES];
+  const int64_t rows = T / B;
+  for (int32_t s = 0; s < S; ++s) {
+    uint16_t* seq = out ? out + (size_t)s * T : NULL;   /* samples of utterance s, time order */
+    const uint16_t* tgt = target ? target + (size_t)s * T : NULL;
+    for (int64_t i = 0; i < rows; ++i) {
+      for (int lane = 0; lane < B; ++lane) {
+        const int64_t st = (int64_t)s * B + lane;   /* state / Philox stream index */
+        const int64_t n = (B == 1) ? t0 + i : B * i + lane; /* absolute sample index */
+        const int64_t local = (B == 1) ? i : n;             /* index into this call's arrays */
+        float* hs = h + (size_t)st * H;
+        const float* frame = NULL;
+        if (m->Dc > 0) {
+          int64_t fr = n / m->frame_len;
+          if (fr >= n_frames) fr = n_frames - 1;
+          frame = feat + ((size_t)s * n_frames + fr) * m->Dc;
+        }
+        if (m->Dx > 0) subscale_context(m, tgt ? tgt : seq, n, B * i, ctx);
+        gate_additive(m, frame, ctx, add);
+        for (int row = 0; row < 3 * H; ++row) G[row] = dot(m->R + (size_t)row * H, hs, H);
+        float x[3] = {orc_scale(cprev[st]), orc_scale(fprev[st]), 0.0f};
+        /* coarse half, coarse head, coarse draw */
+        gru_units(m, G, add, x, hs, hn, 0, Hh);
+        head(m, m->O1, m->b1, m->O2, m->b2, hn, zc);
+        float uc, uf;
+        orc_uniforms(seed, (uint64_t)st, B == 1 ? n : i, &uc, &uf);
+        int c = tgt ? (tgt[local] >> 8) : orc_draw(zc, ORC_MAX_CLASSES, uc);
+        /* fine half sees c_t, fine head, fine draw */
+        x[2] = orc_scale(c);
+        gru_units(m, G, add, x, hs, hn, Hh, H);
+        head(m, m->O3, m->b3, m->O4, m->b4, hn + Hh, zf);
+        int f = tgt ? (tgt[local] & 255) : orc_draw(zf, ORC_MAX_CLASSES, uf);
+        memcpy(hs, hn, sizeof(float) * H);
+        cprev[st] = (uint8_t)c;
+        fprev[st] = (uint8_t)f;
+        if (!tgt) seq[local] = (uint16_t)(256 * c + f);
+        else if (seq) seq[local] = tgt[local];
+        size_t o = (size_t)s * T + local;
+        if (zc_out) memcpy(zc_out + o * ORC_MAX_CLASSES, zc, sizeof zc);
+        if (zf_out) memcpy(zf_out + o * ORC_MAX_CLASSES, zf, sizeof zf);
+        if (nll_out) nll_out[o] = neg_log_prob(zc, ORC_MAX_CLASSES, c) + neg_log_prob(zf, ORC_MAX_CLASSES, f);
+      }
+    }
+  }
+  free(G); free(add); free(hn); free(ctx);
+  return 0;
+}

@@ -1,0 +1,43 @@
+/*
+ * WaveRNN oracle (test infrastructure only) -- C interface used via ctypes by
+ * the tests, the smoke check and the benchmark's CPU baseline.
+ * See wavernn_oracle.c for what is computed and the readings of the paper.
+ */
+#ifndef WAVERNN_ORACLE_H
+#define WAVERNN_ORACLE_H
+#include <stdint.h>
+
+#define ORC_MAX_CLASSES 256   /* 8-bit coarse / fine softmax (Sec. 2) */
+#define ORC_MAX_HIDDEN 4096
+
+/* All matrices fp32 row-major.  Gate order u, r, e.
+ *   R  [3][H][H]      recurrent matrix (Eq. 2); zeroed entries = pruned weights
+ *   I  [3][H][3]      input matrix, columns (c_{t-1}, f_{t-1}, c_t); column 2 of
+ *                     rows i < H/2 is ignored (the I* mask)
+ *   b  [3][H]         gate biases
+ *   Wc [3H][Dc]       conditioning projection (Dc = 0: none)
+ *   Wx [3H][Dx]       subscale context projection (Dx = 0: none)
+ *   O1 [H/2][H/2] b1 [H/2]   O2 [256][H/2] b2 [256]   (coarse head)
+ *   O3 [H/2][H/2] b3 [H/2]   O4 [256][H/2] b4 [256]   (fine head)   */
+typedef struct {
+  int32_t H, Dc, frame_len, B, Dx;
+  const float *R, *I, *b, *Wc, *Wx;
+  const float *O1, *b1, *O2, *b2, *O3, *b3, *O4, *b4;
+} orc_model;
+
+float orc_exp(float y);
+float orc_sigmoid(float x);
+float orc_tanh(float x);
+float orc_scale(int v);
+void orc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+void orc_uniforms(uint64_t seed, uint64_t stream, int64_t t, float* uc, float* uf);
+int orc_draw(const float* z, int n, float u);
+
+/* Runs S utterances of T samples (B = 1: starting at absolute sample t0).
+ * feat [S][n_frames][Dc]; target [S][T] (NULL: sample freely); state h [S*B][H],
+ * cprev/fprev [S*B] are read and updated; out [S][T] (16-bit, 256*c + f);
+ * zc/zf [S][T][256] logits and nll [S][T] (nats) are optional.  Returns 0 or -1. */
+int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* feat, int64_t n_frames,
+            uint64_t seed, const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, uint16_t* out,
+            float* zc, float* zf, double* nll);
+#endif

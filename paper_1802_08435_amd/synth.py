@@ -1,0 +1,116 @@
+"""Seeded synthetic WaveRNN weights and inputs.
+
+Holds none of the method's arithmetic: it only draws random arrays of the
+shapes the model of Sec. 2 (Eq. 2) uses, for the GPU library, the oracle, the
+tests and the benchmark alike.  There are no trained weights or speech data
+here, so weights are ~N(0, 1/fan_in) and conditioning frames ~N(0, 1).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+N_CLASSES = 256
+FRAME_LEN = 120          # 5 ms of 24 kHz audio per conditioning frame
+COND_DIM = 64
+CTX_DIM = 256            # subscale context: 128 preceding samples x (c, f)
+
+
+def _normal(rng, shape, fan_in):
+    return (rng.standard_normal(shape) / math.sqrt(fan_in)).astype(np.float32)
+
+
+def make_weights(H: int, seed: int = 0, cond_dim: int = 0, B: int = 1, ctx_dim: int = 0,
+                 block=None, density: float = 1.0, mask_seed: int = 3) -> dict:
+    """Weights of one WaveRNN with H hidden units (H/2 coarse, H/2 fine).
+
+    block = None (dense R) or (bh, bw) in {(4, 4), (16, 1)}: R keeps exactly
+    round(density * n_blocks) random blocks per gate matrix (seeded by mask_seed),
+    kept values ~N(0, 1/(density * H)); pruned entries are 0 and ``mask`` is the
+    [3][H/bh][H/bw] uint8 block mask.  The masked entries of I (column 2 of the
+    coarse rows) are filled with random values on purpose: the model ignores them."""
+    assert H % 2 == 0
+    Hh = H // 2
+    rng = np.random.default_rng(seed)
+    w = dict(H=H, B=B, frame_len=FRAME_LEN, block=block, mask=None)
+    if block is None:
+        w["R"] = _normal(rng, (3, H, H), H)
+    else:
+        bh, bw = block
+        assert H % bh == 0 and H % bw == 0
+        nbr, nbc = H // bh, H // bw
+        mrng = np.random.default_rng(mask_seed)
+        keep = int(round(density * nbr * nbc))
+        mask = np.zeros((3, nbr * nbc), np.uint8)
+        for g in range(3):
+            mask[g, mrng.choice(nbr * nbc, keep, replace=False)] = 1
+        mask = mask.reshape(3, nbr, nbc)
+        vals = _normal(rng, (3, H, H), density * H)
+        full = np.repeat(np.repeat(mask, bh, axis=1), bw, axis=2).astype(np.float32)
+        w["R"] = (vals * full).astype(np.float32)
+        w["mask"] = mask
+    w["I"] = _normal(rng, (3, H, 3), 3)
+    w["b"] = _normal(rng, (3, H), H)
+    w["O1"] = _normal(rng, (Hh, Hh), Hh)
+    w["b1"] = _normal(rng, (Hh,), Hh)
+    w["O2"] = _normal(rng, (N_CLASSES, Hh), Hh)
+    w["b2"] = _normal(rng, (N_CLASSES,), Hh)
+    w["O3"] = _normal(rng, (Hh, Hh), Hh)
+    w["b3"] = _normal(rng, (Hh,), Hh)
+    w["O4"] = _normal(rng, (N_CLASSES, Hh), Hh)
+    w["b4"] = _normal(rng, (N_CLASSES,), Hh)
+    w["Wc"] = _normal(rng, (3 * H, cond_dim), cond_dim) if cond_dim else None
+    w["Wx"] = _normal(rng, (3 * H, ctx_dim), ctx_dim) if ctx_dim else None
+    return w
+
+
+def features(S: int, T: int, cond_dim: int = COND_DIM, seed: int = 2, frame_len: int = FRAME_LEN,
+             per_stream_seed: bool = False) -> np.ndarray:
+    """Conditioning frames [S][ceil(T/frame_len)][cond_dim] ~N(0, 1)."""
+    n_frames = max(1, -(-T // frame_len))
+    if per_stream_seed:
+        return np.stack([np.random.default_rng(seed + s).standard_normal((n_frames, cond_dim))
+                         for s in range(S)]).astype(np.float32)
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal((S, n_frames, cond_dim)).astype(np.float32)
+
+
+def target_signal(S: int, T: int, seed: int = 4, kind: str = "sines") -> np.ndarray:
+    """16-bit offset-binary sample sequences [S][T] (coarse byte = high 8 bits).
+
+    kind='sines': three sinusoids summing to -10 dBFS plus N(0, 1e-3) noise;
+    kind='uniform': uniform random 16-bit words."""
+    rng = np.random.default_rng(seed)
+    if kind == "uniform":
+        return rng.integers(0, 65536, size=(S, T), dtype=np.uint16)
+    t = np.arange(T) / 24000.0
+    out = np.empty((S, T), np.uint16)
+    amp = 10 ** (-10 / 20) / 3
+    for s in range(S):
+        f = rng.uniform(80, 4000, size=3)
+        ph = rng.uniform(0, 2 * np.pi, size=3)
+        x = sum(amp * np.sin(2 * np.pi * f[k] * t + ph[k]) for k in range(3))
+        x = x + rng.normal(0, 1e-3, size=T)
+        q = np.clip(np.round(x * 32767), -32768, 32767).astype(np.int64) + 32768
+        out[s] = q.astype(np.uint16)
+    return out
+
+
+PRESETS = {
+    # name: (H, cond_dim, B, ctx_dim, block, bf16, streams, samples)
+    "tiny": (64, 0, 1, 0, None, False, 1, 2400),
+    "dense896": (896, COND_DIM, 1, 0, None, True, 1, 24000),
+    "sparse2048_4x4": (2048, COND_DIM, 1, 0, (4, 4), True, 1, 24000),
+    "sparse2048_16x1": (2048, COND_DIM, 1, 0, (16, 1), True, 1, 24000),
+    "subscale16": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
+    "multi64": (896, COND_DIM, 1, 0, None, True, 64, 48000),
+}
+
+
+def preset(name: str, seed: int = 0) -> dict:
+    H, Dc, B, Dx, block, bf16, S, T = PRESETS[name]
+    w = make_weights(H, seed=seed, cond_dim=Dc, B=B, ctx_dim=Dx, block=block,
+                     density=0.04 if block else 1.0)
+    w.update(name=name, bf16=bf16, streams=S, samples=T)
+    return w

@@ -1,0 +1,103 @@
+"""The oracle's pins catch plausible mistakes (CPU only).
+
+Each case plants one mistake in a copy of the oracle's C source (never in the
+oracle itself), builds it with gcc into a temporary directory, swaps it in for
+the real build and runs the pins of ``test_oracle_pins.py``: at least one pin
+must fail for every planted mistake.
+"""
+import os
+import subprocess
+
+import pytest
+
+from oracle import oracle as O
+import test_oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(O.__file__), "wavernn_oracle.c")
+
+MUTANTS = {
+    "u_reads_r_gate": ("float au = G[0 * H + i] + (ix[0] + add[0 * H + i]);",
+                       "float au = G[1 * H + i] + (ix[1] + add[1 * H + i]);"),
+    "reset_gate_dropped": ("orc_tanh(fmaf(r, G[2 * H + i],", "orc_tanh(fmaf(1.0f, G[2 * H + i],"),
+    "interpolation_swapped": ("fmaf(u, h_prev[i], (1.0f - u) * e)", "fmaf(1.0f - u, h_prev[i], u * e)"),
+    "R_transposed": ("for (int row = 0; row < 3 * H; ++row) G[row] = dot(m->R + (size_t)row * H, hs, H);",
+                     "for (int row = 0; row < 3 * H; ++row) { float acc = 0.0f; int g = row / H, q = row % H;"
+                     " for (int j = 0; j < H; ++j) acc = fmaf(m->R[((size_t)g * H + j) * H + q], hs[j], acc);"
+                     " G[row] = acc; }"),
+    "mask_ignored": ("ix[g] = dot(Ig, x, i < Hh ? 2 : 3);", "ix[g] = dot(Ig, x, 3);",
+                     "float x[3] = {orc_scale(cprev[st]), orc_scale(fprev[st]), 0.0f};",
+                     "float x[3] = {orc_scale(cprev[st]), orc_scale(fprev[st]), tgt ? orc_scale(tgt[local] >> 8) : 0.0f};"),
+    "gate_bias_dropped": ("float a = m->b[row];", "float a = 0.0f;",
+                          "feat_frame, m->Dc) + m->b[row];", "feat_frame, m->Dc);"),
+    "conditioning_dropped": ("if (m->Dc > 0) a = dot(", "if (0) a = dot("),
+    "frame_off_by_one": ("int64_t fr = n / m->frame_len;", "int64_t fr = (n + 1) / m->frame_len;"),
+    "heads_read_wrong_half": ("head(m, m->O1, m->b1, m->O2, m->b2, hn, zc);",
+                              "head(m, m->O1, m->b1, m->O2, m->b2, hn + Hh, zc);"),
+    "relu_dropped": ("hid[k] = relu(dot(Oa + (size_t)k * Hh, y, Hh) + ba[k]);",
+                     "hid[k] = dot(Oa + (size_t)k * Hh, y, Hh) + ba[k];"),
+    "head_bias_dropped": ("z[v] = dot(Ob + (size_t)v * Hh, hid, Hh) + bb[v];", "z[v] = dot(Ob + (size_t)v * Hh, hid, Hh);"),
+    "philox_words_swapped": ("*uc = (float)(w[0] >> 40)", "*uc = (float)(w[1] >> 40)",
+                             "*uf = (float)(w[1] >> 40)", "*uf = (float)(w[0] >> 40)"),
+    "philox_counter_layout": ("uint64_t ctr[4] = {(uint64_t)t, stream, 0, 0}", "uint64_t ctr[4] = {stream, (uint64_t)t, 0, 0}"),
+    "philox_no_key_bump": ("if (round > 0) { k0 += W0; k1 += W1; }", "if (0) { k0 += W0; k1 += W1; }"),
+    "draw_strict_compare": ("count += (c[k] <= thr);", "count += (c[k] < thr);"),
+    "draw_without_max_shift": ("w[k] = orc_exp(z[k] - m);", "w[k] = orc_exp(z[k]);"),
+    "scale_formula": ("return (float)(2 * v - 255) / 255.0f;", "return (float)v / 128.0f - 1.0f;"),
+    "sigmoid_sign": ("return 1.0f / (1.0f + orc_exp(-x));", "return 1.0f / (1.0f + orc_exp(x));"),
+    "tanh_as_sigmoid": ("float t = (1.0f - q) / (1.0f + q);", "float t = 1.0f / (1.0f + q);"),
+    "nll_fine_term_dropped": ("neg_log_prob(zc, ORC_MAX_CLASSES, c) + neg_log_prob(zf, ORC_MAX_CLASSES, f)",
+                              "neg_log_prob(zc, ORC_MAX_CLASSES, c)"),
+    "subscale_no_row_mask": ("if (q >= 0 && q < row_start) {", "if (q >= 0 && q < n) {"),
+    "subscale_lane_order": ("const int64_t n = (B == 1) ? t0 + i : B * i + lane;",
+                            "const int64_t n = (B == 1) ? t0 + i : rows * lane + i;"),
+    "exp_low_coeffs_off": ("g_inv_fact[i] = (float)(1.0 / f);", "g_inv_fact[i] = (float)(1.0 / (f + (i == 2)));"),
+}
+
+PINS = [
+    "test_philox_matches_numpy", "test_exp_accuracy_and_specials", "test_sigmoid_tanh_accuracy",
+    "test_scale_is_correctly_rounded", "test_draw_uniform_logits_is_floor_256u",
+    "test_draw_point_mass_and_zero_probability_classes",
+    "test_zero_model_samples_are_floor_256u_and_nll_is_2ln256", "test_zero_model_streams_use_their_own_philox_stream",
+    "test_update_gate_saturated_at_one_keeps_state", "test_hand_case_input_mask_and_heads",
+    "test_hand_case_reset_gate_placement_and_R_orientation", "test_hand_case_update_gate_interpolates",
+    "test_hand_case_conditioning_frames", "test_coarse_logits_do_not_depend_on_current_coarse_byte",
+    "test_chunked_sampling_equals_one_call", "test_subscale_without_context_is_interleaved_plain_streams",
+    "test_subscale_context_masks_samples_of_the_current_row",
+]
+
+_PARAMS = {"test_philox_matches_numpy": [dict(seed=7, stream=3, t=123456), dict(seed=1, stream=0, t=5)],
+           "test_subscale_context_masks_samples_of_the_current_row": [dict(j=0), dict(j=5)]}
+
+
+def _failures(tmp_path, name):
+    src = open(SRC).read()
+    edits = MUTANTS[name]
+    for a, b in zip(edits[::2], edits[1::2]):
+        assert src.count(a) == 1, (name, a)
+        src = src.replace(a, b)
+    d = tmp_path / name
+    d.mkdir()
+    (d / "m.c").write_text(src)
+    (d / "wavernn_oracle.h").write_text(open(os.path.join(os.path.dirname(SRC), "wavernn_oracle.h")).read())
+    so = str(d / "libm.so")
+    subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fPIC", "-shared", "-std=c11", "-I", str(d),
+                           "-o", so, str(d / "m.c"), "-lm"])
+    saved = O._lib
+    O._lib = O.load(so)
+    failed = []
+    try:
+        for pin in PINS:
+            for kw in _PARAMS.get(pin, [dict()]):
+                try:
+                    getattr(P, pin)(**kw)
+                except (AssertionError, ValueError):
+                    failed.append(pin)
+                    break
+    finally:
+        O._lib = saved
+    return failed
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    assert _failures(tmp_path, name), f"no pin caught the planted mistake {name}"
