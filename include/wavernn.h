@@ -1,0 +1,164 @@
+/*
+ * wavernn.h -- C ABI of libwavernn, WaveRNN sampling on MI355X (gfx950).
+ *
+ * The library implements the sampling step of "Efficient Neural Audio
+ * Synthesis" (Kalchbrenner et al., 2018): the single GRU layer of Eq. 2 with
+ * the masked input matrix I* (Sec. 2, text after Eq. 2), the dual 8-bit softmax
+ * (coarse byte first, then the fine byte conditioned on it; Fig. 1 caption),
+ * draws from the two softmaxes, repeated once per 16-bit audio sample, as one
+ * persistent GPU operation per call (Sec. 2.1).  It also covers block-sparse R
+ * (Sparse WaveRNN, Sec. 3.2: 4x4 and 16x1 blocks) and subscale batching
+ * (Subscale WaveRNN, Sec. 4, Eq. 4).
+ *
+ * Conventions shared by every entry point:
+ *  - Weights are passed as host fp32 arrays, row-major, gate order u, r, e.
+ *    The library copies them (the caller may free them on return), applies the
+ *    I* mask, rounds to bf16 (round to nearest even) if asked, packs them for
+ *    the kernels and owns the device copies until wavernn_destroy.
+ *  - Every other buffer is caller-owned *device* memory.  Calls are
+ *    asynchronous and ordered on the given HIP stream (hipStream_t passed as
+ *    void*, NULL = the null stream); inputs must stay valid until the work on
+ *    that stream is done.
+ *  - A 16-bit sample is stored offset-binary: u = 256*c + f, c the coarse
+ *    (high) byte, f the fine (low) byte (Fig. 1 caption).  Bytes enter the
+ *    network scaled to [-1, 1] as (2v - 255) / 255 (Sec. 2).
+ *  - Draws use Philox4x64-10 (Salmon et al., SC'11), key (seed, 0), counter
+ *    (t, stream, 0, 0) with t the absolute step; word 0 gives the coarse
+ *    uniform, word 1 the fine one, U = (word >> 40) * 2^-24.  A class is
+ *    drawn by inverse CDF over exp(z - max z).
+ *  - Functions return a wavernn_status; on failure nothing is launched and
+ *    wavernn_last_error() (per thread) describes the cause.  No exceptions
+ *    cross the ABI.
+ */
+#ifndef WAVERNN_H
+#define WAVERNN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WAVERNN_OK = 0,
+  WAVERNN_E_INVALID = 1,      /* bad argument: null pointer, shape, size, range */
+  WAVERNN_E_UNSUPPORTED = 2,  /* valid request this build cannot run (e.g. grid cannot be co-resident) */
+  WAVERNN_E_OOM = 3,          /* device allocation failed */
+  WAVERNN_E_HIP = 4,          /* a HIP runtime call failed */
+  WAVERNN_E_DEVICE = 5        /* the kernel reported a failure (wavernn_device_status) */
+} wavernn_status;
+
+typedef enum { WAVERNN_F32 = 0, WAVERNN_BF16 = 1 } wavernn_dtype;
+
+/* Storage of R.  BSR formats keep the blocks the mask marks (Sec. 3.2):
+ * 4x4 blocks, or 16x1 blocks (16 consecutive rows of one column). */
+typedef enum { WAVERNN_R_DENSE = 0, WAVERNN_R_BSR_4X4 = 1, WAVERNN_R_BSR_16X1 = 2 } wavernn_r_format;
+
+typedef struct {
+  int32_t hidden;        /* H: hidden units, even; H/2 coarse, H/2 fine (Eq. 2 split) */
+  int32_t cond_dim;      /* Dc: conditioning features per frame, 0 = none */
+  int32_t frame_len;     /* samples per conditioning frame (> 0 when cond_dim > 0) */
+  int32_t subscale;      /* B: samples per step per utterance, 1 (plain) or > 1 (Sec. 4) */
+  int32_t ctx_dim;       /* Dx: subscale context width (2 per context sample), 0 when B = 1 */
+  int32_t weight_dtype;  /* wavernn_dtype of the stored weights; arithmetic is fp32 */
+  int32_t r_format;      /* wavernn_r_format */
+  int32_t max_streams;   /* most utterances one call may sample, 1..64 */
+} wavernn_config;
+
+/* Host fp32 weights.  Shapes (H hidden, Hh = H/2, V = 256 classes):
+ *   R [3][H][H], R_block_mask [3][H/bh][H/bw] (uint8, nonzero = kept; only for BSR),
+ *   I [3][H][3] columns (c_{t-1}, f_{t-1}, c_t): column 2 of rows i < Hh is ignored (I* mask),
+ *   b [3][H], W_cond [3H][Dc], W_ctx [3H][Dx],
+ *   O1 [Hh][Hh], b1 [Hh], O2 [V][Hh], b2 [V] (coarse head, Eq. 2),
+ *   O3 [Hh][Hh], b3 [Hh], O4 [V][Hh], b4 [V] (fine head).
+ * For BSR formats, entries of R outside kept blocks are ignored. */
+typedef struct {
+  const float* R;
+  const uint8_t* R_block_mask;
+  const float* I;
+  const float* b;
+  const float* W_cond;
+  const float* W_ctx;
+  const float *O1, *b1, *O2, *b2, *O3, *b3, *O4, *b4;
+} wavernn_weights;
+
+/* Recurrent state of S utterances x B lanes, device memory:
+ * h [S*B][H] fp32, c_prev / f_prev [S*B] bytes of the previous sample,
+ * t0 = absolute index of the next sample (B = 1 only; 0 otherwise).
+ * Default initial state: h = 0, c_prev = 128, f_prev = 0, t0 = 0. */
+typedef struct {
+  float* h;
+  uint8_t* c_prev;
+  uint8_t* f_prev;
+  int64_t t0;
+} wavernn_state;
+
+typedef struct wavernn_model wavernn_model;
+
+/* Validate cfg, copy and pack the weights to the current HIP device.
+ * *out receives the model handle.  Errors: E_INVALID (null pointer, odd or
+ * unsupported H, bad config field), E_UNSUPPORTED (no kernel of this build
+ * serves the configuration), E_OOM, E_HIP. */
+wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* w, wavernn_model** out);
+
+/* Free the model's device memory.  Null-safe.  Work already queued that uses
+ * the model must have finished. */
+void wavernn_destroy(wavernn_model* m);
+
+/* Sample n_samples 16-bit samples for each of n_streams utterances (Eq. 2,
+ * dual softmax, Fig. 1 order), as one persistent kernel launch per call.
+ *   cond_dev  [n_streams][n_frames][Dc] fp32 feature frames; frame index of
+ *             absolute sample n is n / frame_len (NULL when Dc = 0)
+ *   init      initial state (NULL = default); out_dev [n_streams][n_samples] uint16
+ *   final     where to write the state after the last sample (NULL = nowhere);
+ *             may alias init.
+ * Subscale (B > 1): n_samples must be a multiple of B; lane s of step i makes
+ * sample B*i + s and out_dev is in time order.  Utterance k draws from Philox
+ * stream k*B + lane.  Errors: E_INVALID, E_UNSUPPORTED, E_HIP. */
+wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_samples, const float* cond_dev,
+                              int64_t n_frames, uint64_t seed, const wavernn_state* init, uint16_t* out_dev,
+                              const wavernn_state* final_state, void* stream);
+
+/* Teacher-forced scoring of known audio (the NLL of Sec. 5): the recurrence
+ * runs on target_dev [n_streams][n_samples] instead of drawn samples.  Writes
+ * the pre-softmax logits logits_c_dev / logits_f_dev [n_streams][n_samples][256]
+ * and nll_dev [n_streams][n_samples] = -log P(c_t) - log P(f_t | c_t) in nats;
+ * each output pointer may be NULL.  Initial state as in wavernn_sample. */
+wavernn_status wavernn_score_teacher_forced(wavernn_model* m, int32_t n_streams, int64_t n_samples,
+                                            const float* cond_dev, int64_t n_frames, const uint16_t* target_dev,
+                                            const wavernn_state* init, float* logits_c_dev, float* logits_f_dev,
+                                            float* nll_dev, void* stream);
+
+/* Wait for the model's last call on `stream` and report a failure the kernel
+ * flagged (a bounded wait that expired): WAVERNN_OK or WAVERNN_E_DEVICE. */
+wavernn_status wavernn_device_status(wavernn_model* m, void* stream);
+
+/* Philox uniforms as the device computes them: out_dev [n][2] fp32 =
+ * (coarse, fine) uniforms of steps t0 .. t0+n-1 on `stream_id`. */
+wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t t0, int64_t n, float* out_dev,
+                                      void* stream);
+
+/* Which kernel serves the model: 0 single-workgroup fp32, 1 multi-workgroup
+ * persistent, 2 batched (MFMA).  Fills *grid and *block with its launch shape. */
+int32_t wavernn_model_path(const wavernn_model* m, int32_t* grid, int32_t* block);
+
+/* Diagnostics: make later wavernn_sample / wavernn_score_teacher_forced calls
+ * of the multi-workgroup persistent kernel record, for the first max_steps
+ * steps of the first utterance, timestamps of the 100 MHz constant clock at
+ * the end of each phase of a step into trace_dev [max_steps][32] (device
+ * memory the caller owns and keeps alive while tracing is on).  Slots 0-10:
+ * unit workgroup 0 (step start, coarse gates published, y_c gathered,
+ * R.y_c done, coarse logits summed, c drawn, fine gates published, y_f
+ * gathered, R.y_f done, fine logits summed, f drawn); 16-18 / 20-22: coarse /
+ * fine head workgroup 0 (input gathered, first layer done, partials
+ * published); 25-26: the last unit workgroup's y_c published / gathered.
+ * max_steps = 0 turns tracing off.  Other kernels ignore the setting. */
+wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps);
+
+/* Description of the last error on this thread ("" if none). */
+const char* wavernn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,70 @@
+// Kernel argument blocks of libwavernn (shared by the host launcher and kernels).
+#pragma once
+#include <stdint.h>
+#include "wr_layout.h"
+
+typedef unsigned long long u64;
+
+#define WR_TRACE_SLOTS 32   // per traced step: timestamps (100 MHz) of phase ends
+
+struct SmallArgs {
+  const float* image;        // packed fp32 weights, SmallLayout order
+  const float* Wc;           // [3H][Dc] or null
+  const float* feat;         // [S][n_frames][Dc] or null
+  int64_t n_frames;
+  int H, Dc, frame_len;
+  int64_t T, t0;
+  uint64_t seed;
+  const uint16_t* target;    // [S][T] or null (free sampling)
+  uint16_t* out;             // [S][T] or null
+  float* zc_out;             // [S][T][256] or null
+  float* zf_out;
+  float* nll_out;            // [S][T] or null
+  const float* h_in;         // [S][H] or null
+  const uint8_t* c_in;
+  const uint8_t* f_in;
+  float* h_out;              // or null
+  uint8_t* c_out;
+  uint8_t* f_out;
+};
+
+struct PersistArgs {
+  PersistPlan P;
+  const uint4* wu;      // NU U blocks of P.u_bytes
+  const uint4* whc;     // NC head blocks of P.h_bytes (O1 rows + O2 columns)
+  const uint4* whf;     // NF head blocks (O3 / O4)
+  const float* Iw;      // [3H][3], I* mask applied
+  const float* bias;    // [3H]
+  const float* b1;      // [Hh]
+  const float* b2;      // [256]
+  const float* b3;
+  const float* b4;
+  const float* Wc;      // [3H][Dc] fp32 or null
+  const float* feat;    // [n_frames][Dc] of this utterance or null
+  int64_t n_frames;
+  int Dc, frame_len;
+  int64_t T, t0;
+  uint64_t seed, stream_id;
+  const uint16_t* target;   // [T] or null
+  uint16_t* out;            // [T] or null
+  float* zc_out;            // [T][256] or null
+  float* zf_out;
+  float* nll_out;           // [T] or null
+  const float* h_in;        // [H] or null
+  const uint8_t* c_in;
+  const uint8_t* f_in;
+  float* h_out;
+  uint8_t* c_out;
+  uint8_t* f_out;
+  u64* xc;                  // exchange words, zeroed before the launch
+  unsigned* err;
+  u64 limit;                // wait limit in 100 MHz ticks
+  u64* trace;               // [trace_steps][WR_TRACE_SLOTS] phase timestamps or null
+  int64_t trace_steps;
+};
+
+// Kernel entry points (taken by address in the launcher).
+const void* wr_small_kernel_ptr();
+const void* wr_uniforms_kernel_ptr();
+const void* wr_persist_kernel_ptr(int cpl);
+const void* wr_fill_kernel_ptr();

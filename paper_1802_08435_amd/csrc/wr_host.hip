@@ -1,0 +1,517 @@
+// Host side of libwavernn: validation, weight packing, launch plans, C ABI.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "wavernn.h"
+#include "wr_args.h"
+#include "wr_layout.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+wavernn_status fail(wavernn_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+wavernn_status fail(wavernn_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define HIPOK(call)                                                                        \
+  do {                                                                                     \
+    hipError_t e_ = (call);                                                                \
+    if (e_ != hipSuccess) return fail(WAVERNN_E_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+uint16_t f2bf(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+float bf2f(uint16_t b) {
+  uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+enum Path { PATH_SMALL = 0, PATH_PERSIST = 1, PATH_BATCHED = 2 };
+
+const u64 kWaitTicks = 200000000ull;  // 2 s of the 100 MHz clock per wait
+
+}  // namespace
+
+struct wavernn_model {
+  wavernn_config cfg;
+  int device = 0;
+  Path path = PATH_SMALL;
+  std::vector<void*> allocs;
+  unsigned* d_err = nullptr;
+  // small path
+  float* d_image = nullptr;
+  float* d_Wc = nullptr;
+  SmallLayout sl;
+  // persistent path
+  PersistPlan plan;
+  uint4 *d_wu = nullptr, *d_whc = nullptr, *d_whf = nullptr;
+  float *d_I = nullptr, *d_bias = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr, *d_b4 = nullptr;
+  u64* d_xc = nullptr;
+  int cpl = 0;
+  u64* trace = nullptr;
+  int64_t trace_steps = 0;
+
+  template <typename T>
+  wavernn_status alloc(T** p, size_t bytes) {
+    void* q = nullptr;
+    if (hipMalloc(&q, bytes ? bytes : 16) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(WAVERNN_E_OOM, "device allocation of %zu bytes failed", bytes);
+    }
+    allocs.push_back(q);
+    *p = (T*)q;
+    return WAVERNN_OK;
+  }
+  template <typename T>
+  wavernn_status upload(T** p, const void* host, size_t bytes) {
+    wavernn_status s = alloc(p, bytes);
+    if (s != WAVERNN_OK) return s;
+    HIPOK(hipMemcpy(*p, host, bytes, hipMemcpyHostToDevice));
+    return WAVERNN_OK;
+  }
+  ~wavernn_model() {
+    for (void* q : allocs) (void)hipFree(q);
+  }
+};
+
+namespace {
+
+// Weight value as the model stores it (bf16-rounded in BF16 mode).
+struct Rounder {
+  bool bf16;
+  float operator()(float v) const { return bf16 ? bf2f(f2bf(v)) : v; }
+};
+
+wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w) {
+  if (!c || !w) return fail(WAVERNN_E_INVALID, "null config or weights");
+  if (c->hidden <= 0 || (c->hidden & 1)) return fail(WAVERNN_E_INVALID, "hidden must be positive and even (got %d)", c->hidden);
+  if (c->hidden > 4096) return fail(WAVERNN_E_INVALID, "hidden %d above 4096", c->hidden);
+  if (c->cond_dim < 0 || c->cond_dim > 1024) return fail(WAVERNN_E_INVALID, "cond_dim %d out of range", c->cond_dim);
+  if (c->cond_dim > 0 && c->frame_len <= 0) return fail(WAVERNN_E_INVALID, "frame_len must be > 0 with conditioning");
+  if (c->subscale < 1 || c->subscale > 64) return fail(WAVERNN_E_INVALID, "subscale %d out of range", c->subscale);
+  if (c->subscale == 1 && c->ctx_dim != 0) return fail(WAVERNN_E_INVALID, "ctx_dim must be 0 when subscale is 1");
+  if (c->subscale > 1 && (c->ctx_dim <= 0 || (c->ctx_dim & 1) || c->ctx_dim > 1024))
+    return fail(WAVERNN_E_INVALID, "ctx_dim must be even and in (0, 1024] with subscale");
+  if (c->weight_dtype != WAVERNN_F32 && c->weight_dtype != WAVERNN_BF16) return fail(WAVERNN_E_INVALID, "bad weight_dtype");
+  if (c->r_format < WAVERNN_R_DENSE || c->r_format > WAVERNN_R_BSR_16X1) return fail(WAVERNN_E_INVALID, "bad r_format");
+  if (c->max_streams < 1 || c->max_streams > 64) return fail(WAVERNN_E_INVALID, "max_streams must be in [1, 64]");
+  if (!w->R || !w->I || !w->b || !w->O1 || !w->b1 || !w->O2 || !w->b2 || !w->O3 || !w->b3 || !w->O4 || !w->b4)
+    return fail(WAVERNN_E_INVALID, "a required weight array is null");
+  if (c->cond_dim > 0 && !w->W_cond) return fail(WAVERNN_E_INVALID, "W_cond is null with cond_dim > 0");
+  if (c->ctx_dim > 0 && !w->W_ctx) return fail(WAVERNN_E_INVALID, "W_ctx is null with ctx_dim > 0");
+  if (c->r_format != WAVERNN_R_DENSE) {
+    int bh = c->r_format == WAVERNN_R_BSR_4X4 ? 4 : 16, bw = c->r_format == WAVERNN_R_BSR_4X4 ? 4 : 1;
+    if (c->hidden % bh || c->hidden % bw) return fail(WAVERNN_E_INVALID, "hidden not a multiple of the block shape");
+    if (!w->R_block_mask) return fail(WAVERNN_E_INVALID, "R_block_mask is null for a block-sparse format");
+  }
+  return WAVERNN_OK;
+}
+
+// Effective dense R entry (pruned blocks read as zero).
+struct REff {
+  const wavernn_config* c;
+  const wavernn_weights* w;
+  float operator()(int row, int col) const {
+    const int H = c->hidden;
+    if (c->r_format != WAVERNN_R_DENSE) {
+      int bh = c->r_format == WAVERNN_R_BSR_4X4 ? 4 : 16, bw = c->r_format == WAVERNN_R_BSR_4X4 ? 4 : 1;
+      int g = row / H, i = row % H;
+      size_t mi = ((size_t)g * (H / bh) + i / bh) * (H / bw) + col / bw;
+      if (!w->R_block_mask[mi]) return 0.0f;
+    }
+    return w->R[(size_t)row * H + col];
+  }
+};
+
+wavernn_status build_small(wavernn_model* m, const wavernn_weights* w) {
+  const wavernn_config& c = m->cfg;
+  const int H = c.hidden, Hh = H / 2;
+  const SmallLayout L = small_layout(H);
+  m->sl = L;
+  Rounder rd{c.weight_dtype == WAVERNN_BF16};
+  REff R{&m->cfg, w};
+  std::vector<float> img(L.image_floats, 0.0f);
+  for (int row = 0; row < 3 * H; ++row)
+    for (int j = 0; j < H; ++j) img[L.Rt + (size_t)j * 3 * H + row] = rd(R(row, j));
+  for (int row = 0; row < 3 * H; ++row) {
+    int i = row % H;
+    for (int q = 0; q < 3; ++q) img[L.I + row * 3 + q] = (q == 2 && i < Hh) ? 0.0f : rd(w->I[row * 3 + q]);
+    img[L.bias + row] = rd(w->b[row]);
+  }
+  for (int k = 0; k < Hh; ++k)
+    for (int j = 0; j < Hh; ++j) {
+      img[L.O1t + j * Hh + k] = rd(w->O1[(size_t)k * Hh + j]);
+      img[L.O3t + j * Hh + k] = rd(w->O3[(size_t)k * Hh + j]);
+    }
+  for (int v = 0; v < 256; ++v)
+    for (int j = 0; j < Hh; ++j) {
+      img[L.O2t + j * 256 + v] = rd(w->O2[(size_t)v * Hh + j]);
+      img[L.O4t + j * 256 + v] = rd(w->O4[(size_t)v * Hh + j]);
+    }
+  for (int k = 0; k < Hh; ++k) {
+    img[L.b1 + k] = rd(w->b1[k]);
+    img[L.b3 + k] = rd(w->b3[k]);
+  }
+  for (int v = 0; v < 256; ++v) {
+    img[L.b2 + v] = rd(w->b2[v]);
+    img[L.b4 + v] = rd(w->b4[v]);
+  }
+  wavernn_status s = m->upload(&m->d_image, img.data(), img.size() * 4);
+  if (s != WAVERNN_OK) return s;
+  if (c.cond_dim > 0) {
+    std::vector<float> wc((size_t)3 * H * c.cond_dim);
+    for (size_t i = 0; i < wc.size(); ++i) wc[i] = rd(w->W_cond[i]);
+    s = m->upload(&m->d_Wc, wc.data(), wc.size() * 4);
+    if (s != WAVERNN_OK) return s;
+  }
+  HIPOK(hipFuncSetAttribute(wr_small_kernel_ptr(), hipFuncAttributeMaxDynamicSharedMemorySize, L.total_floats * 4));
+  return WAVERNN_OK;
+}
+
+wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
+  const wavernn_config& c = m->cfg;
+  const PersistPlan& P = m->plan;
+  const int H = P.H, Hh = P.Hh, SEG = P.SEG, CPL = P.CPL, UC = WR_UC;
+  Rounder rd{true};
+  REff R{&m->cfg, w};
+  // U blocks
+  std::vector<uint16_t> ub((size_t)P.NU * P.u_bytes / 2);
+  for (int k = 0; k < P.NU; ++k) {
+    uint16_t* blk = ub.data() + (size_t)k * P.u_bytes / 2;
+    for (int ih = 0; ih < 2; ++ih)
+      for (int rb = 0; rb < 6; ++rb) {
+        int g = rb / 2, half = rb % 2;
+        for (int i = 0; i < CPL; ++i)
+          for (int l = 0; l < 64; ++l) {
+            int r = l / 8, q = l % 8;
+            int row = g * H + half * Hh + k * UC + r;
+            uint16_t* d = blk + ((size_t)((ih * 6 + rb) * CPL + i) * 64 + l) * 8;
+            for (int e = 0; e < 8; ++e) d[e] = f2bf(R(row, ih * Hh + q * SEG + 8 * i + e));
+          }
+      }
+  }
+  // head blocks: first layer rows (padded), second layer columns
+  auto pack_head = [&](const float* O1, const float* O2, std::vector<uint16_t>& out) {
+    out.assign((size_t)P.NC * P.h_bytes / 2, 0);
+    for (int j = 0; j < P.NC; ++j) {
+      uint16_t* blk = out.data() + (size_t)j * P.h_bytes / 2;
+      for (int rb = 0; rb < P.HCP / 8; ++rb)
+        for (int i = 0; i < CPL; ++i)
+          for (int l = 0; l < 64; ++l) {
+            int r = rb * 8 + l / 8, q = l % 8;
+            uint16_t* d = blk + ((size_t)(rb * CPL + i) * 64 + l) * 8;
+            for (int e = 0; e < 8; ++e)
+              d[e] = r < P.HCR ? f2bf(O1[(size_t)(j * P.HCR + r) * Hh + q * SEG + 8 * i + e]) : 0;
+          }
+      uint16_t* blk2 = blk + P.h1_bytes / 2;
+      for (int kb = 0; kb < P.HCP / 8; ++kb)
+        for (int v = 0; v < 256; ++v)
+          for (int e = 0; e < 8; ++e) {
+            int kk = kb * 8 + e;
+            blk2[((size_t)kb * 256 + v) * 8 + e] = kk < P.HCR ? f2bf(O2[(size_t)v * Hh + j * P.HCR + kk]) : 0;
+          }
+    }
+  };
+  std::vector<uint16_t> hc, hf;
+  pack_head(w->O1, w->O2, hc);
+  pack_head(w->O3, w->O4, hf);
+  wavernn_status s;
+  if ((s = m->upload(&m->d_wu, ub.data(), ub.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_whc, hc.data(), hc.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_whf, hf.data(), hf.size() * 2)) != WAVERNN_OK) return s;
+  std::vector<float> Iv((size_t)9 * H), bv((size_t)3 * H);
+  for (int row = 0; row < 3 * H; ++row) {
+    for (int q = 0; q < 3; ++q) Iv[row * 3 + q] = (q == 2 && row % H < Hh) ? 0.0f : rd(w->I[row * 3 + q]);
+    bv[row] = rd(w->b[row]);
+  }
+  std::vector<float> b1(Hh), b2(256), b3(Hh), b4(256);
+  for (int k = 0; k < Hh; ++k) b1[k] = rd(w->b1[k]), b3[k] = rd(w->b3[k]);
+  for (int v = 0; v < 256; ++v) b2[v] = rd(w->b2[v]), b4[v] = rd(w->b4[v]);
+  if ((s = m->upload(&m->d_I, Iv.data(), Iv.size() * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_bias, bv.data(), bv.size() * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_b1, b1.data(), Hh * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_b2, b2.data(), 256 * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_b3, b3.data(), Hh * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_b4, b4.data(), 256 * 4)) != WAVERNN_OK) return s;
+  if (c.cond_dim > 0) {
+    std::vector<float> wc((size_t)3 * H * c.cond_dim);
+    for (size_t i = 0; i < wc.size(); ++i) wc[i] = rd(w->W_cond[i]);
+    if ((s = m->upload(&m->d_Wc, wc.data(), wc.size() * 4)) != WAVERNN_OK) return s;
+  }
+  if ((s = m->alloc(&m->d_xc, (size_t)P.x_words * 8)) != WAVERNN_OK) return s;
+  m->cpl = CPL;
+  const void* kp = wr_persist_kernel_ptr(CPL);
+  if (!kp) return fail(WAVERNN_E_UNSUPPORTED, "no persistent kernel for %d chunks per lane", CPL);
+  HIPOK(hipFuncSetAttribute(kp, hipFuncAttributeMaxDynamicSharedMemorySize, P.lds));
+  int per_cu = 0;
+  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kp, WR_THREADS, P.lds));
+  hipDeviceProp_t prop;
+  HIPOK(hipGetDeviceProperties(&prop, m->device));
+  if (per_cu < 1 || per_cu * prop.multiProcessorCount < P.NU + 2 * P.NC)
+    return fail(WAVERNN_E_UNSUPPORTED, "persistent grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)",
+                P.NU + 2 * P.NC, per_cu, prop.multiProcessorCount);
+  return WAVERNN_OK;
+}
+
+wavernn_status launch_fill(u64* p, int64_t n, hipStream_t st) {
+  int64_t nb = (n + 255) / 256;
+  u64 zero = 0;
+  void* args[] = {&p, &n, &zero};
+  HIPOK(hipLaunchKernel(wr_fill_kernel_ptr(), dim3((unsigned)nb), dim3(256), args, 0, st));
+  return WAVERNN_OK;
+}
+
+struct RunIO {
+  int32_t S;
+  int64_t T;
+  const float* cond;
+  int64_t n_frames;
+  uint64_t seed;
+  const wavernn_state* init;
+  const wavernn_state* fin;
+  const uint16_t* target;
+  uint16_t* out;
+  float* zc;
+  float* zf;
+  float* nll;
+  hipStream_t st;
+};
+
+wavernn_status validate_run(wavernn_model* m, const RunIO& io) {
+  if (!m) return fail(WAVERNN_E_INVALID, "null model");
+  const wavernn_config& c = m->cfg;
+  if (io.S < 1 || io.S > c.max_streams) return fail(WAVERNN_E_INVALID, "n_streams %d not in [1, %d]", io.S, c.max_streams);
+  if (io.T < 0) return fail(WAVERNN_E_INVALID, "negative n_samples");
+  if (io.T > ((int64_t)1 << 31)) return fail(WAVERNN_E_INVALID, "n_samples above 2^31");
+  if (c.subscale > 1 && io.T % c.subscale) return fail(WAVERNN_E_INVALID, "n_samples not a multiple of subscale");
+  const int64_t t0 = io.init ? io.init->t0 : 0;
+  if (t0 < 0) return fail(WAVERNN_E_INVALID, "negative t0");
+  if (c.subscale > 1 && t0 != 0) return fail(WAVERNN_E_INVALID, "t0 must be 0 with subscale");
+  if (io.init && (!io.init->h || !io.init->c_prev || !io.init->f_prev))
+    return fail(WAVERNN_E_INVALID, "init state has a null pointer");
+  if (io.fin && (!io.fin->h || !io.fin->c_prev || !io.fin->f_prev))
+    return fail(WAVERNN_E_INVALID, "final state has a null pointer");
+  if (c.cond_dim > 0) {
+    if (!io.cond) return fail(WAVERNN_E_INVALID, "cond is null with cond_dim > 0");
+    int64_t need = io.T > 0 ? (t0 + io.T - 1) / c.frame_len + 1 : 0;
+    if (io.n_frames < need) return fail(WAVERNN_E_INVALID, "n_frames %lld < %lld frames needed", (long long)io.n_frames, (long long)need);
+  }
+  if (io.T > 0 && !io.target && !io.out) return fail(WAVERNN_E_INVALID, "out is null");
+  return WAVERNN_OK;
+}
+
+wavernn_status run_small(wavernn_model* m, const RunIO& io) {
+  SmallArgs a;
+  memset(&a, 0, sizeof a);
+  a.image = m->d_image;
+  a.Wc = m->d_Wc;
+  a.feat = io.cond;
+  a.n_frames = io.n_frames;
+  a.H = m->cfg.hidden;
+  a.Dc = m->cfg.cond_dim;
+  a.frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
+  a.T = io.T;
+  a.t0 = io.init ? io.init->t0 : 0;
+  a.seed = io.seed;
+  a.target = io.target;
+  a.out = io.out;
+  a.zc_out = io.zc;
+  a.zf_out = io.zf;
+  a.nll_out = io.nll;
+  if (io.init) { a.h_in = io.init->h; a.c_in = io.init->c_prev; a.f_in = io.init->f_prev; }
+  if (io.fin) { a.h_out = io.fin->h; a.c_out = io.fin->c_prev; a.f_out = io.fin->f_prev; }
+  void* args[] = {&a};
+  HIPOK(hipLaunchKernel(wr_small_kernel_ptr(), dim3(io.S), dim3(256), args, m->sl.total_floats * 4, io.st));
+  return WAVERNN_OK;
+}
+
+wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
+  const PersistPlan& P = m->plan;
+  const int H = P.H;
+  for (int s = 0; s < io.S; ++s) {
+    wavernn_status st = launch_fill(m->d_xc, P.x_words, io.st);
+    if (st != WAVERNN_OK) return st;
+    PersistArgs a;
+    memset(&a, 0, sizeof a);
+    a.P = P;
+    a.wu = m->d_wu;
+    a.whc = m->d_whc;
+    a.whf = m->d_whf;
+    a.Iw = m->d_I;
+    a.bias = m->d_bias;
+    a.b1 = m->d_b1;
+    a.b2 = m->d_b2;
+    a.b3 = m->d_b3;
+    a.b4 = m->d_b4;
+    a.Wc = m->d_Wc;
+    a.Dc = m->cfg.cond_dim;
+    a.frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
+    a.feat = io.cond ? io.cond + (size_t)s * io.n_frames * m->cfg.cond_dim : nullptr;
+    a.n_frames = io.n_frames;
+    a.T = io.T;
+    a.t0 = io.init ? io.init->t0 : 0;
+    a.seed = io.seed;
+    a.stream_id = (uint64_t)s;
+    a.target = io.target ? io.target + (size_t)s * io.T : nullptr;
+    a.out = io.out ? io.out + (size_t)s * io.T : nullptr;
+    a.zc_out = io.zc ? io.zc + (size_t)s * io.T * 256 : nullptr;
+    a.zf_out = io.zf ? io.zf + (size_t)s * io.T * 256 : nullptr;
+    a.nll_out = io.nll ? io.nll + (size_t)s * io.T : nullptr;
+    if (io.init) { a.h_in = io.init->h + (size_t)s * H; a.c_in = io.init->c_prev + s; a.f_in = io.init->f_prev + s; }
+    if (io.fin) { a.h_out = io.fin->h + (size_t)s * H; a.c_out = io.fin->c_prev + s; a.f_out = io.fin->f_prev + s; }
+    a.xc = m->d_xc;
+    a.err = m->d_err;
+    a.limit = kWaitTicks;
+    if (s == 0) {
+      a.trace = m->trace;
+      a.trace_steps = m->trace ? m->trace_steps : 0;
+    }
+    void* args[] = {&a};
+    HIPOK(hipLaunchCooperativeKernel(wr_persist_kernel_ptr(m->cpl), dim3(P.NU + P.NC + P.NF), dim3(WR_THREADS), args,
+                                     P.lds, io.st));
+  }
+  return WAVERNN_OK;
+}
+
+wavernn_status run(wavernn_model* m, RunIO& io) {
+  wavernn_status s = validate_run(m, io);
+  if (s != WAVERNN_OK) return s;
+  if (io.T == 0) return WAVERNN_OK;
+  int dev = 0;
+  HIPOK(hipGetDevice(&dev));
+  if (dev != m->device) return fail(WAVERNN_E_INVALID, "model lives on device %d, current device is %d", m->device, dev);
+  if (m->path == PATH_SMALL) return run_small(m, io);
+  if (m->path == PATH_PERSIST) return run_persist(m, io);
+  return fail(WAVERNN_E_UNSUPPORTED, "no kernel for this configuration");
+}
+
+}  // namespace
+
+extern "C" {
+
+wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* w, wavernn_model** out) {
+  if (!out) return fail(WAVERNN_E_INVALID, "null output handle");
+  *out = nullptr;
+  wavernn_status s = validate_config(cfg, w);
+  if (s != WAVERNN_OK) return s;
+  wavernn_model* m = new (std::nothrow) wavernn_model();
+  if (!m) return fail(WAVERNN_E_OOM, "host allocation failed");
+  m->cfg = *cfg;
+  if (hipGetDevice(&m->device) != hipSuccess) {
+    delete m;
+    return fail(WAVERNN_E_HIP, "no HIP device");
+  }
+  const int H = cfg->hidden;
+  const SmallLayout L = small_layout(H);
+  const bool small_fits = (size_t)L.total_floats * 4 + 256 <= 160 * 1024;
+  if (cfg->subscale > 1) {
+    s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling is not available in this build");
+  } else if (small_fits) {
+    m->path = PATH_SMALL;
+    s = build_small(m, w);
+  } else if (persist_plan(H, &m->plan)) {
+    if (cfg->weight_dtype != WAVERNN_BF16) {
+      s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d needs bf16 weights (fp32 weights fit LDS only for small models)", H);
+    } else {
+      m->path = PATH_PERSIST;
+      s = build_persist(m, w);
+    }
+  } else {
+    s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no kernel plan (need a multiple of 128 whose blocks fit LDS)", H);
+  }
+  if (s == WAVERNN_OK) {
+    s = m->alloc(&m->d_err, 64);
+    if (s == WAVERNN_OK && hipMemset(m->d_err, 0, 64) != hipSuccess) s = fail(WAVERNN_E_HIP, "hipMemset failed");
+  }
+  if (s != WAVERNN_OK) {
+    delete m;
+    return s;
+  }
+  *out = m;
+  return WAVERNN_OK;
+}
+
+void wavernn_destroy(wavernn_model* m) { delete m; }
+
+wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_samples, const float* cond_dev,
+                              int64_t n_frames, uint64_t seed, const wavernn_state* init, uint16_t* out_dev,
+                              const wavernn_state* final_state, void* stream) {
+  RunIO io{n_streams, n_samples, cond_dev, n_frames, seed, init, final_state, nullptr, out_dev,
+           nullptr, nullptr, nullptr, (hipStream_t)stream};
+  return run(m, io);
+}
+
+wavernn_status wavernn_score_teacher_forced(wavernn_model* m, int32_t n_streams, int64_t n_samples,
+                                            const float* cond_dev, int64_t n_frames, const uint16_t* target_dev,
+                                            const wavernn_state* init, float* logits_c_dev, float* logits_f_dev,
+                                            float* nll_dev, void* stream) {
+  if (!target_dev) return fail(WAVERNN_E_INVALID, "target is null");
+  RunIO io{n_streams, n_samples, cond_dev, n_frames, 0, init, nullptr, target_dev, nullptr,
+           logits_c_dev, logits_f_dev, nll_dev, (hipStream_t)stream};
+  return run(m, io);
+}
+
+wavernn_status wavernn_device_status(wavernn_model* m, void* stream) {
+  if (!m) return fail(WAVERNN_E_INVALID, "null model");
+  HIPOK(hipStreamSynchronize((hipStream_t)stream));
+  unsigned e[16];
+  HIPOK(hipMemcpy(e, m->d_err, sizeof e, hipMemcpyDeviceToHost));
+  if (e[0]) {
+    HIPOK(hipMemset(m->d_err, 0, 64));
+    return fail(WAVERNN_E_DEVICE, "kernel reported error bits 0x%x (1 = a bounded wait expired)", e[0]);
+  }
+  return WAVERNN_OK;
+}
+
+wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t t0, int64_t n, float* out_dev,
+                                      void* stream) {
+  if (n < 0 || (n > 0 && !out_dev) || t0 < 0) return fail(WAVERNN_E_INVALID, "bad arguments");
+  if (n == 0) return WAVERNN_OK;
+  void* args[] = {&seed, &stream_id, &t0, &n, &out_dev};
+  HIPOK(hipLaunchKernel(wr_uniforms_kernel_ptr(), dim3((unsigned)((n + 255) / 256)), dim3(256), args, 0,
+                        (hipStream_t)stream));
+  return WAVERNN_OK;
+}
+
+int32_t wavernn_model_path(const wavernn_model* m, int32_t* grid, int32_t* block) {
+  if (!m) return -1;
+  int g = 0, b = 0;
+  if (m->path == PATH_SMALL) g = 1, b = 256;
+  else if (m->path == PATH_PERSIST) g = m->plan.NU + m->plan.NC + m->plan.NF, b = WR_THREADS;
+  if (grid) *grid = g;
+  if (block) *block = b;
+  return (int32_t)m->path;
+}
+
+wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps) {
+  if (!m || max_steps < 0 || (max_steps > 0 && !trace_dev)) return fail(WAVERNN_E_INVALID, "bad trace arguments");
+  m->trace = max_steps > 0 ? (u64*)trace_dev : nullptr;
+  m->trace_steps = max_steps;
+  return WAVERNN_OK;
+}
+
+const char* wavernn_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,79 @@
+"""libwavernn loads and exports the C ABI; host-side validation (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1802_08435_amd import synth
+from paper_1802_08435_amd import wavernn as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "wavernn.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(wavernn_[a-z_]+)\s*\(", txt)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ("wavernn_create", "wavernn_sample", "wavernn_score_teacher_forced", "wavernn_destroy",
+              "wavernn_last_error", "wavernn_device_status", "wavernn_debug_uniforms"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = W.lib()
+    for n in _declared():
+        assert hasattr(L, n), n
+
+
+def _cfg(**kw):
+    d = dict(hidden=64, cond_dim=0, frame_len=120, subscale=1, ctx_dim=0, weight_dtype=W.F32,
+             r_format=W.R_DENSE, max_streams=1)
+    d.update(kw)
+    return W.Config(**d)
+
+
+def _weights(H=64):
+    w = synth.make_weights(H)
+    keep = {k: np.ascontiguousarray(w[k], np.float32) for k in ("R", "I", "b", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")}
+    fp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    ws = W.Weights(fp(keep["R"]), None, fp(keep["I"]), fp(keep["b"]), None, None,
+                   *[fp(keep[k]) for k in ("O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")])
+    return ws, keep
+
+
+@pytest.mark.parametrize("bad,msg", [
+    (dict(hidden=63), "even"), (dict(hidden=0), "even"), (dict(max_streams=0), "max_streams"),
+    (dict(max_streams=65), "max_streams"), (dict(cond_dim=8, frame_len=0), "frame_len"),
+    (dict(weight_dtype=7), "weight_dtype"), (dict(r_format=9), "r_format"),
+    (dict(subscale=1, ctx_dim=4), "ctx_dim"), (dict(subscale=16, ctx_dim=0), "ctx_dim"),
+    (dict(cond_dim=8), "W_cond"), (dict(r_format=W.R_BSR_4X4), "R_block_mask"),
+])
+def test_create_rejects_bad_config_before_touching_the_device(bad, msg):
+    L = W.lib()
+    ws, keep = _weights()
+    h = ctypes.c_void_p()
+    st = L.wavernn_create(ctypes.byref(_cfg(**bad)), ctypes.byref(ws), ctypes.byref(h))
+    assert st == W.E_INVALID
+    assert msg in L.wavernn_last_error().decode()
+    assert not h.value
+
+
+def test_null_arguments_are_rejected():
+    L = W.lib()
+    ws, keep = _weights()
+    h = ctypes.c_void_p()
+    assert L.wavernn_create(None, ctypes.byref(ws), ctypes.byref(h)) == W.E_INVALID
+    assert L.wavernn_create(ctypes.byref(_cfg()), None, ctypes.byref(h)) == W.E_INVALID
+    assert L.wavernn_create(ctypes.byref(_cfg()), ctypes.byref(ws), None) == W.E_INVALID
+    ws.O3 = None
+    assert L.wavernn_create(ctypes.byref(_cfg()), ctypes.byref(ws), ctypes.byref(h)) == W.E_INVALID
+    assert L.wavernn_sample(None, 1, 10, None, 0, 1, None, None, None, None) == W.E_INVALID
+    assert L.wavernn_score_teacher_forced(None, 1, 10, None, 0, None, None, None, None, None, None) == W.E_INVALID
+    assert L.wavernn_debug_uniforms(1, 0, 0, -1, None, None) == W.E_INVALID
+    L.wavernn_destroy(None)
