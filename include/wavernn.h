@@ -146,13 +146,12 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t* grid, int32_t* block
  * of the multi-workgroup persistent kernel record, for the first max_steps
  * steps of the first utterance, timestamps of the 100 MHz constant clock at
  * the end of each phase of a step into trace_dev [max_steps][32] (device
- * memory the caller owns and keeps alive while tracing is on).  Slots 0-10:
- * unit workgroup 0 (step start, coarse gates published, y_c gathered,
- * R.y_c done, coarse logits summed, c drawn, fine gates published, y_f
- * gathered, R.y_f done, fine logits summed, f drawn); 16-18 / 20-22: coarse /
- * fine head workgroup 0 (input gathered, first layer done, partials
- * published); 25-26: the last unit workgroup's y_c published / gathered.
- * max_steps = 0 turns tracing off.  Other kernels ignore the setting. */
+ * memory the caller owns and keeps alive while tracing is on).  Slot 0 is
+ * the start of the step on head workgroup 0; the other slots are the ends of
+ * the phases of that step (gates, hidden layers, partial logits published,
+ * logits summed, draws) on head workgroup 0 or on the last head workgroup;
+ * unused slots stay zero.  max_steps = 0 turns tracing off.  Other kernels
+ * ignore the setting. */
 wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps);
 
 /* Description of the last error on this thread ("" if none). */

@@ -30,17 +30,18 @@ struct SmallArgs {
 
 struct PersistArgs {
   PersistPlan P;
-  const uint4* wu;      // NU U blocks of P.u_bytes
-  const uint4* whc;     // NC head blocks of P.h_bytes (O1 rows + O2 columns)
-  const uint4* whf;     // NF head blocks (O3 / O4)
-  const float* Iw;      // [3H][3], I* mask applied
-  const float* bias;    // [3H]
-  const float* b1;      // [Hh]
-  const float* b2;      // [256]
+  const uint4* wh;          // NH head blocks of P.h_bytes
+  const uint4* wu;          // NU unit blocks of P.u_bytes
+  const uint4* o2s;         // [NH][16 class tiles][64 lanes] O2 column-slice fragments
+  const uint4* o4s;         // [NH][16][64] O4 column-slice fragments
+  const float* Iw;          // [3H][3], I* mask applied
+  const float* bias;        // [3H]
+  const float* b1;          // [Hh]
+  const float* b2;          // [256]
   const float* b3;
   const float* b4;
-  const float* Wc;      // [3H][Dc] fp32 or null
-  const float* feat;    // [n_frames][Dc] of this utterance or null
+  const float* Wc;          // [3H][Dc] fp32 or null
+  const float* feat;        // [n_frames][Dc] of this utterance or null
   int64_t n_frames;
   int Dc, frame_len;
   int64_t T, t0;
@@ -66,5 +67,5 @@ struct PersistArgs {
 // Kernel entry points (taken by address in the launcher).
 const void* wr_small_kernel_ptr();
 const void* wr_uniforms_kernel_ptr();
-const void* wr_persist_kernel_ptr(int cpl);
+const void* wr_persist_kernel_ptr();
 const void* wr_fill_kernel_ptr();

@@ -66,7 +66,8 @@ struct wavernn_model {
   SmallLayout sl;
   // persistent path
   PersistPlan plan;
-  uint4 *d_wu = nullptr, *d_whc = nullptr, *d_whf = nullptr;
+  uint4 *d_wu = nullptr, *d_wh = nullptr;
+  uint4 *d_o2s = nullptr, *d_o4s = nullptr;
   float *d_I = nullptr, *d_bias = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr, *d_b4 = nullptr;
   u64* d_xc = nullptr;
   int cpl = 0;
@@ -193,54 +194,54 @@ wavernn_status build_small(wavernn_model* m, const wavernn_weights* w) {
 wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
   const wavernn_config& c = m->cfg;
   const PersistPlan& P = m->plan;
-  const int H = P.H, Hh = P.Hh, SEG = P.SEG, CPL = P.CPL, UC = WR_UC;
+  const int H = P.H, Hh = P.Hh, KT = P.KT;
   Rounder rd{true};
   REff R{&m->cfg, w};
-  // U blocks
-  std::vector<uint16_t> ub((size_t)P.NU * P.u_bytes / 2);
-  for (int k = 0; k < P.NU; ++k) {
-    uint16_t* blk = ub.data() + (size_t)k * P.u_bytes / 2;
-    for (int ih = 0; ih < 2; ++ih)
-      for (int rb = 0; rb < 6; ++rb) {
-        int g = rb / 2, half = rb % 2;
-        for (int i = 0; i < CPL; ++i)
-          for (int l = 0; l < 64; ++l) {
-            int r = l / 8, q = l % 8;
-            int row = g * H + half * Hh + k * UC + r;
-            uint16_t* d = blk + ((size_t)((ih * 6 + rb) * CPL + i) * 64 + l) * 8;
-            for (int e = 0; e < 8; ++e) d[e] = f2bf(R(row, ih * Hh + q * SEG + 8 * i + e));
-          }
-      }
-  }
-  // head blocks: first layer rows (padded), second layer columns
-  auto pack_head = [&](const float* O1, const float* O2, std::vector<uint16_t>& out) {
-    out.assign((size_t)P.NC * P.h_bytes / 2, 0);
-    for (int j = 0; j < P.NC; ++j) {
-      uint16_t* blk = out.data() + (size_t)j * P.h_bytes / 2;
-      for (int rb = 0; rb < P.HCP / 8; ++rb)
-        for (int i = 0; i < CPL; ++i)
-          for (int l = 0; l < 64; ++l) {
-            int r = rb * 8 + l / 8, q = l % 8;
-            uint16_t* d = blk + ((size_t)(rb * CPL + i) * 64 + l) * 8;
-            for (int e = 0; e < 8; ++e)
-              d[e] = r < P.HCR ? f2bf(O1[(size_t)(j * P.HCR + r) * Hh + q * SEG + 8 * i + e]) : 0;
-          }
-      uint16_t* blk2 = blk + P.h1_bytes / 2;
-      for (int kb = 0; kb < P.HCP / 8; ++kb)
-        for (int v = 0; v < 256; ++v)
-          for (int e = 0; e < 8; ++e) {
-            int kk = kb * 8 + e;
-            blk2[((size_t)kb * 256 + v) * 8 + e] = kk < P.HCR ? f2bf(O2[(size_t)v * Hh + j * P.HCR + kk]) : 0;
-          }
-    }
+  // MFMA fragments (operand B of v_mfma_f32_16x16x32_bf16) of a matrix M(row, col):
+  // fragment (mt, kt) of `ktot` column tiles at dst + (mt*ktot + kt) * 512 bf16; lane l holds
+  // row rowof(16*mt + l%16), columns col0 + 32*kt + 8*(l/16) .. +7.
+  auto pack_frags = [&](uint16_t* dst, int mtiles, int ktot, auto&& M, auto&& rowof, int col0) {
+    for (int mt = 0; mt < mtiles; ++mt)
+      for (int kt = 0; kt < ktot; ++kt)
+        for (int l = 0; l < 64; ++l) {
+          int row = rowof(16 * mt + l % 16);
+          uint16_t* o = dst + ((size_t)(mt * ktot + kt) * 64 + l) * 8;
+          for (int e = 0; e < 8; ++e) o[e] = f2bf(M(row, col0 + 32 * kt + 8 * (l / 16) + e));
+        }
   };
-  std::vector<uint16_t> hc, hf;
-  pack_head(w->O1, w->O2, hc);
-  pack_head(w->O3, w->O4, hf);
+  auto Rm = [&](int row, int col) { return R(row, col); };
+  auto O1m = [&](int row, int col) { return w->O1[(size_t)row * Hh + col]; };
+  auto O3m = [&](int row, int col) { return w->O3[(size_t)row * Hh + col]; };
+  auto cr_row = [&](int cr) { return (cr / Hh) * H + cr % Hh; };        // coarse row -> R row
+  auto fr_row = [&](int fr) { return (fr / Hh) * H + Hh + fr % Hh; };   // fine row -> R row
+  // head blocks: O1 rows, O3 rows, R_c[:, fine] rows
+  std::vector<uint16_t> hb((size_t)P.NH * P.h_bytes / 2, 0);
+  for (int j = 0; j < P.NH; ++j) {
+    uint16_t* base = hb.data() + (size_t)j * P.h_bytes / 2;
+    pack_frags(base + P.hb_o1 / 2, WR_HR / 16, KT, O1m, [&](int r) { return j * WR_HR + r; }, 0);
+    pack_frags(base + P.hb_o3 / 2, WR_HR / 16, KT, O3m, [&](int r) { return j * WR_HR + r; }, 0);
+    pack_frags(base + P.hb_rcf / 2, WR_GR / 16, KT, Rm, [&](int r) { return cr_row(j * WR_GR + r); }, Hh);
+  }
+  // unit blocks: GA rows (coarse rows x coarse inputs), GF rows (fine rows x all inputs)
+  std::vector<uint16_t> ub((size_t)P.NU * P.u_bytes / 2, 0);
+  for (int k = 0; k < P.NU; ++k) {
+    uint16_t* base = ub.data() + (size_t)k * P.u_bytes / 2;
+    pack_frags(base + P.ub_ga / 2, WR_UR / 16, KT, Rm, [&](int r) { return cr_row(k * WR_UR + r); }, 0);
+    pack_frags(base + P.ub_gf / 2, WR_UR / 16, 2 * KT, Rm, [&](int r) { return fr_row(k * WR_UR + r); }, 0);
+  }
+  // O2 / O4 column slices per head as fragments: 16 class tiles x (this head's 32 rows)
+  std::vector<uint16_t> o2s((size_t)P.NH * 16 * 64 * 8), o4s(o2s.size());
+  for (int j = 0; j < P.NH; ++j) {
+    auto O2m = [&](int v, int k) { return w->O2[(size_t)v * Hh + j * WR_HR + k]; };
+    auto O4m = [&](int v, int k) { return w->O4[(size_t)v * Hh + j * WR_HR + k]; };
+    pack_frags(o2s.data() + (size_t)j * 16 * 512, 16, 1, O2m, [](int r) { return r; }, 0);
+    pack_frags(o4s.data() + (size_t)j * 16 * 512, 16, 1, O4m, [](int r) { return r; }, 0);
+  }
   wavernn_status s;
+  if ((s = m->upload(&m->d_wh, hb.data(), hb.size() * 2)) != WAVERNN_OK) return s;
   if ((s = m->upload(&m->d_wu, ub.data(), ub.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_whc, hc.data(), hc.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_whf, hf.data(), hf.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_o2s, o2s.data(), o2s.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_o4s, o4s.data(), o4s.size() * 2)) != WAVERNN_OK) return s;
   std::vector<float> Iv((size_t)9 * H), bv((size_t)3 * H);
   for (int row = 0; row < 3 * H; ++row) {
     for (int q = 0; q < 3; ++q) Iv[row * 3 + q] = (q == 2 && row % H < Hh) ? 0.0f : rd(w->I[row * 3 + q]);
@@ -261,17 +262,15 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
     if ((s = m->upload(&m->d_Wc, wc.data(), wc.size() * 4)) != WAVERNN_OK) return s;
   }
   if ((s = m->alloc(&m->d_xc, (size_t)P.x_words * 8)) != WAVERNN_OK) return s;
-  m->cpl = CPL;
-  const void* kp = wr_persist_kernel_ptr(CPL);
-  if (!kp) return fail(WAVERNN_E_UNSUPPORTED, "no persistent kernel for %d chunks per lane", CPL);
+  const void* kp = wr_persist_kernel_ptr();
   HIPOK(hipFuncSetAttribute(kp, hipFuncAttributeMaxDynamicSharedMemorySize, P.lds));
   int per_cu = 0;
   HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kp, WR_THREADS, P.lds));
   hipDeviceProp_t prop;
   HIPOK(hipGetDeviceProperties(&prop, m->device));
-  if (per_cu < 1 || per_cu * prop.multiProcessorCount < P.NU + 2 * P.NC)
+  if (per_cu < 1 || per_cu * prop.multiProcessorCount < P.NH + P.NU)
     return fail(WAVERNN_E_UNSUPPORTED, "persistent grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)",
-                P.NU + 2 * P.NC, per_cu, prop.multiProcessorCount);
+                P.NH + P.NU, per_cu, prop.multiProcessorCount);
   return WAVERNN_OK;
 }
 
@@ -356,9 +355,10 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
     PersistArgs a;
     memset(&a, 0, sizeof a);
     a.P = P;
+    a.wh = m->d_wh;
     a.wu = m->d_wu;
-    a.whc = m->d_whc;
-    a.whf = m->d_whf;
+    a.o2s = m->d_o2s;
+    a.o4s = m->d_o4s;
     a.Iw = m->d_I;
     a.bias = m->d_bias;
     a.b1 = m->d_b1;
@@ -389,7 +389,7 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
       a.trace_steps = m->trace ? m->trace_steps : 0;
     }
     void* args[] = {&a};
-    HIPOK(hipLaunchCooperativeKernel(wr_persist_kernel_ptr(m->cpl), dim3(P.NU + P.NC + P.NF), dim3(WR_THREADS), args,
+    HIPOK(hipLaunchCooperativeKernel(wr_persist_kernel_ptr(), dim3(P.NH + P.NU), dim3(WR_THREADS), args,
                                      P.lds, io.st));
   }
   return WAVERNN_OK;
@@ -499,7 +499,7 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t* grid, int32_t* block
   if (!m) return -1;
   int g = 0, b = 0;
   if (m->path == PATH_SMALL) g = 1, b = 256;
-  else if (m->path == PATH_PERSIST) g = m->plan.NU + m->plan.NC + m->plan.NF, b = WR_THREADS;
+  else if (m->path == PATH_PERSIST) g = m->plan.NH + m->plan.NU, b = WR_THREADS;
   if (grid) *grid = g;
   if (block) *block = b;
   return (int32_t)m->path;

@@ -56,37 +56,39 @@ WR_HD inline SmallLayout small_layout(int H) {
 // ---------------------------------------------------------------------------
 // Persistent multi-workgroup kernel.
 //
-// Roles: NU unit workgroups (U), NC coarse-head workgroups (HC), NF fine-head
-// workgroups (HF).  U workgroup k owns units [k*UC, k*UC+UC) of the coarse half
-// and the same offsets of the fine half, i.e. 6*UC rows of R (3 gates x 2
-// halves).  Local row lr = g*2*UC + half*UC + j  <->  R row g*H + half*H/2 + k*UC + j.
-// HC workgroup j owns rows [j*HC, j*HC+HC) of O1 and the matching columns of
-// O2 (a split of O2's inner dimension); HF likewise for O3 / O4.
+// Head workgroups (NH): head j evaluates the gates of every unit (redundantly,
+// identically in all heads), owns rows [j*HR, j*HR+HR) of O1 and O3, the
+// matching columns of O2 and O4, and coarse rows [j*GR, j*GR+GR) of R's
+// fine-input half (R_c[:, fine], needed right after y_f is known).  Rows of R
+// are indexed per half: coarse row cr = g*Hh + i <-> R row g*H + i, fine row
+// fr = g*Hh + i <-> R row g*H + Hh + i (g = u, r, e).
+// Unit workgroups (NU): unit workgroup k owns coarse rows [k*UR, +UR) of R's
+// coarse-input half (GA rows) and fine rows [k*UR, +UR) of all of R (GF rows).
 //
-// Dense matrices are stored bf16 in "row-block" order: 8 rows x 8 lanes per
-// block, lane l = 8*r + q covers columns q*SEG .. q*SEG+SEG-1 of one half of
-// the input (SEG = K/8), in chunks of 8 bf16 (16 bytes):
-//   chunk(rb, i, l) at ((rb * CPL + i) * 64 + l) * 16 bytes,  CPL = SEG / 8.
-// A wave reading chunk i of a block touches 64 consecutive 16-byte slots.
+// Matrices are stored bf16 as MFMA fragments (v_mfma_f32_16x16x32_bf16 with
+// the matrix as operand B): fragment (mt, kt) covers rows 16*mt .. 16*mt+15 and
+// input columns 32*kt .. 32*kt+31; lane l holds row 16*mt + l%16, columns
+// 32*kt + 8*(l/16) .. +7 (16 bytes).  A fragment is 1 KiB, lanes in order.
 // ---------------------------------------------------------------------------
-#define WR_UC 8           // units per half per U workgroup
-#define WR_THREADS 384    // 6 waves: one row-block of 8 rows per wave in U
+#define WR_THREADS 512    // 8 waves per workgroup
+#define WR_HR 32          // O1 / O3 rows per head workgroup (2 row tiles)
+#define WR_GR 96          // R_c[:, fine] rows per head workgroup (6 row tiles)
+#define WR_UR 32          // GA rows and GF rows per unit workgroup (2 row tiles)
 #define WR_XALIGN 64      // exchange regions aligned to 64 words (512 B)
+#define WR_MAXNH 16       // partial-logit sets summed per draw
+#define WR_FRAG 1024      // bytes per MFMA fragment
 
 struct PersistPlan {
-  int H, Hh, SEG, CPL;    // SEG = Hh / 8 columns per lane, CPL = SEG / 8 chunks
-  int NU, NC, NF;         // workgroups per role
-  int HCR, HCP;           // head rows per HC/HF workgroup, padded to 8
-  int u_rows;             // 6 * WR_UC
-  int u_half_bytes;       // one half (coarse or fine columns) of a U block
-  int u_bytes;            // U weight block bytes
-  int h1_bytes;           // head first-layer block bytes (HCP rows x Hh)
-  int h2_bytes;           // head second-layer block bytes (256 x HCP)
-  int h_bytes;            // h1 + h2
+  int H, Hh, KT;          // KT = Hh / 32 column tiles per input half
+  int NH, NU;
+  // head LDS block (bytes): O1 slice, O3 slice, R_c fine-half slice
+  int hb_o1, hb_o3, hb_rcf, h_bytes;
+  // unit LDS block (bytes): GA rows (coarse half), GF rows (both halves)
+  int ub_ga, ub_gf, u_bytes;
   // exchange words
-  int x_yc, x_yf, x_pc, x_pf, x_words;
+  int x_yc, x_yf, x_ga, x_gf, x_gcf, x_aec, x_aef, x_pc, x_pf, x_words;
   // LDS bytes
-  int lds_u, lds_h, lds;
+  int lds_h, lds_u, lds;
 };
 
 WR_HD inline int wr_rup(int x, int m) { return (x + m - 1) / m * m; }
@@ -95,32 +97,34 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   if (H <= 0 || H % 128) return false;
   P->H = H;
   P->Hh = H / 2;
-  P->SEG = P->Hh / 8;
-  P->CPL = P->SEG / 8;
-  if (P->Hh % WR_UC) return false;
-  P->NU = P->Hh / WR_UC;
-  // head split: at most 32 rows per head workgroup
-  int nc = 1;
-  while (P->Hh / nc > 32 || P->Hh % nc) ++nc;
-  if (nc > 16) return false;   // partial-logit sets read per draw
-  P->NC = P->NF = nc;
-  P->HCR = P->Hh / nc;
-  P->HCP = wr_rup(P->HCR, 8);
-  P->u_rows = 6 * WR_UC;
-  P->u_half_bytes = P->u_rows * P->Hh * 2;
-  P->u_bytes = 2 * P->u_half_bytes;
-  P->h1_bytes = P->HCP * P->Hh * 2;
-  P->h2_bytes = 256 * P->HCP * 2;
-  P->h_bytes = P->h1_bytes + P->h2_bytes;
-  P->x_yc = 0;
-  P->x_yf = wr_rup(P->Hh, WR_XALIGN);
-  P->x_pc = 2 * P->x_yf;
-  P->x_pf = P->x_pc + P->NC * 256;
-  P->x_words = P->x_pf + P->NF * 256;
-  // U: weights, h[H], Gc[3UC], Gf[2][3UC], add[6UC], I[6UC][3], z[256], misc
-  P->lds_u = P->u_bytes + 4 * (H + 3 * WR_UC + 6 * WR_UC + 6 * WR_UC + 18 * WR_UC + 256 + 64);
-  // H: weights, y[Hh], o[HCP], b[HCP], misc
-  P->lds_h = P->h_bytes + 4 * (P->Hh + 2 * P->HCP + 64);
-  P->lds = P->lds_u > P->lds_h ? P->lds_u : P->lds_h;
+  P->KT = P->Hh / 32;
+  if (P->Hh % WR_HR || (3 * P->Hh) % WR_UR) return false;
+  P->NH = P->Hh / WR_HR;
+  P->NU = 3 * P->Hh / WR_UR;
+  if (P->NH > WR_MAXNH || P->Hh > WR_THREADS) return false;
+  P->hb_o1 = 0;
+  P->hb_o3 = P->hb_o1 + (WR_HR / 16) * P->KT * WR_FRAG;
+  P->hb_rcf = P->hb_o3 + (WR_HR / 16) * P->KT * WR_FRAG;
+  P->h_bytes = P->hb_rcf + (WR_GR / 16) * P->KT * WR_FRAG;
+  P->ub_ga = 0;
+  P->ub_gf = (WR_UR / 16) * P->KT * WR_FRAG;
+  P->u_bytes = P->ub_gf + (WR_UR / 16) * 2 * P->KT * WR_FRAG;
+  int o = 0;
+  auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
+  P->x_yc = take(P->Hh);
+  P->x_yf = take(P->Hh);
+  P->x_ga = take(3 * P->Hh);
+  P->x_gf = take(3 * P->Hh);
+  P->x_gcf = take(3 * P->Hh);
+  P->x_aec = take(P->Hh);
+  P->x_aef = take(P->Hh);
+  P->x_pc = take(P->NH * 256);
+  P->x_pf = take(P->NH * 256);
+  P->x_words = o;
+  // head: weights, h[H], z[256], zh[256], op[8][32], rp[4][96], ov[32], bs[64], misc[16]
+  P->lds_h = P->h_bytes + 4 * (H + 256 + 256 + 8 * WR_HR + 4 * WR_GR + WR_HR + 64 + 16);
+  // unit: weights, y[H], partials[2][8][32], misc[16]
+  P->lds_u = P->u_bytes + 4 * (H + 2 * 8 * WR_UR + 16);
+  P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024;
 }
