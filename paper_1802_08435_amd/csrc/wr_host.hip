@@ -389,8 +389,10 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
       a.trace_steps = m->trace ? m->trace_steps : 0;
     }
     void* args[] = {&a};
-    HIPOK(hipLaunchCooperativeKernel(wr_persist_kernel_ptr(), dim3(P.NH + P.NU), dim3(WR_THREADS), args,
-                                     P.lds, io.st));
+    // An ordinary launch: create() checked that the whole grid fits on the
+    // device at once, and every cross-workgroup wait is bounded, so a grid
+    // that did not become co-resident ends with an error, never a hang.
+    HIPOK(hipLaunchKernel(wr_persist_kernel_ptr(), dim3(P.NH + P.NU), dim3(WR_THREADS), args, P.lds, io.st));
   }
   return WAVERNN_OK;
 }
