@@ -30,20 +30,17 @@ struct SmallArgs {
 
 struct PersistArgs {
   PersistPlan P;
-  const uint4* wh;          // NH head blocks of P.h_bytes
-  const uint4* wu;          // NU unit blocks of P.u_bytes
-  const uint4* o2s;         // [NH][16 class tiles][64 lanes] O2 column-slice fragments
-  const uint4* o4s;         // [NH][16][64] O4 column-slice fragments
+  const uint4* hw;          // [NH][8 waves][hw_frags][64 lanes] head fragments
+  const uint4* uw;          // [NU] unit LDS blocks of P.u_lds_w bytes
+  const uint4* ur;          // [NU*UCT][KT][64] coarse tiles x fine columns (VGPR-resident)
   const float* Iw;          // [3H][3], I* mask applied
-  const float* bias;        // [3H]
   const float* b1;          // [Hh]
   const float* b2;          // [256]
   const float* b3;
   const float* b4;
-  const float* Wc;          // [3H][Dc] fp32 or null
-  const float* feat;        // [n_frames][Dc] of this utterance or null
-  int64_t n_frames;
-  int Dc, frame_len;
+  const float* cb;          // [n_cb][3H] gate bias + conditioning per frame
+  int64_t n_cb;
+  int frame_len;
   int64_t T, t0;
   uint64_t seed, stream_id;
   const uint16_t* target;   // [T] or null
@@ -67,5 +64,6 @@ struct PersistArgs {
 // Kernel entry points (taken by address in the launcher).
 const void* wr_small_kernel_ptr();
 const void* wr_uniforms_kernel_ptr();
-const void* wr_persist_kernel_ptr();
+const void* wr_persist_kernel_ptr(int KH);   // null if no instantiation for KH
+const void* wr_cond_kernel_ptr();
 const void* wr_fill_kernel_ptr();

@@ -66,11 +66,12 @@ struct wavernn_model {
   SmallLayout sl;
   // persistent path
   PersistPlan plan;
-  uint4 *d_wu = nullptr, *d_wh = nullptr;
-  uint4 *d_o2s = nullptr, *d_o4s = nullptr;
+  const void* pk = nullptr;          // kernel instantiation for plan.KH
+  uint4 *d_hw = nullptr, *d_uw = nullptr, *d_ur = nullptr;
   float *d_I = nullptr, *d_bias = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr, *d_b4 = nullptr;
+  float* d_cb = nullptr;             // [cb_cap][3H] bias + conditioning per frame
+  int64_t cb_cap = 0;
   u64* d_xc = nullptr;
-  int cpl = 0;
   u64* trace = nullptr;
   int64_t trace_steps = 0;
 
@@ -194,54 +195,64 @@ wavernn_status build_small(wavernn_model* m, const wavernn_weights* w) {
 wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
   const wavernn_config& c = m->cfg;
   const PersistPlan& P = m->plan;
-  const int H = P.H, Hh = P.Hh, KT = P.KT;
+  const int H = P.H, Hh = P.Hh, KT = P.KT, KH = P.KH, UCT = P.UCT;
+  m->pk = wr_persist_kernel_ptr(KH);
+  if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no persistent kernel instantiation", H);
   Rounder rd{true};
   REff R{&m->cfg, w};
-  // MFMA fragments (operand B of v_mfma_f32_16x16x32_bf16) of a matrix M(row, col):
-  // fragment (mt, kt) of `ktot` column tiles at dst + (mt*ktot + kt) * 512 bf16; lane l holds
-  // row rowof(16*mt + l%16), columns col0 + 32*kt + 8*(l/16) .. +7.
-  auto pack_frags = [&](uint16_t* dst, int mtiles, int ktot, auto&& M, auto&& rowof, int col0) {
-    for (int mt = 0; mt < mtiles; ++mt)
-      for (int kt = 0; kt < ktot; ++kt)
-        for (int l = 0; l < 64; ++l) {
-          int row = rowof(16 * mt + l % 16);
-          uint16_t* o = dst + ((size_t)(mt * ktot + kt) * 64 + l) * 8;
-          for (int e = 0; e < 8; ++e) o[e] = f2bf(M(row, col0 + 32 * kt + 8 * (l / 16) + e));
-        }
+  // One MFMA fragment (operand B of v_mfma_f32_16x16x32_bf16) of a matrix M(row, col):
+  // lane l holds row rowof(l % 16), columns col0 + 8*(l/16) .. +7, as bf16.
+  auto frag = [&](uint16_t* dst, auto&& M, auto&& rowof, int col0) {
+    for (int l = 0; l < 64; ++l) {
+      const int row = rowof(l % 16);
+      for (int e = 0; e < 8; ++e) dst[l * 8 + e] = f2bf(M(row, col0 + 8 * (l / 16) + e));
+    }
   };
-  auto Rm = [&](int row, int col) { return R(row, col); };
-  auto O1m = [&](int row, int col) { return w->O1[(size_t)row * Hh + col]; };
-  auto O3m = [&](int row, int col) { return w->O3[(size_t)row * Hh + col]; };
-  auto cr_row = [&](int cr) { return (cr / Hh) * H + cr % Hh; };        // coarse row -> R row
-  auto fr_row = [&](int fr) { return (fr / Hh) * H + Hh + fr % Hh; };   // fine row -> R row
-  // head blocks: O1 rows, O3 rows, R_c[:, fine] rows
-  std::vector<uint16_t> hb((size_t)P.NH * P.h_bytes / 2, 0);
-  for (int j = 0; j < P.NH; ++j) {
-    uint16_t* base = hb.data() + (size_t)j * P.h_bytes / 2;
-    pack_frags(base + P.hb_o1 / 2, WR_HR / 16, KT, O1m, [&](int r) { return j * WR_HR + r; }, 0);
-    pack_frags(base + P.hb_o3 / 2, WR_HR / 16, KT, O3m, [&](int r) { return j * WR_HR + r; }, 0);
-    pack_frags(base + P.hb_rcf / 2, WR_GR / 16, KT, Rm, [&](int r) { return cr_row(j * WR_GR + r); }, Hh);
-  }
-  // unit blocks: GA rows (coarse rows x coarse inputs), GF rows (fine rows x all inputs)
-  std::vector<uint16_t> ub((size_t)P.NU * P.u_bytes / 2, 0);
+  auto O1m = [&](int r, int k) { return w->O1[(size_t)r * Hh + k]; };
+  auto O3m = [&](int r, int k) { return w->O3[(size_t)r * Hh + k]; };
+  auto O2m = [&](int v, int k) { return w->O2[(size_t)v * Hh + k]; };
+  auto O4m = [&](int v, int k) { return w->O4[(size_t)v * Hh + k]; };
+  auto Rm = [&](int r, int k) { return R(r, k); };
+  // heads: wave w of head j holds O1/O3 row tile 4j + (w & 3), column tiles
+  // (w >> 2)*KH .. +KH, and O2/O4 class tiles 2w, 2w+1 over columns 64j .. 64j+63
+  std::vector<uint16_t> hw((size_t)P.NH * 8 * P.hw_frags * 512);
+  for (int j = 0; j < P.NH; ++j)
+    for (int wv = 0; wv < 8; ++wv) {
+      uint16_t* d = hw.data() + (size_t)(j * 8 + wv) * P.hw_frags * 512;
+      const int r0 = 64 * j + 16 * (wv & 3), k0 = 32 * (wv >> 2) * KH;
+      for (int i = 0; i < KH; ++i) {
+        frag(d + (size_t)i * 512, O1m, [&](int r) { return r0 + r; }, k0 + 32 * i);
+        frag(d + (size_t)(KH + i) * 512, O3m, [&](int r) { return r0 + r; }, k0 + 32 * i);
+      }
+      for (int i = 0; i < 4; ++i) {
+        const int v0 = 16 * (2 * wv + (i >> 1)), col = 64 * j + 32 * (i & 1);
+        frag(d + (size_t)(2 * KH + i) * 512, O2m, [&](int r) { return v0 + r; }, col);
+        frag(d + (size_t)(2 * KH + 4 + i) * 512, O4m, [&](int r) { return v0 + r; }, col);
+      }
+    }
+  // units: R row of row tile `tile` of a half, lane row r
+  auto rrow = [&](int tile, bool fine, int r) {
+    const int g = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + r;
+    return g * H + (fine ? Hh : 0) + i;
+  };
+  std::vector<uint16_t> uw((size_t)P.NU * P.u_lds_w / 2), ur((size_t)P.NU * UCT * KT * 512);
   for (int k = 0; k < P.NU; ++k) {
-    uint16_t* base = ub.data() + (size_t)k * P.u_bytes / 2;
-    pack_frags(base + P.ub_ga / 2, WR_UR / 16, KT, Rm, [&](int r) { return cr_row(k * WR_UR + r); }, 0);
-    pack_frags(base + P.ub_gf / 2, WR_UR / 16, 2 * KT, Rm, [&](int r) { return fr_row(k * WR_UR + r); }, 0);
-  }
-  // O2 / O4 column slices per head as fragments: 16 class tiles x (this head's 32 rows)
-  std::vector<uint16_t> o2s((size_t)P.NH * 16 * 64 * 8), o4s(o2s.size());
-  for (int j = 0; j < P.NH; ++j) {
-    auto O2m = [&](int v, int k) { return w->O2[(size_t)v * Hh + j * WR_HR + k]; };
-    auto O4m = [&](int v, int k) { return w->O4[(size_t)v * Hh + j * WR_HR + k]; };
-    pack_frags(o2s.data() + (size_t)j * 16 * 512, 16, 1, O2m, [](int r) { return r; }, 0);
-    pack_frags(o4s.data() + (size_t)j * 16 * 512, 16, 1, O4m, [](int r) { return r; }, 0);
+    uint16_t* d = uw.data() + (size_t)k * P.u_lds_w / 2;
+    for (int q = 0; q < UCT; ++q) {
+      const int tile = k * UCT + q;
+      for (int kt = 0; kt < KT; ++kt) {
+        frag(d + (size_t)(q * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); }, 32 * kt);
+        frag(ur.data() + ((size_t)tile * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); },
+             Hh + 32 * kt);
+      }
+      for (int kt = 0; kt < 2 * KT; ++kt)
+        frag(d + (size_t)(UCT * KT + q * 2 * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, true, r); }, 32 * kt);
+    }
   }
   wavernn_status s;
-  if ((s = m->upload(&m->d_wh, hb.data(), hb.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_wu, ub.data(), ub.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_o2s, o2s.data(), o2s.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_o4s, o4s.data(), o4s.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_hw, hw.data(), hw.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_uw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_ur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
   std::vector<float> Iv((size_t)9 * H), bv((size_t)3 * H);
   for (int row = 0; row < 3 * H; ++row) {
     for (int q = 0; q < 3; ++q) Iv[row * 3 + q] = (q == 2 && row % H < Hh) ? 0.0f : rd(w->I[row * 3 + q]);
@@ -261,16 +272,17 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
     for (size_t i = 0; i < wc.size(); ++i) wc[i] = rd(w->W_cond[i]);
     if ((s = m->upload(&m->d_Wc, wc.data(), wc.size() * 4)) != WAVERNN_OK) return s;
   }
+  m->cb_cap = c.cond_dim > 0 ? 1024 : 1;
+  if ((s = m->alloc(&m->d_cb, (size_t)m->cb_cap * 3 * H * 4)) != WAVERNN_OK) return s;
   if ((s = m->alloc(&m->d_xc, (size_t)P.x_words * 8)) != WAVERNN_OK) return s;
-  const void* kp = wr_persist_kernel_ptr();
-  HIPOK(hipFuncSetAttribute(kp, hipFuncAttributeMaxDynamicSharedMemorySize, P.lds));
+  HIPOK(hipFuncSetAttribute(m->pk, hipFuncAttributeMaxDynamicSharedMemorySize, P.lds));
   int per_cu = 0;
-  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kp, WR_THREADS, P.lds));
+  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->pk, WR_THREADS, P.lds));
   hipDeviceProp_t prop;
   HIPOK(hipGetDeviceProperties(&prop, m->device));
-  if (per_cu < 1 || per_cu * prop.multiProcessorCount < P.NH + P.NU)
+  if (per_cu < 1 || per_cu * prop.multiProcessorCount < P.grid)
     return fail(WAVERNN_E_UNSUPPORTED, "persistent grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)",
-                P.NH + P.NU, per_cu, prop.multiProcessorCount);
+                P.grid, per_cu, prop.multiProcessorCount);
   return WAVERNN_OK;
 }
 
@@ -348,28 +360,46 @@ wavernn_status run_small(wavernn_model* m, const RunIO& io) {
 
 wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
   const PersistPlan& P = m->plan;
-  const int H = P.H;
+  const int H = P.H, Dc = m->cfg.cond_dim;
+  const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
+  const int64_t n_cb = Dc > 0 ? io.n_frames : 1;
+  if (n_cb > m->cb_cap) {   // grow the per-frame table (the only allocation a call can make)
+    HIPOK(hipStreamSynchronize(io.st));
+    float* p = nullptr;
+    wavernn_status s = m->alloc(&p, (size_t)n_cb * 3 * H * 4);
+    if (s != WAVERNN_OK) return s;
+    m->d_cb = p;
+    m->cb_cap = n_cb;
+  }
   for (int s = 0; s < io.S; ++s) {
+    {
+      const float* Wc = m->d_Wc;
+      const float* bias = m->d_bias;
+      const float* feat = io.cond ? io.cond + (size_t)s * io.n_frames * Dc : nullptr;
+      int rows = 3 * H;
+      int64_t nf = n_cb;
+      float* cb = m->d_cb;
+      int dc = Dc;
+      void* args[] = {&Wc, &bias, &feat, &dc, &rows, &nf, &cb};
+      HIPOK(hipLaunchKernel(wr_cond_kernel_ptr(), dim3((unsigned)((nf * rows + 255) / 256)), dim3(256), args, 0,
+                            io.st));
+    }
     wavernn_status st = launch_fill(m->d_xc, P.x_words, io.st);
     if (st != WAVERNN_OK) return st;
     PersistArgs a;
     memset(&a, 0, sizeof a);
     a.P = P;
-    a.wh = m->d_wh;
-    a.wu = m->d_wu;
-    a.o2s = m->d_o2s;
-    a.o4s = m->d_o4s;
+    a.hw = m->d_hw;
+    a.uw = m->d_uw;
+    a.ur = m->d_ur;
     a.Iw = m->d_I;
-    a.bias = m->d_bias;
     a.b1 = m->d_b1;
     a.b2 = m->d_b2;
     a.b3 = m->d_b3;
     a.b4 = m->d_b4;
-    a.Wc = m->d_Wc;
-    a.Dc = m->cfg.cond_dim;
-    a.frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
-    a.feat = io.cond ? io.cond + (size_t)s * io.n_frames * m->cfg.cond_dim : nullptr;
-    a.n_frames = io.n_frames;
+    a.cb = m->d_cb;
+    a.n_cb = n_cb;
+    a.frame_len = Dc > 0 ? frame_len : (1 << 30);
     a.T = io.T;
     a.t0 = io.init ? io.init->t0 : 0;
     a.seed = io.seed;
@@ -392,7 +422,7 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
     // An ordinary launch: create() checked that the whole grid fits on the
     // device at once, and every cross-workgroup wait is bounded, so a grid
     // that did not become co-resident ends with an error, never a hang.
-    HIPOK(hipLaunchKernel(wr_persist_kernel_ptr(), dim3(P.NH + P.NU), dim3(WR_THREADS), args, P.lds, io.st));
+    HIPOK(hipLaunchKernel(m->pk, dim3(P.grid), dim3(WR_THREADS), args, P.lds, io.st));
   }
   return WAVERNN_OK;
 }
@@ -501,7 +531,7 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t* grid, int32_t* block
   if (!m) return -1;
   int g = 0, b = 0;
   if (m->path == PATH_SMALL) g = 1, b = 256;
-  else if (m->path == PATH_PERSIST) g = m->plan.NH + m->plan.NU, b = WR_THREADS;
+  else if (m->path == PATH_PERSIST) g = m->plan.grid, b = WR_THREADS;
   if (grid) *grid = g;
   if (block) *block = b;
   return (int32_t)m->path;

@@ -56,14 +56,17 @@ WR_HD inline SmallLayout small_layout(int H) {
 // ---------------------------------------------------------------------------
 // Persistent multi-workgroup kernel.
 //
-// Head workgroups (NH): head j evaluates the gates of every unit (redundantly,
-// identically in all heads), owns rows [j*HR, j*HR+HR) of O1 and O3, the
-// matching columns of O2 and O4, and coarse rows [j*GR, j*GR+GR) of R's
-// fine-input half (R_c[:, fine], needed right after y_f is known).  Rows of R
-// are indexed per half: coarse row cr = g*Hh + i <-> R row g*H + i, fine row
-// fr = g*Hh + i <-> R row g*H + Hh + i (g = u, r, e).
-// Unit workgroups (NU): unit workgroup k owns coarse rows [k*UR, +UR) of R's
-// coarse-input half (GA rows) and fine rows [k*UR, +UR) of all of R (GF rows).
+// Head workgroups (NH = Hh / 64): every head evaluates the gates of every unit
+// (redundantly and identically), so all heads hold the whole hidden state
+// without exchanging it.  Head j owns rows [64j, 64j+64) of O1 and O3 and the
+// matching 64 columns of O2 and O4, kept in VGPRs as MFMA fragments; it
+// publishes 256 partial logits per half, and every head sums the NH partials
+// in the same order and draws the same class.
+// Unit workgroups (NU): R is cut into 16-row tiles, each tile within one gate
+// and one half (coarse rows: R row g*H + i, i < Hh; fine rows: g*H + Hh + i).
+// Unit k owns coarse tiles [k*UCT, +UCT) and fine tiles [k*UCT, +UCT) over all
+// H columns, so it publishes finished pre-activations R h (+ bias and
+// conditioning for the u and r gates) of those rows for the next step.
 //
 // Matrices are stored bf16 as MFMA fragments (v_mfma_f32_16x16x32_bf16 with
 // the matrix as operand B): fragment (mt, kt) covers rows 16*mt .. 16*mt+15 and
@@ -71,60 +74,66 @@ WR_HD inline SmallLayout small_layout(int H) {
 // 32*kt + 8*(l/16) .. +7 (16 bytes).  A fragment is 1 KiB, lanes in order.
 // ---------------------------------------------------------------------------
 #define WR_THREADS 512    // 8 waves per workgroup
-#define WR_HR 32          // O1 / O3 rows per head workgroup (2 row tiles)
-#define WR_GR 96          // R_c[:, fine] rows per head workgroup (6 row tiles)
-#define WR_UR 32          // GA rows and GF rows per unit workgroup (2 row tiles)
+#define WR_HROWS 64       // O1 / O3 rows per head workgroup (4 row tiles)
 #define WR_XALIGN 64      // exchange regions aligned to 64 words (512 B)
-#define WR_MAXNH 16       // partial-logit sets summed per draw
 #define WR_FRAG 1024      // bytes per MFMA fragment
+#define WR_MAXUCT 4       // coarse (and fine) row tiles per unit workgroup
 
 struct PersistPlan {
-  int H, Hh, KT;          // KT = Hh / 32 column tiles per input half
-  int NH, NU;
-  // head LDS block (bytes): O1 slice, O3 slice, R_c fine-half slice
-  int hb_o1, hb_o3, hb_rcf, h_bytes;
-  // unit LDS block (bytes): GA rows (coarse half), GF rows (both halves)
-  int ub_ga, ub_gf, u_bytes;
-  // exchange words
-  int x_yc, x_yf, x_ga, x_gf, x_gcf, x_aec, x_aef, x_pc, x_pf, x_words;
-  // LDS bytes
-  int lds_h, lds_u, lds;
+  int H, Hh, KT, KH;      // KT = Hh / 32 column tiles per half, KH = KT / 2
+  int NH, NU, UCT, NCT;   // heads, units, row tiles per unit and half, row tiles per half (3 Hh / 16)
+  int grid;               // workgroups launched: head j at block 8j, units on the others
+  int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[4], O4[4]
+  int u_lds_w;            // unit LDS weight block: coarse tiles x coarse columns, fine tiles x all columns
+  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (64-bit words)
+  int lds_h, lds_u, lds;  // LDS bytes
 };
 
 WR_HD inline int wr_rup(int x, int m) { return (x + m - 1) / m * m; }
+
+// Block index of head j and the role of block b (head index, or unit index + NH, or -1 idle).
+WR_HD inline int wr_role(const PersistPlan& P, int b) {
+  if (b % 8 == 0 && b / 8 < P.NH) return b / 8;
+  int before = (b + 7) / 8;                 // head blocks with index < b
+  if (before > P.NH) before = P.NH;
+  int k = b - before;
+  return k < P.NU ? P.NH + k : -1;
+}
 
 WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   if (H <= 0 || H % 128) return false;
   P->H = H;
   P->Hh = H / 2;
   P->KT = P->Hh / 32;
-  if (P->Hh % WR_HR || (3 * P->Hh) % WR_UR) return false;
-  P->NH = P->Hh / WR_HR;
-  P->NU = 3 * P->Hh / WR_UR;
-  if (P->NH > WR_MAXNH || P->Hh > WR_THREADS) return false;
-  P->hb_o1 = 0;
-  P->hb_o3 = P->hb_o1 + (WR_HR / 16) * P->KT * WR_FRAG;
-  P->hb_rcf = P->hb_o3 + (WR_HR / 16) * P->KT * WR_FRAG;
-  P->h_bytes = P->hb_rcf + (WR_GR / 16) * P->KT * WR_FRAG;
-  P->ub_ga = 0;
-  P->ub_gf = (WR_UR / 16) * P->KT * WR_FRAG;
-  P->u_bytes = P->ub_gf + (WR_UR / 16) * 2 * P->KT * WR_FRAG;
+  P->KH = P->KT / 2;
+  P->NH = P->Hh / WR_HROWS;
+  P->NCT = 3 * P->Hh / 16;
+  if (P->NH > 16 || P->Hh > WR_THREADS) return false;
+  P->hw_frags = 2 * P->KH + 8;
+  // head LDS: y_c and y_f operand images (KT fragments each), relu image (2),
+  // first-layer partials [2][64], logit sums [2][256], logits [256], misc [16]
+  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * 64 + 2 * 256 + 256 + 16);
+  P->UCT = 0;
+  for (int u = WR_MAXUCT; u >= 1; --u) {
+    if (P->NCT % u) continue;
+    int w = 3 * u * P->KT * WR_FRAG;
+    int l = w + 2 * P->KT * WR_FRAG + 4 * 16;
+    if (l <= 160 * 1024) { P->UCT = u; P->u_lds_w = w; P->lds_u = l; break; }
+  }
+  if (!P->UCT) return false;
+  P->NU = P->NCT / P->UCT;
+  int g = 8 * (P->NH - 1) + 1;
+  while (g - P->NH < P->NU) ++g;
+  P->grid = g;
   int o = 0;
   auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
   P->x_yc = take(P->Hh);
   P->x_yf = take(P->Hh);
   P->x_ga = take(3 * P->Hh);
   P->x_gf = take(3 * P->Hh);
-  P->x_gcf = take(3 * P->Hh);
-  P->x_aec = take(P->Hh);
-  P->x_aef = take(P->Hh);
   P->x_pc = take(P->NH * 256);
   P->x_pf = take(P->NH * 256);
   P->x_words = o;
-  // head: weights, h[H], z[256], zh[256], op[8][32], rp[4][96], ov[32], bs[64], misc[16]
-  P->lds_h = P->h_bytes + 4 * (H + 256 + 256 + 8 * WR_HR + 4 * WR_GR + WR_HR + 64 + 16);
-  // unit: weights, y[H], partials[2][8][32], misc[16]
-  P->lds_u = P->u_bytes + 4 * (H + 2 * 8 * WR_UR + 16);
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024;
 }

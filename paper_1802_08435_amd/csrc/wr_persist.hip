@@ -1,22 +1,20 @@
 // Persistent multi-workgroup WaveRNN sampler (batch 1 per launch).
 //
-// The whole utterance runs inside one cooperative launch (Sec. 2.1): weights
-// are loaded once into LDS, and every step evaluates the GRU of Eq. 2, the
+// The whole utterance runs inside one launch (Sec. 2.1): weights stay in VGPRs
+// and LDS across the launch, and every step evaluates the GRU of Eq. 2, the
 // coarse head, the coarse draw, the fine half, the fine head and the fine draw.
 // Workgroups exchange vectors through tagged 64-bit words (value + step tag)
-// instead of grid-wide barriers: each dependency costs one one-way hop.
+// instead of grid-wide barriers.
 //
-// Critical path per step, all inside the NH head workgroups:
-//   coarse gates of all units (every head, redundantly)
-//   -> own O1 rows + O2 columns -> partial coarse logits   --hop-->  all heads
-//   -> sum, draw c_t (every head, identically) -> fine gates of all units
-//   -> own O3 rows + O4 columns -> partial fine logits, and own rows of
-//      R_c[:, fine] y_f (the part of the next coarse pre-activation that
-//      depends on y_f)                                      --hop-->  all heads
-//   -> sum, draw f_t -> next step.
-// Off the critical path, NU unit workgroups receive y_c and y_f and compute the
-// rest of R h (coarse rows x coarse inputs, fine rows x all inputs), adding the
-// gate bias and conditioning, one step ahead of when the heads need them.
+// Critical path of a step, inside the NH head workgroups (all on one XCD):
+//   coarse gates of every unit (every head, identically, from pre-activations
+//   the unit workgroups published a step ahead)
+//   -> own 64 rows of O1, relu, own 64 columns of O2 -> 256 partial logits
+//   --one exchange--> every head sums the NH partials, draws c_t
+//   -> fine gates of every unit -> O3 rows, O4 columns -> partial logits
+//   --one exchange--> sum, draw f_t.
+// Off the critical path, the NU unit workgroups receive y_c and y_f and compute
+// R h for the next step (the paper's "gate" work), adding bias + conditioning.
 #include "wr_device.h"
 #include "wr_layout.h"
 #include "wr_args.h"
@@ -64,11 +62,19 @@ __device__ __forceinline__ float wave_maxf(float v) {
   return lane63(v);
 }
 
-// Inverse-CDF draw over softmax(z) by one wave, 4 classes per lane (z in LDS).
-// Returns the class, or `forced` when >= 0; *lse = max z + log sum exp(z - max).
-__device__ int draw_wave(const float* z, float u, int forced, float* lse) {
+// Inverse-CDF draw by one wave over z = zs0 + zs1 + b, 4 classes per lane.
+// The logits are also written to zkeep[256].  Returns the class, or `forced`
+// when >= 0; *lse = max z + log sum exp(z - max).
+__device__ int draw_wave(const float* zs0, const float* zs1, float4 b, float u, int forced, float* zkeep,
+                         float* lse) {
   const int l = threadIdx.x & 63;
-  float4 z4 = *(const float4*)(z + 4 * l);
+  const float4 p = *(const float4*)(zs0 + 4 * l), q = *(const float4*)(zs1 + 4 * l);
+  float4 z4;
+  z4.x = (p.x + q.x) + b.x;
+  z4.y = (p.y + q.y) + b.y;
+  z4.z = (p.z + q.z) + b.z;
+  z4.w = (p.w + q.w) + b.w;
+  *(float4*)(zkeep + 4 * l) = z4;
   float m = wave_maxf(fmaxf(fmaxf(z4.x, z4.y), fmaxf(z4.z, z4.w)));
   float w0 = fexp(z4.x - m), w1 = fexp(z4.y - m), w2 = fexp(z4.z - m), w3 = fexp(z4.w - m);
   float s0 = w0, s1 = s0 + w1, s2 = s1 + w2, s3 = s2 + w3;
@@ -82,11 +88,11 @@ __device__ int draw_wave(const float* z, float u, int forced, float* lse) {
               __popcll(__ballot(excl + s2 <= thr)) + __popcll(__ballot(excl + s3 <= thr));
   if (count == WR_CLASSES) {   // clamp to the last class with nonzero weight
     int last = -1;
-    u64 b;
-    if ((b = __ballot(w3 > 0.0f))) last = max(last, 4 * (63 - __clzll(b)) + 3);
-    if ((b = __ballot(w2 > 0.0f))) last = max(last, 4 * (63 - __clzll(b)) + 2);
-    if ((b = __ballot(w1 > 0.0f))) last = max(last, 4 * (63 - __clzll(b)) + 1);
-    if ((b = __ballot(w0 > 0.0f))) last = max(last, 4 * (63 - __clzll(b)));
+    u64 bb;
+    if ((bb = __ballot(w3 > 0.0f))) last = max(last, 4 * (63 - __clzll(bb)) + 3);
+    if ((bb = __ballot(w2 > 0.0f))) last = max(last, 4 * (63 - __clzll(bb)) + 2);
+    if ((bb = __ballot(w1 > 0.0f))) last = max(last, 4 * (63 - __clzll(bb)) + 1);
+    if ((bb = __ballot(w0 > 0.0f))) last = max(last, 4 * (63 - __clzll(bb)));
     count = last;
   }
   return count;
@@ -96,9 +102,14 @@ __device__ int draw_wave(const float* z, float u, int forced, float* lse) {
 // Matrix-vector products on the matrix cores.  v_mfma_f32_16x16x32_bf16 with
 // the vector as operand A: row 0 holds the bf16 high part of x, row 1 the bf16
 // low part (x - high, rounded), rows 2..15 are zero; the weights are operand B
-// (see the fragment layout in wr_layout.h).  Products of bf16 values are exact
-// in fp32, so W x is carried to about 2^-16 relative per term, and lanes 0..15
-// of the result hold the 16 output rows of the tile: D[0][n] + D[1][n].
+// (fragment layout in wr_layout.h).  Products of bf16 values are exact in
+// fp32, so W x is carried to about 2^-16 relative per term, and lane n < 16 of
+// the result holds output row n of the tile as D[0][n] + D[1][n].
+//
+// The operand-A images live in LDS in fragment order (1 KiB per 32 inputs,
+// lane l's 16 bytes at 16 l), rows 2..15 zeroed once: writing input k of a
+// tile sets two bf16 values, and every lane reads its operand with one
+// 16-byte LDS load.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -106,78 +117,26 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
-
-// Operand-A fragment of x[32*kt .. 32*kt+31] (x fp32 in LDS).  Every lane reads
-// its 8 values (no divergence); lanes of rows >= 2 contribute zeros.
-__device__ __forceinline__ bf16x8 xfrag(const float* x, int kt) {
-  const int l = threadIdx.x & 63, r = l & 15, kq = l >> 4;
-  const float* src = x + 32 * kt + 8 * kq;
-  float4 a = *(const float4*)src, b = *(const float4*)(src + 4);
-  float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-  bf16x8 f;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    float hi = __uint_as_float(__float_as_uint(v[i]) & 0xffff0000u);
-    float sel = r == 0 ? hi : (r == 1 ? v[i] - hi : 0.0f);
-    f[i] = (__bf16)sel;
-  }
-  return f;
+__device__ __forceinline__ bf16x8 afrag(const unsigned char* img, int kt) {
+  return *(const bf16x8*)(img + kt * WR_FRAG + (threadIdx.x & 63) * 16);
 }
-
-__device__ __forceinline__ bf16x8 wfrag(const unsigned char* base, int idx) {
-  return *(const bf16x8*)(base + ((size_t)idx * 64 + (threadIdx.x & 63)) * 16);
+// Store x as input k (0 <= k < 32) of operand tile `img` (rows 0 and 1).
+__device__ __forceinline__ void aput(unsigned char* img, int k, float x) {
+  const float hi = __uint_as_float(__float_as_uint(x) & 0xffff0000u);
+  const __bf16 bh = (__bf16)hi, bl = (__bf16)(x - hi);
+  __bf16* row0 = (__bf16*)(img + (16 * (k >> 3)) * 16) + (k & 7);
+  row0[0] = bh;        // lane 16*(k/8),     element k%8
+  row0[8] = bl;        // lane 16*(k/8) + 1, element k%8
 }
+__device__ __forceinline__ float mfma_row(f32x4 d) { return d[0] + d[1]; }
 
-// Partial products of row tiles m0 .. m0+MT-1 over column tiles kt = k0, k0+ks,
-// ... < KT (x covers all KT tiles; the matrix has KT column tiles per row tile).
-// The MT weight fragments of a column tile are read together before its MFMAs.
-// out[16*m + n] receives row 16*(m0+m) + n from lane n.
-template <int MT>
-__device__ __forceinline__ void tile_rows(const unsigned char* W, int KT, const float* x, int m0, int k0, int ks,
-                                          float* out) {
-  f32x4 acc[MT];
-#pragma unroll
-  for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  for (int kt = k0; kt < KT; kt += ks) {
-    bf16x8 wc[MT];
-#pragma unroll
-    for (int m = 0; m < MT; ++m) wc[m] = wfrag(W, (m0 + m) * KT + kt);
-    const bf16x8 xa = xfrag(x, kt);
-#pragma unroll
-    for (int m = 0; m < MT; ++m) acc[m] = mfma(xa, wc[m], acc[m]);
-  }
-  const int l = threadIdx.x & 63;
-  if (l < 16) {
-#pragma unroll
-    for (int m = 0; m < MT; ++m) out[16 * m + l] = acc[m][0] + acc[m][1];
-  }
-}
-
-// Wait until every word p[k] (k < N) carries `tag`, with all loads of a round in
-// flight together; false on timeout / abort.
+// ---------------------------------------------------------------------------
+// Waits on tagged words (bounded: see WaitBudget).
+// ---------------------------------------------------------------------------
+// Wait until every word p[k] (k < N) carries `tag`, starting from words w[]
+// loaded earlier; only words that did not carry it yet are loaded again.
 template <int N>
-__device__ __forceinline__ bool poll_n(const u64* const* p, uint32_t tag, float* v, WaitBudget& wb,
-                                       const PersistArgs& a) {
-  uint32_t pending = (1u << N) - 1u;
-  for (;;) {
-    u64 w[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1u) ? xpeek(p[k]) : 0;
-#pragma unroll
-    for (int k = 0; k < N; ++k)
-      if ((pending >> k & 1u) && xtag(w[k]) == tag) {
-        v[k] = xval(w[k]);
-        pending &= ~(1u << k);
-      }
-    if (!pending) return true;
-    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
-  }
-}
-
-// Like poll_n, starting from words w[] loaded earlier (prefetched): only the
-// words that did not yet carry `tag` are loaded again.
-template <int N>
-__device__ __forceinline__ bool poll_pref(const u64* const* p, const u64* w, uint32_t tag, float* v, WaitBudget& wb,
+__device__ __forceinline__ bool poll_pref(const u64* const* p, const u64* w, uint32_t tag, float* v,
                                           const PersistArgs& a) {
   uint32_t pending = 0;
 #pragma unroll
@@ -185,6 +144,8 @@ __device__ __forceinline__ bool poll_pref(const u64* const* p, const u64* w, uin
     if (xtag(w[k]) == tag) v[k] = xval(w[k]);
     else pending |= 1u << k;
   }
+  if (!pending) return true;
+  WaitBudget wb{wr_clock(), 0};
   while (pending) {
     u64 x[N];
 #pragma unroll
@@ -200,53 +161,53 @@ __device__ __forceinline__ bool poll_pref(const u64* const* p, const u64* w, uin
   return true;
 }
 
-// Wait until *p carries `tag`; false on timeout / abort.
-__device__ __forceinline__ bool poll1(const u64* p, uint32_t tag, float* v, WaitBudget& wb, const PersistArgs& a) {
-  u64 w;
-  while (xtag(w = xpeek(p)) != tag)
-    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+// Wait until *p carries `tag` (polling with a short sleep between loads).
+__device__ __forceinline__ bool poll_sleepy(const u64* p, uint32_t tag, float* v, const PersistArgs& a) {
+  u64 w = xpeek(p);
+  if (xtag(w) != tag) {
+    WaitBudget wb{wr_clock(), 0};
+    do {
+      if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+      __builtin_amdgcn_s_sleep(1);
+    } while (xtag(w = xpeek(p)) != tag);
+  }
   *v = xval(w);
   return true;
 }
 
-// Gather n tagged words into dst (all threads, up to 2 words each).
-__device__ bool gather_words(const u64* src, int n, uint32_t tag, float* dst, const PersistArgs& a) {
-  WaitBudget wb{wr_clock(), 0};
-  const int nt = blockDim.x;
-  int i0 = threadIdx.x, i1 = threadIdx.x + nt;
-  bool p0 = i0 < n, p1 = i1 < n;
-  while (p0 || p1) {
-    u64 w0 = p0 ? xpeek(src + i0) : 0, w1 = p1 ? xpeek(src + i1) : 0;
-    if (p0 && xtag(w0) == tag) { dst[i0] = xval(w0); p0 = false; }
-    if (p1 && xtag(w1) == tag) { dst[i1] = xval(w1); p1 = false; }
-    if ((p0 || p1) && !wait_ok(wb, a.err, a.limit, a.err)) return false;
-  }
-  return true;
-}
-
-// Sum of partial logits p[j*256 + v] for parts j in [j0, j0 + np) in part
-// order, once all carry `tag` (all pending words of a round loaded together).
+// Sum over parts jj = j0 .. j1-1 of src[jj*256 + v] once all carry `tag`, in
+// part order (every head sums in the same order, so all draw the same class).
 template <int MAXP>
-__device__ bool sum_parts(const u64* src, int j0, int np, int v, uint32_t tag, float* out, const PersistArgs& a) {
-  WaitBudget wb{wr_clock(), 0};
+__device__ bool sum_parts(const u64* src, int j0, int j1, int v, uint32_t tag, float* out, const PersistArgs& a) {
   float vals[MAXP];
-  uint32_t pending = (1u << np) - 1u;
-  while (pending) {
-    u64 w[MAXP];
+  uint32_t pending = 0;
+  u64 w[MAXP];
 #pragma unroll
-    for (int k = 0; k < MAXP; ++k) w[k] = (pending >> k & 1u) ? xpeek(src + (j0 + k) * WR_CLASSES + v) : 0;
+  for (int k = 0; k < MAXP; ++k) w[k] = j0 + k < j1 ? xpeek(src + (j0 + k) * WR_CLASSES + v) : 0;
 #pragma unroll
-    for (int k = 0; k < MAXP; ++k)
-      if ((pending >> k & 1u) && xtag(w[k]) == tag) {
-        vals[k] = xval(w[k]);
-        pending &= ~(1u << k);
-      }
-    if (pending && !wait_ok(wb, a.err, a.limit, a.err)) return false;
+  for (int k = 0; k < MAXP; ++k) {
+    if (j0 + k >= j1) continue;
+    if (xtag(w[k]) == tag) vals[k] = xval(w[k]);
+    else pending |= 1u << k;
+  }
+  if (pending) {
+    WaitBudget wb{wr_clock(), 0};
+    while (pending) {
+      if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+#pragma unroll
+      for (int k = 0; k < MAXP; ++k) w[k] = (pending >> k & 1u) ? xpeek(src + (j0 + k) * WR_CLASSES + v) : 0;
+#pragma unroll
+      for (int k = 0; k < MAXP; ++k)
+        if ((pending >> k & 1u) && xtag(w[k]) == tag) {
+          vals[k] = xval(w[k]);
+          pending &= ~(1u << k);
+        }
+    }
   }
   float acc = 0.0f;
 #pragma unroll
   for (int k = 0; k < MAXP; ++k)
-    if (k < np) acc += vals[k];
+    if (j0 + k < j1) acc += vals[k];
   *out = acc;
   return true;
 }
@@ -255,71 +216,49 @@ __device__ bool sum_parts(const u64* src, int j0, int np, int v, uint32_t tag, f
 __device__ __forceinline__ void trace_at(const PersistArgs& a, int64_t t, int slot) {
   if (a.trace && t < a.trace_steps) a.trace[t * WR_TRACE_SLOTS + slot] = wr_clock();
 }
-
-// Bias + conditioning of R row `row` for absolute sample n.
-__device__ float gate_add(const PersistArgs& a, int row, int64_t n) {
-  float v = a.bias[row];
-  if (a.Dc > 0) {
-    int64_t fr = n / a.frame_len;
-    if (fr >= a.n_frames) fr = a.n_frames - 1;
-    const float* wc = a.Wc + (size_t)row * a.Dc;
-    const float* fv = a.feat + (size_t)fr * a.Dc;
-    float acc = 0.0f;
-    for (int q = 0; q < a.Dc; ++q) acc = __builtin_fmaf(wc[q], fv[q], acc);
-    v = acc + v;
-  }
-  return v;
+// Row of the bias + conditioning table used at absolute sample n.
+__device__ __forceinline__ const float* cb_row(const PersistArgs& a, int64_t n) {
+  int64_t fr = n / a.frame_len;
+  if (fr >= a.n_cb) fr = a.n_cb - 1;
+  return a.cb + (size_t)fr * 3 * a.P.H;
 }
 
 // ------------------------------------------------------------------ head role
+template <int KH>
 __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
+  constexpr int KT = 2 * KH;
   const PersistPlan& P = a.P;
-  const int H = P.H, Hh = P.Hh, NH = P.NH, KT = P.KT;
+  const int H = P.H, Hh = P.Hh, NH = P.NH;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const unsigned char* W1 = lds + P.hb_o1;
-  const unsigned char* W3 = lds + P.hb_o3;
-  const unsigned char* WR = lds + P.hb_rcf;
-  float* h = (float*)(lds + P.h_bytes);  // [H] hidden state (identical in every head)
-  float* z = h + H;                      // [256] logits
-  float* zh = z + 256;                   // [256] second half of the partial-logit sums
-  float* op = zh + 256;                  // [8][32] first-layer partials per wave
-  float* rp = op + 8 * WR_HR;            // [4][96] R_c[:, fine] y_f partials per wave
-  float* ov = rp + 4 * WR_GR;            // [32] relu(first layer) of this head's rows
-  float* bs = ov + WR_HR;                // [0:32] b1 slice, [32:64] b3 slice
-  int* misc = (int*)(bs + 64);           // [0] abort [1] c_t [3] c_prev [4] f_prev
-  float* fmisc = (float*)(misc + 8);     // [0] u_c [1] u_f [2] lse_c [3] z_c[c]
+  unsigned char* imc = lds;                        // y_c operand image [KT]
+  unsigned char* imf = imc + KT * WR_FRAG;         // y_f operand image [KT]
+  unsigned char* imo = imf + KT * WR_FRAG;         // relu(first layer) image [2]
+  float* op = (float*)(imo + 2 * WR_FRAG);         // [2][64] first-layer partials
+  float* zs = op + 2 * 64;                         // [2][256] partial-logit sums
+  float* zk = zs + 2 * 256;                        // [256] logits of the last draw
+  int* misc = (int*)(zk + 256);                    // [0] abort [1] c_t [2] c_prev [3] f_prev
+  float* fmisc = (float*)(misc + 8);               // [0] u_c [1] u_f [2] lse_c [3] z_c[c]
 
-  // --- prologue
+  // --- prologue: zero the operand images, load this wave's fragments
+  for (int i = tid; i < (2 * KT + 2) * WR_FRAG / 16; i += WR_THREADS) ((uint4*)lds)[i] = uint4{0, 0, 0, 0};
+  bf16x8 W1[KH], W3[KH], W2[4], W4[4];
   {
-    const uint4* src = a.wh + (size_t)j * (P.h_bytes / 16);
-    uint4* dst = (uint4*)lds;
-    for (int i = tid; i < P.h_bytes / 16; i += blockDim.x) dst[i] = src[i];
-    for (int i = tid; i < H; i += blockDim.x) h[i] = a.h_in ? a.h_in[i] : 0.0f;
-    if (tid < WR_HR) {
-      bs[tid] = a.b1[j * WR_HR + tid];
-      bs[WR_HR + tid] = a.b3[j * WR_HR + tid];
-    }
-    if (tid == 0) {
-      misc[0] = 0;
-      misc[3] = a.c_in ? a.c_in[0] : 128;
-      misc[4] = a.f_in ? a.f_in[0] : 0;
-    }
-  }
-  // O2 / O4 column-slice fragments of class tiles 4*wave .. 4*wave+3 (waves 0-3)
-  bf16x8 o2f[4], o4f[4];
-  if (wave < 4) {
+    const uint4* src = a.hw + ((size_t)(j * 8 + wave) * P.hw_frags) * 64 + lane;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      uint4 x2 = a.o2s[((size_t)j * 16 + 4 * wave + s) * 64 + lane];
-      uint4 x4 = a.o4s[((size_t)j * 16 + 4 * wave + s) * 64 + lane];
-      o2f[s] = __builtin_bit_cast(bf16x8, x2);
-      o4f[s] = __builtin_bit_cast(bf16x8, x4);
-    }
+    for (int i = 0; i < KH; ++i) W1[i] = __builtin_bit_cast(bf16x8, src[(size_t)i * 64]);
+#pragma unroll
+    for (int i = 0; i < KH; ++i) W3[i] = __builtin_bit_cast(bf16x8, src[(size_t)(KH + i) * 64]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) W2[i] = __builtin_bit_cast(bf16x8, src[(size_t)(2 * KH + i) * 64]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) W4[i] = __builtin_bit_cast(bf16x8, src[(size_t)(2 * KH + 4 + i) * 64]);
   }
-  // I* rows of unit u = tid: coarse (c_{t-1}, f_{t-1}), fine (c_{t-1}, f_{t-1}, c_t)
-  float ic[3][2], ifn[3][3];
+  // gate thread u: coarse unit u and fine unit Hh + u
   const int u = tid;
-  if (u < Hh) {
+  const bool gate = u < Hh;
+  float ic[3][2], ifn[3][3];
+  float hc = 0.0f, hf = 0.0f;
+  if (gate) {
 #pragma unroll
     for (int g = 0; g < 3; ++g) {
       ic[g][0] = a.Iw[3 * (g * H + u) + 0];
@@ -328,341 +267,335 @@ __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
       ifn[g][1] = a.Iw[3 * (g * H + Hh + u) + 1];
       ifn[g][2] = a.Iw[3 * (g * H + Hh + u) + 2];
     }
+    if (a.h_in) {
+      hc = a.h_in[u];
+      hf = a.h_in[Hh + u];
+    }
   }
-  const float b2v = tid < WR_CLASSES ? a.b2[tid] : 0.0f;
-  const float b4v = tid < WR_CLASSES ? a.b4[tid] : 0.0f;
-  __syncthreads();
-
+  const float b1r = tid < 64 ? a.b1[j * 64 + tid] : 0.0f;
+  const float b3r = tid < 64 ? a.b3[j * 64 + tid] : 0.0f;
+  const float4 b2l = wave == 0 ? *(const float4*)(a.b2 + 4 * lane) : float4{0, 0, 0, 0};
+  const float4 b4l = wave == 0 ? *(const float4*)(a.b4 + 4 * lane) : float4{0, 0, 0, 0};
+  if (tid == 0) {
+    misc[0] = 0;
+    misc[2] = a.c_in ? a.c_in[0] : 128;
+    misc[3] = a.f_in ? a.f_in[0] : 0;
+  }
   const u64* GA = a.xc + P.x_ga;
   const u64* GF = a.xc + P.x_gf;
-  u64* GCF = a.xc + P.x_gcf;
-  const u64* AEC = a.xc + P.x_aec;
-  const u64* AEF = a.xc + P.x_aef;
   u64* YC = a.xc + P.x_yc;
   u64* YF = a.xc + P.x_yf;
   u64* PCo = a.xc + P.x_pc + (size_t)j * WR_CLASSES;
   u64* PFo = a.xc + P.x_pf + (size_t)j * WR_CLASSES;
   const u64* PC = a.xc + P.x_pc;
   const u64* PF = a.xc + P.x_pf;
-
-  // R_c[:, fine] y_f partials of this head's rows on waves 4-7, summed by
-  // threads 256..351 after a barrier and published with `tag`.
-  // wave 4 + 2*kh + mh: row tiles 3*mh .. 3*mh+2, column tiles kh, kh+2, ...
-  auto rcf_partial = [&]() {
-    const int w4 = wave - 4, mh = w4 & 1, kh = w4 >> 1;
-    tile_rows<WR_GR / 32>(WR, KT, h + Hh, 3 * mh, kh, 2, rp + kh * WR_GR + mh * (WR_GR / 2));
-  };
-  auto rcf_publish = [&](uint32_t tag) {
-    const int r = tid - 256;
-    if (r >= 0 && r < WR_GR) xpub(GCF + j * WR_GR + r, tag, rp[r] + rp[WR_GR + r]);
-  };
-  // relu(first layer + bias) of this head's rows from nparts wave partials
-  auto relu_rows = [&](int nparts, const float* b) {
-    if (tid < WR_HR) {
-      float s = 0.0f;
-      for (int w = 0; w < nparts; ++w) s += op[w * WR_HR + tid];
-      ov[tid] = wr_relu(s + b[tid]);
+  const bool own = gate && (u >> 6) == j;          // this head publishes y of units 64j .. 64j+63
+  const int rt = wave & 3, kc = wave >> 2;         // first layer: row tile, column-tile half
+  const int NH0 = (NH + 1) / 2;
+  // pre-activation words of this thread's units, loaded ahead
+  u64 pc[3] = {0, 0, 0}, pf[3] = {0, 0, 0};
+  float cbe_c = 0.0f, cbe_f = 0.0f;
+  auto prefetch_coarse = [&](int64_t n) {
+    if (gate) {
+      pc[0] = xpeek(GA + u); pc[1] = xpeek(GA + Hh + u); pc[2] = xpeek(GA + 2 * Hh + u);
+      cbe_c = cb_row(a, n)[2 * H + u];
     }
   };
-  // second layer on waves 0-3: partial logits of class tiles 4*wave .. +3
-  auto second_layer = [&](const bf16x8* of, u64* dst, uint32_t tag) {
-    const bf16x8 xa = xfrag(ov, 0);
+  auto prefetch_fine = [&](int64_t n) {
+    if (gate) {
+      pf[0] = xpeek(GF + u); pf[1] = xpeek(GF + Hh + u); pf[2] = xpeek(GF + 2 * Hh + u);
+      cbe_f = cb_row(a, n)[2 * H + Hh + u];
+    }
+  };
+  // first layer on the 8 waves -> relu -> operand image of the second layer
+  auto first_layer = [&](const bf16x8* W, const unsigned char* img, float b) {
+    f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      f32x4 acc = mfma(xa, of[s], f32x4{0.0f, 0.0f, 0.0f, 0.0f});
-      if (lane < 16) xpub(dst + 16 * (4 * wave + s) + lane, tag, acc[0] + acc[1]);
+    for (int i = 0; i < KH; i += 2) {
+      acc0 = mfma(afrag(img, kc * KH + i), W[i], acc0);
+      if (i + 1 < KH) acc1 = mfma(afrag(img, kc * KH + i + 1), W[i + 1], acc1);
+    }
+    if (lane < 16) op[kc * 64 + 16 * rt + lane] = mfma_row(acc0) + mfma_row(acc1);
+    __syncthreads();
+    if (tid < 64) aput(imo + (tid >> 5) * WR_FRAG, tid & 31, wr_relu((op[tid] + op[64 + tid]) + b));
+    __syncthreads();
+  };
+  // second layer: class tiles 2*wave, 2*wave+1 over this head's 64 columns -> publish
+  auto second_layer = [&](const bf16x8* W, u64* dst, uint32_t tag) {
+    const bf16x8 x0 = afrag(imo, 0), x1 = afrag(imo, 1);
+    f32x4 A = mfma(x0, W[0], f32x4{0, 0, 0, 0});
+    f32x4 B = mfma(x0, W[2], f32x4{0, 0, 0, 0});
+    A = mfma(x1, W[1], A);
+    B = mfma(x1, W[3], B);
+    if (lane < 16) {
+      xpub(dst + 32 * wave + lane, tag, mfma_row(A));
+      xpub(dst + 32 * wave + 16 + lane, tag, mfma_row(B));
     }
   };
-
-  // step 0's R_c[:, fine] y_f(-1) from the initial state
-  if (wave >= 4) rcf_partial();
+  // partial logits of all heads: thread (v, half) sums its half of the parts
+  auto gather_logits = [&](const u64* src, uint32_t tag) {
+    const int v = tid & 255, hh = tid >> 8;
+    float s;
+    if (!sum_parts<8>(src, hh ? NH0 : 0, hh ? NH : NH0, v, tag, &s, a)) misc[0] = 1;
+    else zs[hh * 256 + v] = s;
+  };
   __syncthreads();
-  rcf_publish(1u);
-
-  // prefetched pre-activation words of this thread's unit: coarse (GA x3,
-  // GCF x3, AEC) and fine (GF x3, AEF); loaded a phase before they are needed
-  u64 pc7[7] = {0, 0, 0, 0, 0, 0, 0}, pf4[4] = {0, 0, 0, 0};
-  auto prefetch_coarse = [&]() {
-    if (u < Hh) {
-      pc7[0] = xpeek(GA + u); pc7[1] = xpeek(GA + Hh + u); pc7[2] = xpeek(GA + 2 * Hh + u);
-      pc7[3] = xpeek(GCF + u); pc7[4] = xpeek(GCF + Hh + u); pc7[5] = xpeek(GCF + 2 * Hh + u);
-      pc7[6] = xpeek(AEC + u);
-    }
-  };
-  auto prefetch_fine = [&]() {
-    if (u < Hh) {
-      pf4[0] = xpeek(GF + u); pf4[1] = xpeek(GF + Hh + u); pf4[2] = xpeek(GF + 2 * Hh + u);
-      pf4[3] = xpeek(AEF + u);
-    }
-  };
-  const int half_parts = (NH + 1) / 2;
+  prefetch_coarse(a.t0);
+  prefetch_fine(a.t0);
 
   for (int64_t t = 0; t < a.T; ++t) {
     const int64_t n = a.t0 + t;
     const uint32_t tag = (uint32_t)(t + 1);
     const bool tr = j == 0 && tid == 0;
-    const bool trl = j == NH - 1 && j > 0 && tid == 0;   // last head: fine partials published
     if (tr) trace_at(a, t, 0);
-    if (tid == 64) {
+    if (tid == WR_THREADS - 64) {     // a thread with no gate work draws the step's uniforms
       float uc, uf;
       wr_uniforms(a.seed, a.stream_id, (uint64_t)n, &uc, &uf);
       fmisc[0] = uc;
       fmisc[1] = uf;
     }
-    // (1)-(2) coarse gates of every unit
-    const float x0 = fscale(misc[3]), x1 = fscale(misc[4]);
-    bool ok = true;
-    if (u < Hh) {
-      WaitBudget wb{wr_clock(), 0};
-      const u64* ps[7] = {GA + u, GA + Hh + u, GA + 2 * Hh + u, GCF + u, GCF + Hh + u, GCF + 2 * Hh + u, AEC + u};
-      float v[7];
-      ok = poll_pref<7>(ps, pc7, tag, v, wb, a);
-      if (ok) {
-        float au = (v[0] + v[3]) + __builtin_fmaf(ic[0][1], x1, ic[0][0] * x0);
-        float ar = (v[1] + v[4]) + __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0);
-        float ie = __builtin_fmaf(ic[2][1], x1, ic[2][0] * x0) + v[6];
+    const float x0 = fscale(misc[2]), x1 = fscale(misc[3]);
+    // (1) coarse gates of every unit
+    if (gate) {
+      const u64* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
+      float v[3];
+      if (poll_pref<3>(ps, pc, tag, v, a)) {
+        float au = v[0] + __builtin_fmaf(ic[0][1], x1, ic[0][0] * x0);
+        float ar = v[1] + __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0);
+        float ie = __builtin_fmaf(ic[2][1], x1, ic[2][0] * x0) + cbe_c;
         float uu = fsig(au), rr = fsig(ar);
-        float e = ftanh(__builtin_fmaf(rr, v[2] + v[5], ie));
-        float hn = __builtin_fmaf(uu, h[u], (1.0f - uu) * e);
-        h[u] = hn;
-        if (u >= j * WR_HR && u < (j + 1) * WR_HR) xpub(YC + u, tag, hn);
+        float e = ftanh(__builtin_fmaf(rr, v[2], ie));
+        hc = __builtin_fmaf(uu, hc, (1.0f - uu) * e);
+        aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
+        if (own) xpub(YC + u, tag, hc);
+      } else {
+        misc[0] = 1;
       }
     }
-    if (!ok) misc[0] = 1;
     __syncthreads();
     if (misc[0]) return;
     if (tr) trace_at(a, t, 1);
-    // (3) O1 rows of this head: column tiles split over the 8 waves
-    tile_rows<WR_HR / 16>(W1, KT, h, 0, wave, 8, op + wave * WR_HR);
-    if (tr) trace_at(a, t, 18);
-    __syncthreads();
-    if (tr) trace_at(a, t, 19);
-    relu_rows(8, bs);
-    __syncthreads();
+    // (2) own rows of O1 -> relu -> own columns of O2 -> partial coarse logits
+    first_layer(W1, imc, b1r);
     if (tr) trace_at(a, t, 2);
-    // (4) partial coarse logits
-    if (wave < 4) second_layer(o2f, PCo, tag);
+    second_layer(W2, PCo, tag);
     if (tr) trace_at(a, t, 3);
-
-    // (5) sum partials of all heads (two threads per class), fine words prefetched
-    prefetch_fine();
-    {
-      const int v = tid & 255, hf = tid >> 8;
-      float s;
-      if (!sum_parts<(WR_MAXNH + 1) / 2>(PC, hf ? half_parts : 0, hf ? NH - half_parts : half_parts, v, tag, &s, a))
-        misc[0] = 1;
-      else if (hf) zh[v] = s;
-      else z[v] = s;
-    }
+    // (3) coarse logits of all heads, draw c_t; this step's fine words are
+    // loaded while the draw runs
+    gather_logits(PC, tag);
+    if (t > 0) prefetch_fine(n);
     __syncthreads();
     if (misc[0]) return;
-    if (tid < WR_CLASSES) z[tid] = (z[tid] + zh[tid]) + b2v;
-    __syncthreads();
     if (tr) trace_at(a, t, 4);
-    // (6) draw c_t (every head draws the same class)
-    const int64_t o = t;
-    if (j == 0 && a.zc_out && tid < WR_CLASSES) a.zc_out[o * WR_CLASSES + tid] = z[tid];
     if (wave == 0) {
       float lse;
-      int forced = a.target ? (a.target[o] >> 8) : -1;
-      int c = draw_wave(z, fmisc[0], forced, a.nll_out ? &lse : nullptr);
+      const int forced = a.target ? (a.target[t] >> 8) : -1;
+      const int c = draw_wave(zs, zs + 256, b2l, fmisc[0], forced, zk, a.nll_out ? &lse : nullptr);
+      if (j == 0 && a.zc_out) *(float4*)(a.zc_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {
         misc[1] = c;
         if (a.nll_out) {
           fmisc[2] = lse;
-          fmisc[3] = z[c];
+          fmisc[3] = zk[c];
         }
       }
     }
     __syncthreads();
     if (tr) trace_at(a, t, 5);
-    // (7)-(8) fine gates of every unit (c_t reaches the fine half only)
+    // (4) fine gates of every unit (c_t reaches the fine half only)
     const int c = misc[1];
-    if (u < Hh) {
-      WaitBudget wb{wr_clock(), 0};
-      const u64* ps[4] = {GF + u, GF + Hh + u, GF + 2 * Hh + u, AEF + u};
-      float v[4];
-      ok = poll_pref<4>(ps, pf4, tag, v, wb, a);
-      if (ok) {
+    if (gate) {
+      const u64* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
+      float v[3];
+      if (poll_pref<3>(ps, pf, tag, v, a)) {
         const float x2 = fscale(c);
         float au = v[0] + __builtin_fmaf(ifn[0][2], x2, __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0));
         float ar = v[1] + __builtin_fmaf(ifn[1][2], x2, __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0));
-        float ie = __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0)) + v[3];
+        float ie = __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0)) + cbe_f;
         float uu = fsig(au), rr = fsig(ar);
         float e = ftanh(__builtin_fmaf(rr, v[2], ie));
-        float hn = __builtin_fmaf(uu, h[Hh + u], (1.0f - uu) * e);
-        h[Hh + u] = hn;
-        if (u >= j * WR_HR && u < (j + 1) * WR_HR) xpub(YF + u, tag, hn);
+        hf = __builtin_fmaf(uu, hf, (1.0f - uu) * e);
+        aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
+        if (own) xpub(YF + u, tag, hf);
+      } else {
+        misc[0] = 1;
       }
     }
-    if (!ok) misc[0] = 1;
     __syncthreads();
     if (misc[0]) return;
     if (tr) trace_at(a, t, 6);
-    // (9)-(10) O3 rows on waves 0-3, this head's rows of R_c[:, fine] y_f(t) on waves 4-7
-    if (wave < 4) tile_rows<WR_HR / 16>(W3, KT, h + Hh, 0, wave, 4, op + wave * WR_HR);
-    else if (t + 1 < a.T) rcf_partial();
-    if (tr) trace_at(a, t, 12);
-    if (j == 0 && tid == 256) trace_at(a, t, 13);
-    __syncthreads();
-    if (tr) trace_at(a, t, 14);
-    relu_rows(4, bs + WR_HR);
-    if (t + 1 < a.T) rcf_publish(tag + 1);
-    if (j == 0 && tid == 256) trace_at(a, t, 15);
-    __syncthreads();
-    if (tr) trace_at(a, t, 16);
-    if (wave < 4) second_layer(o4f, PFo, tag);
-    if (tr) trace_at(a, t, 17);
+    // (5) own rows of O3 -> relu -> own columns of O4 -> partial fine logits
+    first_layer(W3, imf, b3r);
     if (tr) trace_at(a, t, 7);
-    if (trl) trace_at(a, t, 11);
-    // (11) sum partials, draw f_t; next step's coarse words prefetched
-    prefetch_coarse();
-    {
-      const int v = tid & 255, hf = tid >> 8;
-      float s;
-      if (!sum_parts<(WR_MAXNH + 1) / 2>(PF, hf ? half_parts : 0, hf ? NH - half_parts : half_parts, v, tag, &s, a))
-        misc[0] = 1;
-      else if (hf) zh[v] = s;
-      else z[v] = s;
-    }
+    second_layer(W4, PFo, tag);
+    if (tr) trace_at(a, t, 8);
+    // (6) fine logits of all heads, draw f_t; next step's coarse words are
+    // loaded while the draw runs
+    gather_logits(PF, tag);
+    if (t + 1 < a.T) prefetch_coarse(n + 1);
     __syncthreads();
     if (misc[0]) return;
-    if (tid < WR_CLASSES) z[tid] = (z[tid] + zh[tid]) + b4v;
-    __syncthreads();
     if (tr) trace_at(a, t, 9);
-    if (j == 0 && a.zf_out && tid < WR_CLASSES) a.zf_out[o * WR_CLASSES + tid] = z[tid];
     if (wave == 0) {
       float lse;
-      int forced = a.target ? (a.target[o] & 255) : -1;
-      int f = draw_wave(z, fmisc[1], forced, a.nll_out ? &lse : nullptr);
+      const int forced = a.target ? (a.target[t] & 255) : -1;
+      const int f = draw_wave(zs, zs + 256, b4l, fmisc[1], forced, zk, a.nll_out ? &lse : nullptr);
+      if (j == 0 && a.zf_out) *(float4*)(a.zf_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {
         if (j == 0) {
-          if (a.out) a.out[o] = (uint16_t)(256 * c + f);
-          if (a.nll_out) a.nll_out[o] = (fmisc[2] - fmisc[3]) + (lse - z[f]);
+          if (a.out) a.out[t] = (uint16_t)(256 * c + f);
+          if (a.nll_out) a.nll_out[t] = (fmisc[2] - fmisc[3]) + (lse - zk[f]);
         }
-        misc[3] = c;
-        misc[4] = f;
+        misc[2] = c;
+        misc[3] = f;
       }
     }
     __syncthreads();
     if (tr) trace_at(a, t, 10);
   }
   if (j == 0) {
-    if (a.h_out)
-      for (int i = tid; i < H; i += blockDim.x) a.h_out[i] = h[i];
+    if (a.h_out && gate) {
+      a.h_out[u] = hc;
+      a.h_out[Hh + u] = hf;
+    }
     if (tid == 0) {
-      if (a.c_out) a.c_out[0] = (uint8_t)misc[3];
-      if (a.f_out) a.f_out[0] = (uint8_t)misc[4];
+      if (a.c_out) a.c_out[0] = (uint8_t)misc[2];
+      if (a.f_out) a.f_out[0] = (uint8_t)misc[3];
     }
   }
 }
 
 // ------------------------------------------------------------------ unit role
-// GA rows cr = k*UR + m (coarse rows x coarse inputs) and GF rows fr = k*UR + m
-// (fine rows x both inputs), m < UR; column tiles split over the 8 waves.
-// Bias + conditioning is added for gates u and r; for gate e it is published
-// separately (AEC / AEF) because the reset gate multiplies R_e h only.
+// Wave q < UCT owns coarse row tile k*UCT + q (coarse columns from LDS, fine
+// columns from VGPRs) and publishes its 16 pre-activations as soon as y_f is
+// in; wave 4 + q owns fine row tile k*UCT + q (all columns from LDS).
+template <int KH>
 __device__ void unit_role(const PersistArgs& a, int k, unsigned char* lds) {
+  constexpr int KT = 2 * KH;
   const PersistPlan& P = a.P;
-  const int H = P.H, Hh = P.Hh, KT = P.KT;
+  const int H = P.H, Hh = P.Hh, UCT = P.UCT;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const unsigned char* WGA = lds + P.ub_ga;
-  const unsigned char* WGF = lds + P.ub_gf;
-  float* y = (float*)(lds + P.u_bytes);  // [H]
-  float* gp = y + H;                     // [8][UR] GA partials
-  float* fp = gp + 8 * WR_UR;            // [8][UR] GF partials
-  int* misc = (int*)(fp + 8 * WR_UR);
+  const unsigned char* WC = lds;                                 // [UCT][KT] coarse tiles, coarse columns
+  const unsigned char* WF = lds + UCT * KT * WR_FRAG;            // [UCT][2KT] fine tiles, all columns
+  unsigned char* img = lds + P.u_lds_w;                          // [2KT] operand image of h
+  int* misc = (int*)(img + 2 * KT * WR_FRAG);
+  const bool cw = wave < UCT, fw = wave >= 4 && wave - 4 < UCT;
+  const int q = cw ? wave : wave - 4;
+  // this wave's tile: gate g, units i0 .. i0+15 of its half
+  const int tile = k * UCT + q;
+  const int g = tile / (Hh / 16), i0 = 16 * (tile % (Hh / 16));
+  const int row = g * H + (fw ? Hh : 0) + i0 + (lane & 15);     // R row of lane n < 16
+  u64* dst = a.xc + (fw ? P.x_gf : P.x_ga) + g * Hh + i0 + lane;
   {
-    const uint4* src = a.wu + (size_t)k * (P.u_bytes / 16);
-    uint4* dst = (uint4*)lds;
-    for (int i = tid; i < P.u_bytes / 16; i += blockDim.x) dst[i] = src[i];
-    for (int i = tid; i < H; i += blockDim.x) y[i] = a.h_in ? a.h_in[i] : 0.0f;
+    const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
+    for (int i = tid; i < P.u_lds_w / 16; i += WR_THREADS) ((uint4*)lds)[i] = src[i];
+    for (int i = tid; i < 2 * KT * WR_FRAG / 16; i += WR_THREADS) ((uint4*)img)[i] = uint4{0, 0, 0, 0};
     if (tid == 0) misc[0] = 0;
   }
-  // row of this thread for the publish phases: tid < UR -> GA row, 64 <= tid < 64+UR -> GF row
-  const bool pub_ga = tid < WR_UR, pub_gf = tid >= 64 && tid < 64 + WR_UR;
-  const int m = pub_ga ? tid : tid - 64;
-  const int xr = k * WR_UR + m;            // row index within its half, g*Hh + i
-  const int g = xr / Hh, i = xr % Hh;
-  const int grow = pub_ga ? g * H + i : g * H + Hh + i;
-  int64_t cur_frame = -2;
-  float addr = 0.0f;
-  auto refresh_add = [&](int64_t n) {      // bias + conditioning of this thread's row for sample n
-    int64_t fr = a.Dc > 0 ? n / a.frame_len : 0;
-    if (fr != cur_frame) {
-      cur_frame = fr;
-      if (pub_ga || pub_gf) addr = gate_add(a, grow, n);
-    }
-  };
-  auto publish = [&](uint32_t tag, const float* part) {
-    if (!(pub_ga || pub_gf)) return;
-    float acc = 0.0f;
-    for (int w = 0; w < 8; ++w) acc += part[w * WR_UR + m];
-    u64* dst = a.xc + (pub_ga ? P.x_ga : P.x_gf) + xr;
-    if (g == 2) {
-      xpub(dst, tag, acc);
-      xpub(a.xc + (pub_ga ? P.x_aec : P.x_aef) + i, tag, addr);
-    } else {
-      xpub(dst, tag, acc + addr);
-    }
-  };
-  // GF rows accumulate over both input halves: column tiles 0..KT-1 (y_c) then KT..2KT-1 (y_f)
-  f32x4 gfa[WR_UR / 16];
-  auto gf_tiles = [&](int k0, int k1) {
-    for (int kt = k0 + ((wave - k0) % 8 + 8) % 8; kt < k1; kt += 8) {
-      bf16x8 wc[WR_UR / 16];
+  bf16x8 WR[KT];
+  if (cw) {
+    const uint4* src = a.ur + ((size_t)tile * KT) * 64 + lane;
 #pragma unroll
-      for (int mt = 0; mt < WR_UR / 16; ++mt) wc[mt] = wfrag(WGF, mt * 2 * KT + kt);
-      const bf16x8 xa = xfrag(y, kt);
-#pragma unroll
-      for (int mt = 0; mt < WR_UR / 16; ++mt) gfa[mt] = mfma(xa, wc[mt], gfa[mt]);
-    }
-  };
-  auto gf_store = [&]() {
-    if (lane < 16) {
-#pragma unroll
-      for (int mt = 0; mt < WR_UR / 16; ++mt) fp[wave * WR_UR + 16 * mt + lane] = gfa[mt][0] + gfa[mt][1];
-    }
-  };
+    for (int i = 0; i < KT; ++i) WR[i] = __builtin_bit_cast(bf16x8, src[(size_t)i * 64]);
+  }
   __syncthreads();
+  for (int i = tid; i < H; i += WR_THREADS) {
+    const float y = a.h_in ? a.h_in[i] : 0.0f;
+    aput(img + (i >> 5) * WR_FRAG, i & 31, y);
+  }
+  __syncthreads();
+  f32x4 acc0, acc1;
+  // columns [0, KT) of the image: coarse inputs
+  auto phase_c = [&]() {
+    acc0 = f32x4{0, 0, 0, 0};
+    acc1 = f32x4{0, 0, 0, 0};
+    const unsigned char* W = cw ? WC + q * KT * WR_FRAG : WF + q * 2 * KT * WR_FRAG;
+    if (cw || fw) {
+#pragma unroll
+      for (int i = 0; i < KT; i += 2) {
+        acc0 = mfma(afrag(img, i), *(const bf16x8*)(W + i * WR_FRAG + lane * 16), acc0);
+        if (i + 1 < KT) acc1 = mfma(afrag(img, i + 1), *(const bf16x8*)(W + (i + 1) * WR_FRAG + lane * 16), acc1);
+      }
+    }
+  };
+  // columns [KT, 2KT): fine inputs; then publish with `tag`
+  auto phase_f = [&](uint32_t tag, const float* cbr) {
+    if (cw) {
+#pragma unroll
+      for (int i = 0; i < KT; i += 2) {
+        acc0 = mfma(afrag(img, KT + i), WR[i], acc0);
+        if (i + 1 < KT) acc1 = mfma(afrag(img, KT + i + 1), WR[i + 1], acc1);
+      }
+    } else if (fw) {
+      const unsigned char* W = WF + (q * 2 * KT + KT) * WR_FRAG;
+#pragma unroll
+      for (int i = 0; i < KT; i += 2) {
+        acc0 = mfma(afrag(img, KT + i), *(const bf16x8*)(W + i * WR_FRAG + lane * 16), acc0);
+        if (i + 1 < KT) acc1 = mfma(afrag(img, KT + i + 1), *(const bf16x8*)(W + (i + 1) * WR_FRAG + lane * 16), acc1);
+      }
+    }
+    if ((cw || fw) && lane < 16) {
+      float v = mfma_row(acc0) + mfma_row(acc1);
+      if (g < 2) v += cbr[row];                 // bias + conditioning of the u and r gates
+      xpub(dst, tag, v);
+    }
+  };
   // step 0's pre-activations from the initial state
-  refresh_add(a.t0);
-  tile_rows<WR_UR / 16>(WGA, KT, y, 0, wave, 8, gp + wave * WR_UR);
-#pragma unroll
-  for (int mt = 0; mt < WR_UR / 16; ++mt) gfa[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  gf_tiles(0, 2 * KT);
-  gf_store();
-  __syncthreads();
-  publish(1u, pub_ga ? gp : fp);
+  phase_c();
+  phase_f(1u, cb_row(a, a.t0));
   const u64* YC = a.xc + P.x_yc;
   const u64* YF = a.xc + P.x_yf;
   for (int64_t t = 0; t + 1 < a.T; ++t) {
-    const uint32_t tag = (uint32_t)(t + 1), ntag = tag + 1;
-    refresh_add(a.t0 + t + 1);
-    if (!gather_words(YC, Hh, tag, y, a)) misc[0] = 1;
+    const uint32_t tag = (uint32_t)(t + 1);
+    const float* cbr = cb_row(a, a.t0 + t + 1);
+    if (tid < Hh) {
+      float y;
+      if (poll_sleepy(YC + tid, tag, &y, a)) aput(img + (tid >> 5) * WR_FRAG, tid & 31, y);
+      else misc[0] = 1;
+    }
     __syncthreads();
     if (misc[0]) return;
-    tile_rows<WR_UR / 16>(WGA, KT, y, 0, wave, 8, gp + wave * WR_UR);
-#pragma unroll
-    for (int mt = 0; mt < WR_UR / 16; ++mt) gfa[mt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    gf_tiles(0, KT);
-    __syncthreads();
-    if (pub_ga) publish(ntag, gp);
-    if (!gather_words(YF, Hh, tag, y + Hh, a)) misc[0] = 1;
+    phase_c();
+    if (tid < Hh) {
+      float y;
+      if (poll_sleepy(YF + tid, tag, &y, a)) aput(img + (KT + (tid >> 5)) * WR_FRAG, tid & 31, y);
+      else misc[0] = 1;
+    }
     __syncthreads();
     if (misc[0]) return;
-    gf_tiles(KT, 2 * KT);
-    gf_store();
-    __syncthreads();
-    if (pub_gf) publish(ntag, fp);
+    if (k == 0 && tid == 0) trace_at(a, t + 1, 11);
+    phase_f(tag + 1, cbr);
+    if (k == 0 && tid == 0) trace_at(a, t + 1, 12);
   }
 }
 
-extern "C" __global__ __launch_bounds__(WR_THREADS, 1) void wr_persist_kernel(PersistArgs a) {
+template <int KH>
+__global__ __launch_bounds__(WR_THREADS, 1) void wr_persist_kernel(PersistArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
-  const int b = blockIdx.x;
-  if (b < a.P.NH) head_role(a, b, lds);
-  else unit_role(a, b - a.P.NH, lds);
+  const int r = wr_role(a.P, blockIdx.x);
+  if (r < 0) return;
+  if (r < a.P.NH) head_role<KH>(a, r, lds);
+  else unit_role<KH>(a, r - a.P.NH, lds);
+}
+
+// Bias + conditioning of every gate row for every frame (Sec. 2 conditioning):
+// cb[f][row] = sum_q W_cond[row][q] feat[f][q] (fma chain in q order) + b[row].
+extern "C" __global__ void wr_cond_kernel(const float* Wc, const float* bias, const float* feat, int Dc, int rows,
+                                          int64_t n_frames, float* cb) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n_frames * rows) return;
+  const int64_t f = idx / rows;
+  const int row = (int)(idx % rows);
+  float acc = 0.0f;
+  if (Dc > 0) {
+    const float* w = Wc + (size_t)row * Dc;
+    const float* x = feat + (size_t)f * Dc;
+    for (int q = 0; q < Dc; ++q) acc = __builtin_fmaf(w[q], x[q], acc);
+    acc = acc + bias[row];
+  } else {
+    acc = bias[row];
+  }
+  cb[idx] = acc;
 }
 
 extern "C" __global__ void wr_fill_u64(u64* p, int64_t n, u64 v) {
@@ -670,6 +603,15 @@ extern "C" __global__ void wr_fill_u64(u64* p, int64_t n, u64 v) {
   if (i < n) p[i] = v;
 }
 
-const void* wr_persist_kernel_ptr() { return (const void*)wr_persist_kernel; }
-
+const void* wr_persist_kernel_ptr(int KH) {
+  switch (KH) {
+    case 1: return (const void*)wr_persist_kernel<1>;
+    case 2: return (const void*)wr_persist_kernel<2>;
+    case 3: return (const void*)wr_persist_kernel<3>;
+    case 4: return (const void*)wr_persist_kernel<4>;
+    case 7: return (const void*)wr_persist_kernel<7>;
+    default: return nullptr;
+  }
+}
+const void* wr_cond_kernel_ptr() { return (const void*)wr_cond_kernel; }
 const void* wr_fill_kernel_ptr() { return (const void*)wr_fill_u64; }
