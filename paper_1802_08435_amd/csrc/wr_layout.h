@@ -77,7 +77,7 @@ WR_HD inline SmallLayout small_layout(int H) {
 #define WR_HROWS 64       // O1 / O3 rows per head workgroup (4 row tiles)
 #define WR_XALIGN 64      // exchange regions aligned to 64 words (512 B)
 #define WR_FRAG 1024      // bytes per MFMA fragment
-#define WR_MAXUCT 4       // coarse (and fine) row tiles per unit workgroup
+#define WR_MAXUCT 3       // coarse (and fine) row tiles per unit workgroup (waves 3, 7 stay free)
 
 struct PersistPlan {
   int H, Hh, KT, KH;      // KT = Hh / 32 column tiles per half, KH = KT / 2
@@ -86,6 +86,7 @@ struct PersistPlan {
   int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[4], O4[4]
   int u_lds_w;            // unit LDS weight block: coarse tiles x coarse columns, fine tiles x all columns
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (64-bit words)
+  int x_ps;               // words between the partial-logit blocks of consecutive heads
   int lds_h, lds_u, lds;  // LDS bytes
 };
 
@@ -108,11 +109,12 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->KH = P->KT / 2;
   P->NH = P->Hh / WR_HROWS;
   P->NCT = 3 * P->Hh / 16;
-  if (P->NH > 16 || P->Hh > WR_THREADS) return false;
+  if (P->NH > 16 || P->Hh > WR_THREADS - 64) return false;   // the last wave draws, free of gate work
   P->hw_frags = 2 * P->KH + 8;
   // head LDS: y_c and y_f operand images (KT fragments each), relu image (2),
-  // first-layer partials [2][64], logit sums [2][256], logits [256], misc [16]
-  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * 64 + 2 * 256 + 256 + 16);
+  // first-layer partials [2][64], logit sums [2][256], logits [256],
+  // y [448], misc [16], uniforms [2][64][2], targets [2][64]
+  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * 64 + 3 * 256 + 448 + 16 + 256 + 128);
   P->UCT = 0;
   for (int u = WR_MAXUCT; u >= 1; --u) {
     if (P->NCT % u) continue;
@@ -131,8 +133,9 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->x_yf = take(P->Hh);
   P->x_ga = take(3 * P->Hh);
   P->x_gf = take(3 * P->Hh);
-  P->x_pc = take(P->NH * 256);
-  P->x_pf = take(P->NH * 256);
+  P->x_ps = 256;
+  P->x_pc = take(P->NH * P->x_ps);
+  P->x_pf = take(P->NH * P->x_ps);
   P->x_words = o;
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024;

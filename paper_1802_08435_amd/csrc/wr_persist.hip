@@ -62,18 +62,23 @@ __device__ __forceinline__ float wave_maxf(float v) {
   return lane63(v);
 }
 
-// Inverse-CDF draw by one wave over z = zs0 + zs1 + b, 4 classes per lane.
-// The logits are also written to zkeep[256].  Returns the class, or `forced`
-// when >= 0; *lse = max z + log sum exp(z - max).
-__device__ int draw_wave(const float* zs0, const float* zs1, float4 b, float u, int forced, float* zkeep,
+// Inverse-CDF draw by one wave over z = (zs + zs2) + b, 4 classes per lane.  The
+// logits are also written to zkeep[256].  Returns the class, or `forced` when
+// >= 0; *lse = max z + log sum exp(z - max).
+__device__ int draw_wave(const float* zs, const float* zs2, float4 b, float u, int forced, float* zkeep,
                          float* lse) {
   const int l = threadIdx.x & 63;
-  const float4 p = *(const float4*)(zs0 + 4 * l), q = *(const float4*)(zs1 + 4 * l);
+  float4 p = *(const float4*)(zs + 4 * l);
+  const float4 q = *(const float4*)(zs2 + 4 * l);
+  p.x += q.x;
+  p.y += q.y;
+  p.z += q.z;
+  p.w += q.w;
   float4 z4;
-  z4.x = (p.x + q.x) + b.x;
-  z4.y = (p.y + q.y) + b.y;
-  z4.z = (p.z + q.z) + b.z;
-  z4.w = (p.w + q.w) + b.w;
+  z4.x = p.x + b.x;
+  z4.y = p.y + b.y;
+  z4.z = p.z + b.z;
+  z4.w = p.w + b.w;
   *(float4*)(zkeep + 4 * l) = z4;
   float m = wave_maxf(fmaxf(fmaxf(z4.x, z4.y), fmaxf(z4.z, z4.w)));
   float w0 = fexp(z4.x - m), w1 = fexp(z4.y - m), w2 = fexp(z4.z - m), w3 = fexp(z4.w - m);
@@ -161,41 +166,44 @@ __device__ __forceinline__ bool poll_pref(const u64* const* p, const u64* w, uin
   return true;
 }
 
-// Wait until *p carries `tag` (polling with a short sleep between loads).
+// Wait until *p carries `tag` (with SLEEP, a short sleep between loads).
+template <bool SLEEP = true>
 __device__ __forceinline__ bool poll_sleepy(const u64* p, uint32_t tag, float* v, const PersistArgs& a) {
   u64 w = xpeek(p);
   if (xtag(w) != tag) {
     WaitBudget wb{wr_clock(), 0};
     do {
       if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
-      __builtin_amdgcn_s_sleep(1);
+      if (SLEEP) __builtin_amdgcn_s_sleep(1);
     } while (xtag(w = xpeek(p)) != tag);
   }
   *v = xval(w);
   return true;
 }
 
-// Sum over parts jj = j0 .. j1-1 of src[jj*256 + v] once all carry `tag`, in
+// Sum over parts jj = j0 .. j1-1 of src[jj*stride + v] once all carry `tag`, in
 // part order (every head sums in the same order, so all draw the same class).
 template <int MAXP>
-__device__ bool sum_parts(const u64* src, int j0, int j1, int v, uint32_t tag, float* out, const PersistArgs& a) {
+__device__ __forceinline__ bool sum_parts(const u64* src, int stride, int j0, int j1, int v, uint32_t tag, float* out,
+                          const PersistArgs& a, u64* first_back = nullptr) {
   float vals[MAXP];
   uint32_t pending = 0;
   u64 w[MAXP];
 #pragma unroll
-  for (int k = 0; k < MAXP; ++k) w[k] = j0 + k < j1 ? xpeek(src + (j0 + k) * WR_CLASSES + v) : 0;
+  for (int k = 0; k < MAXP; ++k) w[k] = j0 + k < j1 ? xpeek(src + (size_t)(j0 + k) * stride + v) : 0;
 #pragma unroll
   for (int k = 0; k < MAXP; ++k) {
     if (j0 + k >= j1) continue;
     if (xtag(w[k]) == tag) vals[k] = xval(w[k]);
     else pending |= 1u << k;
   }
+  if (first_back) *first_back = wr_clock();
   if (pending) {
     WaitBudget wb{wr_clock(), 0};
     while (pending) {
       if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
 #pragma unroll
-      for (int k = 0; k < MAXP; ++k) w[k] = (pending >> k & 1u) ? xpeek(src + (j0 + k) * WR_CLASSES + v) : 0;
+      for (int k = 0; k < MAXP; ++k) w[k] = (pending >> k & 1u) ? xpeek(src + (size_t)(j0 + k) * stride + v) : 0;
 #pragma unroll
       for (int k = 0; k < MAXP; ++k)
         if ((pending >> k & 1u) && xtag(w[k]) == tag) {
@@ -224,20 +232,29 @@ __device__ __forceinline__ const float* cb_row(const PersistArgs& a, int64_t n) 
 }
 
 // ------------------------------------------------------------------ head role
+// Wave roles: waves 0-6 evaluate the gates (one unit per thread), all 8 waves
+// run the MFMA layers and gather the partial logits (two threads per class),
+// wave 7 publishes this head's slice of y for the unit workgroups and draws.
 template <int KH>
 __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
   constexpr int KT = 2 * KH;
+  constexpr int NH = KH;                           // Hh / 64 heads = H / 128
+  constexpr int DW = 7;                            // the draw wave (no gate work: Hh <= 448)
   const PersistPlan& P = a.P;
-  const int H = P.H, Hh = P.Hh, NH = P.NH;
+  const int H = P.H, Hh = P.Hh;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   unsigned char* imc = lds;                        // y_c operand image [KT]
   unsigned char* imf = imc + KT * WR_FRAG;         // y_f operand image [KT]
   unsigned char* imo = imf + KT * WR_FRAG;         // relu(first layer) image [2]
   float* op = (float*)(imo + 2 * WR_FRAG);         // [2][64] first-layer partials
-  float* zs = op + 2 * 64;                         // [2][256] partial-logit sums
-  float* zk = zs + 2 * 256;                        // [256] logits of the last draw
-  int* misc = (int*)(zk + 256);                    // [0] abort [1] c_t [2] c_prev [3] f_prev
-  float* fmisc = (float*)(misc + 8);               // [0] u_c [1] u_f [2] lse_c [3] z_c[c]
+  float* zs2 = op + 2 * 64;                        // [256] sums over the second half of the heads
+  float* zs = zs2 + 256;                           // [256] sums over the first half of the heads
+  float* zk = zs + 256;                            // [256] logits of the last draw
+  float* yv = zk + 256;                            // [448] this half of h (fp32)
+  int* misc = (int*)(yv + 448);                    // [0] abort [1] c_t [2] c_prev [3] f_prev
+  float* fmisc = (float*)(misc + 8);               // [2] lse_c [3] z_c[c]
+  float2* uni = (float2*)(misc + 16);              // [2][64] (u_c, u_f) of a batch of 64 steps
+  int* tgt = (int*)(uni + 128);                    // [2][64] teacher-forcing targets of the batch
 
   // --- prologue: zero the operand images, load this wave's fragments
   for (int i = tid; i < (2 * KT + 2) * WR_FRAG / 16; i += WR_THREADS) ((uint4*)lds)[i] = uint4{0, 0, 0, 0};
@@ -274,8 +291,8 @@ __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
   }
   const float b1r = tid < 64 ? a.b1[j * 64 + tid] : 0.0f;
   const float b3r = tid < 64 ? a.b3[j * 64 + tid] : 0.0f;
-  const float4 b2l = wave == 0 ? *(const float4*)(a.b2 + 4 * lane) : float4{0, 0, 0, 0};
-  const float4 b4l = wave == 0 ? *(const float4*)(a.b4 + 4 * lane) : float4{0, 0, 0, 0};
+  const float4 b2l = wave == DW ? *(const float4*)(a.b2 + 4 * lane) : float4{0, 0, 0, 0};
+  const float4 b4l = wave == DW ? *(const float4*)(a.b4 + 4 * lane) : float4{0, 0, 0, 0};
   if (tid == 0) {
     misc[0] = 0;
     misc[2] = a.c_in ? a.c_in[0] : 128;
@@ -285,13 +302,11 @@ __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
   const u64* GF = a.xc + P.x_gf;
   u64* YC = a.xc + P.x_yc;
   u64* YF = a.xc + P.x_yf;
-  u64* PCo = a.xc + P.x_pc + (size_t)j * WR_CLASSES;
-  u64* PFo = a.xc + P.x_pf + (size_t)j * WR_CLASSES;
+  u64* PCo = a.xc + P.x_pc + (size_t)j * P.x_ps;
+  u64* PFo = a.xc + P.x_pf + (size_t)j * P.x_ps;
   const u64* PC = a.xc + P.x_pc;
   const u64* PF = a.xc + P.x_pf;
-  const bool own = gate && (u >> 6) == j;          // this head publishes y of units 64j .. 64j+63
   const int rt = wave & 3, kc = wave >> 2;         // first layer: row tile, column-tile half
-  const int NH0 = (NH + 1) / 2;
   // pre-activation words of this thread's units, loaded ahead
   u64 pc[3] = {0, 0, 0}, pf[3] = {0, 0, 0};
   float cbe_c = 0.0f, cbe_f = 0.0f;
@@ -320,7 +335,8 @@ __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
     if (tid < 64) aput(imo + (tid >> 5) * WR_FRAG, tid & 31, wr_relu((op[tid] + op[64 + tid]) + b));
     __syncthreads();
   };
-  // second layer: class tiles 2*wave, 2*wave+1 over this head's 64 columns -> publish
+  // second layer: class tiles 2*wave, 2*wave+1 over this head's 64 columns;
+  // waves 4-7 publish the 256 partial logits
   auto second_layer = [&](const bf16x8* W, u64* dst, uint32_t tag) {
     const bf16x8 x0 = afrag(imo, 0), x1 = afrag(imo, 1);
     f32x4 A = mfma(x0, W[0], f32x4{0, 0, 0, 0});
@@ -332,65 +348,108 @@ __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
       xpub(dst + 32 * wave + 16 + lane, tag, mfma_row(B));
     }
   };
-  // partial logits of all heads: thread (v, half) sums its half of the parts
-  auto gather_logits = [&](const u64* src, uint32_t tag) {
-    const int v = tid & 255, hh = tid >> 8;
+  // partial logits of all heads: thread (v, half) sums its half of the heads
+  // in head order (traced steps: head 0 records when its class-0 thread's
+  // first loads came back)
+  auto gather_logits = [&](const u64* src, uint32_t tag, int64_t t, bool trace_parts) {
     float s;
-    if (!sum_parts<8>(src, hh ? NH0 : 0, hh ? NH : NH0, v, tag, &s, a)) misc[0] = 1;
-    else zs[hh * 256 + v] = s;
+    u64 back = 0;
+    const int v = tid & 255, hh = tid >> 8, NH0 = (NH + 1) / 2;
+    const bool rec = trace_parts && j == 0 && tid == 0 && a.trace && t < a.trace_steps;
+    if (!sum_parts<(KH + 1) / 2>(src, P.x_ps, hh ? NH0 : 0, hh ? NH : NH0, v, tag, &s, a, rec ? &back : nullptr))
+      misc[0] = 1;
+    else (hh ? zs2 : zs)[v] = s;
+    if (rec) a.trace[t * WR_TRACE_SLOTS + 15] = back;
   };
+  // Philox blocks of steps t .. t+63 into batch buffer b, one step per lane of
+  // the draw wave: the 64-bit multiplies cost the same for 64 lanes as for one
+  auto fill_batch = [&](int64_t t, int b) {
+    const int64_t s = t + lane;
+    if (s < a.T) {
+      float uc, uf;
+      wr_uniforms(a.seed, a.stream_id, (uint64_t)(a.t0 + s), &uc, &uf);
+      uni[b * 64 + lane] = float2{uc, uf};
+      tgt[b * 64 + lane] = a.target ? a.target[s] : 0;
+    }
+  };
+  if (wave == DW) fill_batch(0, 0);
   __syncthreads();
   prefetch_coarse(a.t0);
   prefetch_fine(a.t0);
+  const bool trw = j == 0 && tid == WR_THREADS - 64;       // tracing thread (draw wave)
+  // Gate work is split around the draws: the part that does not depend on the
+  // class being drawn runs on the gate waves while the draw wave draws.
+  float cu = 0.0f, cr = 0.0f, ce = 0.0f, cie = 0.0f;       // coarse: before f_{t-1} is known
+  float fu = 0.0f, fr = 0.0f, fe = 0.0f, fie = 0.0f;       // fine: before c_t is known
+  auto coarse_pre = [&](uint32_t tag, float x0) {
+    if (!gate) return;
+    const u64* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
+    float v[3];
+    if (!poll_pref<3>(ps, pc, tag, v, a)) {
+      misc[0] = 1;
+      return;
+    }
+    cu = v[0] + ic[0][0] * x0;
+    cr = v[1] + ic[1][0] * x0;
+    ce = v[2];
+    cie = ic[2][0] * x0;
+  };
+  auto fine_pre = [&](uint32_t tag, float x0, float x1) {
+    if (!gate) return;
+    const u64* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
+    float v[3];
+    if (!poll_pref<3>(ps, pf, tag, v, a)) {
+      misc[0] = 1;
+      return;
+    }
+    fu = v[0] + __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0);
+    fr = v[1] + __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0);
+    fe = v[2];
+    fie = __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0);
+  };
+  coarse_pre(1u, fscale(misc[2]));
+  // Every prologue load has landed: no wait inside the loop is left waiting on
+  // them (a wait there would also wait for the wave's outstanding stores).
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (misc[0]) return;
 
   for (int64_t t = 0; t < a.T; ++t) {
     const int64_t n = a.t0 + t;
     const uint32_t tag = (uint32_t)(t + 1);
-    const bool tr = j == 0 && tid == 0;
-    if (tr) trace_at(a, t, 0);
-    if (tid == WR_THREADS - 64) {     // a thread with no gate work draws the step's uniforms
-      float uc, uf;
-      wr_uniforms(a.seed, a.stream_id, (uint64_t)n, &uc, &uf);
-      fmisc[0] = uc;
-      fmisc[1] = uf;
-    }
-    const float x0 = fscale(misc[2]), x1 = fscale(misc[3]);
-    // (1) coarse gates of every unit
+    if (trw) trace_at(a, t, 0);
+    const int bs = (int)((t >> 6) & 1) * 64 + (int)(t & 63);   // this step in the batch buffers
+    if (wave == DW && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
+    // (1) coarse gates of every unit, finished with f_{t-1}
     if (gate) {
-      const u64* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
-      float v[3];
-      if (poll_pref<3>(ps, pc, tag, v, a)) {
-        float au = v[0] + __builtin_fmaf(ic[0][1], x1, ic[0][0] * x0);
-        float ar = v[1] + __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0);
-        float ie = __builtin_fmaf(ic[2][1], x1, ic[2][0] * x0) + cbe_c;
-        float uu = fsig(au), rr = fsig(ar);
-        float e = ftanh(__builtin_fmaf(rr, v[2], ie));
-        hc = __builtin_fmaf(uu, hc, (1.0f - uu) * e);
-        aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
-        if (own) xpub(YC + u, tag, hc);
-      } else {
-        misc[0] = 1;
-      }
+      const float x1 = fscale(misc[3]);
+      const float uu = fsig(__builtin_fmaf(ic[0][1], x1, cu)), rr = fsig(__builtin_fmaf(ic[1][1], x1, cr));
+      const float e = ftanh(__builtin_fmaf(rr, ce, __builtin_fmaf(ic[2][1], x1, cie) + cbe_c));
+      hc = __builtin_fmaf(uu, hc, (1.0f - uu) * e);
+      aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
+      yv[u] = hc;
     }
     __syncthreads();
-    if (misc[0]) return;
-    if (tr) trace_at(a, t, 1);
+    if (trw) trace_at(a, t, 1);
+    if (wave == DW) xpub(YC + 64 * j + lane, tag, yv[64 * j + lane]);   // this head's slice, for the units
     // (2) own rows of O1 -> relu -> own columns of O2 -> partial coarse logits
     first_layer(W1, imc, b1r);
-    if (tr) trace_at(a, t, 2);
+    if (trw) trace_at(a, t, 2);
     second_layer(W2, PCo, tag);
-    if (tr) trace_at(a, t, 3);
-    // (3) coarse logits of all heads, draw c_t; this step's fine words are
-    // loaded while the draw runs
-    gather_logits(PC, tag);
+    if (trw) trace_at(a, t, 3);
+    if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 13);
+    if (j > 0 && NH <= 8 && tid == WR_THREADS - 64) trace_at(a, t, 24 + j);
+    // (3) coarse logits of all heads; this step's fine words are loaded
+    gather_logits(PC, tag, t, true);
     if (t > 0) prefetch_fine(n);
     __syncthreads();
     if (misc[0]) return;
-    if (tr) trace_at(a, t, 4);
-    if (wave == 0) {
+    if (trw) trace_at(a, t, 4);
+    // (4) draw c_t on the draw wave; meanwhile the fine gates start
+    if (wave == DW) {
       float lse;
-      const int forced = a.target ? (a.target[t] >> 8) : -1;
-      const int c = draw_wave(zs, zs + 256, b2l, fmisc[0], forced, zk, a.nll_out ? &lse : nullptr);
+      const int forced = a.target ? (tgt[bs] >> 8) : -1;
+      const int c = draw_wave(zs, zs2, b2l, uni[bs].x, forced, zk, a.nll_out ? &lse : nullptr);
       if (j == 0 && a.zc_out) *(float4*)(a.zc_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {
         misc[1] = c;
@@ -399,47 +458,42 @@ __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
           fmisc[3] = zk[c];
         }
       }
-    }
-    __syncthreads();
-    if (tr) trace_at(a, t, 5);
-    // (4) fine gates of every unit (c_t reaches the fine half only)
-    const int c = misc[1];
-    if (gate) {
-      const u64* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
-      float v[3];
-      if (poll_pref<3>(ps, pf, tag, v, a)) {
-        const float x2 = fscale(c);
-        float au = v[0] + __builtin_fmaf(ifn[0][2], x2, __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0));
-        float ar = v[1] + __builtin_fmaf(ifn[1][2], x2, __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0));
-        float ie = __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0)) + cbe_f;
-        float uu = fsig(au), rr = fsig(ar);
-        float e = ftanh(__builtin_fmaf(rr, v[2], ie));
-        hf = __builtin_fmaf(uu, hf, (1.0f - uu) * e);
-        aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
-        if (own) xpub(YF + u, tag, hf);
-      } else {
-        misc[0] = 1;
-      }
+    } else {
+      fine_pre(tag, fscale(misc[2]), fscale(misc[3]));
     }
     __syncthreads();
     if (misc[0]) return;
-    if (tr) trace_at(a, t, 6);
-    // (5) own rows of O3 -> relu -> own columns of O4 -> partial fine logits
+    if (trw) trace_at(a, t, 5);
+    // (5) fine gates of every unit, finished with c_t (c_t reaches the fine half only)
+    const int c = misc[1];
+    if (gate) {
+      const float x2 = fscale(c);
+      const float uu = fsig(__builtin_fmaf(ifn[0][2], x2, fu)), rr = fsig(__builtin_fmaf(ifn[1][2], x2, fr));
+      const float e = ftanh(__builtin_fmaf(rr, fe, __builtin_fmaf(ifn[2][2], x2, fie) + cbe_f));
+      hf = __builtin_fmaf(uu, hf, (1.0f - uu) * e);
+      aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
+      yv[u] = hf;
+    }
+    __syncthreads();
+    if (trw) trace_at(a, t, 6);
+    if (wave == DW) xpub(YF + 64 * j + lane, tag, yv[64 * j + lane]);
+    // (6) own rows of O3 -> relu -> own columns of O4 -> partial fine logits
     first_layer(W3, imf, b3r);
-    if (tr) trace_at(a, t, 7);
+    if (trw) trace_at(a, t, 7);
     second_layer(W4, PFo, tag);
-    if (tr) trace_at(a, t, 8);
-    // (6) fine logits of all heads, draw f_t; next step's coarse words are
-    // loaded while the draw runs
-    gather_logits(PF, tag);
+    if (trw) trace_at(a, t, 8);
+    if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 14);
+    // (7) fine logits of all heads; next step's coarse words are loaded
+    gather_logits(PF, tag, t, false);
     if (t + 1 < a.T) prefetch_coarse(n + 1);
     __syncthreads();
     if (misc[0]) return;
-    if (tr) trace_at(a, t, 9);
-    if (wave == 0) {
+    if (trw) trace_at(a, t, 9);
+    // (8) draw f_t on the draw wave; meanwhile the next coarse gates start
+    if (wave == DW) {
       float lse;
-      const int forced = a.target ? (a.target[t] & 255) : -1;
-      const int f = draw_wave(zs, zs + 256, b4l, fmisc[1], forced, zk, a.nll_out ? &lse : nullptr);
+      const int forced = a.target ? (tgt[bs] & 255) : -1;
+      const int f = draw_wave(zs, zs2, b4l, uni[bs].y, forced, zk, a.nll_out ? &lse : nullptr);
       if (j == 0 && a.zf_out) *(float4*)(a.zf_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {
         if (j == 0) {
@@ -449,9 +503,12 @@ __device__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
         misc[2] = c;
         misc[3] = f;
       }
+    } else if (t + 1 < a.T) {
+      coarse_pre(tag + 1, fscale(c));
     }
     __syncthreads();
-    if (tr) trace_at(a, t, 10);
+    if (misc[0]) return;
+    if (trw) trace_at(a, t, 10);
   }
   if (j == 0) {
     if (a.h_out && gate) {
@@ -519,7 +576,7 @@ __device__ void unit_role(const PersistArgs& a, int k, unsigned char* lds) {
     }
   };
   // columns [KT, 2KT): fine inputs; then publish with `tag`
-  auto phase_f = [&](uint32_t tag, const float* cbr) {
+  auto phase_f = [&](uint32_t tag, float cbv) {
     if (cw) {
 #pragma unroll
       for (int i = 0; i < KT; i += 2) {
@@ -536,35 +593,74 @@ __device__ void unit_role(const PersistArgs& a, int k, unsigned char* lds) {
     }
     if ((cw || fw) && lane < 16) {
       float v = mfma_row(acc0) + mfma_row(acc1);
-      if (g < 2) v += cbr[row];                 // bias + conditioning of the u and r gates
+      if (g < 2) v += cbv;                      // bias + conditioning of the u and r gates
       xpub(dst, tag, v);
     }
   };
+  __builtin_amdgcn_s_waitcnt(0);   // weights and operands are in before the loop (see head_role)
   // step 0's pre-activations from the initial state
   phase_c();
-  phase_f(1u, cb_row(a, a.t0));
+  phase_f(1u, (cw || fw) && g < 2 ? cb_row(a, a.t0)[row] : 0.0f);
   const u64* YC = a.xc + P.x_yc;
   const u64* YF = a.xc + P.x_yf;
+  // Wait for a half of h.  Waves 3 and 7 own no row tile and never store, so
+  // their loads do not wait for the publishing waves' store acknowledgements:
+  // lane jj of wave 3 watches the last word of head jj's slice (little polling
+  // traffic while the heads exchange logits), then waves 3 and 7 read every
+  // word once and write operand tiles kt0 ...
+  const bool reader = wave == 3 || wave == 7;
+  auto gather_half = [&](const u64* Y, uint32_t tag, int kt0, bool flags) {
+    if (flags) {
+      if (wave == 3) {
+        float y;
+        const int hj = lane < P.NH ? lane : 0;
+        if (!poll_sleepy(Y + 64 * hj + 63, tag, &y, a)) misc[0] = 1;
+      }
+      __syncthreads();
+      if (misc[0]) return;
+    }
+    if (reader) {
+      const int r = (wave == 3 ? 0 : 64) + lane;
+      uint32_t pending = 0;
+      float y[4] = {0, 0, 0, 0};
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+        if (r + 128 * m < Hh) pending |= 1u << m;
+      WaitBudget wb{wr_clock(), 0};
+      while (pending) {
+        u64 w[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) w[m] = (pending >> m & 1u) ? xpeek(Y + r + 128 * m) : 0;
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+          if ((pending >> m & 1u) && xtag(w[m]) == tag) {
+            y[m] = xval(w[m]);
+            pending &= ~(1u << m);
+          }
+        if (pending && !wait_ok(wb, a.err, a.limit, a.err)) {
+          misc[0] = 1;
+          break;
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int i = r + 128 * m;
+        if (i < Hh) aput(img + (kt0 + (i >> 5)) * WR_FRAG, i & 31, y[m]);
+      }
+    }
+    __syncthreads();
+  };
   for (int64_t t = 0; t + 1 < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
-    const float* cbr = cb_row(a, a.t0 + t + 1);
-    if (tid < Hh) {
-      float y;
-      if (poll_sleepy(YC + tid, tag, &y, a)) aput(img + (tid >> 5) * WR_FRAG, tid & 31, y);
-      else misc[0] = 1;
-    }
-    __syncthreads();
+    // bias + conditioning of this lane's row for the next step, loaded early
+    const float cbv = (cw || fw) && lane < 16 && g < 2 ? cb_row(a, a.t0 + t + 1)[row] : 0.0f;
+    gather_half(YC, tag, 0, true);
     if (misc[0]) return;
     phase_c();
-    if (tid < Hh) {
-      float y;
-      if (poll_sleepy(YF + tid, tag, &y, a)) aput(img + (KT + (tid >> 5)) * WR_FRAG, tid & 31, y);
-      else misc[0] = 1;
-    }
-    __syncthreads();
+    gather_half(YF, tag, KT, false);   // y_f gates the next coarse step: no flag phase
     if (misc[0]) return;
     if (k == 0 && tid == 0) trace_at(a, t + 1, 11);
-    phase_f(tag + 1, cbr);
+    phase_f(tag + 1, cbv);
     if (k == 0 && tid == 0) trace_at(a, t + 1, 12);
   }
 }
