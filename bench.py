@@ -35,6 +35,31 @@ def weight_bytes_per_step(w: dict) -> int:
     return n * bytes_per
 
 
+def kernel_source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("wr_persist.hip", "wr_device.h", "wr_layout.h", "wr_args.h"):
+        with open(os.path.join(ROOT, "paper_1802_08435_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary of this workload, or None
+    when the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"wr_persist_kernel_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    i = text.find("```json")
+    if i < 0:
+        return None
+    d = json.loads(text[i + 7:text.index("```", i + 7)])
+    if d.get("kernel_source_sha256_16") != kernel_source_digest():
+        return None
+    return d["fetch_bytes_per_launch"] + d["write_bytes_per_launch"]
+
+
 def cpu_baseline(w: dict, T: int, feat, budget_s: float = 12.0) -> dict:
     """The oracle as it stands, single-threaded on the host, on a bounded prefix."""
     import numpy as np
@@ -59,6 +84,8 @@ def main() -> int:
     ap.add_argument("--config", default="dense896")
     ap.add_argument("--samples", type=int, default=0, help="override samples per utterance")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -70,6 +97,15 @@ def main() -> int:
     from paper_1802_08435_amd import synth, wavernn
 
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}), flush=True)
+        return 0
     w = synth.preset(args.config)
     S, T = w["streams"], args.samples or w["samples"]
     r_format = {None: "dense", (4, 4): "bsr4x4", (16, 1): "bsr16x1"}[w["block"]]
@@ -103,6 +139,8 @@ def main() -> int:
     achieved = wb * steps_per_launch / (ms / 1000.0) / 1e9
     ncu = grid
     lds_peak = ncu * LDS_BYTES_PER_CLK_CU * CLOCK_GHZ
+    tb = measured_traffic(args.config) if T == w["samples"] and S == w["streams"] else None
+    traffic = None if tb is None else round(tb / (ms / 1000.0) / 1e9, 2)
     line = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -122,8 +160,8 @@ def main() -> int:
         "x_realtime": round(value / 24000.0, 3),
         "call_ms_min": round(min(call_ms), 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None,
-                     "bytes_per_step": wb, "steps_per_launch": steps_per_launch,
+                     "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": traffic,
+                     "kernel": path, "bytes_per_step": wb, "steps_per_launch": steps_per_launch,
                      "lds_frac": round(achieved / lds_peak, 5)},
     }
     if not args.no_cpu_baseline:

@@ -393,3 +393,15 @@ def test_pruned_blocks_equal_dense_with_zeroed_blocks():
     assert np.all(d["R"][full == 0] == 0) and np.all(d["R"][full == 1] != 0)
     r = O.run(W(d), 1, 300, seed=1)
     assert r["out"].shape == (1, 300)
+
+
+def test_wavernn896_parameter_count_matches_the_paper():
+    """Sec. 2.1: WaveRNN-896 has about 3M parameters, and streaming them for
+    each of 24,000 samples at 4 bytes each is about 288 GB.  The shapes read
+    from Eq. 2 (R 3H x H, O1/O3 Hh x Hh, O2/O4 256 x Hh) must give that count."""
+    from paper_1802_08435_amd import synth
+    w = synth.preset("dense896")
+    n = sum(w[k].size for k in ("R", "O1", "O2", "O3", "O4"))
+    assert n == 3 * 896 * 896 + 2 * 448 * 448 + 2 * 256 * 448
+    assert abs(n - 3e6) / 3e6 < 0.02
+    assert abs(n * 24e3 * 4 / 1e9 - 288) / 288 < 0.02
