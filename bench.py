@@ -110,7 +110,7 @@ def main() -> int:
     S, T = w["streams"], args.samples or w["samples"]
     r_format = {None: "dense", (4, 4): "bsr4x4", (16, 1): "bsr16x1"}[w["block"]]
     m = wavernn.Model(w, dtype="bf16" if w["bf16"] else "f32", r_format=r_format, max_streams=S)
-    path, grid, block = m.path()
+    path, grid, block = m.path(S)
     feat_np = synth.features(S, T, per_stream_seed=S > 1)
     feat = torch.from_numpy(feat_np).cuda()
     out = torch.empty(S, T, dtype=torch.uint16, device="cuda")

@@ -138,9 +138,12 @@ wavernn_status wavernn_device_status(wavernn_model* m, void* stream);
 wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t t0, int64_t n, float* out_dev,
                                       void* stream);
 
-/* Which kernel serves the model: 0 single-workgroup fp32, 1 multi-workgroup
- * persistent, 2 batched (MFMA).  Fills *grid and *block with its launch shape. */
-int32_t wavernn_model_path(const wavernn_model* m, int32_t* grid, int32_t* block);
+/* Which kernel serves a call on n_streams streams: 0 single-workgroup fp32,
+ * 1 multi-workgroup persistent (one launch per stream), 2 batched persistent
+ * (up to 64 streams in one launch, 8 per group of workgroups; models created
+ * with max_streams > 1 and a hidden size the persistent kernel serves).
+ * Fills *grid and *block with its launch shape; -1 for a null model. */
+int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* grid, int32_t* block);
 
 /* Diagnostics: make later wavernn_sample / wavernn_score_teacher_forced calls
  * of the multi-workgroup persistent kernel record, for the first max_steps

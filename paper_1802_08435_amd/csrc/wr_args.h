@@ -61,9 +61,44 @@ struct PersistArgs {
   int64_t trace_steps;
 };
 
+struct BatchArgs {
+  BatchPlan P;
+  const uint4* hw;          // [NH][8 waves][hw_frags][64 lanes] head fragments (as PersistArgs::hw)
+  const uint4* uw;          // [NU] unit LDS blocks of P.u_lds_w bytes
+  const uint4* ur;          // [NU][8 waves][KT][64] VGPR-resident unit fragments
+  const float* Iw;          // [3H][3], I* mask applied
+  const float* b1;          // [Hh]
+  const float* b2;          // [256]
+  const float* b3;
+  const float* b4;
+  const float* cb;          // [S][n_cb][3H] gate bias + conditioning per vector and frame
+  int64_t n_cb;
+  int frame_len;
+  int S;                    // vectors in use (the last group may be partly idle)
+  int64_t T, t0;
+  uint64_t seed;
+  const uint16_t* target;   // [S][T] or null
+  uint16_t* out;            // [S][T] or null
+  float* zc_out;            // [S][T][256] or null
+  float* zf_out;
+  float* nll_out;           // [S][T] or null
+  const float* h_in;        // [S][H] or null
+  const uint8_t* c_in;      // [S]
+  const uint8_t* f_in;
+  float* h_out;
+  uint8_t* c_out;
+  uint8_t* f_out;
+  u64* xc;                  // [G][P.x_words] exchange words, zeroed before the launch
+  unsigned* err;
+  u64 limit;
+  u64* trace;               // [trace_steps][WR_TRACE_SLOTS] (group 0) or null
+  int64_t trace_steps;
+};
+
 // Kernel entry points (taken by address in the launcher).
 const void* wr_small_kernel_ptr();
 const void* wr_uniforms_kernel_ptr();
 const void* wr_persist_kernel_ptr(int KH);   // null if no instantiation for KH
 const void* wr_cond_kernel_ptr();
+const void* wr_batch_kernel_ptr(int KH);     // null if no instantiation for KH
 const void* wr_fill_kernel_ptr();

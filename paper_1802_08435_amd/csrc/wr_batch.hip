@@ -1,0 +1,541 @@
+// Batched persistent WaveRNN sampler: up to 64 independent utterances per
+// launch, WR_BL = 8 per group (Sec. 2.1; many utterances share one GPU).
+//
+// A group is the batch-1 structure of wr_persist.hip serving 8 vectors at
+// once.  Every matrix-vector product of the step becomes an 8-row product on
+// the matrix cores at the same instruction count: operand A holds vector b in
+// rows 2b (bf16 high part) and 2b+1 (remainder), and lane l of the result
+// holds vectors 2(l/16) and 2(l/16)+1 of row l%16.  Per step and half, the
+// heads evaluate every gate of every vector, run their O1 rows / O2 columns,
+// all-reduce 8 x 256 partial logits, and draw the 8 classes on 8 waves.
+#include "wr_kern.h"
+
+namespace {
+
+constexpr int L = WR_BL;
+
+// Bias + conditioning row of vector b at absolute sample n.
+__device__ __forceinline__ const float* bcb_row(const BatchArgs& a, int b, int64_t n) {
+  int64_t fr = n / a.frame_len;
+  if (fr >= a.n_cb) fr = a.n_cb - 1;
+  return a.cb + ((size_t)b * a.n_cb + fr) * 3 * a.P.H;
+}
+
+// Wait until the N words base[k*stride] (k < N) carry `tag`; values to v[].
+template <int N>
+__device__ __forceinline__ bool poll_strided(const u64* base, int stride, uint32_t tag, float* v, const BatchArgs& a) {
+  uint64_t pending = N >= 64 ? ~0ull : (1ull << N) - 1ull;
+  WaitBudget wb{wr_clock(), 0};
+  for (;;) {
+    u64 w[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1ull) ? xpeek(base + (size_t)k * stride) : 0;
+#pragma unroll
+    for (int k = 0; k < N; ++k)
+      if ((pending >> k & 1ull) && xtag(w[k]) == tag) {
+        v[k] = xval(w[k]);
+        pending &= ~(1ull << k);
+      }
+    if (!pending) return true;
+    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+  }
+}
+
+// Wait until the N words at addr(k) (k < N) carry `tag`; values to v[].
+template <int N, class F>
+__device__ __forceinline__ bool poll_map(F addr, uint32_t tag, float* v, const BatchArgs& a) {
+  uint64_t pending = N >= 64 ? ~0ull : (1ull << N) - 1ull;
+  WaitBudget wb{wr_clock(), 0};
+  for (;;) {
+    u64 w[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1ull) ? xpeek(addr(k)) : 0;
+#pragma unroll
+    for (int k = 0; k < N; ++k)
+      if ((pending >> k & 1ull) && xtag(w[k]) == tag) {
+        v[k] = xval(w[k]);
+        pending &= ~(1ull << k);
+      }
+    if (!pending) return true;
+    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+  }
+}
+
+// Wait until *p carries `tag` (the slow path of the straight-line reads below).
+__device__ __forceinline__ bool wait_word(const u64* p, uint32_t tag, float* v, const BatchArgs& a) {
+  return poll_map<1>([&](int) { return p; }, tag, v, a);
+}
+
+// ------------------------------------------------------------------ head role
+template <int KH>
+__device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, unsigned char* lds) {
+  constexpr int KT = 2 * KH;
+  constexpr int NH = KH;
+  const BatchPlan& P = a.P;
+  const int H = P.H, Hh = P.Hh;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  unsigned char* imc = lds;                        // y_c operand image [KT]
+  unsigned char* imf = imc + KT * WR_FRAG;         // y_f operand image [KT]
+  unsigned char* imo = imf + KT * WR_FRAG;         // relu(first layer) image [2]
+  float* op = (float*)(imo + 2 * WR_FRAG);         // [2][L][64] first-layer partials
+  float* zs = op + 2 * L * 64;                     // [L][256] logit sums over the heads
+  float* zk = zs + L * 256;                        // [L][256] logits of the last draws
+  float* yv = zk + L * 256;                        // [L][448] y_c or y_f (fp32), published by wave 7
+  float* hcs = yv + L * 448;                       // [L][448] coarse half of h
+  float* hfs = hcs + L * 448;                      // [L][448] fine half of h
+  float* gv = hfs + L * 448;                       // [3L][448] polled pre-activations of the gate threads
+  int* misc = (int*)(gv + 3 * L * 448);            // [0] abort, [8+b] c_t, [16+b] c_prev, [24+b] f_prev
+  float* fmisc = (float*)(misc + 32);              // [b] lse_c, [8+b] z_c[c] of vector b
+  float2* uni = (float2*)(misc + 64);              // [2][L][64] (u_c, u_f) of a batch of 64 steps
+  int* tgt = (int*)(uni + 2 * L * 64);             // [2][L][64] teacher-forcing targets
+
+  const int v0 = g * L;                            // first vector of this group
+  for (int i = tid; i < (2 * KT + 2) * WR_FRAG / 16; i += WR_THREADS) ((uint4*)lds)[i] = uint4{0, 0, 0, 0};
+  bf16x8 W1[KH], W3[KH], W2[4], W4[4];
+  {
+    const uint4* src = a.hw + ((size_t)(j * 8 + wave) * P.hw_frags) * 64 + lane;
+#pragma unroll
+    for (int i = 0; i < KH; ++i) W1[i] = __builtin_bit_cast(bf16x8, src[(size_t)i * 64]);
+#pragma unroll
+    for (int i = 0; i < KH; ++i) W3[i] = __builtin_bit_cast(bf16x8, src[(size_t)(KH + i) * 64]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) W2[i] = __builtin_bit_cast(bf16x8, src[(size_t)(2 * KH + i) * 64]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) W4[i] = __builtin_bit_cast(bf16x8, src[(size_t)(2 * KH + 4 + i) * 64]);
+  }
+  const int u = tid;
+  const bool gate = u < Hh;
+  float ic[3][2], ifn[3][3];
+  if (gate) {
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      ic[q][0] = a.Iw[3 * (q * H + u) + 0];
+      ic[q][1] = a.Iw[3 * (q * H + u) + 1];
+      ifn[q][0] = a.Iw[3 * (q * H + Hh + u) + 0];
+      ifn[q][1] = a.Iw[3 * (q * H + Hh + u) + 1];
+      ifn[q][2] = a.Iw[3 * (q * H + Hh + u) + 2];
+    }
+    for (int b = 0; b < L; ++b) {
+      const int vb = min(v0 + b, a.S - 1);
+      hcs[b * 448 + u] = a.h_in ? a.h_in[(size_t)vb * H + u] : 0.0f;
+      hfs[b * 448 + u] = a.h_in ? a.h_in[(size_t)vb * H + Hh + u] : 0.0f;
+    }
+  }
+  // relu thread: vector rb, row rr of this head's 64 first-layer rows
+  const int rb = tid >> 6, rr = tid & 63;
+  const float b1r = a.b1[j * 64 + rr], b3r = a.b3[j * 64 + rr];
+  // draw wave w draws vector w: class biases of its 4 classes per lane
+  const float4 b2l = *(const float4*)(a.b2 + 4 * lane);
+  const float4 b4l = *(const float4*)(a.b4 + 4 * lane);
+  if (tid < L) {
+    const int vb = min(v0 + tid, a.S - 1);
+    misc[0] = 0;
+    misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
+    misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
+  }
+  u64* X = a.xc + (size_t)g * P.x_words;
+  const u64* GA = X + P.x_ga;
+  const u64* GF = X + P.x_gf;
+  u64* YC = X + P.x_yc;
+  u64* YF = X + P.x_yf;
+  u64* PCo = X + P.x_pc + (size_t)j * L * 256;
+  u64* PFo = X + P.x_pf + (size_t)j * L * 256;
+  const u64* PC = X + P.x_pc;
+  const u64* PF = X + P.x_pf;
+  const int rt = wave & 3, kc = wave >> 2;
+  const int bl0 = 2 * (lane >> 4);                 // vectors of this lane's MFMA results: bl0, bl0 + 1
+
+  auto first_layer = [&](const bf16x8* W, const unsigned char* img, float bias) {
+    f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < KH; i += 2) {
+      acc0 = mfma(afrag(img, kc * KH + i), W[i], acc0);
+      if (i + 1 < KH) acc1 = mfma(afrag(img, kc * KH + i + 1), W[i + 1], acc1);
+    }
+    const int r = 16 * rt + (lane & 15);
+    op[(kc * L + bl0) * 64 + r] = mfma_row(acc0) + mfma_row(acc1);
+    op[(kc * L + bl0 + 1) * 64 + r] = mfma_row_hi(acc0) + mfma_row_hi(acc1);
+    __syncthreads();
+    aput(imo + (rr >> 5) * WR_FRAG, rr & 31, wr_relu((op[rb * 64 + rr] + op[(L + rb) * 64 + rr]) + bias), rb);
+    __syncthreads();
+  };
+  // class tiles 2*wave, 2*wave+1 over this head's 64 columns, for all vectors
+  auto second_layer = [&](const bf16x8* W, u64* dst, uint32_t tag) {
+    const bf16x8 x0 = afrag(imo, 0), x1 = afrag(imo, 1);
+    f32x4 A = mfma(x0, W[0], f32x4{0, 0, 0, 0});
+    f32x4 B = mfma(x0, W[2], f32x4{0, 0, 0, 0});
+    A = mfma(x1, W[1], A);
+    B = mfma(x1, W[3], B);
+    const int c0 = 32 * wave + (lane & 15);
+    xpub(dst + bl0 * 256 + c0, tag, mfma_row(A));
+    xpub(dst + (bl0 + 1) * 256 + c0, tag, mfma_row_hi(A));
+    xpub(dst + bl0 * 256 + c0 + 16, tag, mfma_row(B));
+    xpub(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B));
+  };
+  // Sums over the heads, in head order.  Lane jj of wave 0 first watches the
+  // last word head jj publishes; then thread (class v, parity h) reads the
+  // partials of vectors h, h + 2, h + 4, h + 6 of every head in one batch of
+  // loads; a word that is not in yet sends the thread to a slow path that
+  // waits word by word, still in head order.
+  auto gather_logits = [&](const u64* src, uint32_t tag) {
+    if (wave == 0) {
+      float y;
+      const int hj = lane < NH ? lane : 0;
+      if (!wait_word(src + ((size_t)hj * L + L - 1) * 256 + 255, tag, &y, a)) misc[0] = 1;
+    }
+    __syncthreads();
+    if (misc[0]) return;
+    const int v = tid & 255, h = tid >> 8;
+    const u64* base = src + h * 256 + v;            // word (jj, h + 2m) at base + (jj L + 2m) 256
+    float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    bool stale = false;
+    constexpr int NH0 = (NH + 1) / 2;                // heads in the first batch of loads
+    // two batches of loads (all in flight within a batch; more at once would
+    // keep too many addresses live)
+#pragma unroll 1
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int jj = half ? NH0 : 0; jj < (half ? NH : NH0); ++jj)
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const u64 w = xpeek(base + (size_t)(jj * L + 2 * m) * 256);
+          stale |= xtag(w) != tag;
+          s[m] += xval(w);
+        }
+    if (stale) {
+      for (int m = 0; m < 4; ++m) s[m] = 0.0f;
+      for (int jj = 0; jj < NH; ++jj)
+        for (int m = 0; m < 4; ++m) {
+          float x;
+          if (!wait_word(base + (size_t)(jj * L + 2 * m) * 256, tag, &x, a)) {
+            misc[0] = 1;
+            return;
+          }
+          s[m] += x;
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < 4; ++m) zs[(h + 2 * m) * 256 + v] = s[m];
+  };
+  // The 3L pre-activation words of gate thread u, read in one batch into the
+  // LDS staging area gv (word k at gv[k * 448 + u]); stragglers are waited for.
+  auto read_gates = [&](const u64* G, uint32_t tag) {
+    uint32_t stale = 0;
+#pragma unroll 1
+    for (int half = 0; half < 2; ++half) {           // two batches of 12 loads
+      u64 w[3 * L / 2];
+#pragma unroll
+      for (int k = 0; k < 3 * L / 2; ++k) w[k] = xpeek(G + (size_t)(half * 3 * L / 2 + k) * Hh + u);
+#pragma unroll
+      for (int k = 0; k < 3 * L / 2; ++k) {
+        if (xtag(w[k]) != tag) stale |= 1u << (half * 3 * L / 2 + k);
+        gv[(half * 3 * L / 2 + k) * 448 + u] = xval(w[k]);
+      }
+    }
+    while (stale) {
+      const int k = __builtin_ctz(stale);
+      stale &= stale - 1;
+      if (!wait_word(G + (size_t)k * Hh + u, tag, gv + k * 448 + u, a)) {
+        misc[0] = 1;
+        return;
+      }
+    }
+  };
+  auto fill_batch = [&](int64_t t, int buf) {       // wave w: vector w's uniforms / targets
+    const int64_t s = t + lane;
+    const int vb = min(v0 + wave, a.S - 1);
+    if (s < a.T) {
+      float uc, uf;
+      wr_uniforms(a.seed, (uint64_t)vb, (uint64_t)(a.t0 + s), &uc, &uf);
+      uni[(buf * L + wave) * 64 + lane] = float2{uc, uf};
+      tgt[(buf * L + wave) * 64 + lane] = a.target ? a.target[(size_t)vb * a.T + s] : 0;
+    }
+  };
+  fill_batch(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  const bool trw = g == 0 && j == 0 && tid == WR_THREADS - 64;
+  const bool live = v0 + wave < a.S;               // draw wave's vector is in use
+
+  for (int64_t t = 0; t < a.T; ++t) {
+    const int64_t n = a.t0 + t;
+    const uint32_t tag = (uint32_t)(t + 1);
+    if (trw) trace_at(a, t, 0);
+    const int bs = (int)((t >> 6) & 1) * L * 64 + wave * 64 + (int)(t & 63);   // draw wave's batch slot
+    if ((t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
+    // (1) coarse gates of every unit and vector: the 24 pre-activation words of
+    // thread u are polled together and staged in LDS, then one vector at a time
+    if (gate) {
+      read_gates(GA, tag);
+#pragma unroll 1
+      for (int b = 0; b < L; ++b) {
+        const float cbe = bcb_row(a, min(v0 + b, a.S - 1), n)[2 * H + u];
+        const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]);
+        const float uu = fsig(gv[(3 * b) * 448 + u] + __builtin_fmaf(ic[0][1], x1, ic[0][0] * x0));
+        const float rg = fsig(gv[(3 * b + 1) * 448 + u] + __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0));
+        const float e = ftanh(
+            __builtin_fmaf(rg, gv[(3 * b + 2) * 448 + u], __builtin_fmaf(ic[2][1], x1, ic[2][0] * x0) + cbe));
+        const float hn = __builtin_fmaf(uu, hcs[b * 448 + u], (1.0f - uu) * e);
+        hcs[b * 448 + u] = hn;
+        aput(imc + (u >> 5) * WR_FRAG, u & 31, hn, b);
+        yv[b * 448 + u] = hn;
+      }
+    }
+    __syncthreads();
+    if (misc[0]) return;
+    if (trw) trace_at(a, t, 1);
+    if (wave == 7)
+#pragma unroll
+      for (int b = 0; b < L; ++b) xpub(YC + b * Hh + 64 * j + lane, tag, yv[b * 448 + 64 * j + lane]);
+    // (2) O1 rows, relu, O2 columns -> partial coarse logits of 8 vectors
+    first_layer(W1, imc, b1r);
+    second_layer(W2, PCo, tag);
+    if (trw) trace_at(a, t, 3);
+    // (3) sum over the heads, draw 8 coarse classes (wave w: vector w)
+    gather_logits(PC, tag);
+    __syncthreads();
+    if (misc[0]) return;
+    if (trw) trace_at(a, t, 4);
+    {
+      float lse;
+      const int forced = a.target ? (tgt[bs] >> 8) : -1;
+      const int c = draw_wave<false>(zs + wave * 256, nullptr, b2l, uni[bs].x, forced, zk + wave * 256,
+                                     a.nll_out ? &lse : nullptr);
+      if (j == 0 && live && a.zc_out)
+        *(float4*)(a.zc_out + ((size_t)(v0 + wave) * a.T + t) * WR_CLASSES + 4 * lane) =
+            *(const float4*)(zk + wave * 256 + 4 * lane);
+      if (lane == 0) {
+        misc[8 + wave] = c;
+        if (a.nll_out) {
+          fmisc[wave] = lse;
+          fmisc[8 + wave] = zk[wave * 256 + c];
+        }
+      }
+    }
+    __syncthreads();
+    if (trw) trace_at(a, t, 5);
+    // (4) fine gates with c_t
+    if (gate) {
+      read_gates(GF, tag);
+#pragma unroll 1
+      for (int b = 0; b < L; ++b) {
+        const float cbe = bcb_row(a, min(v0 + b, a.S - 1), n)[2 * H + Hh + u];
+        const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]), x2 = fscale(misc[8 + b]);
+        const float uu = fsig(gv[(3 * b) * 448 + u] +
+                              __builtin_fmaf(ifn[0][2], x2, __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0)));
+        const float rg = fsig(gv[(3 * b + 1) * 448 + u] +
+                              __builtin_fmaf(ifn[1][2], x2, __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0)));
+        const float e = ftanh(__builtin_fmaf(
+            rg, gv[(3 * b + 2) * 448 + u],
+            __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0)) + cbe));
+        const float hn = __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e);
+        hfs[b * 448 + u] = hn;
+        aput(imf + (u >> 5) * WR_FRAG, u & 31, hn, b);
+        yv[b * 448 + u] = hn;
+      }
+    }
+    __syncthreads();
+    if (misc[0]) return;
+    if (trw) trace_at(a, t, 6);
+    if (wave == 7)
+#pragma unroll
+      for (int b = 0; b < L; ++b) xpub(YF + b * Hh + 64 * j + lane, tag, yv[b * 448 + 64 * j + lane]);
+    // (5) O3 rows, relu, O4 columns -> partial fine logits
+    first_layer(W3, imf, b3r);
+    second_layer(W4, PFo, tag);
+    if (trw) trace_at(a, t, 8);
+    // (6) sum, draw 8 fine classes
+    gather_logits(PF, tag);
+    __syncthreads();
+    if (misc[0]) return;
+    if (trw) trace_at(a, t, 9);
+    {
+      float lse;
+      const int forced = a.target ? (tgt[bs] & 255) : -1;
+      const int f = draw_wave<false>(zs + wave * 256, nullptr, b4l, uni[bs].y, forced, zk + wave * 256,
+                                     a.nll_out ? &lse : nullptr);
+      const int c = misc[8 + wave];
+      if (j == 0 && live && a.zf_out)
+        *(float4*)(a.zf_out + ((size_t)(v0 + wave) * a.T + t) * WR_CLASSES + 4 * lane) =
+            *(const float4*)(zk + wave * 256 + 4 * lane);
+      if (lane == 0) {
+        if (j == 0 && live) {
+          if (a.out) a.out[(size_t)(v0 + wave) * a.T + t] = (uint16_t)(256 * c + f);
+          if (a.nll_out)
+            a.nll_out[(size_t)(v0 + wave) * a.T + t] = (fmisc[wave] - fmisc[8 + wave]) + (lse - zk[wave * 256 + f]);
+        }
+        misc[16 + wave] = c;
+        misc[24 + wave] = f;
+      }
+    }
+    __syncthreads();
+    if (trw) trace_at(a, t, 10);
+  }
+  if (j == 0) {
+    if (a.h_out && gate)
+      for (int b = 0; b < L; ++b)
+        if (v0 + b < a.S) {
+          a.h_out[(size_t)(v0 + b) * H + u] = hcs[b * 448 + u];
+          a.h_out[(size_t)(v0 + b) * H + Hh + u] = hfs[b * 448 + u];
+        }
+    if (tid < L && v0 + tid < a.S) {
+      if (a.c_out) a.c_out[v0 + tid] = (uint8_t)misc[16 + tid];
+      if (a.f_out) a.f_out[v0 + tid] = (uint8_t)misc[24 + tid];
+    }
+  }
+}
+
+// ------------------------------------------------------------------ unit role
+// Wave q < 4 owns coarse row tile 4k + q, wave 4 + q fine row tile 4k + q;
+// each lane of a wave's result holds two vectors of one row, which it
+// publishes (with bias + conditioning for the u and r gates).
+template <int KH>
+__device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, unsigned char* lds) {
+  constexpr int KT = 2 * KH;
+  const BatchPlan& P = a.P;
+  const int H = P.H, Hh = P.Hh;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const bool fw = wave >= 4;
+  const int q = wave & 3;
+  const unsigned char* WL = lds + (fw ? WR_BUCT * KT + q * KT : q * KT) * WR_FRAG;   // this wave's LDS half
+  unsigned char* img = lds + P.u_lds_w;                                             // [2KT] operand image
+  int* misc = (int*)(img + 2 * KT * WR_FRAG);
+  const int tile = k * WR_BUCT + q;
+  const int gt = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + (lane & 15);
+  const int row = gt * H + (fw ? Hh : 0) + i;                  // R row of this lane
+  const int bl0 = 2 * (lane >> 4);
+  const int v0 = g * L;
+  u64* X = a.xc + (size_t)g * P.x_words;
+  u64* dst = X + (fw ? P.x_gf : P.x_ga) + gt * Hh + i;        // + vector * 3 Hh
+  {
+    const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
+    for (int x = tid; x < P.u_lds_w / 16; x += WR_THREADS) ((uint4*)lds)[x] = src[x];
+    for (int x = tid; x < 2 * KT * WR_FRAG / 16; x += WR_THREADS) ((uint4*)img)[x] = uint4{0, 0, 0, 0};
+    if (tid == 0) misc[0] = 0;
+  }
+  bf16x8 WR[KT];
+  {
+    const uint4* src = a.ur + ((size_t)(k * 8 + wave) * KT) * 64 + lane;
+#pragma unroll
+    for (int x = 0; x < KT; ++x) WR[x] = __builtin_bit_cast(bf16x8, src[(size_t)x * 64]);
+  }
+  __syncthreads();
+  for (int x = tid; x < L * H; x += WR_THREADS) {
+    const int b = x / H, col = x % H;
+    const float y = a.h_in ? a.h_in[(size_t)min(v0 + b, a.S - 1) * H + col] : 0.0f;
+    aput(img + (col >> 5) * WR_FRAG, col & 31, y, b);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  f32x4 acc0, acc1;
+  // coarse inputs (image tiles 0 .. KT-1): coarse waves from LDS, fine waves from VGPRs
+  auto phase_c = [&]() {
+    acc0 = f32x4{0, 0, 0, 0};
+    acc1 = f32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int x = 0; x < KT; x += 2) {
+      const bf16x8 w0 = fw ? WR[x] : *(const bf16x8*)(WL + x * WR_FRAG + lane * 16);
+      acc0 = mfma(afrag(img, x), w0, acc0);
+      if (x + 1 < KT) {
+        const bf16x8 w1 = fw ? WR[x + 1] : *(const bf16x8*)(WL + (x + 1) * WR_FRAG + lane * 16);
+        acc1 = mfma(afrag(img, x + 1), w1, acc1);
+      }
+    }
+  };
+  // fine inputs (image tiles KT .. 2KT-1), then publish with `tag`
+  auto phase_f = [&](uint32_t tag, float cb0, float cb1) {
+#pragma unroll
+    for (int x = 0; x < KT; x += 2) {
+      const bf16x8 w0 = fw ? *(const bf16x8*)(WL + x * WR_FRAG + lane * 16) : WR[x];
+      acc0 = mfma(afrag(img, KT + x), w0, acc0);
+      if (x + 1 < KT) {
+        const bf16x8 w1 = fw ? *(const bf16x8*)(WL + (x + 1) * WR_FRAG + lane * 16) : WR[x + 1];
+        acc1 = mfma(afrag(img, KT + x + 1), w1, acc1);
+      }
+    }
+    xpub(dst + (size_t)bl0 * 3 * Hh, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0);
+    xpub(dst + (size_t)(bl0 + 1) * 3 * Hh, tag, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
+  };
+  auto cbv = [&](int b, int64_t n) {                           // u and r gates carry bias + conditioning
+    return gt < 2 ? bcb_row(a, min(v0 + b, a.S - 1), n)[row] : 0.0f;
+  };
+  // Wait for one half of h of all 8 vectors: lane jj of wave 0 first watches
+  // the last word head jj publishes (vector 7), then every thread reads its
+  // words once and writes the operand tiles kt0 ...
+  auto gather_half = [&](const u64* Y, uint32_t tag, int kt0) {
+    if (wave == 0) {
+      const int hj = lane < P.NH ? lane : 0;
+      float y;
+      if (!poll_strided<1>(Y + (L - 1) * Hh + 64 * hj + 63, 0, tag, &y, a)) misc[0] = 1;
+    }
+    __syncthreads();
+    if (misc[0]) return;
+    constexpr int PER = (L * 448 + WR_THREADS - 1) / WR_THREADS;   // words per thread at most
+    float y[PER];
+    uint32_t pending = 0;
+#pragma unroll
+    for (int m = 0; m < PER; ++m)
+      if (tid + m * WR_THREADS < L * Hh) pending |= 1u << m;
+    WaitBudget wb{wr_clock(), 0};
+    while (pending) {
+      u64 w[PER];
+#pragma unroll
+      for (int m = 0; m < PER; ++m) w[m] = (pending >> m & 1u) ? xpeek(Y + tid + m * WR_THREADS) : 0;
+#pragma unroll
+      for (int m = 0; m < PER; ++m)
+        if ((pending >> m & 1u) && xtag(w[m]) == tag) {
+          y[m] = xval(w[m]);
+          pending &= ~(1u << m);
+        }
+      if (pending && !wait_ok(wb, a.err, a.limit, a.err)) {
+        misc[0] = 1;
+        break;
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      const int x = tid + m * WR_THREADS;
+      if (x < L * Hh && !(pending >> m & 1u)) {
+        const int b = x / Hh, col = x % Hh;
+        aput(img + (kt0 + (col >> 5)) * WR_FRAG, col & 31, y[m], b);
+      }
+    }
+    __syncthreads();
+  };
+  phase_c();
+  phase_f(1u, cbv(bl0, a.t0), cbv(bl0 + 1, a.t0));
+  const u64* YC = X + P.x_yc;
+  const u64* YF = X + P.x_yf;
+  for (int64_t t = 0; t + 1 < a.T; ++t) {
+    const uint32_t tag = (uint32_t)(t + 1);
+    const float cb0 = cbv(bl0, a.t0 + t + 1), cb1 = cbv(bl0 + 1, a.t0 + t + 1);
+    gather_half(YC, tag, 0);
+    if (misc[0]) return;
+    phase_c();
+    gather_half(YF, tag, KT);
+    if (misc[0]) return;
+    phase_f(tag + 1, cb0, cb1);
+  }
+}
+
+}  // namespace
+
+template <int KH>
+__global__ __launch_bounds__(WR_THREADS, 1) void wr_batch_kernel(BatchArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  int g = 0;
+  const int r = wr_batch_role(a.P, blockIdx.x, &g);
+  if (r < 0) return;
+  if (r < a.P.NH) bhead_role<KH>(a, g, r, lds);
+  else bunit_role<KH>(a, g, r - a.P.NH, lds);
+}
+
+const void* wr_batch_kernel_ptr(int KH) {
+  switch (KH) {
+    case 1: return (const void*)wr_batch_kernel<1>;
+    case 2: return (const void*)wr_batch_kernel<2>;
+    case 3: return (const void*)wr_batch_kernel<3>;
+    case 7: return (const void*)wr_batch_kernel<7>;
+    default: return nullptr;
+  }
+}

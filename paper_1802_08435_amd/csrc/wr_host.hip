@@ -74,6 +74,14 @@ struct wavernn_model {
   u64* d_xc = nullptr;
   u64* trace = nullptr;
   int64_t trace_steps = 0;
+  // batched path (several utterances per launch)
+  bool has_batch = false;
+  BatchPlan bplan;
+  const void* bk = nullptr;          // kernel instantiation for bplan.KH
+  uint4 *d_buw = nullptr, *d_bur = nullptr;
+  u64* d_bxc = nullptr;
+  float* d_bcb = nullptr;            // [streams][frames][3H]
+  size_t bcb_cap = 0;                // floats
 
   template <typename T>
   wavernn_status alloc(T** p, size_t bytes) {
@@ -286,6 +294,65 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
   return WAVERNN_OK;
 }
 
+// Batched path: unit blocks for WR_BUCT = 4 row tiles per half (the head
+// fragments are the batch-1 ones).
+wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
+  const BatchPlan& B = m->bplan;
+  const int H = B.H, Hh = B.Hh, KT = B.KT;
+  m->bk = wr_batch_kernel_ptr(B.KH);
+  if (!m->bk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no batched kernel instantiation", H);
+  REff R{&m->cfg, w};
+  auto frag = [&](uint16_t* dst, int tile, bool fine, int col0) {
+    for (int l = 0; l < 64; ++l) {
+      const int g = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + l % 16;
+      const int row = g * H + (fine ? Hh : 0) + i;
+      for (int e = 0; e < 8; ++e) dst[l * 8 + e] = f2bf(R(row, col0 + 8 * (l / 16) + e));
+    }
+  };
+  std::vector<uint16_t> uw((size_t)B.NU * B.u_lds_w / 2), ur((size_t)B.NU * 8 * KT * 512);
+  for (int k = 0; k < B.NU; ++k) {
+    uint16_t* d = uw.data() + (size_t)k * B.u_lds_w / 2;
+    for (int q = 0; q < WR_BUCT; ++q) {
+      const int tile = k * WR_BUCT + q;
+      for (int kt = 0; kt < KT; ++kt) {
+        frag(d + (size_t)(q * KT + kt) * 512, tile, false, 32 * kt);                        // coarse tile, coarse cols
+        frag(d + (size_t)((WR_BUCT + q) * KT + kt) * 512, tile, true, Hh + 32 * kt);         // fine tile, fine cols
+        frag(ur.data() + ((size_t)(k * 8 + q) * KT + kt) * 512, tile, false, Hh + 32 * kt);  // coarse tile, fine cols
+        frag(ur.data() + ((size_t)(k * 8 + 4 + q) * KT + kt) * 512, tile, true, 32 * kt);    // fine tile, coarse cols
+      }
+    }
+  }
+  wavernn_status s;
+  if ((s = m->upload(&m->d_buw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_bur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->alloc(&m->d_bxc, (size_t)B.G * B.x_words * 8)) != WAVERNN_OK) return s;
+  HIPOK(hipFuncSetAttribute(m->bk, hipFuncAttributeMaxDynamicSharedMemorySize, B.lds));
+  int per_cu = 0;
+  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->bk, WR_THREADS, B.lds));
+  hipDeviceProp_t prop;
+  HIPOK(hipGetDeviceProperties(&prop, m->device));
+  if (per_cu < 1 || per_cu * prop.multiProcessorCount < B.grid)
+    return fail(WAVERNN_E_UNSUPPORTED, "batched grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)",
+                B.grid, per_cu, prop.multiProcessorCount);
+  m->has_batch = true;
+  return WAVERNN_OK;
+}
+
+// Bias + conditioning table cb[s][f][3H] for n_streams streams of n_frames frames.
+wavernn_status launch_cond(const wavernn_model* m, const float* feat, int64_t n_frames, int n_streams, float* cb,
+                           hipStream_t st) {
+  const float* Wc = m->d_Wc;
+  const float* bias = m->d_bias;
+  int dc = m->cfg.cond_dim;
+  int rows = 3 * m->cfg.hidden;
+  int64_t nf = n_frames;
+  int ns = n_streams;
+  void* args[] = {&Wc, &bias, &feat, &dc, &rows, &nf, &ns, &cb};
+  const int64_t n = (int64_t)n_streams * n_frames * rows;
+  HIPOK(hipLaunchKernel(wr_cond_kernel_ptr(), dim3((unsigned)((n + 255) / 256)), dim3(256), args, 0, st));
+  return WAVERNN_OK;
+}
+
 wavernn_status launch_fill(u64* p, int64_t n, hipStream_t st) {
   int64_t nb = (n + 255) / 256;
   u64 zero = 0;
@@ -373,16 +440,9 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
   }
   for (int s = 0; s < io.S; ++s) {
     {
-      const float* Wc = m->d_Wc;
-      const float* bias = m->d_bias;
       const float* feat = io.cond ? io.cond + (size_t)s * io.n_frames * Dc : nullptr;
-      int rows = 3 * H;
-      int64_t nf = n_cb;
-      float* cb = m->d_cb;
-      int dc = Dc;
-      void* args[] = {&Wc, &bias, &feat, &dc, &rows, &nf, &cb};
-      HIPOK(hipLaunchKernel(wr_cond_kernel_ptr(), dim3((unsigned)((nf * rows + 255) / 256)), dim3(256), args, 0,
-                            io.st));
+      wavernn_status c = launch_cond(m, feat, n_cb, 1, m->d_cb, io.st);
+      if (c != WAVERNN_OK) return c;
     }
     wavernn_status st = launch_fill(m->d_xc, P.x_words, io.st);
     if (st != WAVERNN_OK) return st;
@@ -427,6 +487,60 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
   return WAVERNN_OK;
 }
 
+wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
+  BatchPlan B;
+  if (!batch_plan(m->cfg.hidden, io.S, &B)) return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d streams", io.S);
+  const int H = B.H, Dc = m->cfg.cond_dim;
+  const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
+  const int64_t n_cb = Dc > 0 ? io.n_frames : 1;
+  const size_t need = (size_t)io.S * n_cb * 3 * H;
+  if (need > m->bcb_cap) {   // grow the per-frame table (the only allocation a call can make)
+    HIPOK(hipStreamSynchronize(io.st));
+    float* p = nullptr;
+    wavernn_status s = m->alloc(&p, need * 4);
+    if (s != WAVERNN_OK) return s;
+    m->d_bcb = p;
+    m->bcb_cap = need;
+  }
+  wavernn_status st = launch_cond(m, io.cond, n_cb, io.S, m->d_bcb, io.st);
+  if (st != WAVERNN_OK) return st;
+  if ((st = launch_fill(m->d_bxc, (int64_t)B.G * B.x_words, io.st)) != WAVERNN_OK) return st;
+  BatchArgs a;
+  memset(&a, 0, sizeof a);
+  a.P = B;
+  a.hw = m->d_hw;
+  a.uw = m->d_buw;
+  a.ur = m->d_bur;
+  a.Iw = m->d_I;
+  a.b1 = m->d_b1;
+  a.b2 = m->d_b2;
+  a.b3 = m->d_b3;
+  a.b4 = m->d_b4;
+  a.cb = m->d_bcb;
+  a.n_cb = n_cb;
+  a.frame_len = Dc > 0 ? frame_len : (1 << 30);
+  a.S = io.S;
+  a.T = io.T;
+  a.t0 = io.init ? io.init->t0 : 0;
+  a.seed = io.seed;
+  a.target = io.target;
+  a.out = io.out;
+  a.zc_out = io.zc;
+  a.zf_out = io.zf;
+  a.nll_out = io.nll;
+  if (io.init) { a.h_in = io.init->h; a.c_in = io.init->c_prev; a.f_in = io.init->f_prev; }
+  if (io.fin) { a.h_out = io.fin->h; a.c_out = io.fin->c_prev; a.f_out = io.fin->f_prev; }
+  a.xc = m->d_bxc;
+  a.err = m->d_err;
+  a.limit = kWaitTicks;
+  a.trace = m->trace;
+  a.trace_steps = m->trace ? m->trace_steps : 0;
+  void* args[] = {&a};
+  // an ordinary launch, as for the batch-1 kernel (co-residency checked at create)
+  HIPOK(hipLaunchKernel(m->bk, dim3(B.grid), dim3(WR_THREADS), args, B.lds, io.st));
+  return WAVERNN_OK;
+}
+
 wavernn_status run(wavernn_model* m, RunIO& io) {
   wavernn_status s = validate_run(m, io);
   if (s != WAVERNN_OK) return s;
@@ -435,7 +549,7 @@ wavernn_status run(wavernn_model* m, RunIO& io) {
   HIPOK(hipGetDevice(&dev));
   if (dev != m->device) return fail(WAVERNN_E_INVALID, "model lives on device %d, current device is %d", m->device, dev);
   if (m->path == PATH_SMALL) return run_small(m, io);
-  if (m->path == PATH_PERSIST) return run_persist(m, io);
+  if (m->path == PATH_PERSIST) return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);
   return fail(WAVERNN_E_UNSUPPORTED, "no kernel for this configuration");
 }
 
@@ -469,6 +583,8 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
     } else {
       m->path = PATH_PERSIST;
       s = build_persist(m, w);
+      if (s == WAVERNN_OK && cfg->max_streams > 1 && batch_plan(H, cfg->max_streams, &m->bplan))
+        s = build_batch(m, w);
     }
   } else {
     s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no kernel plan (need a multiple of 128 whose blocks fit LDS)", H);
@@ -527,14 +643,20 @@ wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t
   return WAVERNN_OK;
 }
 
-int32_t wavernn_model_path(const wavernn_model* m, int32_t* grid, int32_t* block) {
+int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* grid, int32_t* block) {
   if (!m) return -1;
-  int g = 0, b = 0;
-  if (m->path == PATH_SMALL) g = 1, b = 256;
-  else if (m->path == PATH_PERSIST) g = m->plan.grid, b = WR_THREADS;
+  int g = 0, b = 0, path = (int)m->path;
+  BatchPlan B;
+  if (m->path == PATH_SMALL) {
+    g = n_streams > 0 ? n_streams : 1, b = 256;
+  } else if (m->path == PATH_PERSIST && n_streams > 1 && m->has_batch && batch_plan(m->cfg.hidden, n_streams, &B)) {
+    path = PATH_BATCHED, g = B.grid, b = WR_THREADS;
+  } else if (m->path == PATH_PERSIST) {
+    g = m->plan.grid, b = WR_THREADS;
+  }
   if (grid) *grid = g;
   if (block) *block = b;
-  return (int32_t)m->path;
+  return (int32_t)path;
 }
 
 wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps) {

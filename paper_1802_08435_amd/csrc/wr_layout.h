@@ -140,3 +140,75 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024;
 }
+
+// ---------------------------------------------------------------------------
+// Batched persistent kernel: G groups, each a copy of the batch-1 structure
+// serving WR_BL vectors (independent utterances) at once.  The MFMA operand A
+// carries vector b in rows 2b (bf16 high part) and 2b+1 (remainder), so a
+// group does the same number of matrix-core instructions as batch 1.
+// Head j of group g sits at block 8j + g (one XCD per group); the units of all
+// groups take the remaining blocks.  A unit owns UCT = 4 coarse and 4 fine
+// row tiles: waves 0-3 the coarse tiles (coarse columns in LDS, fine columns
+// in VGPRs), waves 4-7 the fine tiles (coarse columns in VGPRs, fine columns
+// in LDS).
+// ---------------------------------------------------------------------------
+#define WR_BL 8           // vectors per group
+#define WR_BUCT 4         // coarse (and fine) row tiles per batched unit
+
+struct BatchPlan {
+  int H, Hh, KT, KH, NH, NCT, NU, G, grid;
+  int hw_frags;           // head fragments per wave (as the batch-1 plan)
+  int u_lds_w;            // unit LDS weights: [UCT][KT] coarse tiles, then [UCT][KT] fine tiles
+  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // per group: y [L][Hh], g [L][3][Hh], p [NH][L][256]
+  int lds_h, lds_u, lds;
+};
+
+// Role of block b: head index j (group *g), NH + unit index, or -1 (idle).
+WR_HD inline int wr_batch_role(const BatchPlan& P, int b, int* g) {
+  if (b < 8 * P.NH && b % 8 < P.G) {
+    *g = b % 8;
+    return b / 8;
+  }
+  const int before = b < 8 * P.NH ? (b / 8) * P.G + (b % 8 < P.G ? b % 8 : P.G) : P.NH * P.G;
+  const int ku = b - before;
+  if (ku >= P.NU * P.G) return -1;
+  *g = ku / P.NU;
+  return P.NH + ku % P.NU;
+}
+
+WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P) {
+  if (H <= 0 || H % 128 || n_vectors < 1 || n_vectors > 8 * WR_BL) return false;
+  P->H = H;
+  P->Hh = H / 2;
+  P->KT = P->Hh / 32;
+  P->KH = P->KT / 2;
+  P->NH = P->Hh / WR_HROWS;
+  P->NCT = 3 * P->Hh / 16;
+  if (P->NH > 7 || P->Hh > WR_THREADS - 64 || P->NCT % WR_BUCT) return false;
+  P->NU = P->NCT / WR_BUCT;
+  P->G = (n_vectors + WR_BL - 1) / WR_BL;
+  int gr = 8 * (P->NH - 1) + P->G;           // the last head block + 1
+  while (gr - P->NH * P->G < P->NU * P->G) ++gr;
+  P->grid = gr;
+  P->hw_frags = 2 * P->KH + 8;
+  P->u_lds_w = 2 * WR_BUCT * P->KT * WR_FRAG;
+  int o = 0;
+  auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
+  P->x_yc = take(WR_BL * P->Hh);
+  P->x_yf = take(WR_BL * P->Hh);
+  P->x_ga = take(WR_BL * 3 * P->Hh);
+  P->x_gf = take(WR_BL * 3 * P->Hh);
+  P->x_pc = take(P->NH * WR_BL * 256);
+  P->x_pf = take(P->NH * WR_BL * 256);
+  P->x_words = o;
+  // head: operand images (2 KT + 2 fragments), first-layer partials [2][L][64],
+  // logit sums [L][256], logits [L][256], y, both halves of h and the polled
+  // pre-activations [6][L][448], misc [64],
+  // uniforms [2][L][64][2], targets [2][L][64]
+  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * WR_BL * 64 + 2 * WR_BL * 256 + 6 * WR_BL * 448 + 64 +
+                                               2 * WR_BL * 64 * 2 + 2 * WR_BL * 64);
+  // unit: weights, operand image (2 KT fragments), misc [16]
+  P->lds_u = P->u_lds_w + 2 * P->KT * WR_FRAG + 4 * 16;
+  P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
+  return P->lds <= 160 * 1024 && P->grid <= 256;
+}

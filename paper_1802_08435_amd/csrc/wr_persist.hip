@@ -464,18 +464,19 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_persist_kernel(PersistArgs a
   else unit_role<KH>(a, r - a.P.NH, lds);
 }
 
-// Bias + conditioning of every gate row for every frame (Sec. 2 conditioning):
-// cb[f][row] = sum_q W_cond[row][q] feat[f][q] (fma chain in q order) + b[row].
+// Bias + conditioning of every gate row for every frame of every stream
+// (Sec. 2 conditioning): cb[s][f][row] = sum_q W_cond[row][q] feat[s][f][q]
+// (fma chain in q order) + b[row].
 extern "C" __global__ void wr_cond_kernel(const float* Wc, const float* bias, const float* feat, int Dc, int rows,
-                                          int64_t n_frames, float* cb) {
+                                          int64_t n_frames, int n_streams, float* cb) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= n_frames * rows) return;
-  const int64_t f = idx / rows;
+  if (idx >= (int64_t)n_streams * n_frames * rows) return;
+  const int64_t sf = idx / rows;                  // stream * n_frames + frame
   const int row = (int)(idx % rows);
   float acc = 0.0f;
   if (Dc > 0) {
     const float* w = Wc + (size_t)row * Dc;
-    const float* x = feat + (size_t)f * Dc;
+    const float* x = feat + (size_t)sf * Dc;
     for (int q = 0; q < Dc; ++q) acc = __builtin_fmaf(w[q], x[q], acc);
     acc = acc + bias[row];
   } else {

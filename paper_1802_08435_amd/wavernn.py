@@ -68,7 +68,7 @@ def lib():
         L.wavernn_set_trace.restype = ctypes.c_int
         L.wavernn_set_trace.argtypes = [vp, vp, i64]
         L.wavernn_model_path.restype = i32
-        L.wavernn_model_path.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.wavernn_model_path.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.wavernn_last_error.restype = ctypes.c_char_p
         L.wavernn_last_error.argtypes = []
         _lib = L
@@ -140,9 +140,10 @@ class Model:
     def handle(self):
         return self._h
 
-    def path(self):
+    def path(self, n_streams: int = 1):
+        """(kernel name, grid, block) serving a call on n_streams streams."""
         g, b = ctypes.c_int32(), ctypes.c_int32()
-        p = lib().wavernn_model_path(self._h, ctypes.byref(g), ctypes.byref(b))
+        p = lib().wavernn_model_path(self._h, n_streams, ctypes.byref(g), ctypes.byref(b))
         return PATHS.get(p, str(p)), g.value, b.value
 
     @staticmethod

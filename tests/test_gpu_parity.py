@@ -96,15 +96,55 @@ def _tf_compare(w, T, S=1, cond_dim=0, seed_t=4):
     return m, {k: host(v) for k, v in r.items()}, ref
 
 
+def _targets(S, T, seed=4):
+    """Sine and uniform-byte targets, alternating over the streams."""
+    kinds = ["sines", "uniform"]
+    return np.concatenate([synth.target_signal(1, T, seed=seed + s, kind=kinds[s % 2]) for s in range(S)])
+
+
 @pytest.mark.parametrize("H", [128, 256, 384])
 def test_persistent_teacher_forced_small_sizes(H):
     w = synth.make_weights(H, seed=1, cond_dim=16)
-    m, r, ref = _tf_compare(w, 300, S=2, cond_dim=16)
+    m, r, ref = _tf_compare(w, 300, S=1, cond_dim=16)
     assert m.path()[0] == "persistent"
     dc = np.abs(r["zc"] - ref["zc"]).max()
     df = np.abs(r["zf"] - ref["zf"]).max()
     assert dc <= 1e-3 and df <= 1e-3, (dc, df)
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
+
+
+@pytest.mark.parametrize("H,S", [(128, 2), (256, 9), (384, 16)])
+def test_batched_teacher_forced_small_sizes(H, S):
+    """Several utterances in one launch (8 per group; S=9 leaves 7 idle vectors
+    in the second group): logits of every stream against the oracle."""
+    w = synth.make_weights(H, seed=1, cond_dim=16)
+    T = 200
+    feat = synth.features(S, T, cond_dim=16, per_stream_seed=True)
+    tgt = _targets(S, T)
+    m = wavernn.Model(w, dtype="bf16", max_streams=S)
+    assert m.path(S)[0] == "batched"
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, T, feat=feat, target=tgt, logits=True, nll=True)
+    dc = np.abs(r["zc"] - ref["zc"]).max()
+    df = np.abs(r["zf"] - ref["zf"]).max()
+    assert dc <= 1e-3 and df <= 1e-3, (dc, df)
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
+
+
+def test_batched_dense896_teacher_forced_within_bf16_tolerance():
+    w = synth.preset("dense896")
+    S, T = 12, 240
+    feat = synth.features(S, T, per_stream_seed=True)
+    tgt = _targets(S, T)
+    m = wavernn.Model(w, dtype="bf16", max_streams=S)
+    assert m.path(S)[0] == "batched"
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, T, feat=feat, target=tgt, logits=True, nll=True)
+    d = max(np.abs(r["zc"] - ref["zc"]).max(), np.abs(r["zf"] - ref["zf"]).max())
+    assert d <= BF16_TOL, d
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
 
 
 def test_dense896_teacher_forced_within_bf16_tolerance():
@@ -146,6 +186,32 @@ def test_dense896_free_running_draws_are_valid():
     assert okc.all() and okf.all(), (np.flatnonzero(~okc)[:10], np.flatnonzero(~okf)[:10])
     # not a degenerate trajectory
     assert len(np.unique(out)) > 100
+
+
+def test_batched_free_running_draws_valid_and_chunked_equals_one_call():
+    """9 utterances in one launch: every draw is valid under the oracle's logits
+    on the GPU trajectory and the stream's own Philox uniforms, and two chained
+    calls give the same samples and state as one."""
+    w = synth.make_weights(256, seed=3, cond_dim=8)
+    S, T = 9, 500
+    feat = synth.features(S, T, cond_dim=8, per_stream_seed=True)
+    m = wavernn.Model(w, dtype="bf16", max_streams=S)
+    fin = m.new_state(S)
+    whole = host(m.sample(T, cond=cuda(feat), seed=7, n_streams=S, final=fin))
+    st = m.new_state(S)
+    a = host(m.sample(300, cond=cuda(feat), seed=7, n_streams=S, final=st))
+    b = host(m.sample(200, cond=cuda(feat), seed=7, n_streams=S, init=st, final=st))
+    m.device_status()
+    np.testing.assert_array_equal(np.concatenate([a, b], axis=1), whole)
+    np.testing.assert_array_equal(host(st["h"]), host(fin["h"]))
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, T, feat=feat, target=whole, logits=True)
+    for s_ in range(S):
+        u = np.array([O.uniforms(7, s_, t) for t in range(T)])
+        c, f = whole[s_] >> 8, whole[s_] & 255
+        okc = _check_draws_valid(ref["zc"][s_], u[:, 0], c, 1e-3)
+        okf = _check_draws_valid(ref["zf"][s_], u[:, 1], f, 1e-3)
+        assert okc.all() and okf.all(), (s_, np.flatnonzero(~okc)[:10], np.flatnonzero(~okf)[:10])
+    assert len({tuple(x[:50]) for x in whole}) == S     # streams differ
 
 
 def test_persistent_chunked_equals_one_call():
