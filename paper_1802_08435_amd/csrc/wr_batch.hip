@@ -80,11 +80,10 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   float* op = (float*)(imo + 2 * WR_FRAG);         // [2][L][64] first-layer partials
   float* zs = op + 2 * L * 64;                     // [L][256] logit sums over the heads
   float* zk = zs + L * 256;                        // [L][256] logits of the last draws
-  float* yv = zk + L * 256;                        // [L][448] y_c or y_f (fp32), published by wave 7
-  float* hcs = yv + L * 448;                       // [L][448] coarse half of h
-  float* hfs = hcs + L * 448;                      // [L][448] fine half of h
-  float* gv = hfs + L * 448;                       // [3L][448] polled pre-activations of the gate threads
-  int* misc = (int*)(gv + 3 * L * 448);            // [0] abort, [8+b] c_t, [16+b] c_prev, [24+b] f_prev
+  float* hcs = zk + L * 256;                       // [L][448] coarse half of h (= y_c, published by wave 7)
+  float* hfs = hcs + L * 448;                      // [L][448] fine half of h (= y_f)
+  float* gv = hfs + L * 448;                       // [4L][448] staged pre-activations and e-gate bias of the gate threads
+  int* misc = (int*)(gv + 4 * L * 448);            // [0] abort, [8+b] c_t, [16+b] c_prev, [24+b] f_prev
   float* fmisc = (float*)(misc + 32);              // [b] lse_c, [8+b] z_c[c] of vector b
   float2* uni = (float2*)(misc + 64);              // [2][L][64] (u_c, u_f) of a batch of 64 steps
   int* tgt = (int*)(uni + 2 * L * 64);             // [2][L][64] teacher-forcing targets
@@ -174,9 +173,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   };
   // Sums over the heads, in head order.  Lane jj of wave 0 first watches the
   // last word head jj publishes; then thread (class v, parity h) reads the
-  // partials of vectors h, h + 2, h + 4, h + 6 of every head in one batch of
-  // loads; a word that is not in yet sends the thread to a slow path that
-  // waits word by word, still in head order.
+  // partials of vectors h, h + 2, h + 4, h + 6 of every head (two batches of
+  // loads, all in flight within a batch; more at once would keep too many
+  // addresses live), again until every word carries the step's tag.
   auto gather_logits = [&](const u64* src, uint32_t tag) {
     if (wave == 0) {
       float y;
@@ -187,55 +186,54 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (misc[0]) return;
     const int v = tid & 255, h = tid >> 8;
     const u64* base = src + h * 256 + v;            // word (jj, h + 2m) at base + (jj L + 2m) 256
-    float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    bool stale = false;
-    constexpr int NH0 = (NH + 1) / 2;                // heads in the first batch of loads
-    // two batches of loads (all in flight within a batch; more at once would
-    // keep too many addresses live)
+    constexpr int NH0 = (NH + 1) / 2;                // heads in the first batch
+    WaitBudget wb{wr_clock(), 0};
+    for (;;) {
+      float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      bool stale = false;
 #pragma unroll 1
-    for (int half = 0; half < 2; ++half)
+      for (int half = 0; half < 2; ++half)
 #pragma unroll
-      for (int jj = half ? NH0 : 0; jj < (half ? NH : NH0); ++jj)
+        for (int jj = half ? NH0 : 0; jj < (half ? NH : NH0); ++jj)
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          const u64 w = xpeek(base + (size_t)(jj * L + 2 * m) * 256);
-          stale |= xtag(w) != tag;
-          s[m] += xval(w);
-        }
-    if (stale) {
-      for (int m = 0; m < 4; ++m) s[m] = 0.0f;
-      for (int jj = 0; jj < NH; ++jj)
-        for (int m = 0; m < 4; ++m) {
-          float x;
-          if (!wait_word(base + (size_t)(jj * L + 2 * m) * 256, tag, &x, a)) {
-            misc[0] = 1;
-            return;
+          for (int m = 0; m < 4; ++m) {
+            const u64 w = xpeek(base + (size_t)(jj * L + 2 * m) * 256);
+            stale |= xtag(w) != tag;
+            s[m] += xval(w);
           }
-          s[m] += x;
-        }
-    }
+      if (!stale) {
 #pragma unroll
-    for (int m = 0; m < 4; ++m) zs[(h + 2 * m) * 256 + v] = s[m];
-  };
-  // The 3L pre-activation words of gate thread u, read in one batch into the
-  // LDS staging area gv (word k at gv[k * 448 + u]); stragglers are waited for.
-  auto read_gates = [&](const u64* G, uint32_t tag) {
-    uint32_t stale = 0;
-#pragma unroll 1
-    for (int half = 0; half < 2; ++half) {           // two batches of 12 loads
-      u64 w[3 * L / 2];
-#pragma unroll
-      for (int k = 0; k < 3 * L / 2; ++k) w[k] = xpeek(G + (size_t)(half * 3 * L / 2 + k) * Hh + u);
-#pragma unroll
-      for (int k = 0; k < 3 * L / 2; ++k) {
-        if (xtag(w[k]) != tag) stale |= 1u << (half * 3 * L / 2 + k);
-        gv[(half * 3 * L / 2 + k) * 448 + u] = xval(w[k]);
+        for (int m = 0; m < 4; ++m) zs[(h + 2 * m) * 256 + v] = s[m];
+        return;
+      }
+      if (!wait_ok(wb, a.err, a.limit, a.err)) {
+        misc[0] = 1;
+        return;
       }
     }
-    while (stale) {
-      const int k = __builtin_ctz(stale);
-      stale &= stale - 1;
-      if (!wait_word(G + (size_t)k * Hh + u, tag, gv + k * 448 + u, a)) {
+  };
+  // The 3L pre-activation words of gate thread u (two batches of loads) and
+  // the L bias + conditioning values of the e gate, staged in LDS: word k at
+  // gv[k * 448 + u], value of vector b at gv[(3L + b) * 448 + u].
+  auto read_gates = [&](const u64* G, uint32_t tag, int col, int64_t n) {
+#pragma unroll
+    for (int b = 0; b < L; ++b) gv[(3 * L + b) * 448 + u] = bcb_row(a, min(v0 + b, a.S - 1), n)[col];
+    WaitBudget wb{wr_clock(), 0};
+    for (;;) {
+      bool stale = false;
+#pragma unroll 1
+      for (int half = 0; half < 2; ++half) {
+        u64 w[3 * L / 2];
+#pragma unroll
+        for (int k = 0; k < 3 * L / 2; ++k) w[k] = xpeek(G + (size_t)(half * 3 * L / 2 + k) * Hh + u);
+#pragma unroll
+        for (int k = 0; k < 3 * L / 2; ++k) {
+          stale |= xtag(w[k]) != tag;
+          gv[(half * 3 * L / 2 + k) * 448 + u] = xval(w[k]);
+        }
+      }
+      if (!stale) return;
+      if (!wait_ok(wb, a.err, a.limit, a.err)) {
         misc[0] = 1;
         return;
       }
@@ -266,10 +264,10 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     // (1) coarse gates of every unit and vector: the 24 pre-activation words of
     // thread u are polled together and staged in LDS, then one vector at a time
     if (gate) {
-      read_gates(GA, tag);
+      read_gates(GA, tag, 2 * H + u, n);
 #pragma unroll 1
       for (int b = 0; b < L; ++b) {
-        const float cbe = bcb_row(a, min(v0 + b, a.S - 1), n)[2 * H + u];
+        const float cbe = gv[(3 * L + b) * 448 + u];
         const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]);
         const float uu = fsig(gv[(3 * b) * 448 + u] + __builtin_fmaf(ic[0][1], x1, ic[0][0] * x0));
         const float rg = fsig(gv[(3 * b + 1) * 448 + u] + __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0));
@@ -278,7 +276,6 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float hn = __builtin_fmaf(uu, hcs[b * 448 + u], (1.0f - uu) * e);
         hcs[b * 448 + u] = hn;
         aput(imc + (u >> 5) * WR_FRAG, u & 31, hn, b);
-        yv[b * 448 + u] = hn;
       }
     }
     __syncthreads();
@@ -286,7 +283,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (trw) trace_at(a, t, 1);
     if (wave == 7)
 #pragma unroll
-      for (int b = 0; b < L; ++b) xpub(YC + b * Hh + 64 * j + lane, tag, yv[b * 448 + 64 * j + lane]);
+      for (int b = 0; b < L; ++b) xpub(YC + b * Hh + 64 * j + lane, tag, hcs[b * 448 + 64 * j + lane]);
     // (2) O1 rows, relu, O2 columns -> partial coarse logits of 8 vectors
     first_layer(W1, imc, b1r);
     second_layer(W2, PCo, tag);
@@ -316,10 +313,10 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
     if (gate) {
-      read_gates(GF, tag);
+      read_gates(GF, tag, 2 * H + Hh + u, n);
 #pragma unroll 1
       for (int b = 0; b < L; ++b) {
-        const float cbe = bcb_row(a, min(v0 + b, a.S - 1), n)[2 * H + Hh + u];
+        const float cbe = gv[(3 * L + b) * 448 + u];
         const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]), x2 = fscale(misc[8 + b]);
         const float uu = fsig(gv[(3 * b) * 448 + u] +
                               __builtin_fmaf(ifn[0][2], x2, __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0)));
@@ -331,7 +328,6 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float hn = __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e);
         hfs[b * 448 + u] = hn;
         aput(imf + (u >> 5) * WR_FRAG, u & 31, hn, b);
-        yv[b * 448 + u] = hn;
       }
     }
     __syncthreads();
@@ -339,7 +335,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (trw) trace_at(a, t, 6);
     if (wave == 7)
 #pragma unroll
-      for (int b = 0; b < L; ++b) xpub(YF + b * Hh + 64 * j + lane, tag, yv[b * 448 + 64 * j + lane]);
+      for (int b = 0; b < L; ++b) xpub(YF + b * Hh + 64 * j + lane, tag, hfs[b * 448 + 64 * j + lane]);
     // (5) O3 rows, relu, O4 columns -> partial fine logits
     first_layer(W3, imf, b3r);
     second_layer(W4, PFo, tag);
@@ -509,12 +505,18 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   for (int64_t t = 0; t + 1 < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     const float cb0 = cbv(bl0, a.t0 + t + 1), cb1 = cbv(bl0 + 1, a.t0 + t + 1);
+    const bool tr = g == 0 && k == 0 && tid == 0;
+    if (tr) trace_at(a, t, 16);
     gather_half(YC, tag, 0);
     if (misc[0]) return;
+    if (tr) trace_at(a, t, 17);
     phase_c();
+    if (tr) trace_at(a, t, 18);
     gather_half(YF, tag, KT);
     if (misc[0]) return;
+    if (tr) trace_at(a, t, 19);
     phase_f(tag + 1, cb0, cb1);
+    if (tr) trace_at(a, t, 20);
   }
 }
 

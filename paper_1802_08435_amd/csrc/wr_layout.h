@@ -202,8 +202,8 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P) {
   P->x_pf = take(P->NH * WR_BL * 256);
   P->x_words = o;
   // head: operand images (2 KT + 2 fragments), first-layer partials [2][L][64],
-  // logit sums [L][256], logits [L][256], y, both halves of h and the polled
-  // pre-activations [6][L][448], misc [64],
+  // logit sums [L][256], logits [L][256], both halves of h and the staged
+  // gate inputs [6][L][448], misc [64],
   // uniforms [2][L][64][2], targets [2][L][64]
   P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * WR_BL * 64 + 2 * WR_BL * 256 + 6 * WR_BL * 448 + 64 +
                                                2 * WR_BL * 64 * 2 + 2 * WR_BL * 64);
