@@ -71,17 +71,19 @@ struct BatchArgs {
   const float* b2;          // [256]
   const float* b3;
   const float* b4;
-  const float* cb;          // [S][n_cb][3H] gate bias + conditioning per vector and frame
+  const uint4* ux;          // [NU][8 waves][KX][64] context-projection fragments (subscale) or null
+  const float* cb;          // [U][n_cb][3H] gate bias + conditioning per utterance and frame
   int64_t n_cb;
   int frame_len;
   int S;                    // vectors in use (the last group may be partly idle)
-  int64_t T, t0;
+  int B;                    // subscale factor: vector v is lane v % B of utterance v / B (1: plain)
+  int64_t T, t0;            // steps (rows when B > 1) and first absolute step
   uint64_t seed;
-  const uint16_t* target;   // [S][T] or null
-  uint16_t* out;            // [S][T] or null
-  float* zc_out;            // [S][T][256] or null
+  const uint16_t* target;   // [U][B T] samples in time order, or null
+  uint16_t* out;            // [U][B T] or null
+  float* zc_out;            // [U][B T][256] or null
   float* zf_out;
-  float* nll_out;           // [S][T] or null
+  float* nll_out;           // [U][B T] or null
   const float* h_in;        // [S][H] or null
   const uint8_t* c_in;      // [S]
   const uint8_t* f_in;
@@ -100,5 +102,5 @@ const void* wr_small_kernel_ptr();
 const void* wr_uniforms_kernel_ptr();
 const void* wr_persist_kernel_ptr(int KH);   // null if no instantiation for KH
 const void* wr_cond_kernel_ptr();
-const void* wr_batch_kernel_ptr(int KH);     // null if no instantiation for KH
+const void* wr_batch_kernel_ptr(int KH, bool ctx);   // null if no instantiation for KH
 const void* wr_fill_kernel_ptr();

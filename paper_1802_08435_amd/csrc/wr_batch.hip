@@ -14,11 +14,17 @@ namespace {
 
 constexpr int L = WR_BL;
 
-// Bias + conditioning row of vector b at absolute sample n.
-__device__ __forceinline__ const float* bcb_row(const BatchArgs& a, int b, int64_t n) {
-  int64_t fr = n / a.frame_len;
+// Vector v is lane v % B of utterance v / B; at step t it makes sample
+// n = B (t0 + t) + v % B of that utterance (Sec. 4; B = 1: n = t0 + t).
+// Index of that sample in the [U][B T] output / target arrays: obase(v) + B t.
+__device__ __forceinline__ size_t obase(const BatchArgs& a, int v) {
+  return (size_t)(v / a.B) * a.B * a.T + v % a.B;
+}
+// Offset (floats) of the bias + conditioning row vector v uses at step t.
+__device__ __forceinline__ int64_t cb_offset(const BatchArgs& a, int v, int64_t t) {
+  int64_t fr = ((int64_t)a.B * (a.t0 + t) + v % a.B) / a.frame_len;
   if (fr >= a.n_cb) fr = a.n_cb - 1;
-  return a.cb + ((size_t)b * a.n_cb + fr) * 3 * a.P.H;
+  return ((int64_t)(v / a.B) * a.n_cb + fr) * 3 * a.P.H;
 }
 
 // Wait until the N words base[k*stride] (k < N) carry `tag`; values to v[].
@@ -67,7 +73,7 @@ __device__ __forceinline__ bool wait_word(const u64* p, uint32_t tag, float* v, 
 }
 
 // ------------------------------------------------------------------ head role
-template <int KH>
+template <int KH, bool CTX>
 __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   constexpr int NH = KH;
@@ -83,7 +89,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   float* hcs = zk + L * 256;                       // [L][448] coarse half of h (= y_c, published by wave 7)
   float* hfs = hcs + L * 448;                      // [L][448] fine half of h (= y_f)
   float* gv = hfs + L * 448;                       // [4L][448] staged pre-activations and e-gate bias of the gate threads
-  int* misc = (int*)(gv + 4 * L * 448);            // [0] abort, [8+b] c_t, [16+b] c_prev, [24+b] f_prev
+  int64_t* cbo = (int64_t*)(gv + 4 * L * 448);    // [L] bias + conditioning row offsets of this step
+  int* misc = (int*)(cbo + L);                     // [0] abort, [8+b] c_t, [16+b] c_prev, [24+b] f_prev
   float* fmisc = (float*)(misc + 32);              // [b] lse_c, [8+b] z_c[c] of vector b
   float2* uni = (float2*)(misc + 64);              // [2][L][64] (u_c, u_f) of a batch of 64 steps
   int* tgt = (int*)(uni + 2 * L * 64);             // [2][L][64] teacher-forcing targets
@@ -128,6 +135,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const float4 b4l = *(const float4*)(a.b4 + 4 * lane);
   if (tid < L) {
     const int vb = min(v0 + tid, a.S - 1);
+    cbo[tid] = cb_offset(a, vb, 0);
     misc[0] = 0;
     misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
     misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
@@ -213,14 +221,23 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     }
   };
   // The 3L pre-activation words of gate thread u (two batches of loads) and
-  // the L bias + conditioning values of the e gate, staged in LDS: word k at
-  // gv[k * 448 + u], value of vector b at gv[(3L + b) * 448 + u].
-  auto read_gates = [&](const u64* G, uint32_t tag, int col, int64_t n) {
-#pragma unroll
-    for (int b = 0; b < L; ++b) gv[(3 * L + b) * 448 + u] = bcb_row(a, min(v0 + b, a.S - 1), n)[col];
+  // the L additive terms of the e gate (bias + conditioning, and with subscale
+  // the context term, which stays outside the reset product), staged in LDS:
+  // word k at gv[k * 448 + u], term of vector b at gv[(3L + b) * 448 + u].
+  auto read_gates = [&](const u64* G, const u64* XE, uint32_t tag, int col) {
     WaitBudget wb{wr_clock(), 0};
     for (;;) {
       bool stale = false;
+#pragma unroll
+      for (int b = 0; b < L; ++b) {
+        float xe = 0.0f;
+        if (CTX) {
+          const u64 w = xpeek(XE + b * Hh + u);
+          stale |= xtag(w) != tag;
+          xe = xval(w);
+        }
+        gv[(3 * L + b) * 448 + u] = a.cb[cbo[b] + col] + xe;
+      }
 #pragma unroll 1
       for (int half = 0; half < 2; ++half) {
         u64 w[3 * L / 2];
@@ -239,14 +256,16 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       }
     }
   };
+  const int vw = min(v0 + wave, a.S - 1);          // the draw wave's vector
+  const size_t ob = obase(a, vw);
   auto fill_batch = [&](int64_t t, int buf) {       // wave w: vector w's uniforms / targets
     const int64_t s = t + lane;
-    const int vb = min(v0 + wave, a.S - 1);
+    const int vb = vw;
     if (s < a.T) {
       float uc, uf;
       wr_uniforms(a.seed, (uint64_t)vb, (uint64_t)(a.t0 + s), &uc, &uf);
       uni[(buf * L + wave) * 64 + lane] = float2{uc, uf};
-      tgt[(buf * L + wave) * 64 + lane] = a.target ? a.target[(size_t)vb * a.T + s] : 0;
+      tgt[(buf * L + wave) * 64 + lane] = a.target ? a.target[ob + (size_t)a.B * s] : 0;
     }
   };
   fill_batch(0, 0);
@@ -256,7 +275,6 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const bool live = v0 + wave < a.S;               // draw wave's vector is in use
 
   for (int64_t t = 0; t < a.T; ++t) {
-    const int64_t n = a.t0 + t;
     const uint32_t tag = (uint32_t)(t + 1);
     if (trw) trace_at(a, t, 0);
     const int bs = (int)((t >> 6) & 1) * L * 64 + wave * 64 + (int)(t & 63);   // draw wave's batch slot
@@ -264,7 +282,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     // (1) coarse gates of every unit and vector: the 24 pre-activation words of
     // thread u are polled together and staged in LDS, then one vector at a time
     if (gate) {
-      read_gates(GA, tag, 2 * H + u, n);
+      read_gates(GA, X + P.x_xc, tag, 2 * H + u);
 #pragma unroll 1
       for (int b = 0; b < L; ++b) {
         const float cbe = gv[(3 * L + b) * 448 + u];
@@ -299,7 +317,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       const int c = draw_wave<false>(zs + wave * 256, nullptr, b2l, uni[bs].x, forced, zk + wave * 256,
                                      a.nll_out ? &lse : nullptr);
       if (j == 0 && live && a.zc_out)
-        *(float4*)(a.zc_out + ((size_t)(v0 + wave) * a.T + t) * WR_CLASSES + 4 * lane) =
+        *(float4*)(a.zc_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
         misc[8 + wave] = c;
@@ -313,7 +331,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
     if (gate) {
-      read_gates(GF, tag, 2 * H + Hh + u, n);
+      read_gates(GF, X + P.x_xf, tag, 2 * H + Hh + u);
 #pragma unroll 1
       for (int b = 0; b < L; ++b) {
         const float cbe = gv[(3 * L + b) * 448 + u];
@@ -352,16 +370,18 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
                                      a.nll_out ? &lse : nullptr);
       const int c = misc[8 + wave];
       if (j == 0 && live && a.zf_out)
-        *(float4*)(a.zf_out + ((size_t)(v0 + wave) * a.T + t) * WR_CLASSES + 4 * lane) =
+        *(float4*)(a.zf_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
         if (j == 0 && live) {
-          if (a.out) a.out[(size_t)(v0 + wave) * a.T + t] = (uint16_t)(256 * c + f);
+          if (a.out) a.out[ob + (size_t)a.B * t] = (uint16_t)(256 * c + f);
           if (a.nll_out)
-            a.nll_out[(size_t)(v0 + wave) * a.T + t] = (fmisc[wave] - fmisc[8 + wave]) + (lse - zk[wave * 256 + f]);
+            a.nll_out[ob + (size_t)a.B * t] = (fmisc[wave] - fmisc[8 + wave]) + (lse - zk[wave * 256 + f]);
+          if (a.ux) xpub(X + P.x_sp + wave, tag, (float)(256 * c + f));   // for the context of later rows
         }
         misc[16 + wave] = c;
         misc[24 + wave] = f;
+        if (t + 1 < a.T) cbo[wave] = cb_offset(a, vw, t + 1);
       }
     }
     __syncthreads();
@@ -385,7 +405,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
 // Wave q < 4 owns coarse row tile 4k + q, wave 4 + q fine row tile 4k + q;
 // each lane of a wave's result holds two vectors of one row, which it
 // publishes (with bias + conditioning for the u and r gates).
-template <int KH>
+template <int KH, bool CTX>
 __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   const BatchPlan& P = a.P;
@@ -395,7 +415,9 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   const int q = wave & 3;
   const unsigned char* WL = lds + (fw ? WR_BUCT * KT + q * KT : q * KT) * WR_FRAG;   // this wave's LDS half
   unsigned char* img = lds + P.u_lds_w;                                             // [2KT] operand image
-  int* misc = (int*)(img + 2 * KT * WR_FRAG);
+  unsigned char* cimg = img + 2 * KT * WR_FRAG;                                     // [KX] context image
+  int* hist = (int*)(cimg + P.KX * WR_FRAG);          // [utterance slot][256]: samples q at q % 256
+  int* misc = hist + WR_HIST * 64;
   const int tile = k * WR_BUCT + q;
   const int gt = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + (lane & 15);
   const int row = gt * H + (fw ? Hh : 0) + i;                  // R row of this lane
@@ -406,8 +428,15 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   {
     const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
     for (int x = tid; x < P.u_lds_w / 16; x += WR_THREADS) ((uint4*)lds)[x] = src[x];
-    for (int x = tid; x < 2 * KT * WR_FRAG / 16; x += WR_THREADS) ((uint4*)img)[x] = uint4{0, 0, 0, 0};
+    for (int x = tid; x < (2 * KT + P.KX) * WR_FRAG / 16; x += WR_THREADS) ((uint4*)img)[x] = uint4{0, 0, 0, 0};
     if (tid == 0) misc[0] = 0;
+  }
+  bf16x8 WX[CTX ? 8 : 1];                              // context-projection fragments of this wave's tile
+  if (CTX) {
+    const uint4* src = a.ux + ((size_t)(k * 8 + wave) * P.KX) * 64 + lane;
+#pragma unroll
+    for (int x = 0; x < (CTX ? 8 : 0); ++x)
+      if (x < P.KX) WX[x] = __builtin_bit_cast(bf16x8, src[(size_t)x * 64]);
   }
   bf16x8 WR[KT];
   {
@@ -438,8 +467,8 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       }
     }
   };
-  // fine inputs (image tiles KT .. 2KT-1), then publish with `tag`
-  auto phase_f = [&](uint32_t tag, float cb0, float cb1) {
+  // fine inputs (image tiles KT .. 2KT-1)
+  auto phase_f = [&]() {
 #pragma unroll
     for (int x = 0; x < KT; x += 2) {
       const bf16x8 w0 = fw ? *(const bf16x8*)(WL + x * WR_FRAG + lane * 16) : WR[x];
@@ -449,11 +478,69 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
         acc1 = mfma(afrag(img, KT + x + 1), w1, acc1);
       }
     }
+  };
+  f32x4 xa0 = {0, 0, 0, 0}, xa1 = {0, 0, 0, 0};        // context term of e-gate rows
+  u64* dstx = X + (fw ? P.x_xf : P.x_xc) + i;          // + vector * Hh
+  auto publish = [&](uint32_t tag, float cb0, float cb1) {
     xpub(dst + (size_t)bl0 * 3 * Hh, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0);
     xpub(dst + (size_t)(bl0 + 1) * 3 * Hh, tag, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
+    if (CTX && gt == 2) {
+      xpub(dstx + (size_t)bl0 * Hh, tag, mfma_row(xa0) + mfma_row(xa1));
+      xpub(dstx + (size_t)(bl0 + 1) * Hh, tag, mfma_row_hi(xa0) + mfma_row_hi(xa1));
+    }
   };
-  auto cbv = [&](int b, int64_t n) {                           // u and r gates carry bias + conditioning
-    return gt < 2 ? bcb_row(a, min(v0 + b, a.S - 1), n)[row] : 0.0f;
+  // Subscale context (Sec. 4): the samples of row t of every utterance of this
+  // group join the history; vector b's context for row t + 1 is the Dx/2
+  // samples before its own, as (c, f) scaled, zero for samples of row t + 1 or
+  // before the start.  Its projection joins the sums of the u and r rows; for
+  // e rows it is kept apart (published on its own: it is not reset-gated).
+  const int ub0 = v0 / a.B;                            // first utterance of this group
+  const int nut = a.B >= L ? 1 : L / a.B;              // utterances of this group
+  auto context = [&](int64_t t) {
+    const uint32_t tag = (uint32_t)(t + 1);
+    if (tid < nut * a.B) {                             // one thread per (utterance, lane)
+      const int vv = ub0 * a.B + tid;                  // vector of that lane
+      float y;
+      if (vv < a.S) {
+        if (!wait_word(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp + vv % L, tag, &y, a)) misc[0] = 1;
+        const int64_t qn = (int64_t)a.B * t + tid % a.B;
+        hist[(tid / a.B) * 256 + (int)(qn & 255)] = (int)y;
+      }
+    }
+    __syncthreads();
+    if (misc[0]) return;
+    const int half = a.P.KX * 16;                      // context samples per vector
+    for (int x = tid; x < L * half; x += WR_THREADS) {
+      const int b = x / half, jj = x % half;
+      const int vb = min(v0 + b, a.S - 1);
+      const int64_t n1 = (int64_t)a.B * (t + 1) + vb % a.B;   // sample this vector makes next
+      const int64_t qn = n1 - 1 - jj;
+      float c = 0.0f, f = 0.0f;
+      if (qn >= 0 && qn < (int64_t)a.B * (t + 1)) {
+        const int sv = hist[(vb / a.B - ub0) * 256 + (int)(qn & 255)];
+        c = fscale(sv >> 8);
+        f = fscale(sv & 255);
+      }
+      aput(cimg + ((2 * jj) >> 5) * WR_FRAG, (2 * jj) & 31, c, b);
+      aput(cimg + ((2 * jj + 1) >> 5) * WR_FRAG, (2 * jj + 1) & 31, f, b);
+    }
+    __syncthreads();
+    f32x4 c0 = gt == 2 ? f32x4{0, 0, 0, 0} : acc0, c1 = gt == 2 ? f32x4{0, 0, 0, 0} : acc1;
+#pragma unroll
+    for (int x = 0; x < (CTX ? 8 : 0); x += 2) {
+      if (x < P.KX) c0 = mfma(afrag(cimg, x), WX[x], c0);
+      if (x + 1 < P.KX) c1 = mfma(afrag(cimg, x + 1), WX[x + 1], c1);
+    }
+    if (gt == 2) {
+      xa0 = c0;
+      xa1 = c1;
+    } else {
+      acc0 = c0;
+      acc1 = c1;
+    }
+  };
+  auto cbv = [&](int b, int64_t t) {                           // u and r gates carry bias + conditioning
+    return gt < 2 ? a.cb[cb_offset(a, min(v0 + b, a.S - 1), t) + row] : 0.0f;
   };
   // Wait for one half of h of all 8 vectors: lane jj of wave 0 first watches
   // the last word head jj publishes (vector 7), then every thread reads its
@@ -499,12 +586,13 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     __syncthreads();
   };
   phase_c();
-  phase_f(1u, cbv(bl0, a.t0), cbv(bl0 + 1, a.t0));
+  phase_f();
+  publish(1u, cbv(bl0, 0), cbv(bl0 + 1, 0));
   const u64* YC = X + P.x_yc;
   const u64* YF = X + P.x_yf;
   for (int64_t t = 0; t + 1 < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
-    const float cb0 = cbv(bl0, a.t0 + t + 1), cb1 = cbv(bl0 + 1, a.t0 + t + 1);
+    const float cb0 = cbv(bl0, t + 1), cb1 = cbv(bl0 + 1, t + 1);
     const bool tr = g == 0 && k == 0 && tid == 0;
     if (tr) trace_at(a, t, 16);
     gather_half(YC, tag, 0);
@@ -515,29 +603,34 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     gather_half(YF, tag, KT);
     if (misc[0]) return;
     if (tr) trace_at(a, t, 19);
-    phase_f(tag + 1, cb0, cb1);
+    phase_f();
+    if (CTX) {
+      context(t);
+      if (misc[0]) return;
+    }
+    publish(tag + 1, cb0, cb1);
     if (tr) trace_at(a, t, 20);
   }
 }
 
 }  // namespace
 
-template <int KH>
+template <int KH, bool CTX>
 __global__ __launch_bounds__(WR_THREADS, 1) void wr_batch_kernel(BatchArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   int g = 0;
   const int r = wr_batch_role(a.P, blockIdx.x, &g);
   if (r < 0) return;
-  if (r < a.P.NH) bhead_role<KH>(a, g, r, lds);
-  else bunit_role<KH>(a, g, r - a.P.NH, lds);
+  if (r < a.P.NH) bhead_role<KH, CTX>(a, g, r, lds);
+  else bunit_role<KH, CTX>(a, g, r - a.P.NH, lds);
 }
 
-const void* wr_batch_kernel_ptr(int KH) {
+const void* wr_batch_kernel_ptr(int KH, bool ctx) {
   switch (KH) {
-    case 1: return (const void*)wr_batch_kernel<1>;
-    case 2: return (const void*)wr_batch_kernel<2>;
-    case 3: return (const void*)wr_batch_kernel<3>;
-    case 7: return (const void*)wr_batch_kernel<7>;
+    case 1: return ctx ? (const void*)wr_batch_kernel<1, true> : (const void*)wr_batch_kernel<1, false>;
+    case 2: return ctx ? (const void*)wr_batch_kernel<2, true> : (const void*)wr_batch_kernel<2, false>;
+    case 3: return ctx ? (const void*)wr_batch_kernel<3, true> : (const void*)wr_batch_kernel<3, false>;
+    case 7: return ctx ? (const void*)wr_batch_kernel<7, true> : (const void*)wr_batch_kernel<7, false>;
     default: return nullptr;
   }
 }

@@ -78,7 +78,7 @@ struct wavernn_model {
   bool has_batch = false;
   BatchPlan bplan;
   const void* bk = nullptr;          // kernel instantiation for bplan.KH
-  uint4 *d_buw = nullptr, *d_bur = nullptr;
+  uint4 *d_buw = nullptr, *d_bur = nullptr, *d_bux = nullptr;
   u64* d_bxc = nullptr;
   float* d_bcb = nullptr;            // [streams][frames][3H]
   size_t bcb_cap = 0;                // floats
@@ -299,7 +299,7 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
 wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   const BatchPlan& B = m->bplan;
   const int H = B.H, Hh = B.Hh, KT = B.KT;
-  m->bk = wr_batch_kernel_ptr(B.KH);
+  m->bk = wr_batch_kernel_ptr(B.KH, B.KX > 0);
   if (!m->bk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no batched kernel instantiation", H);
   REff R{&m->cfg, w};
   auto frag = [&](uint16_t* dst, int tile, bool fine, int col0) {
@@ -323,6 +323,24 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
     }
   }
   wavernn_status s;
+  if (B.KX > 0) {   // context projection W_ctx: [unit][wave][column tile] fragments of the wave's row tile
+    const int Dx = m->cfg.ctx_dim;
+    std::vector<uint16_t> ux((size_t)B.NU * 8 * B.KX * 512);
+    for (int k = 0; k < B.NU; ++k)
+      for (int wv = 0; wv < 8; ++wv) {
+        const int tile = k * WR_BUCT + (wv & 3);
+        const bool fine = wv >= 4;
+        for (int kt = 0; kt < B.KX; ++kt) {
+          uint16_t* d = ux.data() + ((size_t)(k * 8 + wv) * B.KX + kt) * 512;
+          for (int l = 0; l < 64; ++l) {
+            const int g = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + l % 16;
+            const int row = g * H + (fine ? Hh : 0) + i;
+            for (int e = 0; e < 8; ++e) d[l * 8 + e] = f2bf(w->W_ctx[(size_t)row * Dx + 32 * kt + 8 * (l / 16) + e]);
+          }
+        }
+      }
+    if ((s = m->upload(&m->d_bux, ux.data(), ux.size() * 2)) != WAVERNN_OK) return s;
+  }
   if ((s = m->upload(&m->d_buw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
   if ((s = m->upload(&m->d_bur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
   if ((s = m->alloc(&m->d_bxc, (size_t)B.G * B.x_words * 8)) != WAVERNN_OK) return s;
@@ -488,8 +506,11 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
 }
 
 wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
+  const int SB = m->cfg.subscale;                 // lanes per utterance
+  const int V = io.S * SB;                        // vectors
   BatchPlan B;
-  if (!batch_plan(m->cfg.hidden, io.S, &B)) return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d streams", io.S);
+  if (!batch_plan(m->cfg.hidden, V, &B, m->cfg.ctx_dim))
+    return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors", V);
   const int H = B.H, Dc = m->cfg.cond_dim;
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
   const int64_t n_cb = Dc > 0 ? io.n_frames : 1;
@@ -516,11 +537,13 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.b2 = m->d_b2;
   a.b3 = m->d_b3;
   a.b4 = m->d_b4;
+  a.ux = m->d_bux;
   a.cb = m->d_bcb;
   a.n_cb = n_cb;
   a.frame_len = Dc > 0 ? frame_len : (1 << 30);
-  a.S = io.S;
-  a.T = io.T;
+  a.S = V;
+  a.B = SB;
+  a.T = io.T / SB;
   a.t0 = io.init ? io.init->t0 : 0;
   a.seed = io.seed;
   a.target = io.target;
@@ -550,6 +573,7 @@ wavernn_status run(wavernn_model* m, RunIO& io) {
   if (dev != m->device) return fail(WAVERNN_E_INVALID, "model lives on device %d, current device is %d", m->device, dev);
   if (m->path == PATH_SMALL) return run_small(m, io);
   if (m->path == PATH_PERSIST) return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);
+  if (m->path == PATH_BATCHED) return run_batch(m, io);
   return fail(WAVERNN_E_UNSUPPORTED, "no kernel for this configuration");
 }
 
@@ -572,8 +596,22 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
   const int H = cfg->hidden;
   const SmallLayout L = small_layout(H);
   const bool small_fits = (size_t)L.total_floats * 4 + 256 <= 160 * 1024;
-  if (cfg->subscale > 1) {
-    s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling is not available in this build");
+  const int B = cfg->subscale;
+  if (B > 1) {
+    // Subscale (Sec. 4): the B lanes of each utterance are vectors of the
+    // batched kernel; its unit workgroups add the context projection.
+    if (!((B % WR_BL == 0) || (WR_BL % B == 0)) || cfg->ctx_dim % 32 || cfg->ctx_dim > 256)
+      s = fail(WAVERNN_E_UNSUPPORTED, "subscale %d / ctx_dim %d: need B dividing or divided by 8, ctx_dim a multiple "
+               "of 32 up to 256", B, cfg->ctx_dim);
+    else if (cfg->weight_dtype != WAVERNN_BF16)
+      s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling needs bf16 weights");
+    else if (!persist_plan(H, &m->plan) || !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim))
+      s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d with %d x %d lanes: no batched plan", H, cfg->max_streams, B);
+    else {
+      m->path = PATH_BATCHED;
+      s = build_persist(m, w);
+      if (s == WAVERNN_OK) s = build_batch(m, w);
+    }
   } else if (small_fits) {
     m->path = PATH_SMALL;
     s = build_small(m, w);
@@ -649,6 +687,9 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
   BatchPlan B;
   if (m->path == PATH_SMALL) {
     g = n_streams > 0 ? n_streams : 1, b = 256;
+  } else if (m->path == PATH_BATCHED &&
+             batch_plan(m->cfg.hidden, (n_streams > 0 ? n_streams : 1) * m->cfg.subscale, &B, m->cfg.ctx_dim)) {
+    g = B.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST && n_streams > 1 && m->has_batch && batch_plan(m->cfg.hidden, n_streams, &B)) {
     path = PATH_BATCHED, g = B.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST) {

@@ -154,12 +154,15 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
 // ---------------------------------------------------------------------------
 #define WR_BL 8           // vectors per group
 #define WR_BUCT 4         // coarse (and fine) row tiles per batched unit
+#define WR_HIST 16        // rows of drawn samples a batched unit keeps (subscale context)
 
 struct BatchPlan {
   int H, Hh, KT, KH, NH, NCT, NU, G, grid;
   int hw_frags;           // head fragments per wave (as the batch-1 plan)
   int u_lds_w;            // unit LDS weights: [UCT][KT] coarse tiles, then [UCT][KT] fine tiles
-  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // per group: y [L][Hh], g [L][3][Hh], p [NH][L][256]
+  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_sp, x_xc, x_xf, x_words;   // per group: y [L][Hh],
+      // g [L][3][Hh], p [NH][L][256], drawn samples [L], e-gate context terms [L][Hh] x 2
+  int KX;                 // subscale context column tiles (Dx / 32), 0 without context
   int lds_h, lds_u, lds;
 };
 
@@ -176,8 +179,10 @@ WR_HD inline int wr_batch_role(const BatchPlan& P, int b, int* g) {
   return P.NH + ku % P.NU;
 }
 
-WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P) {
+WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0) {
   if (H <= 0 || H % 128 || n_vectors < 1 || n_vectors > 8 * WR_BL) return false;
+  if (ctx_dim < 0 || ctx_dim % 32 || ctx_dim > 256) return false;
+  P->KX = ctx_dim / 32;
   P->H = H;
   P->Hh = H / 2;
   P->KT = P->Hh / 32;
@@ -200,15 +205,19 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P) {
   P->x_gf = take(WR_BL * 3 * P->Hh);
   P->x_pc = take(P->NH * WR_BL * 256);
   P->x_pf = take(P->NH * WR_BL * 256);
+  P->x_sp = take(WR_BL);
+  P->x_xc = take(WR_BL * P->Hh);
+  P->x_xf = take(WR_BL * P->Hh);
   P->x_words = o;
   // head: operand images (2 KT + 2 fragments), first-layer partials [2][L][64],
   // logit sums [L][256], logits [L][256], both halves of h and the staged
-  // gate inputs [6][L][448], misc [64],
+  // gate inputs [2 + 4][L][448], bias row offsets [L], misc [64],
   // uniforms [2][L][64][2], targets [2][L][64]
-  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * WR_BL * 64 + 2 * WR_BL * 256 + 6 * WR_BL * 448 + 64 +
+  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * WR_BL * 64 + 2 * WR_BL * 256 + 6 * WR_BL * 448 + 2 * WR_BL + 64 +
                                                2 * WR_BL * 64 * 2 + 2 * WR_BL * 64);
-  // unit: weights, operand image (2 KT fragments), misc [16]
-  P->lds_u = P->u_lds_w + 2 * P->KT * WR_FRAG + 4 * 16;
+  // unit: weights, operand image (2 KT fragments), context image (KX fragments),
+  // sample history [WR_HIST][64], misc [16]
+  P->lds_u = P->u_lds_w + (2 * P->KT + P->KX) * WR_FRAG + 4 * (WR_HIST * 64 + 16);
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024 && P->grid <= 256;
 }

@@ -214,6 +214,59 @@ def test_batched_free_running_draws_valid_and_chunked_equals_one_call():
     assert len({tuple(x[:50]) for x in whole}) == S     # streams differ
 
 
+# ------------------------------------------------------------- subscale
+
+@pytest.mark.parametrize("H,B,S", [(256, 8, 2), (128, 16, 1)])
+def test_subscale_teacher_forced_small_sizes(H, B, S):
+    """Subscale (Sec. 4): B lanes per utterance in lockstep, each conditioned on
+    the 128 samples before its own (same-row samples masked)."""
+    w = synth.make_weights(H, seed=6, cond_dim=16, B=B, ctx_dim=256)
+    T = 40 * B
+    feat = synth.features(S, T, cond_dim=16, per_stream_seed=True)
+    tgt = _targets(S, T)
+    m = wavernn.Model(w, dtype="bf16", max_streams=S)
+    assert m.path(S)[0] == "batched"
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, T, feat=feat, target=tgt, logits=True, nll=True)
+    dc = np.abs(r["zc"] - ref["zc"]).max()
+    df = np.abs(r["zf"] - ref["zf"]).max()
+    assert dc <= 1e-3 and df <= 1e-3, (dc, df)
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
+
+
+def test_subscale16_dense896_teacher_forced_within_bf16_tolerance():
+    w = synth.preset("subscale16")
+    T = 960
+    feat = synth.features(1, T)
+    tgt = _targets(1, T)
+    m = wavernn.Model(w, dtype="bf16")
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, T, feat=feat, target=tgt, logits=True, nll=True)
+    d = max(np.abs(r["zc"] - ref["zc"]).max(), np.abs(r["zf"] - ref["zf"]).max())
+    assert d <= BF16_TOL, d
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
+
+
+def test_subscale_free_running_draws_are_valid():
+    """Every lane's draw is valid under the oracle's logits on the GPU
+    trajectory, with the lane's Philox stream indexed by row."""
+    B, T = 8, 480
+    w = synth.make_weights(256, seed=7, cond_dim=16, B=B, ctx_dim=256)
+    feat = synth.features(1, T, cond_dim=16)
+    m = wavernn.Model(w, dtype="bf16")
+    out = host(m.sample(T, cond=cuda(feat), seed=3))
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, T, feat=feat, target=out, logits=True)
+    u = np.array([O.uniforms(3, n % B, n // B) for n in range(T)])
+    c, f = out[0] >> 8, out[0] & 255
+    okc = _check_draws_valid(ref["zc"][0], u[:, 0], c, 1e-3)
+    okf = _check_draws_valid(ref["zf"][0], u[:, 1], f, 1e-3)
+    assert okc.all() and okf.all(), (np.flatnonzero(~okc)[:10], np.flatnonzero(~okf)[:10])
+    assert len(np.unique(out)) > 50
+
+
 def test_persistent_chunked_equals_one_call():
     w = synth.make_weights(256, seed=2, cond_dim=8)
     feat = synth.features(1, 900, cond_dim=8)
