@@ -141,7 +141,8 @@ wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t
 /* Which kernel serves a call on n_streams streams: 0 single-workgroup fp32,
  * 1 multi-workgroup persistent (one launch per stream), 2 batched persistent
  * (up to 64 streams in one launch, 8 per group of workgroups; models created
- * with max_streams > 1 and a hidden size the persistent kernel serves).
+ * with max_streams > 1 and a hidden size the persistent kernel serves),
+ * 3 persistent with block-sparse R (Sec. 3.2; one launch per stream).
  * Fills *grid and *block with its launch shape; -1 for a null model. */
 int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* grid, int32_t* block);
 

@@ -66,7 +66,8 @@ struct wavernn_model {
   SmallLayout sl;
   // persistent path
   PersistPlan plan;
-  const void* pk = nullptr;          // kernel instantiation for plan.KH
+  const void* pk = nullptr;          // kernel instantiation for the plan
+  bool sparse = false;               // block-sparse units
   uint4 *d_hw = nullptr, *d_uw = nullptr, *d_ur = nullptr;
   float *d_I = nullptr, *d_bias = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr, *d_b4 = nullptr;
   float* d_cb = nullptr;             // [cb_cap][3H] bias + conditioning per frame
@@ -200,67 +201,72 @@ wavernn_status build_small(wavernn_model* m, const wavernn_weights* w) {
   return WAVERNN_OK;
 }
 
-wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
-  const wavernn_config& c = m->cfg;
-  const PersistPlan& P = m->plan;
-  const int H = P.H, Hh = P.Hh, KT = P.KT, KH = P.KH, UCT = P.UCT;
-  m->pk = wr_persist_kernel_ptr(KH);
-  if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no persistent kernel instantiation", H);
-  Rounder rd{true};
-  REff R{&m->cfg, w};
-  // One MFMA fragment (operand B of v_mfma_f32_16x16x32_bf16) of a matrix M(row, col):
-  // lane l holds row rowof(l % 16), columns col0 + 8*(l/16) .. +7, as bf16.
-  auto frag = [&](uint16_t* dst, auto&& M, auto&& rowof, int col0) {
-    for (int l = 0; l < 64; ++l) {
-      const int row = rowof(l % 16);
-      for (int e = 0; e < 8; ++e) dst[l * 8 + e] = f2bf(M(row, col0 + 8 * (l / 16) + e));
-    }
-  };
+// One MFMA fragment (operand B of v_mfma_f32_16x16x32_bf16) of a matrix M(row, col):
+// lane l holds row rowof(l % 16), columns col0 + 8*(l/16) .. +7, as bf16.
+template <class M, class RowOf>
+void frag(uint16_t* dst, M&& mat, RowOf&& rowof, int col0) {
+  for (int l = 0; l < 64; ++l) {
+    const int row = rowof(l % 16);
+    for (int e = 0; e < 8; ++e) dst[l * 8 + e] = f2bf(mat(row, col0 + 8 * (l / 16) + e));
+  }
+}
+
+// Head fragments: wave w of the head holding slice s holds O1 / O3 row tile
+// RT s + w % RT over column tiles (w / RT) KH .. +KH, and O2 / O4 class tiles
+// 2w, 2w+1 over the slice's HR columns (KO column tiles each).  Without split
+// MLPs head j holds slice j as [O1][O3][O2][O4]; with them head j < NK holds
+// [O1][O2] of slice j and head NK + j [O3][O4] of slice j.
+std::vector<uint16_t> pack_heads(const PersistPlan& P, const wavernn_weights* w) {
+  const int Hh = P.Hh, KH = P.KH, RT = P.RT, HR = P.HR, KO = P.KO;
+  const bool split = P.NH == 2 * P.NK;
   auto O1m = [&](int r, int k) { return w->O1[(size_t)r * Hh + k]; };
   auto O3m = [&](int r, int k) { return w->O3[(size_t)r * Hh + k]; };
   auto O2m = [&](int v, int k) { return w->O2[(size_t)v * Hh + k]; };
   auto O4m = [&](int v, int k) { return w->O4[(size_t)v * Hh + k]; };
-  auto Rm = [&](int r, int k) { return R(r, k); };
-  // heads: wave w of head j holds O1/O3 row tile 4j + (w & 3), column tiles
-  // (w >> 2)*KH .. +KH, and O2/O4 class tiles 2w, 2w+1 over columns 64j .. 64j+63
   std::vector<uint16_t> hw((size_t)P.NH * 8 * P.hw_frags * 512);
   for (int j = 0; j < P.NH; ++j)
     for (int wv = 0; wv < 8; ++wv) {
       uint16_t* d = hw.data() + (size_t)(j * 8 + wv) * P.hw_frags * 512;
-      const int r0 = 64 * j + 16 * (wv & 3), k0 = 32 * (wv >> 2) * KH;
+      const int sl = j % P.NK;
+      const int r0 = HR * sl + 16 * (wv % RT), k0 = 32 * (wv / RT) * KH;
+      auto rows = [&](int r) { return r0 + r; };
+      auto cls = [&](int i) { const int v0 = 16 * (2 * wv + i / KO); return [v0](int r) { return v0 + r; }; };
+      if (split) {
+        const bool fine = j >= P.NK;
+        for (int i = 0; i < KH; ++i)
+          fine ? frag(d + (size_t)i * 512, O3m, rows, k0 + 32 * i) : frag(d + (size_t)i * 512, O1m, rows, k0 + 32 * i);
+        for (int i = 0; i < 2 * KO; ++i) {
+          const int col = HR * sl + 32 * (i % KO);
+          uint16_t* di = d + (size_t)(KH + i) * 512;
+          fine ? frag(di, O4m, cls(i), col) : frag(di, O2m, cls(i), col);
+        }
+        continue;
+      }
       for (int i = 0; i < KH; ++i) {
-        frag(d + (size_t)i * 512, O1m, [&](int r) { return r0 + r; }, k0 + 32 * i);
-        frag(d + (size_t)(KH + i) * 512, O3m, [&](int r) { return r0 + r; }, k0 + 32 * i);
+        frag(d + (size_t)i * 512, O1m, rows, k0 + 32 * i);
+        frag(d + (size_t)(KH + i) * 512, O3m, rows, k0 + 32 * i);
       }
-      for (int i = 0; i < 4; ++i) {
-        const int v0 = 16 * (2 * wv + (i >> 1)), col = 64 * j + 32 * (i & 1);
-        frag(d + (size_t)(2 * KH + i) * 512, O2m, [&](int r) { return v0 + r; }, col);
-        frag(d + (size_t)(2 * KH + 4 + i) * 512, O4m, [&](int r) { return v0 + r; }, col);
+      for (int i = 0; i < 2 * KO; ++i) {
+        const int col = HR * sl + 32 * (i % KO);
+        frag(d + (size_t)(2 * KH + i) * 512, O2m, cls(i), col);
+        frag(d + (size_t)(2 * KH + 2 * KO + i) * 512, O4m, cls(i), col);
       }
     }
-  // units: R row of row tile `tile` of a half, lane row r
-  auto rrow = [&](int tile, bool fine, int r) {
-    const int g = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + r;
-    return g * H + (fine ? Hh : 0) + i;
-  };
-  std::vector<uint16_t> uw((size_t)P.NU * P.u_lds_w / 2), ur((size_t)P.NU * UCT * KT * 512);
-  for (int k = 0; k < P.NU; ++k) {
-    uint16_t* d = uw.data() + (size_t)k * P.u_lds_w / 2;
-    for (int q = 0; q < UCT; ++q) {
-      const int tile = k * UCT + q;
-      for (int kt = 0; kt < KT; ++kt) {
-        frag(d + (size_t)(q * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); }, 32 * kt);
-        frag(ur.data() + ((size_t)tile * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); },
-             Hh + 32 * kt);
-      }
-      for (int kt = 0; kt < 2 * KT; ++kt)
-        frag(d + (size_t)(UCT * KT + q * 2 * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, true, r); }, 32 * kt);
-    }
-  }
+  return hw;
+}
+
+// Arrays every persistent plan uses: head fragments, I*, biases, the
+// conditioning projection, the per-frame table and the exchange words.
+wavernn_status upload_common(wavernn_model* m, const wavernn_weights* w) {
+  const wavernn_config& c = m->cfg;
+  const PersistPlan& P = m->plan;
+  const int H = P.H, Hh = P.Hh;
+  Rounder rd{true};
   wavernn_status s;
-  if ((s = m->upload(&m->d_hw, hw.data(), hw.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_uw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_ur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
+  {
+    std::vector<uint16_t> hw = pack_heads(P, w);
+    if ((s = m->upload(&m->d_hw, hw.data(), hw.size() * 2)) != WAVERNN_OK) return s;
+  }
   std::vector<float> Iv((size_t)9 * H), bv((size_t)3 * H);
   for (int row = 0; row < 3 * H; ++row) {
     for (int q = 0; q < 3; ++q) Iv[row * 3 + q] = (q == 2 && row % H < Hh) ? 0.0f : rd(w->I[row * 3 + q]);
@@ -283,15 +289,120 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
   m->cb_cap = c.cond_dim > 0 ? 1024 : 1;
   if ((s = m->alloc(&m->d_cb, (size_t)m->cb_cap * 3 * H * 4)) != WAVERNN_OK) return s;
   if ((s = m->alloc(&m->d_xc, (size_t)P.x_words * 8)) != WAVERNN_OK) return s;
-  HIPOK(hipFuncSetAttribute(m->pk, hipFuncAttributeMaxDynamicSharedMemorySize, P.lds));
+  return WAVERNN_OK;
+}
+
+// The whole persistent grid must fit on the device at once.
+wavernn_status check_coresident(wavernn_model* m, const void* k, int grid, int lds, const char* what) {
+  HIPOK(hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, lds));
   int per_cu = 0;
-  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->pk, WR_THREADS, P.lds));
+  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, WR_THREADS, lds));
   hipDeviceProp_t prop;
   HIPOK(hipGetDeviceProperties(&prop, m->device));
-  if (per_cu < 1 || per_cu * prop.multiProcessorCount < P.grid)
-    return fail(WAVERNN_E_UNSUPPORTED, "persistent grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)",
-                P.grid, per_cu, prop.multiProcessorCount);
+  if (per_cu < 1 || per_cu * prop.multiProcessorCount < grid)
+    return fail(WAVERNN_E_UNSUPPORTED, "%s grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)", what,
+                grid, per_cu, prop.multiProcessorCount);
   return WAVERNN_OK;
+}
+
+wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
+  const PersistPlan& P = m->plan;
+  const int H = P.H, Hh = P.Hh, KT = P.KT, KH = P.KH, UCT = P.UCT;
+  m->pk = wr_persist_kernel_ptr(KH);
+  if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no persistent kernel instantiation", H);
+  REff R{&m->cfg, w};
+  auto Rm = [&](int r, int k) { return R(r, k); };
+  // units: R row of row tile `tile` of a half, lane row r
+  auto rrow = [&](int tile, bool fine, int r) {
+    const int g = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + r;
+    return g * H + (fine ? Hh : 0) + i;
+  };
+  std::vector<uint16_t> uw((size_t)P.NU * P.u_lds_w / 2), ur((size_t)P.NU * UCT * KT * 512);
+  for (int k = 0; k < P.NU; ++k) {
+    uint16_t* d = uw.data() + (size_t)k * P.u_lds_w / 2;
+    for (int q = 0; q < UCT; ++q) {
+      const int tile = k * UCT + q;
+      for (int kt = 0; kt < KT; ++kt) {
+        frag(d + (size_t)(q * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); }, 32 * kt);
+        frag(ur.data() + ((size_t)tile * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); },
+             Hh + 32 * kt);
+      }
+      for (int kt = 0; kt < 2 * KT; ++kt)
+        frag(d + (size_t)(UCT * KT + q * 2 * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, true, r); }, 32 * kt);
+    }
+  }
+  wavernn_status s;
+  if ((s = m->upload(&m->d_uw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_ur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = upload_common(m, w)) != WAVERNN_OK) return s;
+  return check_coresident(m, m->pk, P.grid, P.lds, "persistent");
+}
+
+// Block-sparse R (Sec. 3.2): the kept entries of every row as records of the
+// block-sparse unit workgroups (layout in sparse_plan).  Rows per unit SR is
+// the first of 64, 128, 32, 16 whose records fit LDS and whose grid fits.
+wavernn_status build_sparse(wavernn_model* m, const wavernn_weights* w) {
+  const wavernn_config& c = m->cfg;
+  const int H = c.hidden, Hh = H / 2;
+  const int bh = c.r_format == WAVERNN_R_BSR_4X4 ? 4 : 16, bw = c.r_format == WAVERNN_R_BSR_4X4 ? 4 : 1;
+  // kept entries (column, bf16 weight) of every row, coarse and fine columns apart, in column order
+  std::vector<std::vector<uint32_t>> ent((size_t)6 * H);
+  size_t maxlen[2] = {0, 0};
+  for (int row = 0; row < 3 * H; ++row) {
+    const int g = row / H, i = row % H;
+    const uint8_t* mrow = w->R_block_mask + ((size_t)g * (H / bh) + i / bh) * (H / bw);
+    for (int bc = 0; bc < H / bw; ++bc) {
+      if (!mrow[bc]) continue;
+      for (int cc = 0; cc < bw; ++cc) {
+        const int col = bc * bw + cc;
+        ent[(size_t)2 * row + (col >= Hh)].push_back((uint32_t)col | (uint32_t)f2bf(w->R[(size_t)row * H + col]) << 16);
+      }
+    }
+    for (int ph = 0; ph < 2; ++ph) maxlen[ph] = std::max(maxlen[ph], ent[(size_t)2 * row + ph].size());
+  }
+  hipDeviceProp_t prop;
+  HIPOK(hipGetDeviceProperties(&prop, m->device));
+  PersistPlan& P = m->plan;
+  bool ok = false;
+  for (int SR : {64, 128, 32, 16}) {
+    const int SL = 256 / SR;
+    auto nrec = [&](size_t len) { return std::max(1, (int)((len + SL - 1) / SL + 3) / 4); };
+    if (sparse_plan(H, SR, nrec(maxlen[0]), nrec(maxlen[1]), &P) && P.grid <= prop.multiProcessorCount) {
+      ok = true;
+      break;
+    }
+  }
+  if (!ok) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: the kept blocks of R do not fit a block-sparse plan", H);
+  m->pk = wr_sparse_kernel_ptr(P.KH, P.GU);
+  if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no block-sparse kernel instantiation", H);
+  const int NR = P.NRC + P.NRF;
+  std::vector<uint32_t> recs((size_t)P.NU * NR * 256 * 4, 0);
+  for (int k = 0; k < P.NU; ++k)
+    for (int L = 0; L < 256; ++L) {
+      const int row = P.SR * k + L / P.SL, part = L % P.SL;
+      for (int ph = 0; ph < 2; ++ph) {
+        const std::vector<uint32_t>& E = ent[(size_t)2 * row + ph];
+        const int nr = ph ? P.NRF : P.NRC, r0 = ph ? P.NRC : 0;
+        for (int r = 0; r < nr; ++r) {
+          uint32_t col[4], wt[4];
+          for (int e = 0; e < 4; ++e) {
+            const size_t idx = (size_t)part + (size_t)P.SL * (4 * r + e);
+            col[e] = idx < E.size() ? (E[idx] & 0xffffu) : (uint32_t)(ph ? Hh : 0);
+            wt[e] = idx < E.size() ? (E[idx] >> 16) : 0u;
+          }
+          uint32_t* d = recs.data() + (((size_t)k * NR + r0 + r) * 256 + L) * 4;
+          d[0] = col[0] | col[1] << 16;
+          d[1] = col[2] | col[3] << 16;
+          d[2] = wt[0] | wt[1] << 16;
+          d[3] = wt[2] | wt[3] << 16;
+        }
+      }
+    }
+  wavernn_status s;
+  if ((s = m->upload(&m->d_uw, recs.data(), recs.size() * 4)) != WAVERNN_OK) return s;
+  if ((s = upload_common(m, w)) != WAVERNN_OK) return s;
+  m->sparse = true;
+  return check_coresident(m, m->pk, P.grid, P.lds, "block-sparse");
 }
 
 // Batched path: unit blocks for WR_BUCT = 4 row tiles per half (the head
@@ -615,6 +726,15 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
   } else if (small_fits) {
     m->path = PATH_SMALL;
     s = build_small(m, w);
+  } else if (cfg->r_format != WAVERNN_R_DENSE) {
+    // Sparse WaveRNN (Sec. 3): block-sparse unit workgroups; several streams
+    // run one after another
+    if (cfg->weight_dtype != WAVERNN_BF16) {
+      s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d needs bf16 weights (fp32 weights fit LDS only for small models)", H);
+    } else {
+      m->path = PATH_PERSIST;
+      s = build_sparse(m, w);
+    }
   } else if (persist_plan(H, &m->plan)) {
     if (cfg->weight_dtype != WAVERNN_BF16) {
       s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d needs bf16 weights (fp32 weights fit LDS only for small models)", H);
@@ -694,6 +814,7 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
     path = PATH_BATCHED, g = B.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST) {
     g = m->plan.grid, b = WR_THREADS;
+    if (m->sparse) path = 3;
   }
   if (grid) *grid = g;
   if (block) *block = b;

@@ -80,11 +80,16 @@ WR_HD inline SmallLayout small_layout(int H) {
 #define WR_MAXUCT 3       // coarse (and fine) row tiles per unit workgroup (waves 3, 7 stay free)
 
 struct PersistPlan {
-  int H, Hh, KT, KH;      // KT = Hh / 32 column tiles per half, KH = KT / 2
+  int H, Hh, KT, KH;      // KT = Hh / 32 column tiles per half, KH = column tiles per head wave
+  int RT, HR, KO, GU;     // head: row tiles (HR = 16 RT rows of O1 / O3), O2 / O4 column tiles
+                          // (HR / 32), gate units per gate thread
   int NH, NU, UCT, NCT;   // heads, units, row tiles per unit and half, row tiles per half (3 Hh / 16)
+  int NK;                 // slices of O1 / O3 rows (Hh / HR): the partial logits per half
+  int SR, SL, NRC, NRF;   // block-sparse units: rows per unit, lanes per row, records per lane
+                          // (coarse columns, fine columns); 0 for the dense kernel
   int grid;               // workgroups launched: head j at block 8j, units on the others
-  int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[4], O4[4]
-  int u_lds_w;            // unit LDS weight block: coarse tiles x coarse columns, fine tiles x all columns
+  int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[2 KO], O4[2 KO]
+  int u_lds_w;            // unit LDS block: dense R tiles, or the block-sparse records
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (64-bit words)
   int x_ps;               // words between the partial-logit blocks of consecutive heads
   int lds_h, lds_u, lds;  // LDS bytes
@@ -108,6 +113,12 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->KT = P->Hh / 32;
   P->KH = P->KT / 2;
   P->NH = P->Hh / WR_HROWS;
+  P->NK = P->NH;
+  P->RT = 4;
+  P->HR = WR_HROWS;
+  P->KO = 2;
+  P->GU = 1;
+  P->SR = P->SL = P->NRC = P->NRF = 0;
   P->NCT = 3 * P->Hh / 16;
   if (P->NH > 16 || P->Hh > WR_THREADS - 64) return false;   // the last wave draws, free of gate work
   P->hw_frags = 2 * P->KH + 8;
@@ -139,6 +150,71 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->x_words = o;
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024;
+}
+
+// ---------------------------------------------------------------------------
+// Block-sparse R (Sparse WaveRNN, Sec. 3.2) on the persistent kernel.
+//
+// Heads: split MLPs (heads j < NK hold 64-row slice j of O1 and the matching
+// columns of O2; heads NK + j the same of O3, O4), NK = Hh / 64, and
+// GU = ceil(Hh / 448) gate slots per preparing thread (GU > 1: gate state in
+// LDS).
+// Unit k owns the SR consecutive R rows SR k .. SR k + SR - 1 (row order
+// g H + i, SR divides Hh, so a unit stays inside one gate and one half).
+// Waves 0-3 compute: SL = 256 / SR consecutive lanes share a row and each
+// walks its own list of records; a record is 4 (column, weight) pairs of the
+// row's kept entries (uint4: columns as 4 x u16, weights as 4 x bf16), the
+// row's entries dealt to its lanes in turn, in column order, padded with zero
+// weights.  Records sit in LDS as [NRC + NRF][256 lanes], coarse columns first.
+// Waves 4-7 read h from the heads and never store.
+// ---------------------------------------------------------------------------
+WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
+  if (H <= 0 || H % 128) return false;
+  P->H = H;
+  P->Hh = H / 2;
+  P->KT = P->Hh / 32;
+  P->RT = 4;
+  P->HR = 64;
+  P->KO = 2;
+  const int KC = 2;
+  P->KH = P->KT / KC;
+  P->NK = P->Hh / P->HR;
+  P->NH = 2 * P->NK;
+  P->GU = (P->Hh + 447) / 448;
+  if (P->NH > 32 || P->GU > 3) return false;
+  if (SR < 16 || SR > 256 || 256 % SR || P->Hh % SR || NRC < 1 || NRF < 1) return false;
+  P->SR = SR;
+  P->SL = 256 / SR;
+  P->NRC = NRC;
+  P->NRF = NRF;
+  P->UCT = 0;
+  P->NCT = 3 * P->Hh / 16;
+  P->NU = 3 * H / SR;
+  P->hw_frags = P->KH + 2 * P->KO;
+  // head LDS: operand image (KT + KO fragments), first-layer partials
+  // [KC][HR], logit sums [2][256], logits [256], then y [Hh] (GU = 1) or
+  // h_c, h_f [2][Hh], prepared terms [5][Hh], I* [Hh][15] (GU > 1), misc [16],
+  // uniforms [2][64][2], targets [2][64]
+  P->lds_h = (P->KT + P->KO) * WR_FRAG +
+             4 * (KC * P->HR + 3 * 256 + (P->GU > 1 ? 22 * P->Hh : P->Hh) + 16 + 256 + 128);
+  // unit LDS: records, h [H], misc [16]
+  P->u_lds_w = (NRC + NRF) * 256 * 16;
+  P->lds_u = P->u_lds_w + 4 * (H + 16);
+  int g = 8 * (P->NH - 1) + 1;
+  while (g - P->NH < P->NU) ++g;
+  P->grid = g;
+  int o = 0;
+  auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
+  P->x_yc = take(P->Hh);
+  P->x_yf = take(P->Hh);
+  P->x_ga = take(3 * P->Hh);
+  P->x_gf = take(3 * P->Hh);
+  P->x_ps = 256;
+  P->x_pc = take(P->NK * P->x_ps);
+  P->x_pf = take(P->NK * P->x_ps);
+  P->x_words = o;
+  P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
+  return P->lds <= 160 * 1024 && P->grid <= 256;
 }
 
 // ---------------------------------------------------------------------------

@@ -27,50 +27,88 @@ __device__ __forceinline__ const float* cb_row(const PersistArgs& a, int64_t n) 
 }
 
 // ------------------------------------------------------------------ head role
-// Wave roles: waves 0-6 evaluate the gates (one unit per thread), all 8 waves
-// run the MFMA layers and gather the partial logits (two threads per class),
-// wave 7 publishes this head's slice of y for the unit workgroups and draws.
-template <int KH>
+// A head owns a slice of HR = 16 RT rows of O1 / O3 (RT row tiles; the 8
+// waves split them into RT row tiles x KC = 8 / RT column-tile chunks of KH
+// tiles each) and the matching HR columns of O2 / O4 (class tiles 2w, 2w+1 of
+// wave w).  NK = Hh / HR slices per half.  Without SPLIT head j holds slice j
+// of both output MLPs; with SPLIT heads j < NK hold slice j of the coarse MLP
+// (O1, O2) and heads NK + j slice j of the fine MLP (O3, O4), half the
+// registers each.
+// Every head evaluates every gate (Eq. 2) and draws both classes.  The work that does not depend on
+// the class being drawn (reading R h from the units, the I* terms of the known
+// inputs) runs on waves 0-6 while wave 7 draws; the rest follows the draw.
+//  GU = 1 (Hh <= 448): thread u < Hh owns coarse unit u and fine unit Hh + u,
+//   its state in registers.
+//  GU > 1 (wide): waves 0-6 prepare the pre-activations of units tid + 448 m
+//   into LDS, then all 8 waves finish units tid + 512 m; the state stays in
+//   LDS (registers are short with the larger O-layer slices).
+// All 8 waves run the MFMA layers and gather the partial logits (two threads
+// per class); wave 7 publishes this head's slice of y for the unit workgroups.
+template <int KH, int RT, int GU, bool SPLIT>
 __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
-  constexpr int KT = 2 * KH;
-  constexpr int NH = KH;                           // Hh / 64 heads = H / 128
-  constexpr int DW = 7;                            // the draw wave (no gate work: Hh <= 448)
+  constexpr int KC = 8 / RT;                       // column-tile chunks
+  constexpr int KT = KH * KC;                      // column tiles per half
+  constexpr int HR = 16 * RT;                      // rows per head
+  constexpr int KO = HR / 32;                      // column tiles of the O2 / O4 slice
+  constexpr int NK = 2 * KT / RT;                  // slices per half (Hh / HR)
+  constexpr int NH = SPLIT ? 2 * NK : NK;          // heads
+  constexpr int NHP = (NK + 1) / 2;                // partials per gathering thread
+  constexpr int DW = 7;                            // the draw wave (no gate preparation)
+  constexpr bool WIDE = GU > 1;
+  constexpr int Hh = 32 * KT;
+  static_assert(8 % RT == 0 && KO >= 1, "head shape");
   const PersistPlan& P = a.P;
-  const int H = P.H, Hh = P.Hh;
+  const int H = P.H;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const bool coarse = !SPLIT || j < NK;           // runs the coarse MLP slice
+  const bool fine = !SPLIT || j >= NK;             // runs the fine MLP slice
+  const int jk = SPLIT ? j % NK : j;               // slice index
   unsigned char* imc = lds;                        // y_c operand image [KT]
-  unsigned char* imf = imc + KT * WR_FRAG;         // y_f operand image [KT]
-  unsigned char* imo = imf + KT * WR_FRAG;         // relu(first layer) image [2]
-  float* op = (float*)(imo + 2 * WR_FRAG);         // [2][64] first-layer partials
-  float* zs2 = op + 2 * 64;                        // [256] sums over the second half of the heads
+  unsigned char* imf = SPLIT ? lds : imc + KT * WR_FRAG;   // y_f operand image [KT] (SPLIT: one image)
+  unsigned char* imo = imf + KT * WR_FRAG;         // relu(first layer) image [KO]
+  float* op = (float*)(imo + KO * WR_FRAG);        // [KC][HR] first-layer partials
+  float* zs2 = op + KC * HR;                       // [256] sums over the second half of the heads
   float* zs = zs2 + 256;                           // [256] sums over the first half of the heads
   float* zk = zs + 256;                            // [256] logits of the last draw
-  float* yv = zk + 256;                            // [448] this half of h (fp32)
-  int* misc = (int*)(yv + 448);                    // [0] abort [1] c_t [2] c_prev [3] f_prev
+  float* yv = zk + 256;                            // [Hh] (GU = 1) this half of h; (wide) h_c
+  float* hfv = yv + Hh;                            // wide: [Hh] h_f
+  float* pre = hfv + Hh;                           // wide: [5][Hh] prepared gate terms
+  float* iws = pre + 5 * Hh;                       // wide: [Hh][15] I* of coarse (2) and fine (3) columns
+  int* misc = (int*)(WIDE ? iws + 15 * Hh : yv + Hh);   // [0] abort [1] c_t [2] c_prev [3] f_prev
   float* fmisc = (float*)(misc + 8);               // [2] lse_c [3] z_c[c]
   float2* uni = (float2*)(misc + 16);              // [2][64] (u_c, u_f) of a batch of 64 steps
   int* tgt = (int*)(uni + 128);                    // [2][64] teacher-forcing targets of the batch
 
   // --- prologue: zero the operand images, load this wave's fragments
-  for (int i = tid; i < (2 * KT + 2) * WR_FRAG / 16; i += WR_THREADS) ((uint4*)lds)[i] = uint4{0, 0, 0, 0};
-  bf16x8 W1[KH], W3[KH], W2[4], W4[4];
+  for (int i = tid; i < ((SPLIT ? 1 : 2) * KT + KO) * WR_FRAG / 16; i += WR_THREADS) ((uint4*)lds)[i] = uint4{0, 0, 0, 0};
+  // fragments: W1 [KH], W2 [2 KO] of the head's (first) MLP slice, then
+  // without SPLIT W3 [KH], W4 [2 KO] of its fine slice; SPLIT: a fine head's
+  // W1, W2 hold O3, O4
+  constexpr int KH3 = SPLIT ? 1 : KH, KO4 = SPLIT ? 1 : 2 * KO;
+  bf16x8 W1[KH], W3[KH3], W2[2 * KO], W4[KO4];
   {
     const uint4* src = a.hw + ((size_t)(j * 8 + wave) * P.hw_frags) * 64 + lane;
 #pragma unroll
     for (int i = 0; i < KH; ++i) W1[i] = __builtin_bit_cast(bf16x8, src[(size_t)i * 64]);
+    if (!SPLIT) {
 #pragma unroll
-    for (int i = 0; i < KH; ++i) W3[i] = __builtin_bit_cast(bf16x8, src[(size_t)(KH + i) * 64]);
+      for (int i = 0; i < KH3; ++i) W3[i] = __builtin_bit_cast(bf16x8, src[(size_t)(KH + i) * 64]);
+    }
+    const uint4* s2 = src + (size_t)(SPLIT ? KH : 2 * KH) * 64;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) W2[i] = __builtin_bit_cast(bf16x8, src[(size_t)(2 * KH + i) * 64]);
+    for (int i = 0; i < 2 * KO; ++i) W2[i] = __builtin_bit_cast(bf16x8, s2[(size_t)i * 64]);
+    if (!SPLIT) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) W4[i] = __builtin_bit_cast(bf16x8, src[(size_t)(2 * KH + 4 + i) * 64]);
+      for (int i = 0; i < KO4; ++i) W4[i] = __builtin_bit_cast(bf16x8, s2[(size_t)(2 * KO + i) * 64]);
+    }
   }
-  // gate thread u: coarse unit u and fine unit Hh + u
+  // GU = 1: gate thread u < Hh.  I* coefficients: coarse row (c_{t-1}, f_{t-1}),
+  // fine row (c_{t-1}, f_{t-1}, c_t) of each gate.
+  const bool gate = tid < Hh;
   const int u = tid;
-  const bool gate = u < Hh;
   float ic[3][2], ifn[3][3];
   float hc = 0.0f, hf = 0.0f;
-  if (gate) {
+  if (!WIDE && gate) {
 #pragma unroll
     for (int g = 0; g < 3; ++g) {
       ic[g][0] = a.Iw[3 * (g * H + u) + 0];
@@ -84,8 +122,22 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       hf = a.h_in[Hh + u];
     }
   }
-  const float b1r = tid < 64 ? a.b1[j * 64 + tid] : 0.0f;
-  const float b3r = tid < 64 ? a.b3[j * 64 + tid] : 0.0f;
+  if (WIDE) {
+    for (int v = tid; v < Hh; v += WR_THREADS) {
+#pragma unroll
+      for (int g = 0; g < 3; ++g) {
+        iws[15 * v + 5 * g + 0] = a.Iw[3 * (g * H + v) + 0];
+        iws[15 * v + 5 * g + 1] = a.Iw[3 * (g * H + v) + 1];
+        iws[15 * v + 5 * g + 2] = a.Iw[3 * (g * H + Hh + v) + 0];
+        iws[15 * v + 5 * g + 3] = a.Iw[3 * (g * H + Hh + v) + 1];
+        iws[15 * v + 5 * g + 4] = a.Iw[3 * (g * H + Hh + v) + 2];
+      }
+      yv[v] = a.h_in ? a.h_in[v] : 0.0f;
+      hfv[v] = a.h_in ? a.h_in[Hh + v] : 0.0f;
+    }
+  }
+  const float b1r = tid < HR && coarse ? a.b1[jk * HR + tid] : 0.0f;
+  const float b3r = tid < HR && fine ? a.b3[jk * HR + tid] : 0.0f;
   const float4 b2l = wave == DW ? *(const float4*)(a.b2 + 4 * lane) : float4{0, 0, 0, 0};
   const float4 b4l = wave == DW ? *(const float4*)(a.b4 + 4 * lane) : float4{0, 0, 0, 0};
   if (tid == 0) {
@@ -97,22 +149,22 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   const u64* GF = a.xc + P.x_gf;
   u64* YC = a.xc + P.x_yc;
   u64* YF = a.xc + P.x_yf;
-  u64* PCo = a.xc + P.x_pc + (size_t)j * P.x_ps;
-  u64* PFo = a.xc + P.x_pf + (size_t)j * P.x_ps;
+  u64* PCo = a.xc + P.x_pc + (size_t)jk * P.x_ps;
+  u64* PFo = a.xc + P.x_pf + (size_t)jk * P.x_ps;
   const u64* PC = a.xc + P.x_pc;
   const u64* PF = a.xc + P.x_pf;
-  const int rt = wave & 3, kc = wave >> 2;         // first layer: row tile, column-tile half
-  // pre-activation words of this thread's units, loaded ahead
+  const int rt = wave % RT, kc = wave / RT;        // first layer: row tile, column-tile chunk
+  // GU = 1: pre-activation words of this thread's units, loaded ahead
   u64 pc[3] = {0, 0, 0}, pf[3] = {0, 0, 0};
   float cbe_c = 0.0f, cbe_f = 0.0f;
   auto prefetch_coarse = [&](int64_t n) {
-    if (gate) {
+    if (!WIDE && gate) {
       pc[0] = xpeek(GA + u); pc[1] = xpeek(GA + Hh + u); pc[2] = xpeek(GA + 2 * Hh + u);
       cbe_c = cb_row(a, n)[2 * H + u];
     }
   };
   auto prefetch_fine = [&](int64_t n) {
-    if (gate) {
+    if (!WIDE && gate) {
       pf[0] = xpeek(GF + u); pf[1] = xpeek(GF + Hh + u); pf[2] = xpeek(GF + 2 * Hh + u);
       cbe_f = cb_row(a, n)[2 * H + Hh + u];
     }
@@ -125,19 +177,25 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       acc0 = mfma(afrag(img, kc * KH + i), W[i], acc0);
       if (i + 1 < KH) acc1 = mfma(afrag(img, kc * KH + i + 1), W[i + 1], acc1);
     }
-    if (lane < 16) op[kc * 64 + 16 * rt + lane] = mfma_row(acc0) + mfma_row(acc1);
+    if (lane < 16) op[kc * HR + 16 * rt + lane] = mfma_row(acc0) + mfma_row(acc1);
     __syncthreads();
-    if (tid < 64) aput(imo + (tid >> 5) * WR_FRAG, tid & 31, wr_relu((op[tid] + op[64 + tid]) + b));
+    if (tid < HR) {
+      float s = op[tid];
+#pragma unroll
+      for (int q = 1; q < KC; ++q) s += op[q * HR + tid];
+      aput(imo + (tid >> 5) * WR_FRAG, tid & 31, wr_relu(s + b));
+    }
     __syncthreads();
   };
-  // second layer: class tiles 2*wave, 2*wave+1 over this head's 64 columns;
-  // waves 4-7 publish the 256 partial logits
+  // second layer: class tiles 2*wave, 2*wave+1 over this head's HR columns
   auto second_layer = [&](const bf16x8* W, u64* dst, uint32_t tag) {
-    const bf16x8 x0 = afrag(imo, 0), x1 = afrag(imo, 1);
-    f32x4 A = mfma(x0, W[0], f32x4{0, 0, 0, 0});
-    f32x4 B = mfma(x0, W[2], f32x4{0, 0, 0, 0});
-    A = mfma(x1, W[1], A);
-    B = mfma(x1, W[3], B);
+    f32x4 A = {0, 0, 0, 0}, B = {0, 0, 0, 0};
+#pragma unroll
+    for (int kt = 0; kt < KO; ++kt) {
+      const bf16x8 x = afrag(imo, kt);
+      A = mfma(x, W[kt], A);
+      B = mfma(x, W[KO + kt], B);
+    }
     if (lane < 16) {
       xpub(dst + 32 * wave + lane, tag, mfma_row(A));
       xpub(dst + 32 * wave + 16 + lane, tag, mfma_row(B));
@@ -147,8 +205,8 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   // in head order
   auto gather_logits = [&](const u64* src, uint32_t tag) {
     float s;
-    const int v = tid & 255, hh = tid >> 8, NH0 = (NH + 1) / 2;
-    if (!sum_parts<(KH + 1) / 2>(src, P.x_ps, hh ? NH0 : 0, hh ? NH : NH0, v, tag, &s, a)) misc[0] = 1;
+    const int v = tid & 255, hh = tid >> 8;
+    if (!sum_parts<NHP>(src, P.x_ps, hh ? NHP : 0, hh ? NK : NHP, v, tag, &s, a)) misc[0] = 1;
     else (hh ? zs2 : zs)[v] = s;
   };
   // Philox blocks of steps t .. t+63 into batch buffer b, one step per lane of
@@ -167,11 +225,41 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   prefetch_coarse(a.t0);
   prefetch_fine(a.t0);
   const bool trw = j == 0 && tid == WR_THREADS - 64;       // tracing thread (draw wave)
-  // Gate work is split around the draws: the part that does not depend on the
-  // class being drawn runs on the gate waves while the draw wave draws.
-  float cu = 0.0f, cr = 0.0f, ce = 0.0f, cie = 0.0f;       // coarse: before f_{t-1} is known
-  float fu = 0.0f, fr = 0.0f, fe = 0.0f, fie = 0.0f;       // fine: before c_t is known
-  auto coarse_pre = [&](uint32_t tag, float x0) {
+  // wide: wait for the words of gate block G (3 gates x Hh) of units tid + 448 m
+  // and call f(v, m, unit) for each (all loads issued at once)
+  auto wide_words = [&](const u64* G, uint32_t tag, auto&& f) -> bool {
+    if (wave == DW) return true;
+    const u64* ps[3 * GU];
+    const u64 none[3 * GU] = {};
+    float v[3 * GU];
+#pragma unroll
+    for (int k = 0; k < 3 * GU; ++k) {
+      const int m = k / 3, un = tid + 448 * m;
+      ps[k] = G + (k % 3) * Hh + (un < Hh ? un : tid);
+    }
+    if (!poll_pref<3 * GU>(ps, none, tag, v, a)) return false;
+#pragma unroll
+    for (int m = 0; m < GU; ++m)
+      if (tid + 448 * m < Hh) f(v + 3 * m, tid + 448 * m);
+    return true;
+  };
+  float cu = 0.0f, cr = 0.0f, ce = 0.0f, cie = 0.0f;       // GU = 1, coarse: before f_{t-1} is known
+  float fu = 0.0f, fr = 0.0f, fe = 0.0f, fie = 0.0f;       // GU = 1, fine: before c_t is known
+  // coarse gate terms known before f_{t-1} (n: the step's sample index)
+  auto coarse_pre = [&](uint32_t tag, float x0, int64_t n) {
+    if (WIDE) {
+      const float* cbr = cb_row(a, n) + 2 * H;
+      if (!wide_words(GA, tag, [&](const float* v, int un) {
+            const float* iv = iws + 15 * un;
+            pre[un] = v[0] + iv[0] * x0;
+            pre[Hh + un] = v[1] + iv[5] * x0;
+            pre[2 * Hh + un] = v[2];
+            pre[3 * Hh + un] = iv[10] * x0;
+            pre[4 * Hh + un] = cbr[un];
+          }))
+        misc[0] = 1;
+      return;
+    }
     if (!gate) return;
     const u64* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
     float v[3];
@@ -184,7 +272,20 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     ce = v[2];
     cie = ic[2][0] * x0;
   };
-  auto fine_pre = [&](uint32_t tag, float x0, float x1) {
+  auto fine_pre = [&](uint32_t tag, float x0, float x1, int64_t n) {
+    if (WIDE) {
+      const float* cbr = cb_row(a, n) + 2 * H + Hh;
+      if (!wide_words(GF, tag, [&](const float* v, int un) {
+            const float* iv = iws + 15 * un;
+            pre[un] = v[0] + __builtin_fmaf(iv[3], x1, iv[2] * x0);
+            pre[Hh + un] = v[1] + __builtin_fmaf(iv[8], x1, iv[7] * x0);
+            pre[2 * Hh + un] = v[2];
+            pre[3 * Hh + un] = __builtin_fmaf(iv[13], x1, iv[12] * x0);
+            pre[4 * Hh + un] = cbr[un];
+          }))
+        misc[0] = 1;
+      return;
+    }
     if (!gate) return;
     const u64* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
     float v[3];
@@ -197,7 +298,23 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     fe = v[2];
     fie = __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0);
   };
-  coarse_pre(1u, fscale(misc[2]));
+  // wide: finish the gates of units tid + 512 m with the drawn input x (I*
+  // column q of the row) into h (LDS) and the operand image
+  auto wide_gates = [&](float x, int q, float* h, unsigned char* img, bool to_img) {
+#pragma unroll
+    for (int m = 0; m < (Hh + WR_THREADS - 1) / WR_THREADS; ++m) {
+      const int un = tid + WR_THREADS * m;
+      if (un >= Hh) break;
+      const float* iv = iws + 15 * un;
+      const float uu = fsig(__builtin_fmaf(iv[q], x, pre[un]));
+      const float rr = fsig(__builtin_fmaf(iv[5 + q], x, pre[Hh + un]));
+      const float e = ftanh(__builtin_fmaf(rr, pre[2 * Hh + un], __builtin_fmaf(iv[10 + q], x, pre[3 * Hh + un]) + pre[4 * Hh + un]));
+      const float hn = __builtin_fmaf(uu, h[un], (1.0f - uu) * e);
+      h[un] = hn;
+      if (to_img) aput(img + (un >> 5) * WR_FRAG, un & 31, hn);
+    }
+  };
+  coarse_pre(1u, fscale(misc[2]), a.t0);
   // Every prologue load has landed: no wait inside the loop is left waiting on
   // them (a wait there would also wait for the wave's outstanding stores).
   __builtin_amdgcn_s_waitcnt(0);
@@ -211,22 +328,26 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     const int bs = (int)((t >> 6) & 1) * 64 + (int)(t & 63);   // this step in the batch buffers
     if (wave == DW && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
     // (1) coarse gates of every unit, finished with f_{t-1}
-    if (gate) {
+    if (WIDE) {
+      wide_gates(fscale(misc[3]), 1, yv, imc, coarse);
+    } else if (gate) {
       const float x1 = fscale(misc[3]);
       const float uu = fsig(__builtin_fmaf(ic[0][1], x1, cu)), rr = fsig(__builtin_fmaf(ic[1][1], x1, cr));
       const float e = ftanh(__builtin_fmaf(rr, ce, __builtin_fmaf(ic[2][1], x1, cie) + cbe_c));
       hc = __builtin_fmaf(uu, hc, (1.0f - uu) * e);
-      aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
+      if (coarse) aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
       yv[u] = hc;
     }
     __syncthreads();
     if (trw) trace_at(a, t, 1);
-    if (wave == DW) xpub(YC + 64 * j + lane, tag, yv[64 * j + lane]);   // this head's slice, for the units
+    if (coarse && wave == DW && lane < HR) xpub(YC + HR * jk + lane, tag, yv[HR * jk + lane]);   // this head's slice
     // (2) own rows of O1 -> relu -> own columns of O2 -> partial coarse logits
-    first_layer(W1, imc, b1r);
-    if (trw) trace_at(a, t, 2);
-    second_layer(W2, PCo, tag);
-    if (trw) trace_at(a, t, 3);
+    if (coarse) {
+      first_layer(W1, imc, b1r);
+      if (trw) trace_at(a, t, 2);
+      second_layer(W2, PCo, tag);
+      if (trw) trace_at(a, t, 3);
+    }
     if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 13);
     if (j > 0 && NH <= 8 && tid == WR_THREADS - 64) trace_at(a, t, 24 + j);
     // (3) coarse logits of all heads; this step's fine words are loaded
@@ -249,29 +370,38 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
         }
       }
     } else {
-      fine_pre(tag, fscale(misc[2]), fscale(misc[3]));
+      fine_pre(tag, fscale(misc[2]), fscale(misc[3]), n);
     }
     __syncthreads();
     if (misc[0]) return;
     if (trw) trace_at(a, t, 5);
     // (5) fine gates of every unit, finished with c_t (c_t reaches the fine half only)
     const int c = misc[1];
-    if (gate) {
+    if (WIDE) {
+      wide_gates(fscale(c), 4, hfv, imf, fine);
+    } else if (gate) {
       const float x2 = fscale(c);
       const float uu = fsig(__builtin_fmaf(ifn[0][2], x2, fu)), rr = fsig(__builtin_fmaf(ifn[1][2], x2, fr));
       const float e = ftanh(__builtin_fmaf(rr, fe, __builtin_fmaf(ifn[2][2], x2, fie) + cbe_f));
       hf = __builtin_fmaf(uu, hf, (1.0f - uu) * e);
-      aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
+      if (fine) aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
       yv[u] = hf;
     }
     __syncthreads();
     if (trw) trace_at(a, t, 6);
-    if (wave == DW) xpub(YF + 64 * j + lane, tag, yv[64 * j + lane]);
+    if (fine && wave == DW && lane < HR) xpub(YF + HR * jk + lane, tag, (WIDE ? hfv : yv)[HR * jk + lane]);
     // (6) own rows of O3 -> relu -> own columns of O4 -> partial fine logits
-    first_layer(W3, imf, b3r);
-    if (trw) trace_at(a, t, 7);
-    second_layer(W4, PFo, tag);
-    if (trw) trace_at(a, t, 8);
+    if (fine) {
+      if (SPLIT) {
+        first_layer(W1, imf, b3r);
+        second_layer(W2, PFo, tag);
+      } else {
+        first_layer(W3, imf, b3r);
+        if (trw) trace_at(a, t, 7);
+        second_layer(W4, PFo, tag);
+        if (trw) trace_at(a, t, 8);
+      }
+    }
     if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 14);
     // (7) fine logits of all heads; next step's coarse words are loaded
     gather_logits(PF, tag);
@@ -294,14 +424,20 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
         misc[3] = f;
       }
     } else if (t + 1 < a.T) {
-      coarse_pre(tag + 1, fscale(c));
+      coarse_pre(tag + 1, fscale(c), n + 1);
     }
     __syncthreads();
     if (misc[0]) return;
     if (trw) trace_at(a, t, 10);
   }
   if (j == 0) {
-    if (a.h_out && gate) {
+    if (WIDE) {
+      if (a.h_out)
+        for (int v = tid; v < Hh; v += WR_THREADS) {
+          a.h_out[v] = yv[v];
+          a.h_out[Hh + v] = hfv[v];
+        }
+    } else if (a.h_out && gate) {
       a.h_out[u] = hc;
       a.h_out[Hh + u] = hf;
     }
@@ -460,8 +596,129 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_persist_kernel(PersistArgs a
   extern __shared__ __align__(16) unsigned char lds[];
   const int r = wr_role(a.P, blockIdx.x);
   if (r < 0) return;
-  if (r < a.P.NH) head_role<KH>(a, r, lds);
+  if (r < a.P.NH) head_role<KH, 4, 1, false>(a, r, lds);
   else unit_role<KH>(a, r - a.P.NH, lds);
+}
+
+// ------------------------------------------------------------ block-sparse unit role
+// Unit k of a block-sparse R (Sec. 3.2): rows SR k .. SR k + SR - 1 of the
+// stacked gate matrices, SL lanes of waves 0-3 per row, each summing its own
+// kept entries (records in LDS) against h in LDS; waves 4-7 gather h.
+__device__ __forceinline__ void sparse_unit_role(const PersistArgs& a, int k, unsigned char* lds) {
+  const PersistPlan& P = a.P;
+  const int H = P.H, Hh = P.Hh, SL = P.SL, NRC = P.NRC, NRF = P.NRF;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const uint4* rec = (const uint4*)lds;           // [NRC + NRF][256]
+  float* hv = (float*)(lds + P.u_lds_w);          // [H] h of the last step
+  int* misc = (int*)(hv + H);
+  const bool cw = tid < 256;                      // computing (and publishing) lanes
+  const int row = P.SR * k + (tid & 255) / SL;    // R row g H + i of a computing lane
+  const bool lead = cw && tid % SL == 0;
+  const int g = row / H, i = row % H;
+  const bool fine = i >= Hh;
+  u64* dst = a.xc + (fine ? P.x_gf : P.x_ga) + g * Hh + (fine ? i - Hh : i);
+  {
+    const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
+    for (int q = tid; q < P.u_lds_w / 16; q += WR_THREADS) ((uint4*)lds)[q] = src[q];
+    for (int c = tid; c < H; c += WR_THREADS) hv[c] = a.h_in ? a.h_in[c] : 0.0f;
+    if (tid == 0) misc[0] = 0;
+  }
+  __syncthreads();
+  float acc = 0.0f;
+  auto mac = [&](int r0, int n) {
+    const uint4* rp = rec + (size_t)r0 * 256 + tid;
+#pragma unroll 2
+    for (int r = 0; r < n; ++r) {
+      const uint4 q = rp[r * 256];
+      acc = __builtin_fmaf(bf_lo(q.z), hv[q.x & 0xffffu], acc);
+      acc = __builtin_fmaf(bf_hi(q.z), hv[q.x >> 16], acc);
+      acc = __builtin_fmaf(bf_lo(q.w), hv[q.y & 0xffffu], acc);
+      acc = __builtin_fmaf(bf_hi(q.w), hv[q.y >> 16], acc);
+    }
+  };
+  // coarse columns [0, Hh)
+  auto phase_c = [&]() {
+    acc = 0.0f;
+    if (cw) mac(0, NRC);
+  };
+  // fine columns [Hh, H); then the SL lanes of a row add up and the first publishes
+  auto phase_f = [&](uint32_t tag, float cbv) {
+    if (!cw) return;
+    mac(NRC, NRF);
+    float v = acc;
+    for (int m = 1; m < SL; m <<= 1) v += __shfl_xor(v, m);
+    if (lead) xpub(dst, tag, g < 2 ? v + cbv : v);   // bias + conditioning of the u and r gates
+  };
+  __builtin_amdgcn_s_waitcnt(0);   // records and h are in before the loop (see head_role)
+  phase_c();
+  phase_f(1u, lead && g < 2 ? cb_row(a, a.t0)[row] : 0.0f);
+  const u64* YC = a.xc + P.x_yc;
+  const u64* YF = a.xc + P.x_yf;
+  // Wait for a half of h: lane jj of wave 4 watches the last word of head
+  // jj's slice, then waves 4-7 read every word once into hv.
+  auto gather_half = [&](const u64* Y, uint32_t tag, float* out, bool flags) {
+    if (flags) {
+      if (wave == 4) {
+        float y;
+        const int hj = lane < P.NK ? lane : 0;
+        if (!poll_sleepy(Y + P.HR * hj + P.HR - 1, tag, &y, a)) misc[0] = 1;
+      }
+      __syncthreads();
+      if (misc[0]) return;
+    }
+    if (!cw) {
+      constexpr int MW = 8;                       // Hh <= 2048
+      const int r = tid - 256;
+      uint32_t pending = 0;
+      float y[MW];
+#pragma unroll
+      for (int m = 0; m < MW; ++m) {
+        y[m] = 0.0f;
+        if (r + 256 * m < Hh) pending |= 1u << m;
+      }
+      WaitBudget wb{wr_clock(), 0};
+      while (pending) {
+        u64 w[MW];
+#pragma unroll
+        for (int m = 0; m < MW; ++m) w[m] = (pending >> m & 1u) ? xpeek(Y + r + 256 * m) : 0;
+#pragma unroll
+        for (int m = 0; m < MW; ++m)
+          if ((pending >> m & 1u) && xtag(w[m]) == tag) {
+            y[m] = xval(w[m]);
+            pending &= ~(1u << m);
+          }
+        if (pending && !wait_ok(wb, a.err, a.limit, a.err)) {
+          misc[0] = 1;
+          break;
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < MW; ++m)
+        if (r + 256 * m < Hh) out[r + 256 * m] = y[m];
+    }
+    __syncthreads();
+  };
+  for (int64_t t = 0; t + 1 < a.T; ++t) {
+    const uint32_t tag = (uint32_t)(t + 1);
+    const float cbv = lead && g < 2 ? cb_row(a, a.t0 + t + 1)[row] : 0.0f;
+    gather_half(YC, tag, hv, true);
+    if (misc[0]) return;
+    phase_c();
+    gather_half(YF, tag, hv + Hh, false);
+    if (misc[0]) return;
+    if (k == 0 && tid == 0) trace_at(a, t + 1, 11);
+    phase_f(tag + 1, cbv);
+    if (k == 0 && tid == 0) trace_at(a, t + 1, 12);
+  }
+}
+
+template <int KH, int GU>
+__global__ __launch_bounds__(WR_THREADS, 1) void wr_sparse_kernel(PersistArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int r = wr_role(a.P, blockIdx.x);
+  if (r < 0) return;
+  if (r < a.P.NH) head_role<KH, 4, GU, true>(a, r, lds);
+  else sparse_unit_role(a, r - a.P.NH, lds);
 }
 
 // Bias + conditioning of every gate row for every frame of every stream
@@ -497,6 +754,17 @@ const void* wr_persist_kernel_ptr(int KH) {
     case 3: return (const void*)wr_persist_kernel<3>;
     case 4: return (const void*)wr_persist_kernel<4>;
     case 7: return (const void*)wr_persist_kernel<7>;
+    default: return nullptr;
+  }
+}
+const void* wr_sparse_kernel_ptr(int KH, int GU) {
+  switch (KH * 4 + GU) {
+    case 1 * 4 + 1: return (const void*)wr_sparse_kernel<1, 1>;
+    case 2 * 4 + 1: return (const void*)wr_sparse_kernel<2, 1>;
+    case 4 * 4 + 1: return (const void*)wr_sparse_kernel<4, 1>;
+    case 7 * 4 + 1: return (const void*)wr_sparse_kernel<7, 1>;
+    case 8 * 4 + 2: return (const void*)wr_sparse_kernel<8, 2>;
+    case 16 * 4 + 3: return (const void*)wr_sparse_kernel<16, 3>;
     default: return nullptr;
   }
 }

@@ -293,3 +293,99 @@ def test_invalid_calls_return_errors_without_launching():
     with pytest.raises(wavernn.WaveRNNError):
         mc.sample(500, cond=cuda(synth.features(1, 100, cond_dim=4)))   # too few frames
     assert host(m.sample(0)).shape == (1, 0)
+
+
+# ------------------------------------------------------------- block-sparse R
+
+_FMT = {(4, 4): "bsr4x4", (16, 1): "bsr16x1"}
+
+
+@pytest.mark.parametrize("H,block,density", [(128, (4, 4), 0.25), (256, (16, 1), 0.1), (256, (4, 4), 0.04)])
+def test_block_sparse_teacher_forced_small_sizes(H, block, density):
+    """Sparse WaveRNN (Sec. 3.2): R kept in 4x4 or 16x1 blocks; the oracle runs
+    the dense R with the pruned blocks zero."""
+    w = synth.make_weights(H, seed=8, cond_dim=16, block=block, density=density)
+    m, r, ref = _tf_compare_fmt(w, 300, _FMT[block], cond_dim=16)
+    assert m.path()[0] == "block-sparse"
+    dc = np.abs(r["zc"] - ref["zc"]).max()
+    df = np.abs(r["zf"] - ref["zf"]).max()
+    assert dc <= 1e-3 and df <= 1e-3, (dc, df)
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
+
+
+def _tf_compare_fmt(w, T, fmt, S=1, cond_dim=0):
+    feat = synth.features(S, T, cond_dim=cond_dim, per_stream_seed=True) if cond_dim else None
+    tgt = _targets(S, T)
+    m = wavernn.Model(w, dtype="bf16", r_format=fmt, max_streams=S)
+    r = m.score(cuda(tgt), cond=None if feat is None else cuda(feat))
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, T, feat=feat, target=tgt, logits=True, nll=True)
+    return m, {k: host(v) for k, v in r.items()}, ref
+
+
+def test_block_sparse_all_blocks_kept_matches_dense_kernel():
+    """With every block kept the block-sparse kernel computes the dense model:
+    its logits agree with the dense persistent kernel's and the oracle's."""
+    w = synth.make_weights(256, seed=9, cond_dim=16, block=(4, 4), density=1.0)
+    assert w["mask"].all()
+    T = 240
+    m, r, ref = _tf_compare_fmt(w, T, "bsr4x4", cond_dim=16)
+    assert m.path()[0] == "block-sparse"
+    feat = synth.features(1, T, cond_dim=16, per_stream_seed=True)
+    md = wavernn.Model(w, dtype="bf16")
+    assert md.path()[0] == "persistent"
+    rd = {k: host(v) for k, v in md.score(cuda(_targets(1, T)), cond=cuda(feat)).items()}
+    md.device_status()
+    for k in ("zc", "zf"):
+        assert np.abs(r[k] - ref[k]).max() <= 1e-3
+        assert np.abs(r[k] - rd[k]).max() <= 1e-3
+
+
+@pytest.mark.parametrize("name,T", [("sparse2048_4x4", 240), ("sparse2048_16x1", 120)])
+def test_sparse2048_teacher_forced_within_bf16_tolerance(name, T):
+    w = synth.preset(name)
+    m, r, ref = _tf_compare_fmt(w, T, _FMT[w["block"]], cond_dim=64)
+    assert m.path()[0] == "block-sparse"
+    d = max(np.abs(r["zc"] - ref["zc"]).max(), np.abs(r["zf"] - ref["zf"]).max())
+    assert d <= BF16_TOL, d
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
+
+
+def test_sparse2048_free_running_draws_are_valid():
+    w = synth.preset("sparse2048_4x4")
+    T = 480
+    feat = synth.features(1, T)
+    m = wavernn.Model(w, dtype="bf16", r_format="bsr4x4")
+    out = host(m.sample(T, cond=cuda(feat), seed=1))
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, T, feat=feat, target=out, logits=True)
+    u = np.array([O.uniforms(1, 0, t) for t in range(T)])
+    c, f = out[0] >> 8, out[0] & 255
+    okc = _check_draws_valid(ref["zc"][0], u[:, 0], c, 1e-3)
+    okf = _check_draws_valid(ref["zf"][0], u[:, 1], f, 1e-3)
+    assert okc.all() and okf.all(), (np.flatnonzero(~okc)[:10], np.flatnonzero(~okf)[:10])
+    assert len(np.unique(out)) > 50
+
+
+def test_block_sparse_streams_and_chunks():
+    """Two utterances (one launch each) sampled in two chained calls equal one
+    call, and the final state matches."""
+    w = synth.make_weights(256, seed=10, cond_dim=8, block=(16, 1), density=0.1)
+    S, T = 2, 500
+    feat = synth.features(S, T, cond_dim=8, per_stream_seed=True)
+    m = wavernn.Model(w, dtype="bf16", r_format="bsr16x1", max_streams=S)
+    assert m.path(S)[0] == "block-sparse"
+    fin = m.new_state(S)
+    whole = host(m.sample(T, cond=cuda(feat), seed=4, n_streams=S, final=fin))
+    st = m.new_state(S)
+    a = host(m.sample(320, cond=cuda(feat), seed=4, n_streams=S, final=st))
+    b = host(m.sample(180, cond=cuda(feat), seed=4, n_streams=S, init=st, final=st))
+    m.device_status()
+    np.testing.assert_array_equal(np.concatenate([a, b], axis=1), whole)
+    np.testing.assert_array_equal(host(st["h"]), host(fin["h"]))
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, T, feat=feat, target=whole, logits=True)
+    for s_ in range(S):
+        u = np.array([O.uniforms(4, s_, t) for t in range(T)])
+        okc = _check_draws_valid(ref["zc"][s_], u[:, 0], whole[s_] >> 8, 1e-3)
+        okf = _check_draws_valid(ref["zf"][s_], u[:, 1], whole[s_] & 255, 1e-3)
+        assert okc.all() and okf.all()
