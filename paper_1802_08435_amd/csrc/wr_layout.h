@@ -193,10 +193,11 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
   P->hw_frags = P->KH + 2 * P->KO;
   // head LDS: operand image (KT + KO fragments), first-layer partials
   // [KC][HR], logit sums [2][256], logits [256], then y [Hh] (GU = 1) or
-  // h_c, h_f [2][Hh], prepared terms [5][Hh], I* [Hh][15] (GU > 1), misc [16],
+  // h_c, h_f [2][Hh], prepared terms [5][Hh], fine words [4][Hh], I* [Hh][15]
+  // (GU > 1), misc [16],
   // uniforms [2][64][2], targets [2][64]
   P->lds_h = (P->KT + P->KO) * WR_FRAG +
-             4 * (KC * P->HR + 3 * 256 + (P->GU > 1 ? 22 * P->Hh : P->Hh) + 16 + 256 + 128);
+             4 * (KC * P->HR + 3 * 256 + (P->GU > 1 ? 26 * P->Hh : P->Hh) + 16 + 256 + 128);
   // unit LDS: records, h [H], misc [16]
   P->u_lds_w = (NRC + NRF) * 256 * 16;
   P->lds_u = P->u_lds_w + 4 * (H + 16);

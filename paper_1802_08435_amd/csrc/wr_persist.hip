@@ -34,7 +34,8 @@ __device__ __forceinline__ const float* cb_row(const PersistArgs& a, int64_t n) 
 // of both output MLPs; with SPLIT heads j < NK hold slice j of the coarse MLP
 // (O1, O2) and heads NK + j slice j of the fine MLP (O3, O4), half the
 // registers each.
-// Every head evaluates every gate (Eq. 2) and draws both classes.  The work that does not depend on
+// Every head draws both classes and evaluates the gates (Eq. 2) of the halves
+// it serves (both without SPLIT).  The work that does not depend on
 // the class being drawn (reading R h from the units, the I* terms of the known
 // inputs) runs on waves 0-6 while wave 7 draws; the rest follows the draw.
 //  GU = 1 (Hh <= 448): thread u < Hh owns coarse unit u and fine unit Hh + u,
@@ -73,7 +74,8 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   float* yv = zk + 256;                            // [Hh] (GU = 1) this half of h; (wide) h_c
   float* hfv = yv + Hh;                            // wide: [Hh] h_f
   float* pre = hfv + Hh;                           // wide: [5][Hh] prepared gate terms
-  float* iws = pre + 5 * Hh;                       // wide: [Hh][15] I* of coarse (2) and fine (3) columns
+  float* prf = pre + 5 * Hh;                       // wide: [4][Hh] fine words (u, r, e) and conditioning
+  float* iws = prf + 4 * Hh;                       // wide: [Hh][15] I* of coarse (2) and fine (3) columns
   int* misc = (int*)(WIDE ? iws + 15 * Hh : yv + Hh);   // [0] abort [1] c_t [2] c_prev [3] f_prev
   float* fmisc = (float*)(misc + 8);               // [2] lse_c [3] z_c[c]
   float2* uni = (float2*)(misc + 16);              // [2][64] (u_c, u_f) of a batch of 64 steps
@@ -158,13 +160,13 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   u64 pc[3] = {0, 0, 0}, pf[3] = {0, 0, 0};
   float cbe_c = 0.0f, cbe_f = 0.0f;
   auto prefetch_coarse = [&](int64_t n) {
-    if (!WIDE && gate) {
+    if (!WIDE && gate && coarse) {
       pc[0] = xpeek(GA + u); pc[1] = xpeek(GA + Hh + u); pc[2] = xpeek(GA + 2 * Hh + u);
       cbe_c = cb_row(a, n)[2 * H + u];
     }
   };
   auto prefetch_fine = [&](int64_t n) {
-    if (!WIDE && gate) {
+    if (!WIDE && gate && fine) {
       pf[0] = xpeek(GF + u); pf[1] = xpeek(GF + Hh + u); pf[2] = xpeek(GF + 2 * Hh + u);
       cbe_f = cb_row(a, n)[2 * H + Hh + u];
     }
@@ -225,22 +227,51 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   prefetch_coarse(a.t0);
   prefetch_fine(a.t0);
   const bool trw = j == 0 && tid == WR_THREADS - 64;       // tracing thread (draw wave)
-  // wide: wait for the words of gate block G (3 gates x Hh) of units tid + 448 m
-  // and call f(v, m, unit) for each (all loads issued at once)
-  auto wide_words = [&](const u64* G, uint32_t tag, auto&& f) -> bool {
+  // wide: the units publish a step's coarse and fine words together, so both
+  // are read at once (one round trip) with the conditioning of the e gates:
+  // coarse terms into pre, the fine words and conditioning into prf
+  // Word k of a thread: half k / (3 GU) (GA, GF), slot m = k / 3 % GU, gate
+  // k % 3; its value lands in LDS (pre rows 0-2 or prf rows 0-2) as it arrives.
+  auto wide_words = [&](uint32_t tag, float x0, int64_t n) -> bool {
     if (wave == DW) return true;
-    const u64* ps[3 * GU];
-    const u64 none[3 * GU] = {};
-    float v[3 * GU];
+    constexpr int NW = 6 * GU;
+    const float* cbr = cb_row(a, n) + 2 * H;
+    int un[GU];
+    float cbc[GU], cbf[GU];
 #pragma unroll
-    for (int k = 0; k < 3 * GU; ++k) {
-      const int m = k / 3, un = tid + 448 * m;
-      ps[k] = G + (k % 3) * Hh + (un < Hh ? un : tid);
+    for (int m = 0; m < GU; ++m) {
+      un[m] = tid + 448 * m < Hh ? tid + 448 * m : tid;
+      cbc[m] = cbr[un[m]];
+      cbf[m] = cbr[Hh + un[m]];
     }
-    if (!poll_pref<3 * GU>(ps, none, tag, v, a)) return false;
+    // with split MLPs a head reads only the half it evaluates
+    uint32_t pending = (coarse ? (1u << 3 * GU) - 1 : 0u) | (fine ? ((1u << 3 * GU) - 1) << 3 * GU : 0u);
+    WaitBudget wb{wr_clock(), 0};
+    for (;;) {
+      u64 x[NW];
 #pragma unroll
-    for (int m = 0; m < GU; ++m)
-      if (tid + 448 * m < Hh) f(v + 3 * m, tid + 448 * m);
+      for (int k = 0; k < NW; ++k)
+        x[k] = (pending >> k & 1u) ? xpeek((k < 3 * GU ? GA : GF) + (k % 3) * Hh + un[k / 3 % GU]) : 0;
+#pragma unroll
+      for (int k = 0; k < NW; ++k)
+        if ((pending >> k & 1u) && xtag(x[k]) == tag) {
+          (k < 3 * GU ? pre : prf)[(k % 3) * Hh + un[k / 3 % GU]] = xval(x[k]);
+          pending &= ~(1u << k);
+        }
+      if (!pending) break;
+      if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+    }
+#pragma unroll
+    for (int m = 0; m < GU; ++m) {
+      if (tid + 448 * m >= Hh) continue;
+      const int v = un[m];
+      const float* iv = iws + 15 * v;
+      pre[v] = pre[v] + iv[0] * x0;
+      pre[Hh + v] = pre[Hh + v] + iv[5] * x0;
+      pre[3 * Hh + v] = iv[10] * x0;
+      pre[4 * Hh + v] = cbc[m];
+      prf[3 * Hh + v] = cbf[m];
+    }
     return true;
   };
   float cu = 0.0f, cr = 0.0f, ce = 0.0f, cie = 0.0f;       // GU = 1, coarse: before f_{t-1} is known
@@ -248,19 +279,10 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   // coarse gate terms known before f_{t-1} (n: the step's sample index)
   auto coarse_pre = [&](uint32_t tag, float x0, int64_t n) {
     if (WIDE) {
-      const float* cbr = cb_row(a, n) + 2 * H;
-      if (!wide_words(GA, tag, [&](const float* v, int un) {
-            const float* iv = iws + 15 * un;
-            pre[un] = v[0] + iv[0] * x0;
-            pre[Hh + un] = v[1] + iv[5] * x0;
-            pre[2 * Hh + un] = v[2];
-            pre[3 * Hh + un] = iv[10] * x0;
-            pre[4 * Hh + un] = cbr[un];
-          }))
-        misc[0] = 1;
+      if (!wide_words(tag, x0, n)) misc[0] = 1;
       return;
     }
-    if (!gate) return;
+    if (!gate || !coarse) return;
     const u64* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
     float v[3];
     if (!poll_pref<3>(ps, pc, tag, v, a)) {
@@ -273,20 +295,19 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     cie = ic[2][0] * x0;
   };
   auto fine_pre = [&](uint32_t tag, float x0, float x1, int64_t n) {
-    if (WIDE) {
-      const float* cbr = cb_row(a, n) + 2 * H + Hh;
-      if (!wide_words(GF, tag, [&](const float* v, int un) {
-            const float* iv = iws + 15 * un;
-            pre[un] = v[0] + __builtin_fmaf(iv[3], x1, iv[2] * x0);
-            pre[Hh + un] = v[1] + __builtin_fmaf(iv[8], x1, iv[7] * x0);
-            pre[2 * Hh + un] = v[2];
-            pre[3 * Hh + un] = __builtin_fmaf(iv[13], x1, iv[12] * x0);
-            pre[4 * Hh + un] = cbr[un];
-          }))
-        misc[0] = 1;
+    if (WIDE) {   // from the words read with the coarse ones (LDS only)
+      if (!fine) return;
+      for (int un = tid; un < Hh; un += 448) {
+        const float* iv = iws + 15 * un;
+        pre[un] = prf[un] + __builtin_fmaf(iv[3], x1, iv[2] * x0);
+        pre[Hh + un] = prf[Hh + un] + __builtin_fmaf(iv[8], x1, iv[7] * x0);
+        pre[2 * Hh + un] = prf[2 * Hh + un];
+        pre[3 * Hh + un] = __builtin_fmaf(iv[13], x1, iv[12] * x0);
+        pre[4 * Hh + un] = prf[3 * Hh + un];
+      }
       return;
     }
-    if (!gate) return;
+    if (!gate || !fine) return;
     const u64* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
     float v[3];
     if (!poll_pref<3>(ps, pf, tag, v, a)) {
@@ -300,7 +321,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   };
   // wide: finish the gates of units tid + 512 m with the drawn input x (I*
   // column q of the row) into h (LDS) and the operand image
-  auto wide_gates = [&](float x, int q, float* h, unsigned char* img, bool to_img) {
+  auto wide_gates = [&](float x, int q, float* h, unsigned char* img) {
 #pragma unroll
     for (int m = 0; m < (Hh + WR_THREADS - 1) / WR_THREADS; ++m) {
       const int un = tid + WR_THREADS * m;
@@ -311,7 +332,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       const float e = ftanh(__builtin_fmaf(rr, pre[2 * Hh + un], __builtin_fmaf(iv[10 + q], x, pre[3 * Hh + un]) + pre[4 * Hh + un]));
       const float hn = __builtin_fmaf(uu, h[un], (1.0f - uu) * e);
       h[un] = hn;
-      if (to_img) aput(img + (un >> 5) * WR_FRAG, un & 31, hn);
+      aput(img + (un >> 5) * WR_FRAG, un & 31, hn);
     }
   };
   coarse_pre(1u, fscale(misc[2]), a.t0);
@@ -329,13 +350,13 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (wave == DW && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
     // (1) coarse gates of every unit, finished with f_{t-1}
     if (WIDE) {
-      wide_gates(fscale(misc[3]), 1, yv, imc, coarse);
-    } else if (gate) {
+      if (coarse) wide_gates(fscale(misc[3]), 1, yv, imc);
+    } else if (gate && coarse) {
       const float x1 = fscale(misc[3]);
       const float uu = fsig(__builtin_fmaf(ic[0][1], x1, cu)), rr = fsig(__builtin_fmaf(ic[1][1], x1, cr));
       const float e = ftanh(__builtin_fmaf(rr, ce, __builtin_fmaf(ic[2][1], x1, cie) + cbe_c));
       hc = __builtin_fmaf(uu, hc, (1.0f - uu) * e);
-      if (coarse) aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
+      aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
       yv[u] = hc;
     }
     __syncthreads();
@@ -349,9 +370,10 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       if (trw) trace_at(a, t, 3);
     }
     if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 13);
-    if (j > 0 && NH <= 8 && tid == WR_THREADS - 64) trace_at(a, t, 24 + j);
+    if (j > 0 && j < 8 && tid == WR_THREADS - 64) trace_at(a, t, 24 + j);
     // (3) coarse logits of all heads; this step's fine words are loaded
     gather_logits(PC, tag);
+    if (trw) trace_at(a, t, 15);
     if (t > 0) prefetch_fine(n);
     __syncthreads();
     if (misc[0]) return;
@@ -361,6 +383,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       float lse;
       const int forced = a.target ? (tgt[bs] >> 8) : -1;
       const int c = draw_wave(zs, zs2, b2l, uni[bs].x, forced, zk, a.nll_out ? &lse : nullptr);
+      if (trw) trace_at(a, t, 16);
       if (j == 0 && a.zc_out) *(float4*)(a.zc_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {
         misc[1] = c;
@@ -378,13 +401,13 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     // (5) fine gates of every unit, finished with c_t (c_t reaches the fine half only)
     const int c = misc[1];
     if (WIDE) {
-      wide_gates(fscale(c), 4, hfv, imf, fine);
-    } else if (gate) {
+      if (fine) wide_gates(fscale(c), 4, hfv, imf);
+    } else if (gate && fine) {
       const float x2 = fscale(c);
       const float uu = fsig(__builtin_fmaf(ifn[0][2], x2, fu)), rr = fsig(__builtin_fmaf(ifn[1][2], x2, fr));
       const float e = ftanh(__builtin_fmaf(rr, fe, __builtin_fmaf(ifn[2][2], x2, fie) + cbe_f));
       hf = __builtin_fmaf(uu, hf, (1.0f - uu) * e);
-      if (fine) aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
+      aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
       yv[u] = hf;
     }
     __syncthreads();
@@ -405,6 +428,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 14);
     // (7) fine logits of all heads; next step's coarse words are loaded
     gather_logits(PF, tag);
+    if (trw) trace_at(a, t, 17);
     if (t + 1 < a.T) prefetch_coarse(n + 1);
     __syncthreads();
     if (misc[0]) return;
@@ -414,6 +438,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       float lse;
       const int forced = a.target ? (tgt[bs] & 255) : -1;
       const int f = draw_wave(zs, zs2, b4l, uni[bs].y, forced, zk, a.nll_out ? &lse : nullptr);
+      if (trw) trace_at(a, t, 18);
       if (j == 0 && a.zf_out) *(float4*)(a.zf_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {
         if (j == 0) {
@@ -430,17 +455,19 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (misc[0]) return;
     if (trw) trace_at(a, t, 10);
   }
-  if (j == 0) {
+  // final state: head 0 writes the halves it evaluated, head NK the fine half with split MLPs
+  if (a.h_out && (j == 0 || (SPLIT && j == NK))) {
     if (WIDE) {
-      if (a.h_out)
-        for (int v = tid; v < Hh; v += WR_THREADS) {
-          a.h_out[v] = yv[v];
-          a.h_out[Hh + v] = hfv[v];
-        }
-    } else if (a.h_out && gate) {
-      a.h_out[u] = hc;
-      a.h_out[Hh + u] = hf;
+      for (int v = tid; v < Hh; v += WR_THREADS) {
+        if (coarse) a.h_out[v] = yv[v];
+        if (fine) a.h_out[Hh + v] = hfv[v];
+      }
+    } else if (gate) {
+      if (coarse) a.h_out[u] = hc;
+      if (fine) a.h_out[Hh + u] = hf;
     }
+  }
+  if (j == 0) {
     if (tid == 0) {
       if (a.c_out) a.c_out[0] = (uint8_t)misc[2];
       if (a.f_out) a.f_out[0] = (uint8_t)misc[3];
