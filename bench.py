@@ -130,6 +130,8 @@ def main() -> int:
     wall = time.perf_counter() - t0
     m.device_status()
     call_ms = [a.elapsed_time(b) for a, b in evs]
+    # synchronization floor: the same grid and exchanged words per step, no arithmetic
+    floor_us = m.sync_floor(T // w["B"]) if path in ("persistent", "block-sparse") else None
     ms = float(np.mean(call_ms))
     samples = S * T
     value = samples * args.steps / wall
@@ -152,13 +154,15 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": round(value / PAPER_SAMPLES_PER_S, 3) if args.config == "dense896" else None,
-        "dtype": "f32",
+        "dtype": "bf16" if w["bf16"] else "f32",
         "data": "synthetic (seeded N(0,1/fan_in) weights, N(0,1) conditioning frames)",
         "config": {"workload": f"{args.config}: H={w['H']}, B={w['B']}, {S} utterance(s) x {T} samples",
                    "weights": "bf16" if w["bf16"] else "f32", "kernel": path, "grid": grid, "block": block},
         "us_per_sample": round(us_per_sample_step, 4),
         "x_realtime": round(value / 24000.0, 3),
         "call_ms_min": round(min(call_ms), 4),
+        "sync_floor": None if floor_us is None else {
+            "us_per_step": round(floor_us, 4), "frac_of_step": round(floor_us / us_per_sample_step, 4)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": traffic,
                      "kernel": path, "bytes_per_step": wb, "steps_per_launch": steps_per_launch,

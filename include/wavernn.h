@@ -158,6 +158,17 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
  * ignore the setting. */
 wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps);
 
+/* Diagnostics: the synchronization floor of the model's persistent kernel
+ * (paths 1 and 3 of wavernn_model_path).  Runs n_steps (>= 2) steps of a
+ * kernel with the same grid, workgroup roles and exchanged words per step as
+ * the sampling kernel but no arithmetic (the per-step synchronization cost
+ * the paper discusses in Sec. 5.1), waits for it on `stream`, and writes its
+ * mean time per step in microseconds to *us_per_step (host memory).  Uses the
+ * model's exchange buffer: calls on other streams must not overlap it.
+ * Errors: E_INVALID (arguments), E_UNSUPPORTED (other paths), E_HIP,
+ * E_DEVICE (a bounded wait expired). */
+wavernn_status wavernn_debug_sync_floor(wavernn_model* m, int64_t n_steps, double* us_per_step, void* stream);
+
 /* Description of the last error on this thread ("" if none). */
 const char* wavernn_last_error(void);
 

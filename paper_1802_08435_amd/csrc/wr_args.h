@@ -105,3 +105,4 @@ const void* wr_sparse_kernel_ptr(int KH, int GU);   // null if no instantiation
 const void* wr_cond_kernel_ptr();
 const void* wr_batch_kernel_ptr(int KH, bool ctx);   // null if no instantiation for KH
 const void* wr_fill_kernel_ptr();
+const void* wr_floor_kernel_ptr();

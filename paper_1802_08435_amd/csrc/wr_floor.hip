@@ -1,0 +1,149 @@
+// Synchronization floor of the persistent kernels: the same grid, roles and
+// exchanged words per step as the batch-1 kernel of a plan (dense or
+// block-sparse), with no arithmetic.  Per step and half each head publishes
+// its slice of y and 256 partial logits and waits for the partials of every
+// slice (the two all-reduces on the critical path of a step); it also reads
+// the gate words of the half(s) it serves, without waiting, as the sampling
+// kernel reads them ahead.  Each unit workgroup reads both halves of h from
+// the heads and publishes its gate words for the next step.  The time per
+// step of this kernel is what the exchange pattern alone costs (Sec. 5.1 of
+// the paper counts such a synchronization cost per step).
+#include "wr_kern.h"
+
+namespace {
+
+__device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned char* lds) {
+  const PersistPlan& P = a.P;
+  const int Hh = P.Hh, NK = P.NK, HR = P.HR;
+  const bool split = P.NH == 2 * NK;
+  const bool coarse = !split || j < NK, fine = !split || j >= NK;
+  const int jk = split ? j % NK : j;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  int* misc = (int*)lds;
+  float* zs = (float*)(misc + 16);               // [2][256] logit sums (written, never read)
+  const u64* GA = a.xc + P.x_ga;
+  const u64* GF = a.xc + P.x_gf;
+  u64* YC = a.xc + P.x_yc;
+  u64* YF = a.xc + P.x_yf;
+  u64* PC = a.xc + P.x_pc;
+  u64* PF = a.xc + P.x_pf;
+  if (tid == 0) misc[0] = 0;
+  __syncthreads();
+  // gate words of every unit of a half (3 per unit), read once without waiting
+  float* gsink = zs + 512;                       // [WR_THREADS]
+  auto gate_words = [&](const u64* G) {
+    float acc = 0.0f;
+    for (int u = tid; u < Hh; u += WR_THREADS)
+      acc += xval(xpeek(G + u)) + xval(xpeek(G + Hh + u)) + xval(xpeek(G + 2 * Hh + u));
+    gsink[tid] = acc;
+  };
+  // partials of all NK slices, read as the sampling kernel reads them: wave 0
+  // waits for the last word of every slice, then thread (v, half) reads its
+  // half of the slices
+  auto gather = [&](const u64* src, uint32_t tag) {
+    if (wave == 0) {
+      float y;
+      const int jj = lane < NK ? lane : 0;
+      if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + 255, tag, &y, a)) misc[0] = 1;
+    }
+    __syncthreads();
+    if (misc[0]) return;
+    const int v = tid & 255, hh = tid >> 8, h0 = (NK + 1) / 2;
+    float s;
+    if (!sum_parts<16>(src, P.x_ps, hh ? h0 : 0, hh ? NK : h0, v, tag, &s, a)) misc[0] = 1;
+    else zs[hh * 256 + v] = s;
+  };
+  for (int64_t t = 0; t < a.T; ++t) {
+    const uint32_t tag = (uint32_t)(t + 1);
+    if (coarse) gate_words(GA);
+    if (coarse && wave == 7 && lane < HR) xpub(YC + HR * jk + lane, tag, 0.0f);
+    if (coarse && lane < 32) xpub(PC + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
+    gather(PC, tag);
+    __syncthreads();
+    if (misc[0]) return;
+    if (fine) gate_words(GF);
+    if (fine && wave == 7 && lane < HR) xpub(YF + HR * jk + lane, tag, 0.0f);
+    if (fine && lane < 32) xpub(PF + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
+    gather(PF, tag);
+    __syncthreads();
+    if (misc[0]) return;
+  }
+}
+
+__device__ __forceinline__ void floor_unit(const PersistArgs& a, int k, unsigned char* lds) {
+  const PersistPlan& P = a.P;
+  const int Hh = P.Hh, NK = P.NK, HR = P.HR;
+  const int wpu = 3 * Hh / P.NU;                 // gate words of each half this unit publishes
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  int* misc = (int*)lds;
+  float* hv = (float*)(misc + 16);               // [Hh] (written, never read)
+  u64* GA = a.xc + P.x_ga + (size_t)k * wpu;
+  u64* GF = a.xc + P.x_gf + (size_t)k * wpu;
+  const u64* YC = a.xc + P.x_yc;
+  const u64* YF = a.xc + P.x_yf;
+  if (tid == 0) misc[0] = 0;
+  __syncthreads();
+  auto publish = [&](uint32_t tag) {
+    if (tid < wpu) {
+      xpub(GA + tid, tag, 0.0f);
+      xpub(GF + tid, tag, 0.0f);
+    }
+  };
+  auto gather_half = [&](const u64* Y, uint32_t tag, bool flags) {
+    if (flags) {
+      if (wave == 4) {
+        float y;
+        const int hj = lane < NK ? lane : 0;
+        if (!poll_sleepy(Y + HR * hj + HR - 1, tag, &y, a)) misc[0] = 1;
+      }
+      __syncthreads();
+      if (misc[0]) return;
+    }
+    if (tid >= 256) {                            // all of a lane's words in flight at once
+      constexpr int MW = 8;                      // Hh <= 2048
+      const int r = tid - 256;
+      uint32_t pending = 0;
+#pragma unroll
+      for (int m = 0; m < MW; ++m)
+        if (r + 256 * m < Hh) pending |= 1u << m;
+      WaitBudget wb{wr_clock(), 0};
+      while (pending) {
+        u64 x[MW];
+#pragma unroll
+        for (int m = 0; m < MW; ++m) x[m] = (pending >> m & 1u) ? xpeek(Y + r + 256 * m) : 0;
+#pragma unroll
+        for (int m = 0; m < MW; ++m)
+          if ((pending >> m & 1u) && xtag(x[m]) == tag) {
+            hv[r + 256 * m] = xval(x[m]);
+            pending &= ~(1u << m);
+          }
+        if (pending && !wait_ok(wb, a.err, a.limit, a.err)) {
+          misc[0] = 1;
+          break;
+        }
+      }
+    }
+    __syncthreads();
+  };
+  publish(1u);
+  for (int64_t t = 0; t + 1 < a.T; ++t) {
+    const uint32_t tag = (uint32_t)(t + 1);
+    gather_half(YC, tag, true);
+    if (misc[0]) return;
+    gather_half(YF, tag, false);
+    if (misc[0]) return;
+    publish(tag + 1);
+  }
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(WR_THREADS, 1) void wr_floor_kernel(PersistArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int r = wr_role(a.P, blockIdx.x);
+  if (r < 0) return;
+  if (r < a.P.NH) floor_head(a, r, lds);
+  else floor_unit(a, r - a.P.NH, lds);
+}
+
+const void* wr_floor_kernel_ptr() { return (const void*)wr_floor_kernel; }

@@ -821,6 +821,41 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
   return (int32_t)path;
 }
 
+wavernn_status wavernn_debug_sync_floor(wavernn_model* m, int64_t n_steps, double* us_per_step, void* stream) {
+  if (!m || n_steps < 2 || n_steps > ((int64_t)1 << 31) || !us_per_step)
+    return fail(WAVERNN_E_INVALID, "bad sync-floor arguments");
+  if (m->path != PATH_PERSIST) return fail(WAVERNN_E_UNSUPPORTED, "the sync floor exists for the persistent kernels only");
+  const PersistPlan& P = m->plan;
+  if ((3 * P.Hh) % P.NU) return fail(WAVERNN_E_UNSUPPORTED, "gate words do not split evenly over the units");
+  hipStream_t st = (hipStream_t)stream;
+  const void* k = wr_floor_kernel_ptr();
+  wavernn_status s = check_coresident(m, k, P.grid, P.lds, "sync-floor");
+  if (s != WAVERNN_OK) return s;
+  if ((s = launch_fill(m->d_xc, P.x_words, st)) != WAVERNN_OK) return s;
+  PersistArgs a;
+  memset(&a, 0, sizeof a);
+  a.P = P;
+  a.T = n_steps;
+  a.xc = m->d_xc;
+  a.err = m->d_err;
+  a.limit = kWaitTicks;
+  void* args[] = {&a};
+  hipEvent_t e0, e1;
+  HIPOK(hipEventCreate(&e0));
+  HIPOK(hipEventCreate(&e1));
+  hipError_t he = hipEventRecord(e0, st);
+  if (he == hipSuccess) he = hipLaunchKernel(k, dim3(P.grid), dim3(WR_THREADS), args, P.lds, st);
+  if (he == hipSuccess) he = hipEventRecord(e1, st);
+  if (he == hipSuccess) he = hipEventSynchronize(e1);
+  float ms = 0.0f;
+  if (he == hipSuccess) he = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (he != hipSuccess) return fail(WAVERNN_E_HIP, "sync floor: %s", hipGetErrorString(he));
+  *us_per_step = (double)ms * 1000.0 / (double)n_steps;
+  return wavernn_device_status(m, stream);
+}
+
 wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps) {
   if (!m || max_steps < 0 || (max_steps > 0 && !trace_dev)) return fail(WAVERNN_E_INVALID, "bad trace arguments");
   m->trace = max_steps > 0 ? (u64*)trace_dev : nullptr;

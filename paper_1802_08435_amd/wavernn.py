@@ -67,6 +67,8 @@ def lib():
         L.wavernn_debug_uniforms.argtypes = [u64, u64, i64, i64, vp, vp]
         L.wavernn_set_trace.restype = ctypes.c_int
         L.wavernn_set_trace.argtypes = [vp, vp, i64]
+        L.wavernn_debug_sync_floor.restype = ctypes.c_int
+        L.wavernn_debug_sync_floor.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_double), vp]
         L.wavernn_model_path.restype = i32
         L.wavernn_model_path.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.wavernn_last_error.restype = ctypes.c_char_p
@@ -198,6 +200,13 @@ class Model:
 
     def device_status(self, stream=None):
         _check(lib().wavernn_device_status(self._h, _stream(stream)))
+
+    def sync_floor(self, n_steps: int = 20000, stream=None) -> float:
+        """Microseconds per step of the persistent kernel's exchange pattern alone
+        (same grid and exchanged words, no arithmetic); waits for it."""
+        us = ctypes.c_double()
+        _check(lib().wavernn_debug_sync_floor(self._h, n_steps, ctypes.byref(us), _stream(stream)))
+        return us.value
 
 
 def debug_uniforms(seed: int, stream_id: int, t0: int, n: int):

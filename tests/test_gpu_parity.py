@@ -389,3 +389,23 @@ def test_block_sparse_streams_and_chunks():
         okc = _check_draws_valid(ref["zc"][s_], u[:, 0], whole[s_] >> 8, 1e-3)
         okf = _check_draws_valid(ref["zf"][s_], u[:, 1], whole[s_] & 255, 1e-3)
         assert okc.all() and okf.all()
+
+
+@pytest.mark.parametrize("name", ["dense896", "sparse2048_4x4"])
+def test_sync_floor_runs_below_the_step_time(name):
+    """The exchange-only kernel (same grid, same words per step) completes and
+    costs less per step than the sampling kernel it mirrors."""
+    w = synth.preset(name)
+    m = wavernn.Model(w, dtype="bf16", r_format=_FMT.get(w["block"], "dense"))
+    floor = m.sync_floor(3000)
+    T = 3000
+    feat = cuda(synth.features(1, T))
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    m.sample(T, cond=feat, seed=1)
+    e1.record()
+    torch.cuda.synchronize()
+    m.device_status()
+    step = e0.elapsed_time(e1) * 1000.0 / T
+    assert 0.5 < floor < step, (floor, step)
