@@ -35,19 +35,27 @@ def weight_bytes_per_step(w: dict) -> int:
     return n * bytes_per
 
 
+# kernel that serves each path of wavernn_model_path
+KERNEL_OF = {"persistent": "wr_persist_kernel", "block-sparse": "wr_sparse_kernel", "batched": "wr_batch_kernel",
+             "single-workgroup": "wr_small_kernel"}
+
+
 def kernel_source_digest() -> str:
+    """Digest of every kernel and host source of the library (any change voids old counters)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("wr_persist.hip", "wr_device.h", "wr_layout.h", "wr_args.h"):
-        with open(os.path.join(ROOT, "paper_1802_08435_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    d = os.path.join(ROOT, "paper_1802_08435_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch from the committed rocprofv3 --pmc summary of this workload, or None
-    when the kernel sources changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"wr_persist_kernel_{workload}.md")
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary of this kernel and workload,
+    or None when the library sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -141,7 +149,8 @@ def main() -> int:
     achieved = wb * steps_per_launch / (ms / 1000.0) / 1e9
     ncu = grid
     lds_peak = ncu * LDS_BYTES_PER_CLK_CU * CLOCK_GHZ
-    tb = measured_traffic(args.config) if T == w["samples"] and S == w["streams"] else None
+    kname = KERNEL_OF.get(path, path)
+    tb = measured_traffic(kname, args.config) if T == w["samples"] and S == w["streams"] else None
     traffic = None if tb is None else round(tb / (ms / 1000.0) / 1e9, 2)
     line = {
         "metric": METRIC,
@@ -165,7 +174,7 @@ def main() -> int:
             "us_per_step": round(floor_us, 4), "frac_of_step": round(floor_us / us_per_sample_step, 4)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": traffic,
-                     "kernel": path, "bytes_per_step": wb, "steps_per_launch": steps_per_launch,
+                     "kernel": kname, "bytes_per_step": wb, "steps_per_launch": steps_per_launch,
                      "lds_frac": round(achieved / lds_peak, 5)},
     }
     if not args.no_cpu_baseline:
