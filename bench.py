@@ -31,6 +31,8 @@ def weight_bytes_per_step(w: dict) -> int:
     Hh = H // 2
     nR = int((w["R"] != 0).sum()) if w.get("mask") is not None else 3 * H * H
     n = nR + 2 * (Hh * Hh + 256 * Hh)
+    if w.get("Wx") is not None:          # subscale context projection
+        n += int(w["Wx"].size)
     bytes_per = 2 if w.get("bf16", True) else 4
     return n * bytes_per
 
