@@ -317,18 +317,21 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
     const int g = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + r;
     return g * H + (fine ? Hh : 0) + i;
   };
-  std::vector<uint16_t> uw((size_t)P.NU * P.u_lds_w / 2), ur((size_t)P.NU * UCT * KT * 512);
+  // unit k's LDS block: [coarse tiles][KT] then [fine tiles][KT] fragments over
+  // the coarse columns; ur: [coarse tiles | fine tiles][KT] over the fine columns
+  const size_t NT = (size_t)P.NU * UCT;
+  std::vector<uint16_t> uw((size_t)P.NU * P.u_lds_w / 2), ur(2 * NT * KT * 512);
   for (int k = 0; k < P.NU; ++k) {
     uint16_t* d = uw.data() + (size_t)k * P.u_lds_w / 2;
     for (int q = 0; q < UCT; ++q) {
       const int tile = k * UCT + q;
-      for (int kt = 0; kt < KT; ++kt) {
-        frag(d + (size_t)(q * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); }, 32 * kt);
-        frag(ur.data() + ((size_t)tile * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, false, r); },
-             Hh + 32 * kt);
+      for (int fine = 0; fine < 2; ++fine) {
+        auto rows = [&](int r) { return rrow(tile, fine != 0, r); };
+        for (int kt = 0; kt < KT; ++kt) {
+          frag(d + (size_t)(fine * UCT * KT + q * KT + kt) * 512, Rm, rows, 32 * kt);
+          frag(ur.data() + ((fine * NT + tile) * KT + kt) * 512, Rm, rows, Hh + 32 * kt);
+        }
       }
-      for (int kt = 0; kt < 2 * KT; ++kt)
-        frag(d + (size_t)(UCT * KT + q * 2 * KT + kt) * 512, Rm, [&](int r) { return rrow(tile, true, r); }, 32 * kt);
     }
   }
   wavernn_status s;

@@ -129,7 +129,7 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->UCT = 0;
   for (int u = WR_MAXUCT; u >= 1; --u) {
     if (P->NCT % u) continue;
-    int w = 3 * u * P->KT * WR_FRAG;
+    int w = 2 * u * P->KT * WR_FRAG;
     int l = w + 2 * P->KT * WR_FRAG + 4 * 16;
     if (l <= 160 * 1024) { P->UCT = u; P->u_lds_w = w; P->lds_u = l; break; }
   }

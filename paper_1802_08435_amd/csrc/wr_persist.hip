@@ -367,10 +367,12 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       hc = __builtin_fmaf(uu, hc, (1.0f - uu) * e);
       aput(imc + (u >> 5) * WR_FRAG, u & 31, hc);
       yv[u] = hc;
+      if (u - HR * jk < (unsigned)HR) xpub(YC + u, tag, hc);   // this head's slice, for the units
     }
     __syncthreads();
     if (trw) trace_at(a, t, 1);
-    if (coarse && wave == DW && lane < HR) xpub(YC + HR * jk + lane, tag, yv[HR * jk + lane]);   // this head's slice
+    if (WIDE && coarse && wave == DW && lane < HR) xpub(YC + HR * jk + lane, tag, yv[HR * jk + lane]);
+    if (trw) trace_at(a, t, 19);
     // (2) own rows of O1 -> relu -> own columns of O2 -> partial coarse logits
     if (coarse) {
       first_layer(W1, imc, b1r);
@@ -418,10 +420,12 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       hf = __builtin_fmaf(uu, hf, (1.0f - uu) * e);
       aput(imf + (u >> 5) * WR_FRAG, u & 31, hf);
       yv[u] = hf;
+      if (u - HR * jk < (unsigned)HR) xpub(YF + u, tag, hf);
     }
     __syncthreads();
     if (trw) trace_at(a, t, 6);
-    if (fine && wave == DW && lane < HR) xpub(YF + HR * jk + lane, tag, (WIDE ? hfv : yv)[HR * jk + lane]);
+    if (WIDE && fine && wave == DW && lane < HR) xpub(YF + HR * jk + lane, tag, hfv[HR * jk + lane]);
+    if (trw) trace_at(a, t, 22);
     // (6) own rows of O3 -> relu -> own columns of O4 -> partial fine logits
     if (fine) {
       if (SPLIT) {
@@ -485,9 +489,10 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
 }
 
 // ------------------------------------------------------------------ unit role
-// Wave q < UCT owns coarse row tile k*UCT + q (coarse columns from LDS, fine
-// columns from VGPRs) and publishes its 16 pre-activations as soon as y_f is
-// in; wave 4 + q owns fine row tile k*UCT + q (all columns from LDS).
+// Wave q < UCT owns coarse row tile k*UCT + q and wave 4 + q fine row tile
+// k*UCT + q: coarse columns from LDS (used when y_c arrives), fine columns from
+// VGPRs (used when y_f arrives, so the part on the way to the heads reads no
+// weights from LDS); each publishes its 16 pre-activations once y_f is in.
 template <int KH>
 __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned char* lds) {
   constexpr int KT = 2 * KH;
@@ -495,7 +500,7 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   const int H = P.H, Hh = P.Hh, UCT = P.UCT;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const unsigned char* WC = lds;                                 // [UCT][KT] coarse tiles, coarse columns
-  const unsigned char* WF = lds + UCT * KT * WR_FRAG;            // [UCT][2KT] fine tiles, all columns
+  const unsigned char* WF = lds + UCT * KT * WR_FRAG;            // [UCT][KT] fine tiles, coarse columns
   unsigned char* img = lds + P.u_lds_w;                          // [2KT] operand image of h
   int* misc = (int*)(img + 2 * KT * WR_FRAG);
   const bool cw = wave < UCT, fw = wave >= 4 && wave - 4 < UCT;
@@ -512,8 +517,8 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
     if (tid == 0) misc[0] = 0;
   }
   bf16x8 WR[KT];
-  if (cw) {
-    const uint4* src = a.ur + ((size_t)tile * KT) * 64 + lane;
+  if (cw || fw) {
+    const uint4* src = a.ur + ((size_t)(fw ? P.NU * UCT + tile : tile) * KT) * 64 + lane;
 #pragma unroll
     for (int i = 0; i < KT; ++i) WR[i] = __builtin_bit_cast(bf16x8, src[(size_t)i * 64]);
   }
@@ -528,7 +533,7 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   auto phase_c = [&]() {
     acc0 = f32x4{0, 0, 0, 0};
     acc1 = f32x4{0, 0, 0, 0};
-    const unsigned char* W = cw ? WC + q * KT * WR_FRAG : WF + q * 2 * KT * WR_FRAG;
+    const unsigned char* W = (cw ? WC : WF) + q * KT * WR_FRAG;
     if (cw || fw) {
 #pragma unroll
       for (int i = 0; i < KT; i += 2) {
@@ -539,18 +544,11 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   };
   // columns [KT, 2KT): fine inputs; then publish with `tag`
   auto phase_f = [&](uint32_t tag, float cbv) {
-    if (cw) {
+    if (cw || fw) {
 #pragma unroll
       for (int i = 0; i < KT; i += 2) {
         acc0 = mfma(afrag(img, KT + i), WR[i], acc0);
         if (i + 1 < KT) acc1 = mfma(afrag(img, KT + i + 1), WR[i + 1], acc1);
-      }
-    } else if (fw) {
-      const unsigned char* W = WF + (q * 2 * KT + KT) * WR_FRAG;
-#pragma unroll
-      for (int i = 0; i < KT; i += 2) {
-        acc0 = mfma(afrag(img, KT + i), *(const bf16x8*)(W + i * WR_FRAG + lane * 16), acc0);
-        if (i + 1 < KT) acc1 = mfma(afrag(img, KT + i + 1), *(const bf16x8*)(W + (i + 1) * WR_FRAG + lane * 16), acc1);
       }
     }
     if ((cw || fw) && lane < 16) {
@@ -618,7 +616,9 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
     const float cbv = (cw || fw) && lane < 16 && g < 2 ? cb_row(a, a.t0 + t + 1)[row] : 0.0f;
     gather_half(YC, tag, 0, true);
     if (misc[0]) return;
+    if (k == 0 && tid == 0) trace_at(a, t, 20);
     phase_c();
+    if (k == 0 && tid == 0) trace_at(a, t, 21);
     gather_half(YF, tag, KT, false);   // y_f gates the next coarse step: no flag phase
     if (misc[0]) return;
     if (k == 0 && tid == 0) trace_at(a, t + 1, 11);
