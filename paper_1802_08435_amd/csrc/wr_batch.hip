@@ -67,6 +67,39 @@ __device__ __forceinline__ bool poll_map(F addr, uint32_t tag, float* v, const B
   }
 }
 
+// A pointer the compiler must treat as recomputed here: keeps address
+// arithmetic inside the step loop instead of hoisting dozens of 64-bit
+// addresses into registers for the whole launch.
+template <class T>
+__device__ __forceinline__ T* opaque(T* p) {
+  asm volatile("" : "+v"(p));
+  return p;
+}
+
+// Wait until the N words base + off(k) carry `tag`, storing each value with
+// put(k, value) as it arrives (LDS, not registers).  The addresses are
+// rebuilt in every round from an opaque base, so only the N words in flight
+// occupy registers.
+template <int N, class O, class F>
+__device__ __forceinline__ bool poll_put(const u64* base, O off, F put, uint32_t tag, const BatchArgs& a) {
+  uint32_t pending = N >= 32 ? ~0u : (1u << N) - 1u;
+  WaitBudget wb{wr_clock(), 0};
+  for (;;) {
+    const u64* b = opaque(base);
+    u64 w[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1u) ? xpeek(b + off(k)) : 0;
+#pragma unroll
+    for (int k = 0; k < N; ++k)
+      if ((pending >> k & 1u) && xtag(w[k]) == tag) {
+        put(k, xval(w[k]));
+        pending &= ~(1u << k);
+      }
+    if (!pending) return true;
+    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+  }
+}
+
 // Wait until *p carries `tag` (the slow path of the straight-line reads below).
 __device__ __forceinline__ bool wait_word(const u64* p, uint32_t tag, float* v, const BatchArgs& a) {
   return poll_map<1>([&](int) { return p; }, tag, v, a);
@@ -179,82 +212,60 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     xpub(dst + bl0 * 256 + c0 + 16, tag, mfma_row(B));
     xpub(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B));
   };
-  // Sums over the heads, in head order.  Lane jj of wave 0 first watches the
-  // last word head jj publishes; then thread (class v, parity h) reads the
-  // partials of vectors h, h + 2, h + 4, h + 6 of every head (two batches of
-  // loads, all in flight within a batch; more at once would keep too many
-  // addresses live), again until every word carries the step's tag.
+  // Sums over the heads, in head order.  Lane jj of every wave first watches
+  // the last word head jj publishes; then thread (class v, parity h) reads the
+  // partials of vectors h, h + 2, h + 4, h + 6 of every head, two vectors at a
+  // time (all their heads' words in flight at once), re-reading only words that
+  // do not carry the step's tag yet.
   auto gather_logits = [&](const u64* src, uint32_t tag) {
-    if (wave == 0) {
+    {
       float y;
       const int hj = lane < NH ? lane : 0;
       if (!wait_word(src + ((size_t)hj * L + L - 1) * 256 + 255, tag, &y, a)) misc[0] = 1;
     }
-    __syncthreads();
-    if (misc[0]) return;
     const int v = tid & 255, h = tid >> 8;
-    const u64* base = src + h * 256 + v;            // word (jj, h + 2m) at base + (jj L + 2m) 256
-    constexpr int NH0 = (NH + 1) / 2;                // heads in the first batch
-    WaitBudget wb{wr_clock(), 0};
-    for (;;) {
-      float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-      bool stale = false;
+    // word k (< 4 NH): head k % NH, vector h + 2 (k / NH); staged in gv (free
+    // here), two vectors' words in flight at a time
+    float* stage = gv + tid;                        // [4 NH][512]
 #pragma unroll 1
-      for (int half = 0; half < 2; ++half)
-#pragma unroll
-        for (int jj = half ? NH0 : 0; jj < (half ? NH : NH0); ++jj)
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const u64 w = xpeek(base + (size_t)(jj * L + 2 * m) * 256);
-            stale |= xtag(w) != tag;
-            s[m] += xval(w);
-          }
-      if (!stale) {
-#pragma unroll
-        for (int m = 0; m < 4; ++m) zs[(h + 2 * m) * 256 + v] = s[m];
-        return;
-      }
-      if (!wait_ok(wb, a.err, a.limit, a.err)) {
+    for (int mp = 0; mp < 2; ++mp)
+      if (!poll_put<2 * NH>(src + h * 256 + v + (size_t)(4 * mp) * 256,
+                            [&](int k) { return (size_t)((k % NH) * L + 2 * (k / NH)) * 256; },
+                            [&](int k, float x) { stage[(2 * NH * mp + k) * WR_THREADS] = x; }, tag, a)) {
         misc[0] = 1;
         return;
       }
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      float s = 0.0f;
+#pragma unroll
+      for (int jj = 0; jj < NH; ++jj) s += stage[(m * NH + jj) * WR_THREADS];
+      zs[(h + 2 * m) * 256 + v] = s;
     }
   };
   // The 3L pre-activation words of gate thread u (two batches of loads) and
   // the L additive terms of the e gate (bias + conditioning, and with subscale
   // the context term, which stays outside the reset product), staged in LDS:
   // word k at gv[k * 448 + u], term of vector b at gv[(3L + b) * 448 + u].
-  auto read_gates = [&](const u64* G, const u64* XE, uint32_t tag, int col) {
-    WaitBudget wb{wr_clock(), 0};
-    for (;;) {
-      bool stale = false;
+  const bool trg = g == 0 && j == 0 && tid == 0;            // a gate thread (tracing)
+  auto read_gates = [&](const u64* G, const u64* XE, uint32_t tag, int col, int64_t t) {
 #pragma unroll
-      for (int b = 0; b < L; ++b) {
-        float xe = 0.0f;
-        if (CTX) {
-          const u64 w = xpeek(XE + b * Hh + u);
-          stale |= xtag(w) != tag;
-          xe = xval(w);
-        }
-        gv[(3 * L + b) * 448 + u] = a.cb[cbo[b] + col] + xe;
-      }
+    for (int b = 0; b < L; ++b) gv[(3 * L + b) * 448 + u] = a.cb[cbo[b] + col];
+    if (trg && col == 2 * H) trace_at(a, t, 13);
+    if (CTX && !poll_put<L>(XE + u, [&](int b) { return (size_t)b * Hh; },
+                             [&](int b, float x) { gv[(3 * L + b) * 448 + u] += x; }, tag, a)) {
+      misc[0] = 1;
+      return;
+    }
 #pragma unroll 1
-      for (int half = 0; half < 2; ++half) {
-        u64 w[3 * L / 2];
-#pragma unroll
-        for (int k = 0; k < 3 * L / 2; ++k) w[k] = xpeek(G + (size_t)(half * 3 * L / 2 + k) * Hh + u);
-#pragma unroll
-        for (int k = 0; k < 3 * L / 2; ++k) {
-          stale |= xtag(w[k]) != tag;
-          gv[(half * 3 * L / 2 + k) * 448 + u] = xval(w[k]);
-        }
-      }
-      if (!stale) return;
-      if (!wait_ok(wb, a.err, a.limit, a.err)) {
+    for (int hb = 0; hb < 2; ++hb)                  // 12 words in flight at a time
+      if (!poll_put<3 * L / 2>(G + u + (size_t)(hb * 3 * L / 2) * Hh, [&](int k) { return (size_t)k * Hh; },
+                               [&](int k, float x) { gv[(hb * 3 * L / 2 + k) * 448 + u] = x; }, tag, a)) {
         misc[0] = 1;
         return;
+      } else if (trg && col == 2 * H && hb == 0) {
+        trace_at(a, t, 14);
       }
-    }
   };
   const int vw = min(v0 + wave, a.S - 1);          // the draw wave's vector
   const size_t ob = obase(a, vw);
@@ -282,8 +293,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     // (1) coarse gates of every unit and vector: the 24 pre-activation words of
     // thread u are polled together and staged in LDS, then one vector at a time
     if (gate) {
-      read_gates(GA, X + P.x_xc, tag, 2 * H + u);
-#pragma unroll 1
+      read_gates(GA, X + P.x_xc, tag, 2 * H + u, t);
+      if (trg) trace_at(a, t, 11);
+#pragma unroll 2
       for (int b = 0; b < L; ++b) {
         const float cbe = gv[(3 * L + b) * 448 + u];
         const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]);
@@ -331,8 +343,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
     if (gate) {
-      read_gates(GF, X + P.x_xf, tag, 2 * H + Hh + u);
-#pragma unroll 1
+      read_gates(GF, X + P.x_xf, tag, 2 * H + Hh + u, t);
+      if (trg) trace_at(a, t, 12);
+#pragma unroll 2
       for (int b = 0; b < L; ++b) {
         const float cbe = gv[(3 * L + b) * 448 + u];
         const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]), x2 = fscale(misc[8 + b]);
@@ -610,6 +623,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     }
     publish(tag + 1, cb0, cb1);
     if (tr) trace_at(a, t, 20);
+    if (g == 0 && k > 0 && k < 8 && tid == 0) trace_at(a, t, 24 + k);
   }
 }
 

@@ -37,17 +37,15 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
       acc += xval(xpeek(G + u)) + xval(xpeek(G + Hh + u)) + xval(xpeek(G + 2 * Hh + u));
     gsink[tid] = acc;
   };
-  // partials of all NK slices, read as the sampling kernel reads them: wave 0
-  // waits for the last word of every slice, then thread (v, half) reads its
-  // half of the slices
+  // partials of all NK slices, read as the sampling kernel reads them: every
+  // wave waits for the last word of every slice, then thread (v, half) reads
+  // its half of the slices
   auto gather = [&](const u64* src, uint32_t tag) {
-    if (wave == 0) {
+    {
       float y;
       const int jj = lane < NK ? lane : 0;
       if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + 255, tag, &y, a)) misc[0] = 1;
     }
-    __syncthreads();
-    if (misc[0]) return;
     const int v = tid & 255, hh = tid >> 8, h0 = (NK + 1) / 2;
     float s;
     if (!sum_parts<16>(src, P.x_ps, hh ? h0 : 0, hh ? NK : h0, v, tag, &s, a)) misc[0] = 1;
@@ -56,13 +54,15 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     if (coarse) gate_words(GA);
-    if (coarse && wave == 7 && lane < HR) xpub(YC + HR * jk + lane, tag, 0.0f);
+    if (coarse && wave == 7)
+      for (int i = lane; i < HR; i += 64) xpub(YC + HR * jk + i, tag, 0.0f);
     if (coarse && lane < 32) xpub(PC + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
     gather(PC, tag);
     __syncthreads();
     if (misc[0]) return;
     if (fine) gate_words(GF);
-    if (fine && wave == 7 && lane < HR) xpub(YF + HR * jk + lane, tag, 0.0f);
+    if (fine && wave == 7)
+      for (int i = lane; i < HR; i += 64) xpub(YF + HR * jk + i, tag, 0.0f);
     if (fine && lane < 32) xpub(PF + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
     gather(PF, tag);
     __syncthreads();

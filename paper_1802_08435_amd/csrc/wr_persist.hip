@@ -203,18 +203,16 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       xpub(dst + 32 * wave + 16 + lane, tag, mfma_row(B));
     }
   };
-  // partial logits of all slices: lane jj of wave 0 first waits for the last
-  // word of slice jj (little polling traffic while the exchange is in
+  // partial logits of all slices: lane jj of every wave first waits for the
+  // last word of slice jj (little polling traffic while the exchange is in
   // flight), then thread (v, half) sums its half of the slices in slice order
   // (every word is still checked for its tag)
   auto gather_logits = [&](const u64* src, uint32_t tag) {
-    if (wave == 0) {
+    {   // every wave waits on the flags itself: no barrier before the reads
       float y;
       const int jj = lane < NK ? lane : 0;
       if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + 255, tag, &y, a)) misc[0] = 1;
     }
-    __syncthreads();
-    if (misc[0]) return;
     float s;
     const int v = tid & 255, hh = tid >> 8;
     if (!sum_parts<NHP>(src, P.x_ps, hh ? NHP : 0, hh ? NK : NHP, v, tag, &s, a)) misc[0] = 1;
