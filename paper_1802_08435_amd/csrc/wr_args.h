@@ -4,6 +4,7 @@
 #include "wr_layout.h"
 
 typedef unsigned long long u64;
+typedef uint32_t xw;        // exchange word (value with the step parity in its lowest bit)
 
 #define WR_TRACE_SLOTS 32   // per traced step: timestamps (100 MHz) of phase ends
 
@@ -54,7 +55,7 @@ struct PersistArgs {
   float* h_out;
   uint8_t* c_out;
   uint8_t* f_out;
-  u64* xc;                  // exchange words, zeroed before the launch
+  xw* xc;                   // exchange words (wr_device.h), zeroed before the launch
   unsigned* err;
   u64 limit;                // wait limit in 100 MHz ticks
   u64* trace;               // [trace_steps][WR_TRACE_SLOTS] phase timestamps or null
@@ -90,7 +91,7 @@ struct BatchArgs {
   float* h_out;
   uint8_t* c_out;
   uint8_t* f_out;
-  u64* xc;                  // [G][P.x_words] exchange words, zeroed before the launch
+  xw* xc;                   // [G][P.x_words] exchange words, zeroed before the launch
   unsigned* err;
   u64 limit;
   u64* trace;               // [trace_steps][WR_TRACE_SLOTS] (group 0) or null

@@ -29,16 +29,16 @@ __device__ __forceinline__ int64_t cb_offset(const BatchArgs& a, int v, int64_t 
 
 // Wait until the N words base[k*stride] (k < N) carry `tag`; values to v[].
 template <int N>
-__device__ __forceinline__ bool poll_strided(const u64* base, int stride, uint32_t tag, float* v, const BatchArgs& a) {
+__device__ __forceinline__ bool poll_strided(const xw* base, int stride, uint32_t tag, float* v, const BatchArgs& a) {
   uint64_t pending = N >= 64 ? ~0ull : (1ull << N) - 1ull;
   WaitBudget wb{wr_clock(), 0};
   for (;;) {
-    u64 w[N];
+    xw w[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1ull) ? xpeek(base + (size_t)k * stride) : 0;
 #pragma unroll
     for (int k = 0; k < N; ++k)
-      if ((pending >> k & 1ull) && xtag(w[k]) == tag) {
+      if ((pending >> k & 1ull) && xok(w[k], tag)) {
         v[k] = xval(w[k]);
         pending &= ~(1ull << k);
       }
@@ -53,12 +53,12 @@ __device__ __forceinline__ bool poll_map(F addr, uint32_t tag, float* v, const B
   uint64_t pending = N >= 64 ? ~0ull : (1ull << N) - 1ull;
   WaitBudget wb{wr_clock(), 0};
   for (;;) {
-    u64 w[N];
+    xw w[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1ull) ? xpeek(addr(k)) : 0;
 #pragma unroll
     for (int k = 0; k < N; ++k)
-      if ((pending >> k & 1ull) && xtag(w[k]) == tag) {
+      if ((pending >> k & 1ull) && xok(w[k], tag)) {
         v[k] = xval(w[k]);
         pending &= ~(1ull << k);
       }
@@ -81,17 +81,17 @@ __device__ __forceinline__ T* opaque(T* p) {
 // rebuilt in every round from an opaque base, so only the N words in flight
 // occupy registers.
 template <int N, class O, class F>
-__device__ __forceinline__ bool poll_put(const u64* base, O off, F put, uint32_t tag, const BatchArgs& a) {
+__device__ __forceinline__ bool poll_put(const xw* base, O off, F put, uint32_t tag, const BatchArgs& a) {
   uint32_t pending = N >= 32 ? ~0u : (1u << N) - 1u;
   WaitBudget wb{wr_clock(), 0};
   for (;;) {
-    const u64* b = opaque(base);
-    u64 w[N];
+    const xw* b = opaque(base);
+    xw w[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1u) ? xpeek(b + off(k)) : 0;
 #pragma unroll
     for (int k = 0; k < N; ++k)
-      if ((pending >> k & 1u) && xtag(w[k]) == tag) {
+      if ((pending >> k & 1u) && xok(w[k], tag)) {
         put(k, xval(w[k]));
         pending &= ~(1u << k);
       }
@@ -101,7 +101,7 @@ __device__ __forceinline__ bool poll_put(const u64* base, O off, F put, uint32_t
 }
 
 // Wait until *p carries `tag` (the slow path of the straight-line reads below).
-__device__ __forceinline__ bool wait_word(const u64* p, uint32_t tag, float* v, const BatchArgs& a) {
+__device__ __forceinline__ bool wait_word(const xw* p, uint32_t tag, float* v, const BatchArgs& a) {
   return poll_map<1>([&](int) { return p; }, tag, v, a);
 }
 
@@ -173,15 +173,15 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
     misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
   }
-  u64* X = a.xc + (size_t)g * P.x_words;
-  const u64* GA = X + P.x_ga;
-  const u64* GF = X + P.x_gf;
-  u64* YC = X + P.x_yc;
-  u64* YF = X + P.x_yf;
-  u64* PCo = X + P.x_pc + (size_t)j * L * 256;
-  u64* PFo = X + P.x_pf + (size_t)j * L * 256;
-  const u64* PC = X + P.x_pc;
-  const u64* PF = X + P.x_pf;
+  xw* X = a.xc + (size_t)g * P.x_words;
+  const xw* GA = X + P.x_ga;
+  const xw* GF = X + P.x_gf;
+  xw* YC = X + P.x_yc;
+  xw* YF = X + P.x_yf;
+  xw* PCo = X + P.x_pc + (size_t)j * L * 256;
+  xw* PFo = X + P.x_pf + (size_t)j * L * 256;
+  const xw* PC = X + P.x_pc;
+  const xw* PF = X + P.x_pf;
   const int rt = wave & 3, kc = wave >> 2;
   const int bl0 = 2 * (lane >> 4);                 // vectors of this lane's MFMA results: bl0, bl0 + 1
 
@@ -200,7 +200,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     __syncthreads();
   };
   // class tiles 2*wave, 2*wave+1 over this head's 64 columns, for all vectors
-  auto second_layer = [&](const bf16x8* W, u64* dst, uint32_t tag) {
+  auto second_layer = [&](const bf16x8* W, xw* dst, uint32_t tag) {
     const bf16x8 x0 = afrag(imo, 0), x1 = afrag(imo, 1);
     f32x4 A = mfma(x0, W[0], f32x4{0, 0, 0, 0});
     f32x4 B = mfma(x0, W[2], f32x4{0, 0, 0, 0});
@@ -217,7 +217,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   // partials of vectors h, h + 2, h + 4, h + 6 of every head, two vectors at a
   // time (all their heads' words in flight at once), re-reading only words that
   // do not carry the step's tag yet.
-  auto gather_logits = [&](const u64* src, uint32_t tag) {
+  auto gather_logits = [&](const xw* src, uint32_t tag) {
     {
       float y;
       const int hj = lane < NH ? lane : 0;
@@ -225,16 +225,13 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     }
     const int v = tid & 255, h = tid >> 8;
     // word k (< 4 NH): head k % NH, vector h + 2 (k / NH); staged in gv (free
-    // here), two vectors' words in flight at a time
+    // here), all in flight at once
     float* stage = gv + tid;                        // [4 NH][512]
-#pragma unroll 1
-    for (int mp = 0; mp < 2; ++mp)
-      if (!poll_put<2 * NH>(src + h * 256 + v + (size_t)(4 * mp) * 256,
-                            [&](int k) { return (size_t)((k % NH) * L + 2 * (k / NH)) * 256; },
-                            [&](int k, float x) { stage[(2 * NH * mp + k) * WR_THREADS] = x; }, tag, a)) {
-        misc[0] = 1;
-        return;
-      }
+    if (!poll_put<4 * NH>(src + h * 256 + v, [&](int k) { return (size_t)((k % NH) * L + 2 * (k / NH)) * 256; },
+                          [&](int k, float x) { stage[k * WR_THREADS] = x; }, tag, a)) {
+      misc[0] = 1;
+      return;
+    }
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       float s = 0.0f;
@@ -248,7 +245,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   // the context term, which stays outside the reset product), staged in LDS:
   // word k at gv[k * 448 + u], term of vector b at gv[(3L + b) * 448 + u].
   const bool trg = g == 0 && j == 0 && tid == 0;            // a gate thread (tracing)
-  auto read_gates = [&](const u64* G, const u64* XE, uint32_t tag, int col, int64_t t) {
+  auto read_gates = [&](const xw* G, const xw* XE, uint32_t tag, int col, int64_t t) {
 #pragma unroll
     for (int b = 0; b < L; ++b) gv[(3 * L + b) * 448 + u] = a.cb[cbo[b] + col];
     if (trg && col == 2 * H) trace_at(a, t, 13);
@@ -257,15 +254,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       misc[0] = 1;
       return;
     }
-#pragma unroll 1
-    for (int hb = 0; hb < 2; ++hb)                  // 12 words in flight at a time
-      if (!poll_put<3 * L / 2>(G + u + (size_t)(hb * 3 * L / 2) * Hh, [&](int k) { return (size_t)k * Hh; },
-                               [&](int k, float x) { gv[(hb * 3 * L / 2 + k) * 448 + u] = x; }, tag, a)) {
-        misc[0] = 1;
-        return;
-      } else if (trg && col == 2 * H && hb == 0) {
-        trace_at(a, t, 14);
-      }
+    if (!poll_put<3 * L>(G + u, [&](int k) { return (size_t)k * Hh; }, [&](int k, float x) { gv[k * 448 + u] = x; },
+                         tag, a))   // all 24 words in flight at once
+      misc[0] = 1;
   };
   const int vw = min(v0 + wave, a.S - 1);          // the draw wave's vector
   const size_t ob = obase(a, vw);
@@ -436,8 +427,8 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   const int row = gt * H + (fw ? Hh : 0) + i;                  // R row of this lane
   const int bl0 = 2 * (lane >> 4);
   const int v0 = g * L;
-  u64* X = a.xc + (size_t)g * P.x_words;
-  u64* dst = X + (fw ? P.x_gf : P.x_ga) + gt * Hh + i;        // + vector * 3 Hh
+  xw* X = a.xc + (size_t)g * P.x_words;
+  xw* dst = X + (fw ? P.x_gf : P.x_ga) + gt * Hh + i;        // + vector * 3 Hh
   {
     const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
     for (int x = tid; x < P.u_lds_w / 16; x += WR_THREADS) ((uint4*)lds)[x] = src[x];
@@ -460,7 +451,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   __syncthreads();
   for (int x = tid; x < L * H; x += WR_THREADS) {
     const int b = x / H, col = x % H;
-    const float y = a.h_in ? a.h_in[(size_t)min(v0 + b, a.S - 1) * H + col] : 0.0f;
+    const float y = a.h_in ? xround(a.h_in[(size_t)min(v0 + b, a.S - 1) * H + col]) : 0.0f;
     aput(img + (col >> 5) * WR_FRAG, col & 31, y, b);
   }
   __builtin_amdgcn_s_waitcnt(0);
@@ -493,7 +484,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     }
   };
   f32x4 xa0 = {0, 0, 0, 0}, xa1 = {0, 0, 0, 0};        // context term of e-gate rows
-  u64* dstx = X + (fw ? P.x_xf : P.x_xc) + i;          // + vector * Hh
+  xw* dstx = X + (fw ? P.x_xf : P.x_xc) + i;          // + vector * Hh
   auto publish = [&](uint32_t tag, float cb0, float cb1) {
     xpub(dst + (size_t)bl0 * 3 * Hh, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0);
     xpub(dst + (size_t)(bl0 + 1) * 3 * Hh, tag, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
@@ -558,7 +549,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   // Wait for one half of h of all 8 vectors: lane jj of wave 0 first watches
   // the last word head jj publishes (vector 7), then every thread reads its
   // words once and writes the operand tiles kt0 ...
-  auto gather_half = [&](const u64* Y, uint32_t tag, int kt0) {
+  auto gather_half = [&](const xw* Y, uint32_t tag, int kt0) {
     if (wave == 0) {
       const int hj = lane < P.NH ? lane : 0;
       float y;
@@ -574,12 +565,12 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       if (tid + m * WR_THREADS < L * Hh) pending |= 1u << m;
     WaitBudget wb{wr_clock(), 0};
     while (pending) {
-      u64 w[PER];
+      xw w[PER];
 #pragma unroll
       for (int m = 0; m < PER; ++m) w[m] = (pending >> m & 1u) ? xpeek(Y + tid + m * WR_THREADS) : 0;
 #pragma unroll
       for (int m = 0; m < PER; ++m)
-        if ((pending >> m & 1u) && xtag(w[m]) == tag) {
+        if ((pending >> m & 1u) && xok(w[m], tag)) {
           y[m] = xval(w[m]);
           pending &= ~(1u << m);
         }
@@ -601,8 +592,8 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   phase_c();
   phase_f();
   publish(1u, cbv(bl0, 0), cbv(bl0 + 1, 0));
-  const u64* YC = X + P.x_yc;
-  const u64* YF = X + P.x_yf;
+  const xw* YC = X + P.x_yc;
+  const xw* YF = X + P.x_yf;
   for (int64_t t = 0; t + 1 < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     const float cb0 = cbv(bl0, t + 1), cb1 = cbv(bl0 + 1, t + 1);

@@ -108,21 +108,29 @@ __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w <<
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 // ---------------------------------------------------------------------------
-// Inter-workgroup exchange.  A 64-bit word carries a value in its low half and
-// the tag of the step that produced it in its high half; naturally aligned
-// 64-bit atomic accesses are single-copy atomic, so a reader that sees the tag
-// also sees the value.  Agent-scope relaxed accesses keep the words coherent
-// across all XCDs (each XCD has its own L2).
+// Inter-workgroup exchange.  A 32-bit word carries an fp32 value whose lowest
+// mantissa bit is replaced by the parity of the tag (step number) that
+// produced it.  Every consumer reads every word it uses once per step, and the
+// dependency chain keeps a producer at most one step ahead of any consumer of
+// its words, so a word is either the previous step's (other parity) or the
+// awaited one: one bit tells them apart, and each exchange moves half the
+// bytes of a value + full-tag pair.  Aligned 32-bit atomic accesses are
+// single-copy atomic; agent-scope relaxed accesses keep the words coherent
+// across all XCDs (each XCD has its own L2).  The cost is 1 ulp on the value.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void xpub(u64* p, uint32_t tag, float v) {
-  u64 w = ((u64)tag << 32) | (u64)__float_as_uint(v);
+typedef uint32_t xw;
+__device__ __forceinline__ void xpub(xw* p, uint32_t tag, float v) {
+  const xw w = (__float_as_uint(v) & ~1u) | (tag & 1u);
   __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ u64 xpeek(const u64* p) {
+__device__ __forceinline__ xw xpeek(const xw* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint32_t xtag(u64 w) { return (uint32_t)(w >> 32); }
-__device__ __forceinline__ float xval(u64 w) { return __uint_as_float((uint32_t)w); }
+__device__ __forceinline__ bool xok(xw w, uint32_t tag) { return ((w ^ tag) & 1u) == 0; }
+__device__ __forceinline__ float xval(xw w) { return __uint_as_float(w & ~1u); }
+// A value as a reader of the exchange sees it (so that state handed in by the
+// caller enters a computation exactly as the exchanged values do).
+__device__ __forceinline__ float xround(float v) { return __uint_as_float(__float_as_uint(v) & ~1u); }
 
 __device__ __forceinline__ u64 wr_clock() { return __builtin_amdgcn_s_memrealtime(); }  // 100 MHz
 

@@ -21,17 +21,17 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   int* misc = (int*)lds;
   float* zs = (float*)(misc + 16);               // [2][256] logit sums (written, never read)
-  const u64* GA = a.xc + P.x_ga;
-  const u64* GF = a.xc + P.x_gf;
-  u64* YC = a.xc + P.x_yc;
-  u64* YF = a.xc + P.x_yf;
-  u64* PC = a.xc + P.x_pc;
-  u64* PF = a.xc + P.x_pf;
+  const xw* GA = a.xc + P.x_ga;
+  const xw* GF = a.xc + P.x_gf;
+  xw* YC = a.xc + P.x_yc;
+  xw* YF = a.xc + P.x_yf;
+  xw* PC = a.xc + P.x_pc;
+  xw* PF = a.xc + P.x_pf;
   if (tid == 0) misc[0] = 0;
   __syncthreads();
   // gate words of every unit of a half (3 per unit), read once without waiting
   float* gsink = zs + 512;                       // [WR_THREADS]
-  auto gate_words = [&](const u64* G) {
+  auto gate_words = [&](const xw* G) {
     float acc = 0.0f;
     for (int u = tid; u < Hh; u += WR_THREADS)
       acc += xval(xpeek(G + u)) + xval(xpeek(G + Hh + u)) + xval(xpeek(G + 2 * Hh + u));
@@ -40,7 +40,7 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   // partials of all NK slices, read as the sampling kernel reads them: every
   // wave waits for the last word of every slice, then thread (v, half) reads
   // its half of the slices
-  auto gather = [&](const u64* src, uint32_t tag) {
+  auto gather = [&](const xw* src, uint32_t tag) {
     {
       float y;
       const int jj = lane < NK ? lane : 0;
@@ -77,10 +77,10 @@ __device__ __forceinline__ void floor_unit(const PersistArgs& a, int k, unsigned
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   int* misc = (int*)lds;
   float* hv = (float*)(misc + 16);               // [Hh] (written, never read)
-  u64* GA = a.xc + P.x_ga + (size_t)k * wpu;
-  u64* GF = a.xc + P.x_gf + (size_t)k * wpu;
-  const u64* YC = a.xc + P.x_yc;
-  const u64* YF = a.xc + P.x_yf;
+  xw* GA = a.xc + P.x_ga + (size_t)k * wpu;
+  xw* GF = a.xc + P.x_gf + (size_t)k * wpu;
+  const xw* YC = a.xc + P.x_yc;
+  const xw* YF = a.xc + P.x_yf;
   if (tid == 0) misc[0] = 0;
   __syncthreads();
   auto publish = [&](uint32_t tag) {
@@ -89,7 +89,7 @@ __device__ __forceinline__ void floor_unit(const PersistArgs& a, int k, unsigned
       xpub(GF + tid, tag, 0.0f);
     }
   };
-  auto gather_half = [&](const u64* Y, uint32_t tag, bool flags) {
+  auto gather_half = [&](const xw* Y, uint32_t tag, bool flags) {
     if (flags) {
       if (wave == 4) {
         float y;
@@ -108,12 +108,12 @@ __device__ __forceinline__ void floor_unit(const PersistArgs& a, int k, unsigned
         if (r + 256 * m < Hh) pending |= 1u << m;
       WaitBudget wb{wr_clock(), 0};
       while (pending) {
-        u64 x[MW];
+        xw x[MW];
 #pragma unroll
         for (int m = 0; m < MW; ++m) x[m] = (pending >> m & 1u) ? xpeek(Y + r + 256 * m) : 0;
 #pragma unroll
         for (int m = 0; m < MW; ++m)
-          if ((pending >> m & 1u) && xtag(x[m]) == tag) {
+          if ((pending >> m & 1u) && xok(x[m], tag)) {
             hv[r + 256 * m] = xval(x[m]);
             pending &= ~(1u << m);
           }

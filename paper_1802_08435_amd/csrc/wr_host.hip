@@ -72,7 +72,7 @@ struct wavernn_model {
   float *d_I = nullptr, *d_bias = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr, *d_b4 = nullptr;
   float* d_cb = nullptr;             // [cb_cap][3H] bias + conditioning per frame
   int64_t cb_cap = 0;
-  u64* d_xc = nullptr;
+  xw* d_xc = nullptr;                // exchange words (zeroed as 64-bit pairs)
   u64* trace = nullptr;
   int64_t trace_steps = 0;
   // batched path (several utterances per launch)
@@ -80,7 +80,7 @@ struct wavernn_model {
   BatchPlan bplan;
   const void* bk = nullptr;          // kernel instantiation for bplan.KH
   uint4 *d_buw = nullptr, *d_bur = nullptr, *d_bux = nullptr;
-  u64* d_bxc = nullptr;
+  xw* d_bxc = nullptr;
   float* d_bcb = nullptr;            // [streams][frames][3H]
   size_t bcb_cap = 0;                // floats
 
@@ -288,7 +288,7 @@ wavernn_status upload_common(wavernn_model* m, const wavernn_weights* w) {
   }
   m->cb_cap = c.cond_dim > 0 ? 1024 : 1;
   if ((s = m->alloc(&m->d_cb, (size_t)m->cb_cap * 3 * H * 4)) != WAVERNN_OK) return s;
-  if ((s = m->alloc(&m->d_xc, (size_t)P.x_words * 8)) != WAVERNN_OK) return s;
+  if ((s = m->alloc(&m->d_xc, (size_t)(P.x_words + 1) / 2 * 8)) != WAVERNN_OK) return s;
   return WAVERNN_OK;
 }
 
@@ -457,7 +457,7 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   }
   if ((s = m->upload(&m->d_buw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
   if ((s = m->upload(&m->d_bur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->alloc(&m->d_bxc, (size_t)B.G * B.x_words * 8)) != WAVERNN_OK) return s;
+  if ((s = m->alloc(&m->d_bxc, ((size_t)B.G * B.x_words + 1) / 2 * 8)) != WAVERNN_OK) return s;
   HIPOK(hipFuncSetAttribute(m->bk, hipFuncAttributeMaxDynamicSharedMemorySize, B.lds));
   int per_cu = 0;
   HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->bk, WR_THREADS, B.lds));
@@ -485,7 +485,10 @@ wavernn_status launch_cond(const wavernn_model* m, const float* feat, int64_t n_
   return WAVERNN_OK;
 }
 
-wavernn_status launch_fill(u64* p, int64_t n, hipStream_t st) {
+// Zero n exchange words (as (n + 1) / 2 64-bit stores; buffers are sized for that).
+wavernn_status launch_fill(xw* words, int64_t n_words, hipStream_t st) {
+  u64* p = (u64*)words;
+  int64_t n = (n_words + 1) / 2;
   int64_t nb = (n + 255) / 256;
   u64 zero = 0;
   void* args[] = {&p, &n, &zero};

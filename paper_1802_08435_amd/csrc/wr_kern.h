@@ -135,22 +135,22 @@ __device__ __forceinline__ float mfma_row_hi(f32x4 d) { return d[2] + d[3]; }
 // Wait until every word p[k] (k < N) carries `tag`, starting from words w[]
 // loaded earlier; only words that did not carry it yet are loaded again.
 template <int N, class A>
-__device__ __forceinline__ bool poll_pref(const u64* const* p, const u64* w, uint32_t tag, float* v, const A& a) {
+__device__ __forceinline__ bool poll_pref(const xw* const* p, const xw* w, uint32_t tag, float* v, const A& a) {
   uint32_t pending = 0;
 #pragma unroll
   for (int k = 0; k < N; ++k) {
-    if (xtag(w[k]) == tag) v[k] = xval(w[k]);
+    if (xok(w[k], tag)) v[k] = xval(w[k]);
     else pending |= 1u << k;
   }
   if (!pending) return true;
   WaitBudget wb{wr_clock(), 0};
   while (pending) {
-    u64 x[N];
+    xw x[N];
 #pragma unroll
     for (int k = 0; k < N; ++k) x[k] = (pending >> k & 1u) ? xpeek(p[k]) : 0;
 #pragma unroll
     for (int k = 0; k < N; ++k)
-      if ((pending >> k & 1u) && xtag(x[k]) == tag) {
+      if ((pending >> k & 1u) && xok(x[k], tag)) {
         v[k] = xval(x[k]);
         pending &= ~(1u << k);
       }
@@ -161,14 +161,14 @@ __device__ __forceinline__ bool poll_pref(const u64* const* p, const u64* w, uin
 
 // Wait until *p carries `tag` (with SLEEP, a short sleep between loads).
 template <bool SLEEP = true, class A>
-__device__ __forceinline__ bool poll_sleepy(const u64* p, uint32_t tag, float* v, const A& a) {
-  u64 w = xpeek(p);
-  if (xtag(w) != tag) {
+__device__ __forceinline__ bool poll_sleepy(const xw* p, uint32_t tag, float* v, const A& a) {
+  xw w = xpeek(p);
+  if (!xok(w, tag)) {
     WaitBudget wb{wr_clock(), 0};
     do {
       if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
       if (SLEEP) __builtin_amdgcn_s_sleep(1);
-    } while (xtag(w = xpeek(p)) != tag);
+    } while (!xok(w = xpeek(p), tag));
   }
   *v = xval(w);
   return true;
@@ -177,17 +177,17 @@ __device__ __forceinline__ bool poll_sleepy(const u64* p, uint32_t tag, float* v
 // Sum over parts jj = j0 .. j1-1 of src[jj*stride + v] once all carry `tag`, in
 // part order (every head sums in the same order, so all draw the same class).
 template <int MAXP, class A>
-__device__ __forceinline__ bool sum_parts(const u64* src, int stride, int j0, int j1, int v, uint32_t tag, float* out,
+__device__ __forceinline__ bool sum_parts(const xw* src, int stride, int j0, int j1, int v, uint32_t tag, float* out,
                                           const A& a) {
   float vals[MAXP];
   uint32_t pending = 0;
-  u64 w[MAXP];
+  xw w[MAXP];
 #pragma unroll
   for (int k = 0; k < MAXP; ++k) w[k] = j0 + k < j1 ? xpeek(src + (size_t)(j0 + k) * stride + v) : 0;
 #pragma unroll
   for (int k = 0; k < MAXP; ++k) {
     if (j0 + k >= j1) continue;
-    if (xtag(w[k]) == tag) vals[k] = xval(w[k]);
+    if (xok(w[k], tag)) vals[k] = xval(w[k]);
     else pending |= 1u << k;
   }
   if (pending) {
@@ -198,7 +198,7 @@ __device__ __forceinline__ bool sum_parts(const u64* src, int stride, int j0, in
       for (int k = 0; k < MAXP; ++k) w[k] = (pending >> k & 1u) ? xpeek(src + (size_t)(j0 + k) * stride + v) : 0;
 #pragma unroll
       for (int k = 0; k < MAXP; ++k)
-        if ((pending >> k & 1u) && xtag(w[k]) == tag) {
+        if ((pending >> k & 1u) && xok(w[k], tag)) {
           vals[k] = xval(w[k]);
           pending &= ~(1u << k);
         }

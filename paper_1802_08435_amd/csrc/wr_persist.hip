@@ -147,17 +147,17 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     misc[2] = a.c_in ? a.c_in[0] : 128;
     misc[3] = a.f_in ? a.f_in[0] : 0;
   }
-  const u64* GA = a.xc + P.x_ga;
-  const u64* GF = a.xc + P.x_gf;
-  u64* YC = a.xc + P.x_yc;
-  u64* YF = a.xc + P.x_yf;
-  u64* PCo = a.xc + P.x_pc + (size_t)jk * P.x_ps;
-  u64* PFo = a.xc + P.x_pf + (size_t)jk * P.x_ps;
-  const u64* PC = a.xc + P.x_pc;
-  const u64* PF = a.xc + P.x_pf;
+  const xw* GA = a.xc + P.x_ga;
+  const xw* GF = a.xc + P.x_gf;
+  xw* YC = a.xc + P.x_yc;
+  xw* YF = a.xc + P.x_yf;
+  xw* PCo = a.xc + P.x_pc + (size_t)jk * P.x_ps;
+  xw* PFo = a.xc + P.x_pf + (size_t)jk * P.x_ps;
+  const xw* PC = a.xc + P.x_pc;
+  const xw* PF = a.xc + P.x_pf;
   const int rt = wave % RT, kc = wave / RT;        // first layer: row tile, column-tile chunk
   // GU = 1: pre-activation words of this thread's units, loaded ahead
-  u64 pc[3] = {0, 0, 0}, pf[3] = {0, 0, 0};
+  xw pc[3] = {0, 0, 0}, pf[3] = {0, 0, 0};
   float cbe_c = 0.0f, cbe_f = 0.0f;
   auto prefetch_coarse = [&](int64_t n) {
     if (!WIDE && gate && coarse) {
@@ -190,7 +190,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     __syncthreads();
   };
   // second layer: class tiles 2*wave, 2*wave+1 over this head's HR columns
-  auto second_layer = [&](const bf16x8* W, u64* dst, uint32_t tag) {
+  auto second_layer = [&](const bf16x8* W, xw* dst, uint32_t tag) {
     f32x4 A = {0, 0, 0, 0}, B = {0, 0, 0, 0};
 #pragma unroll
     for (int kt = 0; kt < KO; ++kt) {
@@ -207,7 +207,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   // last word of slice jj (little polling traffic while the exchange is in
   // flight), then thread (v, half) sums its half of the slices in slice order
   // (every word is still checked for its tag)
-  auto gather_logits = [&](const u64* src, uint32_t tag) {
+  auto gather_logits = [&](const xw* src, uint32_t tag) {
     {   // every wave waits on the flags itself: no barrier before the reads
       float y;
       const int jj = lane < NK ? lane : 0;
@@ -255,13 +255,13 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     uint32_t pending = (coarse ? (1u << 3 * GU) - 1 : 0u) | (fine ? ((1u << 3 * GU) - 1) << 3 * GU : 0u);
     WaitBudget wb{wr_clock(), 0};
     for (;;) {
-      u64 x[NW];
+      xw x[NW];
 #pragma unroll
       for (int k = 0; k < NW; ++k)
         x[k] = (pending >> k & 1u) ? xpeek((k < 3 * GU ? GA : GF) + (k % 3) * Hh + un[k / 3 % GU]) : 0;
 #pragma unroll
       for (int k = 0; k < NW; ++k)
-        if ((pending >> k & 1u) && xtag(x[k]) == tag) {
+        if ((pending >> k & 1u) && xok(x[k], tag)) {
           (k < 3 * GU ? pre : prf)[(k % 3) * Hh + un[k / 3 % GU]] = xval(x[k]);
           pending &= ~(1u << k);
         }
@@ -290,7 +290,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       return;
     }
     if (!gate || !coarse) return;
-    const u64* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
+    const xw* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
     float v[3];
     if (!poll_pref<3>(ps, pc, tag, v, a)) {
       misc[0] = 1;
@@ -315,7 +315,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       return;
     }
     if (!gate || !fine) return;
-    const u64* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
+    const xw* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
     float v[3];
     if (!poll_pref<3>(ps, pf, tag, v, a)) {
       misc[0] = 1;
@@ -507,7 +507,7 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   const int tile = k * UCT + q;
   const int g = tile / (Hh / 16), i0 = 16 * (tile % (Hh / 16));
   const int row = g * H + (fw ? Hh : 0) + i0 + (lane & 15);     // R row of lane n < 16
-  u64* dst = a.xc + (fw ? P.x_gf : P.x_ga) + g * Hh + i0 + lane;
+  xw* dst = a.xc + (fw ? P.x_gf : P.x_ga) + g * Hh + i0 + lane;
   {
     const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
     for (int i = tid; i < P.u_lds_w / 16; i += WR_THREADS) ((uint4*)lds)[i] = src[i];
@@ -522,7 +522,7 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   }
   __syncthreads();
   for (int i = tid; i < H; i += WR_THREADS) {
-    const float y = a.h_in ? a.h_in[i] : 0.0f;
+    const float y = a.h_in ? xround(a.h_in[i]) : 0.0f;   // as the heads' exchanged h
     aput(img + (i >> 5) * WR_FRAG, i & 31, y);
   }
   __syncthreads();
@@ -559,15 +559,15 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   // step 0's pre-activations from the initial state
   phase_c();
   phase_f(1u, (cw || fw) && g < 2 ? cb_row(a, a.t0)[row] : 0.0f);
-  const u64* YC = a.xc + P.x_yc;
-  const u64* YF = a.xc + P.x_yf;
+  const xw* YC = a.xc + P.x_yc;
+  const xw* YF = a.xc + P.x_yf;
   // Wait for a half of h.  Waves 3 and 7 own no row tile and never store, so
   // their loads do not wait for the publishing waves' store acknowledgements:
   // lane jj of wave 3 watches the last word of head jj's slice (little polling
   // traffic while the heads exchange logits), then waves 3 and 7 read every
   // word once and write operand tiles kt0 ...
   const bool reader = wave == 3 || wave == 7;
-  auto gather_half = [&](const u64* Y, uint32_t tag, int kt0, bool flags) {
+  auto gather_half = [&](const xw* Y, uint32_t tag, int kt0, bool flags) {
     if (flags) {
       if (wave == 3) {
         float y;
@@ -586,12 +586,12 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
         if (r + 128 * m < Hh) pending |= 1u << m;
       WaitBudget wb{wr_clock(), 0};
       while (pending) {
-        u64 w[4];
+        xw w[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) w[m] = (pending >> m & 1u) ? xpeek(Y + r + 128 * m) : 0;
 #pragma unroll
         for (int m = 0; m < 4; ++m)
-          if ((pending >> m & 1u) && xtag(w[m]) == tag) {
+          if ((pending >> m & 1u) && xok(w[m], tag)) {
             y[m] = xval(w[m]);
             pending &= ~(1u << m);
           }
@@ -650,11 +650,11 @@ __device__ __forceinline__ void sparse_unit_role(const PersistArgs& a, int k, un
   const bool lead = cw && tid % SL == 0;
   const int g = row / H, i = row % H;
   const bool fine = i >= Hh;
-  u64* dst = a.xc + (fine ? P.x_gf : P.x_ga) + g * Hh + (fine ? i - Hh : i);
+  xw* dst = a.xc + (fine ? P.x_gf : P.x_ga) + g * Hh + (fine ? i - Hh : i);
   {
     const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
     for (int q = tid; q < P.u_lds_w / 16; q += WR_THREADS) ((uint4*)lds)[q] = src[q];
-    for (int c = tid; c < H; c += WR_THREADS) hv[c] = a.h_in ? a.h_in[c] : 0.0f;
+    for (int c = tid; c < H; c += WR_THREADS) hv[c] = a.h_in ? xround(a.h_in[c]) : 0.0f;
     if (tid == 0) misc[0] = 0;
   }
   __syncthreads();
@@ -686,11 +686,11 @@ __device__ __forceinline__ void sparse_unit_role(const PersistArgs& a, int k, un
   __builtin_amdgcn_s_waitcnt(0);   // records and h are in before the loop (see head_role)
   phase_c();
   phase_f(1u, lead && g < 2 ? cb_row(a, a.t0)[row] : 0.0f);
-  const u64* YC = a.xc + P.x_yc;
-  const u64* YF = a.xc + P.x_yf;
+  const xw* YC = a.xc + P.x_yc;
+  const xw* YF = a.xc + P.x_yf;
   // Wait for a half of h: lane jj of wave 4 watches the last word of head
   // jj's slice, then waves 4-7 read every word once into hv.
-  auto gather_half = [&](const u64* Y, uint32_t tag, float* out, bool flags) {
+  auto gather_half = [&](const xw* Y, uint32_t tag, float* out, bool flags) {
     if (flags) {
       if (wave == 4) {
         float y;
@@ -712,12 +712,12 @@ __device__ __forceinline__ void sparse_unit_role(const PersistArgs& a, int k, un
       }
       WaitBudget wb{wr_clock(), 0};
       while (pending) {
-        u64 w[MW];
+        xw w[MW];
 #pragma unroll
         for (int m = 0; m < MW; ++m) w[m] = (pending >> m & 1u) ? xpeek(Y + r + 256 * m) : 0;
 #pragma unroll
         for (int m = 0; m < MW; ++m)
-          if ((pending >> m & 1u) && xtag(w[m]) == tag) {
+          if ((pending >> m & 1u) && xok(w[m], tag)) {
             y[m] = xval(w[m]);
             pending &= ~(1u << m);
           }
