@@ -6,8 +6,10 @@
 // the matrix cores at the same instruction count: operand A holds vector b in
 // rows 2b (bf16 high part) and 2b+1 (remainder), and lane l of the result
 // holds vectors 2(l/16) and 2(l/16)+1 of row l%16.  Per step and half, the
-// heads evaluate every gate of every vector, run their O1 rows / O2 columns,
-// all-reduce 8 x 256 partial logits, and draw the 8 classes on 8 waves.
+// heads evaluate every gate of every vector, run their O1 rows / O2 columns
+// and publish 8 x 256 partial logits; the owner of each vector (head v mod NH)
+// sums that vector's partials, draws its class and publishes it, and every
+// head reads the 8 classes.
 #include "wr_kern.h"
 
 namespace {
@@ -81,8 +83,9 @@ __device__ __forceinline__ T* opaque(T* p) {
 // rebuilt in every round from an opaque base, so only the N words in flight
 // occupy registers.
 template <int N, class O, class F>
-__device__ __forceinline__ bool poll_put(const xw* base, O off, F put, uint32_t tag, const BatchArgs& a) {
-  uint32_t pending = N >= 32 ? ~0u : (1u << N) - 1u;
+__device__ __forceinline__ bool poll_put(const xw* base, O off, F put, uint32_t tag, const BatchArgs& a,
+                                         uint32_t need = ~0u) {
+  uint32_t pending = (N >= 32 ? ~0u : (1u << N) - 1u) & need;
   WaitBudget wb{wr_clock(), 0};
   for (;;) {
     const xw* b = opaque(base);
@@ -93,6 +96,28 @@ __device__ __forceinline__ bool poll_put(const xw* base, O off, F put, uint32_t 
     for (int k = 0; k < N; ++k)
       if ((pending >> k & 1u) && xok(w[k], tag)) {
         put(k, xval(w[k]));
+        pending &= ~(1u << k);
+      }
+    if (!pending) return true;
+    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+  }
+}
+
+// poll_put over N pairs of adjacent words read as 64-bit accesses:
+// put(k, first, second) for pair k at base + off(k) (off even).
+template <int N, class O, class F>
+__device__ __forceinline__ bool poll_put2(const xw* base, O off, F put, uint32_t tag, const BatchArgs& a) {
+  uint32_t pending = (1u << N) - 1u;
+  WaitBudget wb{wr_clock(), 0};
+  for (;;) {
+    const xw* b = opaque(base);
+    uint64_t w[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1u) ? xpeek2(b + off(k)) : 0;
+#pragma unroll
+    for (int k = 0; k < N; ++k)
+      if ((pending >> k & 1u) && xok2(w[k], tag)) {
+        put(k, xval((xw)w[k]), xval((xw)(w[k] >> 32)));
         pending &= ~(1u << k);
       }
     if (!pending) return true;
@@ -212,32 +237,52 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     xpub(dst + bl0 * 256 + c0 + 16, tag, mfma_row(B));
     xpub(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B));
   };
-  // Sums over the heads, in head order.  Lane jj of every wave first watches
-  // the last word head jj publishes; then thread (class v, parity h) reads the
-  // partials of vectors h, h + 2, h + 4, h + 6 of every head, two vectors at a
-  // time (all their heads' words in flight at once), re-reading only words that
-  // do not carry the step's tag yet.
-  auto gather_logits = [&](const xw* src, uint32_t tag) {
+  // Vector ownership: head j draws the vectors j, j + NH, ... of the group
+  // (slot q: vector j + NH q); every other head learns their classes from one
+  // word each.  Only the owner sums a vector's partial logits, so a head reads
+  // the partials of its own vectors, not of all 8.
+  constexpr int OV = (L + NH - 1) / NH;             // most vectors a head owns
+  constexpr int SP = (OV + 1) / 2;                  // owned slots per gathering thread
+  const int nown = (L - j + NH - 1) / NH;           // vectors this head owns
+  // Sums over the heads, in head order, of the owned vectors' partials.  Lane
+  // jj of every wave first watches the last word head jj publishes; then
+  // thread (class v, parity s) reads slots s, s + 2, ... of every head (all
+  // words in flight at once), re-reading only words without the step's tag.
+  auto gather_own = [&](const xw* src, uint32_t tag) {
     {
       float y;
       const int hj = lane < NH ? lane : 0;
       if (!wait_word(src + ((size_t)hj * L + L - 1) * 256 + 255, tag, &y, a)) misc[0] = 1;
     }
-    const int v = tid & 255, h = tid >> 8;
-    // word k (< 4 NH): head k % NH, vector h + 2 (k / NH); staged in gv (free
-    // here), all in flight at once
-    float* stage = gv + tid;                        // [4 NH][512]
-    if (!poll_put<4 * NH>(src + h * 256 + v, [&](int k) { return (size_t)((k % NH) * L + 2 * (k / NH)) * 256; },
-                          [&](int k, float x) { stage[k * WR_THREADS] = x; }, tag, a)) {
+    const int v = tid & 255, sp = tid >> 8;
+    // word k (< SP NH): head k % NH, slot sp + 2 (k / NH); staged in gv (free here)
+    float* stage = gv + tid;                        // [SP NH][512]
+    uint32_t need = 0;
+#pragma unroll
+    for (int k = 0; k < SP * NH; ++k)
+      if (sp + 2 * (k / NH) < nown) need |= 1u << k;
+    if (!poll_put<SP * NH>(src + v,
+                           [&](int k) { return (size_t)((k % NH) * L + j + NH * (sp + 2 * (k / NH))) * 256; },
+                           [&](int k, float x) { stage[k * WR_THREADS] = x; }, tag, a, need)) {
       misc[0] = 1;
       return;
     }
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
+    for (int m = 0; m < SP; ++m) {
+      if (sp + 2 * m >= nown) break;
       float s = 0.0f;
 #pragma unroll
       for (int jj = 0; jj < NH; ++jj) s += stage[(m * NH + jj) * WR_THREADS];
-      zs[(h + 2 * m) * 256 + v] = s;
+      zs[(sp + 2 * m) * 256 + v] = s;
+    }
+  };
+  // every head: the classes of all vectors of the group from their owners
+  auto receive = [&](const xw* cls, uint32_t tag, int slot, int64_t t_next) {
+    if (tid < L) {
+      float y;
+      if (!wait_word(cls + tid, tag, &y, a)) misc[0] = 1;
+      misc[slot + tid] = (int)y;
+      if (t_next >= 0 && t_next < a.T) cbo[tid] = cb_offset(a, min(v0 + tid, a.S - 1), t_next);
     }
   };
   // The 3L pre-activation words of gate thread u (two batches of loads) and
@@ -249,18 +294,35 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
 #pragma unroll
     for (int b = 0; b < L; ++b) gv[(3 * L + b) * 448 + u] = a.cb[cbo[b] + col];
     if (trg && col == 2 * H) trace_at(a, t, 13);
-    if (CTX && !poll_put<L>(XE + u, [&](int b) { return (size_t)b * Hh; },
-                             [&](int b, float x) { gv[(3 * L + b) * 448 + u] += x; }, tag, a)) {
+    // words of unit u: vector b of gate q at G[(q Hh + u) L + b], context term at XE[u L + b];
+    // read as pairs of vectors
+    if (CTX && !poll_put2<L / 2>(XE + (size_t)u * L, [&](int k) { return 2 * k; },
+                                  [&](int k, float x0, float x1) {
+                                    gv[(3 * L + 2 * k) * 448 + u] += x0;
+                                    gv[(3 * L + 2 * k + 1) * 448 + u] += x1;
+                                  }, tag, a)) {
       misc[0] = 1;
       return;
     }
-    if (!poll_put<3 * L>(G + u, [&](int k) { return (size_t)k * Hh; }, [&](int k, float x) { gv[k * 448 + u] = x; },
-                         tag, a))   // all 24 words in flight at once
-      misc[0] = 1;
+#pragma unroll 1
+    for (int hb = 0; hb < 2; ++hb) {                // pairs k = 6 hb .. 6 hb + 5 in flight together
+      const int k0 = hb * (3 * L / 4);
+      if (!poll_put2<3 * L / 4>(G + (size_t)u * L,
+                                [&](int k) { return (size_t)((k0 + k) / (L / 2)) * Hh * L + 2 * ((k0 + k) % (L / 2)); },
+                                [&](int k, float x0, float x1) {
+                                  const int q = (k0 + k) / (L / 2), b = 2 * ((k0 + k) % (L / 2));
+                                  gv[(3 * b + q) * 448 + u] = x0;
+                                  gv[(3 * b + 3 + q) * 448 + u] = x1;
+                                }, tag, a)) {
+        misc[0] = 1;
+        return;
+      }
+    }
   };
-  const int vw = min(v0 + wave, a.S - 1);          // the draw wave's vector
+  const int bw = j + NH * wave;                     // vector (in the group) drawn by this wave, if wave < nown
+  const int vw = min(v0 + bw, a.S - 1);
   const size_t ob = obase(a, vw);
-  auto fill_batch = [&](int64_t t, int buf) {       // wave w: vector w's uniforms / targets
+  auto fill_batch = [&](int64_t t, int buf) {       // wave w: uniforms / targets of its owned vector
     const int64_t s = t + lane;
     const int vb = vw;
     if (s < a.T) {
@@ -270,17 +332,20 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       tgt[(buf * L + wave) * 64 + lane] = a.target ? a.target[ob + (size_t)a.B * s] : 0;
     }
   };
-  fill_batch(0, 0);
+  if (wave < nown) fill_batch(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   const bool trw = g == 0 && j == 0 && tid == WR_THREADS - 64;
-  const bool live = v0 + wave < a.S;               // draw wave's vector is in use
+  const bool own = wave < nown;                     // this wave draws an owned vector
+  const bool live = own && v0 + bw < a.S;          // ... that is in use
+  xw* CC = X + P.x_cc;                              // drawn coarse classes [L]
+  xw* CF = X + P.x_cf;                              // drawn fine classes [L]
 
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     if (trw) trace_at(a, t, 0);
     const int bs = (int)((t >> 6) & 1) * L * 64 + wave * 64 + (int)(t & 63);   // draw wave's batch slot
-    if ((t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
+    if (own && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
     // (1) coarse gates of every unit and vector: the 24 pre-activation words of
     // thread u are polled together and staged in LDS, then one vector at a time
     if (gate) {
@@ -309,27 +374,29 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     first_layer(W1, imc, b1r);
     second_layer(W2, PCo, tag);
     if (trw) trace_at(a, t, 3);
-    // (3) sum over the heads, draw 8 coarse classes (wave w: vector w)
-    gather_logits(PC, tag);
+    // (3) the owned vectors' sums over the heads, their coarse draws (wave w:
+    // slot w), then every vector's class from its owner
+    gather_own(PC, tag);
     __syncthreads();
     if (misc[0]) return;
     if (trw) trace_at(a, t, 4);
-    {
+    if (own) {
       float lse;
       const int forced = a.target ? (tgt[bs] >> 8) : -1;
       const int c = draw_wave<false>(zs + wave * 256, nullptr, b2l, uni[bs].x, forced, zk + wave * 256,
                                      a.nll_out ? &lse : nullptr);
-      if (j == 0 && live && a.zc_out)
+      if (live && a.zc_out)
         *(float4*)(a.zc_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        misc[8 + wave] = c;
+        xpub(CC + bw, tag, (float)c);
         if (a.nll_out) {
           fmisc[wave] = lse;
           fmisc[8 + wave] = zk[wave * 256 + c];
         }
       }
     }
+    receive(CC, tag, 8, -1);
     __syncthreads();
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
@@ -362,32 +429,32 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     first_layer(W3, imf, b3r);
     second_layer(W4, PFo, tag);
     if (trw) trace_at(a, t, 8);
-    // (6) sum, draw 8 fine classes
-    gather_logits(PF, tag);
+    // (6) the owned vectors' fine sums and draws, then every vector's class
+    gather_own(PF, tag);
     __syncthreads();
     if (misc[0]) return;
     if (trw) trace_at(a, t, 9);
-    {
+    if (own) {
       float lse;
       const int forced = a.target ? (tgt[bs] & 255) : -1;
       const int f = draw_wave<false>(zs + wave * 256, nullptr, b4l, uni[bs].y, forced, zk + wave * 256,
                                      a.nll_out ? &lse : nullptr);
-      const int c = misc[8 + wave];
-      if (j == 0 && live && a.zf_out)
+      const int c = misc[8 + bw];
+      if (live && a.zf_out)
         *(float4*)(a.zf_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        if (j == 0 && live) {
+        xpub(CF + bw, tag, (float)f);
+        if (a.ux) xpub(X + P.x_sp + bw, tag, (float)(256 * c + f));   // for the context of later rows
+        if (live) {
           if (a.out) a.out[ob + (size_t)a.B * t] = (uint16_t)(256 * c + f);
           if (a.nll_out)
             a.nll_out[ob + (size_t)a.B * t] = (fmisc[wave] - fmisc[8 + wave]) + (lse - zk[wave * 256 + f]);
-          if (a.ux) xpub(X + P.x_sp + wave, tag, (float)(256 * c + f));   // for the context of later rows
         }
-        misc[16 + wave] = c;
-        misc[24 + wave] = f;
-        if (t + 1 < a.T) cbo[wave] = cb_offset(a, vw, t + 1);
       }
     }
+    receive(CF, tag, 24, t + 1);
+    if (tid < L) misc[16 + tid] = misc[8 + tid];
     __syncthreads();
     if (trw) trace_at(a, t, 10);
   }
@@ -428,7 +495,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   const int bl0 = 2 * (lane >> 4);
   const int v0 = g * L;
   xw* X = a.xc + (size_t)g * P.x_words;
-  xw* dst = X + (fw ? P.x_gf : P.x_ga) + gt * Hh + i;        // + vector * 3 Hh
+  xw* dst = X + (fw ? P.x_gf : P.x_ga) + (size_t)(gt * Hh + i) * L + bl0;   // vectors bl0, bl0 + 1
   {
     const uint4* src = a.uw + (size_t)k * (P.u_lds_w / 16);
     for (int x = tid; x < P.u_lds_w / 16; x += WR_THREADS) ((uint4*)lds)[x] = src[x];
@@ -484,14 +551,10 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     }
   };
   f32x4 xa0 = {0, 0, 0, 0}, xa1 = {0, 0, 0, 0};        // context term of e-gate rows
-  xw* dstx = X + (fw ? P.x_xf : P.x_xc) + i;          // + vector * Hh
+  xw* dstx = X + (fw ? P.x_xf : P.x_xc) + (size_t)i * L + bl0;
   auto publish = [&](uint32_t tag, float cb0, float cb1) {
-    xpub(dst + (size_t)bl0 * 3 * Hh, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0);
-    xpub(dst + (size_t)(bl0 + 1) * 3 * Hh, tag, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
-    if (CTX && gt == 2) {
-      xpub(dstx + (size_t)bl0 * Hh, tag, mfma_row(xa0) + mfma_row(xa1));
-      xpub(dstx + (size_t)(bl0 + 1) * Hh, tag, mfma_row_hi(xa0) + mfma_row_hi(xa1));
-    }
+    xpub2(dst, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
+    if (CTX && gt == 2) xpub2(dstx, tag, mfma_row(xa0) + mfma_row(xa1), mfma_row_hi(xa0) + mfma_row_hi(xa1));
   };
   // Subscale context (Sec. 4): the samples of row t of every utterance of this
   // group join the history; vector b's context for row t + 1 is the Dx/2

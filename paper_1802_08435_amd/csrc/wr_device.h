@@ -128,6 +128,17 @@ __device__ __forceinline__ xw xpeek(const xw* p) {
 }
 __device__ __forceinline__ bool xok(xw w, uint32_t tag) { return ((w ^ tag) & 1u) == 0; }
 __device__ __forceinline__ float xval(xw w) { return __uint_as_float(w & ~1u); }
+// Two adjacent words (p 8-byte aligned) written and read as one 64-bit access.
+__device__ __forceinline__ void xpub2(xw* p, uint32_t tag, float v0, float v1) {
+  const uint64_t w = (uint64_t)((__float_as_uint(v0) & ~1u) | (tag & 1u)) |
+                     (uint64_t)((__float_as_uint(v1) & ~1u) | (tag & 1u)) << 32;
+  __hip_atomic_store((uint64_t*)p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t xpeek2(const xw* p) {
+  return __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool xok2(uint64_t w, uint32_t tag) { return xok((xw)w, tag) && xok((xw)(w >> 32), tag); }
+
 // A value as a reader of the exchange sees it (so that state handed in by the
 // caller enters a computation exactly as the exchanged values do).
 __device__ __forceinline__ float xround(float v) { return __uint_as_float(__float_as_uint(v) & ~1u); }

@@ -237,8 +237,9 @@ struct BatchPlan {
   int H, Hh, KT, KH, NH, NCT, NU, G, grid;
   int hw_frags;           // head fragments per wave (as the batch-1 plan)
   int u_lds_w;            // unit LDS weights: [UCT][KT] coarse tiles, then [UCT][KT] fine tiles
-  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_sp, x_xc, x_xf, x_words;   // per group: y [L][Hh],
-      // g [L][3][Hh], p [NH][L][256], drawn samples [L], e-gate context terms [L][Hh] x 2
+  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_sp, x_xc, x_xf, x_cc, x_cf, x_words;   // per group: y [L][Hh],
+      // g [3][Hh][L], p [NH][L][256], drawn samples [L], e-gate context terms [Hh][L] x 2,
+      // drawn coarse and fine classes [L] each
   int KX;                 // subscale context column tiles (Dx / 32), 0 without context
   int lds_h, lds_u, lds;
 };
@@ -285,6 +286,8 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   P->x_sp = take(WR_BL);
   P->x_xc = take(WR_BL * P->Hh);
   P->x_xf = take(WR_BL * P->Hh);
+  P->x_cc = take(WR_BL);
+  P->x_cf = take(WR_BL);
   P->x_words = o;
   // head: operand images (2 KT + 2 fragments), first-layer partials [2][L][64],
   // logit sums [L][256], logits [L][256], both halves of h and the staged
