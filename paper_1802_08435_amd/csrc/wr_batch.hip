@@ -14,7 +14,6 @@
 
 namespace {
 
-constexpr int L = WR_BL;
 
 // Vector v is lane v % B of utterance v / B; at step t it makes sample
 // n = B (t0 + t) + v % B of that utterance (Sec. 4; B = 1: n = t0 + t).
@@ -125,13 +124,35 @@ __device__ __forceinline__ bool poll_put2(const xw* base, O off, F put, uint32_t
   }
 }
 
+// Drawn samples for the subscale context cross groups, whose heads and units
+// are not chained step by step to each other: a sample word carries the
+// sample (16 bits) and the low 16 bits of its tag, in one of two slots chosen
+// by the tag's parity, so a producer one step ahead writes the other slot.
+__device__ __forceinline__ void spub(xw* slots, int L, int v, uint32_t tag, int sample) {
+  __hip_atomic_store(slots + (tag & 1u) * L + v, (tag & 0xffffu) << 16 | (uint32_t)sample, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool wait_sample(const xw* slots, int L, int v, uint32_t tag, int* sample,
+                                            const BatchArgs& a) {
+  const xw* p = slots + (tag & 1u) * L + v;
+  WaitBudget wb{wr_clock(), 0};
+  for (;;) {
+    const xw w = xpeek(p);
+    if ((w >> 16) == (tag & 0xffffu)) {
+      *sample = (int)(w & 0xffffu);
+      return true;
+    }
+    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
+  }
+}
+
 // Wait until *p carries `tag` (the slow path of the straight-line reads below).
 __device__ __forceinline__ bool wait_word(const xw* p, uint32_t tag, float* v, const BatchArgs& a) {
   return poll_map<1>([&](int) { return p; }, tag, v, a);
 }
 
 // ------------------------------------------------------------------ head role
-template <int KH, bool CTX>
+template <int KH, bool CTX, int L>
 __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   constexpr int NH = KH;
@@ -218,10 +239,13 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       if (i + 1 < KH) acc1 = mfma(afrag(img, kc * KH + i + 1), W[i + 1], acc1);
     }
     const int r = 16 * rt + (lane & 15);
-    op[(kc * L + bl0) * 64 + r] = mfma_row(acc0) + mfma_row(acc1);
-    op[(kc * L + bl0 + 1) * 64 + r] = mfma_row_hi(acc0) + mfma_row_hi(acc1);
+    if (bl0 < L) {                                  // lanes of vectors past L hold rows of zero inputs
+      op[(kc * L + bl0) * 64 + r] = mfma_row(acc0) + mfma_row(acc1);
+      op[(kc * L + bl0 + 1) * 64 + r] = mfma_row_hi(acc0) + mfma_row_hi(acc1);
+    }
     __syncthreads();
-    aput(imo + (rr >> 5) * WR_FRAG, rr & 31, wr_relu((op[rb * 64 + rr] + op[(L + rb) * 64 + rr]) + bias), rb);
+    if (rb < L)
+      aput(imo + (rr >> 5) * WR_FRAG, rr & 31, wr_relu((op[rb * 64 + rr] + op[(L + rb) * 64 + rr]) + bias), rb);
     __syncthreads();
   };
   // class tiles 2*wave, 2*wave+1 over this head's 64 columns, for all vectors
@@ -232,10 +256,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     A = mfma(x1, W[1], A);
     B = mfma(x1, W[3], B);
     const int c0 = 32 * wave + (lane & 15);
-    xpub(dst + bl0 * 256 + c0, tag, mfma_row(A));
-    xpub(dst + (bl0 + 1) * 256 + c0, tag, mfma_row_hi(A));
-    xpub(dst + bl0 * 256 + c0 + 16, tag, mfma_row(B));
-    xpub(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B));
+    if (bl0 < L) {
+      xpub(dst + bl0 * 256 + c0, tag, mfma_row(A));
+      xpub(dst + (bl0 + 1) * 256 + c0, tag, mfma_row_hi(A));
+      xpub(dst + bl0 * 256 + c0 + 16, tag, mfma_row(B));
+      xpub(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B));
+    }
   };
   // Vector ownership: head j draws the vectors j, j + NH, ... of the group
   // (slot q: vector j + NH q); every other head learns their classes from one
@@ -304,10 +330,11 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       misc[0] = 1;
       return;
     }
+    constexpr int NB = L > 4 ? 2 : 1, PB = 3 * L / 2 / NB;   // batches of PB pairs in flight together
 #pragma unroll 1
-    for (int hb = 0; hb < 2; ++hb) {                // pairs k = 6 hb .. 6 hb + 5 in flight together
-      const int k0 = hb * (3 * L / 4);
-      if (!poll_put2<3 * L / 4>(G + (size_t)u * L,
+    for (int hb = 0; hb < NB; ++hb) {
+      const int k0 = hb * PB;
+      if (!poll_put2<PB>(G + (size_t)u * L,
                                 [&](int k) { return (size_t)((k0 + k) / (L / 2)) * Hh * L + 2 * ((k0 + k) % (L / 2)); },
                                 [&](int k, float x0, float x1) {
                                   const int q = (k0 + k) / (L / 2), b = 2 * ((k0 + k) % (L / 2));
@@ -445,7 +472,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
         xpub(CF + bw, tag, (float)f);
-        if (a.ux) xpub(X + P.x_sp + bw, tag, (float)(256 * c + f));   // for the context of later rows
+        if (a.ux) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for the context of later rows
         if (live) {
           if (a.out) a.out[ob + (size_t)a.B * t] = (uint16_t)(256 * c + f);
           if (a.nll_out)
@@ -476,7 +503,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
 // Wave q < 4 owns coarse row tile 4k + q, wave 4 + q fine row tile 4k + q;
 // each lane of a wave's result holds two vectors of one row, which it
 // publishes (with bias + conditioning for the u and r gates).
-template <int KH, bool CTX>
+template <int KH, bool CTX, int L>
 __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   const BatchPlan& P = a.P;
@@ -553,6 +580,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   f32x4 xa0 = {0, 0, 0, 0}, xa1 = {0, 0, 0, 0};        // context term of e-gate rows
   xw* dstx = X + (fw ? P.x_xf : P.x_xc) + (size_t)i * L + bl0;
   auto publish = [&](uint32_t tag, float cb0, float cb1) {
+    if (bl0 >= L) return;                               // rows of vectors past L: zero inputs, not published
     xpub2(dst, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
     if (CTX && gt == 2) xpub2(dstx, tag, mfma_row(xa0) + mfma_row(xa1), mfma_row_hi(xa0) + mfma_row_hi(xa1));
   };
@@ -567,11 +595,11 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     const uint32_t tag = (uint32_t)(t + 1);
     if (tid < nut * a.B) {                             // one thread per (utterance, lane)
       const int vv = ub0 * a.B + tid;                  // vector of that lane
-      float y;
+      int y = 0;
       if (vv < a.S) {
-        if (!wait_word(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp + vv % L, tag, &y, a)) misc[0] = 1;
+        if (!wait_sample(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp, L, vv % L, tag, &y, a)) misc[0] = 1;
         const int64_t qn = (int64_t)a.B * t + tid % a.B;
-        hist[(tid / a.B) * 256 + (int)(qn & 255)] = (int)y;
+        hist[(tid / a.B) * 256 + (int)(qn & 255)] = y;
       }
     }
     __syncthreads();
@@ -607,7 +635,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     }
   };
   auto cbv = [&](int b, int64_t t) {                           // u and r gates carry bias + conditioning
-    return gt < 2 ? a.cb[cb_offset(a, min(v0 + b, a.S - 1), t) + row] : 0.0f;
+    return gt < 2 && b < L ? a.cb[cb_offset(a, min(v0 + b, a.S - 1), t) + row] : 0.0f;
   };
   // Wait for one half of h of all 8 vectors: lane jj of wave 0 first watches
   // the last word head jj publishes (vector 7), then every thread reads its
@@ -683,22 +711,29 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
 
 }  // namespace
 
-template <int KH, bool CTX>
+template <int KH, bool CTX, int L>
 __global__ __launch_bounds__(WR_THREADS, 1) void wr_batch_kernel(BatchArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   int g = 0;
   const int r = wr_batch_role(a.P, blockIdx.x, &g);
   if (r < 0) return;
-  if (r < a.P.NH) bhead_role<KH, CTX>(a, g, r, lds);
-  else bunit_role<KH, CTX>(a, g, r - a.P.NH, lds);
+  if (r < a.P.NH) bhead_role<KH, CTX, L>(a, g, r, lds);
+  else bunit_role<KH, CTX, L>(a, g, r - a.P.NH, lds);
 }
 
-const void* wr_batch_kernel_ptr(int KH, bool ctx) {
+template <int KH>
+static const void* batch_ptr(bool ctx, int L) {
+  if (L == 4) return ctx ? (const void*)wr_batch_kernel<KH, true, 4> : (const void*)wr_batch_kernel<KH, false, 4>;
+  if (L == 8) return ctx ? (const void*)wr_batch_kernel<KH, true, 8> : (const void*)wr_batch_kernel<KH, false, 8>;
+  return nullptr;
+}
+
+const void* wr_batch_kernel_ptr(int KH, bool ctx, int L) {
   switch (KH) {
-    case 1: return ctx ? (const void*)wr_batch_kernel<1, true> : (const void*)wr_batch_kernel<1, false>;
-    case 2: return ctx ? (const void*)wr_batch_kernel<2, true> : (const void*)wr_batch_kernel<2, false>;
-    case 3: return ctx ? (const void*)wr_batch_kernel<3, true> : (const void*)wr_batch_kernel<3, false>;
-    case 7: return ctx ? (const void*)wr_batch_kernel<7, true> : (const void*)wr_batch_kernel<7, false>;
+    case 1: return batch_ptr<1>(ctx, L);
+    case 2: return batch_ptr<2>(ctx, L);
+    case 3: return batch_ptr<3>(ctx, L);
+    case 7: return batch_ptr<7>(ctx, L);
     default: return nullptr;
   }
 }

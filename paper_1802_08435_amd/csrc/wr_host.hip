@@ -78,7 +78,6 @@ struct wavernn_model {
   // batched path (several utterances per launch)
   bool has_batch = false;
   BatchPlan bplan;
-  const void* bk = nullptr;          // kernel instantiation for bplan.KH
   uint4 *d_buw = nullptr, *d_bur = nullptr, *d_bux = nullptr;
   xw* d_bxc = nullptr;
   float* d_bcb = nullptr;            // [streams][frames][3H]
@@ -413,8 +412,6 @@ wavernn_status build_sparse(wavernn_model* m, const wavernn_weights* w) {
 wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   const BatchPlan& B = m->bplan;
   const int H = B.H, Hh = B.Hh, KT = B.KT;
-  m->bk = wr_batch_kernel_ptr(B.KH, B.KX > 0);
-  if (!m->bk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no batched kernel instantiation", H);
   REff R{&m->cfg, w};
   auto frag = [&](uint16_t* dst, int tile, bool fine, int col0) {
     for (int l = 0; l < 64; ++l) {
@@ -457,15 +454,20 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   }
   if ((s = m->upload(&m->d_buw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
   if ((s = m->upload(&m->d_bur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->alloc(&m->d_bxc, ((size_t)B.G * B.x_words + 1) / 2 * 8)) != WAVERNN_OK) return s;
-  HIPOK(hipFuncSetAttribute(m->bk, hipFuncAttributeMaxDynamicSharedMemorySize, B.lds));
-  int per_cu = 0;
-  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->bk, WR_THREADS, B.lds));
-  hipDeviceProp_t prop;
-  HIPOK(hipGetDeviceProperties(&prop, m->device));
-  if (per_cu < 1 || per_cu * prop.multiProcessorCount < B.grid)
-    return fail(WAVERNN_E_UNSUPPORTED, "batched grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)",
-                B.grid, per_cu, prop.multiProcessorCount);
+  // every plan a call may use: 4 vectors per group up to 32 vectors, 8 above;
+  // the largest grid of each group size must fit, and the exchange buffer
+  // holds the largest of them
+  const int maxv = m->cfg.max_streams * m->cfg.subscale;
+  size_t xwords = 0;
+  for (int v : {std::min(maxv, 4 * WR_BL), maxv}) {
+    BatchPlan Q;
+    if (!batch_plan(H, v, &Q, m->cfg.ctx_dim)) return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors", v);
+    const void* k = wr_batch_kernel_ptr(Q.KH, Q.KX > 0, Q.L);
+    if (!k) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no batched kernel instantiation", H);
+    if ((s = check_coresident(m, k, Q.grid, Q.lds, "batched")) != WAVERNN_OK) return s;
+    xwords = std::max(xwords, (size_t)Q.G * Q.x_words);
+  }
+  if ((s = m->alloc(&m->d_bxc, (xwords + 1) / 2 * 8)) != WAVERNN_OK) return s;
   m->has_batch = true;
   return WAVERNN_OK;
 }
@@ -642,6 +644,8 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   }
   wavernn_status st = launch_cond(m, io.cond, n_cb, io.S, m->d_bcb, io.st);
   if (st != WAVERNN_OK) return st;
+  const void* kernel = wr_batch_kernel_ptr(B.KH, B.KX > 0, B.L);
+  if (!kernel) return fail(WAVERNN_E_UNSUPPORTED, "no batched kernel for %d vectors", V);
   if ((st = launch_fill(m->d_bxc, (int64_t)B.G * B.x_words, io.st)) != WAVERNN_OK) return st;
   BatchArgs a;
   memset(&a, 0, sizeof a);
@@ -677,7 +681,7 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.trace_steps = m->trace ? m->trace_steps : 0;
   void* args[] = {&a};
   // an ordinary launch, as for the batch-1 kernel (co-residency checked at create)
-  HIPOK(hipLaunchKernel(m->bk, dim3(B.grid), dim3(WR_THREADS), args, B.lds, io.st));
+  HIPOK(hipLaunchKernel(kernel, dim3(B.grid), dim3(WR_THREADS), args, B.lds, io.st));
   return WAVERNN_OK;
 }
 
@@ -717,9 +721,9 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
   if (B > 1) {
     // Subscale (Sec. 4): the B lanes of each utterance are vectors of the
     // batched kernel; its unit workgroups add the context projection.
-    if (!((B % WR_BL == 0) || (WR_BL % B == 0)) || cfg->ctx_dim % 32 || cfg->ctx_dim > 256)
-      s = fail(WAVERNN_E_UNSUPPORTED, "subscale %d / ctx_dim %d: need B dividing or divided by 8, ctx_dim a multiple "
-               "of 32 up to 256", B, cfg->ctx_dim);
+    if (!((B % 8 == 0) || (4 % B == 0)) || cfg->ctx_dim % 32 || cfg->ctx_dim > 256)
+      s = fail(WAVERNN_E_UNSUPPORTED, "subscale %d / ctx_dim %d: need B a multiple of 8 or a divisor of 4 (lanes "
+               "must tile groups of 4 and 8 vectors), ctx_dim a multiple of 32 up to 256", B, cfg->ctx_dim);
     else if (cfg->weight_dtype != WAVERNN_BF16)
       s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling needs bf16 weights");
     else if (!persist_plan(H, &m->plan) || !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim))

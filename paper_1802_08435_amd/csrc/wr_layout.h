@@ -220,7 +220,8 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
 
 // ---------------------------------------------------------------------------
 // Batched persistent kernel: G groups, each a copy of the batch-1 structure
-// serving WR_BL vectors (independent utterances) at once.  The MFMA operand A
+// serving L vectors (independent utterances or subscale lanes) at once: L = 4
+// up to 32 vectors (more groups, half the words each head reads), else 8.  The MFMA operand A
 // carries vector b in rows 2b (bf16 high part) and 2b+1 (remainder), so a
 // group does the same number of matrix-core instructions as batch 1.
 // Head j of group g sits at block 8j + g (one XCD per group); the units of all
@@ -229,16 +230,17 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
 // in VGPRs), waves 4-7 the fine tiles (coarse columns in VGPRs, fine columns
 // in LDS).
 // ---------------------------------------------------------------------------
-#define WR_BL 8           // vectors per group
+#define WR_BL 8           // most vectors per group
 #define WR_BUCT 4         // coarse (and fine) row tiles per batched unit
 #define WR_HIST 16        // rows of drawn samples a batched unit keeps (subscale context)
 
 struct BatchPlan {
   int H, Hh, KT, KH, NH, NCT, NU, G, grid;
+  int L;                  // vectors per group (4 or 8)
   int hw_frags;           // head fragments per wave (as the batch-1 plan)
   int u_lds_w;            // unit LDS weights: [UCT][KT] coarse tiles, then [UCT][KT] fine tiles
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_sp, x_xc, x_xf, x_cc, x_cf, x_words;   // per group: y [L][Hh],
-      // g [3][Hh][L], p [NH][L][256], drawn samples [L], e-gate context terms [Hh][L] x 2,
+      // g [3][Hh][L], p [NH][L][256], drawn samples [2][L], e-gate context terms [Hh][L] x 2,
       // drawn coarse and fine classes [L] each
   int KX;                 // subscale context column tiles (Dx / 32), 0 without context
   int lds_h, lds_u, lds;
@@ -269,7 +271,8 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   P->NCT = 3 * P->Hh / 16;
   if (P->NH > 7 || P->Hh > WR_THREADS - 64 || P->NCT % WR_BUCT) return false;
   P->NU = P->NCT / WR_BUCT;
-  P->G = (n_vectors + WR_BL - 1) / WR_BL;
+  P->L = n_vectors <= 4 * WR_BL ? WR_BL / 2 : WR_BL;
+  P->G = (n_vectors + P->L - 1) / P->L;
   int gr = 8 * (P->NH - 1) + P->G;           // the last head block + 1
   while (gr - P->NH * P->G < P->NU * P->G) ++gr;
   P->grid = gr;
@@ -277,24 +280,24 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   P->u_lds_w = 2 * WR_BUCT * P->KT * WR_FRAG;
   int o = 0;
   auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
-  P->x_yc = take(WR_BL * P->Hh);
-  P->x_yf = take(WR_BL * P->Hh);
-  P->x_ga = take(WR_BL * 3 * P->Hh);
-  P->x_gf = take(WR_BL * 3 * P->Hh);
-  P->x_pc = take(P->NH * WR_BL * 256);
-  P->x_pf = take(P->NH * WR_BL * 256);
-  P->x_sp = take(WR_BL);
-  P->x_xc = take(WR_BL * P->Hh);
-  P->x_xf = take(WR_BL * P->Hh);
-  P->x_cc = take(WR_BL);
-  P->x_cf = take(WR_BL);
+  P->x_yc = take(P->L * P->Hh);
+  P->x_yf = take(P->L * P->Hh);
+  P->x_ga = take(P->L * 3 * P->Hh);
+  P->x_gf = take(P->L * 3 * P->Hh);
+  P->x_pc = take(P->NH * P->L * 256);
+  P->x_pf = take(P->NH * P->L * 256);
+  P->x_sp = take(2 * P->L);
+  P->x_xc = take(P->L * P->Hh);
+  P->x_xf = take(P->L * P->Hh);
+  P->x_cc = take(P->L);
+  P->x_cf = take(P->L);
   P->x_words = o;
   // head: operand images (2 KT + 2 fragments), first-layer partials [2][L][64],
   // logit sums [L][256], logits [L][256], both halves of h and the staged
   // gate inputs [2 + 4][L][448], bias row offsets [L], misc [64],
   // uniforms [2][L][64][2], targets [2][L][64]
-  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * WR_BL * 64 + 2 * WR_BL * 256 + 6 * WR_BL * 448 + 2 * WR_BL + 64 +
-                                               2 * WR_BL * 64 * 2 + 2 * WR_BL * 64);
+  P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * P->L * 64 + 2 * P->L * 256 + 6 * P->L * 448 + 2 * P->L + 64 +
+                                               2 * P->L * 64 * 2 + 2 * P->L * 64);
   // unit: weights, operand image (2 KT fragments), context image (KX fragments),
   // sample history [WR_HIST][64], misc [16]
   P->lds_u = P->u_lds_w + (2 * P->KT + P->KX) * WR_FRAG + 4 * (WR_HIST * 64 + 16);
