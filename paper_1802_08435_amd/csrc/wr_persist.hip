@@ -328,7 +328,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   };
   // wide: finish the gates of units tid + 512 m with the drawn input x (I*
   // column q of the row) into h (LDS) and the operand image
-  auto wide_gates = [&](float x, int q, float* h, unsigned char* img) {
+  auto wide_gates = [&](float x, int q, float* h, unsigned char* img, xw* Y, uint32_t tag) {
 #pragma unroll
     for (int m = 0; m < (Hh + WR_THREADS - 1) / WR_THREADS; ++m) {
       const int un = tid + WR_THREADS * m;
@@ -340,6 +340,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       const float hn = __builtin_fmaf(uu, h[un], (1.0f - uu) * e);
       h[un] = hn;
       aput(img + (un >> 5) * WR_FRAG, un & 31, hn);
+      if ((unsigned)(un - HR * jk) < (unsigned)HR) xpub(Y + un, tag, hn);   // this head's slice, for the units
     }
   };
   coarse_pre(1u, fscale(misc[2]), a.t0);
@@ -357,7 +358,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (wave == DW && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
     // (1) coarse gates of every unit, finished with f_{t-1}
     if (WIDE) {
-      if (coarse) wide_gates(fscale(misc[3]), 1, yv, imc);
+      if (coarse) wide_gates(fscale(misc[3]), 1, yv, imc, YC, tag);
     } else if (gate && coarse) {
       const float x1 = fscale(misc[3]);
       const float uu = fsig(__builtin_fmaf(ic[0][1], x1, cu)), rr = fsig(__builtin_fmaf(ic[1][1], x1, cr));
@@ -369,7 +370,6 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     }
     __syncthreads();
     if (trw) trace_at(a, t, 1);
-    if (WIDE && coarse && wave == DW && lane < HR) xpub(YC + HR * jk + lane, tag, yv[HR * jk + lane]);
     if (trw) trace_at(a, t, 19);
     // (2) own rows of O1 -> relu -> own columns of O2 -> partial coarse logits
     if (coarse) {
@@ -410,7 +410,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     // (5) fine gates of every unit, finished with c_t (c_t reaches the fine half only)
     const int c = misc[1];
     if (WIDE) {
-      if (fine) wide_gates(fscale(c), 4, hfv, imf);
+      if (fine) wide_gates(fscale(c), 4, hfv, imf, YF, tag);
     } else if (gate && fine) {
       const float x2 = fscale(c);
       const float uu = fsig(__builtin_fmaf(ifn[0][2], x2, fu)), rr = fsig(__builtin_fmaf(ifn[1][2], x2, fr));
@@ -422,7 +422,6 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     }
     __syncthreads();
     if (trw) trace_at(a, t, 6);
-    if (WIDE && fine && wave == DW && lane < HR) xpub(YF + HR * jk + lane, tag, hfv[HR * jk + lane]);
     if (trw) trace_at(a, t, 22);
     // (6) own rows of O3 -> relu -> own columns of O4 -> partial fine logits
     if (fine) {
