@@ -342,7 +342,8 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
 
 // Block-sparse R (Sec. 3.2): the kept entries of every row as records of the
 // block-sparse unit workgroups (layout in sparse_plan).  Rows per unit SR is
-// the first of 64, 128, 32, 16 whose records fit LDS and whose grid fits.
+// the first of 32, 64, 128, 16 whose records fit LDS and whose grid fits
+// (fewer rows per unit: shorter record walks on the way to the heads).
 wavernn_status build_sparse(wavernn_model* m, const wavernn_weights* w) {
   const wavernn_config& c = m->cfg;
   const int H = c.hidden, Hh = H / 2;
@@ -366,7 +367,7 @@ wavernn_status build_sparse(wavernn_model* m, const wavernn_weights* w) {
   HIPOK(hipGetDeviceProperties(&prop, m->device));
   PersistPlan& P = m->plan;
   bool ok = false;
-  for (int SR : {64, 128, 32, 16}) {
+  for (int SR : {32, 64, 128, 16}) {
     const int SL = 256 / SR;
     auto nrec = [&](size_t len) { return std::max(1, (int)((len + SL - 1) / SL + 3) / 4); };
     if (sparse_plan(H, SR, nrec(maxlen[0]), nrec(maxlen[1]), &P) && P.grid <= prop.multiProcessorCount) {
