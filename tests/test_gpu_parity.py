@@ -410,3 +410,33 @@ def test_sync_floor_runs_below_the_step_time(name):
     m.device_status()
     step = e0.elapsed_time(e1) * 1000.0 / T
     assert 0.5 < floor < step, (floor, step)
+
+
+@pytest.mark.parametrize("kind", ["persistent", "block-sparse", "batched", "subscale"])
+@pytest.mark.parametrize("T", [1, 2, 65])
+def test_short_runs_match_the_oracle(kind, T):
+    """Edge lengths: one step (no unit iteration at all), two steps, and one
+    step past a 64-step uniform batch, on every multi-workgroup path."""
+    H, S, fmt, B = 256, 1, "dense", 1
+    kw = dict(cond_dim=16)
+    if kind == "block-sparse":
+        kw.update(block=(4, 4), density=0.1)
+        fmt = "bsr4x4"
+    if kind == "batched":
+        S = 3
+    if kind == "subscale":
+        B = 4
+        kw.update(B=B, ctx_dim=256)
+    w = synth.make_weights(H, seed=12, **kw)
+    n = T * B
+    feat = synth.features(S, n, cond_dim=16, per_stream_seed=True)
+    tgt = _targets(S, n)
+    m = wavernn.Model(w, dtype="bf16", r_format=fmt, max_streams=S)
+    assert m.path(S)[0] == {"subscale": "batched"}.get(kind, kind)
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, n, feat=feat, target=tgt, logits=True, nll=True)
+    assert np.abs(r["zc"] - ref["zc"]).max() <= 1e-3 and np.abs(r["zf"] - ref["zf"]).max() <= 1e-3
+    out = host(m.sample(n, cond=cuda(feat), seed=3, n_streams=S))
+    m.device_status()
+    assert out.shape == (S, n)
