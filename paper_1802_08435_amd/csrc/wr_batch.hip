@@ -723,6 +723,7 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_batch_kernel(BatchArgs a) {
 
 template <int KH>
 static const void* batch_ptr(bool ctx, int L) {
+  if (L == 2) return ctx ? (const void*)wr_batch_kernel<KH, true, 2> : (const void*)wr_batch_kernel<KH, false, 2>;
   if (L == 4) return ctx ? (const void*)wr_batch_kernel<KH, true, 4> : (const void*)wr_batch_kernel<KH, false, 4>;
   if (L == 8) return ctx ? (const void*)wr_batch_kernel<KH, true, 8> : (const void*)wr_batch_kernel<KH, false, 8>;
   return nullptr;

@@ -455,12 +455,12 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   }
   if ((s = m->upload(&m->d_buw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
   if ((s = m->upload(&m->d_bur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
-  // every plan a call may use: 4 vectors per group up to 32 vectors, 8 above;
-  // the largest grid of each group size must fit, and the exchange buffer
-  // holds the largest of them
+  // every plan a call may use (2 vectors per group up to 16 vectors, 4 up to
+  // 32, 8 above): the largest grid of each group size must fit, and the
+  // exchange buffer holds the largest of them
   const int maxv = m->cfg.max_streams * m->cfg.subscale;
   size_t xwords = 0;
-  for (int v : {std::min(maxv, 4 * WR_BL), maxv}) {
+  for (int v : {std::min(maxv, 2 * WR_BL), std::min(maxv, 4 * WR_BL), maxv}) {
     BatchPlan Q;
     if (!batch_plan(H, v, &Q, m->cfg.ctx_dim)) return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors", v);
     const void* k = wr_batch_kernel_ptr(Q.KH, Q.KX > 0, Q.L);
@@ -724,7 +724,7 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
     // batched kernel; its unit workgroups add the context projection.
     if (!((B % 8 == 0) || (4 % B == 0)) || cfg->ctx_dim % 32 || cfg->ctx_dim > 256)
       s = fail(WAVERNN_E_UNSUPPORTED, "subscale %d / ctx_dim %d: need B a multiple of 8 or a divisor of 4 (lanes "
-               "must tile groups of 4 and 8 vectors), ctx_dim a multiple of 32 up to 256", B, cfg->ctx_dim);
+               "must tile groups of 2, 4 and 8 vectors), ctx_dim a multiple of 32 up to 256", B, cfg->ctx_dim);
     else if (cfg->weight_dtype != WAVERNN_BF16)
       s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling needs bf16 weights");
     else if (!persist_plan(H, &m->plan) || !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim))

@@ -220,8 +220,9 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
 
 // ---------------------------------------------------------------------------
 // Batched persistent kernel: G groups, each a copy of the batch-1 structure
-// serving L vectors (independent utterances or subscale lanes) at once: L = 4
-// up to 32 vectors (more groups, half the words each head reads), else 8.  The MFMA operand A
+// serving L vectors (independent utterances or subscale lanes) at once: as
+// few per group as 8 groups allow (L = 2 up to 16 vectors, 4 up to 32, else 8),
+// so each head reads and evaluates as few gate words as possible.  The MFMA operand A
 // carries vector b in rows 2b (bf16 high part) and 2b+1 (remainder), so a
 // group does the same number of matrix-core instructions as batch 1.
 // Head j of group g sits at block 8j + g (one XCD per group); the units of all
@@ -271,7 +272,7 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   P->NCT = 3 * P->Hh / 16;
   if (P->NH > 7 || P->Hh > WR_THREADS - 64 || P->NCT % WR_BUCT) return false;
   P->NU = P->NCT / WR_BUCT;
-  P->L = n_vectors <= 4 * WR_BL ? WR_BL / 2 : WR_BL;
+  P->L = n_vectors <= 2 * WR_BL ? WR_BL / 4 : n_vectors <= 4 * WR_BL ? WR_BL / 2 : WR_BL;
   P->G = (n_vectors + P->L - 1) / P->L;
   int gr = 8 * (P->NH - 1) + P->G;           // the last head block + 1
   while (gr - P->NH * P->G < P->NU * P->G) ++gr;

@@ -113,11 +113,11 @@ def test_persistent_teacher_forced_small_sizes(H):
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
 
 
-@pytest.mark.parametrize("H,S", [(128, 2), (256, 9), (384, 16), (256, 40)])
+@pytest.mark.parametrize("H,S", [(128, 2), (256, 9), (384, 16), (256, 24), (256, 40)])
 def test_batched_teacher_forced_small_sizes(H, S):
-    """Several utterances in one launch (4 per group up to 32 utterances, 8
-    above; S=9 leaves 3 idle vectors in the last group, S=40 takes groups of
-    8): logits of every stream against the oracle."""
+    """Several utterances in one launch (groups of 2 vectors up to 16
+    utterances, 4 up to 32, 8 above; S=9 leaves an idle vector in the last
+    group): logits of every stream against the oracle."""
     w = synth.make_weights(H, seed=1, cond_dim=16)
     T = 200
     feat = synth.features(S, T, cond_dim=16, per_stream_seed=True)
