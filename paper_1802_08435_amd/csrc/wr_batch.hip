@@ -263,13 +263,18 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       xpub(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B));
     }
   };
-  // Vector ownership: head j draws the vectors j, j + NH, ... of the group
-  // (slot q: vector j + NH q); every other head learns their classes from one
-  // word each.  Only the owner sums a vector's partial logits, so a head reads
-  // the partials of its own vectors, not of all 8.
-  constexpr int OV = (L + NH - 1) / NH;             // most vectors a head owns
-  constexpr int SP = (OV + 1) / 2;                  // owned slots per gathering thread
-  const int nown = (L - j + NH - 1) / NH;           // vectors this head owns
+  // Vector ownership.  With 8 vectors per group head j draws the vectors j,
+  // j + NH, ... (slot q: vector j + NH q) and every other head learns their
+  // classes from one word each: only the owner sums a vector's partial
+  // logits, so a head reads 1/NH of the partials.  With up to 4 vectors
+  // (ALL) every head sums and draws every vector (slot q: vector q): the
+  // partials of all of them are no more words per thread than an owner's
+  // share of 8, and no class words have to travel.
+  constexpr bool ALL = L <= 4;
+  constexpr int OV = ALL ? L : (L + NH - 1) / NH;   // most vectors a head draws
+  constexpr int SP = (OV + 1) / 2;                  // drawn slots per gathering thread
+  const int nown = ALL ? L : (L - j + NH - 1) / NH; // vectors this head draws
+  auto vec = [&](int q) { return ALL ? q : j + NH * q; };   // vector of slot q
   // Sums over the heads, in head order, of the owned vectors' partials.  Lane
   // jj of every wave first watches the last word head jj publishes; then
   // thread (class v, parity s) reads slots s, s + 2, ... of every head (all
@@ -288,7 +293,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     for (int k = 0; k < SP * NH; ++k)
       if (sp + 2 * (k / NH) < nown) need |= 1u << k;
     if (!poll_put<SP * NH>(src + v,
-                           [&](int k) { return (size_t)((k % NH) * L + j + NH * (sp + 2 * (k / NH))) * 256; },
+                           [&](int k) { return (size_t)((k % NH) * L + vec(sp + 2 * (k / NH))) * 256; },
                            [&](int k, float x) { stage[k * WR_THREADS] = x; }, tag, a, need)) {
       misc[0] = 1;
       return;
@@ -346,7 +351,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       }
     }
   };
-  const int bw = j + NH * wave;                     // vector (in the group) drawn by this wave, if wave < nown
+  const int bw = vec(wave);                         // vector (in the group) drawn by this wave, if wave < nown
   const int vw = min(v0 + bw, a.S - 1);
   const size_t ob = obase(a, vw);
   auto fill_batch = [&](int64_t t, int buf) {       // wave w: uniforms / targets of its owned vector
@@ -364,7 +369,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   __syncthreads();
   const bool trw = g == 0 && j == 0 && tid == WR_THREADS - 64;
   const bool own = wave < nown;                     // this wave draws an owned vector
-  const bool live = own && v0 + bw < a.S;          // ... that is in use
+  const bool writer = own && (!ALL || bw % NH == j); // ... and writes its outputs (one head per vector)
+  const bool live = writer && v0 + bw < a.S;       // ... of a vector in use
   xw* CC = X + P.x_cc;                              // drawn coarse classes [L]
   xw* CF = X + P.x_cf;                              // drawn fine classes [L]
 
@@ -416,14 +422,15 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         *(float4*)(a.zc_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        xpub(CC + bw, tag, (float)c);
+        if (ALL) misc[8 + bw] = c;
+        else xpub(CC + bw, tag, (float)c);
         if (a.nll_out) {
           fmisc[wave] = lse;
           fmisc[8 + wave] = zk[wave * 256 + c];
         }
       }
     }
-    receive(CC, tag, 8, -1);
+    if (!ALL) receive(CC, tag, 8, -1);
     __syncthreads();
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
@@ -471,17 +478,24 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         *(float4*)(a.zf_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        xpub(CF + bw, tag, (float)f);
-        if (a.ux) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for the context of later rows
+        if (!ALL) xpub(CF + bw, tag, (float)f);
+        if (a.ux && writer) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for the context of later rows
         if (live) {
           if (a.out) a.out[ob + (size_t)a.B * t] = (uint16_t)(256 * c + f);
           if (a.nll_out)
             a.nll_out[ob + (size_t)a.B * t] = (fmisc[wave] - fmisc[8 + wave]) + (lse - zk[wave * 256 + f]);
         }
+        if (ALL) {                                  // this head's own record of the vector's classes
+          misc[16 + bw] = c;
+          misc[24 + bw] = f;
+          if (t + 1 < a.T) cbo[bw] = cb_offset(a, min(v0 + bw, a.S - 1), t + 1);
+        }
       }
     }
-    receive(CF, tag, 24, t + 1);
-    if (tid < L) misc[16 + tid] = misc[8 + tid];
+    if (!ALL) {
+      receive(CF, tag, 24, t + 1);
+      if (tid < L) misc[16 + tid] = misc[8 + tid];
+    }
     __syncthreads();
     if (trw) trace_at(a, t, 10);
   }
