@@ -165,7 +165,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   float* op = (float*)(imo + 2 * WR_FRAG);         // [2][L][64] first-layer partials
   float* zs = op + 2 * L * 64;                     // [L][256] logit sums over the heads
   float* zk = zs + L * 256;                        // [L][256] logits of the last draws
-  float* hcs = zk + L * 256;                       // [L][448] coarse half of h (= y_c, published by wave 7)
+  float* hcs = zk + L * 256;                       // [L][448] coarse half of h (= y_c)
   float* hfs = hcs + L * 448;                      // [L][448] fine half of h (= y_f)
   float* gv = hfs + L * 448;                       // [4L][448] staged pre-activations and e-gate bias of the gate threads
   int64_t* cbo = (int64_t*)(gv + 4 * L * 448);    // [L] bias + conditioning row offsets of this step
@@ -190,6 +190,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   }
   const int u = tid;
   const bool gate = u < Hh;
+  const bool mine = (unsigned)(u - 64 * j) < 64u;   // unit in this head's slice of y
   float ic[3][2], ifn[3][3];
   if (gate) {
 #pragma unroll
@@ -395,14 +396,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float hn = __builtin_fmaf(uu, hcs[b * 448 + u], (1.0f - uu) * e);
         hcs[b * 448 + u] = hn;
         aput(imc + (u >> 5) * WR_FRAG, u & 31, hn, b);
+        if (mine) xpub(YC + b * Hh + u, tag, hn);   // this head's slice, for the units
       }
     }
     __syncthreads();
     if (misc[0]) return;
     if (trw) trace_at(a, t, 1);
-    if (wave == 7)
-#pragma unroll
-      for (int b = 0; b < L; ++b) xpub(YC + b * Hh + 64 * j + lane, tag, hcs[b * 448 + 64 * j + lane]);
     // (2) O1 rows, relu, O2 columns -> partial coarse logits of 8 vectors
     first_layer(W1, imc, b1r);
     second_layer(W2, PCo, tag);
@@ -451,14 +450,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float hn = __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e);
         hfs[b * 448 + u] = hn;
         aput(imf + (u >> 5) * WR_FRAG, u & 31, hn, b);
+        if (mine) xpub(YF + b * Hh + u, tag, hn);
       }
     }
     __syncthreads();
     if (misc[0]) return;
     if (trw) trace_at(a, t, 6);
-    if (wave == 7)
-#pragma unroll
-      for (int b = 0; b < L; ++b) xpub(YF + b * Hh + 64 * j + lane, tag, hfs[b * 448 + 64 * j + lane]);
     // (5) O3 rows, relu, O4 columns -> partial fine logits
     first_layer(W3, imf, b3r);
     second_layer(W4, PFo, tag);
