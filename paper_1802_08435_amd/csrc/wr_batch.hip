@@ -191,16 +191,26 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const int u = tid;
   const bool gate = u < Hh;
   const bool mine = (unsigned)(u - 64 * j) < 64u;   // unit in this head's slice of y
+  // With 8 vectors (SLICE) a head evaluates the gates of its own 64 units
+  // only, one (unit, vector) pair per thread, and the heads exchange their
+  // slices of y; with fewer vectors every head evaluates every unit of every
+  // vector itself (thread u: unit u).
+  constexpr bool SLICE = L == 8;
+  constexpr int HH = 64 * KH;                       // Hh
+  const int su = 64 * j + (tid >> 3), sb = tid & 7; // SLICE: unit and vector of this thread
+  const int gu = SLICE ? su : u;                    // unit whose I* columns this thread holds
   float ic[3][2], ifn[3][3];
-  if (gate) {
+  if (SLICE || gate) {
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
-      ic[q][0] = a.Iw[3 * (q * H + u) + 0];
-      ic[q][1] = a.Iw[3 * (q * H + u) + 1];
-      ifn[q][0] = a.Iw[3 * (q * H + Hh + u) + 0];
-      ifn[q][1] = a.Iw[3 * (q * H + Hh + u) + 1];
-      ifn[q][2] = a.Iw[3 * (q * H + Hh + u) + 2];
+      ic[q][0] = a.Iw[3 * (q * H + gu) + 0];
+      ic[q][1] = a.Iw[3 * (q * H + gu) + 1];
+      ifn[q][0] = a.Iw[3 * (q * H + Hh + gu) + 0];
+      ifn[q][1] = a.Iw[3 * (q * H + Hh + gu) + 1];
+      ifn[q][2] = a.Iw[3 * (q * H + Hh + gu) + 2];
     }
+  }
+  if (gate) {
     for (int b = 0; b < L; ++b) {
       const int vb = min(v0 + b, a.S - 1);
       hcs[b * 448 + u] = a.h_in ? a.h_in[(size_t)vb * H + u] : 0.0f;
@@ -352,6 +362,65 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       }
     }
   };
+  // SLICE: one (unit, vector) pair per thread.  Its three pre-activation
+  // words, the e gate's context term (subscale) and, for the coarse half,
+  // the first word unit k = tid publishes: a unit publishes its words of
+  // step t + 1 only after reading all of h of step t, so once every unit's
+  // word has arrived this head may replace its slice of y of step t.  Then
+  // the gates, this head's slice of y, and the other slices from their heads.
+  size_t uflag = 0;
+  if (SLICE && tid < P.NU) {
+    const int tile = tid * WR_BUCT, gt = tile / (HH / 16);
+    uflag = P.x_ga + (size_t)(gt * HH + 16 * (tile % (HH / 16))) * L;
+  }
+  auto slice_gates = [&](bool fine, uint32_t tag, int64_t t) {
+    const float cb = a.cb[cbo[sb] + 2 * H + (fine ? HH : 0) + su];
+    const size_t go = (fine ? P.x_gf : P.x_ga) + (size_t)su * L + sb;
+    const size_t xo = (fine ? P.x_xf : P.x_xc) + (size_t)su * L + sb;
+    const uint32_t need = 7u | (CTX ? 8u : 0u) | (!fine && tid < P.NU ? 16u : 0u);
+    float gw[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    if (!poll_put<5>(X, [&](int k) { return k < 3 ? go + (size_t)k * HH * L : k == 3 ? xo : uflag; },
+                     [&](int k, float x) { gw[k] = x; }, tag, a, need)) {
+      misc[0] = 1;
+      return;
+    }
+    if (trg) trace_at(a, t, fine ? 12 : 11);
+    const float cbe = cb + gw[3];
+    const float x0 = fscale(misc[16 + sb]), x1 = fscale(misc[24 + sb]);
+    float pu, pr, pe;
+    if (fine) {
+      const float x2 = fscale(misc[8 + sb]);
+      pu = __builtin_fmaf(ifn[0][2], x2, __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0));
+      pr = __builtin_fmaf(ifn[1][2], x2, __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0));
+      pe = __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0));
+    } else {
+      pu = __builtin_fmaf(ic[0][1], x1, ic[0][0] * x0);
+      pr = __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0);
+      pe = __builtin_fmaf(ic[2][1], x1, ic[2][0] * x0);
+    }
+    const float uu = fsig(gw[0] + pu);
+    const float rg = fsig(gw[1] + pr);
+    const float e = ftanh(__builtin_fmaf(rg, gw[2], pe + cbe));
+    float* hs = (fine ? hfs : hcs) + sb * 448 + su;
+    const float hn = __builtin_fmaf(uu, *hs, (1.0f - uu) * e);
+    *hs = hn;
+    unsigned char* img = fine ? imf : imc;
+    aput(img + (su >> 5) * WR_FRAG, su & 31, xround(hn), sb);
+    xw* Y = fine ? YF : YC;
+    xpub(Y + sb * HH + su, tag, hn);
+    // the other heads' slices: word w = tid + 512 m of y [8][Hh] (Hh / 64 per thread)
+    uint32_t own = 0;
+#pragma unroll
+    for (int m = 0; m < KH; ++m)
+      if ((tid + WR_THREADS * m) % HH / 64 == j) own |= 1u << m;
+    if (!poll_put<KH>(Y, [&](int m) { return (size_t)(tid + WR_THREADS * m); },
+                      [&](int m, float y) {
+                        const int w = tid + WR_THREADS * m, b = w / HH, c = w % HH;
+                        aput(img + (c >> 5) * WR_FRAG, c & 31, y, b);
+                      },
+                      tag, a, ~own))
+      misc[0] = 1;
+  };
   const int bw = vec(wave);                         // vector (in the group) drawn by this wave, if wave < nown
   const int vw = min(v0 + bw, a.S - 1);
   const size_t ob = obase(a, vw);
@@ -382,7 +451,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (own && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
     // (1) coarse gates of every unit and vector: the 24 pre-activation words of
     // thread u are polled together and staged in LDS, then one vector at a time
-    if (gate) {
+    if (SLICE) {
+      slice_gates(false, tag, t);
+    } else if (gate) {
       read_gates(GA, X + P.x_xc, tag, 2 * H + u, t);
       if (trg) trace_at(a, t, 11);
 #pragma unroll 2
@@ -433,7 +504,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     __syncthreads();
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
-    if (gate) {
+    if (SLICE) {
+      slice_gates(true, tag, t);
+    } else if (gate) {
       read_gates(GF, X + P.x_xf, tag, 2 * H + Hh + u, t);
       if (trg) trace_at(a, t, 12);
 #pragma unroll 2
@@ -496,8 +569,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     __syncthreads();
     if (trw) trace_at(a, t, 10);
   }
+  if (SLICE && a.h_out && v0 + sb < a.S) {          // each head its own slice
+    a.h_out[(size_t)(v0 + sb) * H + su] = hcs[sb * 448 + su];
+    a.h_out[(size_t)(v0 + sb) * H + Hh + su] = hfs[sb * 448 + su];
+  }
   if (j == 0) {
-    if (a.h_out && gate)
+    if (a.h_out && gate && !SLICE)
       for (int b = 0; b < L; ++b)
         if (v0 + b < a.S) {
           a.h_out[(size_t)(v0 + b) * H + u] = hcs[b * 448 + u];

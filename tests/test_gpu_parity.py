@@ -133,9 +133,12 @@ def test_batched_teacher_forced_small_sizes(H, S):
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
 
 
-def test_batched_dense896_teacher_forced_within_bf16_tolerance():
+@pytest.mark.parametrize("S,T", [(12, 240), (33, 120)])
+def test_batched_dense896_teacher_forced_within_bf16_tolerance(S, T):
+    """WaveRNN-896 with groups of 2 vectors (12 utterances) and of 8 (33: heads
+    evaluate their own slice of units and exchange y; one live vector in the
+    last group)."""
     w = synth.preset("dense896")
-    S, T = 12, 240
     feat = synth.features(S, T, per_stream_seed=True)
     tgt = _targets(S, T)
     m = wavernn.Model(w, dtype="bf16", max_streams=S)
@@ -189,12 +192,13 @@ def test_dense896_free_running_draws_are_valid():
     assert len(np.unique(out)) > 100
 
 
-def test_batched_free_running_draws_valid_and_chunked_equals_one_call():
-    """9 utterances in one launch: every draw is valid under the oracle's logits
-    on the GPU trajectory and the stream's own Philox uniforms, and two chained
-    calls give the same samples and state as one."""
+@pytest.mark.parametrize("S", [9, 40])
+def test_batched_free_running_draws_valid_and_chunked_equals_one_call(S):
+    """9 or 40 utterances in one launch: every draw is valid under the oracle's
+    logits on the GPU trajectory and the stream's own Philox uniforms, and two
+    chained calls give the same samples and state as one."""
     w = synth.make_weights(256, seed=3, cond_dim=8)
-    S, T = 9, 500
+    T = 500
     feat = synth.features(S, T, cond_dim=8, per_stream_seed=True)
     m = wavernn.Model(w, dtype="bf16", max_streams=S)
     fin = m.new_state(S)
@@ -217,10 +221,11 @@ def test_batched_free_running_draws_valid_and_chunked_equals_one_call():
 
 # ------------------------------------------------------------- subscale
 
-@pytest.mark.parametrize("H,B,S", [(256, 8, 2), (128, 16, 1)])
+@pytest.mark.parametrize("H,B,S", [(256, 8, 2), (128, 16, 1), (128, 16, 3)])
 def test_subscale_teacher_forced_small_sizes(H, B, S):
     """Subscale (Sec. 4): B lanes per utterance in lockstep, each conditioned on
-    the 128 samples before its own (same-row samples masked)."""
+    the 128 samples before its own (same-row samples masked); 3 utterances of
+    16 lanes make groups of 8 vectors."""
     w = synth.make_weights(H, seed=6, cond_dim=16, B=B, ctx_dim=256)
     T = 40 * B
     feat = synth.features(S, T, cond_dim=16, per_stream_seed=True)
