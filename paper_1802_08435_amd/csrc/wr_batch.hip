@@ -77,6 +77,14 @@ __device__ __forceinline__ T* opaque(T* p) {
   return p;
 }
 
+// Delay (x 64 clocks) before the first probe of words that other workgroups
+// publish at about the time this one starts waiting.  A probe issued at once
+// would almost surely come back without them, a coherent load takes about a
+// microsecond, and many such early probes at once slow the exchange for all
+// (measured: with 8-vector groups a head's y and partial-logit gathers each
+// take about 0.3 to 0.5 us less with this delay than with none).
+#define WR_POLL_DELAY 12
+
 // Wait until the N words base + off(k) carry `tag`, storing each value with
 // put(k, value) as it arrives (LDS, not registers).  The addresses are
 // rebuilt in every round from an opaque base, so only the N words in flight
@@ -229,6 +237,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     misc[0] = 0;
     misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
     misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
+    misc[8 + tid] = misc[16 + tid];
   }
   xw* X = a.xc + (size_t)g * P.x_words;
   const xw* GA = X + P.x_ga;
@@ -286,16 +295,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   constexpr int SP = (OV + 1) / 2;                  // drawn slots per gathering thread
   const int nown = ALL ? L : (L - j + NH - 1) / NH; // vectors this head draws
   auto vec = [&](int q) { return ALL ? q : j + NH * q; };   // vector of slot q
-  // Sums over the heads, in head order, of the owned vectors' partials.  Lane
-  // jj of every wave first watches the last word head jj publishes; then
+  // Sums over the heads, in head order, of the owned vectors' partials:
   // thread (class v, parity s) reads slots s, s + 2, ... of every head (all
-  // words in flight at once), re-reading only words without the step's tag.
+  // words in flight at once, the first probe after WR_POLL_DELAY), re-reading
+  // only words without the step's tag.
   auto gather_own = [&](const xw* src, uint32_t tag) {
-    {
-      float y;
-      const int hj = lane < NH ? lane : 0;
-      if (!wait_word(src + ((size_t)hj * L + L - 1) * 256 + 255, tag, &y, a)) misc[0] = 1;
-    }
+    __builtin_amdgcn_s_sleep(WR_POLL_DELAY);
     const int v = tid & 255, sp = tid >> 8;
     // word k (< SP NH): head k % NH, slot sp + 2 (k / NH); staged in gv (free here)
     float* stage = gv + tid;                        // [SP NH][512]
@@ -362,12 +367,17 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       }
     }
   };
+  xw* CC = X + P.x_cc;                              // drawn coarse classes [L]
+  xw* CF = X + P.x_cf;                              // drawn fine classes [L]
   // SLICE: one (unit, vector) pair per thread.  Its three pre-activation
   // words, the e gate's context term (subscale) and, for the coarse half,
   // the first word unit k = tid publishes: a unit publishes its words of
   // step t + 1 only after reading all of h of step t, so once every unit's
   // word has arrived this head may replace its slice of y of step t.  Then
   // the gates, this head's slice of y, and the other slices from their heads.
+  // The classes of the thread's vector travel with the same poll: c_{t-1} and
+  // f_{t-1} with the coarse words (from step 1 on), c_t with the fine words.
+  int cprev = 0, fprev = 0, ccur = 0;               // SLICE: classes of vector sb
   size_t uflag = 0;
   if (SLICE && tid < P.NU) {
     const int tile = tid * WR_BUCT, gt = tile / (HH / 16);
@@ -377,19 +387,40 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     const float cb = a.cb[cbo[sb] + 2 * H + (fine ? HH : 0) + su];
     const size_t go = (fine ? P.x_gf : P.x_ga) + (size_t)su * L + sb;
     const size_t xo = (fine ? P.x_xf : P.x_xc) + (size_t)su * L + sb;
-    const uint32_t need = 7u | (CTX ? 8u : 0u) | (!fine && tid < P.NU ? 16u : 0u);
-    float gw[5] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-    if (!poll_put<5>(X, [&](int k) { return k < 3 ? go + (size_t)k * HH * L : k == 3 ? xo : uflag; },
-                     [&](int k, float x) { gw[k] = x; }, tag, a, need)) {
-      misc[0] = 1;
-      return;
+    // words 0-2 gates, 3 context term, 4 unit flag, 5 c (fine: c_t; coarse: c_{t-1}), 6 f_{t-1}
+    uint32_t pending = 7u | (CTX ? 8u : 0u) | (!fine && tid < P.NU ? 16u : 0u) | (fine ? 32u : t > 0 ? 96u : 0u);
+    float gw[7] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    const size_t co = P.x_cc + sb, fo = P.x_cf + sb;
+    WaitBudget wb{wr_clock(), 0};
+    for (;;) {
+      const xw* xb = opaque((const xw*)X);
+      xw w[7];
+#pragma unroll
+      for (int k = 0; k < 7; ++k)
+        w[k] = (pending >> k & 1u) ? xpeek(xb + (k < 3 ? go + (size_t)k * HH * L : k == 3 ? xo : k == 4 ? uflag : k == 5 ? co : fo)) : 0;
+#pragma unroll
+      for (int k = 0; k < 7; ++k)
+        if ((pending >> k & 1u) && xok(w[k], k >= 5 && !fine ? tag - 1u : tag)) {
+          gw[k] = xval(w[k]);
+          pending &= ~(1u << k);
+        }
+      if (!pending) break;
+      if (!wait_ok(wb, a.err, a.limit, a.err)) {
+        misc[0] = 1;
+        return;
+      }
     }
     if (trg) trace_at(a, t, fine ? 12 : 11);
+    if (fine) ccur = (int)gw[5];
+    else if (t > 0) {
+      cprev = (int)gw[5];
+      fprev = (int)gw[6];
+    }
     const float cbe = cb + gw[3];
-    const float x0 = fscale(misc[16 + sb]), x1 = fscale(misc[24 + sb]);
+    const float x0 = fscale(cprev), x1 = fscale(fprev);
     float pu, pr, pe;
     if (fine) {
-      const float x2 = fscale(misc[8 + sb]);
+      const float x2 = fscale(ccur);
       pu = __builtin_fmaf(ifn[0][2], x2, __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0));
       pr = __builtin_fmaf(ifn[1][2], x2, __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0));
       pe = __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0));
@@ -413,6 +444,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
 #pragma unroll
     for (int m = 0; m < KH; ++m)
       if ((tid + WR_THREADS * m) % HH / 64 == j) own |= 1u << m;
+    __builtin_amdgcn_s_sleep(WR_POLL_DELAY);
     if (!poll_put<KH>(Y, [&](int m) { return (size_t)(tid + WR_THREADS * m); },
                       [&](int m, float y) {
                         const int w = tid + WR_THREADS * m, b = w / HH, c = w % HH;
@@ -437,12 +469,14 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   if (wave < nown) fill_batch(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  if (SLICE) {
+    cprev = misc[16 + sb];
+    fprev = misc[24 + sb];
+  }
   const bool trw = g == 0 && j == 0 && tid == WR_THREADS - 64;
   const bool own = wave < nown;                     // this wave draws an owned vector
   const bool writer = own && (!ALL || bw % NH == j); // ... and writes its outputs (one head per vector)
   const bool live = writer && v0 + bw < a.S;       // ... of a vector in use
-  xw* CC = X + P.x_cc;                              // drawn coarse classes [L]
-  xw* CF = X + P.x_cf;                              // drawn fine classes [L]
 
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
@@ -492,15 +526,15 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         *(float4*)(a.zc_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        if (ALL) misc[8 + bw] = c;
-        else xpub(CC + bw, tag, (float)c);
+        if (ALL || SLICE) misc[8 + bw] = c;
+        if (!ALL) xpub(CC + bw, tag, (float)c);
         if (a.nll_out) {
           fmisc[wave] = lse;
           fmisc[8 + wave] = zk[wave * 256 + c];
         }
       }
     }
-    if (!ALL) receive(CC, tag, 8, -1);
+    if (!ALL && !SLICE) receive(CC, tag, 8, -1);
     __syncthreads();
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
@@ -549,6 +583,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
         if (!ALL) xpub(CF + bw, tag, (float)f);
+        if (SLICE) misc[24 + bw] = f;                // the owner's record (final state)
         if (a.ux && writer) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for the context of later rows
         if (live) {
           if (a.out) a.out[ob + (size_t)a.B * t] = (uint16_t)(256 * c + f);
@@ -563,8 +598,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       }
     }
     if (!ALL) {
-      receive(CF, tag, 24, t + 1);
-      if (tid < L) misc[16 + tid] = misc[8 + tid];
+      if (SLICE) {
+        if (tid < L && t + 1 < a.T) cbo[tid] = cb_offset(a, min(v0 + tid, a.S - 1), t + 1);
+      } else {
+        receive(CF, tag, 24, t + 1);
+      }
+      if (tid < L && !SLICE) misc[16 + tid] = misc[8 + tid];
     }
     __syncthreads();
     if (trw) trace_at(a, t, 10);
@@ -580,10 +619,14 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
           a.h_out[(size_t)(v0 + b) * H + u] = hcs[b * 448 + u];
           a.h_out[(size_t)(v0 + b) * H + Hh + u] = hfs[b * 448 + u];
         }
-    if (tid < L && v0 + tid < a.S) {
+    if (tid < L && v0 + tid < a.S && !SLICE) {
       if (a.c_out) a.c_out[v0 + tid] = (uint8_t)misc[16 + tid];
       if (a.f_out) a.f_out[v0 + tid] = (uint8_t)misc[24 + tid];
     }
+  }
+  if (SLICE && lane == 0 && live) {                 // the owner: last classes of its vectors
+    if (a.c_out) a.c_out[v0 + bw] = (uint8_t)misc[8 + bw];
+    if (a.f_out) a.f_out[v0 + bw] = (uint8_t)misc[24 + bw];
   }
 }
 
@@ -725,17 +768,22 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   auto cbv = [&](int b, int64_t t) {                           // u and r gates carry bias + conditioning
     return gt < 2 && b < L ? a.cb[cb_offset(a, min(v0 + b, a.S - 1), t) + row] : 0.0f;
   };
-  // Wait for one half of h of all 8 vectors: lane jj of wave 0 first watches
-  // the last word head jj publishes (vector 7), then every thread reads its
-  // words once and writes the operand tiles kt0 ...
+  // Wait for one half of h of the group's vectors and write the operand
+  // tiles kt0 ...: with 8 vectors (7 words per thread) lane jj of wave 0
+  // first watches the last word head jj publishes, so that only 7 words per
+  // wave are polled while h is not there; with fewer vectors every thread
+  // polls its own words directly, the first probe after WR_POLL_DELAY.
   auto gather_half = [&](const xw* Y, uint32_t tag, int kt0) {
-    if (wave == 0) {
-      const int hj = lane < P.NH ? lane : 0;
-      float y;
-      if (!poll_strided<1>(Y + (L - 1) * Hh + 64 * hj + 63, 0, tag, &y, a)) misc[0] = 1;
+    if (L < 8) __builtin_amdgcn_s_sleep(WR_POLL_DELAY);
+    if (L >= 8) {
+      if (wave == 0) {
+        const int hj = lane < P.NH ? lane : 0;
+        float y;
+        if (!poll_strided<1>(Y + (L - 1) * Hh + 64 * hj + 63, 0, tag, &y, a)) misc[0] = 1;
+      }
+      __syncthreads();
+      if (misc[0]) return;
     }
-    __syncthreads();
-    if (misc[0]) return;
     constexpr int PER = (L * 448 + WR_THREADS - 1) / WR_THREADS;   // words per thread at most
     float y[PER];
     uint32_t pending = 0;

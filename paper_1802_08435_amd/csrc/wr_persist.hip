@@ -203,12 +203,19 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       xpub(dst + 32 * wave + 16 + lane, tag, mfma_row(B));
     }
   };
-  // partial logits of all slices: lane jj of every wave first waits for the
-  // last word of slice jj (little polling traffic while the exchange is in
-  // flight), then thread (v, half) sums its half of the slices in slice order
-  // (every word is still checked for its tag)
+  // partial logits of all slices: thread (v, half) sums its half of the
+  // slices in slice order, each word checked for its tag.  The partials are
+  // being published as this head starts to wait, so the first probe waits a
+  // little (a probe at once comes back without them, and every failed probe
+  // of the whole grid loads the exchange; measured: 7 slices 5.17 us per
+  // step with a 6 x 64-clock delay, 5.59 without, 5.64 with the flag phase
+  // below).  With split heads (16 slices, 8 words per thread) lane jj of
+  // every wave first waits for the last word of slice jj, so that while the
+  // exchange is in flight only those words are polled.
   auto gather_logits = [&](const xw* src, uint32_t tag) {
-    {   // every wave waits on the flags itself: no barrier before the reads
+    if (SPLIT) __builtin_amdgcn_s_sleep(12);
+    else __builtin_amdgcn_s_sleep(6);
+    if (SPLIT) {   // every wave waits on the flags itself: no barrier before the reads
       float y;
       const int jj = lane < NK ? lane : 0;
       if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + 255, tag, &y, a)) misc[0] = 1;
