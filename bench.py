@@ -86,6 +86,55 @@ def cpu_baseline(w: dict, T: int, feat, budget_s: float = 12.0) -> dict:
             "sample": f"first {n} of the {T} samples of one utterance, single-threaded C oracle (gcc -O2)"}
 
 
+# In-kernel timestamps (trace slot -> phase end) of the step loop of head 0
+# (group 0 for the batched kernel), recorded by wavernn_set_trace.
+PHASES = {
+    "persistent": [(1, "coarse gates (Eq. 2, with f_{t-1}) done, own y_c slice published"),
+                   (2, "O1 rows + relu"), (3, "O2 columns: partial coarse logits published"),
+                   (15, "coarse partials of all heads received"), (4, "barrier"),
+                   (16, "c_t drawn (draw wave)"), (5, "barrier: c_t known to all waves"),
+                   (6, "fine gates (with c_t) done, own y_f slice published"), (7, "O3 rows + relu"),
+                   (8, "O4 columns: partial fine logits published"), (17, "fine partials of all heads received"),
+                   (9, "barrier"), (18, "f_t drawn (draw wave)"),
+                   (10, "next step's coarse gate words received (end of step)")],
+    "batched": [(11, "coarse gate words received"), (1, "coarse gates done, y_c of the group exchanged"),
+                (3, "O1/O2: partial coarse logits published"), (4, "owned vectors' coarse partials summed"),
+                (5, "c_t drawn"), (12, "fine gate words and classes received"),
+                (6, "fine gates done, y_f of the group exchanged"), (8, "O3/O4: partial fine logits published"),
+                (9, "owned vectors' fine partials summed"), (10, "f_t drawn (end of step)")],
+}
+PHASES["block-sparse"] = PHASES["persistent"]
+
+
+def phases(m, w, path: str, S: int, feat, n_steps: int) -> dict:
+    """Median per-phase timestamps of one traced launch of n_steps steps (the
+    first and last eighth left out)."""
+    import numpy as np
+    import torch
+    B = w["B"]
+    T = n_steps * B
+    skip = n_steps // 8
+    buf = torch.zeros(n_steps, 32, dtype=torch.int64, device="cuda")
+    m.set_trace(buf)
+    m.sample(T, cond=feat, seed=5, n_streams=S)
+    torch.cuda.synchronize()
+    m.set_trace(None)
+    m.device_status()
+    tr = buf.cpu().numpy()[skip:n_steps - skip].astype(np.int64)
+    step_ns = np.diff(tr[:, 0]) * 10.0                    # 100 MHz clock
+    rel = (tr - tr[:, [0]]) * 10.0
+    out, prev = [], 0.0
+    for slot, name in PHASES[path]:
+        if (tr[:, slot] == 0).any():
+            continue
+        t = float(np.median(rel[:, slot]))
+        out.append({"slot": slot, "phase": name, "end_ns": round(t), "took_ns": round(t - prev)})
+        prev = t
+    return {"phases": out, "step_ns_median": round(float(np.median(step_ns))),
+            "step_ns_p10": round(float(np.percentile(step_ns, 10))),
+            "step_ns_p90": round(float(np.percentile(step_ns, 90))), "traced_steps": int(len(step_ns))}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -96,6 +145,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration) and exit")
+    ap.add_argument("--phases", action="store_true",
+                    help="only time the phases of one traced launch (in-kernel timestamps) and print them")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -125,6 +176,12 @@ def main() -> int:
     feat = torch.from_numpy(feat_np).cuda()
     out = torch.empty(S, T, dtype=torch.uint16, device="cuda")
     stream = torch.cuda.current_stream()
+    if args.phases:
+        m.sample(T, cond=feat, seed=1, n_streams=S, out=out)
+        ph = phases(m, w, path, S, feat, min(T // w["B"], 4000))
+        print(json.dumps({"workload": args.config, "kernel": KERNEL_OF.get(path, path), **ph}), flush=True)
+        m.close()
+        return 0
     for i in range(args.warmup):
         m.sample(T, cond=feat, seed=1 + i, n_streams=S, out=out)
     torch.cuda.synchronize()
