@@ -75,10 +75,12 @@ def cpu_baseline(w: dict, T: int, feat, budget_s: float = 12.0) -> dict:
     import numpy as np
     from oracle import oracle
     W = oracle.Weights.from_dict(w, bf16=w.get("bf16", False))
+    B = w.get("B", 1)                                    # subscale: whole rows of B samples
+    n0 = 48 // B * B or B
     t = time.perf_counter()
-    oracle.run(W, 1, 50, feat=feat[:1], seed=1)
-    per = (time.perf_counter() - t) / 50
-    n = int(max(50, min(T, budget_s / max(per, 1e-9))))
+    oracle.run(W, 1, n0, feat=feat[:1], seed=1)
+    per = (time.perf_counter() - t) / n0
+    n = int(max(n0, min(T, budget_s / max(per, 1e-9)))) // B * B
     t = time.perf_counter()
     oracle.run(W, 1, n, feat=feat[:1], seed=1)
     dt = time.perf_counter() - t

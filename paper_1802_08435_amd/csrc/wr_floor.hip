@@ -37,13 +37,15 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
       acc += xval(xpeek(G + u)) + xval(xpeek(G + Hh + u)) + xval(xpeek(G + 2 * Hh + u));
     gsink[tid] = acc;
   };
-  // partials of all NK slices, read as the sampling kernel reads them: after
-  // a short delay, thread (v, half) reads its half of the slices; with split
-  // heads every wave first waits for the last word of every slice
+  // partials of all NK slices: every wave first waits for the last word of
+  // every slice, then thread (v, half) reads its half of the slices.  With
+  // nothing to compute between the exchanges this is the least polling
+  // traffic per exchange (the sampling kernel, which computes in between,
+  // polls its words directly where there are few per thread: here that
+  // would keep 512 threads per head polling all the time and measure the
+  // polling load instead)
   auto gather = [&](const xw* src, uint32_t tag) {
-    if (split) __builtin_amdgcn_s_sleep(12);
-    else __builtin_amdgcn_s_sleep(6);
-    if (split) {
+    {
       float y;
       const int jj = lane < NK ? lane : 0;
       if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + 255, tag, &y, a)) misc[0] = 1;
