@@ -105,6 +105,7 @@ PRESETS = {
     "sparse2048_16x1": (2048, COND_DIM, 1, 0, (16, 1), True, 1, 24000),
     "subscale16": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
     "multi64": (896, COND_DIM, 1, 0, None, True, 64, 48000),
+    "multi4": (896, COND_DIM, 1, 0, None, True, 4, 24000),   # Sec. 2.1's batch-4 point
 }
 
 
