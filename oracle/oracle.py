@@ -40,7 +40,7 @@ def build(force: bool = False) -> str:
 
 class _Model(ctypes.Structure):
     _fields_ = [("H", ctypes.c_int32), ("Dc", ctypes.c_int32), ("frame_len", ctypes.c_int32),
-                ("B", ctypes.c_int32), ("Dx", ctypes.c_int32)] + [
+                ("B", ctypes.c_int32), ("Dx", ctypes.c_int32), ("F", ctypes.c_int32)] + [
         (n, ctypes.POINTER(ctypes.c_float))
         for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")]
 
@@ -68,6 +68,8 @@ def load(path: str):
     L.orc_uniforms.argtypes = [u64, u64, i64, ctypes.POINTER(f32), ctypes.POINTER(f32)]
     L.orc_draw.restype = ctypes.c_int
     L.orc_draw.argtypes = [vp, ctypes.c_int, f32]
+    L.orc_subscale_context.restype = None
+    L.orc_subscale_context.argtypes = [ctypes.POINTER(_Model), vp, i64, i32, i64, vp]
     L.orc_run.restype = ctypes.c_int
     L.orc_run.argtypes = [ctypes.POINTER(_Model), i32, i64, i64, vp, i64, u64, vp, vp, vp, vp, vp,
                           vp, vp, vp]
@@ -144,6 +146,7 @@ class Weights:
     Wx: np.ndarray | None = None
     frame_len: int = 120
     B: int = 1
+    F: int = -1          # subscale future horizon (Sec. 4.1); < 0: lockstep rows
 
     @staticmethod
     def from_dict(d: dict, bf16: bool = False) -> "Weights":
@@ -156,7 +159,8 @@ class Weights:
                 continue
             v = np.ascontiguousarray(v, dtype=np.float32)
             kw[k] = bf16_round(v) if bf16 else v.copy()
-        return Weights(H=int(d["H"]), frame_len=int(d.get("frame_len", 120)), B=int(d.get("B", 1)), **kw)
+        return Weights(H=int(d["H"]), frame_len=int(d.get("frame_len", 120)), B=int(d.get("B", 1)),
+                       F=int(d.get("F", -1)), **kw)
 
 
 def _model(w: Weights):
@@ -171,9 +175,19 @@ def _model(w: Weights):
     m.Dx = 0 if w.Wx is None else w.Wx.shape[1]
     m.frame_len = w.frame_len
     m.B = w.B
+    m.F = w.F
     for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4"):
         setattr(m, n, fp(getattr(w, n)))
     return m
+
+
+def subscale_context(w: Weights, seq, s: int, i: int) -> np.ndarray:
+    """The context vector [Dx] of sample B*i + s of one utterance whose samples are seq [N]."""
+    seq = np.ascontiguousarray(seq, np.uint16)
+    ctx = np.zeros(w.Wx.shape[1], np.float32)
+    m = _model(w)
+    lib().orc_subscale_context(ctypes.byref(m), _p(seq), len(seq), s, i, _p(ctx))
+    return ctx
 
 
 def run(w: Weights, S: int, T: int, feat=None, seed: int = 1, target=None, h0=None, c0=None, f0=None,

@@ -35,10 +35,18 @@
  *   - initial state h = 0, c_{-1} = 128, f_{-1} = 0 unless given;
  *   - conditioning: a feature frame of Dc values per frame_len samples enters
  *     every gate pre-activation through W_cond (3H x Dc);
- *   - Subscale (Sec. 4, Eq. 4) in lockstep: B lanes, lane s at row i makes
- *     sample n = B*i + s from its own state; its context is the Dx/2 samples
- *     before n, each as (c, f) scaled, zero when the sample is not yet made at
- *     the start of row i, entering the gates through W_ctx (3H x Dx).
+ *   - Subscale (Sec. 4, Eq. 4): sub-tensor s holds the samples n = B*i + s,
+ *     i = 0 .. N/B - 1, generated from its own state (lane s); a context of
+ *     Dx/2 samples, each as (c, f) scaled, enters the gates through W_ctx
+ *     (3H x Dx).  Two readings:
+ *       F < 0, lockstep rows: all B lanes make row i together; the context of
+ *         n is the Dx/2 samples before n, zero for those of row i or later;
+ *       F >= 0, the paper's order with future horizon F (Sec. 4.1): sub-tensor
+ *         s is generated after sub-tensors 0 .. s-1, and sample B*i + s sees
+ *         sub-tensors z < s up to position i + F and its own sub-tensor
+ *         before position i (no distant dependencies); its context is the
+ *         Dx/4 samples before n and the Dx/4 after n, zero where not seen.
+ *         Generated here sub-tensor by sub-tensor, in the paper's order.
  *
  * Build: cc -O2 -ffp-contract=off -fPIC -shared (no fast-math; fmaf only where written).
  */
@@ -226,19 +234,29 @@ static void head(const orc_model* m, const float* Oa, const float* ba, const flo
   for (int v = 0; v < ORC_MAX_CLASSES; ++v) z[v] = dot(Ob + (size_t)v * Hh, hid, Hh) + bb[v];
 }
 
-/* Context of subscale lane s at row i: (c, f) of samples n-1, n-2, ... scaled;
- * zero where the sample does not yet exist at the start of row i. */
-static void subscale_context(const orc_model* m, const uint16_t* seq, int64_t n, int64_t row_start, float* ctx) {
-  const int L = m->Dx / 2;
-  for (int j = 0; j < L; ++j) {
-    int64_t q = n - 1 - j;
-    if (q >= 0 && q < row_start) {
-      ctx[2 * j] = orc_scale(seq[q] >> 8);
-      ctx[2 * j + 1] = orc_scale(seq[q] & 255);
-    } else {
-      ctx[2 * j] = 0.0f;
-      ctx[2 * j + 1] = 0.0f;
+/* Whether sample q = B*k + z of an utterance of N samples is seen by sample
+ * B*i + s under the future-horizon rule. */
+static int seen_lagged(int B, int F, int64_t N, int32_t s, int64_t i, int64_t q) {
+  if (q < 0 || q >= N) return 0;
+  const int64_t k = q / B, z = q % B;
+  return (z < s && k <= i + F) || (z == s && k < i);
+}
+
+void orc_subscale_context(const orc_model* m, const uint16_t* seq, int64_t N, int32_t s, int64_t i, float* ctx) {
+  const int B = m->B, P = m->Dx / 2;
+  const int64_t n = (int64_t)B * i + s;
+  for (int j = 0; j < P; ++j) {
+    int64_t q;
+    int seen;
+    if (m->F < 0) {                 /* lockstep: the samples before n made before row i */
+      q = n - 1 - j;
+      seen = q >= 0 && q < (int64_t)B * i;
+    } else {                        /* horizon F: Dx/4 samples before n, then Dx/4 after */
+      q = j < P / 2 ? n - 1 - j : n + 1 + (j - P / 2);
+      seen = seen_lagged(B, m->F, N, s, i, q);
     }
+    ctx[2 * j] = seen ? orc_scale(seq[q] >> 8) : 0.0f;
+    ctx[2 * j + 1] = seen ? orc_scale(seq[q] & 255) : 0.0f;
   }
 }
 
@@ -249,7 +267,7 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
   if (H <= 0 || (H & 1) || H > ORC_MAX_HIDDEN || S <= 0 || T < 0) return -1;
   if (B > 1 && (T % B != 0 || t0 != 0)) return -1;
   if (m->Dc > 0 && (m->frame_len <= 0 || feat == NULL)) return -1;
-  if (m->Dx > 0 && (B == 1 || m->Dx % 2 != 0)) return -1;
+  if (m->Dx > 0 && (B == 1 || m->Dx % (m->F < 0 ? 2 : 4) != 0)) return -1;
   if (target == NULL && out == NULL) return -1;
   if (T == 0) return 0;
   float* G = (float*)malloc(sizeof(float) * 3 * H);
@@ -258,11 +276,16 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
   float* ctx = (float*)malloc(sizeof(float) * (m->Dx > 0 ? m->Dx : 1));
   float zc[ORC_MAX_CLASSES], zf[ORC_MAX_CLASSES];
   const int64_t rows = T / B;
+  /* lockstep: row by row, lane by lane; horizon F: lane (sub-tensor) by lane */
+  const int lagged = B > 1 && m->F >= 0;
+  const int64_t n_outer = lagged ? B : rows, n_inner = lagged ? rows : B;
   for (int32_t s = 0; s < S; ++s) {
     uint16_t* seq = out ? out + (size_t)s * T : NULL;   /* samples of utterance s, time order */
     const uint16_t* tgt = target ? target + (size_t)s * T : NULL;
-    for (int64_t i = 0; i < rows; ++i) {
-      for (int lane = 0; lane < B; ++lane) {
+    for (int64_t o = 0; o < n_outer; ++o) {
+      for (int64_t in = 0; in < n_inner; ++in) {
+        const int64_t i = lagged ? in : o;
+        const int lane = (int)(lagged ? o : in);
         const int64_t st = (int64_t)s * B + lane;   /* state / Philox stream index */
         const int64_t n = (B == 1) ? t0 + i : B * i + lane; /* absolute sample index */
         const int64_t local = (B == 1) ? i : n;             /* index into this call's arrays */
@@ -273,7 +296,7 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
           if (fr >= n_frames) fr = n_frames - 1;
           frame = feat + ((size_t)s * n_frames + fr) * m->Dc;
         }
-        if (m->Dx > 0) subscale_context(m, tgt ? tgt : seq, n, B * i, ctx);
+        if (m->Dx > 0) orc_subscale_context(m, tgt ? tgt : seq, T, lane, i, ctx);
         gate_additive(m, frame, ctx, add);
         for (int row = 0; row < 3 * H; ++row) G[row] = dot(m->R + (size_t)row * H, hs, H);
         float x[3] = {orc_scale(cprev[st]), orc_scale(fprev[st]), 0.0f};

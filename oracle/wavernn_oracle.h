@@ -21,6 +21,7 @@
  *   O3 [H/2][H/2] b3 [H/2]   O4 [256][H/2] b4 [256]   (fine head)   */
 typedef struct {
   int32_t H, Dc, frame_len, B, Dx;
+  int32_t F;   /* subscale future horizon (Sec. 4.1): < 0 lockstep rows, >= 0 the paper's order */
   const float *R, *I, *b, *Wc, *Wx;
   const float *O1, *b1, *O2, *b2, *O3, *b3, *O4, *b4;
 } orc_model;
@@ -32,6 +33,11 @@ float orc_scale(int v);
 void orc_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
 void orc_uniforms(uint64_t seed, uint64_t stream, int64_t t, float* uc, float* uf);
 int orc_draw(const float* z, int n, float u);
+
+/* Subscale context of sample n = B*i + s of an utterance of N samples whose
+ * samples so far are seq[N] (Dx/2 (c, f) pairs into ctx[Dx]); the rule of
+ * the model (lockstep for F < 0, future horizon F otherwise). */
+void orc_subscale_context(const orc_model* m, const uint16_t* seq, int64_t N, int32_t s, int64_t i, float* ctx);
 
 /* Runs S utterances of T samples (B = 1: starting at absolute sample t0).
  * feat [S][n_frames][Dc]; target [S][T] (NULL: sample freely); state h [S*B][H],

@@ -47,7 +47,11 @@ MUTANTS = {
     "tanh_as_sigmoid": ("float t = (1.0f - q) / (1.0f + q);", "float t = 1.0f / (1.0f + q);"),
     "nll_fine_term_dropped": ("neg_log_prob(zc, ORC_MAX_CLASSES, c) + neg_log_prob(zf, ORC_MAX_CLASSES, f)",
                               "neg_log_prob(zc, ORC_MAX_CLASSES, c)"),
-    "subscale_no_row_mask": ("if (q >= 0 && q < row_start) {", "if (q >= 0 && q < n) {"),
+    "subscale_no_row_mask": ("seen = q >= 0 && q < (int64_t)B * i;", "seen = q >= 0 && q < n;"),
+    "subscale_horizon_plus_one": ("(z < s && k <= i + F)", "(z < s && k <= i + F + 1)"),
+    "subscale_sees_own_future": ("(z < s && k <= i + F)", "(z <= s && k <= i + F)"),
+    "subscale_own_past_dropped": ("(z == s && k < i)", "(z == s && k < i - 1)"),
+    "subscale_window_includes_n": ("n + 1 + (j - P / 2)", "n + (j - P / 2)"),
     "subscale_lane_order": ("const int64_t n = (B == 1) ? t0 + i : B * i + lane;",
                             "const int64_t n = (B == 1) ? t0 + i : rows * lane + i;"),
     "exp_low_coeffs_off": ("g_inv_fact[i] = (float)(1.0 / f);", "g_inv_fact[i] = (float)(1.0 / (f + (i == 2)));"),
@@ -62,11 +66,16 @@ PINS = [
     "test_hand_case_reset_gate_placement_and_R_orientation", "test_hand_case_update_gate_interpolates",
     "test_hand_case_conditioning_frames", "test_coarse_logits_do_not_depend_on_current_coarse_byte",
     "test_chunked_sampling_equals_one_call", "test_subscale_without_context_is_interleaved_plain_streams",
-    "test_subscale_context_masks_samples_of_the_current_row",
+    "test_subscale_context_masks_samples_of_the_current_row", "test_subscale_horizon_context_hand_cases",
+    "test_subscale_horizon_dependencies_precede_in_the_lagged_schedule",
 ]
 
 _PARAMS = {"test_philox_matches_numpy": [dict(seed=7, stream=3, t=123456), dict(seed=1, stream=0, t=5)],
-           "test_subscale_context_masks_samples_of_the_current_row": [dict(j=0), dict(j=5)]}
+           "test_subscale_context_masks_samples_of_the_current_row": [dict(j=0), dict(j=5)],
+           "test_subscale_horizon_context_hand_cases": [
+               dict(zip(("B", "F", "Dx", "s", "i", "idx"), c))
+               for c in P.test_subscale_horizon_context_hand_cases.pytestmark[0].args[1]],
+           "test_subscale_horizon_dependencies_precede_in_the_lagged_schedule": [dict(F=1)]}
 
 
 def _failures(tmp_path, name):

@@ -381,6 +381,80 @@ def test_subscale_context_masks_samples_of_the_current_row(j):
             np.testing.assert_array_equal(a[:, s], b[:, s])
 
 
+def _horizon_model(B, F, Dx, H=8):
+    d = _random_tiny(H=H)
+    return W(dict(d, B=B, F=F, Wx=np.zeros((3 * H, Dx), np.float32)))
+
+
+def _pairs(seq, idx):
+    """Expected context: (c, f) scaled of seq[q] for each q, zeros for None."""
+    out = []
+    for q in idx:
+        out += [0.0, 0.0] if q is None else [O.scale(int(seq[q]) >> 8), O.scale(int(seq[q]) & 255)]
+    return np.array(out, np.float32)
+
+
+@pytest.mark.parametrize("B,F,Dx,s,i,idx", [
+    # Sec. 4.1 by hand: sample 4i + s sees sub-tensors z < s up to position i + F and
+    # its own sub-tensor before i; the window is Dx/4 samples before n, then Dx/4 after.
+    (4, 1, 8, 2, 1, [5, 4, None, 8]),            # n = 6: 5 (z1), 4 (z0); 7 is z3 > s; 8 = (k2, z0), k <= 2
+    (4, 1, 8, 0, 2, [None, None, None, None]),   # n = 8: sub-tensor 0 sees no other sub-tensor
+    (4, 1, 8, 3, 1, [6, 5, 8, 9]),               # n = 7: future 8, 9 of z0, z1 at k = 2 <= 2
+    (4, 1, 8, 3, 2, [10, 9, 12, 13]),            # n = 11: future 12, 13 at k = 3 <= i + F = 3
+    (4, 0, 8, 3, 2, [10, 9, None, None]),        # F = 0: k = 3 > 2 is beyond the horizon
+    (4, 1, 8, 1, 0, [0, None, None, None]),      # n = 1: q = -1 does not exist
+    (4, 1, 8, 2, 3, [13, 12, None, None]),       # n = 14: 15 is z3; 16 is past the end (N = 16)
+    (4, 1, 16, 1, 2, [8, None, None, 5, None, None, 12, None]),   # n = 9: own past 5 (k1 < 2), own future 13 unseen
+])
+def test_subscale_horizon_context_hand_cases(B, F, Dx, s, i, idx):
+    w = _horizon_model(B, F, Dx)
+    seq = (np.arange(16) * 4099 + 77) % 65536
+    np.testing.assert_array_equal(O.subscale_context(w, seq.astype(np.uint16), s, i), _pairs(seq, idx))
+
+
+def test_subscale_horizon_without_context_is_interleaved_plain_streams():
+    """With W_ctx = 0 the order of generation does not matter: the horizon-F
+    run equals the lockstep run and B interleaved plain streams."""
+    d = _random_tiny(H=16)
+    Wx = np.zeros((48, 256), np.float32)
+    lag = O.run(W(dict(d, B=16, F=3, Wx=Wx)), 1, 16 * 40, seed=6)["out"][0]
+    lock = O.run(W(dict(d, B=16, Wx=Wx)), 1, 16 * 40, seed=6)["out"][0]
+    plain = O.run(W(d), 16, 40, seed=6)["out"]
+    np.testing.assert_array_equal(lag, lock)
+    np.testing.assert_array_equal(lag.reshape(40, 16).T, plain)
+
+
+@pytest.mark.parametrize("F", [0, 1, 3])
+def test_subscale_horizon_dependencies_precede_in_the_lagged_schedule(F):
+    """Brute force on a tiny model: change one target sample q = B k + z and see
+    which teacher-forced logits move.  Under the batched schedule of Sec. 4.1
+    sub-tensor s runs position i at step i + s (F + 1); every sample a logit
+    depends on must be made at an earlier step, and some sample of an earlier
+    sub-tensor from the logit's future (within F, so only for F > 0: with F = 0
+    every sample an earlier sub-tensor has made up to position i precedes
+    B i + s in time) must matter."""
+    B, N, H, Dx = 4, 48, 8, 16
+    d = _random_tiny(H=H)
+    rng = np.random.default_rng(5)
+    Wx = (rng.standard_normal((3 * H, Dx)) * 0.6).astype(np.float32)
+    w = W(dict(d, B=B, F=F, Wx=Wx))
+    tgt = rng.integers(0, 65536, size=(1, N)).astype(np.uint16)
+    base = O.run(w, 1, N, target=tgt, logits=True)
+    step = lambda n: n // B + (n % B) * (F + 1)
+    future_dep = False
+    for q in range(N):
+        t2 = tgt.copy()
+        t2[0, q] ^= 0x8181
+        r = O.run(w, 1, N, target=t2, logits=True)
+        moved = (np.abs(r["zc"][0] - base["zc"][0]).max(axis=1) > 0) | (np.abs(r["zf"][0] - base["zf"][0]).max(axis=1) > 0)
+        for n in np.flatnonzero(moved):
+            if n == q:
+                continue            # its own fine logits see its own coarse byte
+            assert step(q) < step(n), (q, n)
+            future_dep |= q > n
+    assert future_dep == (F > 0)
+
+
 def test_pruned_blocks_equal_dense_with_zeroed_blocks():
     """Sparse WaveRNN (Sec. 3): pruned weights are exactly zero, so the dense
     oracle on the masked matrix is the sparse model.  Zeroing one more block
