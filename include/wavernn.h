@@ -63,6 +63,14 @@ typedef struct {
   int32_t weight_dtype;  /* wavernn_dtype of the stored weights; arithmetic is fp32 */
   int32_t r_format;      /* wavernn_r_format */
   int32_t max_streams;   /* most utterances one call may sample, 1..64 */
+  int32_t future_horizon; /* F, subscale only (ignored when B = 1): -1 = lockstep rows (all B lanes
+                            make row i together, each seeing the Dx/2 samples before its own of
+                            earlier rows); F >= 0 = the paper's order with future horizon F
+                            (Sec. 4.1): sample B*i + s sees sub-tensors z < s up to position i + F
+                            and its own sub-tensor before i, its context the Dx/4 samples before
+                            and Dx/4 after it (unseen ones zero); lane s runs position i at step
+                            i + s(F + 1), so a call takes n_samples/B + (B - 1)(F + 1) steps.
+                            0 is a valid horizon: set -1 for lockstep. */
 } wavernn_config;
 
 /* Host fp32 weights.  Shapes (H hidden, Hh = H/2, V = 256 classes):

@@ -15,15 +15,25 @@
 namespace {
 
 
-// Vector v is lane v % B of utterance v / B; at step t it makes sample
-// n = B (t0 + t) + v % B of that utterance (Sec. 4; B = 1: n = t0 + t).
-// Index of that sample in the [U][B T] output / target arrays: obase(v) + B t.
-__device__ __forceinline__ size_t obase(const BatchArgs& a, int v) {
-  return (size_t)(v / a.B) * a.B * a.T + v % a.B;
+// Vector v is lane s = v % B of utterance v / B.  At step t it runs position
+// p = vpos(v, t) and makes sample n = B (t0 + p) + s of that utterance
+// (Sec. 4; B = 1: n = t0 + t): p = t for lockstep rows, p = t - s (F + 1)
+// with future horizon F (Sec. 4.1: a sub-tensor starts F + 1 steps after the
+// one before it, so the lanes of one step are at different positions and a
+// lane idles before its first and after its last position).
+__device__ __forceinline__ int64_t vpos(const BatchArgs& a, int v, int64_t t) {
+  return a.F >= 0 ? t - (int64_t)(v % a.B) * (a.F + 1) : t;
 }
-// Offset (floats) of the bias + conditioning row vector v uses at step t.
+// Index of sample B p + s in the [U][B rows] output / target arrays: obase(v) + B p.
+__device__ __forceinline__ size_t obase(const BatchArgs& a, int v) {
+  return (size_t)(v / a.B) * a.B * a.rows + v % a.B;
+}
+// Offset (floats) of the bias + conditioning row vector v uses at step t
+// (an idle lane's position clamped to its first or last).
 __device__ __forceinline__ int64_t cb_offset(const BatchArgs& a, int v, int64_t t) {
-  int64_t fr = ((int64_t)a.B * (a.t0 + t) + v % a.B) / a.frame_len;
+  int64_t p = vpos(a, v, t);
+  p = p < 0 ? 0 : p >= a.rows ? a.rows - 1 : p;
+  int64_t fr = ((int64_t)a.B * (a.t0 + p) + v % a.B) / a.frame_len;
   if (fr >= a.n_cb) fr = a.n_cb - 1;
   return ((int64_t)(v / a.B) * a.n_cb + fr) * 3 * a.P.H;
 }
@@ -177,7 +187,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   float* hfs = hcs + L * 448;                      // [L][448] fine half of h (= y_f)
   float* gv = hfs + L * 448;                       // [4L][448] staged pre-activations and e-gate bias of the gate threads
   int64_t* cbo = (int64_t*)(gv + 4 * L * 448);    // [L] bias + conditioning row offsets of this step
-  int* misc = (int*)(cbo + L);                     // [0] abort, [8+b] c_t, [16+b] c_prev, [24+b] f_prev
+  int* misc = (int*)(cbo + L);                     // [0] abort, [8+b] c_t, [16+b] c_prev, [24+b] f_prev,
+                                                   // [48+b] step - position of vector b
   float* fmisc = (float*)(misc + 32);              // [b] lse_c, [8+b] z_c[c] of vector b
   float2* uni = (float2*)(misc + 64);              // [2][L][64] (u_c, u_f) of a batch of 64 steps
   int* tgt = (int*)(uni + 2 * L * 64);             // [2][L][64] teacher-forcing targets
@@ -238,6 +249,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
     misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
     misc[8 + tid] = misc[16 + tid];
+    misc[48 + tid] = a.F >= 0 ? ((v0 + tid) % a.B) * (a.F + 1) : 0;   // position of vector tid: t - misc[48 + tid]
   }
   xw* X = a.xc + (size_t)g * P.x_words;
   const xw* GA = X + P.x_ga;
@@ -321,15 +333,6 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
 #pragma unroll
       for (int jj = 0; jj < NH; ++jj) s += stage[(m * NH + jj) * WR_THREADS];
       zs[(sp + 2 * m) * 256 + v] = s;
-    }
-  };
-  // every head: the classes of all vectors of the group from their owners
-  auto receive = [&](const xw* cls, uint32_t tag, int slot, int64_t t_next) {
-    if (tid < L) {
-      float y;
-      if (!wait_word(cls + tid, tag, &y, a)) misc[0] = 1;
-      misc[slot + tid] = (int)y;
-      if (t_next >= 0 && t_next < a.T) cbo[tid] = cb_offset(a, min(v0 + tid, a.S - 1), t_next);
     }
   };
   // The 3L pre-activation words of gate thread u (two batches of loads) and
@@ -433,7 +436,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     const float rg = fsig(gw[1] + pr);
     const float e = ftanh(__builtin_fmaf(rg, gw[2], pe + cbe));
     float* hs = (fine ? hfs : hcs) + sb * 448 + su;
-    const float hn = __builtin_fmaf(uu, *hs, (1.0f - uu) * e);
+    const int64_t pos = t - misc[48 + sb];        // an idle lane keeps its state
+    const float hn = pos >= 0 && pos < a.rows ? __builtin_fmaf(uu, *hs, (1.0f - uu) * e) : *hs;
     *hs = hn;
     unsigned char* img = fine ? imf : imc;
     aput(img + (su >> 5) * WR_FRAG, su & 31, xround(hn), sb);
@@ -457,13 +461,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const int vw = min(v0 + bw, a.S - 1);
   const size_t ob = obase(a, vw);
   auto fill_batch = [&](int64_t t, int buf) {       // wave w: uniforms / targets of its owned vector
-    const int64_t s = t + lane;
-    const int vb = vw;
-    if (s < a.T) {
+    const int64_t s = t + lane, p = vpos(a, vw, s);
+    if (s < a.T && p >= 0 && p < a.rows) {
       float uc, uf;
-      wr_uniforms(a.seed, (uint64_t)vb, (uint64_t)(a.t0 + s), &uc, &uf);
+      wr_uniforms(a.seed, (uint64_t)vw, (uint64_t)(a.t0 + p), &uc, &uf);
       uni[(buf * L + wave) * 64 + lane] = float2{uc, uf};
-      tgt[(buf * L + wave) * 64 + lane] = a.target ? a.target[ob + (size_t)a.B * s] : 0;
+      tgt[(buf * L + wave) * 64 + lane] = a.target ? a.target[ob + (size_t)a.B * p] : 0;
     }
   };
   if (wave < nown) fill_batch(0, 0);
@@ -498,7 +501,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float rg = fsig(gv[(3 * b + 1) * 448 + u] + __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0));
         const float e = ftanh(
             __builtin_fmaf(rg, gv[(3 * b + 2) * 448 + u], __builtin_fmaf(ic[2][1], x1, ic[2][0] * x0) + cbe));
-        const float hn = __builtin_fmaf(uu, hcs[b * 448 + u], (1.0f - uu) * e);
+        const int64_t pos = t - misc[48 + b];      // an idle lane keeps its state
+        const float hn = pos >= 0 && pos < a.rows ? __builtin_fmaf(uu, hcs[b * 448 + u], (1.0f - uu) * e)
+                                                  : hcs[b * 448 + u];
         hcs[b * 448 + u] = hn;
         aput(imc + (u >> 5) * WR_FRAG, u & 31, hn, b);
         if (mine) xpub(YC + b * Hh + u, tag, hn);   // this head's slice, for the units
@@ -522,19 +527,20 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       const int forced = a.target ? (tgt[bs] >> 8) : -1;
       const int c = draw_wave<false>(zs + wave * 256, nullptr, b2l, uni[bs].x, forced, zk + wave * 256,
                                      a.nll_out ? &lse : nullptr);
-      if (live && a.zc_out)
-        *(float4*)(a.zc_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
+      const int64_t pw = t - misc[48 + bw];         // this vector's position; an idle lane keeps its classes
+      const bool act = pw >= 0 && pw < a.rows;
+      if (live && act && a.zc_out)
+        *(float4*)(a.zc_out + (ob + (size_t)a.B * pw) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        if (ALL || SLICE) misc[8 + bw] = c;
-        if (!ALL) xpub(CC + bw, tag, (float)c);
+        if (act) misc[8 + bw] = c;
+        if (!ALL) xpub(CC + bw, tag, (float)misc[8 + bw]);
         if (a.nll_out) {
           fmisc[wave] = lse;
           fmisc[8 + wave] = zk[wave * 256 + c];
         }
       }
     }
-    if (!ALL && !SLICE) receive(CC, tag, 8, -1);
     __syncthreads();
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
@@ -554,7 +560,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float e = ftanh(__builtin_fmaf(
             rg, gv[(3 * b + 2) * 448 + u],
             __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0)) + cbe));
-        const float hn = __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e);
+        const int64_t pos = t - misc[48 + b];
+        const float hn = pos >= 0 && pos < a.rows ? __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e)
+                                                  : hfs[b * 448 + u];
         hfs[b * 448 + u] = hn;
         aput(imf + (u >> 5) * WR_FRAG, u & 31, hn, b);
         if (mine) xpub(YF + b * Hh + u, tag, hn);
@@ -578,33 +586,30 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       const int f = draw_wave<false>(zs + wave * 256, nullptr, b4l, uni[bs].y, forced, zk + wave * 256,
                                      a.nll_out ? &lse : nullptr);
       const int c = misc[8 + bw];
-      if (live && a.zf_out)
-        *(float4*)(a.zf_out + (ob + (size_t)a.B * t) * WR_CLASSES + 4 * lane) =
+      const int64_t pw = t - misc[48 + bw];
+      const bool act = pw >= 0 && pw < a.rows;
+      if (live && act && a.zf_out)
+        *(float4*)(a.zf_out + (ob + (size_t)a.B * pw) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        if (!ALL) xpub(CF + bw, tag, (float)f);
-        if (SLICE) misc[24 + bw] = f;                // the owner's record (final state)
-        if (a.ux && writer) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for the context of later rows
-        if (live) {
-          if (a.out) a.out[ob + (size_t)a.B * t] = (uint16_t)(256 * c + f);
+        if (SLICE && act) misc[24 + bw] = f;         // the owner's record (final state)
+        if (!ALL) xpub(CF + bw, tag, (float)misc[24 + bw]);
+        if (a.ux && writer && act) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for later contexts
+        if (live && act) {
+          if (a.out) a.out[ob + (size_t)a.B * pw] = (uint16_t)(256 * c + f);
           if (a.nll_out)
-            a.nll_out[ob + (size_t)a.B * t] = (fmisc[wave] - fmisc[8 + wave]) + (lse - zk[wave * 256 + f]);
+            a.nll_out[ob + (size_t)a.B * pw] = (fmisc[wave] - fmisc[8 + wave]) + (lse - zk[wave * 256 + f]);
         }
         if (ALL) {                                  // this head's own record of the vector's classes
-          misc[16 + bw] = c;
-          misc[24 + bw] = f;
+          if (act) {
+            misc[16 + bw] = c;
+            misc[24 + bw] = f;
+          }
           if (t + 1 < a.T) cbo[bw] = cb_offset(a, min(v0 + bw, a.S - 1), t + 1);
         }
       }
     }
-    if (!ALL) {
-      if (SLICE) {
-        if (tid < L && t + 1 < a.T) cbo[tid] = cb_offset(a, min(v0 + tid, a.S - 1), t + 1);
-      } else {
-        receive(CF, tag, 24, t + 1);
-      }
-      if (tid < L && !SLICE) misc[16 + tid] = misc[8 + tid];
-    }
+    if (SLICE && tid < L && t + 1 < a.T) cbo[tid] = cb_offset(a, min(v0 + tid, a.S - 1), t + 1);
     __syncthreads();
     if (trw) trace_at(a, t, 10);
   }
@@ -645,8 +650,9 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   const unsigned char* WL = lds + (fw ? WR_BUCT * KT + q * KT : q * KT) * WR_FRAG;   // this wave's LDS half
   unsigned char* img = lds + P.u_lds_w;                                             // [2KT] operand image
   unsigned char* cimg = img + 2 * KT * WR_FRAG;                                     // [KX] context image
-  int* hist = (int*)(cimg + P.KX * WR_FRAG);          // [utterance slot][256]: samples q at q % 256
-  int* misc = hist + WR_HIST * 64;
+  int* hist = (int*)(cimg + P.KX * WR_FRAG);          // [utterance slot][HC]: sample q at q % HC
+  int* misc = hist + (P.KX ? P.HS * P.HC : 0);
+  const int HCm = P.HC - 1;
   const int tile = k * WR_BUCT + q;
   const int gt = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + (lane & 15);
   const int row = gt * H + (fw ? Hh : 0) + i;                  // R row of this lane
@@ -715,11 +721,15 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     xpub2(dst, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
     if (CTX && gt == 2) xpub2(dstx, tag, mfma_row(xa0) + mfma_row(xa1), mfma_row_hi(xa0) + mfma_row_hi(xa1));
   };
-  // Subscale context (Sec. 4): the samples of row t of every utterance of this
-  // group join the history; vector b's context for row t + 1 is the Dx/2
-  // samples before its own, as (c, f) scaled, zero for samples of row t + 1 or
-  // before the start.  Its projection joins the sums of the u and r rows; for
-  // e rows it is kept apart (published on its own: it is not reset-gated).
+  // Subscale context (Sec. 4): the samples drawn at step t by the lanes of
+  // every utterance of this group join the ring; vector b's context for step
+  // t + 1 is Dx/2 samples as (c, f) scaled: lockstep, the ones before its own
+  // sample, zero for samples of row t + 1 or before the start; with horizon F
+  // (Sec. 4.1) Dx/4 before and Dx/4 after its own, zero unless an earlier
+  // sub-tensor made it at a position up to p + F or its own sub-tensor before
+  // p (every such sample was drawn at step t or before).  Its projection
+  // joins the sums of the u and r rows; for e rows it is kept apart
+  // (published on its own: it is not reset-gated).
   const int ub0 = v0 / a.B;                            // first utterance of this group
   const int nut = a.B >= L ? 1 : L / a.B;              // utterances of this group
   auto context = [&](int64_t t) {
@@ -727,10 +737,11 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     if (tid < nut * a.B) {                             // one thread per (utterance, lane)
       const int vv = ub0 * a.B + tid;                  // vector of that lane
       int y = 0;
-      if (vv < a.S) {
+      const int64_t p = vpos(a, vv, t);                // lanes idle at step t drew nothing
+      if (vv < a.S && p >= 0 && p < a.rows) {
         if (!wait_sample(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp, L, vv % L, tag, &y, a)) misc[0] = 1;
-        const int64_t qn = (int64_t)a.B * t + tid % a.B;
-        hist[(tid / a.B) * 256 + (int)(qn & 255)] = y;
+        const int64_t qn = (int64_t)a.B * p + tid % a.B;
+        hist[(tid / a.B) * P.HC + (int)(qn & HCm)] = y;
       }
     }
     __syncthreads();
@@ -738,12 +749,26 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     const int half = a.P.KX * 16;                      // context samples per vector
     for (int x = tid; x < L * half; x += WR_THREADS) {
       const int b = x / half, jj = x % half;
-      const int vb = min(v0 + b, a.S - 1);
-      const int64_t n1 = (int64_t)a.B * (t + 1) + vb % a.B;   // sample this vector makes next
-      const int64_t qn = n1 - 1 - jj;
+      const int vb = min(v0 + b, a.S - 1), s = vb % a.B;
+      const int64_t p1 = vpos(a, vb, t + 1);           // position this vector runs next
+      const int64_t n1 = (int64_t)a.B * p1 + s;        // the sample it makes there
+      int64_t qn;
+      bool seen;
+      if (a.F < 0) {                                   // lockstep: the samples before n1 of earlier rows
+        qn = n1 - 1 - jj;
+        seen = qn >= 0 && qn < (int64_t)a.B * (t + 1);
+      } else {                                         // horizon F: half before n1, half after
+        const int d = jj < half / 2 ? -1 - jj : 1 + (jj - half / 2);
+        qn = n1 + d;
+        // q = B (p1 + dk) + z with 0 <= z < B: small integers only
+        const int sd = s + d + 2 * half * a.B;         // > 0
+        const int dk = sd / a.B - 2 * half, z = sd % a.B;
+        seen = p1 >= 0 && p1 < a.rows && qn >= 0 && qn < (int64_t)a.B * a.rows &&
+               ((z < s && dk <= a.F) || (z == s && dk < 0));
+      }
       float c = 0.0f, f = 0.0f;
-      if (qn >= 0 && qn < (int64_t)a.B * (t + 1)) {
-        const int sv = hist[(vb / a.B - ub0) * 256 + (int)(qn & 255)];
+      if (seen) {
+        const int sv = hist[(vb / a.B - ub0) * P.HC + (int)(qn & HCm)];
         c = fscale(sv >> 8);
         f = fscale(sv & 255);
       }

@@ -233,7 +233,6 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
 // ---------------------------------------------------------------------------
 #define WR_BL 8           // most vectors per group
 #define WR_BUCT 4         // coarse (and fine) row tiles per batched unit
-#define WR_HIST 16        // rows of drawn samples a batched unit keeps (subscale context)
 
 struct BatchPlan {
   int H, Hh, KT, KH, NH, NCT, NU, G, grid;
@@ -244,6 +243,8 @@ struct BatchPlan {
       // g [3][Hh][L], p [NH][L][256], drawn samples [2][L], e-gate context terms [Hh][L] x 2,
       // drawn coarse and fine classes [L] each
   int KX;                 // subscale context column tiles (Dx / 32), 0 without context
+  int HC;                 // drawn samples a unit keeps per utterance (ring, a power of two)
+  int HS;                 // utterances whose samples a unit keeps (slots of HC)
   int lds_h, lds_u, lds;
 };
 
@@ -260,9 +261,11 @@ WR_HD inline int wr_batch_role(const BatchPlan& P, int b, int* g) {
   return P.NH + ku % P.NU;
 }
 
-WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0) {
+// B, F: subscale factor and future horizon (F < 0: lockstep rows), which
+// size the ring of drawn samples a unit keeps for the context.
+WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0, int B = 1, int F = -1) {
   if (H <= 0 || H % 128 || n_vectors < 1 || n_vectors > 8 * WR_BL) return false;
-  if (ctx_dim < 0 || ctx_dim % 32 || ctx_dim > 256) return false;
+  if (ctx_dim < 0 || ctx_dim % 32 || ctx_dim > 256 || B < 1 || F > 1024) return false;
   P->KX = ctx_dim / 32;
   P->H = H;
   P->Hh = H / 2;
@@ -299,9 +302,19 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   // uniforms [2][L][64][2], targets [2][L][64]
   P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * P->L * 64 + 2 * P->L * 256 + 6 * P->L * 448 + 2 * P->L + 64 +
                                                2 * P->L * 64 * 2 + 2 * P->L * 64);
+  // Ring of drawn samples per utterance: lockstep, the Dx/2 samples before
+  // a row plus the row; with horizon F the lanes of an utterance are up to
+  // (B - 1)(F + 1) positions apart, so the newest sample and the oldest one a
+  // context still reads are at most B (B - 1)(F + 1) + Dx/4 apart.
+  {
+    const int need = F < 0 ? ctx_dim / 2 + 2 * B : B * (B - 1) * (F + 1) + ctx_dim / 2 + B;
+    P->HC = 256;
+    while (P->HC < need) P->HC *= 2;
+    P->HS = (ctx_dim > 0 && P->L > B) ? P->L / B : 1;
+  }
   // unit: weights, operand image (2 KT fragments), context image (KX fragments),
-  // sample history [WR_HIST][64], misc [16]
-  P->lds_u = P->u_lds_w + (2 * P->KT + P->KX) * WR_FRAG + 4 * (WR_HIST * 64 + 16);
+  // sample rings [HS][HC], misc [16]
+  P->lds_u = P->u_lds_w + (2 * P->KT + P->KX) * WR_FRAG + 4 * ((ctx_dim > 0 ? P->HS * P->HC : 0) + 16);
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024 && P->grid <= 256;
 }

@@ -106,7 +106,12 @@ PRESETS = {
     "subscale16": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
     "multi64": (896, COND_DIM, 1, 0, None, True, 64, 48000),
     "multi4": (896, COND_DIM, 1, 0, None, True, 4, 24000),   # Sec. 2.1's batch-4 point
+    "subscale16_h4": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
 }
+# Subscale presets in the paper's order with a future horizon (Sec. 4.1):
+# lane s starts F + 1 steps after lane s - 1 (24,000 samples: 1,500 + 15 x 5
+# steps); the others run lockstep rows.
+HORIZON = {"subscale16_h4": 4}
 
 
 def preset(name: str, seed: int = 0) -> dict:
@@ -114,4 +119,6 @@ def preset(name: str, seed: int = 0) -> dict:
     w = make_weights(H, seed=seed, cond_dim=Dc, B=B, ctx_dim=Dx, block=block,
                      density=0.04 if block else 1.0)
     w.update(name=name, bf16=bf16, streams=S, samples=T)
+    if name in HORIZON:
+        w["F"] = HORIZON[name]
     return w

@@ -255,6 +255,69 @@ def test_subscale16_dense896_teacher_forced_within_bf16_tolerance():
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
 
 
+@pytest.mark.parametrize("H,B,S,F", [(256, 8, 2, 1), (128, 16, 1, 2), (256, 4, 2, 0), (128, 16, 3, 1)])
+def test_subscale_horizon_teacher_forced_small_sizes(H, B, S, F):
+    """Subscale in the paper's order with future horizon F (Sec. 4.1): lane s
+    runs position i at step i + s (F + 1) and its context holds samples of
+    earlier sub-tensors up to position i + F (3 utterances of 16 lanes make
+    groups of 8 vectors).  Logits of every sample against the oracle, which
+    generates sub-tensor by sub-tensor."""
+    w = synth.make_weights(H, seed=6, cond_dim=16, B=B, ctx_dim=256)
+    w["F"] = F
+    T = 40 * B
+    feat = synth.features(S, T, cond_dim=16, per_stream_seed=True)
+    tgt = _targets(S, T)
+    m = wavernn.Model(w, dtype="bf16", max_streams=S)
+    assert m.path(S)[0] == "batched"
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, T, feat=feat, target=tgt, logits=True, nll=True)
+    dc = np.abs(r["zc"] - ref["zc"]).max()
+    df = np.abs(r["zf"] - ref["zf"]).max()
+    assert dc <= 1e-3 and df <= 1e-3, (dc, df)
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
+
+
+def test_subscale16_horizon_dense896_teacher_forced_within_bf16_tolerance():
+    w = synth.preset("subscale16_h4")
+    T = 960
+    feat = synth.features(1, T)
+    tgt = _targets(1, T)
+    m = wavernn.Model(w, dtype="bf16")
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, T, feat=feat, target=tgt, logits=True, nll=True)
+    d = max(np.abs(r["zc"] - ref["zc"]).max(), np.abs(r["zf"] - ref["zf"]).max())
+    assert d <= BF16_TOL, d
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
+
+
+def test_subscale_horizon_free_running_draws_valid_and_final_state():
+    """Free-running with horizon F = 2: every lane's draw is valid under the
+    oracle's logits on the GPU trajectory with the lane's Philox stream
+    indexed by position, and the final state is each lane's after its last
+    position."""
+    B, T, F = 8, 480, 2
+    w = synth.make_weights(256, seed=7, cond_dim=16, B=B, ctx_dim=256)
+    w["F"] = F
+    feat = synth.features(1, T, cond_dim=16)
+    m = wavernn.Model(w, dtype="bf16")
+    fin = m.new_state()
+    out = host(m.sample(T, cond=cuda(feat), seed=3, final=fin))
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, T, feat=feat, target=out, logits=True)
+    u = np.array([O.uniforms(3, n % B, n // B) for n in range(T)])
+    c, f = out[0] >> 8, out[0] & 255
+    okc = _check_draws_valid(ref["zc"][0], u[:, 0], c, 1e-3)
+    okf = _check_draws_valid(ref["zf"][0], u[:, 1], f, 1e-3)
+    assert okc.all() and okf.all(), (np.flatnonzero(~okc)[:10], np.flatnonzero(~okf)[:10])
+    assert len(np.unique(out)) > 50
+    last = out[0, T - B:]                            # the last sample of lane s is T - B + s
+    np.testing.assert_array_equal(host(fin["c"]), last >> 8)
+    np.testing.assert_array_equal(host(fin["f"]), last & 255)
+    np.testing.assert_allclose(host(fin["h"]), ref["h"], atol=1e-2)
+
+
 def test_subscale_free_running_draws_are_valid():
     """Every lane's draw is valid under the oracle's logits on the GPU
     trajectory, with the lane's Philox stream indexed by row."""
@@ -417,7 +480,7 @@ def test_sync_floor_runs_below_the_step_time(name):
     assert 0.5 < floor < step, (floor, step)
 
 
-@pytest.mark.parametrize("kind", ["persistent", "block-sparse", "batched", "subscale"])
+@pytest.mark.parametrize("kind", ["persistent", "block-sparse", "batched", "subscale", "subscale-horizon"])
 @pytest.mark.parametrize("T", [1, 2, 65])
 def test_short_runs_match_the_oracle(kind, T):
     """Edge lengths: one step (no unit iteration at all), two steps, and one
@@ -429,15 +492,17 @@ def test_short_runs_match_the_oracle(kind, T):
         fmt = "bsr4x4"
     if kind == "batched":
         S = 3
-    if kind == "subscale":
+    if kind.startswith("subscale"):
         B = 4
         kw.update(B=B, ctx_dim=256)
     w = synth.make_weights(H, seed=12, **kw)
+    if kind == "subscale-horizon":
+        w["F"] = 1
     n = T * B
     feat = synth.features(S, n, cond_dim=16, per_stream_seed=True)
     tgt = _targets(S, n)
     m = wavernn.Model(w, dtype="bf16", r_format=fmt, max_streams=S)
-    assert m.path(S)[0] == {"subscale": "batched"}.get(kind, kind)
+    assert m.path(S)[0] == {"subscale": "batched", "subscale-horizon": "batched"}.get(kind, kind)
     r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
     m.device_status()
     ref = O.run(O.Weights.from_dict(w, bf16=True), S, n, feat=feat, target=tgt, logits=True, nll=True)
