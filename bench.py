@@ -204,9 +204,10 @@ def main() -> int:
     ms = float(np.mean(call_ms))
     samples = S * T
     value = samples * args.steps / wall
-    us_per_sample_step = ms * 1000.0 / (T // w["B"])
+    F = w.get("F", -1)                                 # subscale future horizon: (B - 1)(F + 1) more steps
+    steps_per_launch = T // w["B"] + ((w["B"] - 1) * (F + 1) if F >= 0 else 0)
+    us_per_sample_step = ms * 1000.0 / steps_per_launch
     wb = weight_bytes_per_step(w)
-    steps_per_launch = T // w["B"]
     achieved = wb * steps_per_launch / (ms / 1000.0) / 1e9
     ncu = grid
     lds_peak = ncu * LDS_BYTES_PER_CLK_CU * CLOCK_GHZ
