@@ -107,6 +107,7 @@ const void* wr_uniforms_kernel_ptr();
 const void* wr_persist_kernel_ptr(int KH);   // null if no instantiation for KH
 const void* wr_sparse_kernel_ptr(int KH, int GU);   // null if no instantiation
 const void* wr_cond_kernel_ptr();
-const void* wr_batch_kernel_ptr(int KH, bool ctx, int L);   // null if no instantiation (KH, L vectors per group)
+const void* wr_batch_kernel_ptr(int KH, bool ctx, int L, bool lag);   // null if no instantiation (KH, L vectors
+                                                                      // per group, lag: a future-horizon schedule)
 const void* wr_fill_kernel_ptr();
 const void* wr_floor_kernel_ptr();

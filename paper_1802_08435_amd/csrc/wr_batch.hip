@@ -21,8 +21,11 @@ namespace {
 // with future horizon F (Sec. 4.1: a sub-tensor starts F + 1 steps after the
 // one before it, so the lanes of one step are at different positions and a
 // lane idles before its first and after its last position).
+// (LAG: the kernel instantiated for a horizon schedule; lockstep kernels pay nothing for it.)
+template <bool LAG>
 __device__ __forceinline__ int64_t vpos(const BatchArgs& a, int v, int64_t t) {
-  return a.F >= 0 ? t - (int64_t)(v % a.B) * (a.F + 1) : t;
+  if (!LAG) return t;
+  return t - (int64_t)(v % a.B) * (a.F + 1);
 }
 // Index of sample B p + s in the [U][B rows] output / target arrays: obase(v) + B p.
 __device__ __forceinline__ size_t obase(const BatchArgs& a, int v) {
@@ -30,9 +33,10 @@ __device__ __forceinline__ size_t obase(const BatchArgs& a, int v) {
 }
 // Offset (floats) of the bias + conditioning row vector v uses at step t
 // (an idle lane's position clamped to its first or last).
+template <bool LAG>
 __device__ __forceinline__ int64_t cb_offset(const BatchArgs& a, int v, int64_t t) {
-  int64_t p = vpos(a, v, t);
-  p = p < 0 ? 0 : p >= a.rows ? a.rows - 1 : p;
+  int64_t p = vpos<LAG>(a, v, t);
+  if (LAG) p = p < 0 ? 0 : p >= a.rows ? a.rows - 1 : p;
   int64_t fr = ((int64_t)a.B * (a.t0 + p) + v % a.B) / a.frame_len;
   if (fr >= a.n_cb) fr = a.n_cb - 1;
   return ((int64_t)(v / a.B) * a.n_cb + fr) * 3 * a.P.H;
@@ -170,7 +174,7 @@ __device__ __forceinline__ bool wait_word(const xw* p, uint32_t tag, float* v, c
 }
 
 // ------------------------------------------------------------------ head role
-template <int KH, bool CTX, int L>
+template <int KH, bool CTX, int L, bool LAG>
 __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   constexpr int NH = KH;
@@ -244,12 +248,12 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const float4 b4l = *(const float4*)(a.b4 + 4 * lane);
   if (tid < L) {
     const int vb = min(v0 + tid, a.S - 1);
-    cbo[tid] = cb_offset(a, vb, 0);
+    cbo[tid] = cb_offset<LAG>(a, vb, 0);
     misc[0] = 0;
     misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
     misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
     misc[8 + tid] = misc[16 + tid];
-    misc[48 + tid] = a.F >= 0 ? ((v0 + tid) % a.B) * (a.F + 1) : 0;   // position of vector tid: t - misc[48 + tid]
+    misc[48 + tid] = LAG ? ((v0 + tid) % a.B) * (a.F + 1) : 0;   // position of vector tid: t - misc[48 + tid]
   }
   xw* X = a.xc + (size_t)g * P.x_words;
   const xw* GA = X + P.x_ga;
@@ -386,7 +390,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     const int tile = tid * WR_BUCT, gt = tile / (HH / 16);
     uflag = P.x_ga + (size_t)(gt * HH + 16 * (tile % (HH / 16))) * L;
   }
-  auto slice_gates = [&](bool fine, uint32_t tag, int64_t t) {
+  auto slice_gates = [&](bool fine, uint32_t tag, int64_t t, uint32_t actm) {
     const float cb = a.cb[cbo[sb] + 2 * H + (fine ? HH : 0) + su];
     const size_t go = (fine ? P.x_gf : P.x_ga) + (size_t)su * L + sb;
     const size_t xo = (fine ? P.x_xf : P.x_xc) + (size_t)su * L + sb;
@@ -436,8 +440,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     const float rg = fsig(gw[1] + pr);
     const float e = ftanh(__builtin_fmaf(rg, gw[2], pe + cbe));
     float* hs = (fine ? hfs : hcs) + sb * 448 + su;
-    const int64_t pos = t - misc[48 + sb];        // an idle lane keeps its state
-    const float hn = pos >= 0 && pos < a.rows ? __builtin_fmaf(uu, *hs, (1.0f - uu) * e) : *hs;
+    const float hn = actm >> sb & 1u ? __builtin_fmaf(uu, *hs, (1.0f - uu) * e) : *hs;   // idle: state kept
     *hs = hn;
     unsigned char* img = fine ? imf : imc;
     aput(img + (su >> 5) * WR_FRAG, su & 31, xround(hn), sb);
@@ -461,7 +464,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const int vw = min(v0 + bw, a.S - 1);
   const size_t ob = obase(a, vw);
   auto fill_batch = [&](int64_t t, int buf) {       // wave w: uniforms / targets of its owned vector
-    const int64_t s = t + lane, p = vpos(a, vw, s);
+    const int64_t s = t + lane, p = vpos<LAG>(a, vw, s);
     if (s < a.T && p >= 0 && p < a.rows) {
       float uc, uf;
       wr_uniforms(a.seed, (uint64_t)vw, (uint64_t)(a.t0 + p), &uc, &uf);
@@ -484,12 +487,22 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     if (trw) trace_at(a, t, 0);
+    // bit b: vector b is at one of its lane's positions this step (always so
+    // for lockstep rows; with a horizon lane b runs position t - misc[48 + b])
+    uint32_t actm = ~0u;
+    if (LAG) {
+#pragma unroll
+      for (int b = 0; b < L; ++b) {
+        const int64_t p = t - misc[48 + b];
+        if (p < 0 || p >= a.rows) actm &= ~(1u << b);
+      }
+    }
     const int bs = (int)((t >> 6) & 1) * L * 64 + wave * 64 + (int)(t & 63);   // draw wave's batch slot
     if (own && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
     // (1) coarse gates of every unit and vector: the 24 pre-activation words of
     // thread u are polled together and staged in LDS, then one vector at a time
     if (SLICE) {
-      slice_gates(false, tag, t);
+      slice_gates(false, tag, t, actm);
     } else if (gate) {
       read_gates(GA, X + P.x_xc, tag, 2 * H + u, t);
       if (trg) trace_at(a, t, 11);
@@ -501,9 +514,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float rg = fsig(gv[(3 * b + 1) * 448 + u] + __builtin_fmaf(ic[1][1], x1, ic[1][0] * x0));
         const float e = ftanh(
             __builtin_fmaf(rg, gv[(3 * b + 2) * 448 + u], __builtin_fmaf(ic[2][1], x1, ic[2][0] * x0) + cbe));
-        const int64_t pos = t - misc[48 + b];      // an idle lane keeps its state
-        const float hn = pos >= 0 && pos < a.rows ? __builtin_fmaf(uu, hcs[b * 448 + u], (1.0f - uu) * e)
-                                                  : hcs[b * 448 + u];
+        const float hn = actm >> b & 1u ? __builtin_fmaf(uu, hcs[b * 448 + u], (1.0f - uu) * e)
+                                        : hcs[b * 448 + u];   // an idle lane keeps its state
         hcs[b * 448 + u] = hn;
         aput(imc + (u >> 5) * WR_FRAG, u & 31, hn, b);
         if (mine) xpub(YC + b * Hh + u, tag, hn);   // this head's slice, for the units
@@ -527,14 +539,16 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       const int forced = a.target ? (tgt[bs] >> 8) : -1;
       const int c = draw_wave<false>(zs + wave * 256, nullptr, b2l, uni[bs].x, forced, zk + wave * 256,
                                      a.nll_out ? &lse : nullptr);
-      const int64_t pw = t - misc[48 + bw];         // this vector's position; an idle lane keeps its classes
-      const bool act = pw >= 0 && pw < a.rows;
+      const int64_t pw = LAG ? t - misc[48 + bw] : t;   // this vector's position; an idle lane keeps its classes
+      const bool act = actm >> bw & 1u;
       if (live && act && a.zc_out)
         *(float4*)(a.zc_out + (ob + (size_t)a.B * pw) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
+        int cw = c;                                 // the class word: an idle lane's last class
         if (act) misc[8 + bw] = c;
-        if (!ALL) xpub(CC + bw, tag, (float)misc[8 + bw]);
+        else cw = misc[8 + bw];
+        if (!ALL) xpub(CC + bw, tag, (float)cw);
         if (a.nll_out) {
           fmisc[wave] = lse;
           fmisc[8 + wave] = zk[wave * 256 + c];
@@ -545,7 +559,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (trw) trace_at(a, t, 5);
     // (4) fine gates with c_t
     if (SLICE) {
-      slice_gates(true, tag, t);
+      slice_gates(true, tag, t, actm);
     } else if (gate) {
       read_gates(GF, X + P.x_xf, tag, 2 * H + Hh + u, t);
       if (trg) trace_at(a, t, 12);
@@ -560,9 +574,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         const float e = ftanh(__builtin_fmaf(
             rg, gv[(3 * b + 2) * 448 + u],
             __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0)) + cbe));
-        const int64_t pos = t - misc[48 + b];
-        const float hn = pos >= 0 && pos < a.rows ? __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e)
-                                                  : hfs[b * 448 + u];
+        const float hn = actm >> b & 1u ? __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e)
+                                        : hfs[b * 448 + u];
         hfs[b * 448 + u] = hn;
         aput(imf + (u >> 5) * WR_FRAG, u & 31, hn, b);
         if (mine) xpub(YF + b * Hh + u, tag, hn);
@@ -586,14 +599,18 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       const int f = draw_wave<false>(zs + wave * 256, nullptr, b4l, uni[bs].y, forced, zk + wave * 256,
                                      a.nll_out ? &lse : nullptr);
       const int c = misc[8 + bw];
-      const int64_t pw = t - misc[48 + bw];
-      const bool act = pw >= 0 && pw < a.rows;
+      const int64_t pw = LAG ? t - misc[48 + bw] : t;
+      const bool act = actm >> bw & 1u;
       if (live && act && a.zf_out)
         *(float4*)(a.zf_out + (ob + (size_t)a.B * pw) * WR_CLASSES + 4 * lane) =
             *(const float4*)(zk + wave * 256 + 4 * lane);
       if (lane == 0) {
-        if (SLICE && act) misc[24 + bw] = f;         // the owner's record (final state)
-        if (!ALL) xpub(CF + bw, tag, (float)misc[24 + bw]);
+        int fw = f;
+        if (SLICE) {                                // the owner's record (final state)
+          if (act) misc[24 + bw] = f;
+          else fw = misc[24 + bw];
+        }
+        if (!ALL) xpub(CF + bw, tag, (float)fw);
         if (a.ux && writer && act) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for later contexts
         if (live && act) {
           if (a.out) a.out[ob + (size_t)a.B * pw] = (uint16_t)(256 * c + f);
@@ -605,11 +622,11 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
             misc[16 + bw] = c;
             misc[24 + bw] = f;
           }
-          if (t + 1 < a.T) cbo[bw] = cb_offset(a, min(v0 + bw, a.S - 1), t + 1);
+          if (t + 1 < a.T) cbo[bw] = cb_offset<LAG>(a, min(v0 + bw, a.S - 1), t + 1);
         }
       }
     }
-    if (SLICE && tid < L && t + 1 < a.T) cbo[tid] = cb_offset(a, min(v0 + tid, a.S - 1), t + 1);
+    if (SLICE && tid < L && t + 1 < a.T) cbo[tid] = cb_offset<LAG>(a, min(v0 + tid, a.S - 1), t + 1);
     __syncthreads();
     if (trw) trace_at(a, t, 10);
   }
@@ -639,7 +656,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
 // Wave q < 4 owns coarse row tile 4k + q, wave 4 + q fine row tile 4k + q;
 // each lane of a wave's result holds two vectors of one row, which it
 // publishes (with bias + conditioning for the u and r gates).
-template <int KH, bool CTX, int L>
+template <int KH, bool CTX, int L, bool LAG>
 __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   const BatchPlan& P = a.P;
@@ -652,7 +669,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   unsigned char* cimg = img + 2 * KT * WR_FRAG;                                     // [KX] context image
   int* hist = (int*)(cimg + P.KX * WR_FRAG);          // [utterance slot][HC]: sample q at q % HC
   int* misc = hist + (P.KX ? P.HS * P.HC : 0);
-  const int HCm = P.HC - 1;
+  const int HC = LAG ? P.HC : 256, HCm = HC - 1;   // (256 always holds a lockstep context)
   const int tile = k * WR_BUCT + q;
   const int gt = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + (lane & 15);
   const int row = gt * H + (fw ? Hh : 0) + i;                  // R row of this lane
@@ -737,11 +754,11 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     if (tid < nut * a.B) {                             // one thread per (utterance, lane)
       const int vv = ub0 * a.B + tid;                  // vector of that lane
       int y = 0;
-      const int64_t p = vpos(a, vv, t);                // lanes idle at step t drew nothing
+      const int64_t p = vpos<LAG>(a, vv, t);                // lanes idle at step t drew nothing
       if (vv < a.S && p >= 0 && p < a.rows) {
         if (!wait_sample(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp, L, vv % L, tag, &y, a)) misc[0] = 1;
         const int64_t qn = (int64_t)a.B * p + tid % a.B;
-        hist[(tid / a.B) * P.HC + (int)(qn & HCm)] = y;
+        hist[(tid / a.B) * HC + (int)(qn & HCm)] = y;
       }
     }
     __syncthreads();
@@ -750,11 +767,11 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     for (int x = tid; x < L * half; x += WR_THREADS) {
       const int b = x / half, jj = x % half;
       const int vb = min(v0 + b, a.S - 1), s = vb % a.B;
-      const int64_t p1 = vpos(a, vb, t + 1);           // position this vector runs next
+      const int64_t p1 = vpos<LAG>(a, vb, t + 1);           // position this vector runs next
       const int64_t n1 = (int64_t)a.B * p1 + s;        // the sample it makes there
       int64_t qn;
       bool seen;
-      if (a.F < 0) {                                   // lockstep: the samples before n1 of earlier rows
+      if (!LAG) {                                      // lockstep: the samples before n1 of earlier rows
         qn = n1 - 1 - jj;
         seen = qn >= 0 && qn < (int64_t)a.B * (t + 1);
       } else {                                         // horizon F: half before n1, half after
@@ -768,7 +785,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       }
       float c = 0.0f, f = 0.0f;
       if (seen) {
-        const int sv = hist[(vb / a.B - ub0) * P.HC + (int)(qn & HCm)];
+        const int sv = hist[(vb / a.B - ub0) * HC + (int)(qn & HCm)];
         c = fscale(sv >> 8);
         f = fscale(sv & 255);
       }
@@ -791,7 +808,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     }
   };
   auto cbv = [&](int b, int64_t t) {                           // u and r gates carry bias + conditioning
-    return gt < 2 && b < L ? a.cb[cb_offset(a, min(v0 + b, a.S - 1), t) + row] : 0.0f;
+    return gt < 2 && b < L ? a.cb[cb_offset<LAG>(a, min(v0 + b, a.S - 1), t) + row] : 0.0f;
   };
   // Wait for one half of h of the group's vectors and write the operand
   // tiles kt0 ...: with 8 vectors (7 words per thread) lane jj of wave 0
@@ -872,30 +889,37 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
 
 }  // namespace
 
-template <int KH, bool CTX, int L>
+template <int KH, bool CTX, int L, bool LAG>
 __global__ __launch_bounds__(WR_THREADS, 1) void wr_batch_kernel(BatchArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   int g = 0;
   const int r = wr_batch_role(a.P, blockIdx.x, &g);
   if (r < 0) return;
-  if (r < a.P.NH) bhead_role<KH, CTX, L>(a, g, r, lds);
-  else bunit_role<KH, CTX, L>(a, g, r - a.P.NH, lds);
+  if (r < a.P.NH) bhead_role<KH, CTX, L, LAG>(a, g, r, lds);
+  else bunit_role<KH, CTX, L, LAG>(a, g, r - a.P.NH, lds);
+}
+
+template <int KH, int L>
+static const void* batch_ptr_l(bool ctx, bool lag) {
+  if (!ctx) return (const void*)wr_batch_kernel<KH, false, L, false>;
+  return lag ? (const void*)wr_batch_kernel<KH, true, L, true> : (const void*)wr_batch_kernel<KH, true, L, false>;
 }
 
 template <int KH>
-static const void* batch_ptr(bool ctx, int L) {
-  if (L == 2) return ctx ? (const void*)wr_batch_kernel<KH, true, 2> : (const void*)wr_batch_kernel<KH, false, 2>;
-  if (L == 4) return ctx ? (const void*)wr_batch_kernel<KH, true, 4> : (const void*)wr_batch_kernel<KH, false, 4>;
-  if (L == 8) return ctx ? (const void*)wr_batch_kernel<KH, true, 8> : (const void*)wr_batch_kernel<KH, false, 8>;
+static const void* batch_ptr(bool ctx, int L, bool lag) {
+  if (L == 2) return batch_ptr_l<KH, 2>(ctx, lag);
+  if (L == 4) return batch_ptr_l<KH, 4>(ctx, lag);
+  if (L == 8) return batch_ptr_l<KH, 8>(ctx, lag);
   return nullptr;
 }
 
-const void* wr_batch_kernel_ptr(int KH, bool ctx, int L) {
+const void* wr_batch_kernel_ptr(int KH, bool ctx, int L, bool lag) {
+  if (lag && !ctx) return nullptr;
   switch (KH) {
-    case 1: return batch_ptr<1>(ctx, L);
-    case 2: return batch_ptr<2>(ctx, L);
-    case 3: return batch_ptr<3>(ctx, L);
-    case 7: return batch_ptr<7>(ctx, L);
+    case 1: return batch_ptr<1>(ctx, L, lag);
+    case 2: return batch_ptr<2>(ctx, L, lag);
+    case 3: return batch_ptr<3>(ctx, L, lag);
+    case 7: return batch_ptr<7>(ctx, L, lag);
     default: return nullptr;
   }
 }

@@ -472,7 +472,7 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
     if (!batch_plan(H, v, &Q, m->cfg.ctx_dim, m->cfg.subscale, horizon_of(m->cfg)))
       return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors (future horizon %d: sample ring of the "
                   "units too large for LDS?)", v, horizon_of(m->cfg));
-    const void* k = wr_batch_kernel_ptr(Q.KH, Q.KX > 0, Q.L);
+    const void* k = wr_batch_kernel_ptr(Q.KH, Q.KX > 0, Q.L, horizon_of(m->cfg) >= 0);
     if (!k) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no batched kernel instantiation", H);
     if ((s = check_coresident(m, k, Q.grid, Q.lds, "batched")) != WAVERNN_OK) return s;
     xwords = std::max(xwords, (size_t)Q.G * Q.x_words);
@@ -655,7 +655,7 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   }
   wavernn_status st = launch_cond(m, io.cond, n_cb, io.S, m->d_bcb, io.st);
   if (st != WAVERNN_OK) return st;
-  const void* kernel = wr_batch_kernel_ptr(B.KH, B.KX > 0, B.L);
+  const void* kernel = wr_batch_kernel_ptr(B.KH, B.KX > 0, B.L, F >= 0);
   if (!kernel) return fail(WAVERNN_E_UNSUPPORTED, "no batched kernel for %d vectors", V);
   if ((st = launch_fill(m->d_bxc, (int64_t)B.G * B.x_words, io.st)) != WAVERNN_OK) return st;
   BatchArgs a;
