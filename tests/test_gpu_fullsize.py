@@ -1,0 +1,125 @@
+"""GPU parity at the benchmark's full sizes, in the launch configuration
+bench.py times: one call over the whole utterance(s).
+
+The oracle cannot replay 24,000-step trajectories at H = 896 (or 2048) within a
+test, so it checks sampled windows step by step from the GPU's own state, and
+properties that hold at any size cover the rest:
+
+* the full-length call equals the same call split into chained calls, bit for
+  bit, so the state handed over at a split is the state the full call had there;
+* from that state at a sampled position p, the oracle's teacher-forced logits
+  over the next K samples of the full call's output match the GPU's within the
+  bf16 tolerance, and every one of those samples is a valid draw under the
+  oracle's distribution and the Philox uniforms of its absolute position;
+* subscale calls (which start at sample 0) are checked on their first rows
+  against the oracle, on prefix invariance (the first rows of the full call
+  equal a short call's) and on the state bound |h| <= 1 (a GRU state is a
+  convex mix of tanh values).
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from oracle import oracle as O  # noqa: E402
+from paper_1802_08435_amd import synth, wavernn  # noqa: E402
+
+BF16_TOL = 2e-2
+
+
+def cuda(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.cpu().numpy()
+
+
+def _valid(z, u, k, delta=1e-3):
+    z = z.astype(np.float64)
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    C = np.cumsum(p, axis=1)
+    k = k.astype(np.int64)
+    lo = np.where(k > 0, C[np.arange(len(k)), np.maximum(k - 1, 0)], 0.0)
+    hi = C[np.arange(len(k)), k]
+    return (u >= lo - delta) & (u <= hi + delta)
+
+
+def _state(m, st, rows):
+    return {k: host(st[k])[rows] for k in ("h", "c", "f")}
+
+
+@pytest.mark.parametrize("name,fmt,positions,K,check", [
+    ("dense896", "dense", [11000, 23936], 64, [0]),
+    ("sparse2048_4x4", "bsr4x4", [23968], 32, [0]),
+    ("multi64", "dense", [47936], 48, [0, 37, 63]),
+])
+def test_full_length_call_matches_the_oracle_at_sampled_positions(name, fmt, positions, K, check):
+    w = synth.preset(name)
+    S, T = w["streams"], w["samples"]
+    seed = 11
+    feat = synth.features(S, T, per_stream_seed=S > 1)
+    m = wavernn.Model(w, dtype="bf16", r_format=fmt, max_streams=S)
+    fin = m.new_state(S)
+    full = host(m.sample(T, cond=cuda(feat), seed=seed, n_streams=S, final=fin))
+    m.device_status()
+    assert np.abs(host(fin["h"])).max() <= 1.0
+    W = O.Weights.from_dict(w, bf16=True)
+    for p in positions:
+        st = m.new_state(S)
+        a = host(m.sample(p, cond=cuda(feat), seed=seed, n_streams=S, final=st))
+        sp = _state(m, st, slice(None))                           # the full call's state at p
+        fin2 = m.new_state(S)
+        b = host(m.sample(T - p, cond=cuda(feat), seed=seed, n_streams=S, init=st, final=fin2))
+        m.device_status()
+        np.testing.assert_array_equal(np.concatenate([a, b], axis=1), full)
+        np.testing.assert_array_equal(host(fin2["h"]), host(fin["h"]))
+        # the next K samples of the full call, one step at a time from that state
+        tgt = full[:, p:p + K]
+        st["t0"] = p
+        r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat), init=st).items()}
+        m.device_status()
+        for s_ in check:
+            ref = O.run(W, 1, K, feat=feat[s_:s_ + 1], target=tgt[s_:s_ + 1], h0=sp["h"][s_:s_ + 1],
+                        c0=sp["c"][s_:s_ + 1], f0=sp["f"][s_:s_ + 1], t0=p, logits=True)
+            d = max(np.abs(r["zc"][s_] - ref["zc"][0]).max(), np.abs(r["zf"][s_] - ref["zf"][0]).max())
+            assert d <= BF16_TOL, (name, p, s_, d)
+            u = np.array([O.uniforms(seed, s_, p + i) for i in range(K)])
+            okc = _valid(ref["zc"][0], u[:, 0], tgt[s_] >> 8)
+            okf = _valid(ref["zf"][0], u[:, 1], tgt[s_] & 255)
+            assert okc.all() and okf.all(), (name, p, s_, np.flatnonzero(~okc)[:5], np.flatnonzero(~okf)[:5])
+
+
+@pytest.mark.parametrize("name", ["subscale16", "subscale16_h4"])
+def test_full_length_subscale_call_prefix_and_state(name):
+    w = synth.preset(name)
+    T, B = w["samples"], w["B"]
+    R = 48                                                       # rows checked against the oracle
+    feat = synth.features(1, T)
+    m = wavernn.Model(w, dtype="bf16")
+    fin = m.new_state()
+    full = host(m.sample(T, cond=cuda(feat), seed=5, final=fin))
+    m.device_status()
+    assert np.abs(host(fin["h"])).max() <= 1.0
+    assert len(np.unique(full)) > 1000
+    # teacher-forced over the whole call, on the call's own output
+    r = {k: host(v) for k, v in m.score(cuda(full), cond=cuda(feat)).items()}
+    short = {k: host(v) for k, v in m.score(cuda(full[:, :R * B]), cond=cuda(feat)).items()}
+    m.device_status()
+    assert np.isfinite(r["nll"]).all()
+    # a horizon schedule's first rows see later samples of earlier lanes, so
+    # only lockstep rows are a prefix of the call
+    if "F" not in w:
+        np.testing.assert_array_equal(r["zc"][:, :R * B], short["zc"])
+        np.testing.assert_array_equal(r["zf"][:, :R * B], short["zf"])
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, R * B, feat=feat, target=full[:, :R * B], logits=True)
+    src = short if "F" in w else r
+    d = max(np.abs(src["zc"][0, :R * B] - ref["zc"][0]).max(), np.abs(src["zf"][0, :R * B] - ref["zf"][0]).max())
+    assert d <= BF16_TOL, d
+    if "F" not in w:
+        u = np.array([O.uniforms(5, n % B, n // B) for n in range(R * B)])
+        okc = _valid(ref["zc"][0], u[:, 0], full[0, :R * B] >> 8)
+        okf = _valid(ref["zf"][0], u[:, 1], full[0, :R * B] & 255)
+        assert okc.all() and okf.all()
