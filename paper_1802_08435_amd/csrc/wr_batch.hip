@@ -62,26 +62,6 @@ __device__ __forceinline__ bool poll_strided(const xw* base, int stride, uint32_
   }
 }
 
-// Wait until the N words at addr(k) (k < N) carry `tag`; values to v[].
-template <int N, class F>
-__device__ __forceinline__ bool poll_map(F addr, uint32_t tag, float* v, const BatchArgs& a) {
-  uint64_t pending = N >= 64 ? ~0ull : (1ull << N) - 1ull;
-  WaitBudget wb{wr_clock(), 0};
-  for (;;) {
-    xw w[N];
-#pragma unroll
-    for (int k = 0; k < N; ++k) w[k] = (pending >> k & 1ull) ? xpeek(addr(k)) : 0;
-#pragma unroll
-    for (int k = 0; k < N; ++k)
-      if ((pending >> k & 1ull) && xok(w[k], tag)) {
-        v[k] = xval(w[k]);
-        pending &= ~(1ull << k);
-      }
-    if (!pending) return true;
-    if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
-  }
-}
-
 // A pointer the compiler must treat as recomputed here: keeps address
 // arithmetic inside the step loop instead of hoisting dozens of 64-bit
 // addresses into registers for the whole launch.
@@ -166,11 +146,6 @@ __device__ __forceinline__ bool wait_sample(const xw* slots, int L, int v, uint3
     }
     if (!wait_ok(wb, a.err, a.limit, a.err)) return false;
   }
-}
-
-// Wait until *p carries `tag` (the slow path of the straight-line reads below).
-__device__ __forceinline__ bool wait_word(const xw* p, uint32_t tag, float* v, const BatchArgs& a) {
-  return poll_map<1>([&](int) { return p; }, tag, v, a);
 }
 
 // ------------------------------------------------------------------ head role
