@@ -147,11 +147,16 @@ wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t
                                       void* stream);
 
 /* Which kernel serves a call on n_streams streams: 0 single-workgroup fp32,
- * 1 multi-workgroup persistent (one launch per stream), 2 batched persistent
- * (up to 64 streams in one launch, 8 per group of workgroups; models created
- * with max_streams > 1 and a hidden size the persistent kernel serves),
- * 3 persistent with block-sparse R (Sec. 3.2; one launch per stream).
- * Fills *grid and *block with its launch shape; -1 for a null model. */
+ * 1 multi-workgroup persistent (one launch per stream, one after another),
+ * 2 batched persistent (up to 64 streams in one launch, 2, 4 or 8 per group
+ * of workgroups; models created with max_streams > 1 and a hidden size the
+ * persistent kernel serves, and every subscale model), 3 persistent with
+ * block-sparse R (Sec. 3.2; one launch per stream), 4 concurrent persistent
+ * (2 to 4 streams of a dense model whose grids fit the device together: one
+ * batch-1 launch per stream on internal streams forked from and joined back
+ * into the caller's stream; bit-identical to path 1).
+ * Fills *grid and *block with the launch shape of one launch; -1 for a null
+ * model. */
 int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* grid, int32_t* block);
 
 /* Diagnostics: make later wavernn_sample / wavernn_score_teacher_forced calls

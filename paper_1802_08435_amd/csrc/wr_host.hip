@@ -49,6 +49,9 @@ float bf2f(uint16_t b) {
 }
 
 enum Path { PATH_SMALL = 0, PATH_PERSIST = 1, PATH_BATCHED = 2 };
+constexpr int PATH_SPARSE_ID = 3, PATH_CONCURRENT_ID = 4;   // wavernn_model_path's ids of the variants
+#define WR_FAN 4   // concurrent batch-1 launches: the caller's stream and 3 internal ones (HIP's default
+                   // of 4 hardware queues gives each its own)
 
 const u64 kWaitTicks = 200000000ull;  // 2 s of the 100 MHz clock per wait
 
@@ -75,6 +78,14 @@ struct wavernn_model {
   xw* d_xc = nullptr;                // exchange words (zeroed as 64-bit pairs)
   u64* trace = nullptr;
   int64_t trace_steps = 0;
+  // concurrent batch-1 launches: a few utterances, each on its own persistent
+  // grid and its own internal stream, all grids co-resident at once
+  int nfan = 0;                      // most utterances served this way (0: none)
+  hipStream_t fan_st[WR_FAN - 1] = {};  // launches 1 .. (launch 0 runs on the caller's stream)
+  hipEvent_t fan_fork = nullptr, fan_join[WR_FAN - 1] = {};
+  xw* d_fxc[WR_FAN] = {};            // exchange words of launch i
+  float* d_fcb[WR_FAN] = {};         // [fcb_cap][3H] bias + conditioning of launch i
+  int64_t fcb_cap = 0;
   // batched path (several utterances per launch)
   bool has_batch = false;
   BatchPlan bplan;
@@ -102,6 +113,12 @@ struct wavernn_model {
     return WAVERNN_OK;
   }
   ~wavernn_model() {
+    for (int i = 0; i < WR_FAN - 1; ++i) {
+      if (fan_st[i]) (void)hipStreamSynchronize(fan_st[i]);
+      if (fan_st[i]) (void)hipStreamDestroy(fan_st[i]);
+      if (fan_join[i]) (void)hipEventDestroy(fan_join[i]);
+    }
+    if (fan_fork) (void)hipEventDestroy(fan_fork);
     for (void* q : allocs) (void)hipFree(q);
   }
 };
@@ -308,6 +325,30 @@ wavernn_status check_coresident(wavernn_model* m, const void* k, int grid, int l
   if (per_cu < 1 || per_cu * prop.multiProcessorCount < grid)
     return fail(WAVERNN_E_UNSUPPORTED, "%s grid of %d workgroups cannot be co-resident (%d per CU, %d CUs)", what,
                 grid, per_cu, prop.multiProcessorCount);
+  return WAVERNN_OK;
+}
+
+// Concurrent batch-1 launches for up to WR_FAN utterances, when that many
+// persistent grids fit the device together: internal streams (default
+// priority), fork / join events, and per-launch exchange words.
+wavernn_status build_fanout(wavernn_model* m) {
+  const PersistPlan& P = m->plan;
+  int per_cu = 0;
+  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->pk, WR_THREADS, P.lds));
+  hipDeviceProp_t prop;
+  HIPOK(hipGetDeviceProperties(&prop, m->device));
+  int n = std::min(std::min(WR_FAN, (int)m->cfg.max_streams), per_cu * prop.multiProcessorCount / P.grid);
+  if (n < 2) return WAVERNN_OK;
+  HIPOK(hipEventCreateWithFlags(&m->fan_fork, hipEventDisableTiming));
+  for (int i = 0; i < n; ++i) {
+    if (i + 1 < n) {   // launch 0 runs on the caller's stream
+      HIPOK(hipStreamCreateWithFlags(&m->fan_st[i], hipStreamNonBlocking));
+      HIPOK(hipEventCreateWithFlags(&m->fan_join[i], hipEventDisableTiming));
+    }
+    wavernn_status s = m->alloc(&m->d_fxc[i], (size_t)(P.x_words + 1) / 2 * 8);
+    if (s != WAVERNN_OK) return s;
+  }
+  m->nfan = n;
   return WAVERNN_OK;
 }
 
@@ -572,65 +613,115 @@ wavernn_status run_small(wavernn_model* m, const RunIO& io) {
   return WAVERNN_OK;
 }
 
-wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
+// One persistent launch for utterance s of the call, with exchange words xc
+// and bias + conditioning table cb, on stream st.
+wavernn_status launch_persist_one(wavernn_model* m, const RunIO& io, int s, xw* xc, float* cb, int64_t n_cb,
+                                  hipStream_t st) {
   const PersistPlan& P = m->plan;
   const int H = P.H, Dc = m->cfg.cond_dim;
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
-  const int64_t n_cb = Dc > 0 ? io.n_frames : 1;
-  if (n_cb > m->cb_cap) {   // grow the per-frame table (the only allocation a call can make)
+  {
+    const float* feat = io.cond ? io.cond + (size_t)s * io.n_frames * Dc : nullptr;
+    wavernn_status c = launch_cond(m, feat, n_cb, 1, cb, st);
+    if (c != WAVERNN_OK) return c;
+  }
+  wavernn_status stt = launch_fill(xc, P.x_words, st);
+  if (stt != WAVERNN_OK) return stt;
+  PersistArgs a;
+  memset(&a, 0, sizeof a);
+  a.P = P;
+  a.hw = m->d_hw;
+  a.uw = m->d_uw;
+  a.ur = m->d_ur;
+  a.Iw = m->d_I;
+  a.b1 = m->d_b1;
+  a.b2 = m->d_b2;
+  a.b3 = m->d_b3;
+  a.b4 = m->d_b4;
+  a.cb = cb;
+  a.n_cb = n_cb;
+  a.frame_len = Dc > 0 ? frame_len : (1 << 30);
+  a.T = io.T;
+  a.t0 = io.init ? io.init->t0 : 0;
+  a.seed = io.seed;
+  a.stream_id = (uint64_t)s;
+  a.target = io.target ? io.target + (size_t)s * io.T : nullptr;
+  a.out = io.out ? io.out + (size_t)s * io.T : nullptr;
+  a.zc_out = io.zc ? io.zc + (size_t)s * io.T * 256 : nullptr;
+  a.zf_out = io.zf ? io.zf + (size_t)s * io.T * 256 : nullptr;
+  a.nll_out = io.nll ? io.nll + (size_t)s * io.T : nullptr;
+  if (io.init) { a.h_in = io.init->h + (size_t)s * H; a.c_in = io.init->c_prev + s; a.f_in = io.init->f_prev + s; }
+  if (io.fin) { a.h_out = io.fin->h + (size_t)s * H; a.c_out = io.fin->c_prev + s; a.f_out = io.fin->f_prev + s; }
+  a.xc = xc;
+  a.err = m->d_err;
+  a.limit = kWaitTicks;
+  if (s == 0) {
+    a.trace = m->trace;
+    a.trace_steps = m->trace ? m->trace_steps : 0;
+  }
+  void* args[] = {&a};
+  // An ordinary launch: create() checked that the whole grid fits on the
+  // device at once, and every cross-workgroup wait is bounded, so a grid
+  // that did not become co-resident ends with an error, never a hang.
+  HIPOK(hipLaunchKernel(m->pk, dim3(P.grid), dim3(WR_THREADS), args, P.lds, st));
+  return WAVERNN_OK;
+}
+
+// Grow a per-frame table to n_cb frames (the only allocation a call can
+// make; a replaced table stays allocated until the model is destroyed, so a
+// launch still reading it is unaffected).
+wavernn_status grow_cb(wavernn_model* m, float** cb, int64_t* cap, int64_t n_cb) {
+  if (n_cb <= *cap) return WAVERNN_OK;
+  float* p = nullptr;
+  wavernn_status s = m->alloc(&p, (size_t)n_cb * 3 * m->plan.H * 4);
+  if (s != WAVERNN_OK) return s;
+  *cb = p;
+  *cap = n_cb;
+  return WAVERNN_OK;
+}
+
+// Several utterances one after another on the caller's stream.
+wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
+  const int64_t n_cb = m->cfg.cond_dim > 0 ? io.n_frames : 1;
+  if (n_cb > m->cb_cap) HIPOK(hipStreamSynchronize(io.st));
+  wavernn_status st = grow_cb(m, &m->d_cb, &m->cb_cap, n_cb);
+  if (st != WAVERNN_OK) return st;
+  for (int s = 0; s < io.S; ++s)
+    if ((st = launch_persist_one(m, io, s, m->d_xc, m->d_cb, n_cb, io.st)) != WAVERNN_OK) return st;
+  return WAVERNN_OK;
+}
+
+// A few utterances at once: utterance 0 runs the batch-1 kernel on the
+// caller's stream, utterance s > 0 on internal stream s - 1 (each its own
+// grid, exchange words and table), forked from and joined back into the
+// caller's stream, so the call stays stream-ordered.  The grids are
+// co-resident together (checked at create); with one hardware queue per
+// stream (4 by default, so the caller's stream and 3 more) the launches run
+// side by side: at batch 4 about four times the batch-1 rate, where the
+// batched kernel, which shares one grid among the utterances, gives under
+// three.
+wavernn_status run_fanout(wavernn_model* m, const RunIO& io) {
+  const int64_t n_cb = m->cfg.cond_dim > 0 ? io.n_frames : 1;
+  wavernn_status st = WAVERNN_OK;
+  if (n_cb > m->fcb_cap) {
     HIPOK(hipStreamSynchronize(io.st));
-    float* p = nullptr;
-    wavernn_status s = m->alloc(&p, (size_t)n_cb * 3 * H * 4);
-    if (s != WAVERNN_OK) return s;
-    m->d_cb = p;
-    m->cb_cap = n_cb;
-  }
-  for (int s = 0; s < io.S; ++s) {
-    {
-      const float* feat = io.cond ? io.cond + (size_t)s * io.n_frames * Dc : nullptr;
-      wavernn_status c = launch_cond(m, feat, n_cb, 1, m->d_cb, io.st);
-      if (c != WAVERNN_OK) return c;
+    int64_t cap = 0;
+    for (int i = 0; i < m->nfan && st == WAVERNN_OK; ++i) {
+      cap = m->fcb_cap;
+      st = grow_cb(m, &m->d_fcb[i], &cap, n_cb);
     }
-    wavernn_status st = launch_fill(m->d_xc, P.x_words, io.st);
     if (st != WAVERNN_OK) return st;
-    PersistArgs a;
-    memset(&a, 0, sizeof a);
-    a.P = P;
-    a.hw = m->d_hw;
-    a.uw = m->d_uw;
-    a.ur = m->d_ur;
-    a.Iw = m->d_I;
-    a.b1 = m->d_b1;
-    a.b2 = m->d_b2;
-    a.b3 = m->d_b3;
-    a.b4 = m->d_b4;
-    a.cb = m->d_cb;
-    a.n_cb = n_cb;
-    a.frame_len = Dc > 0 ? frame_len : (1 << 30);
-    a.T = io.T;
-    a.t0 = io.init ? io.init->t0 : 0;
-    a.seed = io.seed;
-    a.stream_id = (uint64_t)s;
-    a.target = io.target ? io.target + (size_t)s * io.T : nullptr;
-    a.out = io.out ? io.out + (size_t)s * io.T : nullptr;
-    a.zc_out = io.zc ? io.zc + (size_t)s * io.T * 256 : nullptr;
-    a.zf_out = io.zf ? io.zf + (size_t)s * io.T * 256 : nullptr;
-    a.nll_out = io.nll ? io.nll + (size_t)s * io.T : nullptr;
-    if (io.init) { a.h_in = io.init->h + (size_t)s * H; a.c_in = io.init->c_prev + s; a.f_in = io.init->f_prev + s; }
-    if (io.fin) { a.h_out = io.fin->h + (size_t)s * H; a.c_out = io.fin->c_prev + s; a.f_out = io.fin->f_prev + s; }
-    a.xc = m->d_xc;
-    a.err = m->d_err;
-    a.limit = kWaitTicks;
-    if (s == 0) {
-      a.trace = m->trace;
-      a.trace_steps = m->trace ? m->trace_steps : 0;
-    }
-    void* args[] = {&a};
-    // An ordinary launch: create() checked that the whole grid fits on the
-    // device at once, and every cross-workgroup wait is bounded, so a grid
-    // that did not become co-resident ends with an error, never a hang.
-    HIPOK(hipLaunchKernel(m->pk, dim3(P.grid), dim3(WR_THREADS), args, P.lds, io.st));
+    m->fcb_cap = cap;
   }
+  HIPOK(hipEventRecord(m->fan_fork, io.st));
+  for (int s = 1; s < io.S; ++s) {
+    HIPOK(hipStreamWaitEvent(m->fan_st[s - 1], m->fan_fork, 0));
+    if ((st = launch_persist_one(m, io, s, m->d_fxc[s], m->d_fcb[s], n_cb, m->fan_st[s - 1])) != WAVERNN_OK)
+      return st;
+    HIPOK(hipEventRecord(m->fan_join[s - 1], m->fan_st[s - 1]));
+  }
+  if ((st = launch_persist_one(m, io, 0, m->d_fxc[0], m->d_fcb[0], n_cb, io.st)) != WAVERNN_OK) return st;
+  for (int s = 1; s < io.S; ++s) HIPOK(hipStreamWaitEvent(io.st, m->fan_join[s - 1], 0));
   return WAVERNN_OK;
 }
 
@@ -706,7 +797,10 @@ wavernn_status run(wavernn_model* m, RunIO& io) {
   HIPOK(hipGetDevice(&dev));
   if (dev != m->device) return fail(WAVERNN_E_INVALID, "model lives on device %d, current device is %d", m->device, dev);
   if (m->path == PATH_SMALL) return run_small(m, io);
-  if (m->path == PATH_PERSIST) return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);
+  if (m->path == PATH_PERSIST) {
+    if (io.S > 1 && io.S <= m->nfan) return run_fanout(m, io);
+    return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);
+  }
   if (m->path == PATH_BATCHED) return run_batch(m, io);
   return fail(WAVERNN_E_UNSUPPORTED, "no kernel for this configuration");
 }
@@ -767,6 +861,7 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
       s = build_persist(m, w);
       if (s == WAVERNN_OK && cfg->max_streams > 1 && batch_plan(H, cfg->max_streams, &m->bplan))
         s = build_batch(m, w);
+      if (s == WAVERNN_OK && cfg->max_streams > 1) s = build_fanout(m);
     }
   } else {
     s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no kernel plan (need a multiple of 128 whose blocks fit LDS)", H);
@@ -835,11 +930,13 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
              batch_plan(m->cfg.hidden, (n_streams > 0 ? n_streams : 1) * m->cfg.subscale, &B, m->cfg.ctx_dim,
                         m->cfg.subscale, horizon_of(m->cfg))) {
     g = B.grid, b = WR_THREADS;
+  } else if (m->path == PATH_PERSIST && n_streams > 1 && n_streams <= m->nfan) {
+    path = PATH_CONCURRENT_ID, g = m->plan.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST && n_streams > 1 && m->has_batch && batch_plan(m->cfg.hidden, n_streams, &B)) {
     path = PATH_BATCHED, g = B.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST) {
     g = m->plan.grid, b = WR_THREADS;
-    if (m->sparse) path = 3;
+    if (m->sparse) path = PATH_SPARSE_ID;
   }
   if (grid) *grid = g;
   if (block) *block = b;

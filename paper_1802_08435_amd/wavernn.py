@@ -18,7 +18,7 @@ _lib = None
 OK, E_INVALID, E_UNSUPPORTED, E_OOM, E_HIP, E_DEVICE = range(6)
 F32, BF16 = 0, 1
 R_DENSE, R_BSR_4X4, R_BSR_16X1 = 0, 1, 2
-PATHS = {0: "single-workgroup", 1: "persistent", 2: "batched", 3: "block-sparse"}
+PATHS = {0: "single-workgroup", 1: "persistent", 2: "batched", 3: "block-sparse", 4: "concurrent"}
 
 
 class WaveRNNError(RuntimeError):

@@ -113,11 +113,12 @@ def test_persistent_teacher_forced_small_sizes(H):
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
 
 
-@pytest.mark.parametrize("H,S", [(128, 2), (256, 9), (384, 16), (256, 24), (256, 40)])
+@pytest.mark.parametrize("H,S", [(128, 6), (256, 9), (384, 16), (256, 24), (256, 40)])
 def test_batched_teacher_forced_small_sizes(H, S):
     """Several utterances in one launch (groups of 2 vectors up to 16
     utterances, 4 up to 32, 8 above; S=9 leaves an idle vector in the last
-    group): logits of every stream against the oracle."""
+    group; up to 4 utterances take the concurrent path instead): logits of
+    every stream against the oracle."""
     w = synth.make_weights(H, seed=1, cond_dim=16)
     T = 200
     feat = synth.features(S, T, cond_dim=16, per_stream_seed=True)
@@ -217,6 +218,45 @@ def test_batched_free_running_draws_valid_and_chunked_equals_one_call(S):
         okf = _check_draws_valid(ref["zf"][s_], u[:, 1], f, 1e-3)
         assert okc.all() and okf.all(), (s_, np.flatnonzero(~okc)[:10], np.flatnonzero(~okf)[:10])
     assert len({tuple(x[:50]) for x in whole}) == S     # streams differ
+
+
+# ------------------------------------------------------------- concurrent batch-1 launches
+
+@pytest.mark.parametrize("H,S", [(256, 3), (896, 4)])
+def test_concurrent_streams_teacher_forced_free_running_and_chunked(H, S):
+    """2 to 4 utterances of a dense model run as concurrent batch-1 launches
+    (one grid per utterance on internal streams): teacher-forced logits
+    against the oracle, free-running draws valid on each utterance's Philox
+    stream, two chained calls equal one, and the caller's stream sees every
+    result (stream-ordered)."""
+    w = synth.preset("dense896") if H == 896 else synth.make_weights(H, seed=5, cond_dim=16)
+    Dc = w["Wc"].shape[1]
+    T = 240
+    feat = synth.features(S, T, cond_dim=Dc, per_stream_seed=True)
+    tgt = _targets(S, T)
+    m = wavernn.Model(w, dtype="bf16", max_streams=S)
+    assert m.path(S)[0] == "concurrent"
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    W = O.Weights.from_dict(w, bf16=True)
+    ref = O.run(W, S, T, feat=feat, target=tgt, logits=True, nll=True)
+    d = max(np.abs(r["zc"] - ref["zc"]).max(), np.abs(r["zf"] - ref["zf"]).max())
+    assert d <= BF16_TOL, d
+    fin = m.new_state(S)
+    whole = host(m.sample(T, cond=cuda(feat), seed=9, n_streams=S, final=fin))
+    st = m.new_state(S)
+    a = host(m.sample(100, cond=cuda(feat), seed=9, n_streams=S, final=st))
+    b = host(m.sample(T - 100, cond=cuda(feat), seed=9, n_streams=S, init=st, final=st))
+    m.device_status()
+    np.testing.assert_array_equal(np.concatenate([a, b], axis=1), whole)
+    np.testing.assert_array_equal(host(st["h"]), host(fin["h"]))
+    ref = O.run(W, S, T, feat=feat, target=whole, logits=True)
+    for s_ in range(S):
+        u = np.array([O.uniforms(9, s_, t) for t in range(T)])
+        okc = _check_draws_valid(ref["zc"][s_], u[:, 0], whole[s_] >> 8, 1e-3)
+        okf = _check_draws_valid(ref["zf"][s_], u[:, 1], whole[s_] & 255, 1e-3)
+        assert okc.all() and okf.all(), (s_, np.flatnonzero(~okc)[:10], np.flatnonzero(~okf)[:10])
+    assert len({tuple(x[:50]) for x in whole}) == S
 
 
 # ------------------------------------------------------------- subscale
@@ -480,7 +520,8 @@ def test_sync_floor_runs_below_the_step_time(name):
     assert 0.5 < floor < step, (floor, step)
 
 
-@pytest.mark.parametrize("kind", ["persistent", "block-sparse", "batched", "subscale", "subscale-horizon"])
+@pytest.mark.parametrize("kind", ["persistent", "block-sparse", "batched", "concurrent", "subscale",
+                                  "subscale-horizon"])
 @pytest.mark.parametrize("T", [1, 2, 65])
 def test_short_runs_match_the_oracle(kind, T):
     """Edge lengths: one step (no unit iteration at all), two steps, and one
@@ -491,7 +532,9 @@ def test_short_runs_match_the_oracle(kind, T):
         kw.update(block=(4, 4), density=0.1)
         fmt = "bsr4x4"
     if kind == "batched":
-        S = 3
+        S = 5
+    if kind == "concurrent":
+        S = 2
     if kind.startswith("subscale"):
         B = 4
         kw.update(B=B, ctx_dim=256)
