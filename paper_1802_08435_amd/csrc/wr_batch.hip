@@ -1,15 +1,18 @@
-// Batched persistent WaveRNN sampler: up to 64 independent utterances per
-// launch, WR_BL = 8 per group (Sec. 2.1; many utterances share one GPU).
+// Batched persistent WaveRNN sampler: up to 64 independent utterances, or
+// the lanes of subscale rows, per launch in groups of L = 2, 4 or 8 vectors
+// (Sec. 2.1: many utterances share one GPU; Sec. 4: B samples per step).
 //
-// A group is the batch-1 structure of wr_persist.hip serving 8 vectors at
-// once.  Every matrix-vector product of the step becomes an 8-row product on
+// A group is the batch-1 structure of wr_persist.hip serving L vectors at
+// once.  Every matrix-vector product of the step becomes an L-row product on
 // the matrix cores at the same instruction count: operand A holds vector b in
 // rows 2b (bf16 high part) and 2b+1 (remainder), and lane l of the result
-// holds vectors 2(l/16) and 2(l/16)+1 of row l%16.  Per step and half, the
-// heads evaluate every gate of every vector, run their O1 rows / O2 columns
-// and publish 8 x 256 partial logits; the owner of each vector (head v mod NH)
-// sums that vector's partials, draws its class and publishes it, and every
-// head reads the 8 classes.
+// holds vectors 2(l/16) and 2(l/16)+1 of row l%16.  Per step and half the
+// heads run their O1 rows / O2 columns for all vectors and publish L x 256
+// partial logits.  With L <= 4 every head evaluates every gate of every
+// vector and sums and draws every vector; with L = 8 head j evaluates the
+// gates of its own 64 units for all vectors and the heads exchange those
+// slices of y, and vector v is owned by head v mod NH, which alone sums its
+// partials, draws it and publishes its classes.
 #include "wr_kern.h"
 
 namespace {

@@ -90,7 +90,7 @@ struct PersistPlan {
   int grid;               // workgroups launched: head j at block 8j, units on the others
   int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[2 KO], O4[2 KO]
   int u_lds_w;            // unit LDS block: dense R tiles, or the block-sparse records
-  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (64-bit words)
+  int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (32-bit words)
   int x_ps;               // words between the partial-logit blocks of consecutive heads
   int lds_h, lds_u, lds;  // LDS bytes
 };
@@ -236,7 +236,7 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
 
 struct BatchPlan {
   int H, Hh, KT, KH, NH, NCT, NU, G, grid;
-  int L;                  // vectors per group (4 or 8)
+  int L;                  // vectors per group (2, 4 or 8)
   int hw_frags;           // head fragments per wave (as the batch-1 plan)
   int u_lds_w;            // unit LDS weights: [UCT][KT] coarse tiles, then [UCT][KT] fine tiles
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_sp, x_xc, x_xf, x_cc, x_cf, x_words;   // per group: y [L][Hh],

@@ -3,18 +3,22 @@
 // The whole utterance runs inside one launch (Sec. 2.1): weights stay in VGPRs
 // and LDS across the launch, and every step evaluates the GRU of Eq. 2, the
 // coarse head, the coarse draw, the fine half, the fine head and the fine draw.
-// Workgroups exchange vectors through tagged 64-bit words (value + step tag)
+// Workgroups exchange vectors through tagged 32-bit words (the fp32 value with
+// its lowest mantissa bit replaced by the parity of the producing step)
 // instead of grid-wide barriers.
 //
-// Critical path of a step, inside the NH head workgroups (all on one XCD):
+// A step, on the NH head workgroups (all on one XCD):
 //   coarse gates of every unit (every head, identically, from pre-activations
-//   the unit workgroups published a step ahead)
+//   the unit workgroups published for this step)
 //   -> own 64 rows of O1, relu, own 64 columns of O2 -> 256 partial logits
 //   --one exchange--> every head sums the NH partials, draws c_t
 //   -> fine gates of every unit -> O3 rows, O4 columns -> partial logits
 //   --one exchange--> sum, draw f_t.
-// Off the critical path, the NU unit workgroups receive y_c and y_f and compute
-// R h for the next step (the paper's "gate" work), adding bias + conditioning.
+// Meanwhile the NU unit workgroups receive y_c and y_f and compute R h for
+// the next step (the paper's "gate" work), adding bias + conditioning; from
+// y_f to the next step's pre-activations (two exchanges and R_f y_f) is the
+// longest chain of a step at H = 896, longer than the fine half's exchange
+// and draw it runs beside.
 #include "wr_kern.h"
 #include "wr_layout.h"
 #include "wr_args.h"
@@ -44,7 +48,8 @@ __device__ __forceinline__ const float* cb_row(const PersistArgs& a, int64_t n) 
 //   into LDS, then all 8 waves finish units tid + 512 m; the state stays in
 //   LDS (registers are short with the larger O-layer slices).
 // All 8 waves run the MFMA layers and gather the partial logits (two threads
-// per class); wave 7 publishes this head's slice of y for the unit workgroups.
+// per class); the gate threads of this head's slice of units publish it for
+// the unit workgroups.
 template <int KH, int RT, int GU, bool SPLIT>
 __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
   constexpr int KC = 8 / RT;                       // column-tile chunks
