@@ -66,7 +66,7 @@ typedef struct {
   int32_t future_horizon; /* F, subscale only (ignored when B = 1): -1 = lockstep rows (all B lanes
                             make row i together, each seeing the Dx/2 samples before its own of
                             earlier rows); F >= 0 = the paper's order with future horizon F
-                            (Sec. 4.1): sample B*i + s sees sub-tensors z < s up to position i + F
+                            (Sec. 4.2): sample B*i + s sees sub-tensors z < s up to position i + F
                             and its own sub-tensor before i, its context the Dx/4 samples before
                             and Dx/4 after it (unseen ones zero); lane s runs position i at step
                             i + s(F + 1), so a call takes n_samples/B + (B - 1)(F + 1) steps.

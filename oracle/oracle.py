@@ -146,7 +146,7 @@ class Weights:
     Wx: np.ndarray | None = None
     frame_len: int = 120
     B: int = 1
-    F: int = -1          # subscale future horizon (Sec. 4.1); < 0: lockstep rows
+    F: int = -1          # subscale future horizon (Sec. 4.2); < 0: lockstep rows
 
     @staticmethod
     def from_dict(d: dict, bf16: bool = False) -> "Weights":

@@ -41,7 +41,7 @@
  *     (3H x Dx).  Two readings:
  *       F < 0, lockstep rows: all B lanes make row i together; the context of
  *         n is the Dx/2 samples before n, zero for those of row i or later;
- *       F >= 0, the paper's order with future horizon F (Sec. 4.1): sub-tensor
+ *       F >= 0, the paper's order with future horizon F (Sec. 4.2): sub-tensor
  *         s is generated after sub-tensors 0 .. s-1, and sample B*i + s sees
  *         sub-tensors z < s up to position i + F and its own sub-tensor
  *         before position i (no distant dependencies); its context is the

@@ -21,7 +21,7 @@
  *   O3 [H/2][H/2] b3 [H/2]   O4 [256][H/2] b4 [256]   (fine head)   */
 typedef struct {
   int32_t H, Dc, frame_len, B, Dx;
-  int32_t F;   /* subscale future horizon (Sec. 4.1): < 0 lockstep rows, >= 0 the paper's order */
+  int32_t F;   /* subscale future horizon (Sec. 4.2): < 0 lockstep rows, >= 0 the paper's order */
   const float *R, *I, *b, *Wc, *Wx;
   const float *O1, *b1, *O2, *b2, *O3, *b3, *O4, *b4;
 } orc_model;

@@ -21,7 +21,7 @@ namespace {
 // Vector v is lane s = v % B of utterance v / B.  At step t it runs position
 // p = vpos(v, t) and makes sample n = B (t0 + p) + s of that utterance
 // (Sec. 4; B = 1: n = t0 + t): p = t for lockstep rows, p = t - s (F + 1)
-// with future horizon F (Sec. 4.1: a sub-tensor starts F + 1 steps after the
+// with future horizon F (Sec. 4.2: a sub-tensor starts F + 1 steps after the
 // one before it, so the lanes of one step are at different positions and a
 // lane idles before its first and after its last position).
 // (LAG: the kernel instantiated for a horizon schedule; lockstep kernels pay nothing for it.)
@@ -720,7 +720,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   // every utterance of this group join the ring; vector b's context for step
   // t + 1 is Dx/2 samples as (c, f) scaled: lockstep, the ones before its own
   // sample, zero for samples of row t + 1 or before the start; with horizon F
-  // (Sec. 4.1) Dx/4 before and Dx/4 after its own, zero unless an earlier
+  // (Sec. 4.2) Dx/4 before and Dx/4 after its own, zero unless an earlier
   // sub-tensor made it at a position up to p + F or its own sub-tensor before
   // p (every such sample was drawn at step t or before).  Its projection
   // joins the sums of the u and r rows; for e rows it is kept apart

@@ -131,7 +131,7 @@ struct Rounder {
   float operator()(float v) const { return bf16 ? bf2f(f2bf(v)) : v; }
 };
 
-// Future horizon of a subscale model (Sec. 4.1), -1 for lockstep rows or B = 1.
+// Future horizon of a subscale model (Sec. 4.2), -1 for lockstep rows or B = 1.
 static int horizon_of(const wavernn_config& c) { return c.subscale > 1 ? c.future_horizon : -1; }
 
 wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w) {

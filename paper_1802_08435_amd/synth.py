@@ -108,7 +108,7 @@ PRESETS = {
     "multi4": (896, COND_DIM, 1, 0, None, True, 4, 24000),   # Sec. 2.1's batch-4 point
     "subscale16_h4": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
 }
-# Subscale presets in the paper's order with a future horizon (Sec. 4.1):
+# Subscale presets in the paper's order with a future horizon (Sec. 4.2):
 # lane s starts F + 1 steps after lane s - 1 (24,000 samples: 1,500 + 15 x 5
 # steps); the others run lockstep rows.
 HORIZON = {"subscale16_h4": 4}

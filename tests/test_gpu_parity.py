@@ -297,7 +297,7 @@ def test_subscale16_dense896_teacher_forced_within_bf16_tolerance():
 
 @pytest.mark.parametrize("H,B,S,F", [(256, 8, 2, 1), (128, 16, 1, 2), (256, 4, 2, 0), (128, 16, 3, 1)])
 def test_subscale_horizon_teacher_forced_small_sizes(H, B, S, F):
-    """Subscale in the paper's order with future horizon F (Sec. 4.1): lane s
+    """Subscale in the paper's order with future horizon F (Sec. 4.2): lane s
     runs position i at step i + s (F + 1) and its context holds samples of
     earlier sub-tensors up to position i + F (3 utterances of 16 lanes make
     groups of 8 vectors).  Logits of every sample against the oracle, which

@@ -395,7 +395,7 @@ def _pairs(seq, idx):
 
 
 @pytest.mark.parametrize("B,F,Dx,s,i,idx", [
-    # Sec. 4.1 by hand: sample 4i + s sees sub-tensors z < s up to position i + F and
+    # Sec. 4.2 by hand: sample 4i + s sees sub-tensors z < s up to position i + F and
     # its own sub-tensor before i; the window is Dx/4 samples before n, then Dx/4 after.
     (4, 1, 8, 2, 1, [5, 4, None, 8]),            # n = 6: 5 (z1), 4 (z0); 7 is z3 > s; 8 = (k2, z0), k <= 2
     (4, 1, 8, 0, 2, [None, None, None, None]),   # n = 8: sub-tensor 0 sees no other sub-tensor
@@ -427,7 +427,7 @@ def test_subscale_horizon_without_context_is_interleaved_plain_streams():
 @pytest.mark.parametrize("F", [0, 1, 3])
 def test_subscale_horizon_dependencies_precede_in_the_lagged_schedule(F):
     """Brute force on a tiny model: change one target sample q = B k + z and see
-    which teacher-forced logits move.  Under the batched schedule of Sec. 4.1
+    which teacher-forced logits move.  Under the batched schedule of Sec. 4.2
     sub-tensor s runs position i at step i + s (F + 1); every sample a logit
     depends on must be made at an earlier step, and some sample of an earlier
     sub-tensor from the logit's future (within F, so only for F > 0: with F = 0
