@@ -42,10 +42,12 @@
  *       F < 0, lockstep rows: all B lanes make row i together; the context of
  *         n is the Dx/2 samples before n, zero for those of row i or later;
  *       F >= 0, the paper's order with future horizon F (Sec. 4.2): sub-tensor
- *         s is generated after sub-tensors 0 .. s-1, and sample B*i + s sees
- *         sub-tensors z < s up to position i + F and its own sub-tensor
- *         before position i (no distant dependencies); its context is the
- *         Dx/4 samples before n and the Dx/4 after n, zero where not seen.
+ *         s is generated after sub-tensors 0 .. s-1; the context of sample
+ *         B*i + s holds the samples of the previous sub-tensors z < s up to
+ *         position i + F (Sec. 4.1: the conditioning sees the previous
+ *         sub-tensors; its own sub-tensor reaches the sample through the
+ *         recurrent state and inputs; no distant dependencies, Sec. 4.3), as
+ *         the Dx/4 samples before n and the Dx/4 after n, zero where not seen.
  *         Generated here sub-tensor by sub-tensor, in the paper's order.
  *
  * Build: cc -O2 -ffp-contract=off -fPIC -shared (no fast-math; fmaf only where written).
@@ -234,12 +236,12 @@ static void head(const orc_model* m, const float* Oa, const float* ba, const flo
   for (int v = 0; v < ORC_MAX_CLASSES; ++v) z[v] = dot(Ob + (size_t)v * Hh, hid, Hh) + bb[v];
 }
 
-/* Whether sample q = B*k + z of an utterance of N samples is seen by sample
- * B*i + s under the future-horizon rule. */
+/* Whether sample q = B*k + z of an utterance of N samples is in the context
+ * of sample B*i + s under the future-horizon rule. */
 static int seen_lagged(int B, int F, int64_t N, int32_t s, int64_t i, int64_t q) {
   if (q < 0 || q >= N) return 0;
   const int64_t k = q / B, z = q % B;
-  return (z < s && k <= i + F) || (z == s && k < i);
+  return z < s && k <= i + F;
 }
 
 void orc_subscale_context(const orc_model* m, const uint16_t* seq, int64_t N, int32_t s, int64_t i, float* ctx) {

@@ -48,9 +48,9 @@ MUTANTS = {
     "nll_fine_term_dropped": ("neg_log_prob(zc, ORC_MAX_CLASSES, c) + neg_log_prob(zf, ORC_MAX_CLASSES, f)",
                               "neg_log_prob(zc, ORC_MAX_CLASSES, c)"),
     "subscale_no_row_mask": ("seen = q >= 0 && q < (int64_t)B * i;", "seen = q >= 0 && q < n;"),
-    "subscale_horizon_plus_one": ("(z < s && k <= i + F)", "(z < s && k <= i + F + 1)"),
-    "subscale_sees_own_future": ("(z < s && k <= i + F)", "(z <= s && k <= i + F)"),
-    "subscale_own_past_dropped": ("(z == s && k < i)", "(z == s && k < i - 1)"),
+    "subscale_horizon_plus_one": ("return z < s && k <= i + F;", "return z < s && k <= i + F + 1;"),
+    "subscale_sees_own_sub_tensor": ("return z < s && k <= i + F;", "return z <= s && k <= i + F;"),
+    "subscale_sees_own_past": ("return z < s && k <= i + F;", "return (z < s && k <= i + F) || (z == s && k < i);"),
     "subscale_window_includes_n": ("n + 1 + (j - P / 2)", "n + (j - P / 2)"),
     "subscale_lane_order": ("const int64_t n = (B == 1) ? t0 + i : B * i + lane;",
                             "const int64_t n = (B == 1) ? t0 + i : rows * lane + i;"),

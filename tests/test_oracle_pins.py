@@ -395,8 +395,8 @@ def _pairs(seq, idx):
 
 
 @pytest.mark.parametrize("B,F,Dx,s,i,idx", [
-    # Sec. 4.2 by hand: sample 4i + s sees sub-tensors z < s up to position i + F and
-    # its own sub-tensor before i; the window is Dx/4 samples before n, then Dx/4 after.
+    # Sec. 4.1-4.2 by hand: the context of sample 4i + s holds the previous sub-tensors
+    # z < s up to position i + F; the window is Dx/4 samples before n, then Dx/4 after.
     (4, 1, 8, 2, 1, [5, 4, None, 8]),            # n = 6: 5 (z1), 4 (z0); 7 is z3 > s; 8 = (k2, z0), k <= 2
     (4, 1, 8, 0, 2, [None, None, None, None]),   # n = 8: sub-tensor 0 sees no other sub-tensor
     (4, 1, 8, 3, 1, [6, 5, 8, 9]),               # n = 7: future 8, 9 of z0, z1 at k = 2 <= 2
@@ -404,7 +404,7 @@ def _pairs(seq, idx):
     (4, 0, 8, 3, 2, [10, 9, None, None]),        # F = 0: k = 3 > 2 is beyond the horizon
     (4, 1, 8, 1, 0, [0, None, None, None]),      # n = 1: q = -1 does not exist
     (4, 1, 8, 2, 3, [13, 12, None, None]),       # n = 14: 15 is z3; 16 is past the end (N = 16)
-    (4, 1, 16, 1, 2, [8, None, None, 5, None, None, 12, None]),   # n = 9: own past 5 (k1 < 2), own future 13 unseen
+    (4, 1, 16, 1, 2, [8, None, None, None, None, None, 12, None]),   # n = 9: own past 5 and own future 13 unseen
 ])
 def test_subscale_horizon_context_hand_cases(B, F, Dx, s, i, idx):
     w = _horizon_model(B, F, Dx)
@@ -428,11 +428,13 @@ def test_subscale_horizon_without_context_is_interleaved_plain_streams():
 def test_subscale_horizon_dependencies_precede_in_the_lagged_schedule(F):
     """Brute force on a tiny model: change one target sample q = B k + z and see
     which teacher-forced logits move.  Under the batched schedule of Sec. 4.2
-    sub-tensor s runs position i at step i + s (F + 1); every sample a logit
-    depends on must be made at an earlier step, and some sample of an earlier
-    sub-tensor from the logit's future (within F, so only for F > 0: with F = 0
-    every sample an earlier sub-tensor has made up to position i precedes
-    B i + s in time) must matter."""
+    sub-tensor s runs position i at step i + s (F + 1 + A), with the context
+    formed A >= 0 steps ahead: every sample of its own sub-tensor a logit
+    depends on is made at an earlier step, every sample of another sub-tensor
+    at least A + 1 steps earlier, for A = 0 and A = 1, and some sample of an
+    earlier sub-tensor from the logit's future (within F, so only for F > 0:
+    with F = 0 every sample an earlier sub-tensor has made up to position i
+    precedes B i + s in time) must matter."""
     B, N, H, Dx = 4, 48, 8, 16
     d = _random_tiny(H=H)
     rng = np.random.default_rng(5)
@@ -440,7 +442,7 @@ def test_subscale_horizon_dependencies_precede_in_the_lagged_schedule(F):
     w = W(dict(d, B=B, F=F, Wx=Wx))
     tgt = rng.integers(0, 65536, size=(1, N)).astype(np.uint16)
     base = O.run(w, 1, N, target=tgt, logits=True)
-    step = lambda n: n // B + (n % B) * (F + 1)
+    step = lambda n, A: n // B + (n % B) * (F + 1 + A)
     future_dep = False
     for q in range(N):
         t2 = tgt.copy()
@@ -450,7 +452,9 @@ def test_subscale_horizon_dependencies_precede_in_the_lagged_schedule(F):
         for n in np.flatnonzero(moved):
             if n == q:
                 continue            # its own fine logits see its own coarse byte
-            assert step(q) < step(n), (q, n)
+            for A in (0, 1):
+                gap = 1 if q % B == n % B else A + 1
+                assert step(q, A) <= step(n, A) - gap, (q, n, A)
             future_dep |= q > n
     assert future_dep == (F > 0)
 
