@@ -204,8 +204,8 @@ def main() -> int:
     ms = float(np.mean(call_ms))
     samples = S * T
     value = samples * args.steps / wall
-    F = w.get("F", -1)                                 # subscale future horizon: (B - 1)(F + 1) more steps
-    steps_per_launch = T // w["B"] + ((w["B"] - 1) * (F + 1) if F >= 0 else 0)
+    F, A = w.get("F", -1), w.get("A", 0)               # subscale horizon and lead: (B - 1)(F + 1 + A) more steps
+    steps_per_launch = T // w["B"] + ((w["B"] - 1) * (F + 1 + A) if F >= 0 else 0)
     us_per_sample_step = ms * 1000.0 / steps_per_launch
     wb = weight_bytes_per_step(w)
     achieved = wb * steps_per_launch / (ms / 1000.0) / 1e9

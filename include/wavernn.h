@@ -67,10 +67,16 @@ typedef struct {
                             make row i together, each seeing the Dx/2 samples before its own of
                             earlier rows); F >= 0 = the paper's order with future horizon F
                             (Sec. 4.2): sample B*i + s sees sub-tensors z < s up to position i + F
-                            and its own sub-tensor before i, its context the Dx/4 samples before
+                            (its own sub-tensor through the state only), its context the Dx/4 samples before
                             and Dx/4 after it (unseen ones zero); lane s runs position i at step
-                            i + s(F + 1), so a call takes n_samples/B + (B - 1)(F + 1) steps.
-                            0 is a valid horizon: set -1 for lockstep. */
+                            i + s(F + 1 + A), so a call takes n_samples/B + (B - 1)(F + 1 + A)
+                            steps.  0 is a valid horizon: set -1 for lockstep. */
+  int32_t context_lead;   /* A in [0, 3], only with a future horizon (must be 0 otherwise; ignored
+                            when B = 1): each sub-tensor starts A steps later than the horizon
+                            alone requires, so that the samples its context needs were drawn A
+                            steps before the step that uses them and the context is formed off
+                            the step's critical chain (Sec. 4.2: the conditioning runs ahead of
+                            the lane it feeds).  The samples drawn do not depend on A. */
 } wavernn_config;
 
 /* Host fp32 weights.  Shapes (H hidden, Hh = H/2, V = 256 classes):

@@ -78,8 +78,9 @@ struct BatchArgs {
   int frame_len;
   int S;                    // vectors in use (the last group may be partly idle)
   int B;                    // subscale factor: vector v is lane v % B of utterance v / B (1: plain)
-  int F;                    // subscale future horizon (Sec. 4.2): lane s runs position t - s (F + 1)
+  int F;                    // subscale future horizon (Sec. 4.2): lane s runs position t - s (F + 1 + A)
                             // at step t; < 0: lockstep rows (position t)
+  int A;                    // steps by which the units form a horizon context ahead (0: at the step before)
   int64_t rows;             // positions per lane (samples per utterance / B)
   int64_t T, t0;            // steps (rows, plus (B - 1)(F + 1) with a horizon) and first absolute step
   uint64_t seed;

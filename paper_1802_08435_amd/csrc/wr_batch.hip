@@ -28,7 +28,7 @@ namespace {
 template <bool LAG>
 __device__ __forceinline__ int64_t vpos(const BatchArgs& a, int v, int64_t t) {
   if (!LAG) return t;
-  return t - (int64_t)(v % a.B) * (a.F + 1);
+  return t - (int64_t)(v % a.B) * (a.F + 1 + a.A);
 }
 // Index of sample B p + s in the [U][B rows] output / target arrays: obase(v) + B p.
 __device__ __forceinline__ size_t obase(const BatchArgs& a, int v) {
@@ -131,15 +131,18 @@ __device__ __forceinline__ bool poll_put2(const xw* base, O off, F put, uint32_t
 
 // Drawn samples for the subscale context cross groups, whose heads and units
 // are not chained step by step to each other: a sample word carries the
-// sample (16 bits) and the low 16 bits of its tag, in one of two slots chosen
-// by the tag's parity, so a producer one step ahead writes the other slot.
-__device__ __forceinline__ void spub(xw* slots, int L, int v, uint32_t tag, int sample) {
-  __hip_atomic_store(slots + (tag & 1u) * L + v, (tag & 0xffffu) << 16 | (uint32_t)sample, __ATOMIC_RELAXED,
+// sample (16 bits) and the low 16 bits of its tag, in one of SS slots chosen
+// by the tag modulo SS.  A head writing the samples of step s has seen the
+// gates of every group's units for step s, which had waited for every
+// group's samples of step s - 1 - A, so no reader still waits for samples
+// older than step s - 1 - 2 A: SS >= 2 A + 2 slots keep the writer off them.
+__device__ __forceinline__ void spub(xw* slots, int L, int SS, int v, uint32_t tag, int sample) {
+  __hip_atomic_store(slots + (tag & (SS - 1)) * L + v, (tag & 0xffffu) << 16 | (uint32_t)sample, __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ bool wait_sample(const xw* slots, int L, int v, uint32_t tag, int* sample,
+__device__ __forceinline__ bool wait_sample(const xw* slots, int L, int SS, int v, uint32_t tag, int* sample,
                                             const BatchArgs& a) {
-  const xw* p = slots + (tag & 1u) * L + v;
+  const xw* p = slots + (tag & (SS - 1)) * L + v;
   WaitBudget wb{wr_clock(), 0};
   for (;;) {
     const xw w = xpeek(p);
@@ -231,7 +234,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
     misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
     misc[8 + tid] = misc[16 + tid];
-    misc[48 + tid] = LAG ? ((v0 + tid) % a.B) * (a.F + 1) : 0;   // position of vector tid: t - misc[48 + tid]
+    misc[48 + tid] = LAG ? ((v0 + tid) % a.B) * (a.F + 1 + a.A) : 0;   // position of vector tid: t - misc[48 + tid]
   }
   xw* X = a.xc + (size_t)g * P.x_words;
   const xw* GA = X + P.x_ga;
@@ -589,7 +592,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
           else fw = misc[24 + bw];
         }
         if (!ALL) xpub(CF + bw, tag, (float)fw);
-        if (a.ux && writer && act) spub(X + P.x_sp, L, bw, tag, 256 * c + f);   // for later contexts
+        if (a.ux && writer && act) spub(X + P.x_sp, L, P.SS, bw, tag, 256 * c + f);   // for later contexts
         if (live && act) {
           if (a.out) a.out[ob + (size_t)a.B * pw] = (uint16_t)(256 * c + f);
           if (a.nll_out)
@@ -711,30 +714,39 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   };
   f32x4 xa0 = {0, 0, 0, 0}, xa1 = {0, 0, 0, 0};        // context term of e-gate rows
   xw* dstx = X + (fw ? P.x_xf : P.x_xc) + (size_t)i * L + bl0;
+  // With the context formed ahead (A > 0) it is built at the start of a
+  // step, before h arrives, into its own sums for every row.
+  const bool ahead = CTX && LAG && a.A > 0;
   auto publish = [&](uint32_t tag, float cb0, float cb1) {
     if (bl0 >= L) return;                               // rows of vectors past L: zero inputs, not published
+    if (ahead && gt < 2) {
+      cb0 += mfma_row(xa0) + mfma_row(xa1);
+      cb1 += mfma_row_hi(xa0) + mfma_row_hi(xa1);
+    }
     xpub2(dst, tag, (mfma_row(acc0) + mfma_row(acc1)) + cb0, (mfma_row_hi(acc0) + mfma_row_hi(acc1)) + cb1);
     if (CTX && gt == 2) xpub2(dstx, tag, mfma_row(xa0) + mfma_row(xa1), mfma_row_hi(xa0) + mfma_row_hi(xa1));
   };
-  // Subscale context (Sec. 4): the samples drawn at step t by the lanes of
-  // every utterance of this group join the ring; vector b's context for step
-  // t + 1 is Dx/2 samples as (c, f) scaled: lockstep, the ones before its own
-  // sample, zero for samples of row t + 1 or before the start; with horizon F
-  // (Sec. 4.2) Dx/4 before and Dx/4 after its own, zero unless an earlier
-  // sub-tensor made it at a position up to p + F or its own sub-tensor before
-  // p (every such sample was drawn at step t or before).  Its projection
-  // joins the sums of the u and r rows; for e rows it is kept apart
-  // (published on its own: it is not reset-gated).
+  // Subscale context (Sec. 4): the samples drawn at step t - A by the lanes
+  // of every utterance of this group join the ring; vector b's context for
+  // step t + 1 is Dx/2 samples as (c, f) scaled: lockstep, the ones before
+  // its own sample, zero for samples of row t + 1 or before the start; with
+  // horizon F (Sec. 4.2) Dx/4 before and Dx/4 after its own, zero unless an
+  // earlier sub-tensor made it at a position up to p + F.  Sub-tensor z runs
+  // position p + F at step p + F + z (F + 1 + A), at most t - A for z < s,
+  // so the ring holds every such sample.  Its projection joins the sums of
+  // the u and r rows; for e rows it is kept apart (published on its own: it
+  // is not reset-gated).
   const int ub0 = v0 / a.B;                            // first utterance of this group
   const int nut = a.B >= L ? 1 : L / a.B;              // utterances of this group
   auto context = [&](int64_t t) {
-    const uint32_t tag = (uint32_t)(t + 1);
-    if (tid < nut * a.B) {                             // one thread per (utterance, lane)
+    const int64_t td = t - (LAG ? a.A : 0);            // the step whose samples join the ring now
+    const uint32_t tag = (uint32_t)(td + 1);
+    if (tid < nut * a.B && td >= 0) {                  // one thread per (utterance, lane)
       const int vv = ub0 * a.B + tid;                  // vector of that lane
       int y = 0;
-      const int64_t p = vpos<LAG>(a, vv, t);                // lanes idle at step t drew nothing
+      const int64_t p = vpos<LAG>(a, vv, td);          // lanes idle at step td drew nothing
       if (vv < a.S && p >= 0 && p < a.rows) {
-        if (!wait_sample(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp, L, vv % L, tag, &y, a)) misc[0] = 1;
+        if (!wait_sample(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp, L, P.SS, vv % L, tag, &y, a)) misc[0] = 1;
         const int64_t qn = (int64_t)a.B * p + tid % a.B;
         hist[(tid / a.B) * HC + (int)(qn & HCm)] = y;
       }
@@ -758,8 +770,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
         // q = B (p1 + dk) + z with 0 <= z < B: small integers only
         const int sd = s + d + 2 * half * a.B;         // > 0
         const int dk = sd / a.B - 2 * half, z = sd % a.B;
-        seen = p1 >= 0 && p1 < a.rows && qn >= 0 && qn < (int64_t)a.B * a.rows &&
-               ((z < s && dk <= a.F) || (z == s && dk < 0));
+        seen = p1 >= 0 && p1 < a.rows && qn >= 0 && qn < (int64_t)a.B * a.rows && z < s && dk <= a.F;
       }
       float c = 0.0f, f = 0.0f;
       if (seen) {
@@ -771,13 +782,14 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       aput(cimg + ((2 * jj + 1) >> 5) * WR_FRAG, (2 * jj + 1) & 31, f, b);
     }
     __syncthreads();
-    f32x4 c0 = gt == 2 ? f32x4{0, 0, 0, 0} : acc0, c1 = gt == 2 ? f32x4{0, 0, 0, 0} : acc1;
+    const bool apart = gt == 2 || ahead;               // kept apart from the products of h
+    f32x4 c0 = apart ? f32x4{0, 0, 0, 0} : acc0, c1 = apart ? f32x4{0, 0, 0, 0} : acc1;
 #pragma unroll
     for (int x = 0; x < (CTX ? 8 : 0); x += 2) {
       if (x < P.KX) c0 = mfma(afrag(cimg, x), WX[x], c0);
       if (x + 1 < P.KX) c1 = mfma(afrag(cimg, x + 1), WX[x + 1], c1);
     }
-    if (gt == 2) {
+    if (apart) {
       xa0 = c0;
       xa1 = c1;
     } else {
@@ -846,6 +858,10 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     const float cb0 = cbv(bl0, t + 1), cb1 = cbv(bl0 + 1, t + 1);
     const bool tr = g == 0 && k == 0 && tid == 0;
     if (tr) trace_at(a, t, 16);
+    if (ahead) {
+      context(t);
+      if (misc[0]) return;
+    }
     gather_half(YC, tag, 0);
     if (misc[0]) return;
     if (tr) trace_at(a, t, 17);
@@ -855,7 +871,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     if (misc[0]) return;
     if (tr) trace_at(a, t, 19);
     phase_f();
-    if (CTX) {
+    if (CTX && !ahead) {
       context(t);
       if (misc[0]) return;
     }

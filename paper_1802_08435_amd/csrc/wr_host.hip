@@ -133,6 +133,8 @@ struct Rounder {
 
 // Future horizon of a subscale model (Sec. 4.2), -1 for lockstep rows or B = 1.
 static int horizon_of(const wavernn_config& c) { return c.subscale > 1 ? c.future_horizon : -1; }
+// Steps by which the units form a horizon context ahead of its use (0 without a horizon).
+static int lead_of(const wavernn_config& c) { return horizon_of(c) >= 0 ? c.context_lead : 0; }
 
 wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w) {
   if (!c || !w) return fail(WAVERNN_E_INVALID, "null config or weights");
@@ -148,6 +150,9 @@ wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w
     return fail(WAVERNN_E_INVALID, "future_horizon %d out of [-1, 1024]", c->future_horizon);
   if (c->subscale > 1 && c->future_horizon >= 0 && c->ctx_dim % 4)
     return fail(WAVERNN_E_INVALID, "ctx_dim must be a multiple of 4 with a future horizon");
+  if (c->subscale > 1 && (c->context_lead < 0 || c->context_lead > 3 || (c->future_horizon < 0 && c->context_lead)))
+    return fail(WAVERNN_E_INVALID, "context_lead %d: must be in [0, 3], and 0 without a future horizon",
+                c->context_lead);
   if (c->weight_dtype != WAVERNN_F32 && c->weight_dtype != WAVERNN_BF16) return fail(WAVERNN_E_INVALID, "bad weight_dtype");
   if (c->r_format < WAVERNN_R_DENSE || c->r_format > WAVERNN_R_BSR_16X1) return fail(WAVERNN_E_INVALID, "bad r_format");
   if (c->max_streams < 1 || c->max_streams > 64) return fail(WAVERNN_E_INVALID, "max_streams must be in [1, 64]");
@@ -510,7 +515,7 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   size_t xwords = 0;
   for (int v : {std::min(maxv, 2 * WR_BL), std::min(maxv, 4 * WR_BL), maxv}) {
     BatchPlan Q;
-    if (!batch_plan(H, v, &Q, m->cfg.ctx_dim, m->cfg.subscale, horizon_of(m->cfg)))
+    if (!batch_plan(H, v, &Q, m->cfg.ctx_dim, m->cfg.subscale, horizon_of(m->cfg), lead_of(m->cfg)))
       return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors (future horizon %d: sample ring of the "
                   "units too large for LDS?)", v, horizon_of(m->cfg));
     const void* k = wr_batch_kernel_ptr(Q.KH, Q.KX > 0, Q.L, horizon_of(m->cfg) >= 0);
@@ -729,8 +734,8 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   const int SB = m->cfg.subscale;                 // lanes per utterance
   const int V = io.S * SB;                        // vectors
   BatchPlan B;
-  const int F = horizon_of(m->cfg);
-  if (!batch_plan(m->cfg.hidden, V, &B, m->cfg.ctx_dim, SB, F))
+  const int F = horizon_of(m->cfg), A = lead_of(m->cfg);
+  if (!batch_plan(m->cfg.hidden, V, &B, m->cfg.ctx_dim, SB, F, A))
     return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors", V);
   const int H = B.H, Dc = m->cfg.cond_dim;
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
@@ -767,8 +772,9 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.S = V;
   a.B = SB;
   a.F = F;
+  a.A = A;
   a.rows = io.T / SB;
-  a.T = a.rows + (F >= 0 ? (int64_t)(SB - 1) * (F + 1) : 0);   // steps: the last lane starts (B - 1)(F + 1) late
+  a.T = a.rows + (F >= 0 ? (int64_t)(SB - 1) * (F + 1 + A) : 0);   // the last lane starts (B - 1)(F + 1 + A) late
   a.t0 = io.init ? io.init->t0 : 0;
   a.seed = io.seed;
   a.target = io.target;
@@ -834,7 +840,7 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
     else if (cfg->weight_dtype != WAVERNN_BF16)
       s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling needs bf16 weights");
     else if (!persist_plan(H, &m->plan) ||
-             !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim, B, horizon_of(*cfg)))
+             !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim, B, horizon_of(*cfg), lead_of(*cfg)))
       s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d with %d x %d lanes: no batched plan", H, cfg->max_streams, B);
     else {
       m->path = PATH_BATCHED;
@@ -928,7 +934,7 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
     g = n_streams > 0 ? n_streams : 1, b = 256;
   } else if (m->path == PATH_BATCHED &&
              batch_plan(m->cfg.hidden, (n_streams > 0 ? n_streams : 1) * m->cfg.subscale, &B, m->cfg.ctx_dim,
-                        m->cfg.subscale, horizon_of(m->cfg))) {
+                        m->cfg.subscale, horizon_of(m->cfg), lead_of(m->cfg))) {
     g = B.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST && n_streams > 1 && n_streams <= m->nfan) {
     path = PATH_CONCURRENT_ID, g = m->plan.grid, b = WR_THREADS;

@@ -245,6 +245,7 @@ struct BatchPlan {
   int KX;                 // subscale context column tiles (Dx / 32), 0 without context
   int HC;                 // drawn samples a unit keeps per utterance (ring, a power of two)
   int HS;                 // utterances whose samples a unit keeps (slots of HC)
+  int SS;                 // slots of the drawn-sample words (a power of two >= 2 A + 2)
   int lds_h, lds_u, lds;
 };
 
@@ -261,11 +262,13 @@ WR_HD inline int wr_batch_role(const BatchPlan& P, int b, int* g) {
   return P.NH + ku % P.NU;
 }
 
-// B, F: subscale factor and future horizon (F < 0: lockstep rows), which
-// size the ring of drawn samples a unit keeps for the context.
-WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0, int B = 1, int F = -1) {
+// B, F, A: subscale factor, future horizon (F < 0: lockstep rows) and the
+// steps A by which the units form the context ahead, which size the ring of
+// drawn samples a unit keeps and the slots of the sample words.
+WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0, int B = 1, int F = -1,
+                             int A = 0) {
   if (H <= 0 || H % 128 || n_vectors < 1 || n_vectors > 8 * WR_BL) return false;
-  if (ctx_dim < 0 || ctx_dim % 32 || ctx_dim > 256 || B < 1 || F > 1024) return false;
+  if (ctx_dim < 0 || ctx_dim % 32 || ctx_dim > 256 || B < 1 || F > 1024 || A < 0 || A > 3) return false;
   P->KX = ctx_dim / 32;
   P->H = H;
   P->Hh = H / 2;
@@ -290,7 +293,9 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   P->x_gf = take(P->L * 3 * P->Hh);
   P->x_pc = take(P->NH * P->L * 256);
   P->x_pf = take(P->NH * P->L * 256);
-  P->x_sp = take(2 * P->L);
+  P->SS = 2;
+  while (P->SS < 2 * A + 2) P->SS *= 2;
+  P->x_sp = take(P->SS * P->L);
   P->x_xc = take(P->L * P->Hh);
   P->x_xf = take(P->L * P->Hh);
   P->x_cc = take(P->L);
@@ -304,10 +309,10 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
                                                2 * P->L * 64 * 2 + 2 * P->L * 64);
   // Ring of drawn samples per utterance: lockstep, the Dx/2 samples before
   // a row plus the row; with horizon F the lanes of an utterance are up to
-  // (B - 1)(F + 1) positions apart, so the newest sample and the oldest one a
-  // context still reads are at most B (B - 1)(F + 1) + Dx/4 apart.
+  // (B - 1)(F + 1 + A) positions apart, so the newest sample and the oldest
+  // one a context still reads are at most B (B - 1)(F + 1 + A) + Dx/4 apart.
   {
-    const int need = F < 0 ? ctx_dim / 2 + 2 * B : B * (B - 1) * (F + 1) + ctx_dim / 2 + B;
+    const int need = F < 0 ? ctx_dim / 2 + 2 * B : B * (B - 1) * (F + 1 + A) + ctx_dim / 2 + B;
     P->HC = 256;
     while (P->HC < need) P->HC *= 2;
     P->HS = (ctx_dim > 0 && P->L > B) ? P->L / B : 1;

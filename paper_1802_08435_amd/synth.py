@@ -107,11 +107,14 @@ PRESETS = {
     "multi64": (896, COND_DIM, 1, 0, None, True, 64, 48000),
     "multi4": (896, COND_DIM, 1, 0, None, True, 4, 24000),   # Sec. 2.1's batch-4 point
     "subscale16_h4": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
+    "subscale16_h4a1": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
 }
 # Subscale presets in the paper's order with a future horizon (Sec. 4.2):
-# lane s starts F + 1 steps after lane s - 1 (24,000 samples: 1,500 + 15 x 5
-# steps); the others run lockstep rows.
-HORIZON = {"subscale16_h4": 4}
+# lane s starts F + 1 + A steps after lane s - 1 (24,000 samples with F = 4:
+# 1,500 + 15 x (5 + A) steps), A the steps by which its context is formed
+# ahead; the others run lockstep rows.
+HORIZON = {"subscale16_h4": 4, "subscale16_h4a1": 4}
+LEAD = {"subscale16_h4a1": 1}
 
 
 def preset(name: str, seed: int = 0) -> dict:
@@ -121,4 +124,5 @@ def preset(name: str, seed: int = 0) -> dict:
     w.update(name=name, bf16=bf16, streams=S, samples=T)
     if name in HORIZON:
         w["F"] = HORIZON[name]
+        w["A"] = LEAD.get(name, 0)
     return w

@@ -29,7 +29,8 @@ class WaveRNNError(RuntimeError):
 
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("hidden", "cond_dim", "frame_len", "subscale", "ctx_dim",
-                                               "weight_dtype", "r_format", "max_streams", "future_horizon")]
+                                               "weight_dtype", "r_format", "max_streams", "future_horizon",
+                                               "context_lead")]
 
 
 _FP = ctypes.POINTER(ctypes.c_float)
@@ -103,7 +104,8 @@ class Model:
 
     ``w`` is a dict of fp32 arrays (keys of ``include/wavernn.h``'s weights:
     R, I, b, O1, b1, O2, b2, O3, b3, O4, b4, optional Wc, Wx, mask) plus H,
-    frame_len, B and, for subscale, F (future horizon; -1 or absent: lockstep rows).  dtype 'bf16' or 'f32' is the weight storage; r_format is
+    frame_len, B and, for subscale, F (future horizon; -1 or absent: lockstep rows) and A (steps by which
+    the context is formed ahead, with F only; absent: 0).  dtype 'bf16' or 'f32' is the weight storage; r_format is
     'dense', 'bsr4x4' or 'bsr16x1'."""
 
     def __init__(self, w: dict, dtype: str = "bf16", r_format: str = "dense", max_streams: int = 1):
@@ -114,10 +116,11 @@ class Model:
         self.frame_len = int(w.get("frame_len", 120))
         self.B = int(w.get("B", 1))
         self.F = int(w.get("F", -1))
+        self.A = int(w.get("A", 0))
         cfg = Config(self.H, self.cond_dim, self.frame_len, self.B, 0 if Wx is None else Wx.shape[1],
                      {"bf16": BF16, "f32": F32}[dtype],
                      {"dense": R_DENSE, "bsr4x4": R_BSR_4X4, "bsr16x1": R_BSR_16X1}[r_format], max_streams,
-                     self.F)
+                     self.F, self.A)
         keep = {k: _f32(w[k]) for k in ("R", "I", "b", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")}
         mask = None if w.get("mask") is None else np.ascontiguousarray(w["mask"], dtype=np.uint8)
         fp = lambda a: None if a is None else a.ctypes.data_as(_FP)

@@ -92,7 +92,7 @@ def test_full_length_call_matches_the_oracle_at_sampled_positions(name, fmt, pos
             assert okc.all() and okf.all(), (name, p, s_, np.flatnonzero(~okc)[:5], np.flatnonzero(~okf)[:5])
 
 
-@pytest.mark.parametrize("name", ["subscale16", "subscale16_h4"])
+@pytest.mark.parametrize("name", ["subscale16", "subscale16_h4", "subscale16_h4a1"])
 def test_full_length_subscale_call_prefix_and_state(name):
     w = synth.preset(name)
     T, B = w["samples"], w["B"]

@@ -295,15 +295,18 @@ def test_subscale16_dense896_teacher_forced_within_bf16_tolerance():
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
 
 
-@pytest.mark.parametrize("H,B,S,F", [(256, 8, 2, 1), (128, 16, 1, 2), (256, 4, 2, 0), (128, 16, 3, 1)])
-def test_subscale_horizon_teacher_forced_small_sizes(H, B, S, F):
+@pytest.mark.parametrize("H,B,S,F,A", [(256, 8, 2, 1, 0), (128, 16, 1, 2, 0), (256, 4, 2, 0, 0),
+                                       (128, 16, 3, 1, 0), (256, 8, 2, 1, 1), (128, 16, 1, 2, 2),
+                                       (256, 4, 2, 0, 3), (128, 16, 3, 1, 1)])
+def test_subscale_horizon_teacher_forced_small_sizes(H, B, S, F, A):
     """Subscale in the paper's order with future horizon F (Sec. 4.2): lane s
-    runs position i at step i + s (F + 1) and its context holds samples of
-    earlier sub-tensors up to position i + F (3 utterances of 16 lanes make
-    groups of 8 vectors).  Logits of every sample against the oracle, which
-    generates sub-tensor by sub-tensor."""
+    runs position i at step i + s (F + 1 + A) and its context holds samples
+    of earlier sub-tensors up to position i + F, formed A steps ahead (3
+    utterances of 16 lanes make groups of 8 vectors).  Logits of every
+    sample against the oracle, which generates sub-tensor by sub-tensor and
+    knows no A: the schedule must not change what is computed."""
     w = synth.make_weights(H, seed=6, cond_dim=16, B=B, ctx_dim=256)
-    w["F"] = F
+    w["F"], w["A"] = F, A
     T = 40 * B
     feat = synth.features(S, T, cond_dim=16, per_stream_seed=True)
     tgt = _targets(S, T)
@@ -318,8 +321,9 @@ def test_subscale_horizon_teacher_forced_small_sizes(H, B, S, F):
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
 
 
-def test_subscale16_horizon_dense896_teacher_forced_within_bf16_tolerance():
-    w = synth.preset("subscale16_h4")
+@pytest.mark.parametrize("name", ["subscale16_h4", "subscale16_h4a1"])
+def test_subscale16_horizon_dense896_teacher_forced_within_bf16_tolerance(name):
+    w = synth.preset(name)
     T = 960
     feat = synth.features(1, T)
     tgt = _targets(1, T)
@@ -332,14 +336,15 @@ def test_subscale16_horizon_dense896_teacher_forced_within_bf16_tolerance():
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
 
 
-def test_subscale_horizon_free_running_draws_valid_and_final_state():
-    """Free-running with horizon F = 2: every lane's draw is valid under the
-    oracle's logits on the GPU trajectory with the lane's Philox stream
-    indexed by position, and the final state is each lane's after its last
-    position."""
+@pytest.mark.parametrize("A", [0, 1])
+def test_subscale_horizon_free_running_draws_valid_and_final_state(A):
+    """Free-running with horizon F = 2 (context formed A steps ahead): every
+    lane's draw is valid under the oracle's logits on the GPU trajectory with
+    the lane's Philox stream indexed by position, and the final state is each
+    lane's after its last position."""
     B, T, F = 8, 480, 2
     w = synth.make_weights(256, seed=7, cond_dim=16, B=B, ctx_dim=256)
-    w["F"] = F
+    w["F"], w["A"] = F, A
     feat = synth.features(1, T, cond_dim=16)
     m = wavernn.Model(w, dtype="bf16")
     fin = m.new_state()
@@ -540,7 +545,7 @@ def test_short_runs_match_the_oracle(kind, T):
         kw.update(B=B, ctx_dim=256)
     w = synth.make_weights(H, seed=12, **kw)
     if kind == "subscale-horizon":
-        w["F"] = 1
+        w["F"], w["A"] = 1, 1
     n = T * B
     feat = synth.features(S, n, cond_dim=16, per_stream_seed=True)
     tgt = _targets(S, n)

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def _cfg(**kw):
     d = dict(hidden=64, cond_dim=0, frame_len=120, subscale=1, ctx_dim=0, weight_dtype=W.F32,
-             r_format=W.R_DENSE, max_streams=1, future_horizon=-1)
+             r_format=W.R_DENSE, max_streams=1, future_horizon=-1, context_lead=0)
     d.update(kw)
     return W.Config(**d)
 
@@ -55,6 +55,8 @@ def _weights(H=64):
     (dict(cond_dim=8), "W_cond"), (dict(r_format=W.R_BSR_4X4), "R_block_mask"),
     (dict(subscale=16, ctx_dim=256, future_horizon=-2), "future_horizon"),
     (dict(subscale=16, ctx_dim=6, future_horizon=2), "multiple of 4"),
+    (dict(subscale=16, ctx_dim=256, future_horizon=2, context_lead=4), "context_lead"),
+    (dict(subscale=16, ctx_dim=256, future_horizon=-1, context_lead=1), "context_lead"),
 ])
 def test_create_rejects_bad_config_before_touching_the_device(bad, msg):
     L = W.lib()
