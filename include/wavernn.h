@@ -128,7 +128,8 @@ void wavernn_destroy(wavernn_model* m);
  *             may alias init.
  * Subscale (B > 1): n_samples must be a multiple of B; lane s of step i makes
  * sample B*i + s and out_dev is in time order.  Utterance k draws from Philox
- * stream k*B + lane.  Errors: E_INVALID, E_UNSUPPORTED, E_HIP. */
+ * stream k*B + lane.  n_samples = 0 is valid: nothing is launched and final
+ * is left as it was.  Errors: E_INVALID, E_UNSUPPORTED, E_HIP. */
 wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_samples, const float* cond_dev,
                               int64_t n_frames, uint64_t seed, const wavernn_state* init, uint16_t* out_dev,
                               const wavernn_state* final_state, void* stream);
@@ -137,7 +138,8 @@ wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_sam
  * runs on target_dev [n_streams][n_samples] instead of drawn samples.  Writes
  * the pre-softmax logits logits_c_dev / logits_f_dev [n_streams][n_samples][256]
  * and nll_dev [n_streams][n_samples] = -log P(c_t) - log P(f_t | c_t) in nats;
- * each output pointer may be NULL.  Initial state as in wavernn_sample. */
+ * each output pointer may be NULL.  Initial state as in wavernn_sample.
+ * n_samples = 0 is valid (target_dev may then be NULL): nothing is launched. */
 wavernn_status wavernn_score_teacher_forced(wavernn_model* m, int32_t n_streams, int64_t n_samples,
                                             const float* cond_dev, int64_t n_frames, const uint16_t* target_dev,
                                             const wavernn_state* init, float* logits_c_dev, float* logits_f_dev,

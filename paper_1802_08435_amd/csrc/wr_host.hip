@@ -898,7 +898,7 @@ wavernn_status wavernn_score_teacher_forced(wavernn_model* m, int32_t n_streams,
                                             const float* cond_dev, int64_t n_frames, const uint16_t* target_dev,
                                             const wavernn_state* init, float* logits_c_dev, float* logits_f_dev,
                                             float* nll_dev, void* stream) {
-  if (!target_dev) return fail(WAVERNN_E_INVALID, "target is null");
+  if (!target_dev && n_samples != 0) return fail(WAVERNN_E_INVALID, "target is null");
   RunIO io{n_streams, n_samples, cond_dev, n_frames, 0, init, nullptr, target_dev, nullptr,
            logits_c_dev, logits_f_dev, nll_dev, (hipStream_t)stream};
   return run(m, io);

@@ -409,6 +409,49 @@ def test_invalid_calls_return_errors_without_launching():
     assert host(m.sample(0)).shape == (1, 0)
 
 
+_EDGE_KINDS = {"single-workgroup": dict(H=64), "persistent": dict(H=256), "block-sparse": dict(H=256, block=(4, 4), density=0.1),
+               "batched": dict(H=256, S=5), "subscale": dict(H=256, B=4), "subscale-horizon": dict(H=256, B=4, F=1, A=1)}
+
+
+@pytest.mark.parametrize("kind", sorted(_EDGE_KINDS))
+def test_degenerate_calls_on_every_path(kind):
+    """Zero-length calls succeed, launch nothing and leave outputs and the
+    final state untouched; a subscale length that is not a multiple of B and
+    more utterances than the model was created for are rejected."""
+    e = dict(_EDGE_KINDS[kind])
+    H, S, B = e.pop("H"), e.pop("S", 1), e.pop("B", 1)
+    kw = dict(cond_dim=16)
+    if "block" in e:
+        kw.update(block=e.pop("block"), density=e.pop("density"))
+    if B > 1:
+        kw.update(B=B, ctx_dim=256)
+    w = synth.make_weights(H, seed=13, **kw)
+    w.update({k: v for k, v in e.items()})
+    m = wavernn.Model(w, dtype="f32" if kind == "single-workgroup" else "bf16", r_format="bsr4x4" if "block" in kw else "dense",
+                      max_streams=S)
+    assert m.path(S)[0] == {"subscale-horizon": "batched", "subscale": "batched"}.get(kind, kind)
+    feat = cuda(synth.features(S, 8 * B, cond_dim=16, per_stream_seed=True))
+    out = torch.full((S, 0), 7, dtype=torch.uint16, device="cuda")
+    fin = m.new_state(S)
+    fin["h"].fill_(0.25)
+    m.sample(0, cond=feat, n_streams=S, out=out, final=fin)
+    r = m.score(torch.empty(S, 0, dtype=torch.uint16, device="cuda"), cond=feat)
+    m.device_status()
+    assert host(r["zc"]).shape == (S, 0, 256) and host(r["nll"]).shape == (S, 0)
+    assert (host(fin["h"]) == 0.25).all() and (host(fin["c"]) == 128).all()
+    if B > 1:
+        with pytest.raises(wavernn.WaveRNNError) as err:
+            m.sample(B + 1, cond=feat, n_streams=S)
+        assert err.value.status == wavernn.E_INVALID
+    with pytest.raises(wavernn.WaveRNNError) as err:
+        m.sample(B, cond=cuda(synth.features(S + 1, 8 * B, cond_dim=16)), n_streams=S + 1)
+    assert err.value.status == wavernn.E_INVALID
+    # the model still samples after the rejected calls
+    o = host(m.sample(2 * B, cond=feat, n_streams=S, seed=4))
+    m.device_status()
+    assert o.shape == (S, 2 * B)
+
+
 # ------------------------------------------------------------- block-sparse R
 
 _FMT = {(4, 4): "bsr4x4", (16, 1): "bsr16x1"}
