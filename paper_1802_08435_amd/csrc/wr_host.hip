@@ -841,7 +841,9 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
       s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling needs bf16 weights");
     else if (!persist_plan(H, &m->plan) ||
              !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim, B, horizon_of(*cfg), lead_of(*cfg)))
-      s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d with %d x %d lanes: no batched plan", H, cfg->max_streams, B);
+      s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d with %d x %d lanes, future horizon %d, context lead %d: no batched "
+               "plan (the units' ring of B (B - 1)(F + 1 + A) + Dx/2 + B samples must fit LDS)", H, cfg->max_streams,
+               B, horizon_of(*cfg), lead_of(*cfg));
     else {
       m->path = PATH_BATCHED;
       s = build_persist(m, w);
