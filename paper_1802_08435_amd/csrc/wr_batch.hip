@@ -20,10 +20,11 @@ namespace {
 
 // Vector v is lane s = v % B of utterance v / B.  At step t it runs position
 // p = vpos(v, t) and makes sample n = B (t0 + p) + s of that utterance
-// (Sec. 4; B = 1: n = t0 + t): p = t for lockstep rows, p = t - s (F + 1)
+// (Sec. 4; B = 1: n = t0 + t): p = t for lockstep rows, p = t - s (F + 1 + A)
 // with future horizon F (Sec. 4.2: a sub-tensor starts F + 1 steps after the
-// one before it, so the lanes of one step are at different positions and a
-// lane idles before its first and after its last position).
+// one before it, A more when its context is formed A steps ahead, so the
+// lanes of one step are at different positions and a lane idles before its
+// first and after its last position).
 // (LAG: the kernel instantiated for a horizon schedule; lockstep kernels pay nothing for it.)
 template <bool LAG>
 __device__ __forceinline__ int64_t vpos(const BatchArgs& a, int v, int64_t t) {
@@ -132,10 +133,15 @@ __device__ __forceinline__ bool poll_put2(const xw* base, O off, F put, uint32_t
 // Drawn samples for the subscale context cross groups, whose heads and units
 // are not chained step by step to each other: a sample word carries the
 // sample (16 bits) and the low 16 bits of its tag, in one of SS slots chosen
-// by the tag modulo SS.  A head writing the samples of step s has seen the
-// gates of every group's units for step s, which had waited for every
-// group's samples of step s - 1 - A, so no reader still waits for samples
-// older than step s - 1 - 2 A: SS >= 2 A + 2 slots keep the writer off them.
+// by the tag modulo SS.  Every lane publishes a word at every step, idle
+// lanes included, and every unit waits for every lane's word of its
+// utterance(s), so a head writing the samples of step s has seen the gates
+// of its units for step s, which had waited for every lane's samples of step
+// s - 1 - A, whose heads had seen their units finish step s - 2 - A.  No
+// reader still waits for samples older than step s - 1 - 2 A, and SS >=
+// 2 A + 2 slots keep the writer off them.  (Were idle lanes skipped, nothing
+// would wait for a group whose lanes are all idle, and its units could fall
+// any number of steps behind.)
 __device__ __forceinline__ void spub(xw* slots, int L, int SS, int v, uint32_t tag, int sample) {
   __hip_atomic_store(slots + (tag & (SS - 1)) * L + v, (tag & 0xffffu) << 16 | (uint32_t)sample, __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_AGENT);
@@ -592,7 +598,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
           else fw = misc[24 + bw];
         }
         if (!ALL) xpub(CF + bw, tag, (float)fw);
-        if (a.ux && writer && act) spub(X + P.x_sp, L, P.SS, bw, tag, 256 * c + f);   // for later contexts
+        // for later contexts; an idle lane publishes a word too (value unused)
+        if (a.ux && writer) spub(X + P.x_sp, L, P.SS, bw, tag, act ? 256 * c + f : 0);
         if (live && act) {
           if (a.out) a.out[ob + (size_t)a.B * pw] = (uint16_t)(256 * c + f);
           if (a.nll_out)
@@ -745,10 +752,10 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       const int vv = ub0 * a.B + tid;                  // vector of that lane
       int y = 0;
       const int64_t p = vpos<LAG>(a, vv, td);          // lanes idle at step td drew nothing
-      if (vv < a.S && p >= 0 && p < a.rows) {
+      if (vv < a.S) {                                  // (but their words are waited for too)
         if (!wait_sample(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp, L, P.SS, vv % L, tag, &y, a)) misc[0] = 1;
         const int64_t qn = (int64_t)a.B * p + tid % a.B;
-        hist[(tid / a.B) * HC + (int)(qn & HCm)] = y;
+        if (p >= 0 && p < a.rows) hist[(tid / a.B) * HC + (int)(qn & HCm)] = y;
       }
     }
     __syncthreads();
