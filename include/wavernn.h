@@ -76,7 +76,8 @@ typedef struct {
                             alone requires, so that the samples its context needs were drawn A
                             steps before the step that uses them and the context is formed off
                             the step's critical chain (Sec. 4.2: the conditioning runs ahead of
-                            the lane it feeds).  The samples drawn do not depend on A. */
+                            the lane it feeds).  The samples drawn do not depend on A.
+                            Currently switched off: create returns E_UNSUPPORTED for A > 0. */
 } wavernn_config;
 
 /* Host fp32 weights.  Shapes (H hidden, Hh = H/2, V = 256 classes):

@@ -153,6 +153,9 @@ wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w
   if (c->subscale > 1 && (c->context_lead < 0 || c->context_lead > 3 || (c->future_horizon < 0 && c->context_lead)))
     return fail(WAVERNN_E_INVALID, "context_lead %d: must be in [0, 3], and 0 without a future horizon",
                 c->context_lead);
+  if (c->subscale > 1 && c->context_lead > 0)
+    return fail(WAVERNN_E_UNSUPPORTED, "context_lead %d: switched off (a traced launch had a bounded wait expire "
+                "with a lead of 1 and the cause is not found; the lead-0 schedule is unaffected)", c->context_lead);
   if (c->weight_dtype != WAVERNN_F32 && c->weight_dtype != WAVERNN_BF16) return fail(WAVERNN_E_INVALID, "bad weight_dtype");
   if (c->r_format < WAVERNN_R_DENSE || c->r_format > WAVERNN_R_BSR_16X1) return fail(WAVERNN_E_INVALID, "bad r_format");
   if (c->max_streams < 1 || c->max_streams > 64) return fail(WAVERNN_E_INVALID, "max_streams must be in [1, 64]");

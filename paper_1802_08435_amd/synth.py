@@ -114,7 +114,7 @@ PRESETS = {
 # 1,500 + 15 x (5 + A) steps), A the steps by which its context is formed
 # ahead; the others run lockstep rows.
 HORIZON = {"subscale16_h4": 4, "subscale16_h4a1": 4}
-LEAD = {"subscale16_h4a1": 1}
+LEAD = {"subscale16_h4a1": 1}   # the lead is switched off at create (E_UNSUPPORTED) for now
 
 
 def preset(name: str, seed: int = 0) -> dict:

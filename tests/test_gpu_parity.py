@@ -19,6 +19,10 @@ from oracle import oracle as O  # noqa: E402
 from paper_1802_08435_amd import synth, wavernn  # noqa: E402
 
 BF16_TOL = 2e-2
+# The context lead (A > 0) is switched off at create: a traced launch with a
+# lead of 1 had a bounded wait expire and the cause is not found.
+LEAD_OFF = pytest.mark.skip(reason="context lead switched off: a traced launch with A = 1 had a bounded wait "
+                                   "expire, cause not found")
 
 
 def cuda(a):
@@ -296,8 +300,11 @@ def test_subscale16_dense896_teacher_forced_within_bf16_tolerance():
 
 
 @pytest.mark.parametrize("H,B,S,F,A", [(256, 8, 2, 1, 0), (128, 16, 1, 2, 0), (256, 4, 2, 0, 0),
-                                       (128, 16, 3, 1, 0), (256, 8, 2, 1, 1), (128, 16, 1, 2, 2),
-                                       (256, 4, 2, 0, 3), (128, 16, 3, 1, 1)])
+                                       (128, 16, 3, 1, 0),
+                                       pytest.param(256, 8, 2, 1, 1, marks=LEAD_OFF),
+                                       pytest.param(128, 16, 1, 2, 2, marks=LEAD_OFF),
+                                       pytest.param(256, 4, 2, 0, 3, marks=LEAD_OFF),
+                                       pytest.param(128, 16, 3, 1, 1, marks=LEAD_OFF)])
 def test_subscale_horizon_teacher_forced_small_sizes(H, B, S, F, A):
     """Subscale in the paper's order with future horizon F (Sec. 4.2): lane s
     runs position i at step i + s (F + 1 + A) and its context holds samples
@@ -321,7 +328,7 @@ def test_subscale_horizon_teacher_forced_small_sizes(H, B, S, F, A):
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=1e-3)
 
 
-@pytest.mark.parametrize("name", ["subscale16_h4", "subscale16_h4a1"])
+@pytest.mark.parametrize("name", ["subscale16_h4", pytest.param("subscale16_h4a1", marks=LEAD_OFF)])
 def test_subscale16_horizon_dense896_teacher_forced_within_bf16_tolerance(name):
     w = synth.preset(name)
     T = 960
@@ -336,7 +343,7 @@ def test_subscale16_horizon_dense896_teacher_forced_within_bf16_tolerance(name):
     np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=2e-2)
 
 
-@pytest.mark.parametrize("A", [0, 1])
+@pytest.mark.parametrize("A", [0, pytest.param(1, marks=LEAD_OFF)])
 def test_subscale_horizon_free_running_draws_valid_and_final_state(A):
     """Free-running with horizon F = 2 (context formed A steps ahead): every
     lane's draw is valid under the oracle's logits on the GPU trajectory with
@@ -410,7 +417,14 @@ def test_invalid_calls_return_errors_without_launching():
 
 
 _EDGE_KINDS = {"single-workgroup": dict(H=64), "persistent": dict(H=256), "block-sparse": dict(H=256, block=(4, 4), density=0.1),
-               "batched": dict(H=256, S=5), "subscale": dict(H=256, B=4), "subscale-horizon": dict(H=256, B=4, F=1, A=1)}
+               "batched": dict(H=256, S=5), "subscale": dict(H=256, B=4), "subscale-horizon": dict(H=256, B=4, F=1)}
+
+
+def test_lead_is_switched_off():
+    w = synth.preset("subscale16_h4a1")
+    with pytest.raises(wavernn.WaveRNNError) as err:
+        wavernn.Model(w)
+    assert err.value.status == wavernn.E_UNSUPPORTED and "switched off" in str(err.value)
 
 
 @pytest.mark.parametrize("kind", sorted(_EDGE_KINDS))
@@ -588,7 +602,7 @@ def test_short_runs_match_the_oracle(kind, T):
         kw.update(B=B, ctx_dim=256)
     w = synth.make_weights(H, seed=12, **kw)
     if kind == "subscale-horizon":
-        w["F"], w["A"] = 1, 1
+        w["F"] = 1
     n = T * B
     feat = synth.features(S, n, cond_dim=16, per_stream_seed=True)
     tgt = _targets(S, n)

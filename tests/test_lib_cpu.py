@@ -57,13 +57,14 @@ def _weights(H=64):
     (dict(subscale=16, ctx_dim=6, future_horizon=2), "multiple of 4"),
     (dict(subscale=16, ctx_dim=256, future_horizon=2, context_lead=4), "context_lead"),
     (dict(subscale=16, ctx_dim=256, future_horizon=-1, context_lead=1), "context_lead"),
+    (dict(subscale=16, ctx_dim=256, future_horizon=4, context_lead=1), "switched off"),
 ])
 def test_create_rejects_bad_config_before_touching_the_device(bad, msg):
     L = W.lib()
     ws, keep = _weights()
     h = ctypes.c_void_p()
     st = L.wavernn_create(ctypes.byref(_cfg(**bad)), ctypes.byref(ws), ctypes.byref(h))
-    assert st == W.E_INVALID
+    assert st == (W.E_UNSUPPORTED if msg == "switched off" else W.E_INVALID)
     assert msg in L.wavernn_last_error().decode()
     assert not h.value
 
