@@ -179,6 +179,11 @@ def main() -> int:
     out = torch.empty(S, T, dtype=torch.uint16, device="cuda")
     stream = torch.cuda.current_stream()
     if args.phases:
+        if path not in PHASES:                          # a kernel without phase stamps
+            print(json.dumps({"workload": args.config, "kernel": KERNEL_OF.get(path, path), "phases": None}),
+                  flush=True)
+            m.close()
+            return 0
         m.sample(T, cond=feat, seed=1, n_streams=S, out=out)
         ph = phases(m, w, path, S, feat, min(T // w["B"], 4000))
         print(json.dumps({"workload": args.config, "kernel": KERNEL_OF.get(path, path), **ph}), flush=True)
