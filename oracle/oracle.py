@@ -45,6 +45,12 @@ class _Model(ctypes.Structure):
         for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")]
 
 
+class _FusedModel(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int32), ("F", ctypes.c_int32), ("Dc", ctypes.c_int32),
+                ("frame_len", ctypes.c_int32)] + [
+        (n, ctypes.POINTER(ctypes.c_float)) for n in ("R", "I", "b", "Wc", "O1", "b1", "O2", "b2")]
+
+
 def lib():
     global _lib
     if _lib is None:
@@ -70,6 +76,8 @@ def load(path: str):
     L.orc_draw.argtypes = [vp, ctypes.c_int, f32]
     L.orc_subscale_context.restype = None
     L.orc_subscale_context.argtypes = [ctypes.POINTER(_Model), vp, i64, i32, i64, vp]
+    L.orc_fused_run.restype = ctypes.c_int
+    L.orc_fused_run.argtypes = [ctypes.POINTER(_FusedModel), i32, i64, vp, i64, u64, vp, vp, vp, vp, vp, vp]
     L.orc_run.restype = ctypes.c_int
     L.orc_run.argtypes = [ctypes.POINTER(_Model), i32, i64, i64, vp, i64, u64, vp, vp, vp, vp, vp,
                           vp, vp, vp]
@@ -216,3 +224,32 @@ def run(w: Weights, S: int, T: int, feat=None, seed: int = 1, target=None, h0=No
     if rc != 0:
         raise ValueError("oracle rejected the inputs")
     return dict(out=out, h=h, c=c, f=f, zc=zc, zf=zf, nll=nl)
+
+
+def fused_run(w: dict, S: int, N: int, feat=None, seed: int = 1, target=None, frame_len: int = 120) -> dict:
+    """Fused Subscale WaveRNN 2x (Sec. 4.4): sample (target None) or teacher-force S
+    utterances of N samples.  w: H, F and fp32 arrays R [3][H][H], I [3][H][6], b [3][H],
+    O1 [4][Q][Q], b1 [4][Q], O2 [4][2][16][Q], b2 [4][2][16], optional Wc [3H][Dc].
+    Returns dict(out [S][N] uint16, zc, zf [S][N][32], nll [S][N], h [S][H])."""
+    H = int(w["H"])
+    keep = {k: np.ascontiguousarray(w[k], np.float32) for k in ("R", "I", "b", "O1", "b1", "O2", "b2")}
+    Wc = None if w.get("Wc") is None else np.ascontiguousarray(w["Wc"], np.float32)
+    fp = lambda a: None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    m = _FusedModel(H, int(w["F"]), 0 if Wc is None else Wc.shape[1], frame_len,
+                    fp(keep["R"]), fp(keep["I"]), fp(keep["b"]), fp(Wc), fp(keep["O1"]), fp(keep["b1"]),
+                    fp(keep["O2"]), fp(keep["b2"]))
+    n_frames = 0
+    if feat is not None:
+        feat = np.ascontiguousarray(feat, np.float32)
+        n_frames = feat.shape[1]
+    tgt = None if target is None else np.ascontiguousarray(target, np.uint16)
+    out = np.zeros((S, N), np.uint16)
+    zc = np.zeros((S, N, 32), np.float32)
+    zf = np.zeros((S, N, 32), np.float32)
+    nl = np.zeros((S, N), np.float64)
+    h = np.zeros((S, H), np.float32)
+    rc = lib().orc_fused_run(ctypes.byref(m), S, N, _p(feat), n_frames, seed, _p(tgt), _p(out), _p(zc), _p(zf),
+                             _p(nl), _p(h))
+    if rc != 0:
+        raise ValueError("oracle rejected the inputs")
+    return dict(out=out, zc=zc, zf=zf, nll=nl, h=h)

@@ -49,6 +49,8 @@
  *         recurrent state and inputs; no distant dependencies, Sec. 4.3), as
  *         the Dx/4 samples before n and the Dx/4 after n, zero where not seen.
  *         Generated here sub-tensor by sub-tensor, in the paper's order.
+ *   - Fused Subscale WaveRNN 2x (Sec. 4.4): orc_fused_run, with its own
+ *     readings in the section at the end of this file.
  *
  * Build: cc -O2 -ffp-contract=off -fPIC -shared (no fast-math; fmaf only where written).
  */
@@ -326,5 +328,150 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
     }
   }
   free(G); free(add); free(hn); free(ctx);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Fused Subscale WaveRNN 2x (Sec. 4.4)                                        */
+/* ------------------------------------------------------------------------- */
+/* The paper describes the model in a few sentences: a Subscale 2x model whose
+ * two sub-tensors, instead of being batched, share one WaveRNN by splitting
+ * its state, with 8 softmaxes of 4 bits and a future horizon of 2, the
+ * samples entering the WaveRNN directly as inputs.  Readings fixed here:
+ *   - units [0,Q) are the coarse quarter of sub-tensor 0, [Q,2Q) the coarse
+ *     quarter of sub-tensor 1, [2Q,3Q) and [3Q,4Q) their fine quarters
+ *     (Q = H/4); R is one full 3H x H matrix (the state is one vector);
+ *   - step t runs position t of sub-tensor 0 and position t - (F + 1) of
+ *     sub-tensor 1, so the state that makes position i of sub-tensor 1 has
+ *     seen sub-tensor 0 up to position i + F (Sec. 4.2);
+ *   - inputs x = (c0, f0, c1, f1) of each sub-tensor's last sample, then the
+ *     coarse bytes c0_t, c1_t of this step: the coarse quarters use the first
+ *     four columns of I, the fine quarter of sub-tensor s those four and the
+ *     column of its own c_t (the I* mask of Eq. 2 per sub-tensor: the coarse
+ *     half is evaluated and its bytes drawn before the fine half), so the two
+ *     parts meet only through the state and the last samples;
+ *   - each byte is two nibbles (high, low) drawn from two 16-way softmaxes of
+ *     one output head per (level, sub-tensor), k = 2 level + s:
+ *     o = relu(O1_k y + b1_k) on that quarter y, z_hi = O2_k,hi o + b2_k,hi,
+ *     z_lo = O2_k,lo o + b2_k,lo, byte = 16 hi + lo; the two nibbles of a byte
+ *     are independent given the state (8 softmaxes per step, 32 bits);
+ *   - a sub-tensor outside its positions (sub-tensor 1 for the first F + 1
+ *     steps, sub-tensor 0 for the last F + 1) is idle: it draws nothing and
+ *     its inputs, its coarse-byte input included, keep its last sample
+ *     (before the first: c = 128, f = 0);
+ *   - conditioning: a unit of sub-tensor s adds W_cond times the frame of the
+ *     sample its sub-tensor makes (its last position while idle);
+ *   - uniforms: Philox4x64-10, key (seed, 0), counter (i, 2 u + s, 0, 0) for
+ *     position i of sub-tensor s of utterance u; words 0..3 give the coarse
+ *     high, coarse low, fine high and fine low nibble.
+ * Sample n = 2 i + s of an utterance is position i of sub-tensor s. */
+
+/* A (level, sub-tensor) head: z[0..15] high nibble, z[16..31] low nibble. */
+static void fused_head(const orc_fused_model* m, int k, const float* y, float* z) {
+  const int Q = m->H / 4;
+  float hid[ORC_MAX_HIDDEN / 4];
+  const float* Oa = m->O1 + (size_t)k * Q * Q;
+  const float* ba = m->b1 + (size_t)k * Q;
+  for (int j = 0; j < Q; ++j) hid[j] = relu(dot(Oa + (size_t)j * Q, y, Q) + ba[j]);
+  for (int v = 0; v < 32; ++v)
+    z[v] = dot(m->O2 + ((size_t)k * 32 + v) * Q, hid, Q) + m->b2[(size_t)k * 32 + v];
+}
+
+/* Gates of units [lo, hi) with the first nx input columns (of six). */
+static void fused_units(const orc_fused_model* m, const float* G, const float* add, const float* x, int nx,
+                        const float* h_prev, float* h_new, int lo, int hi) {
+  const int H = m->H;
+  for (int i = lo; i < hi; ++i) {
+    float ix[3];
+    for (int g = 0; g < 3; ++g) ix[g] = dot(m->I + ((size_t)g * H + i) * 6, x, nx);
+    const float ug = orc_sigmoid(G[0 * H + i] + (ix[0] + add[0 * H + i]));
+    const float rg = orc_sigmoid(G[1 * H + i] + (ix[1] + add[1 * H + i]));
+    const float eg = orc_tanh(fmaf(rg, G[2 * H + i], ix[2] + add[2 * H + i]));
+    h_new[i] = fmaf(ug, h_prev[i], (1.0f - ug) * eg);
+  }
+}
+
+static int fused_nibbles(const float* z, const float* u, int forced) {
+  if (forced >= 0) return forced;
+  return 16 * orc_draw(z, 16, u[0]) + orc_draw(z + 16, 16, u[1]);
+}
+
+int orc_fused_run(const orc_fused_model* m, int32_t S, int64_t N, const float* feat, int64_t n_frames,
+                  uint64_t seed, const uint16_t* target, uint16_t* out, float* zc_out, float* zf_out,
+                  double* nll_out, float* h_final) {
+  const int H = m->H, Q = H / 4;
+  if (H <= 0 || H % 4 || H > ORC_MAX_HIDDEN || S <= 0 || N < 0 || N % 2 || m->F < 0) return -1;
+  if (m->Dc > 0 && (m->frame_len <= 0 || feat == NULL || n_frames <= 0)) return -1;
+  if (target == NULL && out == NULL) return -1;
+  const int64_t rows = N / 2, steps = N > 0 ? rows + m->F + 1 : 0;
+  float* h = (float*)malloc(sizeof(float) * H);
+  float* hn = (float*)malloc(sizeof(float) * H);
+  float* G = (float*)malloc(sizeof(float) * 3 * H);
+  float* add = (float*)malloc(sizeof(float) * 3 * H);
+  for (int32_t ut = 0; ut < S; ++ut) {
+    const uint16_t* tgt = target ? target + (size_t)ut * N : NULL;
+    for (int i = 0; i < H; ++i) h[i] = 0.0f;
+    int cl[2] = {128, 128}, fl[2] = {0, 0};            /* last sample of each sub-tensor */
+    for (int64_t t = 0; t < steps; ++t) {
+      const int64_t p[2] = {t, t - (m->F + 1)};
+      const int act[2] = {p[0] >= 0 && p[0] < rows, p[1] >= 0 && p[1] < rows};
+      int64_t nn[2];                                   /* the sample each sub-tensor makes (or made last) */
+      for (int s = 0; s < 2; ++s) {
+        int64_t pc = p[s] < 0 ? 0 : (p[s] >= rows ? rows - 1 : p[s]);
+        nn[s] = 2 * pc + s;
+      }
+      for (int row = 0; row < 3 * H; ++row) {
+        const int s = (row % H) / Q % 2;
+        float bias_cond = m->b[row];
+        if (m->Dc > 0) {
+          int64_t fr = nn[s] / m->frame_len;
+          if (fr >= n_frames) fr = n_frames - 1;
+          bias_cond = dot(m->Wc + (size_t)row * m->Dc, feat + ((size_t)ut * n_frames + fr) * m->Dc, m->Dc) + m->b[row];
+        }
+        add[row] = bias_cond;
+        G[row] = dot(m->R + (size_t)row * H, h, H);
+      }
+      float u[2][4];
+      for (int s = 0; s < 2; ++s) {
+        uint64_t ctr[4] = {(uint64_t)(act[s] ? p[s] : 0), (uint64_t)(2 * ut + s), 0, 0}, key[2] = {seed, 0}, w[4];
+        orc_philox4x64_10(ctr, key, w);
+        for (int k = 0; k < 4; ++k) u[s][k] = (float)(w[k] >> 40) * (1.0f / 16777216.0f);
+      }
+      float x[6] = {orc_scale(cl[0]), orc_scale(fl[0]), orc_scale(cl[1]), orc_scale(fl[1]), 0.0f, 0.0f};
+      float zc[2][32], zf[2][32];
+      int c[2], f[2];
+      /* coarse half, the two coarse heads, the coarse bytes */
+      fused_units(m, G, add, x, 4, h, hn, 0, 2 * Q);
+      for (int s = 0; s < 2; ++s) {
+        fused_head(m, s, hn + s * Q, zc[s]);
+        c[s] = act[s] ? fused_nibbles(zc[s], u[s], tgt ? tgt[2 * p[s] + s] >> 8 : -1) : cl[s];
+      }
+      /* each fine quarter sees its own coarse byte; the two fine heads, the fine bytes */
+      x[4] = orc_scale(c[0]);
+      fused_units(m, G, add, x, 6, h, hn, 2 * Q, 3 * Q);
+      x[4] = 0.0f;
+      x[5] = orc_scale(c[1]);
+      fused_units(m, G, add, x, 6, h, hn, 3 * Q, 4 * Q);
+      for (int s = 0; s < 2; ++s) {
+        fused_head(m, 2 + s, hn + 2 * Q + s * Q, zf[s]);
+        f[s] = act[s] ? fused_nibbles(zf[s], u[s] + 2, tgt ? tgt[2 * p[s] + s] & 255 : -1) : fl[s];
+      }
+      memcpy(h, hn, sizeof(float) * H);
+      for (int s = 0; s < 2; ++s) {
+        if (!act[s]) continue;
+        const size_t o = (size_t)ut * N + (size_t)(2 * p[s] + s);
+        if (out) out[o] = (uint16_t)(256 * c[s] + f[s]);
+        if (zc_out) memcpy(zc_out + o * 32, zc[s], sizeof zc[s]);
+        if (zf_out) memcpy(zf_out + o * 32, zf[s], sizeof zf[s]);
+        if (nll_out)
+          nll_out[o] = neg_log_prob(zc[s], 16, c[s] >> 4) + neg_log_prob(zc[s] + 16, 16, c[s] & 15) +
+                       neg_log_prob(zf[s], 16, f[s] >> 4) + neg_log_prob(zf[s] + 16, 16, f[s] & 15);
+        cl[s] = c[s];
+        fl[s] = f[s];
+      }
+    }
+    if (h_final) memcpy(h_final + (size_t)ut * H, h, sizeof(float) * H);
+  }
+  free(h); free(hn); free(G); free(add);
   return 0;
 }

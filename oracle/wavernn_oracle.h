@@ -46,4 +46,25 @@ void orc_subscale_context(const orc_model* m, const uint16_t* seq, int64_t N, in
 int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* feat, int64_t n_frames,
             uint64_t seed, const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, uint16_t* out,
             float* zc, float* zf, double* nll);
+/* Fused Subscale WaveRNN 2x (Sec. 4.4); readings in wavernn_oracle.c.  Q = H/4.
+ *   R  [3][H][H]       one recurrent matrix over the whole state
+ *   I  [3][H][6]       columns (c0, f0, c1, f1) of each sub-tensor's last sample,
+ *                      then c0_t, c1_t; coarse units [0, 2Q) use the first four,
+ *                      fine units of sub-tensor s those and the column of c_s,t
+ *   b  [3][H]          gate biases;  Wc [3H][Dc] conditioning (Dc = 0: none)
+ *   O1 [4][Q][Q] b1 [4][Q]          head k = 2 level + s (level 0 coarse, 1 fine)
+ *   O2 [4][2][16][Q] b2 [4][2][16]  [k][0] high nibble, [k][1] low nibble   */
+typedef struct {
+  int32_t H, F, Dc, frame_len;
+  const float *R, *I, *b, *Wc, *O1, *b1, *O2, *b2;
+} orc_fused_model;
+
+/* Runs S utterances of N samples (N even) from h = 0 and last samples
+ * (128, 0): N/2 + F + 1 steps.  feat [S][n_frames][Dc]; target [S][N] (NULL:
+ * sample freely); out [S][N]; zc/zf [S][N][32] (high then low nibble logits),
+ * nll [S][N] (nats, four nibbles) and h_final [S][H] are optional.  Returns 0
+ * or -1. */
+int orc_fused_run(const orc_fused_model* m, int32_t S, int64_t N, const float* feat, int64_t n_frames,
+                  uint64_t seed, const uint16_t* target, uint16_t* out, float* zc, float* zf, double* nll,
+                  float* h_final);
 #endif

@@ -54,6 +54,16 @@ MUTANTS = {
     "subscale_window_includes_n": ("n + 1 + (j - P / 2)", "n + (j - P / 2)"),
     "subscale_lane_order": ("const int64_t n = (B == 1) ? t0 + i : B * i + lane;",
                             "const int64_t n = (B == 1) ? t0 + i : rows * lane + i;"),
+    "fused_lag_short_by_one": ("const int64_t p[2] = {t, t - (m->F + 1)};", "const int64_t p[2] = {t, t - m->F};"),
+    "fused_fine_sees_other_coarse": ("      x[4] = 0.0f;\n", "      x[4] = orc_scale(c[0]);\n"),
+    "fused_nibble_words_swapped": ("return 16 * orc_draw(z, 16, u[0]) + orc_draw(z + 16, 16, u[1]);",
+                                   "return 16 * orc_draw(z, 16, u[1]) + orc_draw(z + 16, 16, u[0]);"),
+    "fused_heads_read_other_quarter": ("fused_head(m, s, hn + s * Q, zc[s]);", "fused_head(m, s, hn + (1 - s) * Q, zc[s]);"),
+    "fused_idle_coarse_input_reset": ("act[s] ? fused_nibbles(zc[s], u[s], tgt ? tgt[2 * p[s] + s] >> 8 : -1) : cl[s];",
+                                      "act[s] ? fused_nibbles(zc[s], u[s], tgt ? tgt[2 * p[s] + s] >> 8 : -1) : 128;"),
+    "fused_stream_index": ("(uint64_t)(2 * ut + s), 0, 0}", "(uint64_t)(ut + s), 0, 0}"),
+    "fused_coarse_sees_current_bytes": ("fused_units(m, G, add, x, 4, h, hn, 0, 2 * Q);",
+                                        "x[4] = 1.0f; fused_units(m, G, add, x, 6, h, hn, 0, 2 * Q);"),
     "exp_low_coeffs_off": ("g_inv_fact[i] = (float)(1.0 / f);", "g_inv_fact[i] = (float)(1.0 / (f + (i == 2)));"),
 }
 
@@ -68,6 +78,8 @@ PINS = [
     "test_chunked_sampling_equals_one_call", "test_subscale_without_context_is_interleaved_plain_streams",
     "test_subscale_context_masks_samples_of_the_current_row", "test_subscale_horizon_context_hand_cases",
     "test_subscale_horizon_dependencies_precede_in_the_lagged_schedule",
+    "test_fused_zero_model_nibbles_are_floor_16u_and_nll_is_4ln16", "test_fused_state_reduces_to_the_plain_oracle",
+    "test_fused_heads_read_their_own_quarter", "test_fused_dependencies_follow_the_fused_order",
 ]
 
 _PARAMS = {"test_philox_matches_numpy": [dict(seed=7, stream=3, t=123456), dict(seed=1, stream=0, t=5)],
@@ -75,7 +87,10 @@ _PARAMS = {"test_philox_matches_numpy": [dict(seed=7, stream=3, t=123456), dict(
            "test_subscale_horizon_context_hand_cases": [
                dict(zip(("B", "F", "Dx", "s", "i", "idx"), c))
                for c in P.test_subscale_horizon_context_hand_cases.pytestmark[0].args[1]],
-           "test_subscale_horizon_dependencies_precede_in_the_lagged_schedule": [dict(F=1)]}
+           "test_subscale_horizon_dependencies_precede_in_the_lagged_schedule": [dict(F=1)],
+           "test_fused_state_reduces_to_the_plain_oracle": [dict(s=0), dict(s=1)],
+           "test_fused_heads_read_their_own_quarter": [dict(k=k) for k in range(4)],
+           "test_fused_dependencies_follow_the_fused_order": [dict(F=2)]}
 
 
 def _failures(tmp_path, name):

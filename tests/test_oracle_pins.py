@@ -483,3 +483,133 @@ def test_wavernn896_parameter_count_matches_the_paper():
     assert n == 3 * 896 * 896 + 2 * 448 * 448 + 2 * 256 * 448
     assert abs(n - 3e6) / 3e6 < 0.02
     assert abs(n * 24e3 * 4 / 1e9 - 288) / 288 < 0.02
+
+
+# ------------------------------------------------- Fused Subscale WaveRNN 2x (Sec. 4.4)
+
+def fused_model(H=8, F=2, seed=0, scale=1.0):
+    Q = H // 4
+    rng = np.random.default_rng(seed)
+    g = lambda *s: (scale * rng.normal(0, 1.0 / math.sqrt(s[-1]), s)).astype(np.float32)
+    return dict(H=H, F=F, R=g(3, H, H), I=g(3, H, 6), b=g(3, H, 1)[..., 0] * 0.3,
+                O1=g(4, Q, Q), b1=g(4, Q, 1)[..., 0] * 0.3, O2=g(4, 2, 16, Q), b2=g(4, 2, 16, 1)[..., 0] * 0.3)
+
+
+def fused_zero_model(H=8, F=2):
+    d = fused_model(H, F)
+    return {k: (np.zeros_like(v) if isinstance(v, np.ndarray) else v) for k, v in d.items()}
+
+
+def numpy_words(seed, stream, t):
+    from numpy.random import Philox
+    return [int(x) >> 40 for x in Philox(key=seed, counter=_counter_minus_one(t, stream)).random_raw(4)]
+
+
+def test_fused_zero_model_nibbles_are_floor_16u_and_nll_is_4ln16():
+    """All weights zero: every nibble softmax is uniform, so sample 2 i + s of
+    utterance u is built from floor(16 U) of the four Philox words of
+    counter (i, 2 u + s) (coarse high, coarse low, fine high, fine low), and
+    each sample costs 4 ln 16 nats."""
+    d = fused_zero_model()
+    S, N = 2, 60
+    r = O.fused_run(d, S, N, seed=11)
+    for u in range(S):
+        for n in range(N):
+            i, s = divmod(n, 2)
+            w = numpy_words(11, 2 * u + s, i)
+            nib = [math.floor(16 * (x / 2.0**24)) for x in w]
+            assert r["out"][u, n] == 256 * (16 * nib[0] + nib[1]) + 16 * nib[2] + nib[3], (u, n)
+    tgt = np.random.default_rng(2).integers(0, 65536, (S, N)).astype(np.uint16)
+    t = O.fused_run(d, S, N, target=tgt)
+    assert np.all(t["zc"] == 0) and np.all(t["zf"] == 0)
+    np.testing.assert_allclose(t["nll"], 4 * math.log(16), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("s", [0, 1])
+def test_fused_state_reduces_to_the_plain_oracle(s):
+    """With the input columns of the other sub-tensor zero (and c_s,t kept
+    from the other fine quarter), the fused state is the plain WaveRNN's
+    state driven by sub-tensor s alone: sub-tensor 0 from step 0, idle (its
+    last sample repeated) for the last F + 1 steps; sub-tensor 1 idle on
+    silence (128, 0) for the first F + 1 steps.  The plain oracle is pinned
+    on its own; this fixes the fused schedule, input layout and masks."""
+    H, F, N = 8, 2, 40
+    Q, rows = H // 4, N // 2
+    rng = np.random.default_rng(5 + s)
+    d = fused_model(H, F, seed=7 + s)
+    Ip = rng.normal(0, 0.7, (3, H, 3)).astype(np.float32)     # plain columns c_{t-1}, f_{t-1}, c_t
+    # the plain model's fine half is [2Q, 4Q); the fine quarter of the other
+    # sub-tensor must not see c_t
+    Ip[:, (3 * Q if s == 0 else 2 * Q):(4 * Q if s == 0 else 3 * Q), 2] = 0.0
+    If = rng.normal(0, 0.7, (3, H, 6)).astype(np.float32)
+    own, other = ((0, 1, 4), (2, 3, 5)) if s == 0 else ((2, 3, 5), (0, 1, 4))
+    for k in range(3):
+        If[:, :, own[k]] = Ip[:, :, k]
+        If[:, :, other[k]] = 0.0
+    If[:, :2 * Q, own[2]] = 5.0                                 # coarse units ignore c_t (mask)
+    If[:, (2 * Q if s == 0 else 3 * Q):(3 * Q if s == 0 else 4 * Q), other[2]] = 5.0   # own fine quarter ignores the other c_t
+    assert np.abs(If[:, :, own[2]]).max() > 0
+    d["I"] = If
+    tgt = rng.integers(0, 65536, (1, N)).astype(np.uint16)
+    fused = O.fused_run(d, 1, N, target=tgt)
+    seq = tgt[0, s::2]
+    if s == 0:
+        plain_t = np.concatenate([seq, np.full(F + 1, seq[-1], np.uint16)])
+    else:
+        plain_t = np.concatenate([np.full(F + 1, 128 * 256, np.uint16), seq])
+    p = zero_model(H=H)
+    p.update(R=d["R"], I=Ip, b=d["b"])
+    plain = O.run(W(p), 1, rows + F + 1, target=plain_t[None, :])
+    np.testing.assert_array_equal(fused["h"][0], plain["h"][0])
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 3])
+def test_fused_heads_read_their_own_quarter(k):
+    """Head k = 2 level + s reads quarter k of the state and feeds the two
+    nibbles of byte (level) of sub-tensor s.  h is pinned by the gates
+    (u = 0, r = 0: h = tanh(b_e)), positive on quarter k only, and head j
+    turns a positive input into a near point mass on nibbles (3 + j, 12 - j);
+    every other head sees zeros and draws uniform nibbles."""
+    H, Q, N = 8, 2, 400
+    d = fused_zero_model(H)
+    d["b"][0] = -100.0
+    d["b"][1] = -100.0
+    d["b"][2] = -2.0
+    d["b"][2, k * Q:(k + 1) * Q] = 2.0
+    for j in range(4):
+        d["O1"][j] = np.eye(Q, dtype=np.float32)
+        d["O2"][j, 0, 3 + j] = 40.0
+        d["O2"][j, 1, 12 - j] = 40.0
+    r = O.fused_run(d, 1, N, seed=4)
+    level, s = divmod(k, 2)
+    byte = (r["out"][0, s::2] >> (8 if level == 0 else 0)) & 255
+    assert np.all(byte == 16 * (3 + k) + (12 - k))
+    other = (r["out"][0, (1 - s)::2] >> (8 if level == 0 else 0)) & 255
+    assert np.mean(other == 16 * (3 + k) + (12 - k)) < 0.05
+
+
+@pytest.mark.parametrize("F", [0, 2])
+def test_fused_dependencies_follow_the_fused_order(F):
+    """Brute force on a tiny model (teacher-forced; change one sample, see
+    which logits move).  Position i of sub-tensor s is made at step
+    tau = i + s (F + 1).  Coarse logits of a sample depend exactly on the
+    samples made at earlier steps; fine logits also on the sample's own
+    coarse byte, and on nothing else of its own step.  Hence sub-tensor 1 at
+    position i sees sub-tensor 0 up to position i + F, not i + F + 1."""
+    H, N = 8, 24
+    d = fused_model(H, F, seed=21, scale=2.0)
+    rng = np.random.default_rng(9)
+    tgt = rng.integers(0, 65536, (1, N)).astype(np.uint16)
+    base = O.fused_run(d, 1, N, target=tgt)
+    tau = lambda n: n // 2 + (n % 2) * (F + 1)
+    for n in range(N):
+        t2 = tgt.copy()
+        t2[0, n] ^= 0x8181                                   # both bytes change
+        r = O.fused_run(d, 1, N, target=t2)
+        dc = np.abs(r["zc"][0] - base["zc"][0]).max(axis=1) > 0
+        df = np.abs(r["zf"][0] - base["zf"][0]).max(axis=1) > 0
+        for m in range(N):
+            assert dc[m] == (tau(n) < tau(m)), (n, m, "coarse")
+            assert df[m] == (tau(n) < tau(m) or n == m), (n, m, "fine")
+    # the horizon, read off the schedule the test just checked
+    assert all(tau(2 * (i + F)) < tau(2 * i + 1) <= tau(2 * (i + F + 1)) for i in range(N // 2 - F - 1))
