@@ -55,6 +55,7 @@ def _state(m, st, rows):
     ("dense896", "dense", [11000, 23936], 64, [0]),
     ("sparse2048_4x4", "bsr4x4", [23968], 32, [0]),
     ("multi64", "dense", [47936], 48, [0, 37, 63]),
+    ("multi4", "dense", [12000, 23952], 48, [0, 3]),      # the concurrent batch-1 launches
 ])
 def test_full_length_call_matches_the_oracle_at_sampled_positions(name, fmt, positions, K, check):
     w = synth.preset(name)
@@ -62,6 +63,8 @@ def test_full_length_call_matches_the_oracle_at_sampled_positions(name, fmt, pos
     seed = 11
     feat = synth.features(S, T, per_stream_seed=S > 1)
     m = wavernn.Model(w, dtype="bf16", r_format=fmt, max_streams=S)
+    assert m.path(S)[0] == {"multi64": "batched", "multi4": "concurrent", "sparse2048_4x4": "block-sparse"}.get(
+        name, "persistent")
     fin = m.new_state(S)
     full = host(m.sample(T, cond=cuda(feat), seed=seed, n_streams=S, final=fin))
     m.device_status()
