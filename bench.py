@@ -39,7 +39,7 @@ def weight_bytes_per_step(w: dict) -> int:
 
 # kernel that serves each path of wavernn_model_path
 KERNEL_OF = {"persistent": "wr_persist_kernel", "block-sparse": "wr_sparse_kernel", "batched": "wr_batch_kernel",
-             "single-workgroup": "wr_small_kernel"}
+             "single-workgroup": "wr_small_kernel", "concurrent": "wr_persist_kernel"}
 
 
 def kernel_source_digest() -> str:
