@@ -51,6 +51,11 @@ class _FusedModel(ctypes.Structure):
         (n, ctypes.POINTER(ctypes.c_float)) for n in ("R", "I", "b", "Wc", "O1", "b1", "O2", "b2")]
 
 
+class _Cnn(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "Rc", "Cc", "Dx", "layers")] + [
+        (n, ctypes.POINTER(ctypes.c_float)) for n in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")]
+
+
 def lib():
     global _lib
     if _lib is None:
@@ -78,6 +83,8 @@ def load(path: str):
     L.orc_subscale_context.argtypes = [ctypes.POINTER(_Model), vp, i64, i32, i64, vp]
     L.orc_fused_run.restype = ctypes.c_int
     L.orc_fused_run.argtypes = [ctypes.POINTER(_FusedModel), i32, i64, vp, i64, u64, vp, vp, vp, vp, vp, vp]
+    L.orc_ctx_cnn.restype = ctypes.c_int
+    L.orc_ctx_cnn.argtypes = [ctypes.POINTER(_Cnn), vp, i64, i32, vp]
     L.orc_run.restype = ctypes.c_int
     L.orc_run.argtypes = [ctypes.POINTER(_Model), i32, i64, i64, vp, i64, u64, vp, vp, vp, vp, vp,
                           vp, vp, vp]
@@ -253,3 +260,21 @@ def fused_run(w: dict, S: int, N: int, feat=None, seed: int = 1, target=None, fr
     if rc != 0:
         raise ValueError("oracle rejected the inputs")
     return dict(out=out, zc=zc, zf=zf, nll=nl, h=h)
+
+
+def ctx_cnn(w: dict, seq, s: int) -> np.ndarray:
+    """Conditioning vectors [N/B][Dx] of sub-tensor s from the masked dilated CNN
+    (Sec. 4.1, 5).  w: B, layers and fp32 arrays Win [Rc][2B], bin [Rc],
+    Wc [layers][Cc][3][Rc], bc [layers][Cc], Wo [layers][Rc][Cc], bo [layers][Rc],
+    Wp [Dx][Rc], bp [Dx]."""
+    keep = {k: np.ascontiguousarray(w[k], np.float32) for k in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")}
+    B, L = int(w["B"]), int(w["layers"])
+    Rc, Dx = keep["Win"].shape[0], keep["Wp"].shape[0]
+    Cc = keep["bc"].shape[1] if L > 0 else 1
+    fp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    m = _Cnn(B, Rc, Cc, Dx, L, *[fp(keep[k]) for k in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")])
+    seq = np.ascontiguousarray(seq, np.uint16)
+    out = np.zeros((len(seq) // B, Dx), np.float32)
+    if lib().orc_ctx_cnn(ctypes.byref(m), _p(seq), len(seq), s, _p(out)) != 0:
+        raise ValueError("oracle rejected the inputs")
+    return out

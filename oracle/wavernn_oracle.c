@@ -49,8 +49,9 @@
  *         recurrent state and inputs; no distant dependencies, Sec. 4.3), as
  *         the Dx/4 samples before n and the Dx/4 after n, zero where not seen.
  *         Generated here sub-tensor by sub-tensor, in the paper's order.
- *   - Fused Subscale WaveRNN 2x (Sec. 4.4): orc_fused_run, with its own
- *     readings in the section at the end of this file.
+ *   - Fused Subscale WaveRNN 2x (Sec. 4.4): orc_fused_run, and the masked
+ *     dilated CNN that conditions the Subscale WaveRNN (Sec. 4.1, 5):
+ *     orc_ctx_cnn, each with its own readings in its section below.
  *
  * Build: cc -O2 -ffp-contract=off -fPIC -shared (no fast-math; fmaf only where written).
  */
@@ -473,5 +474,68 @@ int orc_fused_run(const orc_fused_model* m, int32_t S, int64_t N, const float* f
     if (h_final) memcpy(h_final + (size_t)ut * H, h, sizeof(float) * H);
   }
   free(h); free(hn); free(G); free(add);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Subscale conditioning network: masked dilated 1-D CNN (Sec. 4.1, 5)         */
+/* ------------------------------------------------------------------------- */
+/* The paper: a masked dilated CNN with relus whose mask is applied over past
+ * connections instead of future ones, conditioning each sub-tensor on the
+ * past and future of the previous sub-tensors; ten layers, kernel size 3,
+ * 384 convolution channels, 768 residual channels, 5 stages of increasing
+ * dilation, a future horizon of 128 blocks of B samples.  Readings fixed here:
+ *   - the network runs over rows (blocks) k of an utterance; the input of row
+ *     k for sub-tensor s is the (c, f) pair, scaled, of every sub-tensor z of
+ *     that row, zero for z >= s (the previous sub-tensors only) and zero for
+ *     rows outside the utterance: 2B channels;
+ *   - a 1x1 input layer maps them to Rc residual channels: r = Win x + bin;
+ *   - layer l (dilation d = 2^(l mod 5)) reads r at rows k, k + d, k + 2d
+ *     (the future taps: the mask removes the past ones), a = relu(sum over taps
+ *     of Wc_l,tap r + bc_l) with Cc convolution channels, and adds Wo_l a + bo_l
+ *     back into r (residual);
+ *   - a 1x1 output layer gives the Dx-dim conditioning vector of row k:
+ *     out = Wp r + bp.  Ten layers of dilations 1..16 see rows k .. k + 124.
+ * The sub-tensor s at position i is conditioned on out(s, i), so it sees the
+ * previous sub-tensors at rows i .. i + 124 directly and earlier rows through
+ * its state (the unbounded past horizon). */
+int orc_ctx_cnn(const orc_cnn* m, const uint16_t* seq, int64_t N, int32_t s, float* out) {
+  const int B = m->B, Rc = m->Rc, Cc = m->Cc, Dx = m->Dx;
+  if (B < 1 || N % B || s < 0 || s >= B || Rc <= 0 || Cc <= 0 || Dx <= 0 || m->layers < 0) return -1;
+  const int64_t rows = N / B;
+  float* r = (float*)malloc(sizeof(float) * (size_t)(rows > 0 ? rows : 1) * Rc);
+  float* rn = (float*)malloc(sizeof(float) * (size_t)(rows > 0 ? rows : 1) * Rc);
+  float* x = (float*)malloc(sizeof(float) * 2 * B);
+  float* a = (float*)malloc(sizeof(float) * Cc);
+  for (int64_t k = 0; k < rows; ++k) {
+    for (int z = 0; z < B; ++z) {
+      const int seen = z < s;
+      x[2 * z] = seen ? orc_scale(seq[B * k + z] >> 8) : 0.0f;
+      x[2 * z + 1] = seen ? orc_scale(seq[B * k + z] & 255) : 0.0f;
+    }
+    for (int o = 0; o < Rc; ++o) r[k * Rc + o] = dot(m->Win + (size_t)o * 2 * B, x, 2 * B) + m->bin[o];
+  }
+  for (int l = 0; l < m->layers; ++l) {
+    const int d = 1 << (l % 5);
+    const float* Wc = m->Wc + (size_t)l * Cc * 3 * Rc;   /* [Cc][3][Rc] */
+    const float* Wo = m->Wo + (size_t)l * Rc * Cc;       /* [Rc][Cc] */
+    for (int64_t k = 0; k < rows; ++k) {
+      for (int c = 0; c < Cc; ++c) {
+        float acc = m->bc[(size_t)l * Cc + c];
+        for (int tap = 0; tap < 3; ++tap) {
+          const int64_t kk = k + (int64_t)tap * d;      /* future taps only */
+          if (kk >= rows) continue;                      /* beyond the utterance: zero */
+          acc = acc + dot(Wc + ((size_t)c * 3 + tap) * Rc, r + kk * Rc, Rc);
+        }
+        a[c] = relu(acc);
+      }
+      for (int o = 0; o < Rc; ++o)
+        rn[k * Rc + o] = r[k * Rc + o] + (dot(Wo + (size_t)o * Cc, a, Cc) + m->bo[(size_t)l * Rc + o]);
+    }
+    memcpy(r, rn, sizeof(float) * (size_t)rows * Rc);
+  }
+  for (int64_t k = 0; k < rows; ++k)
+    for (int o = 0; o < Dx; ++o) out[k * Dx + o] = dot(m->Wp + (size_t)o * Rc, r + k * Rc, Rc) + m->bp[o];
+  free(r); free(rn); free(x); free(a);
   return 0;
 }

@@ -67,4 +67,16 @@ typedef struct {
 int orc_fused_run(const orc_fused_model* m, int32_t S, int64_t N, const float* feat, int64_t n_frames,
                   uint64_t seed, const uint16_t* target, uint16_t* out, float* zc, float* zf, double* nll,
                   float* h_final);
+/* Subscale conditioning network (Sec. 4.1, 5); readings in wavernn_oracle.c.
+ *   Win [Rc][2B] bin [Rc]; Wc [layers][Cc][3][Rc] bc [layers][Cc] (taps at rows
+ *   k, k + d, k + 2d, d = 2^(l mod 5)); Wo [layers][Rc][Cc] bo [layers][Rc];
+ *   Wp [Dx][Rc] bp [Dx].  The paper: 10 layers, Cc = 384, Rc = 768. */
+typedef struct {
+  int32_t B, Rc, Cc, Dx, layers;
+  const float *Win, *bin, *Wc, *bc, *Wo, *bo, *Wp, *bp;
+} orc_cnn;
+
+/* Conditioning vectors out [N/B][Dx] of sub-tensor s of one utterance whose
+ * samples are seq [N] (N a multiple of B).  Returns 0 or -1. */
+int orc_ctx_cnn(const orc_cnn* m, const uint16_t* seq, int64_t N, int32_t s, float* out);
 #endif

@@ -64,6 +64,11 @@ MUTANTS = {
     "fused_stream_index": ("(uint64_t)(2 * ut + s), 0, 0}", "(uint64_t)(ut + s), 0, 0}"),
     "fused_coarse_sees_current_bytes": ("fused_units(m, G, add, x, 4, h, hn, 0, 2 * Q);",
                                         "x[4] = 1.0f; fused_units(m, G, add, x, 6, h, hn, 0, 2 * Q);"),
+    "cnn_past_taps": ("const int64_t kk = k + (int64_t)tap * d;", "const int64_t kk = k - (int64_t)tap * d;"),
+    "cnn_dilation_stages_4": ("const int d = 1 << (l % 5);", "const int d = 1 << (l % 4);"),
+    "cnn_sees_own_sub_tensor": ("const int seen = z < s;", "const int seen = z <= s;"),
+    "cnn_no_residual": ("rn[k * Rc + o] = r[k * Rc + o] + (dot(", "rn[k * Rc + o] = 0.0f * r[k * Rc + o] + (dot("),
+    "cnn_relu_dropped": ("        a[c] = relu(acc);", "        a[c] = acc;"),
     "exp_low_coeffs_off": ("g_inv_fact[i] = (float)(1.0 / f);", "g_inv_fact[i] = (float)(1.0 / (f + (i == 2)));"),
 }
 
@@ -80,6 +85,8 @@ PINS = [
     "test_subscale_horizon_dependencies_precede_in_the_lagged_schedule",
     "test_fused_zero_model_nibbles_are_floor_16u_and_nll_is_4ln16", "test_fused_state_reduces_to_the_plain_oracle",
     "test_fused_heads_read_their_own_quarter", "test_fused_dependencies_follow_the_fused_order",
+    "test_cnn_shift_layers_sum_the_future_rows", "test_cnn_sees_only_previous_sub_tensors_within_124_rows_ahead",
+    "test_cnn_first_sub_tensor_sees_nothing", "test_cnn_relu_clips_a_negative_layer",
 ]
 
 _PARAMS = {"test_philox_matches_numpy": [dict(seed=7, stream=3, t=123456), dict(seed=1, stream=0, t=5)],
@@ -90,7 +97,8 @@ _PARAMS = {"test_philox_matches_numpy": [dict(seed=7, stream=3, t=123456), dict(
            "test_subscale_horizon_dependencies_precede_in_the_lagged_schedule": [dict(F=1)],
            "test_fused_state_reduces_to_the_plain_oracle": [dict(s=0), dict(s=1)],
            "test_fused_heads_read_their_own_quarter": [dict(k=k) for k in range(4)],
-           "test_fused_dependencies_follow_the_fused_order": [dict(F=2)]}
+           "test_fused_dependencies_follow_the_fused_order": [dict(F=2)],
+           "test_cnn_shift_layers_sum_the_future_rows": [dict(layers=l) for l in (1, 2, 5, 10)]}
 
 
 def _failures(tmp_path, name):

@@ -613,3 +613,81 @@ def test_fused_dependencies_follow_the_fused_order(F):
             assert df[m] == (tau(n) < tau(m) or n == m), (n, m, "fine")
     # the horizon, read off the schedule the test just checked
     assert all(tau(2 * (i + F)) < tau(2 * i + 1) <= tau(2 * (i + F + 1)) for i in range(N // 2 - F - 1))
+
+
+# ------------------------------- subscale conditioning network (Sec. 4.1, 5): masked dilated CNN
+
+def cnn_model(B=4, Rc=6, Cc=5, Dx=3, layers=10, seed=0):
+    rng = np.random.default_rng(seed)
+    g = lambda *s: rng.normal(0, 1.0 / math.sqrt(s[-1]), s).astype(np.float32)
+    return dict(B=B, layers=layers, Win=g(Rc, 2 * B), bin=g(Rc, 1)[:, 0], Wc=g(layers, Cc, 3, Rc),
+                bc=np.full((layers, Cc), 0.5, np.float32), Wo=g(layers, Rc, Cc), bo=g(layers, Rc, 1)[..., 0],
+                Wp=g(Dx, Rc), bp=g(Dx, 1)[:, 0])
+
+
+@pytest.mark.parametrize("layers", [1, 2, 5, 10])
+def test_cnn_shift_layers_sum_the_future_rows(layers):
+    """One channel carried through: input c of sub-tensor 0 (positive), every
+    layer adds r at the row 2d ahead (tap 2, weight 1; relu passes positives),
+    so with dilations 1, 2, 4, 8, 16 the output of row k is the sum of x over
+    rows k, k + 2, ..., k + 2 (2^layers - 1) (rows past the end are zero)."""
+    B, Rc, Cc, Dx, rows = 2, 1, 1, 1, 80
+    m = dict(B=B, layers=layers, Win=np.zeros((Rc, 2 * B), np.float32), bin=np.zeros(Rc, np.float32),
+             Wc=np.zeros((layers, Cc, 3, Rc), np.float32), bc=np.zeros((layers, Cc), np.float32),
+             Wo=np.ones((layers, Rc, Cc), np.float32), bo=np.zeros((layers, Rc), np.float32),
+             Wp=np.ones((Dx, Rc), np.float32), bp=np.zeros(Dx, np.float32))
+    m["Win"][0, 0] = 1.0                                         # c of sub-tensor 0
+    m["Wc"][:, 0, 2, 0] = 1.0                                    # the tap 2d ahead
+    rng = np.random.default_rng(layers)
+    seq = rng.integers(128 * 256, 65536, rows * B).astype(np.uint16)   # c >= 128: scaled c > 0
+    out = O.ctx_cnn(m, seq, 1)[:, 0]
+    xc = np.array([O.scale(int(v) >> 8) for v in seq[0::B]], np.float64)
+    span = 2 * (2 ** min(layers, 5) - 1) if layers <= 5 else None
+    for k in range(rows):
+        if layers <= 5:
+            want = sum(xc[k + j] for j in range(0, span + 1, 2) if k + j < rows)
+        else:   # layers 6..10 repeat the dilations: offsets are sums of two such sets
+            offs = [a + b for a in range(0, 63, 2) for b in range(0, 2 * (2 ** (layers - 5) - 1) + 1, 2)]
+            want = sum(xc[k + j] for j in offs if k + j < rows)
+        assert abs(out[k] - want) <= 1e-5 * max(1.0, abs(want)), (layers, k, out[k], want)
+
+
+def test_cnn_sees_only_previous_sub_tensors_within_124_rows_ahead():
+    """Brute force: change one sample (row k, sub-tensor z); the conditioning
+    of sub-tensor s moves exactly at rows k - 124 .. k when z < s, nowhere
+    when z >= s (the mask over sub-tensors, the future taps, ten layers)."""
+    m = cnn_model()
+    B, rows, s = 4, 150, 2
+    rng = np.random.default_rng(4)
+    seq = rng.integers(0, 65536, rows * B).astype(np.uint16)
+    base = O.ctx_cnn(m, seq, s)
+    for k, z in [(0, 0), (60, 1), (149, 0), (130, 1), (70, 2), (70, 3)]:
+        q = seq.copy()
+        q[B * k + z] ^= 0x8080
+        moved = np.flatnonzero(np.abs(O.ctx_cnn(m, q, s) - base).max(axis=1) > 0)
+        want = np.arange(max(0, k - 124), k + 1) if z < s else np.array([], int)
+        np.testing.assert_array_equal(moved, want, err_msg=f"k={k} z={z}")
+
+
+def test_cnn_first_sub_tensor_sees_nothing():
+    m = cnn_model()
+    seq = np.random.default_rng(5).integers(0, 65536, 4 * 40).astype(np.uint16)
+    out = O.ctx_cnn(m, seq, 0)
+    zero = O.ctx_cnn(m, np.full_like(seq, 128 * 256), 0)
+    np.testing.assert_array_equal(out, zero)
+
+
+def test_cnn_relu_clips_a_negative_layer():
+    """The shift network of one layer with bias -10 on the convolution: every
+    pre-activation is below zero (|x| <= 1), relu gives 0, and the residual
+    passes the input row through unchanged."""
+    B, rows = 2, 30
+    m = dict(B=B, layers=1, Win=np.zeros((1, 2 * B), np.float32), bin=np.zeros(1, np.float32),
+             Wc=np.zeros((1, 1, 3, 1), np.float32), bc=np.full((1, 1), -10.0, np.float32),
+             Wo=np.ones((1, 1, 1), np.float32), bo=np.zeros((1, 1), np.float32),
+             Wp=np.ones((1, 1), np.float32), bp=np.zeros(1, np.float32))
+    m["Win"][0, 0] = 1.0
+    m["Wc"][0, 0, 2, 0] = 1.0
+    seq = np.random.default_rng(8).integers(0, 65536, rows * B).astype(np.uint16)
+    out = O.ctx_cnn(m, seq, 1)[:, 0]
+    np.testing.assert_array_equal(out, np.array([O.scale(int(v) >> 8) for v in seq[0::B]], np.float32))
