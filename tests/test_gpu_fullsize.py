@@ -128,3 +128,26 @@ def test_full_length_subscale_call_prefix_and_state(name):
         okc = _valid(ref["zc"][0], u[:, 0], full[0, :R * B] >> 8)
         okf = _valid(ref["zf"][0], u[:, 1], full[0, :R * B] & 255)
         assert okc.all() and okf.all()
+
+
+def test_ten_second_utterance_in_one_launch():
+    """240,000 samples (10 s at 24 kHz) in one persistent launch: no bounded
+    wait fires, the state stays bounded, and the call equals two chained
+    calls bit for bit (so no step's exchange was lost over the long run)."""
+    w = synth.preset("dense896")
+    T, cut = 240000, 131072
+    feat = synth.features(1, T)
+    m = wavernn.Model(w, dtype="bf16")
+    assert m.path()[0] == "persistent"
+    fin = m.new_state()
+    full = host(m.sample(T, cond=cuda(feat), seed=21, final=fin))
+    m.device_status()
+    st = m.new_state()
+    a = host(m.sample(cut, cond=cuda(feat), seed=21, final=st))
+    fin2 = m.new_state()
+    b = host(m.sample(T - cut, cond=cuda(feat), seed=21, init=st, final=fin2))
+    m.device_status()
+    np.testing.assert_array_equal(np.concatenate([a, b], axis=1), full)
+    np.testing.assert_array_equal(host(fin2["h"]), host(fin["h"]))
+    assert np.abs(host(fin["h"])).max() <= 1.0
+    assert len(np.unique(full)) > 5000
