@@ -265,7 +265,7 @@ def test_concurrent_streams_teacher_forced_free_running_and_chunked(H, S):
 
 # ------------------------------------------------------------- subscale
 
-@pytest.mark.parametrize("H,B,S", [(256, 8, 2), (128, 16, 1), (128, 16, 3)])
+@pytest.mark.parametrize("H,B,S", [(256, 8, 2), (128, 16, 1), (128, 16, 3), (128, 16, 4)])   # 4 x 16: 64 vectors, the most
 def test_subscale_teacher_forced_small_sizes(H, B, S):
     """Subscale (Sec. 4): B lanes per utterance in lockstep, each conditioned on
     the 128 samples before its own (same-row samples masked); 3 utterances of
@@ -300,7 +300,7 @@ def test_subscale16_dense896_teacher_forced_within_bf16_tolerance():
 
 
 @pytest.mark.parametrize("H,B,S,F,A", [(256, 8, 2, 1, 0), (128, 16, 1, 2, 0), (256, 4, 2, 0, 0),
-                                       (128, 16, 3, 1, 0),
+                                       (128, 16, 3, 1, 0), (128, 16, 4, 2, 0),
                                        pytest.param(256, 8, 2, 1, 1, marks=LEAD_OFF),
                                        pytest.param(128, 16, 1, 2, 2, marks=LEAD_OFF),
                                        pytest.param(256, 4, 2, 0, 3, marks=LEAD_OFF),
