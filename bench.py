@@ -84,7 +84,8 @@ def cpu_baseline(w: dict, T: int, feat, budget_s: float = 12.0) -> dict:
     t = time.perf_counter()
     oracle.run(W, 1, n, feat=feat[:1], seed=1)
     dt = time.perf_counter() - t
-    return {"value": round(n / dt, 2), "unit": "samples/s", "cores": 1, "kind": "oracle",
+    return {"value": round(n / dt, 2), "unit": "samples/s", "cores": 1, "host_cores": os.cpu_count(),
+            "kind": "oracle",
             "sample": f"first {n} of the {T} samples of one utterance, single-threaded C oracle (gcc -O2)"}
 
 
@@ -237,6 +238,7 @@ def main() -> int:
         "us_per_sample": round(us_per_sample_step, 4),
         "x_realtime": round(value / 24000.0, 3),
         "call_ms_min": round(min(call_ms), 4),
+        "call_ms_median": round(float(np.median(call_ms)), 4),
         "sync_floor": None if floor_us is None else {
             "us_per_step": round(floor_us, 4), "frac_of_step": round(floor_us / us_per_sample_step, 4)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",

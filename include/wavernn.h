@@ -29,6 +29,19 @@
  *  - Functions return a wavernn_status; on failure nothing is launched and
  *    wavernn_last_error() (per thread) describes the cause.  No exceptions
  *    cross the ABI.
+ *  - A model serves one call at a time.  Every sample, score and sync-floor
+ *    call of a model uses the model's own exchange words, per-frame tables and
+ *    error word, so two calls of one model whose GPU work overlaps (on two
+ *    streams, or from two threads) race and may time out or corrupt each
+ *    other; calls queued on one stream are safe.  Separate models are
+ *    independent.
+ *  - A failure a kernel flags (a bounded wait that expired) stays recorded in
+ *    the model's error word: the launch that flagged it ends early, and every
+ *    later launch of the model ends at the first wait that has to spin (the
+ *    outputs of those launches are undefined) while the launching calls still
+ *    return WAVERNN_OK, until wavernn_device_status reports WAVERNN_E_DEVICE
+ *    and clears the word.  Check wavernn_device_status after work whose
+ *    outputs matter.
  */
 #ifndef WAVERNN_H
 #define WAVERNN_H
@@ -184,7 +197,7 @@ wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t 
  * (paths 1 and 3 of wavernn_model_path).  Runs n_steps (>= 2) steps of a
  * kernel with the same grid, workgroup roles and exchanged words per step as
  * the sampling kernel but no arithmetic (the per-step synchronization cost
- * the paper discusses in Sec. 5.1), waits for it on `stream`, and writes its
+ * the paper discusses in Sec. 2.1), waits for it on `stream`, and writes its
  * mean time per step in microseconds to *us_per_step (host memory).  Uses the
  * model's exchange buffer: calls on other streams must not overlap it.
  * Errors: E_INVALID (arguments), E_UNSUPPORTED (other paths), E_HIP,

@@ -6,7 +6,7 @@
 // the gate words of the half(s) it serves, without waiting, as the sampling
 // kernel reads them ahead.  Each unit workgroup reads both halves of h from
 // the heads and publishes its gate words for the next step.  The time per
-// step of this kernel is what the exchange pattern alone costs (Sec. 5.1 of
+// step of this kernel is what the exchange pattern alone costs (Sec. 2.1 of
 // the paper counts such a synchronization cost per step).
 #include "wr_kern.h"
 

@@ -47,6 +47,17 @@ MUTANTS = {
     "tanh_as_sigmoid": ("float t = (1.0f - q) / (1.0f + q);", "float t = 1.0f / (1.0f + q);"),
     "nll_fine_term_dropped": ("neg_log_prob(zc, ORC_MAX_CLASSES, c) + neg_log_prob(zf, ORC_MAX_CLASSES, f)",
                               "neg_log_prob(zc, ORC_MAX_CLASSES, c)"),
+    "nll_coarse_fine_swapped": ("neg_log_prob(zc, ORC_MAX_CLASSES, c) + neg_log_prob(zf, ORC_MAX_CLASSES, f)",
+                                "neg_log_prob(zc, ORC_MAX_CLASSES, f) + neg_log_prob(zf, ORC_MAX_CLASSES, c)"),
+    "sample_bytes_swapped": ("if (!tgt) seq[local] = (uint16_t)(256 * c + f);", "if (!tgt) seq[local] = (uint16_t)(256 * f + c);"),
+    "fused_nll_coarse_nibbles_swapped": ("neg_log_prob(zc[s], 16, c[s] >> 4) + neg_log_prob(zc[s] + 16, 16, c[s] & 15)",
+                                         "neg_log_prob(zc[s], 16, c[s] & 15) + neg_log_prob(zc[s] + 16, 16, c[s] >> 4)"),
+    "fused_nll_fine_nibbles_swapped": ("neg_log_prob(zf[s], 16, f[s] >> 4) + neg_log_prob(zf[s] + 16, 16, f[s] & 15)",
+                                       "neg_log_prob(zf[s], 16, f[s] & 15) + neg_log_prob(zf[s] + 16, 16, f[s] >> 4)"),
+    "fused_nll_levels_swapped": ("neg_log_prob(zc[s], 16, c[s] >> 4) + neg_log_prob(zc[s] + 16, 16, c[s] & 15) +\n"
+                                 "                       neg_log_prob(zf[s], 16, f[s] >> 4) + neg_log_prob(zf[s] + 16, 16, f[s] & 15)",
+                                 "neg_log_prob(zc[s], 16, f[s] >> 4) + neg_log_prob(zc[s] + 16, 16, f[s] & 15) +\n"
+                                 "                       neg_log_prob(zf[s], 16, c[s] >> 4) + neg_log_prob(zf[s] + 16, 16, c[s] & 15)"),
     "subscale_no_row_mask": ("seen = q >= 0 && q < (int64_t)B * i;", "seen = q >= 0 && q < n;"),
     "subscale_horizon_plus_one": ("return z < s && k <= i + F;", "return z < s && k <= i + F + 1;"),
     "subscale_sees_own_sub_tensor": ("return z < s && k <= i + F;", "return z <= s && k <= i + F;"),
@@ -77,6 +88,8 @@ PINS = [
     "test_scale_is_correctly_rounded", "test_draw_uniform_logits_is_floor_256u",
     "test_draw_point_mass_and_zero_probability_classes",
     "test_zero_model_samples_are_floor_256u_and_nll_is_2ln256", "test_zero_model_streams_use_their_own_philox_stream",
+    "test_nll_and_samples_at_point_mass_logits", "test_nll_at_unequal_coarse_and_fine_distributions",
+    "test_fused_nll_at_point_mass_nibbles",
     "test_update_gate_saturated_at_one_keeps_state", "test_hand_case_input_mask_and_heads",
     "test_hand_case_reset_gate_placement_and_R_orientation", "test_hand_case_update_gate_interpolates",
     "test_hand_case_conditioning_frames", "test_coarse_logits_do_not_depend_on_current_coarse_byte",

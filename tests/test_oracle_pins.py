@@ -188,6 +188,65 @@ def test_zero_model_samples_are_floor_256u_and_nll_is_2ln256():
     np.testing.assert_allclose(r["nll"], 2 * math.log(256), rtol=0, atol=1e-12)
 
 
+def _point_mass_nll(hot):
+    """-log P of class k under logits 40 at class ``hot`` and 0 elsewhere
+    (closed form): log(1 + 255 e^-40) for the hot class, 40 more for any other."""
+    base = math.log1p(255.0 * math.exp(-40.0))
+    return lambda k: base if k == hot else 40.0 + base
+
+
+def test_nll_and_samples_at_point_mass_logits():
+    """Zero weights except the head biases: h stays 0 (u = r = 1/2, e = 0), so the
+    logits are exactly b2 and b4 (Eq. 2 with relu(0) = 0).  b2 puts 40 on class
+    c* = 3, b4 on f* = 200.  Free-running draws are (c*, f*) at every step, and
+    the NLL of a target (c, f) is the closed form of each softmax: coarse and
+    fine terms differ, so a coarse/fine mix-up changes the value."""
+    d = zero_model(H=4)
+    d["b2"][3] = 40.0
+    d["b4"][200] = 40.0
+    r = O.run(W(d), 1, 64, seed=5)
+    assert np.all(r["out"] == 256 * 3 + 200)
+    tgt = np.array([[256 * 3 + 200, 256 * 200 + 3, 256 * 3 + 7, 256 * 9 + 200, 0, 65535]], np.uint16)
+    t = O.run(W(d), 1, tgt.shape[1], target=tgt, nll=True, logits=True)
+    assert np.all(t["zc"][0] == d["b2"]) and np.all(t["zf"][0] == d["b4"])
+    pc, pf = _point_mass_nll(3), _point_mass_nll(200)
+    for k, u in enumerate(tgt[0]):
+        want = pc(int(u) >> 8) + pf(int(u) & 255)
+        assert abs(t["nll"][0, k] - want) <= 1e-12 * max(1.0, want), (k, t["nll"][0, k], want)
+
+
+def test_nll_at_unequal_coarse_and_fine_distributions():
+    """Two different non-uniform softmaxes with closed-form probabilities: the
+    coarse logits are 2 on the 16 classes 32..47 and 0 elsewhere, the fine
+    logits ln 3 on the 64 even classes below 128 and 0 elsewhere.  So
+    P(c) = e^2 / (16 e^2 + 240) or 1 / (16 e^2 + 240), and
+    P(f) = 3 / 448 or 1 / 448.  Sampled free-running, the class frequencies
+    follow the same probabilities (binomial bound)."""
+    d = zero_model(H=4)
+    d["b2"][32:48] = 2.0
+    d["b4"][0:128:2] = np.float32(math.log(3.0))
+    zc2 = float(np.float32(2.0))
+    l3 = float(np.float32(math.log(3.0)))
+    Zc = 16 * math.exp(zc2) + 240
+    Zf = 64 * math.exp(l3) + 192
+    pc = lambda c: (math.exp(zc2) if 32 <= c < 48 else 1.0) / Zc
+    pf = lambda f: (math.exp(l3) if (f < 128 and f % 2 == 0) else 1.0) / Zf
+    rng = np.random.default_rng(8)
+    tgt = rng.integers(0, 65536, (2, 400)).astype(np.uint16)
+    tgt[0, :4] = [256 * 40 + 2, 256 * 2 + 40, 256 * 130 + 130, 256 * 47 + 127]
+    t = O.run(W(d), 2, 400, target=tgt, nll=True)
+    for s in range(2):
+        for k in range(400):
+            c, f = int(tgt[s, k]) >> 8, int(tgt[s, k]) & 255
+            want = -math.log(pc(c)) - math.log(pf(f))
+            assert abs(t["nll"][s, k] - want) <= 1e-12 * want, (s, k)
+    r = O.run(W(d), 1, 20000, seed=3)["out"][0].astype(np.int64)
+    n = len(r)
+    for frac, p in ((np.mean((r >> 8 >= 32) & (r >> 8 < 48)), 16 * math.exp(zc2) / Zc),
+                    (np.mean(((r & 255) < 128) & ((r & 255) % 2 == 0)), 64 * math.exp(l3) / Zf)):
+        assert abs(frac - p) < 5 * math.sqrt(p * (1 - p) / n), (frac, p)
+
+
 def test_zero_model_streams_use_their_own_philox_stream():
     d = zero_model(H=2)
     r = O.run(W(d), 5, 40, seed=3)
@@ -523,6 +582,39 @@ def test_fused_zero_model_nibbles_are_floor_16u_and_nll_is_4ln16():
     t = O.fused_run(d, S, N, target=tgt)
     assert np.all(t["zc"] == 0) and np.all(t["zf"] == 0)
     np.testing.assert_allclose(t["nll"], 4 * math.log(16), rtol=0, atol=1e-12)
+
+
+def test_fused_nll_at_point_mass_nibbles():
+    """Fused model with zero weights except the nibble biases b2: the state stays
+    0, so each nibble's logits are exactly its bias row.  Head k = 2 level + s
+    puts 40 on high nibble (1 + k) and on low nibble (14 - 3k).  Free-running,
+    every byte is that pair; the NLL of a target is the sum over the four
+    nibbles of the point-mass closed form (log(1 + 15 e^-40), 40 more off the
+    hot nibble), which a high/low or coarse/fine mix-up changes."""
+    d = fused_zero_model(H=8, F=2)
+    hot = {}
+    for k in range(4):
+        hot[(k, 0)], hot[(k, 1)] = 1 + k, 14 - 3 * k
+        d["b2"][k, 0, hot[(k, 0)]] = 40.0
+        d["b2"][k, 1, hot[(k, 1)]] = 40.0
+    S, N = 1, 40
+    r = O.fused_run(d, S, N, seed=2)
+    for n in range(N):
+        s = n % 2
+        c, f = int(r["out"][0, n]) >> 8, int(r["out"][0, n]) & 255
+        assert (c >> 4, c & 15, f >> 4, f & 15) == (hot[(s, 0)], hot[(s, 1)], hot[(2 + s, 0)], hot[(2 + s, 1)]), n
+    base = math.log1p(15.0 * math.exp(-40.0))
+    pm = lambda k, part, v: base if v == hot[(k, part)] else 40.0 + base
+    rng = np.random.default_rng(6)
+    tgt = rng.integers(0, 65536, (S, N)).astype(np.uint16)
+    tgt[0, 0] = 256 * (16 * hot[(0, 0)] + hot[(0, 1)]) + 16 * hot[(2, 0)] + hot[(2, 1)]
+    tgt[0, 1] = 256 * (16 * hot[(1, 1)] + hot[(1, 0)]) + 16 * hot[(3, 0)] + hot[(3, 1)]
+    t = O.fused_run(d, S, N, target=tgt)
+    for n in range(N):
+        s = n % 2
+        c, f = int(tgt[0, n]) >> 8, int(tgt[0, n]) & 255
+        want = pm(s, 0, c >> 4) + pm(s, 1, c & 15) + pm(2 + s, 0, f >> 4) + pm(2 + s, 1, f & 15)
+        assert abs(t["nll"][0, n] - want) <= 1e-12 * max(1.0, want), (n, t["nll"][0, n], want)
 
 
 @pytest.mark.parametrize("s", [0, 1])
