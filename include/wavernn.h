@@ -148,6 +148,28 @@ wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_sam
                               int64_t n_frames, uint64_t seed, const wavernn_state* init, uint16_t* out_dev,
                               const wavernn_state* final_state, void* stream);
 
+/* wavernn_sample without any device allocation, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, kernels and results as wavernn_sample
+ * (bit for bit), but the exchange words and the per-frame bias + conditioning
+ * tables of the call live in a workspace the library holds per device: a
+ * static device array of 16 MiB, kept until the process
+ * ends, never in buffers the model grows.  A call needs, per launch, the
+ * exchange words (under 64 KiB) plus n_frames * 3 * hidden * 4 bytes of table
+ * (per utterance on the batched path; 2-4 concurrent utterances take one
+ * launch each), each part rounded up to 256 bytes; a call that needs more
+ * than 16 MiB fails with E_INVALID before anything is launched (WaveRNN-896
+ * with 64-dim frames of 120 samples: up to about 1,500 frames, 7.5 s, per
+ * utterance at batch 1).  The workspace is shared by every model and call on
+ * the device and keeps the last call's contents (each call clears what must
+ * start at zero and writes every table entry it reads): no-allocation calls
+ * whose GPU work overlaps on one device race, whichever model they use.
+ * Errors: as wavernn_sample, E_HIP if the workspace's address cannot be
+ * looked up. */
+wavernn_status wavernn_sample_noalloc(wavernn_model* m, int32_t n_streams, int64_t n_samples, const float* cond_dev,
+                                      int64_t n_frames, uint64_t seed, const wavernn_state* init, uint16_t* out_dev,
+                                      const wavernn_state* final_state, void* stream);
+
 /* Teacher-forced scoring of known audio (the NLL of Sec. 5): the recurrence
  * runs on target_dev [n_streams][n_samples] instead of drawn samples.  Writes
  * the pre-softmax logits logits_c_dev / logits_f_dev [n_streams][n_samples][256]

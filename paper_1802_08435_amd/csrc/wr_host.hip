@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -571,7 +572,25 @@ struct RunIO {
   float* zf;
   float* nll;
   hipStream_t st;
+  unsigned char* ws = nullptr;   // caller-provided workspace (device) instead of the model's buffers, or null
+  size_t ws_cap = 0;             // its bytes
 };
+
+inline size_t rup256(size_t n) { return (n + 255) / 256 * 256; }
+
+// Exchange words and a per-frame table for each of n_launch launches, carved
+// from the call's workspace: [launch][exchange words | table], 256-byte aligned.
+wavernn_status carve_ws(const RunIO& io, int n_launch, size_t x_words, size_t cb_floats, xw** xc, float** cb) {
+  const size_t xb = rup256((x_words + 1) / 2 * 8), cbb = rup256(cb_floats * 4), per = xb + cbb;
+  if (per * (size_t)n_launch > io.ws_cap)
+    return fail(WAVERNN_E_INVALID, "the call needs %zu bytes of workspace (%d launch(es) x (%zu exchange + %zu table)), "
+                "more than the %zu available", per * (size_t)n_launch, n_launch, xb, cbb, io.ws_cap);
+  for (int i = 0; i < n_launch; ++i) {
+    xc[i] = (xw*)(io.ws + per * i);
+    cb[i] = (float*)(io.ws + per * i + xb);
+  }
+  return WAVERNN_OK;
+}
 
 wavernn_status validate_run(wavernn_model* m, const RunIO& io) {
   if (!m) return fail(WAVERNN_E_INVALID, "null model");
@@ -691,6 +710,13 @@ wavernn_status grow_cb(wavernn_model* m, float** cb, int64_t* cap, int64_t n_cb)
 // Several utterances one after another on the caller's stream.
 wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
   const int64_t n_cb = m->cfg.cond_dim > 0 ? io.n_frames : 1;
+  if (io.ws) {   // every launch of the call reuses one region of the workspace, in stream order
+    xw* xc;
+    float* cb;
+    wavernn_status st = carve_ws(io, 1, m->plan.x_words, (size_t)n_cb * 3 * m->plan.H, &xc, &cb);
+    for (int s = 0; s < io.S && st == WAVERNN_OK; ++s) st = launch_persist_one(m, io, s, xc, cb, n_cb, io.st);
+    return st;
+  }
   if (n_cb > m->cb_cap) HIPOK(hipStreamSynchronize(io.st));
   wavernn_status st = grow_cb(m, &m->d_cb, &m->cb_cap, n_cb);
   if (st != WAVERNN_OK) return st;
@@ -711,7 +737,14 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
 wavernn_status run_fanout(wavernn_model* m, const RunIO& io) {
   const int64_t n_cb = m->cfg.cond_dim > 0 ? io.n_frames : 1;
   wavernn_status st = WAVERNN_OK;
-  if (n_cb > m->fcb_cap) {
+  xw* xc[WR_FAN] = {};
+  float* cb[WR_FAN] = {};
+  if (io.ws) {
+    if ((st = carve_ws(io, io.S, m->plan.x_words, (size_t)n_cb * 3 * m->plan.H, xc, cb)) != WAVERNN_OK) return st;
+  } else {
+    for (int i = 0; i < io.S; ++i) xc[i] = m->d_fxc[i];
+  }
+  if (!io.ws && n_cb > m->fcb_cap) {
     HIPOK(hipStreamSynchronize(io.st));
     int64_t cap = 0;
     for (int i = 0; i < m->nfan && st == WAVERNN_OK; ++i) {
@@ -721,14 +754,15 @@ wavernn_status run_fanout(wavernn_model* m, const RunIO& io) {
     if (st != WAVERNN_OK) return st;
     m->fcb_cap = cap;
   }
+  if (!io.ws)
+    for (int i = 0; i < io.S; ++i) cb[i] = m->d_fcb[i];
   HIPOK(hipEventRecord(m->fan_fork, io.st));
   for (int s = 1; s < io.S; ++s) {
     HIPOK(hipStreamWaitEvent(m->fan_st[s - 1], m->fan_fork, 0));
-    if ((st = launch_persist_one(m, io, s, m->d_fxc[s], m->d_fcb[s], n_cb, m->fan_st[s - 1])) != WAVERNN_OK)
-      return st;
+    if ((st = launch_persist_one(m, io, s, xc[s], cb[s], n_cb, m->fan_st[s - 1])) != WAVERNN_OK) return st;
     HIPOK(hipEventRecord(m->fan_join[s - 1], m->fan_st[s - 1]));
   }
-  if ((st = launch_persist_one(m, io, 0, m->d_fxc[0], m->d_fcb[0], n_cb, io.st)) != WAVERNN_OK) return st;
+  if ((st = launch_persist_one(m, io, 0, xc[0], cb[0], n_cb, io.st)) != WAVERNN_OK) return st;
   for (int s = 1; s < io.S; ++s) HIPOK(hipStreamWaitEvent(io.st, m->fan_join[s - 1], 0));
   return WAVERNN_OK;
 }
@@ -744,19 +778,23 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
   const int64_t n_cb = Dc > 0 ? io.n_frames : 1;
   const size_t need = (size_t)io.S * n_cb * 3 * H;
-  if (need > m->bcb_cap) {   // grow the per-frame table (the only allocation a call can make)
+  xw* xc = m->d_bxc;
+  float* cbt = m->d_bcb;
+  wavernn_status st;
+  if (io.ws) {
+    if ((st = carve_ws(io, 1, (size_t)B.G * B.x_words, need, &xc, &cbt)) != WAVERNN_OK) return st;
+  } else if (need > m->bcb_cap) {   // grow the per-frame table (the only allocation a call can make)
     HIPOK(hipStreamSynchronize(io.st));
     float* p = nullptr;
     wavernn_status s = m->alloc(&p, need * 4);
     if (s != WAVERNN_OK) return s;
-    m->d_bcb = p;
+    m->d_bcb = cbt = p;
     m->bcb_cap = need;
   }
-  wavernn_status st = launch_cond(m, io.cond, n_cb, io.S, m->d_bcb, io.st);
-  if (st != WAVERNN_OK) return st;
   const void* kernel = wr_batch_kernel_ptr(B.KH, B.KX > 0, B.L, F >= 0);
   if (!kernel) return fail(WAVERNN_E_UNSUPPORTED, "no batched kernel for %d vectors", V);
-  if ((st = launch_fill(m->d_bxc, (int64_t)B.G * B.x_words, io.st)) != WAVERNN_OK) return st;
+  if ((st = launch_cond(m, io.cond, n_cb, io.S, cbt, io.st)) != WAVERNN_OK) return st;
+  if ((st = launch_fill(xc, (int64_t)B.G * B.x_words, io.st)) != WAVERNN_OK) return st;
   BatchArgs a;
   memset(&a, 0, sizeof a);
   a.P = B;
@@ -769,7 +807,7 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.b3 = m->d_b3;
   a.b4 = m->d_b4;
   a.ux = m->d_bux;
-  a.cb = m->d_bcb;
+  a.cb = cbt;
   a.n_cb = n_cb;
   a.frame_len = Dc > 0 ? frame_len : (1 << 30);
   a.S = V;
@@ -787,7 +825,7 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.nll_out = io.nll;
   if (io.init) { a.h_in = io.init->h; a.c_in = io.init->c_prev; a.f_in = io.init->f_prev; }
   if (io.fin) { a.h_out = io.fin->h; a.c_out = io.fin->c_prev; a.f_out = io.fin->f_prev; }
-  a.xc = m->d_bxc;
+  a.xc = xc;
   a.err = m->d_err;
   a.limit = kWaitTicks;
   a.trace = m->trace;
@@ -798,13 +836,16 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   return WAVERNN_OK;
 }
 
-wavernn_status run(wavernn_model* m, RunIO& io) {
+wavernn_status scratch_of(int dev, unsigned char** out, size_t* cap);
+
+wavernn_status run(wavernn_model* m, RunIO& io, bool noalloc = false) {
   wavernn_status s = validate_run(m, io);
   if (s != WAVERNN_OK) return s;
   if (io.T == 0) return WAVERNN_OK;
   int dev = 0;
   HIPOK(hipGetDevice(&dev));
   if (dev != m->device) return fail(WAVERNN_E_INVALID, "model lives on device %d, current device is %d", m->device, dev);
+  if (noalloc && (s = scratch_of(dev, &io.ws, &io.ws_cap)) != WAVERNN_OK) return s;
   if (m->path == PATH_SMALL) return run_small(m, io);
   if (m->path == PATH_PERSIST) {
     if (io.S > 1 && io.S <= m->nfan) return run_fanout(m, io);
@@ -812,6 +853,37 @@ wavernn_status run(wavernn_model* m, RunIO& io) {
   }
   if (m->path == PATH_BATCHED) return run_batch(m, io);
   return fail(WAVERNN_E_UNSUPPORTED, "no kernel for this configuration");
+}
+
+}  // namespace
+
+// Workspace of wavernn_sample_noalloc: one array per device (each device that
+// runs the library holds its own copy until the process ends).  Host code
+// never uses the array's name as an address: the device address is looked up
+// once per device with hipGetSymbolAddress and kept in g_scratch.
+#define WR_SCRATCH_BYTES ((size_t)16 << 20)
+#define WR_MAX_DEVICES 64
+static __device__ __align__(256) uint64_t scratch[WR_SCRATCH_BYTES / 8];
+
+namespace {
+
+std::mutex g_scratch_mu;
+unsigned char* g_scratch[WR_MAX_DEVICES] = {};
+
+// Device address of the workspace on device `dev`, which must be current.
+wavernn_status scratch_of(int dev, unsigned char** out, size_t* cap) {
+  if (dev < 0 || dev >= WR_MAX_DEVICES) return fail(WAVERNN_E_UNSUPPORTED, "device %d: above %d devices", dev, WR_MAX_DEVICES);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(WAVERNN_E_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch[dev] = (unsigned char*)p;
+  }
+  *out = g_scratch[dev];
+  *cap = WR_SCRATCH_BYTES;
+  return WAVERNN_OK;
 }
 
 }  // namespace
@@ -897,6 +969,14 @@ wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_sam
   RunIO io{n_streams, n_samples, cond_dev, n_frames, seed, init, final_state, nullptr, out_dev,
            nullptr, nullptr, nullptr, (hipStream_t)stream};
   return run(m, io);
+}
+
+wavernn_status wavernn_sample_noalloc(wavernn_model* m, int32_t n_streams, int64_t n_samples, const float* cond_dev,
+                                      int64_t n_frames, uint64_t seed, const wavernn_state* init, uint16_t* out_dev,
+                                      const wavernn_state* final_state, void* stream) {
+  RunIO io{n_streams, n_samples, cond_dev, n_frames, seed, init, final_state, nullptr, out_dev,
+           nullptr, nullptr, nullptr, (hipStream_t)stream};
+  return run(m, io, true);
 }
 
 wavernn_status wavernn_score_teacher_forced(wavernn_model* m, int32_t n_streams, int64_t n_samples,

@@ -60,6 +60,9 @@ def lib():
         L.wavernn_destroy.argtypes = [vp]
         L.wavernn_sample.restype = ctypes.c_int
         L.wavernn_sample.argtypes = [vp, i32, i64, vp, i64, u64, ctypes.POINTER(State), vp, ctypes.POINTER(State), vp]
+        L.wavernn_sample_noalloc.restype = ctypes.c_int
+        L.wavernn_sample_noalloc.argtypes = [vp, i32, i64, vp, i64, u64, ctypes.POINTER(State), vp,
+                                             ctypes.POINTER(State), vp]
         L.wavernn_score_teacher_forced.restype = ctypes.c_int
         L.wavernn_score_teacher_forced.argtypes = [vp, i32, i64, vp, i64, vp, ctypes.POINTER(State), vp, vp, vp, vp]
         L.wavernn_device_status.restype = ctypes.c_int
@@ -167,17 +170,22 @@ class Model:
                     f=torch.zeros(n_streams * self.B, dtype=torch.uint8, device=d), t0=0)
 
     def sample(self, n_samples: int, cond=None, seed: int = 1, n_streams: int = 1, init=None, final=None,
-               out=None, stream=None):
+               out=None, stream=None, noalloc: bool = False):
         """Draw n_samples per utterance; returns the [n_streams][n_samples] uint16 tensor.
-        ``final`` (a dict from new_state) receives the state after the last sample."""
+        ``final`` (a dict from new_state) receives the state after the last sample.
+        ``noalloc``: call wavernn_sample_noalloc (the library's per-device workspace,
+        no device allocation; ``out`` must then be given)."""
         import torch
         if out is None:
+            if noalloc:
+                raise ValueError("sample(noalloc=True) needs a preallocated out tensor")
             out = torch.empty(n_streams, n_samples, dtype=torch.uint16, device="cuda")
         n_frames = 0 if cond is None else cond.shape[1]
         si, sf = self._state(init), self._state(final)
-        _check(lib().wavernn_sample(self._h, n_streams, n_samples, _ptr(cond), n_frames, seed,
-                                    None if si is None else ctypes.byref(si), _ptr(out),
-                                    None if sf is None else ctypes.byref(sf), _stream(stream)))
+        fn = lib().wavernn_sample_noalloc if noalloc else lib().wavernn_sample
+        _check(fn(self._h, n_streams, n_samples, _ptr(cond), n_frames, seed,
+                  None if si is None else ctypes.byref(si), _ptr(out),
+                  None if sf is None else ctypes.byref(sf), _stream(stream)))
         if final is not None:
             final["t0"] = (init["t0"] if init is not None else 0) + n_samples
         return out
