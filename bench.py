@@ -29,6 +29,9 @@ def weight_bytes_per_step(w: dict) -> int:
     """Algorithmic bytes one sampling step must read: every weight once (bf16)."""
     H = w["H"]
     Hh = H // 2
+    if w.get("fused"):                   # R, four Q x Q first layers, four 32 x Q nibble layers
+        Q = H // 4
+        return 2 * (3 * H * H + 4 * Q * Q + 4 * 32 * Q)
     nR = int((w["R"] != 0).sum()) if w.get("mask") is not None else 3 * H * H
     n = nR + 2 * (Hh * Hh + 256 * Hh)
     if w.get("Wx") is not None:          # subscale context projection
@@ -39,7 +42,7 @@ def weight_bytes_per_step(w: dict) -> int:
 
 # kernel that serves each path of wavernn_model_path
 KERNEL_OF = {"persistent": "wr_persist_kernel", "block-sparse": "wr_sparse_kernel", "batched": "wr_batch_kernel",
-             "single-workgroup": "wr_small_kernel", "concurrent": "wr_persist_kernel"}
+             "single-workgroup": "wr_small_kernel", "concurrent": "wr_persist_kernel", "fused": "wr_fused_kernel"}
 
 
 def kernel_source_digest() -> str:
@@ -74,6 +77,21 @@ def cpu_baseline(w: dict, T: int, feat, budget_s: float = 12.0) -> dict:
     """The oracle as it stands, single-threaded on the host, on a bounded prefix."""
     import numpy as np
     from oracle import oracle
+    if w.get("fused"):
+        keys = ("R", "I", "b", "O1", "b1", "O2", "b2", "Wc")
+        d = {k: (None if w.get(k) is None else oracle.bf16_round(w[k])) for k in keys}
+        d.update(H=w["H"], F=w["F"])
+        run = lambda n: oracle.fused_run(d, 1, n, feat=feat[:1], seed=1, frame_len=w["frame_len"])
+        t = time.perf_counter()
+        run(48)
+        per = (time.perf_counter() - t) / 48
+        n = int(max(48, min(T, budget_s / max(per, 1e-9)))) // 2 * 2
+        t = time.perf_counter()
+        run(n)
+        dt = time.perf_counter() - t
+        return {"value": round(n / dt, 2), "unit": "samples/s", "cores": 1, "host_cores": os.cpu_count(),
+                "kind": "oracle",
+                "sample": f"first {n} of the {T} samples of one utterance, single-threaded C oracle (gcc -O2)"}
     W = oracle.Weights.from_dict(w, bf16=w.get("bf16", False))
     B = w.get("B", 1)                                    # subscale: whole rows of B samples
     n0 = 48 // B * B or B
@@ -107,6 +125,13 @@ PHASES = {
                 (9, "owned vectors' fine partials summed"), (10, "f_t drawn (end of step)")],
 }
 PHASES["block-sparse"] = PHASES["persistent"]
+PHASES["fused"] = [(1, "coarse gates (last f of both sub-tensors) done, own y_c slice published"),
+                   (3, "coarse MLPs: 64 partial nibble logits published"),
+                   (16, "partials of all heads summed, 4 coarse nibbles drawn (draw wave)"),
+                   (5, "barrier: coarse bytes known to all waves"),
+                   (6, "fine gates (own coarse byte) done, own y_f slice published"),
+                   (8, "fine MLPs: partial nibble logits published"),
+                   (18, "4 fine nibbles drawn (draw wave)"), (10, "next step's coarse gate words received (end of step)")]
 
 
 def phases(m, w, path: str, S: int, feat, n_steps: int) -> dict:
@@ -172,7 +197,7 @@ def main() -> int:
         return 0
     w = synth.preset(args.config)
     S, T = w["streams"], args.samples or w["samples"]
-    r_format = {None: "dense", (4, 4): "bsr4x4", (16, 1): "bsr16x1"}[w["block"]]
+    r_format = {None: "dense", (4, 4): "bsr4x4", (16, 1): "bsr16x1"}[w.get("block")]
     m = wavernn.Model(w, dtype="bf16" if w["bf16"] else "f32", r_format=r_format, max_streams=S)
     path, grid, block = m.path(S)
     feat_np = synth.features(S, T, per_stream_seed=S > 1)
@@ -206,12 +231,12 @@ def main() -> int:
     m.device_status()
     call_ms = [a.elapsed_time(b) for a, b in evs]
     # synchronization floor: the same grid and exchanged words per step, no arithmetic
-    floor_us = m.sync_floor(T // w["B"]) if path in ("persistent", "block-sparse") else None
+    floor_us = m.sync_floor(T // w["B"]) if path in ("persistent", "block-sparse", "fused") else None
     ms = float(np.mean(call_ms))
     samples = S * T
     value = samples * args.steps / wall
     F, A = w.get("F", -1), w.get("A", 0)               # subscale horizon and lead: (B - 1)(F + 1 + A) more steps
-    steps_per_launch = T // w["B"] + ((w["B"] - 1) * (F + 1 + A) if F >= 0 else 0)
+    steps_per_launch = T // w["B"] + ((w["B"] - 1) * (F + 1 + A) if F >= 0 else 0)   # fused 2x: T / 2 + F + 1
     us_per_sample_step = ms * 1000.0 / steps_per_launch
     wb = weight_bytes_per_step(w)
     achieved = wb * steps_per_launch / (ms / 1000.0) / 1e9

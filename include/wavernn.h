@@ -91,6 +91,16 @@ typedef struct {
                             the step's critical chain (Sec. 4.2: the conditioning runs ahead of
                             the lane it feeds).  The samples drawn do not depend on A.
                             Currently switched off: create returns E_UNSUPPORTED for A > 0. */
+  int32_t fused;          /* 1 = Fused Subscale WaveRNN 2x (Sec. 4.4): the two sub-tensors of a
+                            Subscale 2x model share one WaveRNN by splitting its state into
+                            quarters (units [0, H/4) coarse of sub-tensor 0, [H/4, H/2) coarse of
+                            sub-tensor 1, then their fine quarters), each byte is drawn as two
+                            4-bit nibbles from 16-way softmaxes (8 per step), and sub-tensor 1
+                            runs future_horizon + 1 steps behind sub-tensor 0 (the paper uses 2).
+                            Needs subscale = 2, ctx_dim = 0, context_lead = 0, future_horizon
+                            >= 0, dense bf16 R and an H the batch-1 kernel serves (a multiple of
+                            128 up to 896).  Sample 2 i + s of an utterance is position i of
+                            sub-tensor s; a call takes n_samples / 2 + F + 1 steps.  0 = plain. */
 } wavernn_config;
 
 /* Host fp32 weights.  Shapes (H hidden, Hh = H/2, V = 256 classes):
@@ -99,7 +109,14 @@ typedef struct {
  *   b [3][H], W_cond [3H][Dc], W_ctx [3H][Dx],
  *   O1 [Hh][Hh], b1 [Hh], O2 [V][Hh], b2 [V] (coarse head, Eq. 2),
  *   O3 [Hh][Hh], b3 [Hh], O4 [V][Hh], b4 [V] (fine head).
- * For BSR formats, entries of R outside kept blocks are ignored. */
+ * For BSR formats, entries of R outside kept blocks are ignored.
+ * Fused 2x models (Q = H/4) take instead:
+ *   I [3][H][6] columns (c0, f0, c1, f1) of each sub-tensor's last sample, then
+ *     c0_t, c1_t of this step; the coarse half reads columns 0-3 only, the fine
+ *     quarter of sub-tensor s columns 0-3 and 4 + s (the others are ignored);
+ *   O1 [4][Q][Q], b1 [4][Q]: first layer of head k = 2 level + s (level 0 coarse,
+ *     1 fine) on quarter k of the state; O2 [4][2][16][Q], b2 [4][2][16]: its
+ *     high-nibble and low-nibble logits; O3, b3, O4, b4 are unused (may be NULL). */
 typedef struct {
   const float* R;
   const uint8_t* R_block_mask;
@@ -113,6 +130,8 @@ typedef struct {
 /* Recurrent state of S utterances x B lanes, device memory:
  * h [S*B][H] fp32, c_prev / f_prev [S*B] bytes of the previous sample,
  * t0 = absolute index of the next sample (B = 1 only; 0 otherwise).
+ * Fused 2x models: h [S][H] (one state per utterance), c_prev / f_prev [2S]
+ * the last sample of sub-tensors 0 and 1 of each utterance, t0 = 0.
  * Default initial state: h = 0, c_prev = 128, f_prev = 0, t0 = 0. */
 typedef struct {
   float* h;
@@ -174,7 +193,9 @@ wavernn_status wavernn_sample_noalloc(wavernn_model* m, int32_t n_streams, int64
  * runs on target_dev [n_streams][n_samples] instead of drawn samples.  Writes
  * the pre-softmax logits logits_c_dev / logits_f_dev [n_streams][n_samples][256]
  * and nll_dev [n_streams][n_samples] = -log P(c_t) - log P(f_t | c_t) in nats;
- * each output pointer may be NULL.  Initial state as in wavernn_sample.
+ * each output pointer may be NULL.  Fused 2x models write 32 logits per
+ * sample and byte instead of 256 (high nibble 16, then low nibble 16), and
+ * the NLL is the sum over the sample's four nibbles.  Initial state as in wavernn_sample.
  * n_samples = 0 is valid (target_dev may then be NULL): nothing is launched. */
 wavernn_status wavernn_score_teacher_forced(wavernn_model* m, int32_t n_streams, int64_t n_samples,
                                             const float* cond_dev, int64_t n_frames, const uint16_t* target_dev,
@@ -198,7 +219,8 @@ wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t
  * block-sparse R (Sec. 3.2; one launch per stream), 4 concurrent persistent
  * (2 to 4 streams of a dense model whose grids fit the device together: one
  * batch-1 launch per stream on internal streams forked from and joined back
- * into the caller's stream; bit-identical to path 1).
+ * into the caller's stream; bit-identical to path 1), 5 fused 2x persistent
+ * (Sec. 4.4; one launch per stream).
  * Fills *grid and *block with the launch shape of one launch; -1 for a null
  * model. */
 int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* grid, int32_t* block);

@@ -60,6 +60,8 @@ struct PersistArgs {
   u64 limit;                // wait limit in 100 MHz ticks
   u64* trace;               // [trace_steps][WR_TRACE_SLOTS] phase timestamps or null
   int64_t trace_steps;
+  int F;                    // fused 2x model: future horizon (sub-tensor 1 runs F + 1 steps behind)
+  int64_t rows;             // fused 2x model: positions per sub-tensor (samples / 2)
 };
 
 struct BatchArgs {
@@ -111,4 +113,5 @@ const void* wr_cond_kernel_ptr();
 const void* wr_batch_kernel_ptr(int KH, bool ctx, int L, bool lag);   // null if no instantiation (KH, L vectors
                                                                       // per group, lag: a future-horizon schedule)
 const void* wr_fill_kernel_ptr();
+const void* wr_fused_kernel_ptr(int KH);     // null if no instantiation
 const void* wr_floor_kernel_ptr();

@@ -50,7 +50,7 @@ float bf2f(uint16_t b) {
 }
 
 enum Path { PATH_SMALL = 0, PATH_PERSIST = 1, PATH_BATCHED = 2 };
-constexpr int PATH_SPARSE_ID = 3, PATH_CONCURRENT_ID = 4;   // wavernn_model_path's ids of the variants
+constexpr int PATH_SPARSE_ID = 3, PATH_CONCURRENT_ID = 4, PATH_FUSED_ID = 5;   // wavernn_model_path's ids of the variants
 #define WR_FAN 4   // concurrent batch-1 launches: the caller's stream and 3 internal ones (HIP's default
                    // of 4 hardware queues gives each its own)
 
@@ -72,6 +72,7 @@ struct wavernn_model {
   PersistPlan plan;
   const void* pk = nullptr;          // kernel instantiation for the plan
   bool sparse = false;               // block-sparse units
+  bool fused = false;                // Fused Subscale WaveRNN 2x heads (Sec. 4.4)
   uint4 *d_hw = nullptr, *d_uw = nullptr, *d_ur = nullptr;
   float *d_I = nullptr, *d_bias = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr, *d_b4 = nullptr;
   float* d_cb = nullptr;             // [cb_cap][3H] bias + conditioning per frame
@@ -145,7 +146,7 @@ wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w
   if (c->cond_dim > 0 && c->frame_len <= 0) return fail(WAVERNN_E_INVALID, "frame_len must be > 0 with conditioning");
   if (c->subscale < 1 || c->subscale > 64) return fail(WAVERNN_E_INVALID, "subscale %d out of range", c->subscale);
   if (c->subscale == 1 && c->ctx_dim != 0) return fail(WAVERNN_E_INVALID, "ctx_dim must be 0 when subscale is 1");
-  if (c->subscale > 1 && (c->ctx_dim <= 0 || (c->ctx_dim & 1) || c->ctx_dim > 1024))
+  if (c->subscale > 1 && !c->fused && (c->ctx_dim <= 0 || (c->ctx_dim & 1) || c->ctx_dim > 1024))
     return fail(WAVERNN_E_INVALID, "ctx_dim must be even and in (0, 1024] with subscale");
   if (c->subscale > 1 && (c->future_horizon < -1 || c->future_horizon > 1024))
     return fail(WAVERNN_E_INVALID, "future_horizon %d out of [-1, 1024]", c->future_horizon);
@@ -160,7 +161,13 @@ wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w
   if (c->weight_dtype != WAVERNN_F32 && c->weight_dtype != WAVERNN_BF16) return fail(WAVERNN_E_INVALID, "bad weight_dtype");
   if (c->r_format < WAVERNN_R_DENSE || c->r_format > WAVERNN_R_BSR_16X1) return fail(WAVERNN_E_INVALID, "bad r_format");
   if (c->max_streams < 1 || c->max_streams > 64) return fail(WAVERNN_E_INVALID, "max_streams must be in [1, 64]");
-  if (!w->R || !w->I || !w->b || !w->O1 || !w->b1 || !w->O2 || !w->b2 || !w->O3 || !w->b3 || !w->O4 || !w->b4)
+  if (c->fused != 0 && c->fused != 1) return fail(WAVERNN_E_INVALID, "fused must be 0 or 1");
+  if (c->fused && (c->subscale != 2 || c->ctx_dim != 0 || c->future_horizon < 0 || c->context_lead != 0 ||
+                   c->r_format != WAVERNN_R_DENSE || c->hidden % 4))
+    return fail(WAVERNN_E_INVALID, "fused 2x: needs subscale 2, ctx_dim 0, future_horizon >= 0, context_lead 0, "
+                "dense R and hidden a multiple of 4");
+  if (!w->R || !w->I || !w->b || !w->O1 || !w->b1 || !w->O2 || !w->b2 ||
+      (!c->fused && (!w->O3 || !w->b3 || !w->O4 || !w->b4)))
     return fail(WAVERNN_E_INVALID, "a required weight array is null");
   if (c->cond_dim > 0 && !w->W_cond) return fail(WAVERNN_E_INVALID, "W_cond is null with cond_dim > 0");
   if (c->ctx_dim > 0 && !w->W_ctx) return fail(WAVERNN_E_INVALID, "W_ctx is null with ctx_dim > 0");
@@ -361,11 +368,10 @@ wavernn_status build_fanout(wavernn_model* m) {
   return WAVERNN_OK;
 }
 
-wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
+// Dense unit workgroups of the persistent plan (R tiles in LDS and VGPRs).
+wavernn_status upload_dense_units(wavernn_model* m, const wavernn_weights* w) {
   const PersistPlan& P = m->plan;
-  const int H = P.H, Hh = P.Hh, KT = P.KT, KH = P.KH, UCT = P.UCT;
-  m->pk = wr_persist_kernel_ptr(KH);
-  if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no persistent kernel instantiation", H);
+  const int H = P.H, Hh = P.Hh, KT = P.KT, UCT = P.UCT;
   REff R{&m->cfg, w};
   auto Rm = [&](int r, int k) { return R(r, k); };
   // units: R row of row tile `tile` of a half, lane row r
@@ -392,9 +398,91 @@ wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
   }
   wavernn_status s;
   if ((s = m->upload(&m->d_uw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
-  if ((s = m->upload(&m->d_ur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
+  return m->upload(&m->d_ur, ur.data(), ur.size() * 2);
+}
+
+wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
+  const PersistPlan& P = m->plan;
+  m->pk = wr_persist_kernel_ptr(P.KH);
+  if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no persistent kernel instantiation", P.H);
+  wavernn_status s;
+  if ((s = upload_dense_units(m, w)) != WAVERNN_OK) return s;
   if ((s = upload_common(m, w)) != WAVERNN_OK) return s;
   return check_coresident(m, m->pk, P.grid, P.lds, "persistent");
+}
+
+// Fused Subscale WaveRNN 2x (Sec. 4.4): the dense units of the batch-1 plan,
+// fused heads (block-diagonal first layers and 64 nibble logits per half),
+// I* with its six columns masked per quarter.  Head j, wave w holds O1 / O3
+// rows 64 j + 16 (w % 4) over column chunk w / 4 (KH tiles), then class tile
+// w (< 4) of the 64 nibble logits over the head's 64 columns.
+wavernn_status build_fused(wavernn_model* m, const wavernn_weights* w) {
+  const wavernn_config& c = m->cfg;
+  PersistPlan& P = m->plan;
+  const int H = P.H, Hh = P.Hh, Q = Hh / 2, KH = P.KH, KO = P.KO;
+  m->pk = wr_fused_kernel_ptr(KH);
+  if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no fused kernel instantiation", H);
+  wavernn_status s;
+  if ((s = upload_dense_units(m, w)) != WAVERNN_OK) return s;
+  // first layer of the half at level lv (Hh x Hh, block diagonal) and its 64 nibble-logit rows
+  auto O1f = [&](int lv) {
+    return [=](int r, int k) {
+      return r / Q == k / Q ? w->O1[((size_t)(2 * lv + r / Q) * Q + r % Q) * Q + k % Q] : 0.0f;
+    };
+  };
+  auto O2f = [&](int lv) {
+    return [=](int v, int k) {   // v = 32 s + 16 part + nibble
+      const int sv = v / 32;
+      return sv == k / Q ? w->O2[((size_t)((2 * lv + sv) * 2 + (v / 16) % 2) * 16 + v % 16) * Q + k % Q] : 0.0f;
+    };
+  };
+  std::vector<uint16_t> hw((size_t)P.NH * 8 * P.hw_frags * 512, 0);
+  for (int j = 0; j < P.NH; ++j)
+    for (int wv = 0; wv < 8; ++wv) {
+      uint16_t* d = hw.data() + (size_t)(j * 8 + wv) * P.hw_frags * 512;
+      const int r0 = 64 * j + 16 * (wv % 4), k0 = 32 * (wv / 4) * KH;
+      auto rows = [&](int r) { return r0 + r; };
+      for (int i = 0; i < KH; ++i) {
+        frag(d + (size_t)i * 512, O1f(0), rows, k0 + 32 * i);
+        frag(d + (size_t)(KH + i) * 512, O1f(1), rows, k0 + 32 * i);
+      }
+      if (wv >= 4) continue;
+      auto cls = [&](int r) { return 16 * wv + r; };
+      for (int kt = 0; kt < KO; ++kt) {
+        frag(d + (size_t)(2 * KH + kt) * 512, O2f(0), cls, 64 * j + 32 * kt);
+        frag(d + (size_t)(2 * KH + KO + kt) * 512, O2f(1), cls, 64 * j + 32 * kt);
+      }
+    }
+  if ((s = m->upload(&m->d_hw, hw.data(), hw.size() * 2)) != WAVERNN_OK) return s;
+  Rounder rd{true};
+  std::vector<float> Iv((size_t)18 * H), bv((size_t)3 * H);
+  for (int row = 0; row < 3 * H; ++row) {
+    const int i = row % H;
+    for (int q = 0; q < 6; ++q) {
+      const bool keep = q < 4 || (i >= Hh && q == 4 + (i - Hh) / Q);   // the I* mask per quarter
+      Iv[(size_t)row * 6 + q] = keep ? rd(w->I[(size_t)row * 6 + q]) : 0.0f;
+    }
+    bv[row] = rd(w->b[row]);
+  }
+  std::vector<float> b1(2 * Hh), b2(128);
+  for (int k = 0; k < 2 * Hh; ++k) b1[k] = rd(w->b1[k]);   // [level][s][Q]: coarse half, then fine half
+  for (int v = 0; v < 128; ++v) b2[v] = rd(w->b2[v]);      // [level][s][part][16]
+  if ((s = m->upload(&m->d_I, Iv.data(), Iv.size() * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_bias, bv.data(), bv.size() * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_b1, b1.data(), b1.size() * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_b2, b2.data(), b2.size() * 4)) != WAVERNN_OK) return s;
+  m->d_b3 = m->d_b1 + Hh;
+  m->d_b4 = m->d_b2 + 64;
+  if (c.cond_dim > 0) {
+    std::vector<float> wc((size_t)3 * H * c.cond_dim);
+    for (size_t i = 0; i < wc.size(); ++i) wc[i] = rd(w->W_cond[i]);
+    if ((s = m->upload(&m->d_Wc, wc.data(), wc.size() * 4)) != WAVERNN_OK) return s;
+  }
+  m->cb_cap = c.cond_dim > 0 ? 1024 : 1;
+  if ((s = m->alloc(&m->d_cb, (size_t)m->cb_cap * 3 * H * 4)) != WAVERNN_OK) return s;
+  if ((s = m->alloc(&m->d_xc, (size_t)(P.x_words + 1) / 2 * 8)) != WAVERNN_OK) return s;
+  m->fused = true;
+  return check_coresident(m, m->pk, P.grid, P.lds, "fused");
 }
 
 // Block-sparse R (Sec. 3.2): the kept entries of every row as records of the
@@ -602,6 +690,7 @@ wavernn_status validate_run(wavernn_model* m, const RunIO& io) {
   const int64_t t0 = io.init ? io.init->t0 : 0;
   if (t0 < 0) return fail(WAVERNN_E_INVALID, "negative t0");
   if (c.subscale > 1 && t0 != 0) return fail(WAVERNN_E_INVALID, "t0 must be 0 with subscale");
+  if (c.fused && io.T > ((int64_t)1 << 30)) return fail(WAVERNN_E_INVALID, "n_samples above 2^30 for a fused model");
   if (io.init && (!io.init->h || !io.init->c_prev || !io.init->f_prev))
     return fail(WAVERNN_E_INVALID, "init state has a null pointer");
   if (io.fin && (!io.fin->h || !io.fin->c_prev || !io.fin->f_prev))
@@ -668,17 +757,30 @@ wavernn_status launch_persist_one(wavernn_model* m, const RunIO& io, int s, xw* 
   a.cb = cb;
   a.n_cb = n_cb;
   a.frame_len = Dc > 0 ? frame_len : (1 << 30);
-  a.T = io.T;
+  // fused 2x: N / 2 positions per sub-tensor, sub-tensor 1 F + 1 steps behind;
+  // 32 logits per sample and byte; two last samples per utterance
+  const int nz = m->fused ? 32 : 256, nb = m->fused ? 2 : 1;
+  a.F = m->fused ? m->cfg.future_horizon : 0;
+  a.rows = m->fused ? io.T / 2 : io.T;
+  a.T = m->fused ? a.rows + a.F + 1 : io.T;
   a.t0 = io.init ? io.init->t0 : 0;
   a.seed = io.seed;
   a.stream_id = (uint64_t)s;
   a.target = io.target ? io.target + (size_t)s * io.T : nullptr;
   a.out = io.out ? io.out + (size_t)s * io.T : nullptr;
-  a.zc_out = io.zc ? io.zc + (size_t)s * io.T * 256 : nullptr;
-  a.zf_out = io.zf ? io.zf + (size_t)s * io.T * 256 : nullptr;
+  a.zc_out = io.zc ? io.zc + (size_t)s * io.T * nz : nullptr;
+  a.zf_out = io.zf ? io.zf + (size_t)s * io.T * nz : nullptr;
   a.nll_out = io.nll ? io.nll + (size_t)s * io.T : nullptr;
-  if (io.init) { a.h_in = io.init->h + (size_t)s * H; a.c_in = io.init->c_prev + s; a.f_in = io.init->f_prev + s; }
-  if (io.fin) { a.h_out = io.fin->h + (size_t)s * H; a.c_out = io.fin->c_prev + s; a.f_out = io.fin->f_prev + s; }
+  if (io.init) {
+    a.h_in = io.init->h + (size_t)s * H;
+    a.c_in = io.init->c_prev + (size_t)nb * s;
+    a.f_in = io.init->f_prev + (size_t)nb * s;
+  }
+  if (io.fin) {
+    a.h_out = io.fin->h + (size_t)s * H;
+    a.c_out = io.fin->c_prev + (size_t)nb * s;
+    a.f_out = io.fin->f_prev + (size_t)nb * s;
+  }
   a.xc = xc;
   a.err = m->d_err;
   a.limit = kWaitTicks;
@@ -847,6 +949,7 @@ wavernn_status run(wavernn_model* m, RunIO& io, bool noalloc = false) {
   if (dev != m->device) return fail(WAVERNN_E_INVALID, "model lives on device %d, current device is %d", m->device, dev);
   if (noalloc && (s = scratch_of(dev, &io.ws, &io.ws_cap)) != WAVERNN_OK) return s;
   if (m->path == PATH_SMALL) return run_small(m, io);
+  if (m->fused) return run_persist(m, io);   // one fused launch per utterance
   if (m->path == PATH_PERSIST) {
     if (io.S > 1 && io.S <= m->nfan) return run_fanout(m, io);
     return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);
@@ -906,7 +1009,18 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
   const SmallLayout L = small_layout(H);
   const bool small_fits = (size_t)L.total_floats * 4 + 256 <= 160 * 1024;
   const int B = cfg->subscale;
-  if (B > 1) {
+  if (cfg->fused) {
+    // Fused Subscale WaveRNN 2x (Sec. 4.4): the batch-1 persistent structure
+    // with fused heads, one launch per utterance
+    if (cfg->weight_dtype != WAVERNN_BF16)
+      s = fail(WAVERNN_E_UNSUPPORTED, "fused 2x sampling needs bf16 weights");
+    else if (!fused_plan(H, &m->plan))
+      s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no fused plan (need a multiple of 128 up to 896)", H);
+    else {
+      m->path = PATH_PERSIST;
+      s = build_fused(m, w);
+    }
+  } else if (B > 1) {
     // Subscale (Sec. 4): the B lanes of each utterance are vectors of the
     // batched kernel; its unit workgroups add the context projection.
     if (!((B % 8 == 0) || (4 % B == 0)) || cfg->ctx_dim % 32 || cfg->ctx_dim > 256)
@@ -1028,6 +1142,7 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
   } else if (m->path == PATH_PERSIST) {
     g = m->plan.grid, b = WR_THREADS;
     if (m->sparse) path = PATH_SPARSE_ID;
+    if (m->fused) path = PATH_FUSED_ID;
   }
   if (grid) *grid = g;
   if (block) *block = b;

@@ -152,6 +152,31 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   return P->lds <= 160 * 1024;
 }
 
+// Fused Subscale WaveRNN 2x (Sec. 4.4) on the persistent kernel: the batch-1
+// plan with 64 partial logits per head and half (high and low nibble of both
+// sub-tensors' bytes) instead of 256.  Head fragments per wave: O1 [KH],
+// O3 [KH] (block diagonal over the two quarters of a half), then the
+// wave's class tile of O2 and of O4 over the head's KO column tiles.
+WR_HD inline bool fused_plan(int H, PersistPlan* P) {
+  if (!persist_plan(H, P)) return false;
+  P->hw_frags = 2 * P->KH + 2 * P->KO;
+  // head LDS: y_c and y_f operand images (KT fragments each), relu image (KO),
+  // first-layer partials [2][64], misc [16], uniforms [2][64][8], targets [2][64][2]
+  P->lds_h = (2 * P->KT + P->KO) * WR_FRAG + 4 * (2 * 64 + 16 + 2 * 64 * 8 + 2 * 64 * 2);
+  int o = 0;
+  auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
+  P->x_yc = take(P->Hh);
+  P->x_yf = take(P->Hh);
+  P->x_ga = take(3 * P->Hh);
+  P->x_gf = take(3 * P->Hh);
+  P->x_ps = 64;
+  P->x_pc = take(P->NH * P->x_ps);
+  P->x_pf = take(P->NH * P->x_ps);
+  P->x_words = o;
+  P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
+  return P->lds <= 160 * 1024;
+}
+
 // ---------------------------------------------------------------------------
 // Block-sparse R (Sparse WaveRNN, Sec. 3.2) on the persistent kernel.
 //

@@ -65,6 +65,29 @@ def make_weights(H: int, seed: int = 0, cond_dim: int = 0, B: int = 1, ctx_dim: 
     return w
 
 
+def make_fused_weights(H: int, F: int = 2, seed: int = 0, cond_dim: int = 0) -> dict:
+    """Weights of a Fused Subscale WaveRNN 2x (Sec. 4.4) with H units (four
+    quarters of Q = H/4), N(0, 1/fan_in): R [3][H][H], I [3][H][6] (last (c, f)
+    of both sub-tensors, then their current coarse bytes), b [3][H], one MLP per
+    (level, sub-tensor): O1 [4][Q][Q], b1 [4][Q], O2 [4][2][16][Q] (high and low
+    nibble), b2 [4][2][16]; optional W_cond [3H][Dc].  The I columns a unit
+    must ignore (the mask) hold random values on purpose."""
+    assert H % 4 == 0
+    Q = H // 4
+    rng = np.random.default_rng(seed)
+    w = dict(H=H, B=2, F=F, fused=True, frame_len=FRAME_LEN, block=None, mask=None)
+    w["R"] = _normal(rng, (3, H, H), H)
+    w["I"] = _normal(rng, (3, H, 6), 5)
+    w["b"] = _normal(rng, (3, H), H)
+    w["O1"] = _normal(rng, (4, Q, Q), Q)
+    w["b1"] = _normal(rng, (4, Q), Q)
+    w["O2"] = _normal(rng, (4, 2, 16, Q), Q)
+    w["b2"] = _normal(rng, (4, 2, 16), Q)
+    w["Wc"] = _normal(rng, (3 * H, cond_dim), cond_dim) if cond_dim else None
+    w["Wx"] = None
+    return w
+
+
 def features(S: int, T: int, cond_dim: int = COND_DIM, seed: int = 2, frame_len: int = FRAME_LEN,
              per_stream_seed: bool = False) -> np.ndarray:
     """Conditioning frames [S][ceil(T/frame_len)][cond_dim] ~N(0, 1)."""
@@ -117,7 +140,17 @@ HORIZON = {"subscale16_h4": 4, "subscale16_h4a1": 4}
 LEAD = {"subscale16_h4a1": 1}   # the lead is switched off at create (E_UNSUPPORTED) for now
 
 
+# Fused Subscale WaveRNN 2x (Sec. 4.4): WaveRNN-896 with its state in quarters,
+# F = 2 as the paper uses, 24,000 samples (12,000 positions per sub-tensor).
+FUSED = {"fused896": (896, 2, COND_DIM, 1, 24000)}
+
+
 def preset(name: str, seed: int = 0) -> dict:
+    if name in FUSED:
+        H, F, Dc, S, T = FUSED[name]
+        w = make_fused_weights(H, F=F, seed=seed, cond_dim=Dc)
+        w.update(name=name, bf16=True, streams=S, samples=T)
+        return w
     H, Dc, B, Dx, block, bf16, S, T = PRESETS[name]
     w = make_weights(H, seed=seed, cond_dim=Dc, B=B, ctx_dim=Dx, block=block,
                      density=0.04 if block else 1.0)

@@ -18,7 +18,7 @@ _lib = None
 OK, E_INVALID, E_UNSUPPORTED, E_OOM, E_HIP, E_DEVICE = range(6)
 F32, BF16 = 0, 1
 R_DENSE, R_BSR_4X4, R_BSR_16X1 = 0, 1, 2
-PATHS = {0: "single-workgroup", 1: "persistent", 2: "batched", 3: "block-sparse", 4: "concurrent"}
+PATHS = {0: "single-workgroup", 1: "persistent", 2: "batched", 3: "block-sparse", 4: "concurrent", 5: "fused"}
 
 
 class WaveRNNError(RuntimeError):
@@ -30,7 +30,7 @@ class WaveRNNError(RuntimeError):
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("hidden", "cond_dim", "frame_len", "subscale", "ctx_dim",
                                                "weight_dtype", "r_format", "max_streams", "future_horizon",
-                                               "context_lead")]
+                                               "context_lead", "fused")]
 
 
 _FP = ctypes.POINTER(ctypes.c_float)
@@ -109,7 +109,8 @@ class Model:
     R, I, b, O1, b1, O2, b2, O3, b3, O4, b4, optional Wc, Wx, mask) plus H,
     frame_len, B and, for subscale, F (future horizon; -1 or absent: lockstep rows) and A (steps by which
     the context is formed ahead, with F only; absent: 0).  dtype 'bf16' or 'f32' is the weight storage; r_format is
-    'dense', 'bsr4x4' or 'bsr16x1'."""
+    'dense', 'bsr4x4' or 'bsr16x1'.  A Fused Subscale 2x model (``fused`` true) has B = 2, F, I [3][H][6],
+    O1 [4][Q][Q], b1 [4][Q], O2 [4][2][16][Q], b2 [4][2][16] and no O3, b3, O4, b4."""
 
     def __init__(self, w: dict, dtype: str = "bf16", r_format: str = "dense", max_streams: int = 1):
         L = lib()
@@ -120,11 +121,12 @@ class Model:
         self.B = int(w.get("B", 1))
         self.F = int(w.get("F", -1))
         self.A = int(w.get("A", 0))
+        self.fused = bool(w.get("fused", False))
         cfg = Config(self.H, self.cond_dim, self.frame_len, self.B, 0 if Wx is None else Wx.shape[1],
                      {"bf16": BF16, "f32": F32}[dtype],
                      {"dense": R_DENSE, "bsr4x4": R_BSR_4X4, "bsr16x1": R_BSR_16X1}[r_format], max_streams,
-                     self.F, self.A)
-        keep = {k: _f32(w[k]) for k in ("R", "I", "b", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")}
+                     self.F, self.A, int(self.fused))
+        keep = {k: _f32(w.get(k)) for k in ("R", "I", "b", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")}
         mask = None if w.get("mask") is None else np.ascontiguousarray(w["mask"], dtype=np.uint8)
         fp = lambda a: None if a is None else a.ctypes.data_as(_FP)
         ws = Weights(fp(keep["R"]), None if mask is None else mask.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
@@ -163,9 +165,11 @@ class Model:
         return State(st["h"].data_ptr(), st["c"].data_ptr(), st["f"].data_ptr(), int(st.get("t0", 0)))
 
     def new_state(self, n_streams: int = 1):
+        """Default state: h [S B][H] (fused: [S][H]), last bytes [S B] (fused: [2 S])."""
         import torch
         d = torch.device("cuda")
-        return dict(h=torch.zeros(n_streams * self.B, self.H, device=d),
+        nh = n_streams if self.fused else n_streams * self.B
+        return dict(h=torch.zeros(nh, self.H, device=d),
                     c=torch.full((n_streams * self.B,), 128, dtype=torch.uint8, device=d),
                     f=torch.zeros(n_streams * self.B, dtype=torch.uint8, device=d), t0=0)
 
@@ -191,11 +195,12 @@ class Model:
         return out
 
     def score(self, target, cond=None, init=None, logits: bool = True, nll: bool = True, stream=None):
-        """Teacher-forced logits [S][T][256] x2 and NLL [S][T] (nats) on target [S][T] uint16."""
+        """Teacher-forced logits [S][T][256] x2 (fused: [S][T][32]) and NLL [S][T] (nats) on target [S][T] uint16."""
         import torch
         S, T = target.shape
-        zc = torch.empty(S, T, 256, device="cuda") if logits else None
-        zf = torch.empty(S, T, 256, device="cuda") if logits else None
+        nz = 32 if self.fused else 256
+        zc = torch.empty(S, T, nz, device="cuda") if logits else None
+        zf = torch.empty(S, T, nz, device="cuda") if logits else None
         nl = torch.empty(S, T, device="cuda") if nll else None
         n_frames = 0 if cond is None else cond.shape[1]
         si = self._state(init)

@@ -58,6 +58,11 @@ def _weights(H=64):
     (dict(subscale=16, ctx_dim=256, future_horizon=2, context_lead=4), "context_lead"),
     (dict(subscale=16, ctx_dim=256, future_horizon=-1, context_lead=1), "context_lead"),
     (dict(subscale=16, ctx_dim=256, future_horizon=4, context_lead=1), "switched off"),
+    (dict(fused=1, subscale=16, ctx_dim=0, future_horizon=2), "fused 2x"),
+    (dict(fused=1, subscale=2, ctx_dim=32, future_horizon=2), "fused 2x"),
+    (dict(fused=1, subscale=2, ctx_dim=0, future_horizon=-1), "fused 2x"),
+    (dict(fused=1, subscale=2, ctx_dim=0, future_horizon=2, r_format=W.R_BSR_4X4), "fused 2x"),
+    (dict(fused=2), "fused must be"),
 ])
 def test_create_rejects_bad_config_before_touching_the_device(bad, msg):
     L = W.lib()
@@ -82,3 +87,22 @@ def test_null_arguments_are_rejected():
     assert L.wavernn_score_teacher_forced(None, 1, 10, None, 0, None, None, None, None, None, None) == W.E_INVALID
     assert L.wavernn_debug_uniforms(1, 0, 0, -1, None, None) == W.E_INVALID
     L.wavernn_destroy(None)
+
+
+def test_fused_config_passes_host_validation():
+    """A well-formed Fused Subscale 2x config (I with 6 columns, no O3/O4) gets
+    past every host check and stops only where the device is needed."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a device is present: create would build the model")
+    L = W.lib()
+    w = synth.make_fused_weights(128, F=2)
+    keep = {k: np.ascontiguousarray(w[k], np.float32) for k in ("R", "I", "b", "O1", "b1", "O2", "b2")}
+    fp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    ws = W.Weights(fp(keep["R"]), None, fp(keep["I"]), fp(keep["b"]), None, None,
+                   fp(keep["O1"]), fp(keep["b1"]), fp(keep["O2"]), fp(keep["b2"]), None, None, None, None)
+    h = ctypes.c_void_p()
+    cfg = _cfg(hidden=128, subscale=2, ctx_dim=0, future_horizon=2, fused=1, weight_dtype=W.BF16)
+    st = L.wavernn_create(ctypes.byref(cfg), ctypes.byref(ws), ctypes.byref(h))
+    assert st == W.E_HIP, L.wavernn_last_error().decode()
+    assert not h.value
