@@ -117,6 +117,31 @@ typedef struct {
  *   O1 [4][Q][Q], b1 [4][Q]: first layer of head k = 2 level + s (level 0 coarse,
  *     1 fine) on quarter k of the state; O2 [4][2][16][Q], b2 [4][2][16]: its
  *     high-nibble and low-nibble logits; O3, b3, O4, b4 are unused (may be NULL). */
+/* The masked dilated 1-D CNN that conditions a Subscale WaveRNN on the
+ * previous sub-tensors (Sec. 4.1; shape in Sec. 5: ten layers, kernel size 3,
+ * 384 convolution channels, 768 residual channels, five stages of increasing
+ * dilation).  It runs over rows k (blocks of B samples).  The input of row k
+ * for sub-tensor s is the (c, f) pair, scaled as every byte, of each
+ * sub-tensor z < s of that row (2B channels, zero for z >= s and outside the
+ * utterance):  r = Win x + bin;  then for each layer l (dilation
+ * d = 2^(l mod 5)), with the mask keeping the future taps only,
+ *   a = relu(Wc_l [r_k ; r_k+d ; r_k+2d] + bc_l)  (rows past the end: zero),
+ *   r = r + (Wo_l a + bo_l);
+ * and the context vector of row k is Wp r + bp (Dx = the model's ctx_dim).
+ * Ten layers see rows k .. k + 124.  Sub-tensor s at position i is
+ * conditioned on its vector of row i, through W_ctx as the window context is.
+ * Res/conv channels and Dx must be multiples of 128; weights are rounded to
+ * bf16 like the model's. */
+typedef struct {
+  int32_t res_channels;    /* Rc */
+  int32_t conv_channels;   /* Cc */
+  int32_t layers;          /* >= 0 */
+  const float *Win, *bin;  /* [Rc][2B], [Rc] */
+  const float *Wc, *bc;    /* [layers][Cc][3][Rc] (taps k, k + d, k + 2d), [layers][Cc] */
+  const float *Wo, *bo;    /* [layers][Rc][Cc], [layers][Rc] */
+  const float *Wp, *bp;    /* [Dx][Rc], [Dx] */
+} wavernn_ctx_cnn;
+
 typedef struct {
   const float* R;
   const uint8_t* R_block_mask;
@@ -125,6 +150,8 @@ typedef struct {
   const float* W_cond;
   const float* W_ctx;
   const float *O1, *b1, *O2, *b2, *O3, *b3, *O4, *b4;
+  const wavernn_ctx_cnn* ctx_cnn;   /* subscale with a future horizon only: the conditioning CNN that
+                                       replaces the window context; NULL = window context */
 } wavernn_weights;
 
 /* Recurrent state of S utterances x B lanes, device memory:
@@ -247,6 +274,18 @@ wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t 
  * Errors: E_INVALID (arguments), E_UNSUPPORTED (other paths), E_HIP,
  * E_DEVICE (a bounded wait expired). */
 wavernn_status wavernn_debug_sync_floor(wavernn_model* m, int64_t n_steps, double* us_per_step, void* stream);
+
+/* The conditioning CNN of a model created with ctx_cnn (Sec. 4.1) over whole
+ * utterances: out_dev [n_streams][B][n_samples / B][Dx] fp32 receives the
+ * context vector of every sub-tensor s and row k from the samples seq_dev
+ * [n_streams][n_samples] (n_samples a multiple of B).  Every layer runs as one
+ * matrix-core GEMM over all rows of all sub-tensors, activations at fp32
+ * accuracy (bf16 high and low parts) against the bf16 weights.  Scratch
+ * activations are the model's (grown on demand: 4 (Rc + Cc + 32) bytes per
+ * row of every sub-tensor).  Errors: E_INVALID (no CNN, bad sizes), E_OOM,
+ * E_HIP. */
+wavernn_status wavernn_ctx_cnn_run(wavernn_model* m, int32_t n_streams, int64_t n_samples, const uint16_t* seq_dev,
+                                   float* out_dev, void* stream);
 
 /* Description of the last error on this thread ("" if none). */
 const char* wavernn_last_error(void);

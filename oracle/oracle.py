@@ -38,22 +38,23 @@ def build(force: bool = False) -> str:
     return _LIB_PATH
 
 
+class _Cnn(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "Rc", "Cc", "Dx", "layers")] + [
+        (n, ctypes.POINTER(ctypes.c_float)) for n in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")]
+
+
 class _Model(ctypes.Structure):
     _fields_ = [("H", ctypes.c_int32), ("Dc", ctypes.c_int32), ("frame_len", ctypes.c_int32),
                 ("B", ctypes.c_int32), ("Dx", ctypes.c_int32), ("F", ctypes.c_int32)] + [
         (n, ctypes.POINTER(ctypes.c_float))
-        for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")]
+        for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")] + [
+        ("cnn", ctypes.POINTER(_Cnn))]
 
 
 class _FusedModel(ctypes.Structure):
     _fields_ = [("H", ctypes.c_int32), ("F", ctypes.c_int32), ("Dc", ctypes.c_int32),
                 ("frame_len", ctypes.c_int32)] + [
         (n, ctypes.POINTER(ctypes.c_float)) for n in ("R", "I", "b", "Wc", "O1", "b1", "O2", "b2")]
-
-
-class _Cnn(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("B", "Rc", "Cc", "Dx", "layers")] + [
-        (n, ctypes.POINTER(ctypes.c_float)) for n in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")]
 
 
 def lib():
@@ -85,6 +86,8 @@ def load(path: str):
     L.orc_fused_run.argtypes = [ctypes.POINTER(_FusedModel), i32, i64, vp, i64, u64, vp, vp, vp, vp, vp, vp]
     L.orc_ctx_cnn.restype = ctypes.c_int
     L.orc_ctx_cnn.argtypes = [ctypes.POINTER(_Cnn), vp, i64, i32, vp]
+    L.orc_run_lanes.restype = ctypes.c_int
+    L.orc_run_lanes.argtypes = [ctypes.POINTER(_Model), i32, i64, vp, i64, vp, vp, vp, vp, vp, vp, vp, i32, i32]
     L.orc_run.restype = ctypes.c_int
     L.orc_run.argtypes = [ctypes.POINTER(_Model), i32, i64, i64, vp, i64, u64, vp, vp, vp, vp, vp,
                           vp, vp, vp]
@@ -162,6 +165,7 @@ class Weights:
     frame_len: int = 120
     B: int = 1
     F: int = -1          # subscale future horizon (Sec. 4.2); < 0: lockstep rows
+    cnn: dict | None = None   # conditioning network (ctx_cnn's keys), replaces the window context
 
     @staticmethod
     def from_dict(d: dict, bf16: bool = False) -> "Weights":
@@ -174,8 +178,27 @@ class Weights:
                 continue
             v = np.ascontiguousarray(v, dtype=np.float32)
             kw[k] = bf16_round(v) if bf16 else v.copy()
+        cnn = d.get("cnn")
+        if cnn is not None:
+            cnn = dict(cnn, **{k: (bf16_round(cnn[k]) if bf16 else np.ascontiguousarray(cnn[k], np.float32))
+                               for k in CNN_KEYS})
         return Weights(H=int(d["H"]), frame_len=int(d.get("frame_len", 120)), B=int(d.get("B", 1)),
-                       F=int(d.get("F", -1)), **kw)
+                       F=int(d.get("F", -1)), cnn=cnn, **kw)
+
+
+CNN_KEYS = ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")
+
+
+def _cnn(w: dict) -> _Cnn:
+    """The C view of a conditioning-network dict (arrays must stay alive with it)."""
+    keep = {k: np.ascontiguousarray(w[k], np.float32) for k in CNN_KEYS}
+    B, L = int(w["B"]), int(w["layers"])
+    Rc, Dx = keep["Win"].shape[0], keep["Wp"].shape[0]
+    Cc = keep["bc"].shape[1] if L > 0 else 1
+    fp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+    c = _Cnn(B, Rc, Cc, Dx, L, *[fp(keep[k]) for k in CNN_KEYS])
+    c._keep = keep
+    return c
 
 
 def _model(w: Weights):
@@ -193,6 +216,10 @@ def _model(w: Weights):
     m.F = w.F
     for n in ("R", "I", "b", "Wc", "Wx", "O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4"):
         setattr(m, n, fp(getattr(w, n)))
+    if w.cnn is not None:
+        c = _cnn(w.cnn)
+        m.cnn = ctypes.pointer(c)
+        m._cnn = c
     return m
 
 
@@ -233,6 +260,30 @@ def run(w: Weights, S: int, T: int, feat=None, seed: int = 1, target=None, h0=No
     return dict(out=out, h=h, c=c, f=f, zc=zc, zf=zf, nll=nl)
 
 
+def run_lanes(w: Weights, S: int, T: int, target, lanes, feat=None) -> dict:
+    """Teacher-forced run of the subscale lanes [lanes[0], lanes[1]) only (they are
+    independent given the target): dict(zc, zf [S][T][256], nll [S][T]) with the
+    other lanes' entries zero."""
+    B, H = w.B, w.H
+    h = np.zeros((S * B, H), np.float32)
+    c = np.full(S * B, 128, np.uint8)
+    f = np.zeros(S * B, np.uint8)
+    n_frames = 0
+    if feat is not None:
+        feat = np.ascontiguousarray(feat, np.float32)
+        n_frames = feat.shape[1]
+    tgt = np.ascontiguousarray(target, np.uint16)
+    zc = np.zeros((S, T, N_CLASSES), np.float32)
+    zf = np.zeros((S, T, N_CLASSES), np.float32)
+    nl = np.zeros((S, T), np.float64)
+    m = _model(w)
+    rc = lib().orc_run_lanes(ctypes.byref(m), S, T, _p(feat), n_frames, _p(tgt), _p(h), _p(c), _p(f), _p(zc), _p(zf),
+                             _p(nl), int(lanes[0]), int(lanes[1]))
+    if rc != 0:
+        raise ValueError("oracle rejected the inputs")
+    return dict(zc=zc, zf=zf, nll=nl, h=h)
+
+
 def fused_run(w: dict, S: int, N: int, feat=None, seed: int = 1, target=None, frame_len: int = 120) -> dict:
     """Fused Subscale WaveRNN 2x (Sec. 4.4): sample (target None) or teacher-force S
     utterances of N samples.  w: H, F and fp32 arrays R [3][H][H], I [3][H][6], b [3][H],
@@ -267,12 +318,8 @@ def ctx_cnn(w: dict, seq, s: int) -> np.ndarray:
     (Sec. 4.1, 5).  w: B, layers and fp32 arrays Win [Rc][2B], bin [Rc],
     Wc [layers][Cc][3][Rc], bc [layers][Cc], Wo [layers][Rc][Cc], bo [layers][Rc],
     Wp [Dx][Rc], bp [Dx]."""
-    keep = {k: np.ascontiguousarray(w[k], np.float32) for k in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")}
-    B, L = int(w["B"]), int(w["layers"])
-    Rc, Dx = keep["Win"].shape[0], keep["Wp"].shape[0]
-    Cc = keep["bc"].shape[1] if L > 0 else 1
-    fp = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
-    m = _Cnn(B, Rc, Cc, Dx, L, *[fp(keep[k]) for k in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")])
+    m = _cnn(w)
+    B, Dx = m.B, m.Dx
     seq = np.ascontiguousarray(seq, np.uint16)
     out = np.zeros((len(seq) // B, Dx), np.float32)
     if lib().orc_ctx_cnn(ctypes.byref(m), _p(seq), len(seq), s, _p(out)) != 0:

@@ -49,6 +49,10 @@
  *         recurrent state and inputs; no distant dependencies, Sec. 4.3), as
  *         the Dx/4 samples before n and the Dx/4 after n, zero where not seen.
  *         Generated here sub-tensor by sub-tensor, in the paper's order.
+ *       With a conditioning network attached (F >= 0), the context of sample
+ *         B*i + s is row i of orc_ctx_cnn for sub-tensor s, computed once the
+ *         sub-tensors before s are complete (Sec. 4.1: each sub-tensor is
+ *         generated conditioned on the previous ones through the CNN).
  *   - Fused Subscale WaveRNN 2x (Sec. 4.4): orc_fused_run, and the masked
  *     dilated CNN that conditions the Subscale WaveRNN (Sec. 4.1, 5):
  *     orc_ctx_cnn, each with its own readings in its section below.
@@ -265,14 +269,17 @@ void orc_subscale_context(const orc_model* m, const uint16_t* seq, int64_t N, in
   }
 }
 
-int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* feat, int64_t n_frames,
-            uint64_t seed, const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, uint16_t* out,
-            float* zc_out, float* zf_out, double* nll_out) {
+/* Lanes [lane_lo, lane_hi) of every utterance; the others are skipped (teacher forcing only). */
+static int run_lanes(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* feat, int64_t n_frames,
+                     uint64_t seed, const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, uint16_t* out,
+                     float* zc_out, float* zf_out, double* nll_out, int32_t lane_lo, int32_t lane_hi) {
   const int H = m->H, Hh = H / 2, B = m->B > 0 ? m->B : 1;
   if (H <= 0 || (H & 1) || H > ORC_MAX_HIDDEN || S <= 0 || T < 0) return -1;
+  if (lane_lo < 0 || lane_hi > B || lane_lo >= lane_hi || ((lane_lo > 0 || lane_hi < B) && target == NULL)) return -1;
   if (B > 1 && (T % B != 0 || t0 != 0)) return -1;
   if (m->Dc > 0 && (m->frame_len <= 0 || feat == NULL)) return -1;
   if (m->Dx > 0 && (B == 1 || m->Dx % (m->F < 0 ? 2 : 4) != 0)) return -1;
+  if (m->cnn && (m->F < 0 || m->cnn->B != B || m->cnn->Dx != m->Dx)) return -1;
   if (target == NULL && out == NULL) return -1;
   if (T == 0) return 0;
   float* G = (float*)malloc(sizeof(float) * 3 * H);
@@ -281,6 +288,7 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
   float* ctx = (float*)malloc(sizeof(float) * (m->Dx > 0 ? m->Dx : 1));
   float zc[ORC_MAX_CLASSES], zf[ORC_MAX_CLASSES];
   const int64_t rows = T / B;
+  float* ctab = m->cnn ? (float*)malloc(sizeof(float) * (size_t)(rows > 0 ? rows : 1) * m->Dx) : NULL;
   /* lockstep: row by row, lane by lane; horizon F: lane (sub-tensor) by lane */
   const int lagged = B > 1 && m->F >= 0;
   const int64_t n_outer = lagged ? B : rows, n_inner = lagged ? rows : B;
@@ -288,9 +296,13 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
     uint16_t* seq = out ? out + (size_t)s * T : NULL;   /* samples of utterance s, time order */
     const uint16_t* tgt = target ? target + (size_t)s * T : NULL;
     for (int64_t o = 0; o < n_outer; ++o) {
+      if (lagged && (o < lane_lo || o >= lane_hi)) continue;
+      /* conditioning CNN: sub-tensor o's context rows from the finished sub-tensors before it */
+      if (m->cnn) orc_ctx_cnn(m->cnn, tgt ? tgt : seq, T, (int32_t)o, ctab);
       for (int64_t in = 0; in < n_inner; ++in) {
         const int64_t i = lagged ? in : o;
         const int lane = (int)(lagged ? o : in);
+        if (lane < lane_lo || lane >= lane_hi) continue;
         const int64_t st = (int64_t)s * B + lane;   /* state / Philox stream index */
         const int64_t n = (B == 1) ? t0 + i : B * i + lane; /* absolute sample index */
         const int64_t local = (B == 1) ? i : n;             /* index into this call's arrays */
@@ -301,7 +313,8 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
           if (fr >= n_frames) fr = n_frames - 1;
           frame = feat + ((size_t)s * n_frames + fr) * m->Dc;
         }
-        if (m->Dx > 0) orc_subscale_context(m, tgt ? tgt : seq, T, lane, i, ctx);
+        if (m->cnn) memcpy(ctx, ctab + (size_t)i * m->Dx, sizeof(float) * m->Dx);
+        else if (m->Dx > 0) orc_subscale_context(m, tgt ? tgt : seq, T, lane, i, ctx);
         gate_additive(m, frame, ctx, add);
         for (int row = 0; row < 3 * H; ++row) G[row] = dot(m->R + (size_t)row * H, hs, H);
         float x[3] = {orc_scale(cprev[st]), orc_scale(fprev[st]), 0.0f};
@@ -328,8 +341,22 @@ int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* f
       }
     }
   }
-  free(G); free(add); free(hn); free(ctx);
+  free(G); free(add); free(hn); free(ctx); free(ctab);
   return 0;
+}
+
+int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* feat, int64_t n_frames,
+            uint64_t seed, const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, uint16_t* out,
+            float* zc_out, float* zf_out, double* nll_out) {
+  return run_lanes(m, S, T, t0, feat, n_frames, seed, target, h, cprev, fprev, out, zc_out, zf_out, nll_out, 0,
+                   m->B > 0 ? m->B : 1);
+}
+
+int orc_run_lanes(const orc_model* m, int32_t S, int64_t T, const float* feat, int64_t n_frames,
+                  const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, float* zc_out, float* zf_out,
+                  double* nll_out, int32_t lane_lo, int32_t lane_hi) {
+  return run_lanes(m, S, T, 0, feat, n_frames, 0, target, h, cprev, fprev, NULL, zc_out, zf_out, nll_out, lane_lo,
+                   lane_hi);
 }
 
 /* ------------------------------------------------------------------------- */

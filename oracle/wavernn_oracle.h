@@ -10,6 +10,15 @@
 #define ORC_MAX_CLASSES 256   /* 8-bit coarse / fine softmax (Sec. 2) */
 #define ORC_MAX_HIDDEN 4096
 
+/* Subscale conditioning network (Sec. 4.1, 5); readings in wavernn_oracle.c.
+ *   Win [Rc][2B] bin [Rc]; Wc [layers][Cc][3][Rc] bc [layers][Cc] (taps at rows
+ *   k, k + d, k + 2d, d = 2^(l mod 5)); Wo [layers][Rc][Cc] bo [layers][Rc];
+ *   Wp [Dx][Rc] bp [Dx].  The paper: 10 layers, Cc = 384, Rc = 768. */
+typedef struct {
+  int32_t B, Rc, Cc, Dx, layers;
+  const float *Win, *bin, *Wc, *bc, *Wo, *bo, *Wp, *bp;
+} orc_cnn;
+
 /* All matrices fp32 row-major.  Gate order u, r, e.
  *   R  [3][H][H]      recurrent matrix (Eq. 2); zeroed entries = pruned weights
  *   I  [3][H][3]      input matrix, columns (c_{t-1}, f_{t-1}, c_t); column 2 of
@@ -18,12 +27,14 @@
  *   Wc [3H][Dc]       conditioning projection (Dc = 0: none)
  *   Wx [3H][Dx]       subscale context projection (Dx = 0: none)
  *   O1 [H/2][H/2] b1 [H/2]   O2 [256][H/2] b2 [256]   (coarse head)
- *   O3 [H/2][H/2] b3 [H/2]   O4 [256][H/2] b4 [256]   (fine head)   */
+ *   O3 [H/2][H/2] b3 [H/2]   O4 [256][H/2] b4 [256]   (fine head)
+ *   cnn               optional conditioning network of a subscale model with F >= 0 */
 typedef struct {
   int32_t H, Dc, frame_len, B, Dx;
   int32_t F;   /* subscale future horizon (Sec. 4.2): < 0 lockstep rows, >= 0 the paper's order */
   const float *R, *I, *b, *Wc, *Wx;
   const float *O1, *b1, *O2, *b2, *O3, *b3, *O4, *b4;
+  const orc_cnn* cnn;   /* with F >= 0: the context of sub-tensor s is this network's output (NULL: window) */
 } orc_model;
 
 float orc_exp(float y);
@@ -46,6 +57,12 @@ void orc_subscale_context(const orc_model* m, const uint16_t* seq, int64_t N, in
 int orc_run(const orc_model* m, int32_t S, int64_t T, int64_t t0, const float* feat, int64_t n_frames,
             uint64_t seed, const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, uint16_t* out,
             float* zc, float* zf, double* nll);
+/* orc_run teacher-forced on the lanes (sub-tensors) [lane_lo, lane_hi) of every
+ * utterance only (with a target the lanes are independent); the outputs of
+ * the other lanes are left as they were.  Returns 0 or -1. */
+int orc_run_lanes(const orc_model* m, int32_t S, int64_t T, const float* feat, int64_t n_frames,
+                  const uint16_t* target, float* h, uint8_t* cprev, uint8_t* fprev, float* zc, float* zf,
+                  double* nll, int32_t lane_lo, int32_t lane_hi);
 /* Fused Subscale WaveRNN 2x (Sec. 4.4); readings in wavernn_oracle.c.  Q = H/4.
  *   R  [3][H][H]       one recurrent matrix over the whole state
  *   I  [3][H][6]       columns (c0, f0, c1, f1) of each sub-tensor's last sample,
@@ -67,15 +84,6 @@ typedef struct {
 int orc_fused_run(const orc_fused_model* m, int32_t S, int64_t N, const float* feat, int64_t n_frames,
                   uint64_t seed, const uint16_t* target, uint16_t* out, float* zc, float* zf, double* nll,
                   float* h_final);
-/* Subscale conditioning network (Sec. 4.1, 5); readings in wavernn_oracle.c.
- *   Win [Rc][2B] bin [Rc]; Wc [layers][Cc][3][Rc] bc [layers][Cc] (taps at rows
- *   k, k + d, k + 2d, d = 2^(l mod 5)); Wo [layers][Rc][Cc] bo [layers][Rc];
- *   Wp [Dx][Rc] bp [Dx].  The paper: 10 layers, Cc = 384, Rc = 768. */
-typedef struct {
-  int32_t B, Rc, Cc, Dx, layers;
-  const float *Win, *bin, *Wc, *bc, *Wo, *bo, *Wp, *bp;
-} orc_cnn;
-
 /* Conditioning vectors out [N/B][Dx] of sub-tensor s of one utterance whose
  * samples are seq [N] (N a multiple of B).  Returns 0 or -1. */
 int orc_ctx_cnn(const orc_cnn* m, const uint16_t* seq, int64_t N, int32_t s, float* out);

@@ -75,6 +75,10 @@ struct BatchArgs {
   const float* b3;
   const float* b4;
   const uint4* ux;          // [NU][8 waves][KX][64] context-projection fragments (subscale) or null
+  const float* ctab;        // horizon schedule only: context table [S][ctab_rows][Dx], or null (window
+                            // context); vector v = lane s at position p reads row
+                            // p - (ctab_row0 + s ctab_step) of its block
+  int64_t ctab_rows, ctab_row0, ctab_step;
   const float* cb;          // [U][n_cb][3H] gate bias + conditioning per utterance and frame
   int64_t n_cb;
   int frame_len;
@@ -85,6 +89,7 @@ struct BatchArgs {
   int A;                    // steps by which the units form a horizon context ahead (0: at the step before)
   int64_t rows;             // positions per lane (samples per utterance / B)
   int64_t T, t0;            // steps (rows, plus (B - 1)(F + 1) with a horizon) and first absolute step
+                            // (with a horizon: the first step of the schedule)
   uint64_t seed;
   const uint16_t* target;   // [U][B T] samples in time order, or null
   uint16_t* out;            // [U][B T] or null
@@ -104,6 +109,44 @@ struct BatchArgs {
   int64_t trace_steps;
 };
 
+// One GEMM of the conditioning CNN: dst[m][n] (epilogue) over
+// acc = sum_k A[m][k] W[n][k], n < N, on 128 x 128 tiles.
+struct CnnGemmArgs {
+  const float* src;       // activations [M][kin]
+  int kin;                // source row width (a multiple of 32)
+  int taps, dil;          // A row m = [src row m + tap dil (same block, tap < taps)], zero past the block
+                          // and past the utterance's last row
+  int rows;               // rows per block (one utterance's sub-tensor, or its window)
+  int B;                  // blocks per utterance (sub-tensors): block (u, s) = m / rows
+  int64_t row0, row_step, rows_utt;   // row k of block (u, s) is utterance row row0 + s row_step + k,
+                                      // of rows_utt
+  int M;                  // activation rows
+  int K;                  // taps x kin
+  const uint4* w;         // weight fragments [N / 16][K / 32] x 64 lanes
+  const float* bias;      // [N]
+  int N;                  // a multiple of 128
+  float* dst;             // [M][N]
+  int epi;                // 0: acc + bias; 1: relu(acc + bias); 2: dst + (acc + bias)
+  int tiles_m, tiles, per_xcd;   // 128-row tiles, all tiles, tiles per XCD slot
+};
+#define CNN_TM 128
+#define CNN_TN 128
+#define CNN_THREADS 512
+#define CNN_LDS_BUF (3 * 8 * 1024)   // A high, A low (8 row tiles each), W (8 column tiles), fragments of 1 KiB
+
+// Input rows of the conditioning CNN (see wr_cnn_input).
+struct CnnInputArgs {
+  const uint16_t* seq;    // [U][n_samples] samples in time order
+  int64_t n_samples;
+  int B;
+  int64_t rows;           // rows of the utterance (n_samples / B)
+  int win;                // rows per (utterance, sub-tensor) block
+  int64_t row0, row_step; // block (u, s) covers utterance rows row0 + s row_step ...
+  int64_t front0, front_step;   // sub-tensor z has made rows up to front0 + z front_step
+  int M, kin;
+  float* x;               // [M][kin]
+};
+
 // Kernel entry points (taken by address in the launcher).
 const void* wr_small_kernel_ptr();
 const void* wr_uniforms_kernel_ptr();
@@ -115,3 +158,5 @@ const void* wr_batch_kernel_ptr(int KH, bool ctx, int L, bool lag);   // null if
 const void* wr_fill_kernel_ptr();
 const void* wr_fused_kernel_ptr(int KH);     // null if no instantiation
 const void* wr_floor_kernel_ptr();
+const void* wr_cnn_gemm_ptr();
+const void* wr_cnn_input_ptr();

@@ -20,16 +20,17 @@ namespace {
 
 // Vector v is lane s = v % B of utterance v / B.  At step t it runs position
 // p = vpos(v, t) and makes sample n = B (t0 + p) + s of that utterance
-// (Sec. 4; B = 1: n = t0 + t): p = t for lockstep rows, p = t - s (F + 1 + A)
-// with future horizon F (Sec. 4.2: a sub-tensor starts F + 1 steps after the
-// one before it, A more when its context is formed A steps ahead, so the
-// lanes of one step are at different positions and a lane idles before its
-// first and after its last position).
+// (Sec. 4; B = 1: n = t0 + t): p = t for lockstep rows; with future horizon F
+// (Sec. 4.2: a sub-tensor starts F + 1 steps after the one before it, A more
+// when its context is formed A steps ahead, so the lanes of one step are at
+// different positions and a lane idles before its first and after its last
+// position) t0 is the schedule step the launch starts at, p = t0 + t -
+// s (F + 1 + A) is the lane's absolute position and n = B p + s.
 // (LAG: the kernel instantiated for a horizon schedule; lockstep kernels pay nothing for it.)
 template <bool LAG>
 __device__ __forceinline__ int64_t vpos(const BatchArgs& a, int v, int64_t t) {
   if (!LAG) return t;
-  return t - (int64_t)(v % a.B) * (a.F + 1 + a.A);
+  return a.t0 + t - (int64_t)(v % a.B) * (a.F + 1 + a.A);
 }
 // Index of sample B p + s in the [U][B rows] output / target arrays: obase(v) + B p.
 __device__ __forceinline__ size_t obase(const BatchArgs& a, int v) {
@@ -41,7 +42,7 @@ template <bool LAG>
 __device__ __forceinline__ int64_t cb_offset(const BatchArgs& a, int v, int64_t t) {
   int64_t p = vpos<LAG>(a, v, t);
   if (LAG) p = p < 0 ? 0 : p >= a.rows ? a.rows - 1 : p;
-  int64_t fr = ((int64_t)a.B * (a.t0 + p) + v % a.B) / a.frame_len;
+  int64_t fr = ((int64_t)a.B * ((LAG ? 0 : a.t0) + p) + v % a.B) / a.frame_len;
   if (fr >= a.n_cb) fr = a.n_cb - 1;
   return ((int64_t)(v / a.B) * a.n_cb + fr) * 3 * a.P.H;
 }
@@ -240,7 +241,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     misc[16 + tid] = a.c_in ? a.c_in[vb] : 128;
     misc[24 + tid] = a.f_in ? a.f_in[vb] : 0;
     misc[8 + tid] = misc[16 + tid];
-    misc[48 + tid] = LAG ? ((v0 + tid) % a.B) * (a.F + 1 + a.A) : 0;   // position of vector tid: t - misc[48 + tid]
+    misc[48 + tid] = LAG ? (int)(((v0 + tid) % a.B) * (a.F + 1 + a.A) - a.t0) : 0;   // position: t - misc[48 + tid]
   }
   xw* X = a.xc + (size_t)g * P.x_words;
   const xw* GA = X + P.x_ga;
@@ -454,7 +455,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     const int64_t s = t + lane, p = vpos<LAG>(a, vw, s);
     if (s < a.T && p >= 0 && p < a.rows) {
       float uc, uf;
-      wr_uniforms(a.seed, (uint64_t)vw, (uint64_t)(a.t0 + p), &uc, &uf);
+      wr_uniforms(a.seed, (uint64_t)vw, (uint64_t)((LAG ? 0 : a.t0) + p), &uc, &uf);
       uni[(buf * L + wave) * 64 + lane] = float2{uc, uf};
       tgt[(buf * L + wave) * 64 + lane] = a.target ? a.target[ob + (size_t)a.B * p] : 0;
     }
@@ -656,7 +657,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   unsigned char* img = lds + P.u_lds_w;                                             // [2KT] operand image
   unsigned char* cimg = img + 2 * KT * WR_FRAG;                                     // [KX] context image
   int* hist = (int*)(cimg + P.KX * WR_FRAG);          // [utterance slot][HC]: sample q at q % HC
-  int* misc = hist + (P.KX ? P.HS * P.HC : 0);
+  int* misc = hist + P.RING;
   const int HC = LAG ? P.HC : 256, HCm = HC - 1;   // (256 always holds a lockstep context)
   const int tile = k * WR_BUCT + q;
   const int gt = tile / (Hh / 16), i = 16 * (tile % (Hh / 16)) + (lane & 15);
@@ -721,9 +722,10 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   };
   f32x4 xa0 = {0, 0, 0, 0}, xa1 = {0, 0, 0, 0};        // context term of e-gate rows
   xw* dstx = X + (fw ? P.x_xf : P.x_xc) + (size_t)i * L + bl0;
-  // With the context formed ahead (A > 0) it is built at the start of a
-  // step, before h arrives, into its own sums for every row.
-  const bool ahead = CTX && LAG && a.A > 0;
+  // With the context formed ahead (A > 0, or read from a table) it is built
+  // at the start of a step, before h arrives, into its own sums for every row.
+  const bool table = CTX && LAG && a.ctab;
+  const bool ahead = CTX && LAG && (a.A > 0 || table);
   auto publish = [&](uint32_t tag, float cb0, float cb1) {
     if (bl0 >= L) return;                               // rows of vectors past L: zero inputs, not published
     if (ahead && gt < 2) {
@@ -745,7 +747,25 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   // is not reset-gated).
   const int ub0 = v0 / a.B;                            // first utterance of this group
   const int nut = a.B >= L ? 1 : L / a.B;              // utterances of this group
+  // Table context (the conditioning CNN's output, Sec. 4.1): vector b's
+  // context for step t + 1 is the table row of the position it runs there
+  // (block of the vector, rows from ctab_row0 + s ctab_step on; an idle
+  // lane's row clamped into the block); nothing to wait for.
+  auto table_image = [&](int64_t t) {
+    const int Dx = a.P.KX * 32;
+    for (int x = tid; x < L * Dx; x += WR_THREADS) {
+      const int b = x / Dx, col = x % Dx;
+      const int vb = min(v0 + b, a.S - 1);
+      int64_t r = vpos<LAG>(a, vb, t + 1) - (a.ctab_row0 + (int64_t)(vb % a.B) * a.ctab_step);
+      r = r < 0 ? 0 : r >= a.ctab_rows ? a.ctab_rows - 1 : r;
+      aput(cimg + (col >> 5) * WR_FRAG, col & 31, a.ctab[((size_t)vb * a.ctab_rows + r) * Dx + col], b);
+    }
+    __syncthreads();
+  };
   auto context = [&](int64_t t) {
+    if (table) {
+      table_image(t);
+    } else {
     const int64_t td = t - (LAG ? a.A : 0);            // the step whose samples join the ring now
     const uint32_t tag = (uint32_t)(td + 1);
     if (tid < nut * a.B && td >= 0) {                  // one thread per (utterance, lane)
@@ -789,6 +809,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       aput(cimg + ((2 * jj + 1) >> 5) * WR_FRAG, (2 * jj + 1) & 31, f, b);
     }
     __syncthreads();
+    }
     const bool apart = gt == 2 || ahead;               // kept apart from the products of h
     f32x4 c0 = apart ? f32x4{0, 0, 0, 0} : acc0, c1 = apart ? f32x4{0, 0, 0, 0} : acc1;
 #pragma unroll
@@ -857,6 +878,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   };
   phase_c();
   phase_f();
+  if (table) context(-1);                              // step 0's context: row 0 of the table
   publish(1u, cbv(bl0, 0), cbv(bl0 + 1, 0));
   const xw* YC = X + P.x_yc;
   const xw* YF = X + P.x_yf;

@@ -46,6 +46,15 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   // would keep 512 threads per head polling all the time and measure the
   // polling load instead)
   auto gather = [&](const xw* src, uint32_t tag) {
+    if (P.x_ps == 64) {   // fused 2x heads: the draw wave alone sums, lane v polling partial v of every slice
+      if (wave == 7) {
+        __builtin_amdgcn_s_sleep(6);
+        float s;
+        if (!sum_parts<16>(src, P.x_ps, 0, NK, lane, tag, &s, a)) misc[0] = 1;
+        else zs[lane] = s;
+      }
+      return;
+    }
     {
       float y;
       const int jj = lane < NK ? lane : 0;

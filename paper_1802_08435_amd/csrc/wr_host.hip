@@ -88,6 +88,22 @@ struct wavernn_model {
   xw* d_fxc[WR_FAN] = {};            // exchange words of launch i
   float* d_fcb[WR_FAN] = {};         // [fcb_cap][3H] bias + conditioning of launch i
   int64_t fcb_cap = 0;
+  // conditioning CNN of a subscale model (Sec. 4.1): weight fragments of the
+  // input layer, then per layer the convolution and the projection, then the
+  // output layer, in one buffer; biases likewise; activations grown on demand
+  struct Cnn {
+    int Rc = 0, Cc = 0, layers = 0, kin = 32;
+    uint4* w = nullptr;
+    float* bias = nullptr;
+    std::vector<size_t> woff, boff;   // [input, conv 0, proj 0, conv 1, ..., output] in uint4 / floats
+    float *x = nullptr, *r = nullptr, *act = nullptr;
+    int64_t cap = 0;                   // activation rows the buffers hold
+  } cnn;
+  bool has_cnn = false;
+  int64_t cnn_chunk = 0, cnn_win = 0;   // sampling: steps per chunk, CNN window rows
+  float* d_ctab = nullptr;              // context table [max_streams][B][rows or window][Dx]
+  int64_t ctab_cap = 0;                 // floats
+  wavernn_state cnn_state[2] = {};      // state between chunks (ping-pong)
   // batched path (several utterances per launch)
   bool has_batch = false;
   BatchPlan bplan;
@@ -170,6 +186,17 @@ wavernn_status validate_config(const wavernn_config* c, const wavernn_weights* w
       (!c->fused && (!w->O3 || !w->b3 || !w->O4 || !w->b4)))
     return fail(WAVERNN_E_INVALID, "a required weight array is null");
   if (c->cond_dim > 0 && !w->W_cond) return fail(WAVERNN_E_INVALID, "W_cond is null with cond_dim > 0");
+  if (w->ctx_cnn) {
+    const wavernn_ctx_cnn* n = w->ctx_cnn;
+    if (c->subscale < 2 || c->fused || c->future_horizon < 0)
+      return fail(WAVERNN_E_INVALID, "ctx_cnn: needs a subscale model with a future horizon");
+    if (n->res_channels <= 0 || n->res_channels % 128 || n->conv_channels <= 0 || n->conv_channels % 128 ||
+        n->layers < 0 || n->layers > 64 || c->ctx_dim % 128 || 2 * c->subscale > 1024)
+      return fail(WAVERNN_E_INVALID, "ctx_cnn: res/conv channels and ctx_dim must be positive multiples of 128, "
+                  "layers in [0, 64]");
+    if (!n->Win || !n->bin || !n->Wp || !n->bp || (n->layers > 0 && (!n->Wc || !n->bc || !n->Wo || !n->bo)))
+      return fail(WAVERNN_E_INVALID, "ctx_cnn: a weight array is null");
+  }
   if (c->ctx_dim > 0 && !w->W_ctx) return fail(WAVERNN_E_INVALID, "W_ctx is null with ctx_dim > 0");
   if (c->r_format != WAVERNN_R_DENSE) {
     int bh = c->r_format == WAVERNN_R_BSR_4X4 ? 4 : 16, bw = c->r_format == WAVERNN_R_BSR_4X4 ? 4 : 1;
@@ -607,7 +634,7 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   size_t xwords = 0;
   for (int v : {std::min(maxv, 2 * WR_BL), std::min(maxv, 4 * WR_BL), maxv}) {
     BatchPlan Q;
-    if (!batch_plan(H, v, &Q, m->cfg.ctx_dim, m->cfg.subscale, horizon_of(m->cfg), lead_of(m->cfg)))
+    if (!batch_plan(H, v, &Q, m->cfg.ctx_dim, m->cfg.subscale, horizon_of(m->cfg), lead_of(m->cfg), m->has_cnn))
       return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors (future horizon %d: sample ring of the "
                   "units too large for LDS?)", v, horizon_of(m->cfg));
     const void* k = wr_batch_kernel_ptr(Q.KH, Q.KX > 0, Q.L, horizon_of(m->cfg) >= 0);
@@ -618,6 +645,164 @@ wavernn_status build_batch(wavernn_model* m, const wavernn_weights* w) {
   if ((s = m->alloc(&m->d_bxc, (xwords + 1) / 2 * 8)) != WAVERNN_OK) return s;
   m->has_batch = true;
   return WAVERNN_OK;
+}
+
+// Fragments [N / 16][K / 32] (operand B of v_mfma_f32_16x16x32_bf16) of a
+// matrix W(n, k), n < N, k < K (K a multiple of 32), bf16 round to nearest even.
+template <class M>
+void pack_gemm(std::vector<uint16_t>& dst, M&& mat, int N, int K) {
+  const size_t base = dst.size();
+  dst.resize(base + (size_t)N * K);
+  for (int nt = 0; nt < N / 16; ++nt)
+    for (int kt = 0; kt < K / 32; ++kt)
+      frag(dst.data() + base + ((size_t)nt * (K / 32) + kt) * 512, mat, [&](int r) { return 16 * nt + r; }, 32 * kt);
+}
+
+// Rows a conditioning CNN of `layers` layers sees past its own row: each layer
+// reaches 2 d further, d = 2^(l mod 5) (124 for ten layers).
+int cnn_reach(int layers) {
+  int r = 0;
+  for (int l = 0; l < layers; ++l) r += 2 << (l % 5);
+  return r;
+}
+
+// Grow the context table to `floats` (waits for `st` first when it has work that may read the old one).
+wavernn_status grow_ctab(wavernn_model* m, size_t floats, hipStream_t* st) {
+  if (floats <= (size_t)m->ctab_cap) return WAVERNN_OK;
+  if (st) HIPOK(hipStreamSynchronize(*st));
+  float* p = nullptr;
+  wavernn_status s = m->alloc(&p, floats * 4);
+  if (s != WAVERNN_OK) return s;
+  m->d_ctab = p;
+  m->ctab_cap = (int64_t)floats;
+  return WAVERNN_OK;
+}
+
+// The conditioning CNN's weights as GEMM fragments (input layer with its 2B
+// columns padded to kin, then per layer convolution [Cc][3 Rc] and projection
+// [Rc][Cc], then the output layer [Dx][Rc]) and biases.
+wavernn_status build_cnn(wavernn_model* m, const wavernn_ctx_cnn* n) {
+  auto& C = m->cnn;
+  const int B = m->cfg.subscale, Dx = m->cfg.ctx_dim;
+  C.Rc = n->res_channels;
+  C.Cc = n->conv_channels;
+  C.layers = n->layers;
+  C.kin = (2 * B + 31) / 32 * 32;
+  const int Rc = C.Rc, Cc = C.Cc, kin = C.kin;
+  Rounder rd{true};
+  std::vector<uint16_t> w;
+  std::vector<float> b;
+  auto mark = [&]() {
+    C.woff.push_back(w.size() / 8);
+    C.boff.push_back(b.size());
+  };
+  mark();
+  pack_gemm(w, [&](int o, int q) { return q < 2 * B ? n->Win[(size_t)o * 2 * B + q] : 0.0f; }, Rc, kin);
+  for (int o = 0; o < Rc; ++o) b.push_back(rd(n->bin[o]));
+  for (int l = 0; l < C.layers; ++l) {
+    mark();
+    const float* Wc = n->Wc + (size_t)l * Cc * 3 * Rc;
+    pack_gemm(w, [&](int c, int q) { return Wc[(size_t)c * 3 * Rc + q]; }, Cc, 3 * Rc);
+    for (int c = 0; c < Cc; ++c) b.push_back(rd(n->bc[(size_t)l * Cc + c]));
+    mark();
+    const float* Wo = n->Wo + (size_t)l * Rc * Cc;
+    pack_gemm(w, [&](int o, int c) { return Wo[(size_t)o * Cc + c]; }, Rc, Cc);
+    for (int o = 0; o < Rc; ++o) b.push_back(rd(n->bo[(size_t)l * Rc + o]));
+  }
+  mark();
+  pack_gemm(w, [&](int o, int q) { return n->Wp[(size_t)o * Rc + q]; }, Dx, Rc);
+  for (int o = 0; o < Dx; ++o) b.push_back(rd(n->bp[o]));
+  wavernn_status s;
+  if ((s = m->upload(&C.w, w.data(), w.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&C.bias, b.data(), b.size() * 4)) != WAVERNN_OK) return s;
+  HIPOK(hipFuncSetAttribute(wr_cnn_gemm_ptr(), hipFuncAttributeMaxDynamicSharedMemorySize, 2 * CNN_LDS_BUF));
+  m->has_cnn = true;
+  return WAVERNN_OK;
+}
+
+// One CNN layer as a GEMM (see CnnGemmArgs).
+struct CnnRows {   // which utterance rows the blocks of a CNN run cover
+  int B;
+  int64_t row0, row_step, rows_utt;
+};
+
+wavernn_status cnn_gemm(const float* src, int kin, int taps, int dil, int rows, const CnnRows& cr, int M,
+                        const uint4* w, const float* bias, int N, float* dst, int epi, hipStream_t st) {
+  CnnGemmArgs g;
+  g.src = src;
+  g.kin = kin;
+  g.taps = taps;
+  g.dil = dil;
+  g.rows = rows;
+  g.B = cr.B;
+  g.row0 = cr.row0;
+  g.row_step = cr.row_step;
+  g.rows_utt = cr.rows_utt;
+  g.M = M;
+  g.K = taps * kin;
+  g.w = w;
+  g.bias = bias;
+  g.N = N;
+  g.dst = dst;
+  g.epi = epi;
+  g.tiles_m = (M + CNN_TM - 1) / CNN_TM;
+  g.tiles = g.tiles_m * (N / CNN_TN);
+  g.per_xcd = (g.tiles + 7) / 8;
+  void* args[] = {&g};
+  HIPOK(hipLaunchKernel(wr_cnn_gemm_ptr(), dim3(8 * g.per_xcd), dim3(CNN_THREADS), args, 2 * CNN_LDS_BUF, st));
+  return WAVERNN_OK;
+}
+
+// The conditioning CNN over windows of `win` rows per (utterance, sub-tensor):
+// block (u, s) covers utterance rows row0 + s row_step .. + win - 1, samples
+// of sub-tensor z counted up to row front0 + z front_step; out [U][B][win][Dx].
+wavernn_status run_cnn(wavernn_model* m, int U, const uint16_t* seq, int64_t n_samples, int win, int64_t row0,
+                       int64_t row_step, int64_t front0, int64_t front_step, float* out, hipStream_t st) {
+  auto& C = m->cnn;
+  const int B = m->cfg.subscale, Dx = m->cfg.ctx_dim;
+  const int64_t M64 = (int64_t)U * B * win;
+  if (M64 > (1 << 28)) return fail(WAVERNN_E_INVALID, "conditioning CNN: %lld rows, above 2^28", (long long)M64);
+  const int M = (int)M64;
+  if (M > C.cap) {   // grow the activations (an allocation: only when a call needs more rows than any before)
+    HIPOK(hipStreamSynchronize(st));
+    wavernn_status s;
+    if ((s = m->alloc(&C.x, (size_t)M * C.kin * 4)) != WAVERNN_OK) return s;
+    if ((s = m->alloc(&C.r, (size_t)M * C.Rc * 4)) != WAVERNN_OK) return s;
+    if ((s = m->alloc(&C.act, (size_t)M * C.Cc * 4)) != WAVERNN_OK) return s;
+    C.cap = M;
+  }
+  CnnInputArgs in;
+  in.seq = seq;
+  in.n_samples = n_samples;
+  in.B = B;
+  in.rows = n_samples / B;
+  in.win = win;
+  in.row0 = row0;
+  in.row_step = row_step;
+  in.front0 = front0;
+  in.front_step = front_step;
+  in.M = M;
+  in.kin = C.kin;
+  in.x = C.x;
+  void* args[] = {&in};
+  const int64_t nx = (int64_t)M * C.kin;
+  HIPOK(hipLaunchKernel(wr_cnn_input_ptr(), dim3((unsigned)((nx + 255) / 256)), dim3(256), args, 0, st));
+  wavernn_status s;
+  size_t i = 0;
+  const CnnRows cr{B, row0, row_step, n_samples / B};
+  if ((s = cnn_gemm(C.x, C.kin, 1, 0, win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], C.Rc, C.r, 0, st)) !=
+      WAVERNN_OK)
+    return s;
+  ++i;
+  for (int l = 0; l < C.layers; ++l, i += 2) {
+    if ((s = cnn_gemm(C.r, C.Rc, 3, 1 << (l % 5), win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], C.Cc, C.act, 1,
+                      st)) != WAVERNN_OK)
+      return s;
+    if ((s = cnn_gemm(C.act, C.Cc, 1, 0, win, cr, M, C.w + C.woff[i + 1], C.bias + C.boff[i + 1], C.Rc, C.r, 2,
+                      st)) != WAVERNN_OK)
+      return s;
+  }
+  return cnn_gemm(C.r, C.Rc, 1, 0, win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], Dx, out, 0, st);
 }
 
 // Bias + conditioning table cb[s][f][3H] for n_streams streams of n_frames frames.
@@ -874,8 +1059,10 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   const int V = io.S * SB;                        // vectors
   BatchPlan B;
   const int F = horizon_of(m->cfg), A = lead_of(m->cfg);
-  if (!batch_plan(m->cfg.hidden, V, &B, m->cfg.ctx_dim, SB, F, A))
+  const bool table = m->has_cnn;
+  if (!batch_plan(m->cfg.hidden, V, &B, m->cfg.ctx_dim, SB, F, A, table))
     return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors", V);
+  if (table && io.ws) return fail(WAVERNN_E_UNSUPPORTED, "the conditioning CNN needs its own activation buffers");
   const int H = B.H, Dc = m->cfg.cond_dim;
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
   const int64_t n_cb = Dc > 0 ? io.n_frames : 1;
@@ -896,7 +1083,6 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   const void* kernel = wr_batch_kernel_ptr(B.KH, B.KX > 0, B.L, F >= 0);
   if (!kernel) return fail(WAVERNN_E_UNSUPPORTED, "no batched kernel for %d vectors", V);
   if ((st = launch_cond(m, io.cond, n_cb, io.S, cbt, io.st)) != WAVERNN_OK) return st;
-  if ((st = launch_fill(xc, (int64_t)B.G * B.x_words, io.st)) != WAVERNN_OK) return st;
   BatchArgs a;
   memset(&a, 0, sizeof a);
   a.P = B;
@@ -917,24 +1103,72 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.F = F;
   a.A = A;
   a.rows = io.T / SB;
-  a.T = a.rows + (F >= 0 ? (int64_t)(SB - 1) * (F + 1 + A) : 0);   // the last lane starts (B - 1)(F + 1 + A) late
-  a.t0 = io.init ? io.init->t0 : 0;
   a.seed = io.seed;
   a.target = io.target;
   a.out = io.out;
   a.zc_out = io.zc;
   a.zf_out = io.zf;
   a.nll_out = io.nll;
-  if (io.init) { a.h_in = io.init->h; a.c_in = io.init->c_prev; a.f_in = io.init->f_prev; }
-  if (io.fin) { a.h_out = io.fin->h; a.c_out = io.fin->c_prev; a.f_out = io.fin->f_prev; }
   a.xc = xc;
   a.err = m->d_err;
   a.limit = kWaitTicks;
   a.trace = m->trace;
   a.trace_steps = m->trace ? m->trace_steps : 0;
-  void* args[] = {&a};
-  // an ordinary launch, as for the batch-1 kernel (co-residency checked at create)
-  HIPOK(hipLaunchKernel(kernel, dim3(B.grid), dim3(WR_THREADS), args, B.lds, io.st));
+  const int64_t steps = a.rows + (F >= 0 ? (int64_t)(SB - 1) * (F + 1 + A) : 0);   // the last lane starts late
+  // one launch of steps [t0, t0 + n) from state `in` to state `out` (null: default / nowhere)
+  auto launch = [&](int64_t t0, int64_t n, const wavernn_state* in, const wavernn_state* out) -> wavernn_status {
+    wavernn_status e = launch_fill(xc, (int64_t)B.G * B.x_words, io.st);
+    if (e != WAVERNN_OK) return e;
+    a.t0 = t0;
+    a.T = n;
+    a.h_in = in ? in->h : nullptr;
+    a.c_in = in ? in->c_prev : nullptr;
+    a.f_in = in ? in->f_prev : nullptr;
+    a.h_out = out ? out->h : nullptr;
+    a.c_out = out ? out->c_prev : nullptr;
+    a.f_out = out ? out->f_prev : nullptr;
+    void* args[] = {&a};
+    // an ordinary launch, as for the batch-1 kernel (co-residency checked at create)
+    HIPOK(hipLaunchKernel(kernel, dim3(B.grid), dim3(WR_THREADS), args, B.lds, io.st));
+    return WAVERNN_OK;
+  };
+  if (!table) return launch(io.init ? io.init->t0 : 0, steps, io.init, io.fin);
+  // Conditioning CNN (Sec. 4.1).  Teacher forcing: the whole context table
+  // from the targets, one launch.
+  const int64_t rows = a.rows;
+  if (io.target) {
+    hipStream_t s0 = io.st;
+    if ((st = grow_ctab(m, (size_t)V * rows * m->cfg.ctx_dim, &s0)) != WAVERNN_OK) return st;
+    if ((st = run_cnn(m, io.S, io.target, io.T, (int)rows, 0, 0, rows, 0, m->d_ctab, io.st)) != WAVERNN_OK) return st;
+    a.ctab = m->d_ctab;
+    a.ctab_rows = rows;
+    a.ctab_row0 = 0;
+    a.ctab_step = 0;
+    return launch(0, steps, io.init, io.fin);
+  }
+  // Sampling: chunks of LC = F - R + 1 steps (R the CNN's reach in rows).
+  // Before chunk [t0, t0 + LC) the CNN runs on windows of LC + R rows, lane s
+  // from its position t0 - s (F + 1) on: sub-tensor z < s has made its rows up
+  // to t0 - 1 - z (F + 1), which covers the window's first LC rows with their
+  // reach (Sec. 4.2: the conditioning runs ahead by a chosen number of
+  // samples; the lag between sub-tensors pays for it).
+  const int64_t LC = m->cnn_chunk, W = m->cnn_win;
+  a.ctab = m->d_ctab;
+  a.ctab_rows = W;
+  a.ctab_step = -(int64_t)(F + 1);
+  int cur = 0;
+  for (int64_t t0 = 0; t0 < steps; t0 += LC) {
+    const int64_t n = std::min(LC, steps - t0);
+    if ((st = run_cnn(m, io.S, io.out, io.T, (int)W, t0, -(int64_t)(F + 1), t0 - 1, -(int64_t)(F + 1), m->d_ctab,
+                      io.st)) != WAVERNN_OK)
+      return st;
+    a.ctab_row0 = t0;
+    const bool last = t0 + n >= steps;
+    const wavernn_state* in = t0 == 0 ? io.init : &m->cnn_state[cur];
+    const wavernn_state* out = last ? io.fin : &m->cnn_state[cur ^ 1];
+    if ((st = launch(t0, n, in, out)) != WAVERNN_OK) return st;
+    cur ^= 1;
+  }
   return WAVERNN_OK;
 }
 
@@ -1028,8 +1262,12 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
                "must tile groups of 2, 4 and 8 vectors), ctx_dim a multiple of 32 up to 256", B, cfg->ctx_dim);
     else if (cfg->weight_dtype != WAVERNN_BF16)
       s = fail(WAVERNN_E_UNSUPPORTED, "subscale sampling needs bf16 weights");
+    else if ((m->has_cnn = w->ctx_cnn != nullptr) && cnn_reach(w->ctx_cnn->layers) > cfg->future_horizon)
+      s = fail(WAVERNN_E_INVALID, "ctx_cnn: the future horizon %d is below the CNN's reach of %d rows (the "
+               "CNN runs ahead in chunks of F - reach + 1 steps)", cfg->future_horizon, cnn_reach(w->ctx_cnn->layers));
     else if (!persist_plan(H, &m->plan) ||
-             !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim, B, horizon_of(*cfg), lead_of(*cfg)))
+             !batch_plan(H, cfg->max_streams * B, &m->bplan, cfg->ctx_dim, B, horizon_of(*cfg), lead_of(*cfg),
+                         m->has_cnn))
       s = fail(WAVERNN_E_UNSUPPORTED, "hidden %d with %d x %d lanes, future horizon %d, context lead %d: no batched "
                "plan (the units' ring of B (B - 1)(F + 1 + A) + Dx/2 + B samples must fit LDS)", H, cfg->max_streams,
                B, horizon_of(*cfg), lead_of(*cfg));
@@ -1037,6 +1275,18 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
       m->path = PATH_BATCHED;
       s = build_persist(m, w);
       if (s == WAVERNN_OK) s = build_batch(m, w);
+      if (s == WAVERNN_OK && w->ctx_cnn) s = build_cnn(m, w->ctx_cnn);
+      if (s == WAVERNN_OK && w->ctx_cnn) {   // sampling chunks, their context window and the state between them
+        const int R = cnn_reach(w->ctx_cnn->layers), V = cfg->max_streams * B;
+        m->cnn_chunk = cfg->future_horizon - R + 1;
+        m->cnn_win = m->cnn_chunk + R;
+        s = grow_ctab(m, (size_t)V * m->cnn_win * cfg->ctx_dim, nullptr);
+        for (int i = 0; i < 2 && s == WAVERNN_OK; ++i) {
+          s = m->alloc(&m->cnn_state[i].h, (size_t)V * H * 4);
+          if (s == WAVERNN_OK) s = m->alloc(&m->cnn_state[i].c_prev, V);
+          if (s == WAVERNN_OK) s = m->alloc(&m->cnn_state[i].f_prev, V);
+        }
+      }
     }
   } else if (small_fits) {
     m->path = PATH_SMALL;
@@ -1133,7 +1383,7 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
     g = n_streams > 0 ? n_streams : 1, b = 256;
   } else if (m->path == PATH_BATCHED &&
              batch_plan(m->cfg.hidden, (n_streams > 0 ? n_streams : 1) * m->cfg.subscale, &B, m->cfg.ctx_dim,
-                        m->cfg.subscale, horizon_of(m->cfg), lead_of(m->cfg))) {
+                        m->cfg.subscale, horizon_of(m->cfg), lead_of(m->cfg), m->has_cnn)) {
     g = B.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST && n_streams > 1 && n_streams <= m->nfan) {
     path = PATH_CONCURRENT_ID, g = m->plan.grid, b = WR_THREADS;
@@ -1189,6 +1439,19 @@ wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t 
   m->trace = max_steps > 0 ? (u64*)trace_dev : nullptr;
   m->trace_steps = max_steps;
   return WAVERNN_OK;
+}
+
+wavernn_status wavernn_ctx_cnn_run(wavernn_model* m, int32_t n_streams, int64_t n_samples, const uint16_t* seq_dev,
+                                   float* out_dev, void* stream) {
+  if (!m) return fail(WAVERNN_E_INVALID, "null model");
+  if (!m->has_cnn) return fail(WAVERNN_E_INVALID, "the model has no conditioning CNN");
+  const int B = m->cfg.subscale;
+  if (n_streams < 1 || n_streams > m->cfg.max_streams || n_samples < 0 || n_samples % B || n_samples / B > (1 << 26))
+    return fail(WAVERNN_E_INVALID, "n_streams %d / n_samples %lld: bad sizes", n_streams, (long long)n_samples);
+  if (n_samples == 0) return WAVERNN_OK;
+  if (!seq_dev || !out_dev) return fail(WAVERNN_E_INVALID, "null buffer");
+  const int64_t rows = n_samples / B;
+  return run_cnn(m, n_streams, seq_dev, n_samples, (int)rows, 0, 0, rows, 0, out_dev, (hipStream_t)stream);
 }
 
 const char* wavernn_last_error(void) { return g_err.c_str(); }

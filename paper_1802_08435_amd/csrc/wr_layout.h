@@ -270,6 +270,7 @@ struct BatchPlan {
   int KX;                 // subscale context column tiles (Dx / 32), 0 without context
   int HC;                 // drawn samples a unit keeps per utterance (ring, a power of two)
   int HS;                 // utterances whose samples a unit keeps (slots of HC)
+  int RING;               // ints of LDS the sample rings take (0 with a context table)
   int SS;                 // slots of the drawn-sample words (a power of two >= 2 A + 2)
   int lds_h, lds_u, lds;
 };
@@ -291,7 +292,7 @@ WR_HD inline int wr_batch_role(const BatchPlan& P, int b, int* g) {
 // steps A by which the units form the context ahead, which size the ring of
 // drawn samples a unit keeps and the slots of the sample words.
 WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0, int B = 1, int F = -1,
-                             int A = 0) {
+                             int A = 0, bool table = false) {
   if (H <= 0 || H % 128 || n_vectors < 1 || n_vectors > 8 * WR_BL) return false;
   if (ctx_dim < 0 || ctx_dim % 32 || ctx_dim > 256 || B < 1 || F > 1024 || A < 0 || A > 3) return false;
   P->KX = ctx_dim / 32;
@@ -336,15 +337,17 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   // a row plus the row; with horizon F the lanes of an utterance are up to
   // (B - 1)(F + 1 + A) positions apart, so the newest sample and the oldest
   // one a context still reads are at most B (B - 1)(F + 1 + A) + Dx/4 apart.
+  // (With a context table, read from HBM at each step, there is no ring.)
   {
     const int need = F < 0 ? ctx_dim / 2 + 2 * B : B * (B - 1) * (F + 1 + A) + ctx_dim / 2 + B;
     P->HC = 256;
-    while (P->HC < need) P->HC *= 2;
+    while (!table && P->HC < need) P->HC *= 2;
     P->HS = (ctx_dim > 0 && P->L > B) ? P->L / B : 1;
+    P->RING = ctx_dim > 0 && !table ? P->HS * P->HC : 0;
   }
   // unit: weights, operand image (2 KT fragments), context image (KX fragments),
   // sample rings [HS][HC], misc [16]
-  P->lds_u = P->u_lds_w + (2 * P->KT + P->KX) * WR_FRAG + 4 * ((ctx_dim > 0 ? P->HS * P->HC : 0) + 16);
+  P->lds_u = P->u_lds_w + (2 * P->KT + P->KX) * WR_FRAG + 4 * (P->RING + 16);
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024 && P->grid <= 256;
 }

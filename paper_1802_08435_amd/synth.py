@@ -88,6 +88,21 @@ def make_fused_weights(H: int, F: int = 2, seed: int = 0, cond_dim: int = 0) -> 
     return w
 
 
+def make_cnn_weights(B: int, Rc: int = 768, Cc: int = 384, Dx: int = 256, layers: int = 10, seed: int = 5) -> dict:
+    """The masked dilated CNN that conditions a Subscale WaveRNN (Sec. 4.1, 5):
+    Win [Rc][2B], per layer Wc [Cc][3][Rc] (taps k, k + d, k + 2d), Wo [Rc][Cc],
+    and Wp [Dx][Rc], N(0, 1/fan_in), biases N(0, 0.1^2); the paper's widths by
+    default (768 residual, 384 convolution channels, ten layers).  The residual
+    stream grows over the layers (to about 4 at ten), so Wp is scaled by 1/4:
+    context values of order one."""
+    rng = np.random.default_rng(seed)
+    b = lambda *shape: (0.1 * rng.standard_normal(shape)).astype(np.float32)
+    return dict(B=B, layers=layers, Win=_normal(rng, (Rc, 2 * B), 2 * B), bin=b(Rc),
+                Wc=_normal(rng, (layers, Cc, 3, Rc), 3 * Rc), bc=b(layers, Cc),
+                Wo=_normal(rng, (layers, Rc, Cc), Cc), bo=b(layers, Rc),
+                Wp=_normal(rng, (Dx, Rc), 16 * Rc), bp=b(Dx))
+
+
 def features(S: int, T: int, cond_dim: int = COND_DIM, seed: int = 2, frame_len: int = FRAME_LEN,
              per_stream_seed: bool = False) -> np.ndarray:
     """Conditioning frames [S][ceil(T/frame_len)][cond_dim] ~N(0, 1)."""
@@ -131,13 +146,17 @@ PRESETS = {
     "multi4": (896, COND_DIM, 1, 0, None, True, 4, 24000),   # Sec. 2.1's batch-4 point
     "subscale16_h4": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
     "subscale16_h4a1": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
+    "subscale16_cnn": (896, COND_DIM, 16, CTX_DIM, None, True, 1, 24000),
 }
 # Subscale presets in the paper's order with a future horizon (Sec. 4.2):
 # lane s starts F + 1 + A steps after lane s - 1 (24,000 samples with F = 4:
 # 1,500 + 15 x (5 + A) steps), A the steps by which its context is formed
 # ahead; the others run lockstep rows.
-HORIZON = {"subscale16_h4": 4, "subscale16_h4a1": 4}
+HORIZON = {"subscale16_h4": 4, "subscale16_h4a1": 4, "subscale16_cnn": 223}
 LEAD = {"subscale16_h4a1": 1}   # the lead is switched off at create (E_UNSUPPORTED) for now
+# Subscale conditioned by the masked dilated CNN at the paper's widths (Sec. 4.1, 5): it
+# reaches 124 rows ahead, so with F = 223 it runs ahead in chunks of 100 rows (Sec. 4.2's L).
+CNN = {"subscale16_cnn": dict(Rc=768, Cc=384, layers=10)}
 
 
 # Fused Subscale WaveRNN 2x (Sec. 4.4): WaveRNN-896 with its state in quarters,
@@ -158,4 +177,6 @@ def preset(name: str, seed: int = 0) -> dict:
     if name in HORIZON:
         w["F"] = HORIZON[name]
         w["A"] = LEAD.get(name, 0)
+    if name in CNN:
+        w["cnn"] = make_cnn_weights(B, Dx=Dx, **CNN[name])
     return w

@@ -36,9 +36,15 @@ class Config(ctypes.Structure):
 _FP = ctypes.POINTER(ctypes.c_float)
 
 
+class CtxCnn(ctypes.Structure):
+    _fields_ = [("res_channels", ctypes.c_int32), ("conv_channels", ctypes.c_int32), ("layers", ctypes.c_int32)] + [
+        (n, _FP) for n in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")]
+
+
 class Weights(ctypes.Structure):
     _fields_ = [("R", _FP), ("R_block_mask", ctypes.POINTER(ctypes.c_uint8)), ("I", _FP), ("b", _FP),
-                ("W_cond", _FP), ("W_ctx", _FP)] + [(n, _FP) for n in ("O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")]
+                ("W_cond", _FP), ("W_ctx", _FP)] + [(n, _FP) for n in ("O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")] + [
+        ("ctx_cnn", ctypes.POINTER(CtxCnn))]
 
 
 class State(ctypes.Structure):
@@ -75,6 +81,8 @@ def lib():
         L.wavernn_debug_sync_floor.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_double), vp]
         L.wavernn_model_path.restype = i32
         L.wavernn_model_path.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.wavernn_ctx_cnn_run.restype = ctypes.c_int
+        L.wavernn_ctx_cnn_run.argtypes = [vp, i32, i64, vp, vp, vp]
         L.wavernn_last_error.restype = ctypes.c_char_p
         L.wavernn_last_error.argtypes = []
         _lib = L
@@ -110,7 +118,9 @@ class Model:
     frame_len, B and, for subscale, F (future horizon; -1 or absent: lockstep rows) and A (steps by which
     the context is formed ahead, with F only; absent: 0).  dtype 'bf16' or 'f32' is the weight storage; r_format is
     'dense', 'bsr4x4' or 'bsr16x1'.  A Fused Subscale 2x model (``fused`` true) has B = 2, F, I [3][H][6],
-    O1 [4][Q][Q], b1 [4][Q], O2 [4][2][16][Q], b2 [4][2][16] and no O3, b3, O4, b4."""
+    O1 [4][Q][Q], b1 [4][Q], O2 [4][2][16][Q], b2 [4][2][16] and no O3, b3, O4, b4.  A subscale model
+    with a future horizon may carry ``cnn``: the conditioning CNN's arrays (Win, bin, Wc, bc, Wo, bo,
+    Wp, bp; include/wavernn.h's wavernn_ctx_cnn), which replaces the window context."""
 
     def __init__(self, w: dict, dtype: str = "bf16", r_format: str = "dense", max_streams: int = 1):
         L = lib()
@@ -132,6 +142,13 @@ class Model:
         ws = Weights(fp(keep["R"]), None if mask is None else mask.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
                      fp(keep["I"]), fp(keep["b"]), fp(Wc), fp(Wx),
                      *[fp(keep[k]) for k in ("O1", "b1", "O2", "b2", "O3", "b3", "O4", "b4")])
+        self.cnn = w.get("cnn")
+        if self.cnn is not None:
+            ck = {k: _f32(self.cnn[k]) for k in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")}
+            cc = CtxCnn(ck["Win"].shape[0], ck["bc"].shape[1] if int(self.cnn["layers"]) > 0 else 128,
+                        int(self.cnn["layers"]), *[fp(ck[k]) for k in ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")])
+            ws.ctx_cnn = ctypes.pointer(cc)
+            keep["_cnn"] = (ck, cc)
         h = ctypes.c_void_p()
         _check(L.wavernn_create(ctypes.byref(cfg), ctypes.byref(ws), ctypes.byref(h)))
         self._h = h
@@ -208,6 +225,14 @@ class Model:
                                                   None if si is None else ctypes.byref(si),
                                                   _ptr(zc), _ptr(zf), _ptr(nl), _stream(stream)))
         return dict(zc=zc, zf=zf, nll=nl)
+
+    def ctx_cnn(self, seq, stream=None):
+        """Conditioning CNN over whole utterances seq [S][N] uint16: tensor [S][B][N/B][Dx]."""
+        import torch
+        S, N = seq.shape
+        out = torch.empty(S, self.B, N // self.B, int(self.cnn["Wp"].shape[0]), device="cuda")
+        _check(lib().wavernn_ctx_cnn_run(self._h, S, N, _ptr(seq), _ptr(out), _stream(stream)))
+        return out
 
     def set_trace(self, buf=None):
         """Record per-phase timestamps of later persistent-kernel calls into buf,

@@ -1,0 +1,188 @@
+"""GPU parity of the conditioning CNN of the Subscale WaveRNN (Sec. 4.1, 5)
+and of subscale sampling conditioned by it, through the C ABI, against the
+oracle's orc_ctx_cnn and orc_run (sub-tensor by sub-tensor, each conditioned
+on the previous ones through the CNN).
+
+Bars: CNN outputs within 1e-3 (1 + |oracle|) elementwise (bf16 weights as the
+oracle reads them; fp32 activations carried as bf16 high and low parts, about
+2^-16 relative per product, over at most 2,304-term sums and ten residual
+layers); teacher-forced logits within 1e-3 at small sizes; free-running draws
+valid under the oracle's logits; samples independent of the chunking.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from oracle import oracle as O  # noqa: E402
+from paper_1802_08435_amd import synth, wavernn  # noqa: E402
+
+CNN_KEYS = ("Win", "bin", "Wc", "bc", "Wo", "bo", "Wp", "bp")
+
+
+def cuda(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.cpu().numpy()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def oracle_cnn(c):
+    return dict(c, **{k: O.bf16_round(c[k]) for k in CNN_KEYS})
+
+
+def cnn_model(H=128, B=4, Dx=128, F=124, Rc=128, Cc=128, layers=10, seed=1, cond_dim=16):
+    w = synth.make_weights(H, seed=seed, cond_dim=cond_dim, B=B, ctx_dim=Dx)
+    w["F"] = F
+    w["cnn"] = synth.make_cnn_weights(B, Rc=Rc, Cc=Cc, Dx=Dx, layers=layers, seed=seed + 10)
+    return w
+
+
+def check_cnn(out, ref):
+    d = np.abs(out - ref) / (1.0 + np.abs(ref))
+    print(f"  cnn max |d| / (1 + |ref|) = {d.max():.2e} (|ref| up to {np.abs(ref).max():.2f})", flush=True)
+    assert d.max() <= 1e-3, d.max()
+
+
+@pytest.mark.parametrize("layers,rows,S", [(0, 40, 1), (1, 137, 2), (3, 64, 1), (10, 137, 2)])
+def test_ctx_cnn_small_widths(layers, rows, S):
+    """Several 128-row tiles with a ragged last one (2 x 4 x 137 rows), one
+    layer to ten (dilations 1 .. 16 twice), two utterances."""
+    B = 4
+    w = cnn_model(layers=layers, F=max(1, sum(2 << (l % 5) for l in range(layers))))
+    print(f"cnn small layers={layers} rows={rows} S={S}", flush=True)
+    m = wavernn.Model(w, max_streams=S)
+    seq = synth.target_signal(S, B * rows, kind="uniform")
+    out = host(m.ctx_cnn(cuda(seq)))
+    m.device_status()
+    c = oracle_cnn(w["cnn"])
+    for u in range(S):
+        for s in range(B):
+            check_cnn(out[u, s], O.ctx_cnn(c, seq[u], s))
+    m.close()
+
+
+def test_ctx_cnn_paper_widths():
+    """Ten layers, 768 residual and 384 convolution channels, B = 16, Dx = 256
+    (Sec. 5), 140 rows: the first, second, a middle and the last sub-tensor."""
+    w = synth.preset("subscale16_cnn")
+    m = wavernn.Model(w)
+    seq = synth.target_signal(1, 16 * 140, kind="uniform")
+    out = host(m.ctx_cnn(cuda(seq)))
+    m.device_status()
+    c = oracle_cnn(w["cnn"])
+    for s in (0, 1, 8, 15):
+        check_cnn(out[0, s], O.ctx_cnn(c, seq[0], s))
+    m.close()
+
+
+def _score_both(w, S, N):
+    feat = synth.features(S, N, cond_dim=16, per_stream_seed=True)
+    kinds = ["sines", "uniform"]
+    tgt = np.concatenate([synth.target_signal(1, N, seed=4 + s, kind=kinds[s % 2]) for s in range(S)])
+    m = wavernn.Model(w, max_streams=S)
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, N, feat=feat, target=tgt, logits=True, nll=True)
+    return m, r, ref
+
+
+@pytest.mark.parametrize("B,S", [(4, 1), (4, 2), (2, 1)])
+def test_cnn_subscale_teacher_forced_small(B, S):
+    """Logits of every lane with the CNN's context (the whole table from the
+    targets, one launch of the horizon schedule) against the oracle, which
+    generates sub-tensor by sub-tensor."""
+    w = cnn_model(B=B)
+    m, r, ref = _score_both(w, S, B * 150)
+    assert m.path(S)[0] == "batched"
+    d = max(np.abs(r["zc"] - ref["zc"]).max(), np.abs(r["zf"] - ref["zf"]).max())
+    assert d <= 1e-3, d
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=2e-3)
+    m.close()
+
+
+def _check_draws_valid(z, u, k, delta=1e-3):
+    z = z.astype(np.float64)
+    k = np.asarray(k).astype(np.int64)
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    C = np.cumsum(p, axis=1)
+    idx = np.arange(len(k))
+    lo = np.where(k > 0, C[idx, np.maximum(k - 1, 0)], 0.0)
+    return (u >= lo - delta) & (u <= C[idx, k] + delta)
+
+
+def test_cnn_subscale_free_running_valid_and_independent_of_the_chunking():
+    """Sampling runs the CNN ahead in chunks of F - 123 steps (F = 130: 7-step
+    chunks over 493 steps).  Every draw is valid under the oracle's logits on
+    the GPU's trajectory, the final state hands over, and F = 170 (47-step
+    chunks, another schedule) draws the same samples bit for bit: the samples
+    do not depend on the lag or the chunking."""
+    B, N, S = 4, 4 * 100, 2
+    feat = synth.features(S, N, cond_dim=16, per_stream_seed=True)
+    outs = []
+    for F in (130, 170):
+        w = cnn_model(B=B, F=F)
+        m = wavernn.Model(w, max_streams=S)
+        fin = m.new_state(S)
+        outs.append(host(m.sample(N, cond=cuda(feat), seed=3, n_streams=S, final=fin)))
+        m.device_status()
+        fins = {k: host(v) for k, v in fin.items() if k != "t0"}
+        m.close()
+    np.testing.assert_array_equal(outs[0], outs[1])
+    out = outs[0]
+    ref = O.run(O.Weights.from_dict(w, bf16=True), S, N, feat=feat, target=out, logits=True)
+    for u in range(S):
+        for s in range(B):
+            n = np.arange(s, N, B)
+            U = np.array([O.uniforms(3, u * B + s, i) for i in range(N // B)])
+            okc = _check_draws_valid(ref["zc"][u][n], U[:, 0], out[u][n] >> 8)
+            okf = _check_draws_valid(ref["zf"][u][n], U[:, 1], out[u][n] & 255)
+            assert okc.all() and okf.all(), (u, s, np.flatnonzero(~okc)[:5], np.flatnonzero(~okf)[:5])
+            assert fins["c"][u * B + s] == out[u][n[-1]] >> 8 and fins["f"][u * B + s] == out[u][n[-1]] & 255
+    assert np.abs(fins["h"] - ref["h"]).max() <= 2e-2
+    assert all(len(np.unique(out[u])) > 100 for u in range(S))
+
+
+def test_subscale16_cnn_full_length_call():
+    """The benchmarked call (Subscale WaveRNN-896, B = 16, the paper's CNN
+    widths, 24,000 samples, 49 chunks of 100 steps): the CNN's table over the
+    generated audio equals the oracle's at sampled rows (a window of 125 rows
+    from the row on holds the whole reach), every sub-tensor is active to its
+    end, and the draws are valid under the library's own teacher-forced
+    logits on the same audio (which the smaller tests pin to the oracle)."""
+    w = synth.preset("subscale16_cnn")
+    N, B = w["samples"], 16
+    feat = synth.features(1, N)
+    m = wavernn.Model(w)
+    out = m.sample(N, cond=cuda(feat), seed=1)
+    m.device_status()
+    tab = host(m.ctx_cnn(out))
+    out = host(out)
+    c = oracle_cnn(w["cnn"])
+    rows = N // B
+    for s, k0 in ((1, 0), (15, 700), (8, rows - 130)):
+        win = out[0, B * k0:B * min(rows, k0 + 130)]
+        ref = O.ctx_cnn(c, win, s)
+        n = min(6, len(ref))
+        check_cnn(tab[0, s, k0:k0 + n], ref[:n])
+    for s in range(B):
+        assert len(np.unique(out[0, s::B][-200:])) > 50
+    r = m.score(cuda(out), cond=cuda(feat))
+    m.device_status()
+    zc, zf = host(r["zc"])[0], host(r["zf"])[0]
+    for s in (0, 7, 15):
+        n = np.arange(s, N, B)
+        U = np.array([O.uniforms(1, s, i) for i in range(rows)])
+        assert _check_draws_valid(zc[n], U[:, 0], out[0][n] >> 8).all()
+        assert _check_draws_valid(zf[n], U[:, 1], out[0][n] & 255).all()
+    m.close()

@@ -151,3 +151,51 @@ def test_ten_second_utterance_in_one_launch():
     np.testing.assert_array_equal(host(fin2["h"]), host(fin["h"]))
     assert np.abs(host(fin["h"])).max() <= 1.0
     assert len(np.unique(full)) > 5000
+
+
+@pytest.mark.parametrize("name", ["subscale16", "subscale16_h4"])
+def test_full_length_subscale_call_late_rows_match_the_oracle(name):
+    """The benchmarked 24,000-sample call to its last row: lanes 0 and 15 of
+    the GPU's own output replayed by the oracle (teacher-forced, those lanes
+    only: given the samples, lanes are independent) over all 1,500 rows,
+    through about 11 wraps of the units' 2,048-sample ring and, with the
+    horizon, the ramp-down.  The GPU's teacher-forced logits on the same
+    output match within the bf16 tolerance, and every draw of those lanes is
+    valid under the oracle's distribution at its Philox uniforms."""
+    w = synth.preset(name)
+    T, B = w["samples"], w["B"]
+    feat = synth.features(1, T)
+    m = wavernn.Model(w, dtype="bf16")
+    full = host(m.sample(T, cond=cuda(feat), seed=5))
+    r = {k: host(v) for k, v in m.score(cuda(full), cond=cuda(feat)).items()}
+    m.device_status()
+    W = O.Weights.from_dict(w, bf16=True)
+    for s_ in (0, B - 1):
+        print(f"late rows {name} lane {s_}", flush=True)
+        ref = O.run_lanes(W, 1, T, full, (s_, s_ + 1), feat=feat)
+        idx = np.arange(s_, T, B)
+        d = max(np.abs(r["zc"][0, idx] - ref["zc"][0, idx]).max(), np.abs(r["zf"][0, idx] - ref["zf"][0, idx]).max())
+        assert d <= BF16_TOL, (s_, d)
+        u = np.array([O.uniforms(5, s_, i) for i in range(T // B)])
+        okc = _valid(ref["zc"][0, idx], u[:, 0], full[0, idx] >> 8)
+        okf = _valid(ref["zf"][0, idx], u[:, 1], full[0, idx] & 255)
+        assert okc.all() and okf.all(), (s_, np.flatnonzero(~okc)[:5], np.flatnonzero(~okf)[:5])
+
+
+@pytest.mark.parametrize("F", [-1, 2])
+def test_subscale_b16_teacher_forced_after_the_ring_wraps(F):
+    """B = 16 at H = 128 over 3,200 samples: the units' sample ring (256 samples
+    lockstep, 1,024 with F = 2) wraps 12 or 3 times; every logit of every lane
+    matches the oracle."""
+    B, T = 16, 16 * 200
+    w = synth.make_weights(128, seed=2, cond_dim=16, B=B, ctx_dim=256)
+    w["F"] = F
+    feat = synth.features(1, T, cond_dim=16)
+    tgt = synth.target_signal(1, T, seed=6)
+    m = wavernn.Model(w, dtype="bf16")
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, T, feat=feat, target=tgt, logits=True, nll=True)
+    d = max(np.abs(r["zc"] - ref["zc"]).max(), np.abs(r["zf"] - ref["zf"]).max())
+    assert d <= 1e-3, d
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-4, atol=2e-3)

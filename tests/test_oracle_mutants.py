@@ -75,6 +75,10 @@ MUTANTS = {
     "fused_stream_index": ("(uint64_t)(2 * ut + s), 0, 0}", "(uint64_t)(ut + s), 0, 0}"),
     "fused_coarse_sees_current_bytes": ("fused_units(m, G, add, x, 4, h, hn, 0, 2 * Q);",
                                         "x[4] = 1.0f; fused_units(m, G, add, x, 6, h, hn, 0, 2 * Q);"),
+    "cnn_context_of_previous_sub_tensor": ("if (m->cnn) orc_ctx_cnn(m->cnn, tgt ? tgt : seq, T, (int32_t)o, ctab);",
+                                           "if (m->cnn) orc_ctx_cnn(m->cnn, tgt ? tgt : seq, T, (int32_t)(o > 0 ? o - 1 : 0), ctab);"),
+    "cnn_context_row_ahead": ("if (m->cnn) memcpy(ctx, ctab + (size_t)i * m->Dx,",
+                              "if (m->cnn) memcpy(ctx, ctab + (size_t)(i + 1 < rows ? i + 1 : i) * m->Dx,"),
     "cnn_past_taps": ("const int64_t kk = k + (int64_t)tap * d;", "const int64_t kk = k - (int64_t)tap * d;"),
     "cnn_dilation_stages_4": ("const int d = 1 << (l % 5);", "const int d = 1 << (l % 4);"),
     "cnn_sees_own_sub_tensor": ("const int seen = z < s;", "const int seen = z <= s;"),
@@ -100,6 +104,7 @@ PINS = [
     "test_fused_heads_read_their_own_quarter", "test_fused_dependencies_follow_the_fused_order",
     "test_cnn_shift_layers_sum_the_future_rows", "test_cnn_sees_only_previous_sub_tensors_within_124_rows_ahead",
     "test_cnn_first_sub_tensor_sees_nothing", "test_cnn_relu_clips_a_negative_layer",
+    "test_cnn_conditioned_subscale_dependencies", "test_cnn_with_zero_output_is_the_plain_subscale_model",
 ]
 
 _PARAMS = {"test_philox_matches_numpy": [dict(seed=7, stream=3, t=123456), dict(seed=1, stream=0, t=5)],

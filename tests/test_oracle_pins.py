@@ -157,6 +157,17 @@ def test_draw_point_mass_and_zero_probability_classes():
         assert 10 <= k < 20
 
 
+def test_draw_block_of_equal_classes_among_zero_probability_ones():
+    """Logits +100 on the four classes 37..40 and -200 elsewhere (max shift and
+    252 zero-probability classes): the running sums are 0 .. 0, 1, 2, 3, 4, so
+    the class is 37 + floor(4 U) exactly, at both ends of [0, 1) too."""
+    z = np.full(N, -200.0, np.float32)
+    z[37:41] = 100.0
+    for q in [0, 1, 2**22 - 1, 2**22, 2**23 + 5, 3 * 2**22, 2**24 - 1]:
+        u = q / 2.0**24
+        assert O.draw(z, u) == 37 + math.floor(4 * u)
+
+
 def test_draw_distribution_chi_square():
     from scipy import stats
     rng = np.random.default_rng(5)
@@ -769,6 +780,66 @@ def test_cnn_first_sub_tensor_sees_nothing():
     np.testing.assert_array_equal(out, zero)
 
 
+def _cnn_subscale(B=3, H=8, Dx=4, layers=2, seed=11):
+    """A tiny subscale WaveRNN (head biases positive, so the heads' relus pass)
+    conditioned by a tiny CNN (reach 2 + 4 = 6 rows)."""
+    rng = np.random.default_rng(seed)
+    d = zero_model(H=H, Dx=Dx, B=B)
+    for k in ("R", "I", "b", "O1", "O2", "b2", "O3", "O4", "b4", "Wx"):
+        d[k] = (rng.normal(0, 1.5, d[k].shape) / math.sqrt(max(1, d[k].shape[-1]))).astype(np.float32)
+    d["b1"][:] = 1.0
+    d["b3"][:] = 1.0
+    d["F"] = 6
+    d["cnn"] = cnn_model(B=B, Rc=5, Cc=4, Dx=Dx, layers=layers, seed=seed + 1)
+    return d
+
+
+def test_cnn_conditioned_subscale_dependencies():
+    """Brute force on the CNN-conditioned Subscale WaveRNN (teacher-forced):
+    change one sample (sub-tensor z, row k) and see which logits move.  Those
+    of sub-tensor s at position i move exactly when z < s and the change
+    reaches s's conditioning at some row j <= i (the CNN's own dependencies,
+    pinned above: rows k - 6 .. k here; earlier rows reach position i through
+    the state: Fig. 3's unbounded past, future horizon tied to the CNN's
+    receptive field), or z = s and k < i (its own past); the fine logits also
+    at k = i (the sample's own coarse byte).  Nothing else: not the sample's
+    own future, not a later sub-tensor."""
+    d = _cnn_subscale()
+    B, rows = 3, 12
+    N = B * rows
+    rng = np.random.default_rng(2)
+    tgt = rng.integers(0, 65536, (1, N)).astype(np.uint16)
+    base = O.run(W(d), 1, N, target=tgt, logits=True)
+    cb = [O.ctx_cnn(d["cnn"], tgt[0], s_) for s_ in range(B)]
+    for q in range(N):
+        t = tgt.copy()
+        t[0, q] ^= 0x8181
+        r = O.run(W(d), 1, N, target=t, logits=True)
+        k, z = divmod(q, B)
+        first = [np.flatnonzero(np.abs(O.ctx_cnn(d["cnn"], t[0], s_) - cb[s_]).max(axis=1) > 0) for s_ in range(B)]
+        for n in range(N):
+            i, s_ = divmod(n, B)
+            dep = (z < s_ and len(first[s_]) > 0 and first[s_].min() <= i) or (z == s_ and k < i)
+            mc = np.abs(r["zc"][0, n] - base["zc"][0, n]).max() > 0
+            mf = np.abs(r["zf"][0, n] - base["zf"][0, n]).max() > 0
+            assert mc == dep, ("coarse", q, n)
+            assert mf == (dep or q == n), ("fine", q, n)
+
+
+def test_cnn_with_zero_output_is_the_plain_subscale_model():
+    """A CNN whose output layer is zero gives every sub-tensor a zero context:
+    the run equals the same subscale model without context, which is the
+    interleaving of plain per-sub-tensor streams (pinned separately)."""
+    d = _cnn_subscale()
+    d["cnn"]["Wp"][:] = 0.0
+    d["cnn"]["bp"][:] = 0.0
+    plain = {k: v for k, v in d.items() if k not in ("cnn", "Wx")}
+    a = O.run(W(d), 2, 36, seed=4, nll=True)
+    b = O.run(W(plain), 2, 36, seed=4, nll=True)
+    np.testing.assert_array_equal(a["out"], b["out"])
+    np.testing.assert_array_equal(a["h"], b["h"])
+
+
 def test_cnn_relu_clips_a_negative_layer():
     """The shift network of one layer with bias -10 on the convolution: every
     pre-activation is below zero (|x| <= 1), relu gives 0, and the residual
@@ -783,3 +854,25 @@ def test_cnn_relu_clips_a_negative_layer():
     seq = np.random.default_rng(8).integers(0, 65536, rows * B).astype(np.uint16)
     out = O.ctx_cnn(m, seq, 1)[:, 0]
     np.testing.assert_array_equal(out, np.array([O.scale(int(v) >> 8) for v in seq[0::B]], np.float32))
+
+
+def test_lane_subset_equals_the_full_teacher_forced_run():
+    """With a target the subscale lanes are independent: a run over lanes
+    [2, 4) reproduces those lanes of the full run bit for bit, lockstep and
+    with a horizon (the test path that replays long subscale calls)."""
+    for F in (-1, 1):
+        d = zero_model(H=4, Dx=8, B=5)
+        rng = np.random.default_rng(9)
+        for k in ("R", "I", "b", "O1", "O2", "O3", "O4", "Wx"):
+            d[k] = rng.normal(0, 0.7, d[k].shape).astype(np.float32)
+        d["F"] = F
+        tgt = rng.integers(0, 65536, (2, 40)).astype(np.uint16)
+        full = O.run(W(d), 2, 40, target=tgt, logits=True, nll=True)
+        part = O.run_lanes(W(d), 2, 40, tgt, (2, 4))
+        for s_ in range(5):
+            idx = np.arange(s_, 40, 5)
+            if 2 <= s_ < 4:
+                np.testing.assert_array_equal(part["zc"][:, idx], full["zc"][:, idx])
+                np.testing.assert_array_equal(part["nll"][:, idx], full["nll"][:, idx])
+            else:
+                assert not part["zc"][:, idx].any()
