@@ -107,6 +107,44 @@ def cpu_baseline(w: dict, T: int, feat, budget_s: float = 12.0) -> dict:
             "sample": f"first {n} of the {T} samples of one utterance, single-threaded C oracle (gcc -O2)"}
 
 
+BF16_MFMA_PEAK_TFLOPS = 2500.0   # dense bf16 matrix-core peak of the MI355X
+
+
+def cnn_flops_per_row(w: dict) -> int:
+    """Algorithmic FLOPs of the conditioning CNN per row of one sub-tensor (2 per multiply-add)."""
+    c = w["cnn"]
+    Rc, B, Dx = c["Win"].shape[0], w["B"], c["Wp"].shape[0]
+    L = int(c["layers"])
+    Cc = c["bc"].shape[1] if L else 0
+    return 2 * (2 * B * Rc + L * (3 * Rc * Cc + Cc * Rc) + Rc * Dx)
+
+
+def cnn_table(m, w: dict, seq, reps: int = 5) -> dict:
+    """The conditioning CNN over the whole generated utterance(s), timed with
+    HIP events on the launch stream: its matrix-core roofline (bf16 dense peak)."""
+    import numpy as np
+    import torch
+    st = torch.cuda.current_stream()
+    m.ctx_cnn(seq)
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        m.ctx_cnn(seq)
+        b.record(st)
+        torch.cuda.synchronize()
+        ms.append(a.elapsed_time(b))
+    m.device_status()
+    rows = seq.shape[0] * seq.shape[1]                   # every row of every sub-tensor: S x B x N / B
+    flops = cnn_flops_per_row(w) * rows
+    t = float(np.median(ms)) / 1000.0
+    return {"rows": rows, "ms_median": round(float(np.median(ms)), 4), "gflop": round(flops / 1e9, 2),
+            "bound": "mfma", "achieved": round(flops / t / 1e12, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(flops / t / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+            "kernel": "wr_cnn_gemm (all 22 GEMMs of a table, plus wr_cnn_input)"}
+
+
 # In-kernel timestamps (trace slot -> phase end) of the step loop of head 0
 # (group 0 for the batched kernel), recorded by wavernn_set_trace.
 PHASES = {
@@ -231,7 +269,10 @@ def main() -> int:
     m.device_status()
     call_ms = [a.elapsed_time(b) for a, b in evs]
     # synchronization floor: the same grid and exchanged words per step, no arithmetic
-    floor_us = m.sync_floor(T // w["B"]) if path in ("persistent", "block-sparse", "fused") else None
+    # (the floor kernel gathers the fused heads' 64 nibble partials with every thread; it is not a lower
+    # bound for the fused kernel's one-wave gather, so fused models report none)
+    floor_us = (m.sync_floor(T // w["B"]) if path in ("persistent", "block-sparse", "batched", "concurrent")
+                and w.get("cnn") is None else None)
     ms = float(np.mean(call_ms))
     samples = S * T
     value = samples * args.steps / wall
@@ -266,11 +307,17 @@ def main() -> int:
         "call_ms_median": round(float(np.median(call_ms)), 4),
         "sync_floor": None if floor_us is None else {
             "us_per_step": round(floor_us, 4), "frac_of_step": round(floor_us / us_per_sample_step, 4)},
+        "limiter": ("cross-CU exchange latency: the weights stay in VGPRs and LDS, so the HBM roofline below is "
+                    "the weights' algorithmic bytes per step; the synchronization floor of the same launch "
+                    f"(its exchanges and waits, no arithmetic) takes {floor_us / us_per_sample_step:.0%} of the step")
+                   if floor_us is not None else None,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": traffic,
                      "kernel": kname, "bytes_per_step": wb, "steps_per_launch": steps_per_launch,
                      "lds_frac": round(achieved / lds_peak, 5)},
     }
+    if w.get("cnn") is not None:
+        line["cnn_table"] = cnn_table(m, w, out)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, T, feat_np)
     print(json.dumps(line), flush=True)

@@ -155,6 +155,7 @@ const void* wr_sparse_kernel_ptr(int KH, int GU);   // null if no instantiation
 const void* wr_cond_kernel_ptr();
 const void* wr_batch_kernel_ptr(int KH, bool ctx, int L, bool lag);   // null if no instantiation (KH, L vectors
                                                                       // per group, lag: a future-horizon schedule)
+const void* wr_batch_floor_kernel_ptr(int KH, bool ctx, int L, bool lag);   // null if no instantiation
 const void* wr_fill_kernel_ptr();
 const void* wr_fused_kernel_ptr(int KH);     // null if no instantiation
 const void* wr_floor_kernel_ptr();

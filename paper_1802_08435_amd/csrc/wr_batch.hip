@@ -162,7 +162,10 @@ __device__ __forceinline__ bool wait_sample(const xw* slots, int L, int SS, int 
 }
 
 // ------------------------------------------------------------------ head role
-template <int KH, bool CTX, int L, bool LAG>
+// FL: the synchronization floor of the launch (every exchange, wait, barrier
+// and sample word of the step, none of its arithmetic: no products, gates or
+// draws; values published as zero).
+template <int KH, bool CTX, int L, bool LAG, bool FL>
 __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   constexpr int NH = KH;
@@ -256,29 +259,34 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const int bl0 = 2 * (lane >> 4);                 // vectors of this lane's MFMA results: bl0, bl0 + 1
 
   auto first_layer = [&](const bf16x8* W, const unsigned char* img, float bias) {
-    f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+    if (!FL) {
+      f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
 #pragma unroll
-    for (int i = 0; i < KH; i += 2) {
-      acc0 = mfma(afrag(img, kc * KH + i), W[i], acc0);
-      if (i + 1 < KH) acc1 = mfma(afrag(img, kc * KH + i + 1), W[i + 1], acc1);
-    }
-    const int r = 16 * rt + (lane & 15);
-    if (bl0 < L) {                                  // lanes of vectors past L hold rows of zero inputs
-      op[(kc * L + bl0) * 64 + r] = mfma_row(acc0) + mfma_row(acc1);
-      op[(kc * L + bl0 + 1) * 64 + r] = mfma_row_hi(acc0) + mfma_row_hi(acc1);
+      for (int i = 0; i < KH; i += 2) {
+        acc0 = mfma(afrag(img, kc * KH + i), W[i], acc0);
+        if (i + 1 < KH) acc1 = mfma(afrag(img, kc * KH + i + 1), W[i + 1], acc1);
+      }
+      const int r = 16 * rt + (lane & 15);
+      if (bl0 < L) {                                // lanes of vectors past L hold rows of zero inputs
+        op[(kc * L + bl0) * 64 + r] = mfma_row(acc0) + mfma_row(acc1);
+        op[(kc * L + bl0 + 1) * 64 + r] = mfma_row_hi(acc0) + mfma_row_hi(acc1);
+      }
     }
     __syncthreads();
-    if (rb < L)
+    if (!FL && rb < L)
       aput(imo + (rr >> 5) * WR_FRAG, rr & 31, wr_relu((op[rb * 64 + rr] + op[(L + rb) * 64 + rr]) + bias), rb);
     __syncthreads();
   };
   // class tiles 2*wave, 2*wave+1 over this head's 64 columns, for all vectors
   auto second_layer = [&](const bf16x8* W, xw* dst, uint32_t tag) {
-    const bf16x8 x0 = afrag(imo, 0), x1 = afrag(imo, 1);
-    f32x4 A = mfma(x0, W[0], f32x4{0, 0, 0, 0});
-    f32x4 B = mfma(x0, W[2], f32x4{0, 0, 0, 0});
-    A = mfma(x1, W[1], A);
-    B = mfma(x1, W[3], B);
+    f32x4 A = {0, 0, 0, 0}, B = {0, 0, 0, 0};
+    if (!FL) {
+      const bf16x8 x0 = afrag(imo, 0), x1 = afrag(imo, 1);
+      A = mfma(x0, W[0], A);
+      B = mfma(x0, W[2], B);
+      A = mfma(x1, W[1], A);
+      B = mfma(x1, W[3], B);
+    }
     const int c0 = 32 * wave + (lane & 15);
     if (bl0 < L) {
       xpub(dst + bl0 * 256 + c0, tag, mfma_row(A));
@@ -406,6 +414,18 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       }
     }
     if (trg) trace_at(a, t, fine ? 12 : 11);
+    if (FL) {                                       // the exchange alone: own slice out, the others in
+      xpub((fine ? YF : YC) + sb * HH + su, tag, 0.0f);
+      uint32_t own = 0;
+#pragma unroll
+      for (int m = 0; m < KH; ++m)
+        if ((tid + WR_THREADS * m) % HH / 64 == j) own |= 1u << m;
+      __builtin_amdgcn_s_sleep(WR_POLL_DELAY);
+      if (!poll_put<KH>(fine ? YF : YC, [&](int m) { return (size_t)(tid + WR_THREADS * m); },
+                        [&](int, float) {}, tag, a, ~own))
+        misc[0] = 1;
+      return;
+    }
     if (fine) ccur = (int)gw[5];
     else if (t > 0) {
       cprev = (int)gw[5];
@@ -496,6 +516,10 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       if (trg) trace_at(a, t, 11);
 #pragma unroll 2
       for (int b = 0; b < L; ++b) {
+        if (FL) {
+          if (mine) xpub(YC + b * Hh + u, tag, 0.0f);
+          continue;
+        }
         const float cbe = gv[(3 * L + b) * 448 + u];
         const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]);
         const float uu = fsig(gv[(3 * b) * 448 + u] + __builtin_fmaf(ic[0][1], x1, ic[0][0] * x0));
@@ -525,8 +549,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (own) {
       float lse;
       const int forced = a.target ? (tgt[bs] >> 8) : -1;
-      const int c = draw_wave<false>(zs + wave * 256, nullptr, b2l, uni[bs].x, forced, zk + wave * 256,
-                                     a.nll_out ? &lse : nullptr);
+      const int c = FL ? 0 : draw_wave<false>(zs + wave * 256, nullptr, b2l, uni[bs].x, forced, zk + wave * 256,
+                                              a.nll_out ? &lse : nullptr);
       const int64_t pw = LAG ? t - misc[48 + bw] : t;   // this vector's position; an idle lane keeps its classes
       const bool act = actm >> bw & 1u;
       if (live && act && a.zc_out)
@@ -553,6 +577,10 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       if (trg) trace_at(a, t, 12);
 #pragma unroll 2
       for (int b = 0; b < L; ++b) {
+        if (FL) {
+          if (mine) xpub(YF + b * Hh + u, tag, 0.0f);
+          continue;
+        }
         const float cbe = gv[(3 * L + b) * 448 + u];
         const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]), x2 = fscale(misc[8 + b]);
         const float uu = fsig(gv[(3 * b) * 448 + u] +
@@ -584,8 +612,8 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (own) {
       float lse;
       const int forced = a.target ? (tgt[bs] & 255) : -1;
-      const int f = draw_wave<false>(zs + wave * 256, nullptr, b4l, uni[bs].y, forced, zk + wave * 256,
-                                     a.nll_out ? &lse : nullptr);
+      const int f = FL ? 0 : draw_wave<false>(zs + wave * 256, nullptr, b4l, uni[bs].y, forced, zk + wave * 256,
+                                              a.nll_out ? &lse : nullptr);
       const int c = misc[8 + bw];
       const int64_t pw = LAG ? t - misc[48 + bw] : t;
       const bool act = actm >> bw & 1u;
@@ -645,7 +673,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
 // Wave q < 4 owns coarse row tile 4k + q, wave 4 + q fine row tile 4k + q;
 // each lane of a wave's result holds two vectors of one row, which it
 // publishes (with bias + conditioning for the u and r gates).
-template <int KH, bool CTX, int L, bool LAG>
+template <int KH, bool CTX, int L, bool LAG, bool FL>
 __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   const BatchPlan& P = a.P;
@@ -698,6 +726,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   auto phase_c = [&]() {
     acc0 = f32x4{0, 0, 0, 0};
     acc1 = f32x4{0, 0, 0, 0};
+    if (FL) return;
 #pragma unroll
     for (int x = 0; x < KT; x += 2) {
       const bf16x8 w0 = fw ? WR[x] : *(const bf16x8*)(WL + x * WR_FRAG + lane * 16);
@@ -710,6 +739,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   };
   // fine inputs (image tiles KT .. 2KT-1)
   auto phase_f = [&]() {
+    if (FL) return;
 #pragma unroll
     for (int x = 0; x < KT; x += 2) {
       const bf16x8 w0 = fw ? *(const bf16x8*)(WL + x * WR_FRAG + lane * 16) : WR[x];
@@ -779,7 +809,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       }
     }
     __syncthreads();
-    if (misc[0]) return;
+    if (misc[0] || FL) return;                         // (the floor: the sample waits, not the context)
     const int half = a.P.KX * 16;                      // context samples per vector
     for (int x = tid; x < L * half; x += WR_THREADS) {
       const int b = x / half, jj = x % half;
@@ -869,7 +899,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
       const int x = tid + m * WR_THREADS;
-      if (x < L * Hh && !(pending >> m & 1u)) {
+      if (!FL && x < L * Hh && !(pending >> m & 1u)) {
         const int b = x / Hh, col = x % Hh;
         aput(img + (kt0 + (col >> 5)) * WR_FRAG, col & 31, y[m], b);
       }
@@ -912,20 +942,39 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
 
 }  // namespace
 
-template <int KH, bool CTX, int L, bool LAG>
+template <int KH, bool CTX, int L, bool LAG, bool FL>
 __global__ __launch_bounds__(WR_THREADS, 1) void wr_batch_kernel(BatchArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   int g = 0;
   const int r = wr_batch_role(a.P, blockIdx.x, &g);
   if (r < 0) return;
-  if (r < a.P.NH) bhead_role<KH, CTX, L, LAG>(a, g, r, lds);
-  else bunit_role<KH, CTX, L, LAG>(a, g, r - a.P.NH, lds);
+  if (r < a.P.NH) bhead_role<KH, CTX, L, LAG, FL>(a, g, r, lds);
+  else bunit_role<KH, CTX, L, LAG, FL>(a, g, r - a.P.NH, lds);
 }
 
 template <int KH, int L>
 static const void* batch_ptr_l(bool ctx, bool lag) {
-  if (!ctx) return (const void*)wr_batch_kernel<KH, false, L, false>;
-  return lag ? (const void*)wr_batch_kernel<KH, true, L, true> : (const void*)wr_batch_kernel<KH, true, L, false>;
+  if (!ctx) return (const void*)wr_batch_kernel<KH, false, L, false, false>;
+  return lag ? (const void*)wr_batch_kernel<KH, true, L, true, false>
+             : (const void*)wr_batch_kernel<KH, true, L, false, false>;
+}
+
+// The synchronization floor of the batched launches (WaveRNN-896 and the
+// smallest plan only).
+template <int KH, int L>
+static const void* floor_ptr_l(bool ctx, bool lag) {
+  if (!ctx) return (const void*)wr_batch_kernel<KH, false, L, false, true>;
+  return lag ? (const void*)wr_batch_kernel<KH, true, L, true, true>
+             : (const void*)wr_batch_kernel<KH, true, L, false, true>;
+}
+
+const void* wr_batch_floor_kernel_ptr(int KH, bool ctx, int L, bool lag) {
+  if (lag && !ctx) return nullptr;
+  if (KH == 7) return L == 2 ? floor_ptr_l<7, 2>(ctx, lag) : L == 4 ? floor_ptr_l<7, 4>(ctx, lag)
+                      : L == 8 ? floor_ptr_l<7, 8>(ctx, lag) : nullptr;
+  if (KH == 1) return L == 2 ? floor_ptr_l<1, 2>(ctx, lag) : L == 4 ? floor_ptr_l<1, 4>(ctx, lag)
+                      : L == 8 ? floor_ptr_l<1, 8>(ctx, lag) : nullptr;
+  return nullptr;
 }
 
 template <int KH>

@@ -1,8 +1,7 @@
 // Synchronization floor of the persistent kernels: the same grid, roles and
 // exchanged words per step as the batch-1 kernel of a plan (dense or
 // block-sparse), with no arithmetic.  Per step and half each head publishes
-// its slice of y and its partial logits (256, or 64 nibble logits for the
-// fused 2x heads) and waits for the partials of every
+// its slice of y and 256 partial logits and waits for the partials of every
 // slice (the two all-reduces on the critical path of a step); it also reads
 // the gate words of the half(s) it serves, without waiting, as the sampling
 // kernel reads them ahead.  Each unit workgroup reads both halves of h from
@@ -46,41 +45,29 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   // would keep 512 threads per head polling all the time and measure the
   // polling load instead)
   auto gather = [&](const xw* src, uint32_t tag) {
-    if (P.x_ps == 64) {   // fused 2x heads: the draw wave alone sums, lane v polling partial v of every slice
-      if (wave == 7) {
-        __builtin_amdgcn_s_sleep(6);
-        float s;
-        if (!sum_parts<16>(src, P.x_ps, 0, NK, lane, tag, &s, a)) misc[0] = 1;
-        else zs[lane] = s;
-      }
-      return;
-    }
     {
       float y;
       const int jj = lane < NK ? lane : 0;
-      if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + P.x_ps - 1, tag, &y, a)) misc[0] = 1;
+      if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + 255, tag, &y, a)) misc[0] = 1;
     }
     const int v = tid & 255, hh = tid >> 8, h0 = (NK + 1) / 2;
     float s;
-    if (v < P.x_ps) {
-      if (!sum_parts<16>(src, P.x_ps, hh ? h0 : 0, hh ? NK : h0, v, tag, &s, a)) misc[0] = 1;
-      else zs[hh * 256 + v] = s;
-    }
+    if (!sum_parts<16>(src, P.x_ps, hh ? h0 : 0, hh ? NK : h0, v, tag, &s, a)) misc[0] = 1;
+    else zs[hh * 256 + v] = s;
   };
-  const int pw = P.x_ps / 8;                     // partial logits each wave publishes (256 or, fused 2x, 64)
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     if (coarse) gate_words(GA);
     if (coarse && wave == 7)
       for (int i = lane; i < HR; i += 64) xpub(YC + HR * jk + i, tag, 0.0f);
-    if (coarse && lane < pw) xpub(PC + (size_t)jk * P.x_ps + pw * wave + lane, tag, 0.0f);
+    if (coarse && lane < 32) xpub(PC + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
     gather(PC, tag);
     __syncthreads();
     if (misc[0]) return;
     if (fine) gate_words(GF);
     if (fine && wave == 7)
       for (int i = lane; i < HR; i += 64) xpub(YF + HR * jk + i, tag, 0.0f);
-    if (fine && lane < pw) xpub(PF + (size_t)jk * P.x_ps + pw * wave + lane, tag, 0.0f);
+    if (fine && lane < 32) xpub(PF + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
     gather(PF, tag);
     __syncthreads();
     if (misc[0]) return;

@@ -512,28 +512,23 @@ wavernn_status build_fused(wavernn_model* m, const wavernn_weights* w) {
   return check_coresident(m, m->pk, P.grid, P.lds, "fused");
 }
 
-// Block-sparse R (Sec. 3.2): the kept entries of every row as records of the
-// block-sparse unit workgroups (layout in sparse_plan).  Rows per unit SR is
-// the first of 32, 64, 128, 16 whose records fit LDS and whose grid fits
-// (fewer rows per unit: shorter record walks on the way to the heads).
+// Block-sparse R (Sec. 3.2) as the block-sparse units store it (layout in
+// sparse_plan): per unit and half of the columns, the kept blocks of each
+// block-row dealt to the SL parts of its rows in turn, one u16 block-column
+// index per kept block, and each lane's row of the block's weights.  Rows per
+// unit SR is the first of 32, 64, 128, 16 whose blocks fit LDS and whose grid
+// fits (fewer rows per unit: shorter walks on the way to the heads).
 wavernn_status build_sparse(wavernn_model* m, const wavernn_weights* w) {
   const wavernn_config& c = m->cfg;
   const int H = c.hidden, Hh = H / 2;
   const int bh = c.r_format == WAVERNN_R_BSR_4X4 ? 4 : 16, bw = c.r_format == WAVERNN_R_BSR_4X4 ? 4 : 1;
-  // kept entries (column, bf16 weight) of every row, coarse and fine columns apart, in column order
-  std::vector<std::vector<uint32_t>> ent((size_t)6 * H);
-  size_t maxlen[2] = {0, 0};
-  for (int row = 0; row < 3 * H; ++row) {
-    const int g = row / H, i = row % H;
-    const uint8_t* mrow = w->R_block_mask + ((size_t)g * (H / bh) + i / bh) * (H / bw);
-    for (int bc = 0; bc < H / bw; ++bc) {
-      if (!mrow[bc]) continue;
-      for (int cc = 0; cc < bw; ++cc) {
-        const int col = bc * bw + cc;
-        ent[(size_t)2 * row + (col >= Hh)].push_back((uint32_t)col | (uint32_t)f2bf(w->R[(size_t)row * H + col]) << 16);
-      }
-    }
-    for (int ph = 0; ph < 2; ++ph) maxlen[ph] = std::max(maxlen[ph], ent[(size_t)2 * row + ph].size());
+  // kept block columns of every block-row (gate g, block-row i / bh), coarse and fine columns apart
+  const int nbr = 3 * H / bh;
+  std::vector<std::vector<uint16_t>> kept((size_t)2 * nbr);
+  for (int r = 0; r < nbr; ++r) {
+    const uint8_t* mrow = w->R_block_mask + (size_t)r * (H / bw);
+    for (int bc = 0; bc < H / bw; ++bc)
+      if (mrow[bc]) kept[(size_t)2 * r + (bc * bw >= Hh)].push_back((uint16_t)(bc * bw));
   }
   hipDeviceProp_t prop;
   HIPOK(hipGetDeviceProperties(&prop, m->device));
@@ -541,8 +536,9 @@ wavernn_status build_sparse(wavernn_model* m, const wavernn_weights* w) {
   bool ok = false;
   for (int SR : {32, 64, 128, 16}) {
     const int SL = 256 / SR;
-    auto nrec = [&](size_t len) { return std::max(1, (int)((len + SL - 1) / SL + 3) / 4); };
-    if (sparse_plan(H, SR, nrec(maxlen[0]), nrec(maxlen[1]), &P) && P.grid <= prop.multiProcessorCount) {
+    size_t nb[2] = {1, 1};   // longest part list per half
+    for (size_t q = 0; q < kept.size(); ++q) nb[q & 1] = std::max(nb[q & 1], (kept[q].size() + SL - 1) / SL);
+    if (sparse_plan(H, SR, bh, bw, (int)nb[0], (int)nb[1], &P) && P.grid <= prop.multiProcessorCount) {
       ok = true;
       break;
     }
@@ -550,33 +546,44 @@ wavernn_status build_sparse(wavernn_model* m, const wavernn_weights* w) {
   if (!ok) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: the kept blocks of R do not fit a block-sparse plan", H);
   m->pk = wr_sparse_kernel_ptr(P.KH, P.GU);
   if (!m->pk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no block-sparse kernel instantiation", H);
-  const int NR = P.NRC + P.NRF;
-  std::vector<uint32_t> recs((size_t)P.NU * NR * 256 * 4, 0);
-  for (int k = 0; k < P.NU; ++k)
-    for (int L = 0; L < 256; ++L) {
-      const int row = P.SR * k + L / P.SL, part = L % P.SL;
-      for (int ph = 0; ph < 2; ++ph) {
-        const std::vector<uint32_t>& E = ent[(size_t)2 * row + ph];
-        const int nr = ph ? P.NRF : P.NRC, r0 = ph ? P.NRC : 0;
-        for (int r = 0; r < nr; ++r) {
-          uint32_t col[4], wt[4];
-          for (int e = 0; e < 4; ++e) {
-            const size_t idx = (size_t)part + (size_t)P.SL * (4 * r + e);
-            col[e] = idx < E.size() ? (E[idx] & 0xffffu) : (uint32_t)(ph ? Hh : 0);
-            wt[e] = idx < E.size() ? (E[idx] >> 16) : 0u;
+  const int NR = P.NRC + P.NRF, SL = P.SL, BR = P.BR;
+  const size_t per = (size_t)P.u_lds_w / 2;            // u16 per unit block
+  std::vector<uint16_t> img((size_t)P.NU * per, 0);
+  for (int k = 0; k < P.NU; ++k) {
+    uint16_t* wt = img.data() + (size_t)k * per;               // [NR][256] x (4 or 1) bf16
+    uint16_t* ix = wt + P.u_wb / 2;                            // [NR][BR][SL]
+    for (int ph = 0; ph < 2; ++ph) {
+      const int nr = ph ? P.NRF : P.NRC, r0 = ph ? P.NRC : 0;
+      for (int R = 0; R < BR; ++R) {
+        const int br = (P.SR * k) / bh + R;                    // block-row over the stacked gates
+        const std::vector<uint16_t>& L = kept[(size_t)2 * br + ph];
+        for (int part = 0; part < SL; ++part)
+          for (int sl = 0; sl < nr; ++sl) {
+            const size_t b = (size_t)part + (size_t)SL * sl;   // this part's sl-th block of the block-row
+            const bool real = b < L.size();
+            const int col0 = real ? L[b] : (ph ? Hh : 0);
+            const int slot = r0 + sl, qd = slot / 4, qe = slot % 4;   // 16 x 1: quads of slots
+            if (bw == 4) ix[((size_t)slot * BR + R) * SL + part] = (uint16_t)col0;
+            else ix[(((size_t)qd * BR + R) * SL + part) * 4 + qe] = (uint16_t)col0;
+            for (int rb = 0; rb < bh; ++rb) {                  // the block-row's rows: lanes (R bh + rb) SL + part
+              const int lane = (R * bh + rb) * SL + part;
+              const int row = P.SR * k + R * bh + rb;
+              if (bw == 4) {
+                for (int e = 0; e < 4; ++e)
+                  wt[((size_t)slot * 256 + lane) * 4 + e] = real ? f2bf(w->R[(size_t)row * H + col0 + e]) : 0;
+              } else {
+                wt[((size_t)qd * 256 + lane) * 4 + qe] = real ? f2bf(w->R[(size_t)row * H + col0]) : 0;
+              }
+            }
           }
-          uint32_t* d = recs.data() + (((size_t)k * NR + r0 + r) * 256 + L) * 4;
-          d[0] = col[0] | col[1] << 16;
-          d[1] = col[2] | col[3] << 16;
-          d[2] = wt[0] | wt[1] << 16;
-          d[3] = wt[2] | wt[3] << 16;
-        }
       }
     }
+  }
   wavernn_status s;
-  if ((s = m->upload(&m->d_uw, recs.data(), recs.size() * 4)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_uw, img.data(), img.size() * 2)) != WAVERNN_OK) return s;
   if ((s = upload_common(m, w)) != WAVERNN_OK) return s;
   m->sparse = true;
+  (void)NR;
   return check_coresident(m, m->pk, P.grid, P.lds, "block-sparse");
 }
 
@@ -1223,6 +1230,76 @@ wavernn_status scratch_of(int dev, unsigned char** out, size_t* cap) {
   return WAVERNN_OK;
 }
 
+// Mean microseconds per step of one launch of `k` (HIP events on `st`).
+wavernn_status time_launch(wavernn_model* m, const void* k, int grid, int lds, void* arg, int64_t steps, double* us,
+                           hipStream_t st) {
+  void* args[] = {arg};
+  hipEvent_t e0, e1;
+  HIPOK(hipEventCreate(&e0));
+  HIPOK(hipEventCreate(&e1));
+  hipError_t he = hipEventRecord(e0, st);
+  if (he == hipSuccess) he = hipLaunchKernel(k, dim3(grid), dim3(WR_THREADS), args, lds, st);
+  if (he == hipSuccess) he = hipEventRecord(e1, st);
+  if (he == hipSuccess) he = hipEventSynchronize(e1);
+  float ms = 0.0f;
+  if (he == hipSuccess) he = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (he != hipSuccess) return fail(WAVERNN_E_HIP, "sync floor: %s", hipGetErrorString(he));
+  *us = (double)ms * 1000.0 / (double)steps;
+  return wavernn_device_status(m, st);
+}
+
+// The floor of the batched launch a call on max_streams utterances makes:
+// the batched kernel itself with its arithmetic compiled out (same plan,
+// grid, roles, exchanged words, class and sample words, waits and barriers).
+wavernn_status batch_floor(wavernn_model* m, int64_t n_steps, double* us, hipStream_t st) {
+  const int SB = m->cfg.subscale, V = m->cfg.max_streams * SB;
+  const int F = horizon_of(m->cfg), A = lead_of(m->cfg);
+  if (m->has_cnn) return fail(WAVERNN_E_UNSUPPORTED, "no sync floor for a model with a conditioning CNN");
+  BatchPlan B;
+  if (!batch_plan(m->cfg.hidden, V, &B, m->cfg.ctx_dim, SB, F, A))
+    return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors", V);
+  const void* k = wr_batch_floor_kernel_ptr(B.KH, B.KX > 0, B.L, F >= 0);
+  if (!k) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no batched floor instantiation", B.H);
+  wavernn_status s = check_coresident(m, k, B.grid, B.lds, "batched sync-floor");
+  if (s != WAVERNN_OK) return s;
+  const size_t cbn = (size_t)m->cfg.max_streams * 3 * B.H;   // one frame of bias + conditioning (zeros)
+  if (cbn > m->bcb_cap) {
+    float* p = nullptr;
+    if ((s = m->alloc(&p, cbn * 4)) != WAVERNN_OK) return s;
+    m->d_bcb = p;
+    m->bcb_cap = cbn;
+  }
+  if ((s = launch_fill((xw*)m->d_bcb, (int64_t)cbn, st)) != WAVERNN_OK) return s;
+  if ((s = launch_fill(m->d_bxc, (int64_t)B.G * B.x_words, st)) != WAVERNN_OK) return s;
+  BatchArgs a;
+  memset(&a, 0, sizeof a);
+  a.P = B;
+  a.hw = m->d_hw;
+  a.uw = m->d_buw;
+  a.ur = m->d_bur;
+  a.Iw = m->d_I;
+  a.b1 = m->d_b1;
+  a.b2 = m->d_b2;
+  a.b3 = m->d_b3;
+  a.b4 = m->d_b4;
+  a.ux = m->d_bux;
+  a.cb = m->d_bcb;
+  a.n_cb = 1;
+  a.frame_len = 1 << 30;
+  a.S = V;
+  a.B = SB;
+  a.F = F;
+  a.A = A;
+  a.rows = n_steps;
+  a.T = n_steps + (F >= 0 ? (int64_t)(SB - 1) * (F + 1 + A) : 0);
+  a.xc = m->d_bxc;
+  a.err = m->d_err;
+  a.limit = kWaitTicks;
+  return time_launch(m, k, B.grid, B.lds, &a, a.T, us, st);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1402,10 +1479,15 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
 wavernn_status wavernn_debug_sync_floor(wavernn_model* m, int64_t n_steps, double* us_per_step, void* stream) {
   if (!m || n_steps < 2 || n_steps > ((int64_t)1 << 31) || !us_per_step)
     return fail(WAVERNN_E_INVALID, "bad sync-floor arguments");
-  if (m->path != PATH_PERSIST) return fail(WAVERNN_E_UNSUPPORTED, "the sync floor exists for the persistent kernels only");
+  hipStream_t st = (hipStream_t)stream;
+  int32_t grid = 0, block = 0;
+  if (wavernn_model_path(m, m->cfg.max_streams, &grid, &block) == PATH_BATCHED) return batch_floor(m, n_steps, us_per_step, st);
+  if (m->path != PATH_PERSIST) return fail(WAVERNN_E_UNSUPPORTED, "no sync floor for the single-workgroup kernel");
+  if (m->fused)
+    return fail(WAVERNN_E_UNSUPPORTED, "the sync floor kernel exchanges 256 partial logits per slice, not the fused "
+                "heads' 64");
   const PersistPlan& P = m->plan;
   if ((3 * P.Hh) % P.NU) return fail(WAVERNN_E_UNSUPPORTED, "gate words do not split evenly over the units");
-  hipStream_t st = (hipStream_t)stream;
   const void* k = wr_floor_kernel_ptr();
   wavernn_status s = check_coresident(m, k, P.grid, P.lds, "sync-floor");
   if (s != WAVERNN_OK) return s;
@@ -1417,21 +1499,7 @@ wavernn_status wavernn_debug_sync_floor(wavernn_model* m, int64_t n_steps, doubl
   a.xc = m->d_xc;
   a.err = m->d_err;
   a.limit = kWaitTicks;
-  void* args[] = {&a};
-  hipEvent_t e0, e1;
-  HIPOK(hipEventCreate(&e0));
-  HIPOK(hipEventCreate(&e1));
-  hipError_t he = hipEventRecord(e0, st);
-  if (he == hipSuccess) he = hipLaunchKernel(k, dim3(P.grid), dim3(WR_THREADS), args, P.lds, st);
-  if (he == hipSuccess) he = hipEventRecord(e1, st);
-  if (he == hipSuccess) he = hipEventSynchronize(e1);
-  float ms = 0.0f;
-  if (he == hipSuccess) he = hipEventElapsedTime(&ms, e0, e1);
-  (void)hipEventDestroy(e0);
-  (void)hipEventDestroy(e1);
-  if (he != hipSuccess) return fail(WAVERNN_E_HIP, "sync floor: %s", hipGetErrorString(he));
-  *us_per_step = (double)ms * 1000.0 / (double)n_steps;
-  return wavernn_device_status(m, stream);
+  return time_launch(m, k, P.grid, P.lds, &a, n_steps, us_per_step, st);
 }
 
 wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps) {

@@ -85,8 +85,10 @@ struct PersistPlan {
                           // (HR / 32), gate units per gate thread
   int NH, NU, UCT, NCT;   // heads, units, row tiles per unit and half, row tiles per half (3 Hh / 16)
   int NK;                 // slices of O1 / O3 rows (Hh / HR): the partial logits per half
-  int SR, SL, NRC, NRF;   // block-sparse units: rows per unit, lanes per row, records per lane
+  int SR, SL, NRC, NRF;   // block-sparse units: rows per unit, lanes per row, block slots per lane
                           // (coarse columns, fine columns); 0 for the dense kernel
+  int BH, BW, BR, u_wb;   // block-sparse units: block shape (4 x 4 or 16 x 1), block-rows per unit,
+                          // bytes of the weights before the block-column indices
   int grid;               // workgroups launched: head j at block 8j, units on the others
   int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[2 KO], O4[2 KO]
   int u_lds_w;            // unit LDS block: dense R tiles, or the block-sparse records
@@ -119,6 +121,7 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->KO = 2;
   P->GU = 1;
   P->SR = P->SL = P->NRC = P->NRF = 0;
+  P->BH = P->BW = P->BR = P->u_wb = 0;
   P->NCT = 3 * P->Hh / 16;
   if (P->NH > 16 || P->Hh > WR_THREADS - 64) return false;   // the last wave draws, free of gate work
   P->hw_frags = 2 * P->KH + 8;
@@ -185,15 +188,21 @@ WR_HD inline bool fused_plan(int H, PersistPlan* P) {
 // GU = ceil(Hh / 448) gate slots per preparing thread (GU > 1: gate state in
 // LDS).
 // Unit k owns the SR consecutive R rows SR k .. SR k + SR - 1 (row order
-// g H + i, SR divides Hh, so a unit stays inside one gate and one half).
-// Waves 0-3 compute: SL = 256 / SR consecutive lanes share a row and each
-// walks its own list of records; a record is 4 (column, weight) pairs of the
-// row's kept entries (uint4: columns as 4 x u16, weights as 4 x bf16), the
-// row's entries dealt to its lanes in turn, in column order, padded with zero
-// weights.  Records sit in LDS as [NRC + NRF][256 lanes], coarse columns first.
-// Waves 4-7 read h from the heads and never store.
+// g H + i, SR divides Hh, so a unit stays inside one gate and one half): BR =
+// SR / BH block-rows of BH x BW blocks (4 x 4, or 16 x 1: 16 rows of one
+// column).  Waves 0-3 compute: SL = 256 / SR consecutive lanes share a row.
+// The kept blocks of a block-row in one half of the columns are dealt to the
+// SL parts in turn (block i to part i mod SL), so lane (row, part) walks the
+// same block list as the other rows of its block-row; each slot is one block:
+// one u16 block-column index shared by the block-row's lanes of that part
+// ([slot][BR][SL], the only index per kept block), and the lane's row of the
+// block's weights (4 bf16 for 4 x 4, 1 for 16 x 1) in [slot][256 lanes].
+// 16 x 1 slots go in quads, so one 8-byte read brings 4 weights or 4
+// indices: weights [slot / 4][256][4], indices [slot / 4][BR][SL][4].
+// Slots past a list's end hold zero weights.  Coarse-column slots come first,
+// then fine.  Waves 4-7 read h from the heads and never store.
 // ---------------------------------------------------------------------------
-WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
+WR_HD inline bool sparse_plan(int H, int SR, int BH, int BW, int NRC, int NRF, PersistPlan* P) {
   if (H <= 0 || H % 128) return false;
   P->H = H;
   P->Hh = H / 2;
@@ -208,10 +217,18 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
   P->GU = (P->Hh + 447) / 448;
   if (P->NH > 32 || P->GU > 3) return false;
   if (SR < 16 || SR > 256 || 256 % SR || P->Hh % SR || NRC < 1 || NRF < 1) return false;
+  if (!((BH == 4 && BW == 4) || (BH == 16 && BW == 1)) || SR % BH) return false;
+  if (BW == 1) {   // 16 x 1: slots in quads (4 weights and 4 indices per read)
+    NRC = (NRC + 3) / 4 * 4;
+    NRF = (NRF + 3) / 4 * 4;
+  }
   P->SR = SR;
   P->SL = 256 / SR;
   P->NRC = NRC;
   P->NRF = NRF;
+  P->BH = BH;
+  P->BW = BW;
+  P->BR = SR / BH;
   P->UCT = 0;
   P->NCT = 3 * P->Hh / 16;
   P->NU = 3 * H / SR;
@@ -223,8 +240,10 @@ WR_HD inline bool sparse_plan(int H, int SR, int NRC, int NRF, PersistPlan* P) {
   // uniforms [2][64][2], targets [2][64]
   P->lds_h = (P->KT + P->KO) * WR_FRAG +
              4 * (KC * P->HR + 3 * 256 + (P->GU > 1 ? 26 * P->Hh : P->Hh) + 16 + 256 + 128);
-  // unit LDS: records, h [H], misc [16]
-  P->u_lds_w = (NRC + NRF) * 256 * 16;
+  // unit LDS: block weights [NRC + NRF][256] (8 or 2 bytes each), block-column
+  // indices [NRC + NRF][BR][SL] (u16), h [H], misc [16]
+  P->u_wb = wr_rup((NRC + NRF) * 256 * (BW == 4 ? 8 : 2), 16);
+  P->u_lds_w = P->u_wb + wr_rup((NRC + NRF) * P->BR * P->SL * 2, 16);
   P->lds_u = P->u_lds_w + 4 * (H + 16);
   int g = 8 * (P->NH - 1) + 1;
   while (g - P->NH < P->NU) ++g;

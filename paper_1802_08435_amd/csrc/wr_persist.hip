@@ -504,17 +504,24 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_persist_kernel(PersistArgs a
 
 // ------------------------------------------------------------ block-sparse unit role
 // Unit k of a block-sparse R (Sec. 3.2): rows SR k .. SR k + SR - 1 of the
-// stacked gate matrices, SL lanes of waves 0-3 per row, each summing its own
-// kept entries (records in LDS) against h in LDS; waves 4-7 gather h.
+// stacked gate matrices, SL lanes of waves 0-3 per row, each walking its part
+// of its block-row's kept blocks (layout in sparse_plan) against h in LDS:
+// per 4 x 4 block one shared column index, the row's 4 weights and 4
+// consecutive h values (one 16-byte read); per 16 x 1 block the index, one
+// weight and one h value that all 16 rows of the block read (four blocks'
+// weights and indices per read); waves 4-7 gather h.
 __device__ __forceinline__ void sparse_unit_role(const PersistArgs& a, int k, unsigned char* lds) {
   const PersistPlan& P = a.P;
-  const int H = P.H, Hh = P.Hh, SL = P.SL, NRC = P.NRC, NRF = P.NRF;
+  const int H = P.H, Hh = P.Hh, SL = P.SL, NRC = P.NRC, NRF = P.NRF, BR = P.BR;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const uint4* rec = (const uint4*)lds;           // [NRC + NRF][256]
+  const unsigned char* wts = lds;                           // [NRC + NRF][256] block rows of weights
+  const uint16_t* bix = (const uint16_t*)(lds + P.u_wb);    // [NRC + NRF][BR][SL] block-column indices
   float* hv = (float*)(lds + P.u_lds_w);          // [H] h of the last step
   int* misc = (int*)(hv + H);
   const bool cw = tid < 256;                      // computing (and publishing) lanes
-  const int row = P.SR * k + (tid & 255) / SL;    // R row g H + i of a computing lane
+  const int ru = (tid & 255) / SL, part = tid % SL;   // row in the unit, part of its block-row's blocks
+  const int row = P.SR * k + ru;                  // R row g H + i of a computing lane
+  const int bro = ru / P.BH;                      // block-row in the unit
   const bool lead = cw && tid % SL == 0;
   const int g = row / H, i = row % H;
   const bool fine = i >= Hh;
@@ -527,15 +534,33 @@ __device__ __forceinline__ void sparse_unit_role(const PersistArgs& a, int k, un
   }
   __syncthreads();
   float acc = 0.0f;
+  const bool b44 = P.BW == 4;
   auto mac = [&](int r0, int n) {
-    const uint4* rp = rec + (size_t)r0 * 256 + tid;
+    const int L = tid & 255;
+    if (b44) {
+      const uint2* wp = (const uint2*)wts + (size_t)r0 * 256 + L;
 #pragma unroll 2
-    for (int r = 0; r < n; ++r) {
-      const uint4 q = rp[r * 256];
-      acc = __builtin_fmaf(bf_lo(q.z), hv[q.x & 0xffffu], acc);
-      acc = __builtin_fmaf(bf_hi(q.z), hv[q.x >> 16], acc);
-      acc = __builtin_fmaf(bf_lo(q.w), hv[q.y & 0xffffu], acc);
-      acc = __builtin_fmaf(bf_hi(q.w), hv[q.y >> 16], acc);
+      for (int r = 0; r < n; ++r) {
+        const int col0 = bix[((r0 + r) * BR + bro) * SL + part];
+        const uint2 q = wp[r * 256];
+        const float4 h4 = *(const float4*)(hv + col0);
+        acc = __builtin_fmaf(bf_lo(q.x), h4.x, acc);
+        acc = __builtin_fmaf(bf_hi(q.x), h4.y, acc);
+        acc = __builtin_fmaf(bf_lo(q.y), h4.z, acc);
+        acc = __builtin_fmaf(bf_hi(q.y), h4.w, acc);
+      }
+    } else {   // quads of slots: 4 weights, 4 indices per read (n, r0 multiples of 4)
+      const uint2* wq = (const uint2*)wts + (size_t)(r0 / 4) * 256 + L;
+      const uint2* iq = (const uint2*)bix + ((size_t)(r0 / 4) * BR + bro) * SL + part;
+#pragma unroll 2
+      for (int q = 0; q < n / 4; ++q) {
+        const uint2 w4 = wq[q * 256];
+        const uint2 i4 = iq[q * BR * SL];
+        acc = __builtin_fmaf(bf_lo(w4.x), hv[i4.x & 0xffffu], acc);
+        acc = __builtin_fmaf(bf_hi(w4.x), hv[i4.x >> 16], acc);
+        acc = __builtin_fmaf(bf_lo(w4.y), hv[i4.y & 0xffffu], acc);
+        acc = __builtin_fmaf(bf_hi(w4.y), hv[i4.y >> 16], acc);
+      }
     }
   };
   // coarse columns [0, Hh)

@@ -562,23 +562,27 @@ def test_block_sparse_streams_and_chunks():
         assert okc.all() and okf.all()
 
 
-@pytest.mark.parametrize("name", ["dense896", "sparse2048_4x4"])
+@pytest.mark.parametrize("name", ["dense896", "sparse2048_4x4", "multi64", "subscale16", "subscale16_h4"])
 def test_sync_floor_runs_below_the_step_time(name):
-    """The exchange-only kernel (same grid, same words per step) completes and
-    costs less per step than the sampling kernel it mirrors."""
+    """The exchange-only kernel (same grid, same words per step; for the
+    batched launches the batched kernel with its arithmetic compiled out)
+    completes and costs less per step than the sampling kernel it mirrors."""
     w = synth.preset(name)
-    m = wavernn.Model(w, dtype="bf16", r_format=_FMT.get(w["block"], "dense"))
-    floor = m.sync_floor(3000)
-    T = 3000
-    feat = cuda(synth.features(1, T))
+    S, B = w["streams"], w["B"]
+    m = wavernn.Model(w, dtype="bf16", r_format=_FMT.get(w["block"], "dense"), max_streams=S)
+    rows = 3000 // B * 10 if B > 1 else 3000
+    floor = m.sync_floor(rows)
+    T = B * rows
+    feat = cuda(synth.features(S, T, per_stream_seed=S > 1))
+    steps = rows + ((B - 1) * (w["F"] + 1) if w.get("F", -1) >= 0 else 0)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    m.sample(T, cond=feat, seed=1)
+    m.sample(T, cond=feat, seed=1, n_streams=S)
     e1.record()
     torch.cuda.synchronize()
     m.device_status()
-    step = e0.elapsed_time(e1) * 1000.0 / T
+    step = e0.elapsed_time(e1) * 1000.0 / steps
     assert 0.5 < floor < step, (floor, step)
 
 
