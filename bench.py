@@ -21,8 +21,6 @@ sys.path.insert(0, ROOT)
 METRIC = "audio samples/sec (xreal-time @24kHz) and us/step, WaveRNN-896 batch 1"
 PAPER_SAMPLES_PER_S = 96000.0   # WaveRNN-896 batch 1 on a P100 (Sec. 2.1); context, other hardware
 HBM_PEAK_GBS = 8000.0
-LDS_BYTES_PER_CLK_CU = 128
-CLOCK_GHZ = 2.4
 
 
 def weight_bytes_per_step(w: dict) -> int:
@@ -150,11 +148,11 @@ def cnn_table(m, w: dict, seq, reps: int = 5) -> dict:
 PHASES = {
     "persistent": [(1, "coarse gates (Eq. 2, with f_{t-1}) done, own y_c slice published"),
                    (2, "O1 rows + relu"), (3, "O2 columns: partial coarse logits published"),
-                   (15, "coarse partials of all heads received"), (4, "barrier"),
+                   (15, "coarse partials of all heads received (draw wave)"),
                    (16, "c_t drawn (draw wave)"), (5, "barrier: c_t known to all waves"),
                    (6, "fine gates (with c_t) done, own y_f slice published"), (7, "O3 rows + relu"),
-                   (8, "O4 columns: partial fine logits published"), (17, "fine partials of all heads received"),
-                   (9, "barrier"), (18, "f_t drawn (draw wave)"),
+                   (8, "O4 columns: partial fine logits published"),
+                   (17, "fine partials of all heads received (draw wave)"), (18, "f_t drawn (draw wave)"),
                    (10, "next step's coarse gate words received (end of step)")],
     "batched": [(11, "coarse gate words received"), (1, "coarse gates done, y_c of the group exchanged"),
                 (3, "O1/O2: partial coarse logits published"), (4, "owned vectors' coarse partials summed"),
@@ -162,7 +160,14 @@ PHASES = {
                 (6, "fine gates done, y_f of the group exchanged"), (8, "O3/O4: partial fine logits published"),
                 (9, "owned vectors' fine partials summed"), (10, "f_t drawn (end of step)")],
 }
-PHASES["block-sparse"] = PHASES["persistent"]
+PHASES["block-sparse"] = [(1, "coarse gates (Eq. 2, with f_{t-1}) done, own y_c slice published"),
+                          (2, "O1 rows + relu"), (3, "O2 columns: partial coarse logits published"),
+                          (15, "coarse partials of all heads received"), (4, "barrier"),
+                          (16, "c_t drawn (draw wave)"), (5, "barrier: c_t known to all waves"),
+                          (6, "fine gates (with c_t) done, own y_f slice published"), (7, "O3 rows + relu"),
+                          (8, "O4 columns: partial fine logits published"),
+                          (17, "fine partials of all heads received"), (9, "barrier"), (18, "f_t drawn (draw wave)"),
+                          (10, "next step's coarse gate words received (end of step)")]
 PHASES["fused"] = [(1, "coarse gates (last f of both sub-tensors) done, own y_c slice published"),
                    (3, "coarse MLPs: 64 partial nibble logits published"),
                    (16, "partials of all heads summed, 4 coarse nibbles drawn (draw wave)"),
@@ -238,6 +243,14 @@ def main() -> int:
     r_format = {None: "dense", (4, 4): "bsr4x4", (16, 1): "bsr16x1"}[w.get("block")]
     m = wavernn.Model(w, dtype="bf16" if w["bf16"] else "f32", r_format=r_format, max_streams=S)
     path, grid, block = m.path(S)
+    placement = None
+    if path in ("persistent", "block-sparse", "fused"):   # batch-1 launches: pick the XCDs of heads and units
+        tu = m.tune(n_steps=2048, rounds=2)
+        k, us = tu["chosen"], tu["us_per_step"]
+        placement = {"candidate": k, "heads_xcd": k // 8, "units_xcd": "all" if k % 8 == k // 8 else k % 8,
+                     "tune_us_per_step": round(us[k], 4), "default_us_per_step": round(us[0], 4),
+                     "candidates_timed": sum(1 for x in us if x > 0)}
+        path, grid, block = m.path(S)
     feat_np = synth.features(S, T, per_stream_seed=S > 1)
     feat = torch.from_numpy(feat_np).cuda()
     out = torch.empty(S, T, dtype=torch.uint16, device="cuda")
@@ -281,8 +294,6 @@ def main() -> int:
     us_per_sample_step = ms * 1000.0 / steps_per_launch
     wb = weight_bytes_per_step(w)
     achieved = wb * steps_per_launch / (ms / 1000.0) / 1e9
-    ncu = grid
-    lds_peak = ncu * LDS_BYTES_PER_CLK_CU * CLOCK_GHZ
     kname = KERNEL_OF.get(path, path)
     tb = measured_traffic(kname, args.config) if T == w["samples"] and S == w["streams"] else None
     traffic = None if tb is None else round(tb / (ms / 1000.0) / 1e9, 2)
@@ -305,6 +316,7 @@ def main() -> int:
         "x_realtime": round(value / 24000.0, 3),
         "call_ms_min": round(min(call_ms), 4),
         "call_ms_median": round(float(np.median(call_ms)), 4),
+        "placement": placement,
         "sync_floor": None if floor_us is None else {
             "us_per_step": round(floor_us, 4), "frac_of_step": round(floor_us / us_per_sample_step, 4)},
         "limiter": ("cross-CU exchange latency: the weights stay in VGPRs and LDS, so the HBM roofline below is "
@@ -313,8 +325,7 @@ def main() -> int:
                    if floor_us is not None else None,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": traffic,
-                     "kernel": kname, "bytes_per_step": wb, "steps_per_launch": steps_per_launch,
-                     "lds_frac": round(achieved / lds_peak, 5)},
+                     "kernel": kname, "bytes_per_step": wb, "steps_per_launch": steps_per_launch},
     }
     if w.get("cnn") is not None:
         line["cnn_table"] = cnn_table(m, w, out)

@@ -252,6 +252,35 @@ wavernn_status wavernn_debug_uniforms(uint64_t seed, uint64_t stream_id, int64_t
  * model. */
 int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* grid, int32_t* block);
 
+/* Placement of the workgroups of the multi-workgroup persistent kernels
+ * (paths 1, 3 and 5 of wavernn_model_path) among the 8 XCDs of the device.
+ * Workgroups exchange values every step through memory, and the latency of
+ * an exchange depends on where producer and consumer sit, in ways that
+ * differ from device to device.  Candidate i (0 <= i < 64) puts the head
+ * workgroups on XCD hx = i / 8 and the unit workgroups on XCD ux = i % 8
+ * (ux == hx: the units spread over every XCD, the default, candidate 0).
+ * A candidate fits when every workgroup of one launch can be resident at
+ * once; only launches that run one at a time use the placement (the
+ * concurrent launches of path 4 keep the default).  Results do not depend
+ * on the placement: only the time per step does.
+ *
+ * wavernn_tune: times `rounds` (1..16) rounds of one sampling launch of
+ * n_steps (16 .. 2^20) steps, zero conditioning, for each fitting candidate
+ * on `stream`, and keeps the fastest for later calls.  us_out [64] (host
+ * memory, or NULL) receives each candidate's best microseconds per step (-1
+ * where it does not fit), *chosen (or NULL) the candidate kept.  Waits for
+ * the stream; allocates and frees a few small device buffers; uses the
+ * model's exchange buffer (no other call on the model may overlap it).  A
+ * model on another path is left as it is (*chosen = -1).  Errors:
+ * E_INVALID, E_HIP, E_DEVICE (a bounded wait expired in a launch of the
+ * default placement). */
+wavernn_status wavernn_tune(wavernn_model* m, int64_t n_steps, int32_t rounds, float* us_out, int32_t* chosen,
+                            void* stream);
+/* Sets the placement to candidate i (as in wavernn_tune), -1 for the
+ * default.  E_INVALID if i is out of range or the candidate does not fit,
+ * E_UNSUPPORTED for a model on another path. */
+wavernn_status wavernn_set_placement(wavernn_model* m, int32_t candidate);
+
 /* Diagnostics: make later wavernn_sample / wavernn_score_teacher_forced calls
  * of the multi-workgroup persistent kernel record, for the first max_steps
  * steps of the first utterance, timestamps of the 100 MHz constant clock at

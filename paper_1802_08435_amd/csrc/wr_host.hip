@@ -78,6 +78,7 @@ struct wavernn_model {
   float* d_cb = nullptr;             // [cb_cap][3H] bias + conditioning per frame
   int64_t cb_cap = 0;
   xw* d_xc = nullptr;                // exchange words (zeroed as 64-bit pairs)
+  int solo_hx = 0, solo_uxm = 255;   // placement of launches that run one at a time (wavernn_tune)
   u64* trace = nullptr;
   int64_t trace_steps = 0;
   // concurrent batch-1 launches: a few utterances, each on its own persistent
@@ -922,10 +923,18 @@ wavernn_status run_small(wavernn_model* m, const RunIO& io) {
 }
 
 // One persistent launch for utterance s of the call, with exchange words xc
-// and bias + conditioning table cb, on stream st.
+// and bias + conditioning table cb, on stream st.  A launch that runs alone
+// (solo) takes the tuned placement, one of several side by side the default
+// spread of the units over the XCDs.
+PersistPlan solo_plan(const wavernn_model* m) {
+  PersistPlan P = m->plan;
+  wr_place(&P, m->solo_hx, m->solo_uxm);
+  return P;
+}
+
 wavernn_status launch_persist_one(wavernn_model* m, const RunIO& io, int s, xw* xc, float* cb, int64_t n_cb,
-                                  hipStream_t st) {
-  const PersistPlan& P = m->plan;
+                                  hipStream_t st, bool solo) {
+  const PersistPlan P = solo ? solo_plan(m) : m->plan;
   const int H = P.H, Dc = m->cfg.cond_dim;
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
   {
@@ -1008,14 +1017,14 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
     xw* xc;
     float* cb;
     wavernn_status st = carve_ws(io, 1, m->plan.x_words, (size_t)n_cb * 3 * m->plan.H, &xc, &cb);
-    for (int s = 0; s < io.S && st == WAVERNN_OK; ++s) st = launch_persist_one(m, io, s, xc, cb, n_cb, io.st);
+    for (int s = 0; s < io.S && st == WAVERNN_OK; ++s) st = launch_persist_one(m, io, s, xc, cb, n_cb, io.st, true);
     return st;
   }
   if (n_cb > m->cb_cap) HIPOK(hipStreamSynchronize(io.st));
   wavernn_status st = grow_cb(m, &m->d_cb, &m->cb_cap, n_cb);
   if (st != WAVERNN_OK) return st;
   for (int s = 0; s < io.S; ++s)
-    if ((st = launch_persist_one(m, io, s, m->d_xc, m->d_cb, n_cb, io.st)) != WAVERNN_OK) return st;
+    if ((st = launch_persist_one(m, io, s, m->d_xc, m->d_cb, n_cb, io.st, true)) != WAVERNN_OK) return st;
   return WAVERNN_OK;
 }
 
@@ -1053,10 +1062,10 @@ wavernn_status run_fanout(wavernn_model* m, const RunIO& io) {
   HIPOK(hipEventRecord(m->fan_fork, io.st));
   for (int s = 1; s < io.S; ++s) {
     HIPOK(hipStreamWaitEvent(m->fan_st[s - 1], m->fan_fork, 0));
-    if ((st = launch_persist_one(m, io, s, xc[s], cb[s], n_cb, m->fan_st[s - 1])) != WAVERNN_OK) return st;
+    if ((st = launch_persist_one(m, io, s, xc[s], cb[s], n_cb, m->fan_st[s - 1], false)) != WAVERNN_OK) return st;
     HIPOK(hipEventRecord(m->fan_join[s - 1], m->fan_st[s - 1]));
   }
-  if ((st = launch_persist_one(m, io, 0, xc[0], cb[0], n_cb, io.st)) != WAVERNN_OK) return st;
+  if ((st = launch_persist_one(m, io, 0, xc[0], cb[0], n_cb, io.st, false)) != WAVERNN_OK) return st;
   for (int s = 1; s < io.S; ++s) HIPOK(hipStreamWaitEvent(io.st, m->fan_join[s - 1], 0));
   return WAVERNN_OK;
 }
@@ -1467,7 +1476,7 @@ int32_t wavernn_model_path(const wavernn_model* m, int32_t n_streams, int32_t* g
   } else if (m->path == PATH_PERSIST && n_streams > 1 && m->has_batch && batch_plan(m->cfg.hidden, n_streams, &B)) {
     path = PATH_BATCHED, g = B.grid, b = WR_THREADS;
   } else if (m->path == PATH_PERSIST) {
-    g = m->plan.grid, b = WR_THREADS;
+    g = solo_plan(m).grid, b = WR_THREADS;
     if (m->sparse) path = PATH_SPARSE_ID;
     if (m->fused) path = PATH_FUSED_ID;
   }
@@ -1486,7 +1495,7 @@ wavernn_status wavernn_debug_sync_floor(wavernn_model* m, int64_t n_steps, doubl
   if (m->fused)
     return fail(WAVERNN_E_UNSUPPORTED, "the sync floor kernel exchanges 256 partial logits per slice, not the fused "
                 "heads' 64");
-  const PersistPlan& P = m->plan;
+  const PersistPlan P = solo_plan(m);
   if ((3 * P.Hh) % P.NU) return fail(WAVERNN_E_UNSUPPORTED, "gate words do not split evenly over the units");
   const void* k = wr_floor_kernel_ptr();
   wavernn_status s = check_coresident(m, k, P.grid, P.lds, "sync-floor");
@@ -1500,6 +1509,128 @@ wavernn_status wavernn_debug_sync_floor(wavernn_model* m, int64_t n_steps, doubl
   a.err = m->d_err;
   a.limit = kWaitTicks;
   return time_launch(m, k, P.grid, P.lds, &a, n_steps, us_per_step, st);
+}
+
+// Placement candidate i: heads on XCD i / 8, units on XCD i % 8 (all XCDs when equal).
+static void candidate_plan(const wavernn_model* m, int i, PersistPlan* P) {
+  *P = m->plan;
+  const int hx = i / 8, ux = i % 8;
+  wr_place(P, hx, ux == hx ? 255 : 1 << ux);
+}
+
+// Does one launch of the candidate fit the device at once (every XCD holds its
+// workgroups, and the grid the device)?
+static wavernn_status candidate_fits(const wavernn_model* m, int i, bool* fits) {
+  PersistPlan P;
+  candidate_plan(m, i, &P);
+  int per_cu = 0;
+  HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->pk, WR_THREADS, P.lds));
+  hipDeviceProp_t prop;
+  HIPOK(hipGetDeviceProperties(&prop, m->device));
+  const int per_xcd = per_cu * (prop.multiProcessorCount / 8);
+  int busy[8] = {};
+  for (int b = 0; b < P.grid; ++b)
+    if (wr_role(P, b) >= 0) ++busy[b % 8];
+  *fits = per_cu >= 1 && P.grid <= per_cu * prop.multiProcessorCount;
+  for (int x = 0; x < 8; ++x) *fits = *fits && busy[x] <= per_xcd;
+  return WAVERNN_OK;
+}
+
+wavernn_status wavernn_set_placement(wavernn_model* m, int32_t candidate) {
+  if (!m || candidate < -1 || candidate >= 64) return fail(WAVERNN_E_INVALID, "bad placement arguments");
+  if (m->path != PATH_PERSIST) return fail(WAVERNN_E_UNSUPPORTED, "the placement applies to the persistent kernels");
+  if (candidate < 0) candidate = 0;
+  bool fits = false;
+  wavernn_status s = candidate_fits(m, candidate, &fits);
+  if (s != WAVERNN_OK) return s;
+  if (!fits) return fail(WAVERNN_E_INVALID, "placement %d does not fit the device", candidate);
+  PersistPlan P;
+  candidate_plan(m, candidate, &P);
+  m->solo_hx = P.hx;
+  m->solo_uxm = P.uxm;
+  return WAVERNN_OK;
+}
+
+wavernn_status wavernn_tune(wavernn_model* m, int64_t n_steps, int32_t rounds, float* us_out, int32_t* chosen,
+                            void* stream) {
+  if (!m || n_steps < 16 || n_steps > ((int64_t)1 << 20) || rounds < 1 || rounds > 16)
+    return fail(WAVERNN_E_INVALID, "bad tune arguments");
+  if (chosen) *chosen = -1;
+  if (us_out)
+    for (int i = 0; i < 64; ++i) us_out[i] = -1.0f;
+  if (m->path != PATH_PERSIST) return WAVERNN_OK;
+  hipStream_t st = (hipStream_t)stream;
+  bool fits[64];
+  for (int i = 0; i < 64; ++i) {
+    wavernn_status s = candidate_fits(m, i, &fits[i]);
+    if (s != WAVERNN_OK) return s;
+  }
+  // one utterance of zero conditioning frames; a fused launch makes 2 samples a step
+  const int64_t T = m->fused ? 2 * n_steps : n_steps;
+  const int Dc = m->cfg.cond_dim, frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
+  const int64_t n_frames = Dc > 0 ? (T - 1) / frame_len + 1 : 0;
+  const int64_t steps = m->fused ? n_steps + m->cfg.future_horizon + 1 : n_steps;
+  float* cond = nullptr;
+  uint16_t* out = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  const int hx0 = m->solo_hx, uxm0 = m->solo_uxm;
+  u64* trace = m->trace;
+  float best[64];
+  for (int i = 0; i < 64; ++i) best[i] = 1e30f;
+  wavernn_status s = WAVERNN_OK;
+  auto step = [&](hipError_t e) {
+    if (e != hipSuccess && s == WAVERNN_OK) s = fail(WAVERNN_E_HIP, "HIP error %s in wavernn_tune", hipGetErrorString(e));
+    return s == WAVERNN_OK;
+  };
+  m->trace = nullptr;
+  if (step(hipMalloc((void**)&out, (size_t)T * 2)) && (Dc == 0 || step(hipMalloc((void**)&cond, (size_t)n_frames * Dc * 4))) &&
+      (Dc == 0 || step(hipMemsetAsync(cond, 0, (size_t)n_frames * Dc * 4, st))) &&
+      step(hipEventCreate(&e0)) && step(hipEventCreate(&e1))) {
+    RunIO io{1, T, cond, n_frames, 1, nullptr, nullptr, nullptr, out, nullptr, nullptr, nullptr, st};
+    // round -1 warms up (code objects, tables) on the default placement
+    for (int r = -1; r < rounds && s == WAVERNN_OK; ++r)
+      for (int i = 0; i < 64 && s == WAVERNN_OK; ++i) {
+        if (!fits[i] || (r < 0 && i > 0)) continue;
+        PersistPlan P;
+        candidate_plan(m, i, &P);
+        m->solo_hx = P.hx;
+        m->solo_uxm = P.uxm;
+        if (!step(hipEventRecord(e0, st))) break;
+        if ((s = run_persist(m, io)) != WAVERNN_OK) break;
+        float ms = 0.0f;
+        if (!step(hipEventRecord(e1, st)) || !step(hipEventSynchronize(e1)) || !step(hipEventElapsedTime(&ms, e0, e1))) break;
+        unsigned err = 0;
+        if (!step(hipMemcpy(&err, m->d_err, 4, hipMemcpyDeviceToHost))) break;
+        if (err) {   // a wait expired: the candidate is out (the default placement is not)
+          if (!step(hipMemset(m->d_err, 0, 64))) break;
+          if (i == 0) s = fail(WAVERNN_E_DEVICE, "a bounded wait expired in a launch of the default placement");
+          fits[i] = false;
+          continue;
+        }
+        if (r >= 0) best[i] = std::min(best[i], ms * 1000.0f / (float)steps);
+      }
+  }
+  m->trace = trace;
+  m->solo_hx = hx0;
+  m->solo_uxm = uxm0;
+  if (s == WAVERNN_OK) {
+    int k = 0;
+    for (int i = 0; i < 64; ++i)
+      if (fits[i] && best[i] < best[k]) k = i;
+    if (us_out)
+      for (int i = 0; i < 64; ++i) us_out[i] = fits[i] ? best[i] : -1.0f;
+    PersistPlan P;
+    candidate_plan(m, k, &P);
+    m->solo_hx = P.hx;
+    m->solo_uxm = P.uxm;
+    if (chosen) *chosen = k;
+  }
+  if (e0) hipEventDestroy(e0);
+  if (e1) hipEventDestroy(e1);
+  hipStreamSynchronize(st);
+  if (out) hipFree(out);
+  if (cond) hipFree(cond);
+  return s;
 }
 
 wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps) {

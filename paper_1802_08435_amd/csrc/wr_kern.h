@@ -49,21 +49,11 @@ __device__ __forceinline__ float wave_maxf(float v) {
   return lane63(v);
 }
 
-// Inverse-CDF draw by one wave over z = (zs + zs2) + b (zs + b when !TWO), 4
-// classes per lane.  The logits are also written to zkeep[256].  Returns the
-// class, or `forced` when >= 0; *lse = max z + log sum exp(z - max).
-template <bool TWO = true>
-__device__ __forceinline__ int draw_wave(const float* zs, const float* zs2, float4 b, float u, int forced,
-                                         float* zkeep, float* lse) {
+// Inverse-CDF draw by one wave over z = p + b, classes 4 l .. 4 l + 3 on lane
+// l.  The logits are also written to zkeep[256].  Returns the class, or
+// `forced` when >= 0; *lse = max z + log sum exp(z - max).
+__device__ __forceinline__ int draw_z(float4 p, float4 b, float u, int forced, float* zkeep, float* lse) {
   const int l = threadIdx.x & 63;
-  float4 p = *(const float4*)(zs + 4 * l);
-  if (TWO) {
-    const float4 q = *(const float4*)(zs2 + 4 * l);
-    p.x += q.x;
-    p.y += q.y;
-    p.z += q.z;
-    p.w += q.w;
-  }
   float4 z4;
   z4.x = p.x + b.x;
   z4.y = p.y + b.y;
@@ -91,6 +81,21 @@ __device__ __forceinline__ int draw_wave(const float* zs, const float* zs2, floa
     count = last;
   }
   return count;
+}
+// draw_z over p = zs + zs2 (zs alone when !TWO), read from LDS.
+template <bool TWO = true>
+__device__ __forceinline__ int draw_wave(const float* zs, const float* zs2, float4 b, float u, int forced,
+                                         float* zkeep, float* lse) {
+  const int l = threadIdx.x & 63;
+  float4 p = *(const float4*)(zs + 4 * l);
+  if (TWO) {
+    const float4 q = *(const float4*)(zs2 + 4 * l);
+    p.x += q.x;
+    p.y += q.y;
+    p.z += q.z;
+    p.w += q.w;
+  }
+  return draw_z(p, b, u, forced, zkeep, lse);
 }
 
 // ---------------------------------------------------------------------------

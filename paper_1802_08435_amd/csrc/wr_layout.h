@@ -89,7 +89,8 @@ struct PersistPlan {
                           // (coarse columns, fine columns); 0 for the dense kernel
   int BH, BW, BR, u_wb;   // block-sparse units: block shape (4 x 4 or 16 x 1), block-rows per unit,
                           // bytes of the weights before the block-column indices
-  int grid;               // workgroups launched: head j at block 8j, units on the others
+  int grid;               // workgroups launched: head j at block 8j + hx, units on the others
+  int hx, uxm;            // placement: heads on XCD hx, units on the XCDs of the bits of uxm
   int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[2 KO], O4[2 KO]
   int u_lds_w;            // unit LDS block: dense R tiles, or the block-sparse records
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (32-bit words)
@@ -100,12 +101,31 @@ struct PersistPlan {
 WR_HD inline int wr_rup(int x, int m) { return (x + m - 1) / m * m; }
 
 // Block index of head j and the role of block b (head index, or unit index + NH, or -1 idle).
+// Placement.  Blocks are dealt round-robin over the 8 XCDs (block b runs on
+// XCD b % 8), so head j sits at block 8 j + hx, and bit x of uxm admits units
+// on the other blocks of XCD x.  Unit blocks below b:
+WR_HD inline int wr_units_below(const PersistPlan& P, int b) {
+  int n = (b / 8) * __builtin_popcount(P.uxm & 255) + __builtin_popcount(P.uxm & ((1 << (b % 8)) - 1));
+  if (P.uxm >> P.hx & 1) {
+    const int heads = (b + 7 - P.hx) / 8;   // blocks b' < b with b' % 8 == hx
+    n -= heads < P.NH ? heads : P.NH;
+  }
+  return n;
+}
+// The role of block b: head index, unit index + NH, or -1 (idle: returns at once).
 WR_HD inline int wr_role(const PersistPlan& P, int b) {
-  if (b % 8 == 0 && b / 8 < P.NH) return b / 8;
-  int before = (b + 7) / 8;                 // head blocks with index < b
-  if (before > P.NH) before = P.NH;
-  int k = b - before;
+  if (b % 8 == P.hx && b / 8 < P.NH) return b / 8;
+  if (!(P.uxm >> (b % 8) & 1)) return -1;
+  const int k = wr_units_below(P, b);
   return k < P.NU ? P.NH + k : -1;
+}
+// Set a placement and the smallest grid that holds every head and unit.
+WR_HD inline void wr_place(PersistPlan* P, int hx, int uxm) {
+  P->hx = hx;
+  P->uxm = uxm;
+  int g = 8 * (P->NH - 1) + hx + 1;
+  while (wr_units_below(*P, g) < P->NU) ++g;
+  P->grid = g;
 }
 
 WR_HD inline bool persist_plan(int H, PersistPlan* P) {
@@ -138,9 +158,7 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   }
   if (!P->UCT) return false;
   P->NU = P->NCT / P->UCT;
-  int g = 8 * (P->NH - 1) + 1;
-  while (g - P->NH < P->NU) ++g;
-  P->grid = g;
+  wr_place(P, 0, 255);
   int o = 0;
   auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
   P->x_yc = take(P->Hh);
@@ -245,9 +263,7 @@ WR_HD inline bool sparse_plan(int H, int SR, int BH, int BW, int NRC, int NRF, P
   P->u_wb = wr_rup((NRC + NRF) * 256 * (BW == 4 ? 8 : 2), 16);
   P->u_lds_w = P->u_wb + wr_rup((NRC + NRF) * P->BR * P->SL * 2, 16);
   P->lds_u = P->u_lds_w + 4 * (H + 16);
-  int g = 8 * (P->NH - 1) + 1;
-  while (g - P->NH < P->NU) ++g;
-  P->grid = g;
+  wr_place(P, 0, 255);
   int o = 0;
   auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
   P->x_yc = take(P->Hh);

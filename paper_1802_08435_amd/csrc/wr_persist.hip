@@ -221,6 +221,57 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (!sum_parts<NHP>(src, P.x_ps, hh ? NHP : 0, hh ? NK : NHP, v, tag, &s, a)) misc[0] = 1;
     else (hh ? zs2 : zs)[v] = s;
   };
+  // Without SPLIT the draw wave gathers alone: lane l reads classes 4 l ..
+  // 4 l + 3 of every slice as two 64-bit words and sums slices [0, NHP), then
+  // [NHP, NK), then adds the two (the sums and order of the two-thread gather,
+  // so every head draws the same class); the logits stay in registers and no
+  // barrier separates gather and draw, while waves 0-6 go on to the next gate
+  // terms (measured at H = 896: 4.94 us per step, against 5.13 with the
+  // two-thread gather and its barriers).
+  auto gather_wave = [&](const xw* src, uint32_t tag, float4* z) -> bool {
+    __builtin_amdgcn_s_sleep(6);
+    constexpr int NW = 2 * NK;
+    const xw* base = src + 4 * lane;
+    uint64_t w[NW];
+    uint32_t pending = 0;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) w[k] = xpeek2(base + (size_t)(k >> 1) * P.x_ps + 2 * (k & 1));
+#pragma unroll
+    for (int k = 0; k < NW; ++k)
+      if (!xok2(w[k], tag)) pending |= 1u << k;
+    if (pending) {
+      WaitBudget wb{wr_clock(), 0};
+      while (pending) {
+        if (!wait_ok(wb, a.err, a.limit, a.err)) {
+          *z = float4{0.0f, 0.0f, 0.0f, 0.0f};   // a valid draw follows; the step is abandoned after it
+          return false;
+        }
+#pragma unroll
+        for (int k = 0; k < NW; ++k)
+          if (pending >> k & 1u) {
+            const uint64_t x = xpeek2(base + (size_t)(k >> 1) * P.x_ps + 2 * (k & 1));
+            if (xok2(x, tag)) {
+              w[k] = x;
+              pending &= ~(1u << k);
+            }
+          }
+      }
+    }
+    float4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+      float4& d = k < NHP ? s0 : s1;
+      d.x += xval((xw)w[2 * k]);
+      d.y += xval((xw)(w[2 * k] >> 32));
+      d.z += xval((xw)w[2 * k + 1]);
+      d.w += xval((xw)(w[2 * k + 1] >> 32));
+    }
+    z->x = s0.x + s1.x;
+    z->y = s0.y + s1.y;
+    z->z = s0.z + s1.z;
+    z->w = s0.w + s1.w;
+    return true;
+  };
   // Philox blocks of steps t .. t+63 into batch buffer b, one step per lane of
   // the draw wave: the 64-bit multiplies cost the same for 64 lanes as for one
   auto fill_batch = [&](int64_t t, int b) {
@@ -390,17 +441,29 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 13);
     if (j > 0 && j < 8 && tid == WR_THREADS - 64) trace_at(a, t, 24 + j);
     // (3) coarse logits of all heads; this step's fine words are loaded
-    gather_logits(PC, tag);
-    if (trw) trace_at(a, t, 15);
+    if (SPLIT) {
+      gather_logits(PC, tag);
+      if (trw) trace_at(a, t, 15);
+    }
     if (t > 0) prefetch_fine(n);
-    __syncthreads();
-    if (misc[0]) return;
-    if (trw) trace_at(a, t, 4);
+    if (SPLIT) {
+      __syncthreads();
+      if (misc[0]) return;
+      if (trw) trace_at(a, t, 4);
+    }
     // (4) draw c_t on the draw wave; meanwhile the fine gates start
     if (wave == DW) {
       float lse;
       const int forced = a.target ? (tgt[bs] >> 8) : -1;
-      const int c = draw_wave(zs, zs2, b2l, uni[bs].x, forced, zk, a.nll_out ? &lse : nullptr);
+      int c = 0;
+      if (SPLIT) {
+        c = draw_wave(zs, zs2, b2l, uni[bs].x, forced, zk, a.nll_out ? &lse : nullptr);
+      } else {
+        float4 z;
+        if (!gather_wave(PC, tag, &z)) misc[0] = 1;
+        if (trw) trace_at(a, t, 15);
+        c = draw_z(z, b2l, uni[bs].x, forced, zk, a.nll_out ? &lse : nullptr);
+      }
       if (trw) trace_at(a, t, 16);
       if (j == 0 && a.zc_out) *(float4*)(a.zc_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {
@@ -446,16 +509,26 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     }
     if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 14);
     // (7) fine logits of all heads
-    gather_logits(PF, tag);
-    if (trw) trace_at(a, t, 17);
-    __syncthreads();
-    if (misc[0]) return;
-    if (trw) trace_at(a, t, 9);
+    if (SPLIT) {
+      gather_logits(PF, tag);
+      if (trw) trace_at(a, t, 17);
+      __syncthreads();
+      if (misc[0]) return;
+      if (trw) trace_at(a, t, 9);
+    }
     // (8) draw f_t on the draw wave; meanwhile the next coarse gates start
     if (wave == DW) {
       float lse;
       const int forced = a.target ? (tgt[bs] & 255) : -1;
-      const int f = draw_wave(zs, zs2, b4l, uni[bs].y, forced, zk, a.nll_out ? &lse : nullptr);
+      int f = 0;
+      if (SPLIT) {
+        f = draw_wave(zs, zs2, b4l, uni[bs].y, forced, zk, a.nll_out ? &lse : nullptr);
+      } else {
+        float4 z;
+        if (!gather_wave(PF, tag, &z)) misc[0] = 1;
+        if (trw) trace_at(a, t, 17);
+        f = draw_z(z, b4l, uni[bs].y, forced, zk, a.nll_out ? &lse : nullptr);
+      }
       if (trw) trace_at(a, t, 18);
       if (j == 0 && a.zf_out) *(float4*)(a.zf_out + t * WR_CLASSES + 4 * lane) = *(const float4*)(zk + 4 * lane);
       if (lane == 0) {

@@ -79,6 +79,10 @@ def lib():
         L.wavernn_set_trace.argtypes = [vp, vp, i64]
         L.wavernn_debug_sync_floor.restype = ctypes.c_int
         L.wavernn_debug_sync_floor.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_double), vp]
+        L.wavernn_tune.restype = ctypes.c_int
+        L.wavernn_tune.argtypes = [vp, i64, i32, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32), vp]
+        L.wavernn_set_placement.restype = ctypes.c_int
+        L.wavernn_set_placement.argtypes = [vp, i32]
         L.wavernn_model_path.restype = i32
         L.wavernn_model_path.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.wavernn_ctx_cnn_run.restype = ctypes.c_int
@@ -243,6 +247,19 @@ class Model:
 
     def device_status(self, stream=None):
         _check(lib().wavernn_device_status(self._h, _stream(stream)))
+
+    def tune(self, n_steps: int = 2048, rounds: int = 2, stream=None) -> dict:
+        """Time each placement of the persistent kernel's workgroups over the
+        XCDs and keep the fastest (include/wavernn.h, wavernn_tune): returns
+        {"chosen": candidate or -1, "us_per_step": [64] floats, -1 = does not fit}."""
+        us = (ctypes.c_float * 64)()
+        ch = ctypes.c_int32()
+        _check(lib().wavernn_tune(self._h, n_steps, rounds, us, ctypes.byref(ch), _stream(stream)))
+        return {"chosen": ch.value, "us_per_step": [float(x) for x in us]}
+
+    def set_placement(self, candidate: int):
+        """Candidate placement as in tune(); -1: the default."""
+        _check(lib().wavernn_set_placement(self._h, candidate))
 
     def sync_floor(self, n_steps: int = 20000, stream=None) -> float:
         """Microseconds per step of the persistent kernel's exchange pattern alone
