@@ -139,6 +139,30 @@ __device__ __forceinline__ uint64_t xpeek2(const xw* p) {
 }
 __device__ __forceinline__ bool xok2(uint64_t w, uint32_t tag) { return xok((xw)w, tag) && xok((xw)(w >> 32), tag); }
 
+// Four adjacent words (16-byte aligned) read by one 16-byte buffer load with
+// the coherence bit of the agent-scope loads above (sc1).  Each 32-bit word
+// of it is read whole, but the four need not be from one moment, so each
+// keeps its own tag.  The resource bounds every access to `bytes` from base
+// (reads beyond return zero).  The compiler takes such a load for a pure
+// function of its operands, so a polling loop must build the resource in
+// every round from a base it cannot see through (xopaque), or the loads are
+// hoisted out of the loop.
+typedef uint32_t xw4 __attribute__((ext_vector_type(4)));
+template <class T>
+__device__ __forceinline__ T* xopaque(T* p) {
+  asm volatile("" : "+s"(p));
+  return p;
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t xrsrc(const xw* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, 0, (int)bytes, 0x00020000);   // raw 32-bit data (gfx9)
+}
+__device__ __forceinline__ xw4 xpeek4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 16);   // cache policy 16: sc1
+}
+__device__ __forceinline__ bool xok4(xw4 w, uint32_t tag) {
+  return (((w.x ^ tag) | (w.y ^ tag) | (w.z ^ tag) | (w.w ^ tag)) & 1u) == 0;
+}
+
 // A value as a reader of the exchange sees it (so that state handed in by the
 // caller enters a computation exactly as the exchanged values do).
 __device__ __forceinline__ float xround(float v) { return __uint_as_float(__float_as_uint(v) & ~1u); }

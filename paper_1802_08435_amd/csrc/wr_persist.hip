@@ -222,23 +222,26 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     else (hh ? zs2 : zs)[v] = s;
   };
   // Without SPLIT the draw wave gathers alone: lane l reads classes 4 l ..
-  // 4 l + 3 of every slice as two 64-bit words and sums slices [0, NHP), then
-  // [NHP, NK), then adds the two (the sums and order of the two-thread gather,
-  // so every head draws the same class); the logits stay in registers and no
-  // barrier separates gather and draw, while waves 0-6 go on to the next gate
-  // terms (measured at H = 896: 4.94 us per step, against 5.13 with the
-  // two-thread gather and its barriers).
+  // 4 l + 3 of every slice with one 16-byte load (a wave's load covers whole
+  // cache lines) and sums slices [0, NHP), then [NHP, NK), then adds the two
+  // (the sums and order of the two-thread gather, so every head draws the
+  // same class); the logits stay in registers and no barrier separates
+  // gather and draw, while waves 0-6 go on to the next gate terms (measured
+  // at H = 896: 4.94 us per step, against 5.13 with the two-thread gather
+  // and its barriers).
   auto gather_wave = [&](const xw* src, uint32_t tag, float4* z) -> bool {
     __builtin_amdgcn_s_sleep(6);
-    constexpr int NW = 2 * NK;
-    const xw* base = src + 4 * lane;
-    uint64_t w[NW];
+    const uint32_t bytes = (uint32_t)(NK * P.x_ps * 4), lo = 16u * lane, ps = (uint32_t)P.x_ps * 4u;
+    xw4 w[NK];
     uint32_t pending = 0;
+    {
+      const __amdgpu_buffer_rsrc_t r = xrsrc(xopaque(src), bytes);
 #pragma unroll
-    for (int k = 0; k < NW; ++k) w[k] = xpeek2(base + (size_t)(k >> 1) * P.x_ps + 2 * (k & 1));
+      for (int k = 0; k < NK; ++k) w[k] = xpeek4(r, k * ps + lo);
+    }
 #pragma unroll
-    for (int k = 0; k < NW; ++k)
-      if (!xok2(w[k], tag)) pending |= 1u << k;
+    for (int k = 0; k < NK; ++k)
+      if (!xok4(w[k], tag)) pending |= 1u << k;
     if (pending) {
       WaitBudget wb{wr_clock(), 0};
       while (pending) {
@@ -246,14 +249,16 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
           *z = float4{0.0f, 0.0f, 0.0f, 0.0f};   // a valid draw follows; the step is abandoned after it
           return false;
         }
+        const __amdgpu_buffer_rsrc_t r = xrsrc(xopaque(src), bytes);
+        xw4 x[NK];
 #pragma unroll
-        for (int k = 0; k < NW; ++k)
-          if (pending >> k & 1u) {
-            const uint64_t x = xpeek2(base + (size_t)(k >> 1) * P.x_ps + 2 * (k & 1));
-            if (xok2(x, tag)) {
-              w[k] = x;
-              pending &= ~(1u << k);
-            }
+        for (int k = 0; k < NK; ++k)
+          if (pending >> k & 1u) x[k] = xpeek4(r, k * ps + lo);
+#pragma unroll
+        for (int k = 0; k < NK; ++k)
+          if ((pending >> k & 1u) && xok4(x[k], tag)) {
+            w[k] = x[k];
+            pending &= ~(1u << k);
           }
       }
     }
@@ -261,10 +266,10 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
       float4& d = k < NHP ? s0 : s1;
-      d.x += xval((xw)w[2 * k]);
-      d.y += xval((xw)(w[2 * k] >> 32));
-      d.z += xval((xw)w[2 * k + 1]);
-      d.w += xval((xw)(w[2 * k + 1] >> 32));
+      d.x += xval(w[k].x);
+      d.y += xval(w[k].y);
+      d.z += xval(w[k].z);
+      d.w += xval(w[k].w);
     }
     z->x = s0.x + s1.x;
     z->y = s0.y + s1.y;
