@@ -56,8 +56,8 @@ def kernel_source_digest() -> str:
 
 
 def measured_traffic(kernel: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 --pmc summary of this kernel and workload,
-    or None when the library sources changed since the counters were taken."""
+    """HBM bytes per call (its launches of the kernel) from the committed rocprofv3 --pmc summary of
+    this kernel and workload, or None when the library sources changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -68,7 +68,7 @@ def measured_traffic(kernel: str, workload: str):
     d = json.loads(text[i + 7:text.index("```", i + 7)])
     if d.get("kernel_source_sha256_16") != kernel_source_digest():
         return None
-    return d["fetch_bytes_per_launch"] + d["write_bytes_per_launch"]
+    return (d["fetch_bytes_per_launch"] + d["write_bytes_per_launch"]) * d.get("launches_per_call", 1)
 
 
 def cpu_baseline(w: dict, T: int, feat, budget_s: float = 12.0) -> dict:
@@ -216,6 +216,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration) and exit")
+    ap.add_argument("--placement", type=int, default=None, metavar="K",
+                    help="fix the batch-1 launches' placement to candidate K (wavernn_tune's numbering) instead "
+                         "of tuning it (-1: the default placement)")
     ap.add_argument("--phases", action="store_true",
                     help="only time the phases of one traced launch (in-kernel timestamps) and print them")
     args = ap.parse_args()
@@ -245,11 +248,16 @@ def main() -> int:
     path, grid, block = m.path(S)
     placement = None
     if path in ("persistent", "block-sparse", "fused"):   # batch-1 launches: pick the XCDs of heads and units
-        tu = m.tune(n_steps=2048, rounds=2)
-        k, us = tu["chosen"], tu["us_per_step"]
-        placement = {"candidate": k, "heads_xcd": k // 8, "units_xcd": "all" if k % 8 == k // 8 else k % 8,
-                     "tune_us_per_step": round(us[k], 4), "default_us_per_step": round(us[0], 4),
-                     "candidates_timed": sum(1 for x in us if x > 0)}
+        if args.placement is None:
+            tu = m.tune(n_steps=2048, rounds=2)
+            k, us = tu["chosen"], tu["us_per_step"]
+            placement = {"candidate": k, "tuned": True, "tune_us_per_step": round(us[k], 4),
+                         "default_us_per_step": round(us[0], 4), "candidates_timed": sum(1 for x in us if x > 0)}
+        else:
+            m.set_placement(args.placement)
+            k = max(args.placement, 0)
+            placement = {"candidate": k, "tuned": False}
+        placement.update(heads_xcd=k // 8, units_xcd="all" if k % 8 == k // 8 else k % 8)
         path, grid, block = m.path(S)
     feat_np = synth.features(S, T, per_stream_seed=S > 1)
     feat = torch.from_numpy(feat_np).cuda()
