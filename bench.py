@@ -294,6 +294,24 @@ def main() -> int:
     # bound for the fused kernel's one-wave gather, so fused models report none)
     floor_us = (m.sync_floor(T // w["B"]) if path in ("persistent", "block-sparse", "batched", "concurrent")
                 and w.get("cnn") is None else None)
+    # teacher-forced scoring of the last sampled utterance (logits of both heads and the NLL)
+    score = None
+    if path == "persistent" and S == 1:
+        m.score(out, cond=feat)
+        torch.cuda.synchronize()
+        sm = []
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            m.score(out, cond=feat)
+            b.record(stream)
+            torch.cuda.synchronize()
+            sm.append(a.elapsed_time(b))
+        m.device_status()
+        smed = float(np.median(sm))
+        score = {"call_ms_median": round(smed, 4), "samples_per_s": round(T / (smed / 1000.0), 1),
+                 "us_per_step": round(smed * 1000.0 / T, 4),
+                 "kernels": "wr_score_kernel (recurrence) + wr_cnn_gemm (output layers over all steps) + wr_score_nll"}
     ms = float(np.mean(call_ms))
     samples = S * T
     value = samples * args.steps / wall
@@ -325,6 +343,7 @@ def main() -> int:
         "call_ms_min": round(min(call_ms), 4),
         "call_ms_median": round(float(np.median(call_ms)), 4),
         "placement": placement,
+        "teacher_forced_score": score,
         "sync_floor": None if floor_us is None else {
             "us_per_step": round(floor_us, 4), "frac_of_step": round(floor_us / us_per_sample_step, 4)},
         "limiter": ("cross-CU exchange latency: the weights stay in VGPRs and LDS, so the HBM roofline below is "

@@ -223,7 +223,16 @@ wavernn_status wavernn_sample_noalloc(wavernn_model* m, int32_t n_streams, int64
  * each output pointer may be NULL.  Fused 2x models write 32 logits per
  * sample and byte instead of 256 (high nibble 16, then low nibble 16), and
  * the NLL is the sum over the sample's four nibbles.  Initial state as in wavernn_sample.
- * n_samples = 0 is valid (target_dev may then be NULL): nothing is launched. */
+ * n_samples = 0 is valid (target_dev may then be NULL): nothing is launched.
+ * One utterance of a dense model on the multi-workgroup persistent path
+ * (or several, one after another, on a model made for one) scores on a
+ * recurrence-only kernel (with the bytes given, a step only updates h: one
+ * exchange per step) and then runs the output layers over all steps as
+ * matrix-core GEMMs.  That path keeps h of every step (4 H bytes per sample)
+ * and the output layers' intermediates (4 (Hh rounded up to 128) + 2 KiB per
+ * sample, for at most 65,536 samples at a time) in model-owned buffers, grown
+ * the first time a longer call needs them; its initial state, conditioning
+ * and outputs are as above. */
 wavernn_status wavernn_score_teacher_forced(wavernn_model* m, int32_t n_streams, int64_t n_samples,
                                             const float* cond_dev, int64_t n_frames, const uint16_t* target_dev,
                                             const wavernn_state* init, float* logits_c_dev, float* logits_f_dev,

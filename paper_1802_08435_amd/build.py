@@ -11,7 +11,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libwavernn.so")
-SOURCES = ["wr_small.hip", "wr_persist.hip", "wr_fused.hip", "wr_batch.hip", "wr_floor.hip", "wr_cnn.hip", "wr_host.hip"]
+SOURCES = ["wr_small.hip", "wr_persist.hip", "wr_fused.hip", "wr_batch.hip", "wr_floor.hip", "wr_cnn.hip", "wr_score.hip",
+           "wr_host.hip"]
 ARCH = os.environ.get("WAVERNN_ARCH", "gfx950")
 
 

@@ -64,6 +64,29 @@ struct PersistArgs {
   int64_t rows;             // fused 2x model: positions per sub-tensor (samples / 2)
 };
 
+// Teacher-forced recurrence of the dense batch-1 model (wr_score.hip).
+struct ScoreArgs {
+  const uint4* w;           // [H/16][3][H/32][64 lanes] R fragments: workgroup k, gate g: rows g H + 16 k ..
+  const float* Iw;          // [3H][3], I* mask applied
+  const float* cb;          // [n_cb][3H] gate bias + conditioning per frame
+  int64_t n_cb;
+  int frame_len;
+  int H, Hh;
+  int64_t T, t0;
+  const uint16_t* target;   // [T]
+  const float* h_in;        // [H] or null
+  const uint8_t* c_in;
+  const uint8_t* f_in;
+  float* h_out;             // [H] or null
+  uint8_t* c_out;
+  uint8_t* f_out;
+  float* traj_c;            // [T][Hh] coarse half of h after each step
+  float* traj_f;            // [T][Hh] fine half
+  xw* xc;                   // [2][H] exchange words, zeroed before the launch
+  unsigned* err;
+  u64 limit;
+};
+
 struct BatchArgs {
   BatchPlan P;
   const uint4* hw;          // [NH][8 waves][hw_frags][64 lanes] head fragments (as PersistArgs::hw)
@@ -151,6 +174,8 @@ struct CnnInputArgs {
 const void* wr_small_kernel_ptr();
 const void* wr_uniforms_kernel_ptr();
 const void* wr_persist_kernel_ptr(int KH);   // null if no instantiation for KH
+const void* wr_score_kernel_ptr(int KT2);    // teacher-forced recurrence for H = 32 KT2; null if none
+const void* wr_score_nll_ptr();
 const void* wr_sparse_kernel_ptr(int KH, int GU);   // null if no instantiation
 const void* wr_cond_kernel_ptr();
 const void* wr_batch_kernel_ptr(int KH, bool ctx, int L, bool lag);   // null if no instantiation (KH, L vectors

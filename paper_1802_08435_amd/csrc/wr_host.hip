@@ -79,6 +79,19 @@ struct wavernn_model {
   int64_t cb_cap = 0;
   xw* d_xc = nullptr;                // exchange words (zeroed as 64-bit pairs)
   int solo_hx = 0, solo_uxm = 255;   // placement of launches that run one at a time (wavernn_tune)
+  // teacher-forced scoring on the dense batch-1 plan: the recurrence kernel, the
+  // output layers as GEMM fragments (O1 [NP][Hh], O2 [256][NP], O3, O4; NP = Hh
+  // rounded up to 128) and biases, and the buffers of a call
+  const void* sk = nullptr;
+  uint4* d_srw = nullptr;             // [H/16][3][H/32][64] R fragments of the scoring recurrence
+  uint4* d_sw = nullptr;
+  float* d_sb = nullptr;
+  size_t sw_off[4] = {}, sb_off[4] = {};
+  int sc_np = 0;
+  float* d_traj = nullptr;            // [2][rows][Hh] h after each step (coarse half, then fine half)
+  int64_t traj_cap = 0;               // rows
+  float *d_so = nullptr, *d_sz = nullptr;   // [rows][NP] first-layer output, [2][rows][256] logits
+  int64_t so_cap = 0;                       // rows of d_so and d_sz (at most one chunk of the output layers)
   u64* trace = nullptr;
   int64_t trace_steps = 0;
   // concurrent batch-1 launches: a few utterances, each on its own persistent
@@ -728,6 +741,57 @@ wavernn_status build_cnn(wavernn_model* m, const wavernn_ctx_cnn* n) {
   return WAVERNN_OK;
 }
 
+// LDS of the scoring recurrence: the operand image of h, [3][16] pre-activations, misc.
+int score_lds(int H) { return H / 32 * WR_FRAG + 48 * 4 + 64; }
+
+// Teacher-forced scoring on the dense batch-1 plan: the recurrence kernel
+// (the plan's units, heads that evaluate their own slices from the given
+// bytes) and the output layers as GEMM fragments for the matrix cores: O1 and
+// O3 with their rows padded to NP = Hh rounded up to 128, O2 and O4 with their
+// columns padded to NP, biases rounded like the sampling heads' and padded
+// with zeros (a padded first-layer row is relu(0) = 0 and meets a zero column).
+wavernn_status build_score(wavernn_model* m, const wavernn_weights* w) {
+  const PersistPlan& P = m->plan;
+  const int H = P.H, Hh = P.Hh, NP = (Hh + 127) / 128 * 128, KT2 = H / 32;
+  m->sk = wr_score_kernel_ptr(KT2);
+  if (!m->sk) return fail(WAVERNN_E_UNSUPPORTED, "hidden %d: no scoring kernel instantiation", H);
+  {   // recurrence: workgroup k, gate g holds rows g H + 16 k .. + 15 over every column tile
+    REff R{&m->cfg, w};
+    auto Rm = [&](int r, int c) { return R(r, c); };
+    std::vector<uint16_t> rw((size_t)H / 16 * 3 * KT2 * 512);
+    for (int k = 0; k < H / 16; ++k)
+      for (int g = 0; g < 3; ++g)
+        for (int kt = 0; kt < KT2; ++kt)
+          frag(rw.data() + ((size_t)(k * 3 + g) * KT2 + kt) * 512, Rm, [&](int r) { return g * H + 16 * k + r; },
+               32 * kt);
+    wavernn_status s = m->upload(&m->d_srw, rw.data(), rw.size() * 2);
+    if (s != WAVERNN_OK) return s;
+  }
+  Rounder rd{m->cfg.weight_dtype == WAVERNN_BF16};
+  std::vector<uint16_t> wv;
+  std::vector<float> bv;
+  const float* Os[4] = {w->O1, w->O2, w->O3, w->O4};
+  const float* bs[4] = {w->b1, w->b2, w->b3, w->b4};
+  for (int k = 0; k < 4; ++k) {
+    m->sw_off[k] = wv.size() / 8;
+    m->sb_off[k] = bv.size();
+    const float* O = Os[k];
+    if (k % 2 == 0) {
+      pack_gemm(wv, [&](int o, int q) { return o < Hh ? O[(size_t)o * Hh + q] : 0.0f; }, NP, Hh);
+      for (int o = 0; o < NP; ++o) bv.push_back(o < Hh ? rd(bs[k][o]) : 0.0f);
+    } else {
+      pack_gemm(wv, [&](int o, int q) { return q < Hh ? O[(size_t)o * Hh + q] : 0.0f; }, 256, NP);
+      for (int o = 0; o < 256; ++o) bv.push_back(rd(bs[k][o]));
+    }
+  }
+  m->sc_np = NP;
+  wavernn_status s;
+  if ((s = m->upload(&m->d_sw, wv.data(), wv.size() * 2)) != WAVERNN_OK) return s;
+  if ((s = m->upload(&m->d_sb, bv.data(), bv.size() * 4)) != WAVERNN_OK) return s;
+  HIPOK(hipFuncSetAttribute(wr_cnn_gemm_ptr(), hipFuncAttributeMaxDynamicSharedMemorySize, 2 * CNN_LDS_BUF));
+  return check_coresident(m, m->sk, H / 16, score_lds(H), "scoring");
+}
+
 // One CNN layer as a GEMM (see CnnGemmArgs).
 struct CnnRows {   // which utterance rows the blocks of a CNN run cover
   int B;
@@ -1028,6 +1092,95 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
   return WAVERNN_OK;
 }
 
+// Teacher-forced scoring of one or more utterances on the dense batch-1 plan
+// (Sec. 5's NLL; Eq. 2 with the bytes given).  Per utterance the scoring
+// kernel runs the recurrence and writes h after every step; then the output
+// layers of all steps run as GEMMs on the matrix cores (O2 relu(O1 y_c + b1)
+// + b2, the same for the fine half; up to 65,536 steps at a time) and the
+// NLL as one reduction per step.
+wavernn_status run_score(wavernn_model* m, const RunIO& io) {
+  const int Hh = m->plan.Hh, NP = m->sc_np;
+  const int64_t rows = (int64_t)io.S * io.T, CH = 65536;
+  const int64_t n_cb = m->cfg.cond_dim > 0 ? io.n_frames : 1;
+  const bool post = io.zc || io.zf || io.nll;
+  const int64_t ch = std::min(CH, rows);   // rows of one chunk of the output layers
+  if (rows > m->traj_cap || (post && ch > m->so_cap) || n_cb > m->cb_cap) HIPOK(hipStreamSynchronize(io.st));
+  wavernn_status st = grow_cb(m, &m->d_cb, &m->cb_cap, n_cb);
+  if (st != WAVERNN_OK) return st;
+  if (rows > m->traj_cap) {
+    if ((st = m->alloc(&m->d_traj, (size_t)2 * rows * Hh * 4)) != WAVERNN_OK) return st;
+    m->traj_cap = rows;
+  }
+  if (post && ch > m->so_cap) {   // (a replaced buffer stays allocated until the model is destroyed)
+    if ((st = m->alloc(&m->d_so, (size_t)ch * NP * 4)) != WAVERNN_OK) return st;
+    if ((st = m->alloc(&m->d_sz, (size_t)2 * ch * 256 * 4)) != WAVERNN_OK) return st;
+    m->so_cap = ch;
+  }
+  const int H = m->plan.H, Dc = m->cfg.cond_dim;
+  for (int s = 0; s < io.S; ++s) {
+    const float* feat = io.cond ? io.cond + (size_t)s * io.n_frames * Dc : nullptr;
+    if ((st = launch_cond(m, feat, n_cb, 1, m->d_cb, io.st)) != WAVERNN_OK) return st;
+    if ((st = launch_fill(m->d_xc, 2 * H, io.st)) != WAVERNN_OK) return st;
+    ScoreArgs a;
+    memset(&a, 0, sizeof a);
+    a.w = m->d_srw;
+    a.Iw = m->d_I;
+    a.cb = m->d_cb;
+    a.n_cb = n_cb;
+    a.frame_len = Dc > 0 ? (m->cfg.frame_len > 0 ? m->cfg.frame_len : 1) : (1 << 30);
+    a.H = H;
+    a.Hh = Hh;
+    a.T = io.T;
+    a.t0 = io.init ? io.init->t0 : 0;
+    a.target = io.target + (size_t)s * io.T;
+    if (io.init) {
+      a.h_in = io.init->h + (size_t)s * H;
+      a.c_in = io.init->c_prev + s;
+      a.f_in = io.init->f_prev + s;
+    }
+    if (io.fin) {
+      a.h_out = io.fin->h + (size_t)s * H;
+      a.c_out = io.fin->c_prev + s;
+      a.f_out = io.fin->f_prev + s;
+    }
+    a.traj_c = m->d_traj + (size_t)s * io.T * Hh;
+    a.traj_f = m->d_traj + (size_t)(io.S + s) * io.T * Hh;
+    a.xc = m->d_xc;
+    a.err = m->d_err;
+    a.limit = kWaitTicks;
+    void* args[] = {&a};
+    // an ordinary launch of H / 16 workgroups (co-residency checked at create; waits bounded)
+    HIPOK(hipLaunchKernel(m->sk, dim3(H / 16), dim3(WR_THREADS), args, score_lds(H), io.st));
+  }
+  if (!post) return WAVERNN_OK;
+  for (int64_t r0 = 0; r0 < rows; r0 += CH) {
+    const int n = (int)std::min(CH, rows - r0);
+    const CnnRows cr{1, 0, 0, n};
+    float* z[2];
+    for (int k = 0; k < 2; ++k) {
+      float* user = k ? io.zf : io.zc;
+      z[k] = user ? user + (size_t)r0 * 256 : m->d_sz + (size_t)k * ch * 256;
+      const float* src = m->d_traj + ((size_t)k * rows + r0) * Hh;
+      if ((st = cnn_gemm(src, Hh, 1, 0, n, cr, n, m->d_sw + m->sw_off[2 * k], m->d_sb + m->sb_off[2 * k], NP,
+                         m->d_so, 1, io.st)) != WAVERNN_OK)
+        return st;
+      if ((st = cnn_gemm(m->d_so, NP, 1, 0, n, cr, n, m->d_sw + m->sw_off[2 * k + 1], m->d_sb + m->sb_off[2 * k + 1],
+                         256, z[k], 0, io.st)) != WAVERNN_OK)
+        return st;
+    }
+    if (io.nll) {
+      const float* zc = z[0];
+      const float* zf = z[1];
+      const uint16_t* tg = io.target + r0;
+      int64_t nn = n;
+      float* nl = io.nll + r0;
+      void* args[] = {&zc, &zf, &tg, &nn, &nl};
+      HIPOK(hipLaunchKernel(wr_score_nll_ptr(), dim3((unsigned)((n + 3) / 4)), dim3(256), args, 0, io.st));
+    }
+  }
+  return WAVERNN_OK;
+}
+
 // A few utterances at once: utterance 0 runs the batch-1 kernel on the
 // caller's stream, utterance s > 0 on internal stream s - 1 (each its own
 // grid, exchange words and table), forked from and joined back into the
@@ -1201,6 +1354,8 @@ wavernn_status run(wavernn_model* m, RunIO& io, bool noalloc = false) {
   if (m->path == PATH_SMALL) return run_small(m, io);
   if (m->fused) return run_persist(m, io);   // one fused launch per utterance
   if (m->path == PATH_PERSIST) {
+    // one utterance (or a model that runs its utterances one after another) scores on the recurrence kernel
+    if (io.target && m->sk && (io.S == 1 || (!m->nfan && !m->has_batch))) return run_score(m, io);
     if (io.S > 1 && io.S <= m->nfan) return run_fanout(m, io);
     return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);
   }
@@ -1392,6 +1547,7 @@ wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* 
     } else {
       m->path = PATH_PERSIST;
       s = build_persist(m, w);
+      if (s == WAVERNN_OK) s = build_score(m, w);
       if (s == WAVERNN_OK && cfg->max_streams > 1 && batch_plan(H, cfg->max_streams, &m->bplan))
         s = build_batch(m, w);
       if (s == WAVERNN_OK && cfg->max_streams > 1) s = build_fanout(m);

@@ -1,0 +1,113 @@
+"""Teacher-forced scoring on the dense batch-1 plan: the recurrence kernel
+(heads that evaluate their own slices from the given bytes) and the output
+layers as GEMMs over all steps afterwards, through the C ABI.
+
+Bars: scoring the sampler's own output reproduces the sampler's state bit
+for bit (the gate arithmetic is the sampling head's), shown by scoring
+a sampled utterance whole and from the sampler's state at a midpoint; logits
+and NLL against the oracle within 1e-3 at small sizes and 2e-2 (bf16
+weights) at H = 896; against the sampling kernel run with forced classes (the
+path that scores several utterances side by side) within the same bounds.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from oracle import oracle as O  # noqa: E402
+from paper_1802_08435_amd import synth, wavernn  # noqa: E402
+
+
+def cuda(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.cpu().numpy()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def state_np(st):
+    return {k: host(v) for k, v in st.items() if k != "t0"}
+
+
+@pytest.mark.parametrize("H,N,K", [(256, 600, 264), (896, 2400, 1000)])
+def test_scoring_reproduces_the_samplers_state(H, N, K):
+    """Sample K samples, hand the state over, sample the rest.  Scoring the
+    whole output in one call and scoring its tail from the sampler's state at
+    K give the same tail logits and NLL bit for bit: after K steps of the same
+    bytes the scoring recurrence holds the sampler's state exactly."""
+    w = synth.make_weights(H, seed=5, cond_dim=64)
+    feat = synth.features(1, N, cond_dim=64)
+    m = wavernn.Model(w)
+    assert m.path()[0] == "persistent"
+    mid = m.new_state()
+    out = torch.zeros(1, N, dtype=torch.uint16, device="cuda")
+    m.sample(K, cond=cuda(feat), seed=9, out=out[:, :K], final=mid)
+    mid["t0"] = K
+    m.sample(N - K, cond=cuda(feat), seed=9, init=mid, out=out[:, K:])
+    m.device_status()
+    whole = {k: host(v) for k, v in m.score(out, cond=cuda(feat)).items()}
+    tail = {k: host(v) for k, v in m.score(out[:, K:].contiguous(), cond=cuda(feat), init=mid).items()}
+    m.device_status()
+    for k in ("zc", "zf", "nll"):
+        np.testing.assert_array_equal(tail[k], whole[k][:, K:], err_msg=k)
+    assert np.isfinite(whole["nll"]).all()
+    m.close()
+
+
+@pytest.mark.parametrize("H,tol", [(128, 1e-3), (256, 1e-3), (896, 2e-2)])
+def test_scoring_logits_and_nll_against_the_oracle(H, tol):
+    N = 480 if H < 896 else 960
+    w = synth.make_weights(H, seed=6, cond_dim=16)
+    feat = synth.features(1, N, cond_dim=16)
+    tgt = synth.target_signal(1, N, seed=4, kind="sines")
+    m = wavernn.Model(w)
+    r = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, N, feat=feat, target=tgt, logits=True, nll=True)
+    dc = np.abs(r["zc"] - ref["zc"]).max()
+    df = np.abs(r["zf"] - ref["zf"]).max()
+    assert dc <= tol and df <= tol, (dc, df)
+    np.testing.assert_allclose(r["nll"], ref["nll"], rtol=1e-3, atol=20 * tol)
+    m.close()
+
+
+def test_scoring_matches_the_sampling_kernel_with_forced_classes():
+    """With max_streams = 2, two utterances score side by side on the sampling
+    kernel (forced classes); one utterance scores on the recurrence kernel."""
+    H, N = 896, 1200
+    w = synth.make_weights(H, seed=7, cond_dim=64)
+    feat = synth.features(2, N, per_stream_seed=True)
+    tgt = np.concatenate([synth.target_signal(1, N, seed=4 + s, kind=k) for s, k in ((0, "sines"), (1, "uniform"))])
+    m = wavernn.Model(w, max_streams=2)
+    assert m.path(2)[0] == "concurrent"
+    both = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    for s in range(2):
+        one = {k: host(v) for k, v in m.score(cuda(tgt[s:s + 1]), cond=cuda(feat[s:s + 1])).items()}
+        m.device_status()
+        assert np.abs(one["zc"][0] - both["zc"][s]).max() <= 2e-2
+        assert np.abs(one["zf"][0] - both["zf"][s]).max() <= 2e-2
+        np.testing.assert_allclose(one["nll"][0], both["nll"][s], rtol=1e-3, atol=4e-2)
+    m.close()
+
+
+def test_scoring_degenerate_lengths():
+    w = synth.make_weights(256, seed=2, cond_dim=0)
+    m = wavernn.Model(w)
+    one = np.array([[37 * 256 + 200]], dtype=np.uint16)
+    r = {k: host(v) for k, v in m.score(cuda(one)).items()}
+    m.device_status()
+    ref = O.run(O.Weights.from_dict(w, bf16=True), 1, 1, target=one, logits=True)
+    assert np.abs(r["zc"] - ref["zc"]).max() <= 1e-3 and np.abs(r["zf"] - ref["zf"]).max() <= 1e-3
+    empty = m.score(cuda(np.zeros((1, 0), dtype=np.uint16)))
+    m.device_status()
+    assert all(v.numel() == 0 for v in empty.values())
+    m.close()
