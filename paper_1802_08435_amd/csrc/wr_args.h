@@ -148,9 +148,14 @@ struct CnnGemmArgs {
   const uint4* w;         // weight fragments [N / 16][K / 32] x 64 lanes
   const float* bias;      // [N]
   int N;                  // a multiple of 128
-  float* dst;             // [M][N]
+  float* dst;             // [M][N] rows, or with out_B > B block (u, s) of the run at block u out_B + out_s0 + s
+  int out_B, out_s0;      // (out_B = B, out_s0 = 0: row m at row m)
   int epi;                // 0: acc + bias; 1: relu(acc + bias); 2: dst + (acc + bias)
-  int tiles_m, tiles, per_xcd;   // 128-row tiles, all tiles, tiles per XCD slot
+  int group;              // K-steps per accumulation group (the sum is ((g0 + g1) + g2) + ..., each g_q from 0)
+  int split;              // 1: a workgroup runs every group of its tile; > 1 (= the number of groups):
+                          // workgroup (tile, q) writes g_q to part[q] and wr_cnn_reduce adds them in order
+  float* part;            // [groups][M][N] (split > 1)
+  int tiles_m, tiles, per_xcd;   // 128-row tiles, all tiles, tiles x split per XCD slot
 };
 #define CNN_TM 128
 #define CNN_TN 128
@@ -166,6 +171,8 @@ struct CnnInputArgs {
   int win;                // rows per (utterance, sub-tensor) block
   int64_t row0, row_step; // block (u, s) covers utterance rows row0 + s row_step ...
   int64_t front0, front_step;   // sub-tensor z has made rows up to front0 + z front_step
+  int s0, nsb;            // the run covers sub-tensors s0 .. s0 + nsb - 1 of each utterance: block m / win =
+                          // (u, s - s0)
   int M, kin;
   float* x;               // [M][kin]
 };
@@ -186,3 +193,4 @@ const void* wr_fused_kernel_ptr(int KH);     // null if no instantiation
 const void* wr_floor_kernel_ptr();
 const void* wr_cnn_gemm_ptr();
 const void* wr_cnn_input_ptr();
+const void* wr_cnn_reduce_ptr();

@@ -62,32 +62,65 @@ __device__ __forceinline__ void cnn_stage(unsigned char* buf, const float4* x, u
 
 }  // namespace
 
-// Workgroup b takes tile L = (b % 8) per_xcd + b / 8: consecutive tiles (the
-// column tiles of one row tile, which read the same activations) share an
-// XCD and its L2.  Wave w computes rows 64 (w / 4) .. +63 and columns
-// 32 (w % 4) .. +31 of the tile: 4 x 2 MFMA tiles, each as a high and a low
-// product.
+// Workgroup b takes work item L = (b % 8) per_xcd + b / 8 (tile L mod tiles,
+// group L / tiles when split): consecutive tiles (the column tiles of one row
+// tile, which read the same activations) share an XCD and its L2.  Wave w
+// computes rows 64 (w / 4) .. +63 and columns 32 (w % 4) .. +31 of the tile:
+// 4 x 2 MFMA tiles, each as a high and a low product.  The K loop sums in
+// groups of `group` K-steps, each group from zero, added in order: the same
+// arithmetic whether one workgroup runs every group (a small GEMM has fewer
+// tiles than CUs, and one tile's K loop would set its time) or each group
+// runs on its own workgroup and wr_cnn_reduce adds them, so results never
+// depend on how many rows a run has.
+__device__ __forceinline__ void cnn_store(const CnnGemmArgs& a, int m0, int n0, const f32x4 (&v)[4][2], float* part) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wm = wave >> 2, wn = wave & 3;
+  // lane l of tile (i, j) holds rows 4 (l / 16) .. +3, column l % 16
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = n0 + 32 * wn + 16 * j + (lane & 15);
+    const float bn = part ? 0.0f : a.bias[n];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + 64 * wm + 16 * i + 4 * (lane >> 4) + r;
+        if (m >= a.M) continue;
+        if (part) {
+          part[(size_t)m * a.N + n] = v[i][j][r];
+          continue;
+        }
+        const int blk = m / a.rows;
+        const size_t dm = (size_t)((blk / a.B) * a.out_B + a.out_s0 + blk % a.B) * a.rows + m % a.rows;
+        float* d = a.dst + dm * a.N + n;
+        const float x = v[i][j][r] + bn;
+        *d = a.epi == 0 ? x : a.epi == 1 ? wr_relu(x) : *d + x;
+      }
+  }
+}
+
 __global__ __launch_bounds__(CNN_THREADS, 1) void wr_cnn_gemm(CnnGemmArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int b = blockIdx.x;
   const int L = (b % 8) * a.per_xcd + b / 8;
-  if (b / 8 >= a.per_xcd || L >= a.tiles) return;
-  const int m0 = (L % a.tiles_m) * CNN_TM, n0 = (L / a.tiles_m) * CNN_TN;
+  if (b / 8 >= a.per_xcd || L >= a.tiles * a.split) return;
+  const int tile = L % a.tiles, q = L / a.tiles;
+  const int m0 = (tile % a.tiles_m) * CNN_TM, n0 = (tile / a.tiles_m) * CNN_TN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, wm = wave >> 2, wn = wave & 3;
-  f32x4 acc[4][2];
+  f32x4 acc[4][2], grp[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0, 0, 0, 0};
+    for (int j = 0; j < 2; ++j) acc[i][j] = grp[i][j] = f32x4{0, 0, 0, 0};
   const int KT = a.K / 32;
+  const int k_lo = a.split > 1 ? q * a.group : 0, k_hi = a.split > 1 ? min(KT, k_lo + a.group) : KT;
   float4 x[2];
   uint4 wv;
-  cnn_load(a, m0, n0, 0, x, &wv);
-  for (int kt = 0; kt < KT; ++kt) {
+  cnn_load(a, m0, n0, k_lo, x, &wv);
+  for (int kt = k_lo; kt < k_hi; ++kt) {
     unsigned char* buf = lds + (kt & 1) * CNN_LDS_BUF;
     cnn_stage(buf, x, wv);
     __syncthreads();
-    if (kt + 1 < KT) cnn_load(a, m0, n0, kt + 1, x, &wv);   // in flight during the products
+    if (kt + 1 < k_hi) cnn_load(a, m0, n0, kt + 1, x, &wv);   // in flight during the products
     bf16x8 bw[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) bw[j] = *(const bf16x8*)(buf + (16 + 2 * wn + j) * WR_FRAG + lane * 16);
@@ -97,31 +130,42 @@ __global__ __launch_bounds__(CNN_THREADS, 1) void wr_cnn_gemm(CnnGemmArgs a) {
       const bf16x8 al = *(const bf16x8*)(buf + (8 + 4 * wm + i) * WR_FRAG + lane * 16);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        acc[i][j] = mfma(ah, bw[j], acc[i][j]);
-        acc[i][j] = mfma(al, bw[j], acc[i][j]);
+        grp[i][j] = mfma(ah, bw[j], grp[i][j]);
+        grp[i][j] = mfma(al, bw[j], grp[i][j]);
       }
     }
+    if ((kt + 1) % a.group == 0 || kt + 1 == KT) {   // a group ends: acc = acc + g (the first: acc = g)
+      const bool first = kt + 1 <= a.group;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = first ? grp[i][j] : acc[i][j] + grp[i][j];
+          grp[i][j] = f32x4{0, 0, 0, 0};
+        }
+    }
   }
-  // lane l of tile (i, j) holds rows 4 (l / 16) .. +3, column l % 16
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = n0 + 32 * wn + 16 * j + (lane & 15);
-    const float bn = a.bias[n];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 64 * wm + 16 * i + 4 * (lane >> 4) + r;
-        if (m >= a.M) continue;
-        float* d = a.dst + (size_t)m * a.N + n;
-        const float v = acc[i][j][r] + bn;
-        *d = a.epi == 0 ? v : a.epi == 1 ? wr_relu(v) : *d + v;
-      }
-  }
+  cnn_store(a, m0, n0, acc, a.split > 1 ? a.part + (size_t)q * a.M * a.N : nullptr);
 }
 
-// Input rows of a window of `win` rows per (utterance u, sub-tensor s): row m =
-// (u B + s) win + k is utterance row q = row0 + s row_step + k.  x[m][2z],
+// Split GEMMs: out = ((part[0] + part[1]) + part[2]) + ... + bias, then the
+// epilogue, as wr_cnn_gemm's own when one workgroup runs every group.
+__global__ void wr_cnn_reduce(CnnGemmArgs a) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)a.M * a.N) return;
+  const int m = (int)(idx / a.N), n = (int)(idx % a.N);
+  float v = a.part[idx];
+  for (int q = 1; q < a.split; ++q) v = v + a.part[(size_t)q * a.M * a.N + idx];
+  const int blk = m / a.rows;
+  const size_t dm = (size_t)((blk / a.B) * a.out_B + a.out_s0 + blk % a.B) * a.rows + m % a.rows;
+  float* d = a.dst + dm * a.N + n;
+  const float x = v + a.bias[n];
+  *d = a.epi == 0 ? x : a.epi == 1 ? wr_relu(x) : *d + x;
+}
+
+// Input rows of a window of `win` rows per (utterance u, sub-tensor s) for the
+// sub-tensors s0 .. s0 + nsb - 1: row m = (u nsb + s - s0) win + k is
+// utterance row q = row0 + s row_step + k.  x[m][2z],
 // x[m][2z + 1] = the scaled (c, f) of sample B q + z for z < s (the previous
 // sub-tensors of row q) when q is a row of the utterance and sub-tensor z has
 // made it (q <= front0 + z front_step); zero otherwise and in the padding up
@@ -130,7 +174,7 @@ __global__ void wr_cnn_input(CnnInputArgs a) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (int64_t)a.M * a.kin) return;
   const int m = (int)(idx / a.kin), ch = (int)(idx % a.kin);
-  const int k = m % a.win, s = (m / a.win) % a.B, u = m / a.win / a.B, z = ch >> 1;
+  const int k = m % a.win, s = a.s0 + (m / a.win) % a.nsb, u = m / a.win / a.nsb, z = ch >> 1;
   const int64_t q = a.row0 + (int64_t)s * a.row_step + k;
   float v = 0.0f;
   if (z < s && q >= 0 && q < a.rows && q <= a.front0 + (int64_t)z * a.front_step) {
@@ -142,3 +186,4 @@ __global__ void wr_cnn_input(CnnInputArgs a) {
 
 const void* wr_cnn_gemm_ptr() { return (const void*)wr_cnn_gemm; }
 const void* wr_cnn_input_ptr() { return (const void*)wr_cnn_input; }
+const void* wr_cnn_reduce_ptr() { return (const void*)wr_cnn_reduce; }

@@ -112,6 +112,8 @@ struct wavernn_model {
     std::vector<size_t> woff, boff;   // [input, conv 0, proj 0, conv 1, ..., output] in uint4 / floats
     float *x = nullptr, *r = nullptr, *act = nullptr;
     int64_t cap = 0;                   // activation rows the buffers hold
+    float* part = nullptr;             // per-group partial products of split GEMMs
+    int64_t part_cap = 0;              // floats
   } cnn;
   bool has_cnn = false;
   int64_t cnn_chunk = 0, cnn_win = 0;   // sampling: steps per chunk, CNN window rows
@@ -694,6 +696,10 @@ wavernn_status grow_ctab(wavernn_model* m, size_t floats, hipStream_t* st) {
   float* p = nullptr;
   wavernn_status s = m->alloc(&p, floats * 4);
   if (s != WAVERNN_OK) return s;
+  // zeroed: a sampling chunk writes only the blocks of the sub-tensors it
+  // runs, and idle lanes read (and discard) the others
+  if (st) HIPOK(hipMemsetAsync(p, 0, floats * 4, *st));
+  else HIPOK(hipMemset(p, 0, floats * 4));
   m->d_ctab = p;
   m->ctab_cap = (int64_t)floats;
   return WAVERNN_OK;
@@ -798,8 +804,18 @@ struct CnnRows {   // which utterance rows the blocks of a CNN run cover
   int64_t row0, row_step, rows_utt;
 };
 
+// A CNN GEMM's K loop sums in groups of CNN_GROUP K-steps (always, so that results
+// never depend on the rows of a run); a GEMM with fewer tiles than CUs runs
+// each group on its own workgroup and adds them in wr_cnn_reduce.
+#define CNN_GROUP 6
+int cnn_split(int M, int N, int K) {
+  const int tiles = (M + CNN_TM - 1) / CNN_TM * (N / CNN_TN), groups = (K / 32 + CNN_GROUP - 1) / CNN_GROUP;
+  return tiles < 256 && groups > 1 ? groups : 1;
+}
+
 wavernn_status cnn_gemm(const float* src, int kin, int taps, int dil, int rows, const CnnRows& cr, int M,
-                        const uint4* w, const float* bias, int N, float* dst, int epi, hipStream_t st) {
+                        const uint4* w, const float* bias, int N, float* dst, int epi, hipStream_t st,
+                        float* part = nullptr, int out_B = 0, int out_s0 = 0) {
   CnnGemmArgs g;
   g.src = src;
   g.kin = kin;
@@ -816,23 +832,34 @@ wavernn_status cnn_gemm(const float* src, int kin, int taps, int dil, int rows, 
   g.bias = bias;
   g.N = N;
   g.dst = dst;
+  g.out_B = out_B ? out_B : cr.B;
+  g.out_s0 = out_s0;
   g.epi = epi;
+  g.group = CNN_GROUP;
+  g.split = part ? cnn_split(M, N, g.K) : 1;
+  g.part = part;
   g.tiles_m = (M + CNN_TM - 1) / CNN_TM;
   g.tiles = g.tiles_m * (N / CNN_TN);
-  g.per_xcd = (g.tiles + 7) / 8;
+  g.per_xcd = (g.tiles * g.split + 7) / 8;
   void* args[] = {&g};
   HIPOK(hipLaunchKernel(wr_cnn_gemm_ptr(), dim3(8 * g.per_xcd), dim3(CNN_THREADS), args, 2 * CNN_LDS_BUF, st));
+  if (g.split > 1)
+    HIPOK(hipLaunchKernel(wr_cnn_reduce_ptr(), dim3((unsigned)(((int64_t)M * N + 255) / 256)), dim3(256), args, 0, st));
   return WAVERNN_OK;
 }
 
-// The conditioning CNN over windows of `win` rows per (utterance, sub-tensor):
-// block (u, s) covers utterance rows row0 + s row_step .. + win - 1, samples
-// of sub-tensor z counted up to row front0 + z front_step; out [U][B][win][Dx].
+// The conditioning CNN over windows of `win` rows per (utterance, sub-tensor),
+// for the sub-tensors s0 .. s0 + nsb - 1: block (u, s) covers utterance rows
+// row0 + s row_step .. + win - 1, samples of sub-tensor z counted up to row
+// front0 + z front_step; out [U][B][win][Dx] (the other sub-tensors' blocks
+// are left as they are).
 wavernn_status run_cnn(wavernn_model* m, int U, const uint16_t* seq, int64_t n_samples, int win, int64_t row0,
-                       int64_t row_step, int64_t front0, int64_t front_step, float* out, hipStream_t st) {
+                       int64_t row_step, int64_t front0, int64_t front_step, float* out, hipStream_t st, int s0 = 0,
+                       int nsb = 0) {
   auto& C = m->cnn;
   const int B = m->cfg.subscale, Dx = m->cfg.ctx_dim;
-  const int64_t M64 = (int64_t)U * B * win;
+  if (nsb <= 0) nsb = B;
+  const int64_t M64 = (int64_t)U * nsb * win;
   if (M64 > (1 << 28)) return fail(WAVERNN_E_INVALID, "conditioning CNN: %lld rows, above 2^28", (long long)M64);
   const int M = (int)M64;
   if (M > C.cap) {   // grow the activations (an allocation: only when a call needs more rows than any before)
@@ -842,6 +869,20 @@ wavernn_status run_cnn(wavernn_model* m, int U, const uint16_t* seq, int64_t n_s
     if ((s = m->alloc(&C.r, (size_t)M * C.Rc * 4)) != WAVERNN_OK) return s;
     if ((s = m->alloc(&C.act, (size_t)M * C.Cc * 4)) != WAVERNN_OK) return s;
     C.cap = M;
+  }
+  {   // the split GEMMs' partial products (the largest of the run's layers)
+    int64_t need = 0;
+    const int KN[4][2] = {{C.kin, C.Rc}, {3 * C.Rc, C.Cc}, {C.Cc, C.Rc}, {C.Rc, Dx}};
+    for (auto& kn : KN) {
+      const int sp = cnn_split(M, kn[1], kn[0]);
+      if (sp > 1) need = std::max(need, (int64_t)sp * M * kn[1]);
+    }
+    if (need > C.part_cap) {
+      HIPOK(hipStreamSynchronize(st));
+      wavernn_status s;
+      if ((s = m->alloc(&C.part, (size_t)need * 4)) != WAVERNN_OK) return s;
+      C.part_cap = need;
+    }
   }
   CnnInputArgs in;
   in.seq = seq;
@@ -853,6 +894,8 @@ wavernn_status run_cnn(wavernn_model* m, int U, const uint16_t* seq, int64_t n_s
   in.row_step = row_step;
   in.front0 = front0;
   in.front_step = front_step;
+  in.s0 = s0;
+  in.nsb = nsb;
   in.M = M;
   in.kin = C.kin;
   in.x = C.x;
@@ -861,20 +904,20 @@ wavernn_status run_cnn(wavernn_model* m, int U, const uint16_t* seq, int64_t n_s
   HIPOK(hipLaunchKernel(wr_cnn_input_ptr(), dim3((unsigned)((nx + 255) / 256)), dim3(256), args, 0, st));
   wavernn_status s;
   size_t i = 0;
-  const CnnRows cr{B, row0, row_step, n_samples / B};
-  if ((s = cnn_gemm(C.x, C.kin, 1, 0, win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], C.Rc, C.r, 0, st)) !=
+  const CnnRows cr{nsb, row0 + s0 * row_step, row_step, n_samples / B};
+  if ((s = cnn_gemm(C.x, C.kin, 1, 0, win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], C.Rc, C.r, 0, st, C.part)) !=
       WAVERNN_OK)
     return s;
   ++i;
   for (int l = 0; l < C.layers; ++l, i += 2) {
     if ((s = cnn_gemm(C.r, C.Rc, 3, 1 << (l % 5), win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], C.Cc, C.act, 1,
-                      st)) != WAVERNN_OK)
+                      st, C.part)) != WAVERNN_OK)
       return s;
     if ((s = cnn_gemm(C.act, C.Cc, 1, 0, win, cr, M, C.w + C.woff[i + 1], C.bias + C.boff[i + 1], C.Rc, C.r, 2,
-                      st)) != WAVERNN_OK)
+                      st, C.part)) != WAVERNN_OK)
       return s;
   }
-  return cnn_gemm(C.r, C.Rc, 1, 0, win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], Dx, out, 0, st);
+  return cnn_gemm(C.r, C.Rc, 1, 0, win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], Dx, out, 0, st, C.part, B, s0);
 }
 
 // Bias + conditioning table cb[s][f][3H] for n_streams streams of n_frames frames.
@@ -1328,8 +1371,16 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   int cur = 0;
   for (int64_t t0 = 0; t0 < steps; t0 += LC) {
     const int64_t n = std::min(LC, steps - t0);
-    if ((st = run_cnn(m, io.S, io.out, io.T, (int)W, t0, -(int64_t)(F + 1), t0 - 1, -(int64_t)(F + 1), m->d_ctab,
-                      io.st)) != WAVERNN_OK)
+    // only the sub-tensors that make a position in this chunk (a contiguous
+    // range: the lag grows with s); an idle lane's table rows are never used
+    int s_lo = SB, s_hi = -1;
+    for (int s = 0; s < SB; ++s) {
+      const int64_t p0 = t0 - (int64_t)s * (F + 1);
+      if (p0 + n > 0 && p0 < a.rows) s_lo = std::min(s_lo, s), s_hi = s;
+    }
+    if (s_hi >= s_lo &&
+        (st = run_cnn(m, io.S, io.out, io.T, (int)W, t0, -(int64_t)(F + 1), t0 - 1, -(int64_t)(F + 1), m->d_ctab,
+                      io.st, s_lo, s_hi - s_lo + 1)) != WAVERNN_OK)
       return st;
     a.ctab_row0 = t0;
     const bool last = t0 + n >= steps;
