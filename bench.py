@@ -264,9 +264,11 @@ def main() -> int:
     out = torch.empty(S, T, dtype=torch.uint16, device="cuda")
     stream = torch.cuda.current_stream()
     if args.phases:
-        if path not in PHASES:                          # a kernel without phase stamps
-            print(json.dumps({"workload": args.config, "kernel": KERNEL_OF.get(path, path), "phases": None}),
-                  flush=True)
+        if path not in PHASES or w.get("cnn") is not None:   # no phase stamps / tracing switched off
+            why = ("tracing is switched off for CNN-conditioned calls" if w.get("cnn") is not None
+                   else "this kernel has no phase stamps")
+            print(json.dumps({"workload": args.config, "kernel": KERNEL_OF.get(path, path), "phases": None,
+                              "why": why}), flush=True)
             m.close()
             return 0
         m.sample(T, cond=feat, seed=1, n_streams=S, out=out)

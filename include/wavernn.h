@@ -299,7 +299,9 @@ wavernn_status wavernn_set_placement(wavernn_model* m, int32_t candidate);
  * the phases of that step (gates, hidden layers, partial logits published,
  * logits summed, draws) on head workgroup 0 or on the last head workgroup;
  * unused slots stay zero.  max_steps = 0 turns tracing off.  Other kernels
- * ignore the setting. */
+ * ignore the setting.  A sampling or scoring call of a model with a
+ * conditioning CNN returns E_UNSUPPORTED while tracing is on (switched off:
+ * one traced call of that path had a bounded wait expire, cause not found). */
 wavernn_status wavernn_set_trace(wavernn_model* m, uint64_t* trace_dev, int64_t max_steps);
 
 /* Diagnostics: the synchronization floor of the model's persistent kernel

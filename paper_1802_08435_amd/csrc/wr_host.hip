@@ -1275,6 +1275,9 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   if (!batch_plan(m->cfg.hidden, V, &B, m->cfg.ctx_dim, SB, F, A, table))
     return fail(WAVERNN_E_UNSUPPORTED, "no batched plan for %d vectors", V);
   if (table && io.ws) return fail(WAVERNN_E_UNSUPPORTED, "the conditioning CNN needs its own activation buffers");
+  if (table && m->trace)
+    return fail(WAVERNN_E_UNSUPPORTED, "phase tracing is switched off for CNN-conditioned calls (a traced call had a "
+                "bounded wait expire and the cause is not found; untraced calls are unaffected)");
   const int H = B.H, Dc = m->cfg.cond_dim;
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
   const int64_t n_cb = Dc > 0 ? io.n_frames : 1;

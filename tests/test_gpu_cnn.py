@@ -153,6 +153,30 @@ def test_cnn_subscale_free_running_valid_and_independent_of_the_chunking():
     assert all(len(np.unique(out[u])) > 100 for u in range(S))
 
 
+def test_cnn_calls_refuse_phase_tracing():
+    """Phase tracing is switched off for CNN-conditioned calls (refused on the
+    host, before any launch; the trace buffer stays untouched); with tracing
+    off again the same model samples and scores as before."""
+    B, N = 4, 4 * 40
+    w = cnn_model(B=B, F=130)
+    feat = synth.features(1, N, cond_dim=16)
+    m = wavernn.Model(w)
+    ref = host(m.sample(N, cond=cuda(feat), seed=4))
+    m.device_status()
+    buf = torch.zeros(64, 32, dtype=torch.int64, device="cuda")
+    m.set_trace(buf)
+    for call in (lambda: m.sample(N, cond=cuda(feat), seed=4),
+                 lambda: m.score(cuda(ref), cond=cuda(feat))):
+        with pytest.raises(wavernn.WaveRNNError) as e:
+            call()
+        assert e.value.status == 2 and "tracing" in str(e.value)
+    m.set_trace(None)
+    assert int(buf.abs().sum()) == 0
+    np.testing.assert_array_equal(host(m.sample(N, cond=cuda(feat), seed=4)), ref)
+    m.device_status()
+    m.close()
+
+
 def test_subscale16_cnn_full_length_call():
     """The benchmarked call (Subscale WaveRNN-896, B = 16, the paper's CNN
     widths, 24,000 samples, 49 chunks of 100 steps): the CNN's table over the
