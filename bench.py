@@ -156,7 +156,7 @@ PHASES = {
                    (10, "next step's coarse gate words received (end of step)")],
     "batched": [(11, "coarse gate words received"), (1, "coarse gates done, y_c of the group exchanged"),
                 (3, "O1/O2: partial coarse logits published"), (4, "owned vectors' coarse partials summed"),
-                (5, "c_t drawn"), (12, "fine gate words and classes received"),
+                (5, "c_t drawn"), (12, "fine gate words (groups of 2 and 4: read with the coarse ones) and classes received"),
                 (6, "fine gates done, y_f of the group exchanged"), (8, "O3/O4: partial fine logits published"),
                 (9, "owned vectors' fine partials summed"), (10, "f_t drawn (end of step)")],
 }

@@ -187,6 +187,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   float* fmisc = (float*)(misc + 32);              // [b] lse_c, [8+b] z_c[c] of vector b
   float2* uni = (float2*)(misc + 64);              // [2][L][64] (u_c, u_f) of a batch of 64 steps
   int* tgt = (int*)(uni + 2 * L * 64);             // [2][L][64] teacher-forcing targets
+  float* gvf = (float*)(tgt + 2 * L * 64);         // ALL: [4L][448] the fine half's words (as gv), read with the coarse
 
   const int v0 = g * L;                            // first vector of this group
   for (int i = tid; i < (2 * KT + 2) * WR_FRAG / 16; i += WR_THREADS) ((uint4*)lds)[i] = uint4{0, 0, 0, 0};
@@ -247,8 +248,6 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     misc[48 + tid] = LAG ? (int)(((v0 + tid) % a.B) * (a.F + 1 + a.A) - a.t0) : 0;   // position: t - misc[48 + tid]
   }
   xw* X = a.xc + (size_t)g * P.x_words;
-  const xw* GA = X + P.x_ga;
-  const xw* GF = X + P.x_gf;
   xw* YC = X + P.x_yc;
   xw* YF = X + P.x_yf;
   xw* PCo = X + P.x_pc + (size_t)j * L * 256;
@@ -335,40 +334,45 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
       zs[(sp + 2 * m) * 256 + v] = s;
     }
   };
-  // The 3L pre-activation words of gate thread u (two batches of loads) and
-  // the L additive terms of the e gate (bias + conditioning, and with subscale
-  // the context term, which stays outside the reset product), staged in LDS:
-  // word k at gv[k * 448 + u], term of vector b at gv[(3L + b) * 448 + u].
+  // The 3L pre-activation words of gate thread u of each half and the L
+  // additive terms of each half's e gate (bias + conditioning, and with
+  // subscale the context term, which stays outside the reset product), staged
+  // in LDS: coarse word k at gv[k * 448 + u] and the term of vector b at
+  // gv[(3L + b) * 448 + u], fine ones likewise in gvf.  The units publish
+  // both halves at once, so all 4L word pairs are polled together at the
+  // start of the step: the fine gates wait for nothing but c_t.
   const bool trg = g == 0 && j == 0 && tid == 0;            // a gate thread (tracing)
-  auto read_gates = [&](const xw* G, const xw* XE, uint32_t tag, int col, int64_t t) {
+  auto read_gates = [&](uint32_t tag, int64_t t) {
 #pragma unroll
-    for (int b = 0; b < L; ++b) gv[(3 * L + b) * 448 + u] = a.cb[cbo[b] + col];
-    if (trg && col == 2 * H) trace_at(a, t, 13);
-    // words of unit u: vector b of gate q at G[(q Hh + u) L + b], context term at XE[u L + b];
-    // read as pairs of vectors
-    if (CTX && !poll_put2<L / 2>(XE + (size_t)u * L, [&](int k) { return 2 * k; },
-                                  [&](int k, float x0, float x1) {
-                                    gv[(3 * L + 2 * k) * 448 + u] += x0;
-                                    gv[(3 * L + 2 * k + 1) * 448 + u] += x1;
-                                  }, tag, a)) {
+    for (int b = 0; b < L; ++b) {
+      gv[(3 * L + b) * 448 + u] = a.cb[cbo[b] + 2 * H + u];
+      gvf[(3 * L + b) * 448 + u] = a.cb[cbo[b] + 2 * H + Hh + u];
+    }
+    if (trg) trace_at(a, t, 13);
+    // pair k: half k / HP; in a half, the context pairs (vectors 2r, 2r + 1) and
+    // then the gate pairs (gate q, vectors b, b + 1) of unit u
+    constexpr int XP = CTX ? L / 2 : 0, HP = XP + 3 * L / 2;
+    if (!poll_put2<2 * HP>((const xw*)X,
+                           [&](int k) -> size_t {
+                             const int h = k / HP, r = k % HP;
+                             if (r < XP) return (size_t)(h ? P.x_xf : P.x_xc) + (size_t)u * L + 2 * r;
+                             const int q = (r - XP) / (L / 2), b = 2 * ((r - XP) % (L / 2));
+                             return (size_t)(h ? P.x_gf : P.x_ga) + (size_t)q * Hh * L + (size_t)u * L + b;
+                           },
+                           [&](int k, float x0, float x1) {
+                             const int h = k / HP, r = k % HP;
+                             float* gw = h ? gvf : gv;
+                             if (r < XP) {
+                               gw[(3 * L + 2 * r) * 448 + u] += x0;
+                               gw[(3 * L + 2 * r + 1) * 448 + u] += x1;
+                             } else {
+                               const int q = (r - XP) / (L / 2), b = 2 * ((r - XP) % (L / 2));
+                               gw[(3 * b + q) * 448 + u] = x0;
+                               gw[(3 * b + 3 + q) * 448 + u] = x1;
+                             }
+                           },
+                           tag, a))
       misc[0] = 1;
-      return;
-    }
-    constexpr int NB = L > 4 ? 2 : 1, PB = 3 * L / 2 / NB;   // batches of PB pairs in flight together
-#pragma unroll 1
-    for (int hb = 0; hb < NB; ++hb) {
-      const int k0 = hb * PB;
-      if (!poll_put2<PB>(G + (size_t)u * L,
-                                [&](int k) { return (size_t)((k0 + k) / (L / 2)) * Hh * L + 2 * ((k0 + k) % (L / 2)); },
-                                [&](int k, float x0, float x1) {
-                                  const int q = (k0 + k) / (L / 2), b = 2 * ((k0 + k) % (L / 2));
-                                  gv[(3 * b + q) * 448 + u] = x0;
-                                  gv[(3 * b + 3 + q) * 448 + u] = x1;
-                                }, tag, a)) {
-        misc[0] = 1;
-        return;
-      }
-    }
   };
   xw* CC = X + P.x_cc;                              // drawn coarse classes [L]
   xw* CF = X + P.x_cf;                              // drawn fine classes [L]
@@ -512,7 +516,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (SLICE) {
       slice_gates(false, tag, t, actm);
     } else if (gate) {
-      read_gates(GA, X + P.x_xc, tag, 2 * H + u, t);
+      read_gates(tag, t);
       if (trg) trace_at(a, t, 11);
 #pragma unroll 2
       for (int b = 0; b < L; ++b) {
@@ -573,22 +577,21 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     if (SLICE) {
       slice_gates(true, tag, t, actm);
     } else if (gate) {
-      read_gates(GF, X + P.x_xf, tag, 2 * H + Hh + u, t);
-      if (trg) trace_at(a, t, 12);
+      if (trg) trace_at(a, t, 12);                 // (the fine words came with the coarse ones)
 #pragma unroll 2
       for (int b = 0; b < L; ++b) {
         if (FL) {
           if (mine) xpub(YF + b * Hh + u, tag, 0.0f);
           continue;
         }
-        const float cbe = gv[(3 * L + b) * 448 + u];
+        const float cbe = gvf[(3 * L + b) * 448 + u];
         const float x0 = fscale(misc[16 + b]), x1 = fscale(misc[24 + b]), x2 = fscale(misc[8 + b]);
-        const float uu = fsig(gv[(3 * b) * 448 + u] +
+        const float uu = fsig(gvf[(3 * b) * 448 + u] +
                               __builtin_fmaf(ifn[0][2], x2, __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0)));
-        const float rg = fsig(gv[(3 * b + 1) * 448 + u] +
+        const float rg = fsig(gvf[(3 * b + 1) * 448 + u] +
                               __builtin_fmaf(ifn[1][2], x2, __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0)));
         const float e = ftanh(__builtin_fmaf(
-            rg, gv[(3 * b + 2) * 448 + u],
+            rg, gvf[(3 * b + 2) * 448 + u],
             __builtin_fmaf(ifn[2][2], x2, __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0)) + cbe));
         const float hn = actm >> b & 1u ? __builtin_fmaf(uu, hfs[b * 448 + u], (1.0f - uu) * e)
                                         : hfs[b * 448 + u];

@@ -365,9 +365,10 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   // head: operand images (2 KT + 2 fragments), first-layer partials [2][L][64],
   // logit sums [L][256], logits [L][256], both halves of h and the staged
   // gate inputs [2 + 4][L][448], bias row offsets [L], misc [64],
-  // uniforms [2][L][64][2], targets [2][L][64]
+  // uniforms [2][L][64][2], targets [2][L][64], and with up to 4 vectors the
+  // fine half's staged gate inputs [4][L][448]
   P->lds_h = (2 * P->KT + 2) * WR_FRAG + 4 * (2 * P->L * 64 + 2 * P->L * 256 + 6 * P->L * 448 + 2 * P->L + 64 +
-                                               2 * P->L * 64 * 2 + 2 * P->L * 64);
+                                               2 * P->L * 64 * 2 + 2 * P->L * 64 + (P->L <= 4 ? 4 * P->L * 448 : 0));
   // Ring of drawn samples per utterance: lockstep, the Dx/2 samples before
   // a row plus the row; with horizon F the lanes of an utterance are up to
   // (B - 1)(F + 1 + A) positions apart, so the newest sample and the oldest

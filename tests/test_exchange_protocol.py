@@ -13,8 +13,8 @@ strongly skewed speeds.  The words carry the kernel's tags:
   forever (a lost word, seen as a deadlock).
 
 Both group modes are modelled: ALL (2 or 4 vectors per group: every head
-reads every gate word and draws every vector; one writer head per vector's
-sample word) and SLICE (8 vectors: head j evaluates its own slice of units and
+reads every gate word of both halves in one poll at the start of the step and
+draws every vector; one writer head per vector's sample word) and SLICE (8 vectors: head j evaluates its own slice of units and
 the heads exchange y slices, vector v is owned by head v mod NH, which alone
 gathers its partials, draws it and publishes its class words; the coarse gate
 poll also waits for the first word of every unit and for the owners' classes
@@ -91,10 +91,11 @@ def run(mode="ALL", G=8, NH=3, NU=3, L=2, B=16, F=4, A=1, rows=12, SS=None, seed
             if mode == "SLICE":
                 for v in own:
                     yield pub(("CC", g, v), tag)
-            # fine: gate words (published with the coarse ones), SLICE: this step's classes
-            for k in range(NU):
-                yield wait1(("GATE", g, k), tag)
+            # fine: SLICE polls its gate words (published with the coarse ones) with this
+            # step's classes; ALL read them with the coarse words above
             if mode == "SLICE":
+                for k in range(NU):
+                    yield wait1(("GATE", g, k), tag)
                 for v in range(L):
                     yield wait1(("CC", g, v), tag)
             yield pub(("YF", g, j), tag)
