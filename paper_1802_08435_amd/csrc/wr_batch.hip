@@ -511,8 +511,9 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     }
     const int bs = (int)((t >> 6) & 1) * L * 64 + wave * 64 + (int)(t & 63);   // draw wave's batch slot
     if (own && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
-    // (1) coarse gates of every unit and vector: the 24 pre-activation words of
-    // thread u are polled together and staged in LDS, then one vector at a time
+    // (1) coarse gates of every unit and vector: the pre-activation words of
+    // thread u (both halves with up to 4 vectors) are polled together and
+    // staged in LDS, then one vector at a time
     if (SLICE) {
       slice_gates(false, tag, t, actm);
     } else if (gate) {
