@@ -194,6 +194,36 @@ wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_sam
                               int64_t n_frames, uint64_t seed, const wavernn_state* init, uint16_t* out_dev,
                               const wavernn_state* final_state, void* stream);
 
+/* Subscale models on the batched path (B > 1, not fused; Sec. 4): run steps
+ * [step0, step0 + n_steps) of the schedule of a call of n_samples samples per
+ * utterance, so that an utterance can be generated over several calls
+ * (streaming, or resuming from a saved state).  The schedule has
+ * wavernn_schedule_steps(m, n_samples) steps; step i runs position
+ * i - s (F + 1) of lane s with a future horizon F (Sec. 4.2), position i of
+ * every lane without one, and lane s at position p makes sample B p + s.
+ *   out_dev   [n_streams][n_samples] uint16: the whole utterances.  The call
+ *             writes the samples its steps make and reads, for the context of
+ *             its first steps, the ones earlier steps made, which earlier calls
+ *             must have written there.
+ *   init      the state after step step0 - 1 (required when step0 > 0; NULL =
+ *             default when step0 = 0); final: the state after the call's last
+ *             step (NULL = nowhere; may alias init).  Both with t0 = 0.
+ *   cond_dev, n_frames, seed: as for one wavernn_sample call of n_samples.
+ * Running steps [0, K) in any number of calls makes the same samples and
+ * final state as one wavernn_sample call, bit for bit.  The samples of lane s
+ * up to position p are final once step p + s (F + 1) has run.  n_steps = 0
+ * is valid (nothing launched).  Errors: E_INVALID (step range, missing init,
+ * as wavernn_sample), E_UNSUPPORTED (not a subscale model on the batched path;
+ * step0 > 0 with the window context and B not a power of two), E_HIP. */
+wavernn_status wavernn_sample_steps(wavernn_model* m, int32_t n_streams, int64_t n_samples, const float* cond_dev,
+                                    int64_t n_frames, uint64_t seed, int64_t step0, int64_t n_steps,
+                                    const wavernn_state* init, uint16_t* out_dev, const wavernn_state* final_state,
+                                    void* stream);
+/* Steps of the schedule of a subscale call of n_samples samples per utterance
+ * (n_samples / B, plus (B - 1)(F + 1) with a future horizon F); -1 for a model
+ * that wavernn_sample_steps does not serve or an invalid n_samples. */
+int64_t wavernn_schedule_steps(const wavernn_model* m, int64_t n_samples);
+
 /* wavernn_sample without any device allocation, for callers that cannot
  * allocate (code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc).  Same arguments, kernels and results as wavernn_sample

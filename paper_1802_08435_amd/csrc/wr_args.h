@@ -111,11 +111,14 @@ struct BatchArgs {
                             // at step t; < 0: lockstep rows (position t)
   int A;                    // steps by which the units form a horizon context ahead (0: at the step before)
   int64_t rows;             // positions per lane (samples per utterance / B)
-  int64_t T, t0;            // steps (rows, plus (B - 1)(F + 1) with a horizon) and first absolute step
-                            // (with a horizon: the first step of the schedule)
+  int64_t T, t0;            // steps of this launch and its first absolute step (with a horizon: the
+                            // first step of the schedule; lockstep rows: the first row)
   uint64_t seed;
-  const uint16_t* target;   // [U][B T] samples in time order, or null
-  uint16_t* out;            // [U][B T] or null
+  const uint16_t* target;   // [U][B rows] samples in time order, or null
+  uint16_t* out;            // [U][B rows] (with a horizon; lockstep rows: from row t0 on, utterances
+                            // B rows apart) or null
+  const uint16_t* prev;     // window context, t0 > 0: the utterances' samples [U][B rows] made before
+                            // step t0, which start the units' rings; null otherwise
   float* zc_out;            // [U][B T][256] or null
   float* zf_out;
   float* nll_out;           // [U][B T] or null

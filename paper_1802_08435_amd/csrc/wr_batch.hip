@@ -723,6 +723,27 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
     const float y = a.h_in ? xround(a.h_in[(size_t)min(v0 + b, a.S - 1) * H + col]) : 0.0f;
     aput(img + (col >> 5) * WR_FRAG, col & 31, y, b);
   }
+  // A launch that starts at step t0 > 0 of a call (the call resumed) starts
+  // each ring slot with what a launch from step 0 would hold there now: slot
+  // sl of an utterance holds sample q = B p + z, q = sl mod HC, of the last
+  // position p of lane z = sl mod B (B divides HC) made before step t0.
+  if (CTX && !(LAG && a.ctab) && a.prev && a.t0 > 0) {
+    const int per = HC / a.B;
+    const int u0 = v0 / a.B, nu = a.B >= L ? 1 : L / a.B;
+    for (int x = tid; x < nu * HC; x += WR_THREADS) {
+      const int uo = x / HC, sl = x % HC, z = sl % a.B, r = (sl - z) / a.B;
+      int y = 0;
+      if ((u0 + uo) * a.B < a.S) {
+        int64_t pz = LAG ? a.t0 - (int64_t)z * (a.F + 1 + a.A) : a.t0;   // lane z's positions made so far
+        if (pz > a.rows) pz = a.rows;
+        if (pz > 0) {
+          const int64_t p = pz - 1 - ((pz - 1 - r) % per + per) % per;   // last such p with p = r mod per
+          if (p >= 0) y = a.prev[(size_t)(u0 + uo) * a.B * a.rows + (size_t)a.B * p + z];
+        }
+      }
+      hist[uo * HC + sl] = y;
+    }
+  }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   f32x4 acc0, acc1;
@@ -808,7 +829,7 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       const int64_t p = vpos<LAG>(a, vv, td);          // lanes idle at step td drew nothing
       if (vv < a.S) {                                  // (but their words are waited for too)
         if (!wait_sample(a.xc + (size_t)(vv / L) * P.x_words + P.x_sp, L, P.SS, vv % L, tag, &y, a)) misc[0] = 1;
-        const int64_t qn = (int64_t)a.B * p + tid % a.B;
+        const int64_t qn = (int64_t)a.B * (p + (LAG ? 0 : a.t0)) + tid % a.B;   // the sample's index
         if (p >= 0 && p < a.rows) hist[(tid / a.B) * HC + (int)(qn & HCm)] = y;
       }
     }
@@ -819,12 +840,12 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
       const int b = x / half, jj = x % half;
       const int vb = min(v0 + b, a.S - 1), s = vb % a.B;
       const int64_t p1 = vpos<LAG>(a, vb, t + 1);           // position this vector runs next
-      const int64_t n1 = (int64_t)a.B * p1 + s;        // the sample it makes there
+      const int64_t n1 = (int64_t)a.B * (p1 + (LAG ? 0 : a.t0)) + s;   // the sample it makes there
       int64_t qn;
       bool seen;
       if (!LAG) {                                      // lockstep: the samples before n1 of earlier rows
         qn = n1 - 1 - jj;
-        seen = qn >= 0 && qn < (int64_t)a.B * (t + 1);
+        seen = qn >= 0 && qn < (int64_t)a.B * (a.t0 + t + 1);
       } else {                                         // horizon F: half before n1, half after
         const int d = jj < half / 2 ? -1 - jj : 1 + (jj - half / 2);
         qn = n1 + d;
@@ -912,7 +933,10 @@ __device__ __forceinline__ void bunit_role(const BatchArgs& a, int g, int k, uns
   };
   phase_c();
   phase_f();
-  if (table) context(-1);                              // step 0's context: row 0 of the table
+  // the first step's context: row 0 of the table; for a resumed window
+  // context, from the refilled rings (nothing to wait for: those samples were
+  // made before the launch); a call's step 0 has none
+  if (table || (CTX && a.prev)) context(-1);
   publish(1u, cbv(bl0, 0), cbv(bl0 + 1, 0));
   const xw* YC = X + P.x_yc;
   const xw* YF = X + P.x_yf;

@@ -962,6 +962,8 @@ struct RunIO {
   hipStream_t st;
   unsigned char* ws = nullptr;   // caller-provided workspace (device) instead of the model's buffers, or null
   size_t ws_cap = 0;             // its bytes
+  int64_t step0 = 0;             // subscale: the schedule steps [step0, step0 + n_steps) of the call run
+  int64_t n_steps = -1;          // (-1: the whole schedule, a wavernn_sample call)
 };
 
 inline size_t rup256(size_t n) { return (n + 255) / 256 * 256; }
@@ -1330,12 +1332,17 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.trace = m->trace;
   a.trace_steps = m->trace ? m->trace_steps : 0;
   const int64_t steps = a.rows + (F >= 0 ? (int64_t)(SB - 1) * (F + 1 + A) : 0);   // the last lane starts late
+  // the steps this call runs (a resumed subscale call: a part of the schedule)
+  const int64_t s0 = io.n_steps >= 0 ? io.step0 : 0, s1 = io.n_steps >= 0 ? io.step0 + io.n_steps : steps;
   // one launch of steps [t0, t0 + n) from state `in` to state `out` (null: default / nowhere)
   auto launch = [&](int64_t t0, int64_t n, const wavernn_state* in, const wavernn_state* out) -> wavernn_status {
     wavernn_status e = launch_fill(xc, (int64_t)B.G * B.x_words, io.st);
     if (e != WAVERNN_OK) return e;
     a.t0 = t0;
     a.T = n;
+    if (SB > 1 && F < 0 && io.out) a.out = io.out + (size_t)SB * t0;   // lockstep rows: from row t0 on
+    // a resumed window-context launch starts the units' sample rings from the utterances' buffer
+    a.prev = m->cfg.ctx_dim > 0 && !table && SB > 1 && t0 > 0 ? io.out : nullptr;
     a.h_in = in ? in->h : nullptr;
     a.c_in = in ? in->c_prev : nullptr;
     a.f_in = in ? in->f_prev : nullptr;
@@ -1347,7 +1354,7 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
     HIPOK(hipLaunchKernel(kernel, dim3(B.grid), dim3(WR_THREADS), args, B.lds, io.st));
     return WAVERNN_OK;
   };
-  if (!table) return launch(io.init ? io.init->t0 : 0, steps, io.init, io.fin);
+  if (!table) return SB > 1 ? launch(s0, s1 - s0, io.init, io.fin) : launch(io.init ? io.init->t0 : 0, steps, io.init, io.fin);
   // Conditioning CNN (Sec. 4.1).  Teacher forcing: the whole context table
   // from the targets, one launch.
   const int64_t rows = a.rows;
@@ -1359,7 +1366,7 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
     a.ctab_rows = rows;
     a.ctab_row0 = 0;
     a.ctab_step = 0;
-    return launch(0, steps, io.init, io.fin);
+    return launch(0, steps, io.init, io.fin);   // (scoring runs whole calls only)
   }
   // Sampling: chunks of LC = F - R + 1 steps (R the CNN's reach in rows).
   // Before chunk [t0, t0 + LC) the CNN runs on windows of LC + R rows, lane s
@@ -1372,8 +1379,8 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
   a.ctab_rows = W;
   a.ctab_step = -(int64_t)(F + 1);
   int cur = 0;
-  for (int64_t t0 = 0; t0 < steps; t0 += LC) {
-    const int64_t n = std::min(LC, steps - t0);
+  for (int64_t t0 = s0; t0 < s1; t0 += LC) {
+    const int64_t n = std::min(LC, s1 - t0);
     // only the sub-tensors that make a position in this chunk (a contiguous
     // range: the lag grows with s); an idle lane's table rows are never used
     int s_lo = SB, s_hi = -1;
@@ -1386,8 +1393,8 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
                       io.st, s_lo, s_hi - s_lo + 1)) != WAVERNN_OK)
       return st;
     a.ctab_row0 = t0;
-    const bool last = t0 + n >= steps;
-    const wavernn_state* in = t0 == 0 ? io.init : &m->cnn_state[cur];
+    const bool last = t0 + n >= s1;
+    const wavernn_state* in = t0 == s0 ? io.init : &m->cnn_state[cur];
     const wavernn_state* out = last ? io.fin : &m->cnn_state[cur ^ 1];
     if ((st = launch(t0, n, in, out)) != WAVERNN_OK) return st;
     cur ^= 1;
@@ -1628,6 +1635,37 @@ wavernn_status wavernn_sample(wavernn_model* m, int32_t n_streams, int64_t n_sam
                               const wavernn_state* final_state, void* stream) {
   RunIO io{n_streams, n_samples, cond_dev, n_frames, seed, init, final_state, nullptr, out_dev,
            nullptr, nullptr, nullptr, (hipStream_t)stream};
+  return run(m, io);
+}
+
+int64_t wavernn_schedule_steps(const wavernn_model* m, int64_t n_samples) {
+  if (!m || m->cfg.subscale <= 1 || m->fused || m->path != PATH_BATCHED) return -1;
+  const int B = m->cfg.subscale, F = horizon_of(m->cfg), A = lead_of(m->cfg);
+  if (n_samples < 0 || n_samples > ((int64_t)1 << 31) || n_samples % B) return -1;
+  return n_samples / B + (F >= 0 ? (int64_t)(B - 1) * (F + 1 + A) : 0);
+}
+
+wavernn_status wavernn_sample_steps(wavernn_model* m, int32_t n_streams, int64_t n_samples, const float* cond_dev,
+                                    int64_t n_frames, uint64_t seed, int64_t step0, int64_t n_steps,
+                                    const wavernn_state* init, uint16_t* out_dev, const wavernn_state* final_state,
+                                    void* stream) {
+  if (!m) return fail(WAVERNN_E_INVALID, "null model");
+  if (m->cfg.subscale <= 1 || m->fused || m->path != PATH_BATCHED)
+    return fail(WAVERNN_E_UNSUPPORTED, "wavernn_sample_steps serves subscale models on the batched path");
+  const int64_t K = wavernn_schedule_steps(m, n_samples);
+  if (K < 0) return fail(WAVERNN_E_INVALID, "n_samples %lld: not a multiple of subscale in [0, 2^31]", (long long)n_samples);
+  if (step0 < 0 || n_steps < 0 || step0 > K || n_steps > K - step0)
+    return fail(WAVERNN_E_INVALID, "steps [%lld, %lld) outside the call's schedule of %lld steps", (long long)step0,
+                (long long)(step0 + n_steps), (long long)K);
+  if (n_steps == 0) return WAVERNN_OK;
+  if (step0 > 0 && !init) return fail(WAVERNN_E_INVALID, "step0 > 0 needs the state after step0 - 1 (init)");
+  const int B = m->cfg.subscale;
+  if (step0 > 0 && m->cfg.ctx_dim > 0 && !m->has_cnn && (B & (B - 1)))
+    return fail(WAVERNN_E_UNSUPPORTED, "resuming a window-context call needs B a power of two (B = %d)", B);
+  RunIO io{n_streams, n_samples, cond_dev, n_frames, seed, init, final_state, nullptr, out_dev,
+           nullptr, nullptr, nullptr, (hipStream_t)stream};
+  io.step0 = step0;
+  io.n_steps = n_steps;
   return run(m, io);
 }
 

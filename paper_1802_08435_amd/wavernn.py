@@ -69,6 +69,11 @@ def lib():
         L.wavernn_sample_noalloc.restype = ctypes.c_int
         L.wavernn_sample_noalloc.argtypes = [vp, i32, i64, vp, i64, u64, ctypes.POINTER(State), vp,
                                              ctypes.POINTER(State), vp]
+        L.wavernn_sample_steps.restype = ctypes.c_int
+        L.wavernn_sample_steps.argtypes = [vp, i32, i64, vp, i64, u64, i64, i64, ctypes.POINTER(State), vp,
+                                           ctypes.POINTER(State), vp]
+        L.wavernn_schedule_steps.restype = i64
+        L.wavernn_schedule_steps.argtypes = [vp, i64]
         L.wavernn_score_teacher_forced.restype = ctypes.c_int
         L.wavernn_score_teacher_forced.argtypes = [vp, i32, i64, vp, i64, vp, ctypes.POINTER(State), vp, vp, vp, vp]
         L.wavernn_device_status.restype = ctypes.c_int
@@ -213,6 +218,25 @@ class Model:
                   None if sf is None else ctypes.byref(sf), _stream(stream)))
         if final is not None:
             final["t0"] = (init["t0"] if init is not None else 0) + n_samples
+        return out
+
+    def schedule_steps(self, n_samples: int) -> int:
+        """Steps of the schedule of a subscale call of n_samples per utterance (-1: not served)."""
+        return int(lib().wavernn_schedule_steps(self._h, n_samples))
+
+    def sample_steps(self, out, step0: int, n_steps: int, cond=None, seed: int = 1, init=None, final=None,
+                     stream=None):
+        """Run steps [step0, step0 + n_steps) of the schedule of a subscale call
+        whose whole utterances are out [S][n_samples] (uint16, holding every
+        sample earlier steps made); init: the state after step0 - 1 (a dict from
+        new_state, required when step0 > 0); final receives the state after the
+        last step (include/wavernn.h, wavernn_sample_steps)."""
+        S, n_samples = out.shape
+        n_frames = 0 if cond is None else cond.shape[1]
+        si, sf = self._state(init), self._state(final)
+        _check(lib().wavernn_sample_steps(self._h, S, n_samples, _ptr(cond), n_frames, seed, step0, n_steps,
+                                          None if si is None else ctypes.byref(si), _ptr(out),
+                                          None if sf is None else ctypes.byref(sf), _stream(stream)))
         return out
 
     def score(self, target, cond=None, init=None, logits: bool = True, nll: bool = True, stream=None):
