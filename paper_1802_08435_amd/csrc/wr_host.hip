@@ -97,6 +97,7 @@ struct wavernn_model {
   // concurrent batch-1 launches: a few utterances, each on its own persistent
   // grid and its own internal stream, all grids co-resident at once
   int nfan = 0;                      // most utterances served this way (0: none)
+  bool score_fan = false;            // scoring runs up to nfan utterances' recurrence grids side by side
   hipStream_t fan_st[WR_FAN - 1] = {};  // launches 1 .. (launch 0 runs on the caller's stream)
   hipEvent_t fan_fork = nullptr, fan_join[WR_FAN - 1] = {};
   xw* d_fxc[WR_FAN] = {};            // exchange words of launch i
@@ -387,6 +388,8 @@ wavernn_status check_coresident(wavernn_model* m, const void* k, int grid, int l
   return WAVERNN_OK;
 }
 
+int score_lds(int H);
+
 // Concurrent batch-1 launches for up to WR_FAN utterances, when that many
 // persistent grids fit the device together: internal streams (default
 // priority), fork / join events, and per-launch exchange words.
@@ -408,6 +411,12 @@ wavernn_status build_fanout(wavernn_model* m) {
     if (s != WAVERNN_OK) return s;
   }
   m->nfan = n;
+  if (m->sk) {   // the scoring recurrence's grids (H / 16 workgroups each) of n utterances together
+    const int H = P.H;
+    int sc_cu = 0;
+    HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&sc_cu, m->sk, WR_THREADS, score_lds(H)));
+    m->score_fan = sc_cu * prop.multiProcessorCount >= n * (H / 16) && 2 * H <= P.x_words;
+  }
   return WAVERNN_OK;
 }
 
@@ -1149,9 +1158,23 @@ wavernn_status run_score(wavernn_model* m, const RunIO& io) {
   const int64_t n_cb = m->cfg.cond_dim > 0 ? io.n_frames : 1;
   const bool post = io.zc || io.zf || io.nll;
   const int64_t ch = std::min(CH, rows);   // rows of one chunk of the output layers
-  if (rows > m->traj_cap || (post && ch > m->so_cap) || n_cb > m->cb_cap) HIPOK(hipStreamSynchronize(io.st));
+  // up to nfan utterances: one recurrence grid each, side by side on the
+  // caller's stream and the internal ones (each its own exchange words and
+  // table, as concurrent sampling), joined before the output layers
+  const bool fan = io.S > 1 && io.S <= m->nfan && m->score_fan;
+  if (rows > m->traj_cap || (post && ch > m->so_cap) || n_cb > m->cb_cap || (fan && n_cb > m->fcb_cap))
+    HIPOK(hipStreamSynchronize(io.st));
   wavernn_status st = grow_cb(m, &m->d_cb, &m->cb_cap, n_cb);
   if (st != WAVERNN_OK) return st;
+  if (fan && n_cb > m->fcb_cap) {
+    int64_t cap = 0;
+    for (int i = 0; i < m->nfan && st == WAVERNN_OK; ++i) {
+      cap = m->fcb_cap;
+      st = grow_cb(m, &m->d_fcb[i], &cap, n_cb);
+    }
+    if (st != WAVERNN_OK) return st;
+    m->fcb_cap = cap;
+  }
   if (rows > m->traj_cap) {
     if ((st = m->alloc(&m->d_traj, (size_t)2 * rows * Hh * 4)) != WAVERNN_OK) return st;
     m->traj_cap = rows;
@@ -1162,15 +1185,20 @@ wavernn_status run_score(wavernn_model* m, const RunIO& io) {
     m->so_cap = ch;
   }
   const int H = m->plan.H, Dc = m->cfg.cond_dim;
+  if (fan) HIPOK(hipEventRecord(m->fan_fork, io.st));
   for (int s = 0; s < io.S; ++s) {
+    hipStream_t sst = fan && s > 0 ? m->fan_st[s - 1] : io.st;
+    xw* xc = fan ? m->d_fxc[s] : m->d_xc;
+    float* cbt = fan ? m->d_fcb[s] : m->d_cb;
+    if (fan && s > 0) HIPOK(hipStreamWaitEvent(sst, m->fan_fork, 0));
     const float* feat = io.cond ? io.cond + (size_t)s * io.n_frames * Dc : nullptr;
-    if ((st = launch_cond(m, feat, n_cb, 1, m->d_cb, io.st)) != WAVERNN_OK) return st;
-    if ((st = launch_fill(m->d_xc, 2 * H, io.st)) != WAVERNN_OK) return st;
+    if ((st = launch_cond(m, feat, n_cb, 1, cbt, sst)) != WAVERNN_OK) return st;
+    if ((st = launch_fill(xc, 2 * H, sst)) != WAVERNN_OK) return st;
     ScoreArgs a;
     memset(&a, 0, sizeof a);
     a.w = m->d_srw;
     a.Iw = m->d_I;
-    a.cb = m->d_cb;
+    a.cb = cbt;
     a.n_cb = n_cb;
     a.frame_len = Dc > 0 ? (m->cfg.frame_len > 0 ? m->cfg.frame_len : 1) : (1 << 30);
     a.H = H;
@@ -1190,13 +1218,16 @@ wavernn_status run_score(wavernn_model* m, const RunIO& io) {
     }
     a.traj_c = m->d_traj + (size_t)s * io.T * Hh;
     a.traj_f = m->d_traj + (size_t)(io.S + s) * io.T * Hh;
-    a.xc = m->d_xc;
+    a.xc = xc;
     a.err = m->d_err;
     a.limit = kWaitTicks;
     void* args[] = {&a};
     // an ordinary launch of H / 16 workgroups (co-residency checked at create; waits bounded)
-    HIPOK(hipLaunchKernel(m->sk, dim3(H / 16), dim3(WR_THREADS), args, score_lds(H), io.st));
+    HIPOK(hipLaunchKernel(m->sk, dim3(H / 16), dim3(WR_THREADS), args, score_lds(H), sst));
+    if (fan && s > 0) HIPOK(hipEventRecord(m->fan_join[s - 1], sst));
   }
+  if (fan)
+    for (int s = 1; s < io.S; ++s) HIPOK(hipStreamWaitEvent(io.st, m->fan_join[s - 1], 0));
   if (!post) return WAVERNN_OK;
   for (int64_t r0 = 0; r0 < rows; r0 += CH) {
     const int n = (int)std::min(CH, rows - r0);
@@ -1416,7 +1447,8 @@ wavernn_status run(wavernn_model* m, RunIO& io, bool noalloc = false) {
   if (m->fused) return run_persist(m, io);   // one fused launch per utterance
   if (m->path == PATH_PERSIST) {
     // one utterance (or a model that runs its utterances one after another) scores on the recurrence kernel
-    if (io.target && m->sk && (io.S == 1 || (!m->nfan && !m->has_batch))) return run_score(m, io);
+    if (io.target && m->sk && (io.S == 1 || (io.S <= m->nfan && m->score_fan) || (!m->nfan && !m->has_batch)))
+      return run_score(m, io);
     if (io.S > 1 && io.S <= m->nfan) return run_fanout(m, io);
     return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);
   }

@@ -6,8 +6,9 @@ Bars: scoring the sampler's own output reproduces the sampler's state bit
 for bit (the gate arithmetic is the sampling head's), shown by scoring
 a sampled utterance whole and from the sampler's state at a midpoint; logits
 and NLL against the oracle within 1e-3 at small sizes and 2e-2 (bf16
-weights) at H = 896; against the sampling kernel run with forced classes (the
-path that scores several utterances side by side) within the same bounds.
+weights) at H = 896; several utterances side by side (one recurrence grid
+each) equal to one at a time bit for bit; against the batched sampling kernel
+run with forced classes (the path for more utterances) within the same bounds.
 """
 import numpy as np
 import pytest
@@ -80,22 +81,46 @@ def test_scoring_logits_and_nll_against_the_oracle(H, tol):
     m.close()
 
 
-def test_scoring_matches_the_sampling_kernel_with_forced_classes():
-    """With max_streams = 2, two utterances score side by side on the sampling
-    kernel (forced classes); one utterance scores on the recurrence kernel."""
+def test_scoring_utterances_side_by_side_equal_one_at_a_time():
+    """With max_streams = 3, three utterances score side by side: one
+    recurrence grid each on its own stream, their output layers together;
+    every logit and NLL equals scoring the utterance alone, bit for bit."""
     H, N = 896, 1200
     w = synth.make_weights(H, seed=7, cond_dim=64)
-    feat = synth.features(2, N, per_stream_seed=True)
-    tgt = np.concatenate([synth.target_signal(1, N, seed=4 + s, kind=k) for s, k in ((0, "sines"), (1, "uniform"))])
-    m = wavernn.Model(w, max_streams=2)
-    assert m.path(2)[0] == "concurrent"
-    both = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
-    for s in range(2):
+    feat = synth.features(3, N, per_stream_seed=True)
+    tgt = np.concatenate([synth.target_signal(1, N, seed=4 + s, kind=k)
+                          for s, k in ((0, "sines"), (1, "uniform"), (2, "sines"))])
+    m = wavernn.Model(w, max_streams=3)
+    assert m.path(3)[0] == "concurrent"
+    all3 = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    for s in range(3):
         one = {k: host(v) for k, v in m.score(cuda(tgt[s:s + 1]), cond=cuda(feat[s:s + 1])).items()}
         m.device_status()
-        assert np.abs(one["zc"][0] - both["zc"][s]).max() <= 2e-2
-        assert np.abs(one["zf"][0] - both["zf"][s]).max() <= 2e-2
-        np.testing.assert_allclose(one["nll"][0], both["nll"][s], rtol=1e-3, atol=4e-2)
+        for k in ("zc", "zf", "nll"):
+            np.testing.assert_array_equal(one[k][0], all3[k][s], err_msg=f"{k} of utterance {s}")
+    m.close()
+
+
+def test_scoring_matches_the_batched_sampling_kernel_with_forced_classes():
+    """Five utterances of a model for up to 8 score on the batched sampling
+    kernel with forced classes; each utterance alone on the recurrence kernel
+    agrees within the bf16 bounds."""
+    H, N, S = 896, 600, 5
+    w = synth.make_weights(H, seed=7, cond_dim=64)
+    feat = synth.features(S, N, per_stream_seed=True)
+    tgt = np.concatenate([synth.target_signal(1, N, seed=4 + s, kind="sines" if s % 2 else "uniform")
+                          for s in range(S)])
+    m = wavernn.Model(w, max_streams=8)
+    assert m.path(S)[0] == "batched"
+    many = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m.device_status()
+    for s in range(S):
+        one = {k: host(v) for k, v in m.score(cuda(tgt[s:s + 1]), cond=cuda(feat[s:s + 1])).items()}
+        m.device_status()
+        assert np.abs(one["zc"][0] - many["zc"][s]).max() <= 2e-2
+        assert np.abs(one["zf"][0] - many["zf"][s]).max() <= 2e-2
+        np.testing.assert_allclose(one["nll"][0], many["nll"][s], rtol=1e-3, atol=4e-2)
     m.close()
 
 
