@@ -298,7 +298,7 @@ def main() -> int:
                 and w.get("cnn") is None else None)
     # teacher-forced scoring of the last sampled utterance (logits of both heads and the NLL)
     score = None
-    if path == "persistent" and S == 1 or path == "concurrent":   # one recurrence grid per utterance
+    if w["B"] == 1 and path in ("persistent", "concurrent", "batched"):   # dense models: the recurrence kernels
         m.score(out, cond=feat)
         torch.cuda.synchronize()
         sm = []
@@ -313,7 +313,9 @@ def main() -> int:
         smed = float(np.median(sm))
         score = {"call_ms_median": round(smed, 4), "samples_per_s": round(S * T / (smed / 1000.0), 1),
                  "utterances": S, "us_per_step": round(smed * 1000.0 / T, 4),
-                 "kernels": "wr_score_kernel (recurrence) + wr_cnn_gemm (output layers over all steps) + wr_score_nll"}
+                 "kernels": ("wr_score_kernel (one grid per utterance)" if S <= 4 else
+                             "wr_score_multi (8 utterances per grid, 4 grids side by side)") +
+                            " + wr_cnn_gemm (output layers over all steps) + wr_score_nll"}
     ms = float(np.mean(call_ms))
     samples = S * T
     value = samples * args.steps / wall

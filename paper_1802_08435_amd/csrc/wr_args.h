@@ -65,6 +65,9 @@ struct PersistArgs {
 };
 
 // Teacher-forced recurrence of the dense batch-1 model (wr_score.hip).
+// With several utterances (wr_score_multi, nv of them) every per-utterance
+// array holds them one after another: cb [nv][n_cb][3H], target [nv][T],
+// h [nv][H], c / f [nv], traj [nv][T][Hh]; xc is [2][8][H].
 struct ScoreArgs {
   const uint4* w;           // [H/16][3][H/32][64 lanes] R fragments: workgroup k, gate g: rows g H + 16 k ..
   const float* Iw;          // [3H][3], I* mask applied
@@ -85,6 +88,7 @@ struct ScoreArgs {
   xw* xc;                   // [2][H] exchange words, zeroed before the launch
   unsigned* err;
   u64 limit;
+  int nv;                   // wr_score_multi: utterances of the launch (1..8)
 };
 
 struct BatchArgs {
@@ -185,6 +189,7 @@ const void* wr_small_kernel_ptr();
 const void* wr_uniforms_kernel_ptr();
 const void* wr_persist_kernel_ptr(int KH);   // null if no instantiation for KH
 const void* wr_score_kernel_ptr(int KT2);    // teacher-forced recurrence for H = 32 KT2; null if none
+const void* wr_score_multi_ptr(int KT2);     // the same for up to 8 utterances at once
 const void* wr_score_nll_ptr();
 const void* wr_sparse_kernel_ptr(int KH, int GU);   // null if no instantiation
 const void* wr_cond_kernel_ptr();

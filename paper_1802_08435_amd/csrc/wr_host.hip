@@ -83,6 +83,10 @@ struct wavernn_model {
   // output layers as GEMM fragments (O1 [NP][Hh], O2 [256][NP], O3, O4; NP = Hh
   // rounded up to 128) and biases, and the buffers of a call
   const void* sk = nullptr;
+  const void* smk = nullptr;         // the scoring recurrence for up to 8 utterances at once (null: none)
+  xw* d_sxc[WR_FAN] = {};            // its exchange words [2][8][H] per slot
+  float* d_scb[WR_FAN] = {};         // its tables [8][frames][3H] per slot
+  int64_t scb_cap = 0;               // floats of each
   uint4* d_srw = nullptr;             // [H/16][3][H/32][64] R fragments of the scoring recurrence
   uint4* d_sw = nullptr;
   float* d_sb = nullptr;
@@ -389,6 +393,7 @@ wavernn_status check_coresident(wavernn_model* m, const void* k, int grid, int l
 }
 
 int score_lds(int H);
+int score_multi_lds(int H);
 
 // Concurrent batch-1 launches for up to WR_FAN utterances, when that many
 // persistent grids fit the device together: internal streams (default
@@ -411,11 +416,13 @@ wavernn_status build_fanout(wavernn_model* m) {
     if (s != WAVERNN_OK) return s;
   }
   m->nfan = n;
-  if (m->sk) {   // the scoring recurrence's grids (H / 16 workgroups each) of n utterances together
+  if (m->sk) {   // the scoring recurrences' grids (H / 16 workgroups each) of n launches together
     const int H = P.H;
-    int sc_cu = 0;
-    HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&sc_cu, m->sk, WR_THREADS, score_lds(H)));
-    m->score_fan = sc_cu * prop.multiProcessorCount >= n * (H / 16) && 2 * H <= P.x_words;
+    int c1 = 0, c8 = 0;
+    HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&c1, m->sk, WR_THREADS, score_lds(H)));
+    if (m->smk) HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&c8, m->smk, WR_THREADS, score_multi_lds(H)));
+    const int per_cu = m->smk ? std::min(c1, c8) : c1;
+    m->score_fan = per_cu * prop.multiProcessorCount >= n * (H / 16);
   }
   return WAVERNN_OK;
 }
@@ -758,6 +765,7 @@ wavernn_status build_cnn(wavernn_model* m, const wavernn_ctx_cnn* n) {
 
 // LDS of the scoring recurrence: the operand image of h, [3][16] pre-activations, misc.
 int score_lds(int H) { return H / 32 * WR_FRAG + 48 * 4 + 64; }
+int score_multi_lds(int H) { return H / 32 * WR_FRAG + 3 * 8 * 16 * 4 + 64; }
 
 // Teacher-forced scoring on the dense batch-1 plan: the recurrence kernel
 // (the plan's units, heads that evaluate their own slices from the given
@@ -804,7 +812,11 @@ wavernn_status build_score(wavernn_model* m, const wavernn_weights* w) {
   if ((s = m->upload(&m->d_sw, wv.data(), wv.size() * 2)) != WAVERNN_OK) return s;
   if ((s = m->upload(&m->d_sb, bv.data(), bv.size() * 4)) != WAVERNN_OK) return s;
   HIPOK(hipFuncSetAttribute(wr_cnn_gemm_ptr(), hipFuncAttributeMaxDynamicSharedMemorySize, 2 * CNN_LDS_BUF));
-  return check_coresident(m, m->sk, H / 16, score_lds(H), "scoring");
+  if ((s = check_coresident(m, m->sk, H / 16, score_lds(H), "scoring")) != WAVERNN_OK) return s;
+  // several utterances per launch where its grid fits too (else one at a time)
+  m->smk = wr_score_multi_ptr(H / 32);
+  if (m->smk && check_coresident(m, m->smk, H / 16, score_multi_lds(H), "scoring") != WAVERNN_OK) m->smk = nullptr;
+  return WAVERNN_OK;
 }
 
 // One CNN layer as a GEMM (see CnnGemmArgs).
@@ -1158,22 +1170,30 @@ wavernn_status run_score(wavernn_model* m, const RunIO& io) {
   const int64_t n_cb = m->cfg.cond_dim > 0 ? io.n_frames : 1;
   const bool post = io.zc || io.zf || io.nll;
   const int64_t ch = std::min(CH, rows);   // rows of one chunk of the output layers
-  // up to nfan utterances: one recurrence grid each, side by side on the
-  // caller's stream and the internal ones (each its own exchange words and
-  // table, as concurrent sampling), joined before the output layers
-  const bool fan = io.S > 1 && io.S <= m->nfan && m->score_fan;
-  if (rows > m->traj_cap || (post && ch > m->so_cap) || n_cb > m->cb_cap || (fan && n_cb > m->fcb_cap))
+  // Up to nfan utterances: one single-utterance grid each, side by side on
+  // the caller's stream and the internal ones (measured faster than one grid
+  // carrying them); more: launches of up to 8 on the several-utterance
+  // kernel, nfan of them side by side.  Each slot has its own exchange words
+  // and table; all are joined before the output layers.
+  const int nf = m->score_fan ? m->nfan : 1;
+  const int LV = io.S > nf && m->smk ? 8 : 1;
+  const int G = (io.S + LV - 1) / LV;
+  const int conc = std::min(G, nf);
+  const bool slots = conc > 1 || LV > 1;   // per-slot buffers (else the model's own)
+  const int H = m->plan.H, Dc = m->cfg.cond_dim;
+  const int64_t cbf = (int64_t)8 * n_cb * 3 * H;    // table floats per slot (up to 8 utterances)
+  if (rows > m->traj_cap || (post && ch > m->so_cap) || n_cb > m->cb_cap || (slots && cbf > m->scb_cap))
     HIPOK(hipStreamSynchronize(io.st));
   wavernn_status st = grow_cb(m, &m->d_cb, &m->cb_cap, n_cb);
   if (st != WAVERNN_OK) return st;
-  if (fan && n_cb > m->fcb_cap) {
-    int64_t cap = 0;
-    for (int i = 0; i < m->nfan && st == WAVERNN_OK; ++i) {
-      cap = m->fcb_cap;
-      st = grow_cb(m, &m->d_fcb[i], &cap, n_cb);
+  if (slots) {
+    for (int i = 0; i < WR_FAN; ++i)
+      if (!m->d_sxc[i] && (st = m->alloc(&m->d_sxc[i], (size_t)(2 * 8 * H + 1) / 2 * 8)) != WAVERNN_OK) return st;
+    if (cbf > m->scb_cap) {
+      for (int i = 0; i < WR_FAN; ++i)
+        if ((st = m->alloc(&m->d_scb[i], (size_t)cbf * 4)) != WAVERNN_OK) return st;
+      m->scb_cap = cbf;
     }
-    if (st != WAVERNN_OK) return st;
-    m->fcb_cap = cap;
   }
   if (rows > m->traj_cap) {
     if ((st = m->alloc(&m->d_traj, (size_t)2 * rows * Hh * 4)) != WAVERNN_OK) return st;
@@ -1184,16 +1204,16 @@ wavernn_status run_score(wavernn_model* m, const RunIO& io) {
     if ((st = m->alloc(&m->d_sz, (size_t)2 * ch * 256 * 4)) != WAVERNN_OK) return st;
     m->so_cap = ch;
   }
-  const int H = m->plan.H, Dc = m->cfg.cond_dim;
-  if (fan) HIPOK(hipEventRecord(m->fan_fork, io.st));
-  for (int s = 0; s < io.S; ++s) {
-    hipStream_t sst = fan && s > 0 ? m->fan_st[s - 1] : io.st;
-    xw* xc = fan ? m->d_fxc[s] : m->d_xc;
-    float* cbt = fan ? m->d_fcb[s] : m->d_cb;
-    if (fan && s > 0) HIPOK(hipStreamWaitEvent(sst, m->fan_fork, 0));
-    const float* feat = io.cond ? io.cond + (size_t)s * io.n_frames * Dc : nullptr;
-    if ((st = launch_cond(m, feat, n_cb, 1, cbt, sst)) != WAVERNN_OK) return st;
-    if ((st = launch_fill(xc, 2 * H, sst)) != WAVERNN_OK) return st;
+  if (conc > 1) HIPOK(hipEventRecord(m->fan_fork, io.st));
+  for (int g = 0; g < G; ++g) {
+    const int slot = g % conc, s0 = g * LV, nv = std::min(LV, io.S - s0);
+    hipStream_t sst = slot > 0 ? m->fan_st[slot - 1] : io.st;
+    xw* xc = slots ? m->d_sxc[slot] : m->d_xc;
+    float* cbt = slots ? m->d_scb[slot] : m->d_cb;
+    if (slot > 0 && g < conc) HIPOK(hipStreamWaitEvent(sst, m->fan_fork, 0));
+    const float* feat = io.cond ? io.cond + (size_t)s0 * io.n_frames * Dc : nullptr;
+    if ((st = launch_cond(m, feat, n_cb, nv, cbt, sst)) != WAVERNN_OK) return st;
+    if ((st = launch_fill(xc, 2 * LV * H, sst)) != WAVERNN_OK) return st;
     ScoreArgs a;
     memset(&a, 0, sizeof a);
     a.w = m->d_srw;
@@ -1205,29 +1225,34 @@ wavernn_status run_score(wavernn_model* m, const RunIO& io) {
     a.Hh = Hh;
     a.T = io.T;
     a.t0 = io.init ? io.init->t0 : 0;
-    a.target = io.target + (size_t)s * io.T;
+    a.target = io.target + (size_t)s0 * io.T;
     if (io.init) {
-      a.h_in = io.init->h + (size_t)s * H;
-      a.c_in = io.init->c_prev + s;
-      a.f_in = io.init->f_prev + s;
+      a.h_in = io.init->h + (size_t)s0 * H;
+      a.c_in = io.init->c_prev + s0;
+      a.f_in = io.init->f_prev + s0;
     }
     if (io.fin) {
-      a.h_out = io.fin->h + (size_t)s * H;
-      a.c_out = io.fin->c_prev + s;
-      a.f_out = io.fin->f_prev + s;
+      a.h_out = io.fin->h + (size_t)s0 * H;
+      a.c_out = io.fin->c_prev + s0;
+      a.f_out = io.fin->f_prev + s0;
     }
-    a.traj_c = m->d_traj + (size_t)s * io.T * Hh;
-    a.traj_f = m->d_traj + (size_t)(io.S + s) * io.T * Hh;
+    a.traj_c = m->d_traj + (size_t)s0 * io.T * Hh;
+    a.traj_f = m->d_traj + (size_t)(io.S + s0) * io.T * Hh;
     a.xc = xc;
     a.err = m->d_err;
     a.limit = kWaitTicks;
+    a.nv = nv;
     void* args[] = {&a};
     // an ordinary launch of H / 16 workgroups (co-residency checked at create; waits bounded)
-    HIPOK(hipLaunchKernel(m->sk, dim3(H / 16), dim3(WR_THREADS), args, score_lds(H), sst));
-    if (fan && s > 0) HIPOK(hipEventRecord(m->fan_join[s - 1], sst));
+    if (LV > 1)
+      HIPOK(hipLaunchKernel(m->smk, dim3(H / 16), dim3(WR_THREADS), args, score_multi_lds(H), sst));
+    else
+      HIPOK(hipLaunchKernel(m->sk, dim3(H / 16), dim3(WR_THREADS), args, score_lds(H), sst));
   }
-  if (fan)
-    for (int s = 1; s < io.S; ++s) HIPOK(hipStreamWaitEvent(io.st, m->fan_join[s - 1], 0));
+  for (int i = 1; i < conc; ++i) {
+    HIPOK(hipEventRecord(m->fan_join[i - 1], m->fan_st[i - 1]));
+    HIPOK(hipStreamWaitEvent(io.st, m->fan_join[i - 1], 0));
+  }
   if (!post) return WAVERNN_OK;
   for (int64_t r0 = 0; r0 < rows; r0 += CH) {
     const int n = (int)std::min(CH, rows - r0);
@@ -1447,7 +1472,7 @@ wavernn_status run(wavernn_model* m, RunIO& io, bool noalloc = false) {
   if (m->fused) return run_persist(m, io);   // one fused launch per utterance
   if (m->path == PATH_PERSIST) {
     // one utterance (or a model that runs its utterances one after another) scores on the recurrence kernel
-    if (io.target && m->sk && (io.S == 1 || (io.S <= m->nfan && m->score_fan) || (!m->nfan && !m->has_batch)))
+    if (io.target && m->sk && (io.S == 1 || m->smk || (io.S <= m->nfan && m->score_fan) || (!m->nfan && !m->has_batch)))
       return run_score(m, io);
     if (io.S > 1 && io.S <= m->nfan) return run_fanout(m, io);
     return io.S > 1 && m->has_batch ? run_batch(m, io) : run_persist(m, io);

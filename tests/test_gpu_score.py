@@ -6,9 +6,8 @@ Bars: scoring the sampler's own output reproduces the sampler's state bit
 for bit (the gate arithmetic is the sampling head's), shown by scoring
 a sampled utterance whole and from the sampler's state at a midpoint; logits
 and NLL against the oracle within 1e-3 at small sizes and 2e-2 (bf16
-weights) at H = 896; several utterances side by side (one recurrence grid
-each) equal to one at a time bit for bit; against the batched sampling kernel
-run with forced classes (the path for more utterances) within the same bounds.
+weights) at H = 896; several utterances at once (up to 8 per grid, grids side
+by side) equal to one at a time bit for bit, from a given state.
 """
 import numpy as np
 import pytest
@@ -81,46 +80,32 @@ def test_scoring_logits_and_nll_against_the_oracle(H, tol):
     m.close()
 
 
-def test_scoring_utterances_side_by_side_equal_one_at_a_time():
-    """With max_streams = 3, three utterances score side by side: one
-    recurrence grid each on its own stream, their output layers together;
-    every logit and NLL equals scoring the utterance alone, bit for bit."""
-    H, N = 896, 1200
+@pytest.mark.parametrize("S,max_streams", [(3, 3), (11, 16)])
+def test_scoring_several_utterances_equals_one_at_a_time(S, max_streams):
+    """Several utterances score together: up to 8 per recurrence grid (the
+    vectors in the operand rows of the same products), up to 4 grids side by
+    side (11 utterances: launches of 8 and 3), then the output layers over all
+    of them; every logit and NLL equals scoring the utterance alone on the
+    single-utterance kernel, bit for bit."""
+    H, N = 896, 600
     w = synth.make_weights(H, seed=7, cond_dim=64)
-    feat = synth.features(3, N, per_stream_seed=True)
-    tgt = np.concatenate([synth.target_signal(1, N, seed=4 + s, kind=k)
-                          for s, k in ((0, "sines"), (1, "uniform"), (2, "sines"))])
-    m = wavernn.Model(w, max_streams=3)
-    assert m.path(3)[0] == "concurrent"
-    all3 = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
-    m.device_status()
-    for s in range(3):
-        one = {k: host(v) for k, v in m.score(cuda(tgt[s:s + 1]), cond=cuda(feat[s:s + 1])).items()}
-        m.device_status()
-        for k in ("zc", "zf", "nll"):
-            np.testing.assert_array_equal(one[k][0], all3[k][s], err_msg=f"{k} of utterance {s}")
-    m.close()
-
-
-def test_scoring_matches_the_batched_sampling_kernel_with_forced_classes():
-    """Five utterances of a model for up to 8 score on the batched sampling
-    kernel with forced classes; each utterance alone on the recurrence kernel
-    agrees within the bf16 bounds."""
-    H, N, S = 896, 600, 5
-    w = synth.make_weights(H, seed=7, cond_dim=64)
-    feat = synth.features(S, N, per_stream_seed=True)
+    feat = synth.features(S, N + 120, per_stream_seed=True)   # frames from sample 0 (the state is at 120)
     tgt = np.concatenate([synth.target_signal(1, N, seed=4 + s, kind="sines" if s % 2 else "uniform")
                           for s in range(S)])
-    m = wavernn.Model(w, max_streams=8)
-    assert m.path(S)[0] == "batched"
-    many = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat)).items()}
+    m = wavernn.Model(w, max_streams=max_streams)
+    init = m.new_state(S)
+    init["h"].normal_(0.0, 0.3, generator=torch.Generator(device="cuda").manual_seed(5))
+    init["c"].random_(0, 256, generator=torch.Generator(device="cuda").manual_seed(6))
+    init["f"].random_(0, 256, generator=torch.Generator(device="cuda").manual_seed(7))
+    init["t0"] = 120
+    many = {k: host(v) for k, v in m.score(cuda(tgt), cond=cuda(feat), init=init).items()}
     m.device_status()
     for s in range(S):
-        one = {k: host(v) for k, v in m.score(cuda(tgt[s:s + 1]), cond=cuda(feat[s:s + 1])).items()}
+        one_init = {k: (v[s:s + 1] if k != "t0" else v) for k, v in init.items()}
+        one = {k: host(v) for k, v in m.score(cuda(tgt[s:s + 1]), cond=cuda(feat[s:s + 1]), init=one_init).items()}
         m.device_status()
-        assert np.abs(one["zc"][0] - many["zc"][s]).max() <= 2e-2
-        assert np.abs(one["zf"][0] - many["zf"][s]).max() <= 2e-2
-        np.testing.assert_allclose(one["nll"][0], many["nll"][s], rtol=1e-3, atol=4e-2)
+        for k in ("zc", "zf", "nll"):
+            np.testing.assert_array_equal(one[k][0], many[k][s], err_msg=f"{k} of utterance {s}")
     m.close()
 
 
