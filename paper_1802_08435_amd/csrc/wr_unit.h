@@ -120,33 +120,25 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
       __syncthreads();
       if (misc[0]) return;
     }
-    if (reader) {
-      const int r = (wave == 3 ? 0 : 64) + lane;
-      uint32_t pending = 0;
-      float y[4] = {0, 0, 0, 0};
-#pragma unroll
-      for (int m = 0; m < 4; ++m)
-        if (r + 128 * m < Hh) pending |= 1u << m;
-      WaitBudget wb{wr_clock(), 0};
-      while (pending) {
-        xw w[4];
-#pragma unroll
-        for (int m = 0; m < 4; ++m) w[m] = (pending >> m & 1u) ? xpeek(Y + r + 128 * m) : 0;
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-          if ((pending >> m & 1u) && xok(w[m], tag)) {
-            y[m] = xval(w[m]);
-            pending &= ~(1u << m);
+    if (reader) {   // words 4 q .. 4 q + 3 (one head's) per 16-byte load, q = lane of the two waves
+      const int q = (wave == 3 ? 0 : 64) + lane;
+      if (4 * q < Hh) {
+        WaitBudget wb{wr_clock(), 0};
+        xw4 w;
+        for (;;) {
+          w = xpeek4(xrsrc(xopaque(Y), (uint32_t)Hh * 4u), 16u * q);
+          if (xok4(w, tag)) break;
+          if (!wait_ok(wb, a.err, a.limit, a.err)) {
+            misc[0] = 1;
+            break;
           }
-        if (pending && !wait_ok(wb, a.err, a.limit, a.err)) {
-          misc[0] = 1;
-          break;
         }
-      }
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const int i = r + 128 * m;
-        if (i < Hh) aput(img + (kt0 + (i >> 5)) * WR_FRAG, i & 31, y[m]);
+        const int i = 4 * q;
+        unsigned char* f = img + (kt0 + (i >> 5)) * WR_FRAG;
+        aput(f, i & 31, xval(w.x));
+        aput(f, (i & 31) + 1, xval(w.y));
+        aput(f, (i & 31) + 2, xval(w.z));
+        aput(f, (i & 31) + 3, xval(w.w));
       }
     }
     __syncthreads();
