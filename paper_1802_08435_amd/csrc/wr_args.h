@@ -34,6 +34,7 @@ struct PersistArgs {
   const uint4* hw;          // [NH][8 waves][hw_frags][64 lanes] head fragments
   const uint4* uw;          // [NU] unit LDS blocks of P.u_lds_w bytes
   const uint4* ur;          // [2][NU*UCT][KT][64] coarse, then fine tiles x fine columns (VGPR-resident)
+  const uint4* mw;          // [NM][8 waves][mw_frags][64 lanes] mirror fragments, or null (no mirrors)
   const float* Iw;          // [3H][3], I* mask applied
   const float* b1;          // [Hh]
   const float* b2;          // [256]

@@ -5,7 +5,11 @@
 // slice (the two all-reduces on the critical path of a step); it also reads
 // the gate words of the half(s) it serves, without waiting, as the sampling
 // kernel reads them ahead.  Each unit workgroup reads both halves of h from
-// the heads and publishes its gate words for the next step.  The time per
+// the heads and publishes its gate words for the next step.  With mirrors
+// (the dense plan) each mirror waits for the coarse partials, publishes its
+// words of the coarse rows for the next step and waits for the fine partials;
+// the heads wait for those words at the start of a step, and the fine words
+// and fine partials sit in the sampling kernel's two buffers.  The time per
 // step of this kernel is what the exchange pattern alone costs (Sec. 2.1 of
 // the paper counts such a synchronization cost per step).
 #include "wr_kern.h"
@@ -23,14 +27,25 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   float* zs = (float*)(misc + 16);               // [2][256] logit sums (written, never read)
   const xw* GA = a.xc + P.x_ga;
   const xw* GF = a.xc + P.x_gf;
+  const xw* HF = a.xc + P.x_hf;
+  float* gsink = zs + 512;                       // [WR_THREADS] (written, never read)
+  auto gsink_add = [&](float v) { gsink[tid] = v; };
   xw* YC = a.xc + P.x_yc;
   xw* YF = a.xc + P.x_yf;
   xw* PC = a.xc + P.x_pc;
   xw* PF = a.xc + P.x_pf;
   if (tid == 0) misc[0] = 0;
   __syncthreads();
+  // with mirrors: wait for their words of the coarse rows (3 per unit)
+  auto mirror_words = [&](uint32_t tag) {
+    if (P.NM == 0 || tid >= Hh) return;
+    const xw* ps[3] = {HF + tid, HF + Hh + tid, HF + 2 * Hh + tid};
+    const xw w0[3] = {xpeek(ps[0]), xpeek(ps[1]), xpeek(ps[2])};
+    float v[3];
+    if (!poll_pref<3>(ps, w0, tag, v, a)) misc[0] = 1;
+    else gsink_add(v[0] + v[1] + v[2]);
+  };
   // gate words of every unit of a half (3 per unit), read once without waiting
-  float* gsink = zs + 512;                       // [WR_THREADS]
   auto gate_words = [&](const xw* G) {
     float acc = 0.0f;
     for (int u = tid; u < Hh; u += WR_THREADS)
@@ -57,18 +72,68 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   };
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
-    if (coarse) gate_words(GA);
+    if (coarse) mirror_words(tag);
     if (coarse && wave == 7)
       for (int i = lane; i < HR; i += 64) xpub(YC + HR * jk + i, tag, 0.0f);
     if (coarse && lane < 32) xpub(PC + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
+    if (coarse) gate_words(GA);   // (read while the partials are exchanged, as the sampling heads prefetch)
     gather(PC, tag);
     __syncthreads();
     if (misc[0]) return;
-    if (fine) gate_words(GF);
     if (fine && wave == 7)
       for (int i = lane; i < HR; i += 64) xpub(YF + HR * jk + i, tag, 0.0f);
-    if (fine && lane < 32) xpub(PF + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
-    gather(PF, tag);
+    xw* PFt = PF + wr_dbuf(t, P.x_pfs);
+    const uint32_t ftag = wr_dtag(t, P.x_pfs);
+    if (fine && lane < 32) xpub(PFt + (size_t)jk * P.x_ps + 32 * wave + lane, ftag, 0.0f);
+    if (fine) gate_words(GF + wr_dbuf(t, P.x_gfs));
+    gather(PFt, ftag);
+    __syncthreads();
+    if (misc[0]) return;
+  }
+}
+
+// A mirror: the coarse partials of step t, then its words of the coarse rows
+// for step t + 1, then the fine partials of step t (reading the fine rows'
+// words of step t meanwhile, without waiting).
+__device__ __forceinline__ void floor_mirror(const PersistArgs& a, int j, unsigned char* lds) {
+  const PersistPlan& P = a.P;
+  const int Hh = P.Hh, NK = P.NK;
+  const int tid = threadIdx.x, lane = tid & 63;
+  constexpr int MRW = 16 * WR_MTILES;
+  int* misc = (int*)lds;
+  float* zs = (float*)(misc + 16);               // [2][256] logit sums, then [WR_THREADS] (written, never read)
+  const xw* GF = a.xc + P.x_gf;
+  const xw* PC = a.xc + P.x_pc;
+  const xw* PF = a.xc + P.x_pf;
+  xw* HF = a.xc + P.x_hf + (size_t)MRW * j;
+  if (tid == 0) misc[0] = 0;
+  __syncthreads();
+  auto gather = [&](const xw* src, uint32_t tag) {
+    {
+      float y;
+      const int jj = lane < NK ? lane : 0;
+      if (!poll_sleepy<false>(src + (size_t)jj * P.x_ps + 255, tag, &y, a)) misc[0] = 1;
+    }
+    const int v = tid & 255, hh = tid >> 8, h0 = (NK + 1) / 2;
+    float s;
+    if (!sum_parts<16>(src, P.x_ps, hh ? h0 : 0, hh ? NK : h0, v, tag, &s, a)) misc[0] = 1;
+    else zs[hh * 256 + v] = s;
+  };
+  if (tid < MRW) xpub(HF + tid, 1u, 0.0f);
+  for (int64_t t = 0; t < a.T; ++t) {
+    const uint32_t tag = (uint32_t)(t + 1);
+    gather(PC, tag);
+    __syncthreads();
+    if (misc[0]) return;
+    if (t + 1 < a.T && tid < MRW) xpub(HF + tid, tag + 1, 0.0f);
+    {   // the fine rows' words of step t (read without waiting, while the fine partials are exchanged)
+      const xw* G = GF + wr_dbuf(t, P.x_gfs);
+      float acc = 0.0f;
+      for (int u = tid; u < Hh; u += WR_THREADS)
+        acc += xval(xpeek(G + u)) + xval(xpeek(G + Hh + u)) + xval(xpeek(G + 2 * Hh + u));
+      zs[512 + tid] = acc;
+    }
+    gather(PF + wr_dbuf(t, P.x_pfs), wr_dtag(t, P.x_pfs));
     __syncthreads();
     if (misc[0]) return;
   }
@@ -87,11 +152,12 @@ __device__ __forceinline__ void floor_unit(const PersistArgs& a, int k, unsigned
   const xw* YF = a.xc + P.x_yf;
   if (tid == 0) misc[0] = 0;
   __syncthreads();
-  auto publish = [&](uint32_t tag) {
-    if (tid < wpu) {
-      xpub(GA + tid, tag, 0.0f);
-      xpub(GF + tid, tag, 0.0f);
-    }
+  // the gate words of step s (the fine rows' in their buffer)
+  auto publish_c = [&](int64_t s) {
+    if (tid < wpu) xpub(GA + tid, (uint32_t)s + 1u, 0.0f);
+  };
+  auto publish_f = [&](int64_t s) {
+    if (tid < wpu) xpub(GF + wr_dbuf(s, P.x_gfs) + tid, wr_dtag(s, P.x_gfs), 0.0f);
   };
   auto gather_half = [&](const xw* Y, uint32_t tag, bool flags) {
     if (flags) {
@@ -129,14 +195,17 @@ __device__ __forceinline__ void floor_unit(const PersistArgs& a, int k, unsigned
     }
     __syncthreads();
   };
-  publish(1u);
+  publish_c(0);
+  publish_f(0);
   for (int64_t t = 0; t + 1 < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     gather_half(YC, tag, true);
     if (misc[0]) return;
+    if (P.NM) publish_c(t + 1);                  // with mirrors: the coarse columns' part once y_c is in
     gather_half(YF, tag, false);
     if (misc[0]) return;
-    publish(tag + 1);
+    if (!P.NM) publish_c(t + 1);
+    publish_f(t + 1);
   }
 }
 
@@ -147,7 +216,8 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_floor_kernel(PersistArgs a) 
   const int r = wr_role(a.P, blockIdx.x);
   if (r < 0) return;
   if (r < a.P.NH) floor_head(a, r, lds);
-  else floor_unit(a, r - a.P.NH, lds);
+  else if (r < a.P.NH + a.P.NM) floor_mirror(a, r - a.P.NH, lds);
+  else floor_unit(a, r - a.P.NH - a.P.NM, lds);
 }
 
 const void* wr_floor_kernel_ptr() { return (const void*)wr_floor_kernel; }

@@ -74,6 +74,7 @@ struct wavernn_model {
   bool sparse = false;               // block-sparse units
   bool fused = false;                // Fused Subscale WaveRNN 2x heads (Sec. 4.4)
   uint4 *d_hw = nullptr, *d_uw = nullptr, *d_ur = nullptr;
+  uint4* d_mw = nullptr;             // mirror fragments (dense batch-1 plan)
   float *d_I = nullptr, *d_bias = nullptr, *d_b1 = nullptr, *d_b2 = nullptr, *d_b3 = nullptr, *d_b4 = nullptr;
   float* d_cb = nullptr;             // [cb_cap][3H] bias + conditioning per frame
   int64_t cb_cap = 0;
@@ -395,6 +396,14 @@ wavernn_status check_coresident(wavernn_model* m, const void* k, int grid, int l
 int score_lds(int H);
 int score_multi_lds(int H);
 
+// Launch s of n persistent grids side by side: heads and mirrors on XCD
+// 8 s / n, units spread over the XCDs.
+PersistPlan fan_plan(const wavernn_model* m, int s, int n) {
+  PersistPlan P = m->plan;
+  wr_place(&P, 8 * s / n, 255);
+  return P;
+}
+
 // Concurrent batch-1 launches for up to WR_FAN utterances, when that many
 // persistent grids fit the device together: internal streams (default
 // priority), fork / join events, and per-launch exchange words.
@@ -404,7 +413,21 @@ wavernn_status build_fanout(wavernn_model* m) {
   HIPOK(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, m->pk, WR_THREADS, P.lds));
   hipDeviceProp_t prop;
   HIPOK(hipGetDeviceProperties(&prop, m->device));
-  int n = std::min(std::min(WR_FAN, (int)m->cfg.max_streams), per_cu * prop.multiProcessorCount / P.grid);
+  // launch i of n side by side puts its heads and mirrors on XCD 8 i / n and
+  // spreads its units (fan_plan); n fits when every XCD holds the busy blocks
+  // of all n grids at once (idle blocks return at once)
+  int n = std::min(WR_FAN, (int)m->cfg.max_streams);
+  for (; n >= 2; --n) {
+    int busy[8] = {};
+    for (int i = 0; i < n; ++i) {
+      const PersistPlan Q = fan_plan(m, i, n);
+      for (int b = 0; b < Q.grid; ++b)
+        if (wr_role(Q, b) >= 0) ++busy[b % 8];
+    }
+    bool fits = per_cu >= 1;
+    for (int x = 0; x < 8; ++x) fits = fits && busy[x] <= per_cu * (prop.multiProcessorCount / 8);
+    if (fits) break;
+  }
   if (n < 2) return WAVERNN_OK;
   HIPOK(hipEventCreateWithFlags(&m->fan_fork, hipEventDisableTiming));
   for (int i = 0; i < n; ++i) {
@@ -457,7 +480,22 @@ wavernn_status upload_dense_units(wavernn_model* m, const wavernn_weights* w) {
   }
   wavernn_status s;
   if ((s = m->upload(&m->d_uw, uw.data(), uw.size() * 2)) != WAVERNN_OK) return s;
-  return m->upload(&m->d_ur, ur.data(), ur.size() * 2);
+  if ((s = m->upload(&m->d_ur, ur.data(), ur.size() * 2)) != WAVERNN_OK) return s;
+  if (P.NM == 0) return WAVERNN_OK;
+  // mirror j, wave w: coarse row tiles 12 j + 3 (w % 4) + r (r < 3) over the
+  // fine column tiles (w / 4) MK + i (i < MK = KT / 2), as [r][i] fragments
+  const int MK = KT / 2;
+  std::vector<uint16_t> mw((size_t)P.NM * 8 * P.mw_frags * 512);
+  for (int j = 0; j < P.NM; ++j)
+    for (int wv = 0; wv < 8; ++wv) {
+      uint16_t* d = mw.data() + (size_t)(j * 8 + wv) * P.mw_frags * 512;
+      for (int r = 0; r < 3; ++r) {
+        const int tile = WR_MTILES * j + 3 * (wv % 4) + r;
+        auto rows = [&](int rr) { return rrow(tile, false, rr); };
+        for (int i = 0; i < MK; ++i) frag(d + (size_t)(r * MK + i) * 512, Rm, rows, Hh + 32 * ((wv / 4) * MK + i));
+      }
+    }
+  return m->upload(&m->d_mw, mw.data(), mw.size() * 2);
 }
 
 wavernn_status build_persist(wavernn_model* m, const wavernn_weights* w) {
@@ -1054,8 +1092,8 @@ wavernn_status run_small(wavernn_model* m, const RunIO& io) {
 
 // One persistent launch for utterance s of the call, with exchange words xc
 // and bias + conditioning table cb, on stream st.  A launch that runs alone
-// (solo) takes the tuned placement, one of several side by side the default
-// spread of the units over the XCDs.
+// (fan = 0) takes the tuned placement, one of fan side by side the placement
+// of fan_plan.
 PersistPlan solo_plan(const wavernn_model* m) {
   PersistPlan P = m->plan;
   wr_place(&P, m->solo_hx, m->solo_uxm);
@@ -1063,8 +1101,8 @@ PersistPlan solo_plan(const wavernn_model* m) {
 }
 
 wavernn_status launch_persist_one(wavernn_model* m, const RunIO& io, int s, xw* xc, float* cb, int64_t n_cb,
-                                  hipStream_t st, bool solo) {
-  const PersistPlan P = solo ? solo_plan(m) : m->plan;
+                                  hipStream_t st, int fan) {
+  const PersistPlan P = fan ? fan_plan(m, s, fan) : solo_plan(m);
   const int H = P.H, Dc = m->cfg.cond_dim;
   const int frame_len = m->cfg.frame_len > 0 ? m->cfg.frame_len : 1;
   {
@@ -1080,6 +1118,7 @@ wavernn_status launch_persist_one(wavernn_model* m, const RunIO& io, int s, xw* 
   a.hw = m->d_hw;
   a.uw = m->d_uw;
   a.ur = m->d_ur;
+  a.mw = m->d_mw;
   a.Iw = m->d_I;
   a.b1 = m->d_b1;
   a.b2 = m->d_b2;
@@ -1147,14 +1186,14 @@ wavernn_status run_persist(wavernn_model* m, const RunIO& io) {
     xw* xc;
     float* cb;
     wavernn_status st = carve_ws(io, 1, m->plan.x_words, (size_t)n_cb * 3 * m->plan.H, &xc, &cb);
-    for (int s = 0; s < io.S && st == WAVERNN_OK; ++s) st = launch_persist_one(m, io, s, xc, cb, n_cb, io.st, true);
+    for (int s = 0; s < io.S && st == WAVERNN_OK; ++s) st = launch_persist_one(m, io, s, xc, cb, n_cb, io.st, 0);
     return st;
   }
   if (n_cb > m->cb_cap) HIPOK(hipStreamSynchronize(io.st));
   wavernn_status st = grow_cb(m, &m->d_cb, &m->cb_cap, n_cb);
   if (st != WAVERNN_OK) return st;
   for (int s = 0; s < io.S; ++s)
-    if ((st = launch_persist_one(m, io, s, m->d_xc, m->d_cb, n_cb, io.st, true)) != WAVERNN_OK) return st;
+    if ((st = launch_persist_one(m, io, s, m->d_xc, m->d_cb, n_cb, io.st, 0)) != WAVERNN_OK) return st;
   return WAVERNN_OK;
 }
 
@@ -1316,10 +1355,10 @@ wavernn_status run_fanout(wavernn_model* m, const RunIO& io) {
   HIPOK(hipEventRecord(m->fan_fork, io.st));
   for (int s = 1; s < io.S; ++s) {
     HIPOK(hipStreamWaitEvent(m->fan_st[s - 1], m->fan_fork, 0));
-    if ((st = launch_persist_one(m, io, s, xc[s], cb[s], n_cb, m->fan_st[s - 1], false)) != WAVERNN_OK) return st;
+    if ((st = launch_persist_one(m, io, s, xc[s], cb[s], n_cb, m->fan_st[s - 1], io.S)) != WAVERNN_OK) return st;
     HIPOK(hipEventRecord(m->fan_join[s - 1], m->fan_st[s - 1]));
   }
-  if ((st = launch_persist_one(m, io, 0, xc[0], cb[0], n_cb, io.st, false)) != WAVERNN_OK) return st;
+  if ((st = launch_persist_one(m, io, 0, xc[0], cb[0], n_cb, io.st, io.S)) != WAVERNN_OK) return st;
   for (int s = 1; s < io.S; ++s) HIPOK(hipStreamWaitEvent(io.st, m->fan_join[s - 1], 0));
   return WAVERNN_OK;
 }

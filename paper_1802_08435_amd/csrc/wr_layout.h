@@ -67,6 +67,16 @@ WR_HD inline SmallLayout small_layout(int H) {
 // Unit k owns coarse tiles [k*UCT, +UCT) and fine tiles [k*UCT, +UCT) over all
 // H columns, so it publishes finished pre-activations R h (+ bias and
 // conditioning for the u and r gates) of those rows for the next step.
+// Mirror workgroups (NM, the dense batch-1 plan only; 0 in the fused and
+// block-sparse plans): mirror j draws c_t from the heads' partial logits as
+// every head does, evaluates the gates of the fine half itself and forms the
+// coarse rows' products with y_f, R[g*H + i][Hh + c] y_f[c] for i < Hh, of 12
+// coarse row tiles (192 rows: mirror j owns coarse row tiles 12j .. 12j + 11),
+// which it publishes straight to the heads.  The units then publish only the
+// coarse columns' part of the coarse rows (as soon as y_c is in) and the
+// whole fine rows, so y_f no longer has to reach the units and come back
+// before the next step's coarse gates.  Wave w of a mirror holds row tiles
+// 12j + 3(w % 4) .. +2 over the fine column tiles of half w / 4 (KT / 2 each).
 //
 // Matrices are stored bf16 as MFMA fragments (v_mfma_f32_16x16x32_bf16 with
 // the matrix as operand B): fragment (mt, kt) covers rows 16*mt .. 16*mt+15 and
@@ -78,12 +88,14 @@ WR_HD inline SmallLayout small_layout(int H) {
 #define WR_XALIGN 64      // exchange regions aligned to 64 words (512 B)
 #define WR_FRAG 1024      // bytes per MFMA fragment
 #define WR_MAXUCT 3       // coarse (and fine) row tiles per unit workgroup (waves 3, 7 stay free)
+#define WR_MTILES 12      // coarse row tiles per mirror workgroup (3 Hh / 16 = 12 NH of them)
 
 struct PersistPlan {
   int H, Hh, KT, KH;      // KT = Hh / 32 column tiles per half, KH = column tiles per head wave
   int RT, HR, KO, GU;     // head: row tiles (HR = 16 RT rows of O1 / O3), O2 / O4 column tiles
                           // (HR / 32), gate units per gate thread
   int NH, NU, UCT, NCT;   // heads, units, row tiles per unit and half, row tiles per half (3 Hh / 16)
+  int NM, mw_frags;       // mirrors (0: none) and their fragments per wave (3 row tiles x KT / 2)
   int NK;                 // slices of O1 / O3 rows (Hh / HR): the partial logits per half
   int SR, SL, NRC, NRF;   // block-sparse units: rows per unit, lanes per row, block slots per lane
                           // (coarse columns, fine columns); 0 for the dense kernel
@@ -94,36 +106,54 @@ struct PersistPlan {
   int hw_frags;           // head fragments per wave: O1[KH], O3[KH], O2[2 KO], O4[2 KO]
   int u_lds_w;            // unit LDS block: dense R tiles, or the block-sparse records
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (32-bit words)
+  int x_hf;               // with mirrors: the coarse rows' products with y_f [3 Hh]
   int x_ps;               // words between the partial-logit blocks of consecutive heads
-  int lds_h, lds_u, lds;  // LDS bytes
+  int x_gfs, x_pfs;       // with mirrors the fine rows' words and the fine partial logits are
+                          // double-buffered by step parity: words between the two buffers (0: one)
+  int lds_h, lds_u, lds_m, lds;  // LDS bytes
 };
+
+// Double-buffered words of step s (the fine rows' pre-activations and the fine
+// partial logits when mirrors read them too): buffer s mod 2, tagged with the
+// parity of the buffer's generation s / 2 + 1.  A writer of step s + 2 has
+// waited, through its own inputs, for every reader of step s (see the head
+// and mirror roles), and the generation bit tells step s from step s - 2.
+WR_HD inline int wr_dbuf(int64_t s, int stride) { return (int)(s & 1) * stride; }
+WR_HD inline uint32_t wr_dtag(int64_t s, int stride) {
+  return stride ? (uint32_t)(s >> 1) + 1u : (uint32_t)s + 1u;
+}
 
 WR_HD inline int wr_rup(int x, int m) { return (x + m - 1) / m * m; }
 
-// Block index of head j and the role of block b (head index, or unit index + NH, or -1 idle).
+// Block index of head j and the role of block b (head index, mirror index +
+// NH, unit index + NH + NM, or -1 idle).
 // Placement.  Blocks are dealt round-robin over the 8 XCDs (block b runs on
-// XCD b % 8), so head j sits at block 8 j + hx, and bit x of uxm admits units
-// on the other blocks of XCD x.  Unit blocks below b:
+// XCD b % 8), so lead block i (head i < NH, then mirror i - NH) sits at block
+// 8 i + hx, and bit x of uxm admits units on the other blocks of XCD x.  Unit
+// blocks below b:
 WR_HD inline int wr_units_below(const PersistPlan& P, int b) {
+  const int NL = P.NH + P.NM;
   int n = (b / 8) * __builtin_popcount(P.uxm & 255) + __builtin_popcount(P.uxm & ((1 << (b % 8)) - 1));
   if (P.uxm >> P.hx & 1) {
-    const int heads = (b + 7 - P.hx) / 8;   // blocks b' < b with b' % 8 == hx
-    n -= heads < P.NH ? heads : P.NH;
+    const int leads = (b + 7 - P.hx) / 8;   // blocks b' < b with b' % 8 == hx
+    n -= leads < NL ? leads : NL;
   }
   return n;
 }
-// The role of block b: head index, unit index + NH, or -1 (idle: returns at once).
+// The role of block b: head index, mirror index + NH, unit index + NH + NM, or
+// -1 (idle: returns at once).
 WR_HD inline int wr_role(const PersistPlan& P, int b) {
-  if (b % 8 == P.hx && b / 8 < P.NH) return b / 8;
+  const int NL = P.NH + P.NM;
+  if (b % 8 == P.hx && b / 8 < NL) return b / 8;
   if (!(P.uxm >> (b % 8) & 1)) return -1;
   const int k = wr_units_below(P, b);
-  return k < P.NU ? P.NH + k : -1;
+  return k < P.NU ? NL + k : -1;
 }
-// Set a placement and the smallest grid that holds every head and unit.
+// Set a placement and the smallest grid that holds every head, mirror and unit.
 WR_HD inline void wr_place(PersistPlan* P, int hx, int uxm) {
   P->hx = hx;
   P->uxm = uxm;
-  int g = 8 * (P->NH - 1) + hx + 1;
+  int g = 8 * (P->NH + P->NM - 1) + hx + 1;
   while (wr_units_below(*P, g) < P->NU) ++g;
   P->grid = g;
 }
@@ -144,6 +174,8 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->BH = P->BW = P->BR = P->u_wb = 0;
   P->NCT = 3 * P->Hh / 16;
   if (P->NH > 16 || P->Hh > WR_THREADS - 64) return false;   // the last wave draws, free of gate work
+  P->NM = P->NCT / WR_MTILES;                                 // = NH
+  P->mw_frags = 3 * (P->KT / 2);
   P->hw_frags = 2 * P->KH + 8;
   // head LDS: y_c and y_f operand images (KT fragments each), relu image (2),
   // first-layer partials [2][64], logit sums [2][256], logits [256],
@@ -158,18 +190,25 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   }
   if (!P->UCT) return false;
   P->NU = P->NCT / P->UCT;
+  // mirror LDS: y_f operand image (KT fragments), products of the two column
+  // halves [2][192], logits [256], misc [16], uniforms [2][64][2], targets [2][64]
+  P->lds_m = P->KT * WR_FRAG + 4 * (2 * 16 * WR_MTILES + 256 + 16 + 256 + 128);
   wr_place(P, 0, 255);
   int o = 0;
   auto take = [&](int n) { int r = o; o += wr_rup(n, WR_XALIGN); return r; };
   P->x_yc = take(P->Hh);
   P->x_yf = take(P->Hh);
   P->x_ga = take(3 * P->Hh);
-  P->x_gf = take(3 * P->Hh);
+  P->x_gfs = wr_rup(3 * P->Hh, WR_XALIGN);
+  P->x_gf = take(2 * P->x_gfs);
+  P->x_hf = take(3 * P->Hh);
   P->x_ps = 256;
   P->x_pc = take(P->NH * P->x_ps);
-  P->x_pf = take(P->NH * P->x_ps);
+  P->x_pfs = P->NH * P->x_ps;
+  P->x_pf = take(2 * P->x_pfs);
   P->x_words = o;
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
+  if (P->lds_m > P->lds) P->lds = P->lds_m;
   return P->lds <= 160 * 1024;
 }
 
@@ -180,6 +219,9 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
 // wave's class tile of O2 and of O4 over the head's KO column tiles.
 WR_HD inline bool fused_plan(int H, PersistPlan* P) {
   if (!persist_plan(H, P)) return false;
+  P->NM = P->mw_frags = P->lds_m = 0;             // no mirrors: single-buffered words
+  P->x_hf = P->x_gfs = P->x_pfs = 0;
+  wr_place(P, 0, 255);
   P->hw_frags = 2 * P->KH + 2 * P->KO;
   // head LDS: y_c and y_f operand images (KT fragments each), relu image (KO),
   // first-layer partials [2][64], misc [16], uniforms [2][64][8], targets [2][64][2]
@@ -250,6 +292,8 @@ WR_HD inline bool sparse_plan(int H, int SR, int BH, int BW, int NRC, int NRF, P
   P->UCT = 0;
   P->NCT = 3 * P->Hh / 16;
   P->NU = 3 * H / SR;
+  P->NM = P->mw_frags = P->lds_m = 0;             // no mirrors: single-buffered words
+  P->x_hf = P->x_gfs = P->x_pfs = 0;
   P->hw_frags = P->KH + 2 * P->KO;
   // head LDS: operand image (KT + KO fragments), first-layer partials
   // [KC][HR], logit sums [2][256], logits [256], then y [Hh] (GU = 1) or

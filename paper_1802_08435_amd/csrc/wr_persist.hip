@@ -21,6 +21,66 @@
 // and draw it runs beside.
 #include "wr_unit.h"
 
+// The draw wave of a head (or mirror) gathers the partial logits of all NK
+// slices alone: lane l reads classes 4 l .. 4 l + 3 of every slice with one
+// 16-byte load (a wave's load covers whole cache lines) and sums slices
+// [0, NHP), then [NHP, NK), then adds the two (the sums and order of the
+// two-thread gather, so every head and mirror draws the same class); the
+// logits stay in registers and no barrier separates gather and draw, while
+// the other waves go on to the next gate terms (measured at H = 896: 4.94 us
+// per step, against 5.13 with the two-thread gather and its barriers).
+template <int NK>
+__device__ __forceinline__ bool gather_partials(const PersistArgs& a, const xw* src, uint32_t tag, float4* z) {
+  constexpr int NHP = (NK + 1) / 2;
+  const int lane = threadIdx.x & 63;
+  __builtin_amdgcn_s_sleep(6);
+  const uint32_t bytes = (uint32_t)(NK * a.P.x_ps * 4), lo = 16u * lane, ps = (uint32_t)a.P.x_ps * 4u;
+  xw4 w[NK];
+  uint32_t pending = 0;
+  {
+    const __amdgpu_buffer_rsrc_t r = xrsrc(xopaque(src), bytes);
+#pragma unroll
+    for (int k = 0; k < NK; ++k) w[k] = xpeek4(r, k * ps + lo);
+  }
+#pragma unroll
+  for (int k = 0; k < NK; ++k)
+    if (!xok4(w[k], tag)) pending |= 1u << k;
+  if (pending) {
+    WaitBudget wb{wr_clock(), 0};
+    while (pending) {
+      if (!wait_ok(wb, a.err, a.limit, a.err)) {
+        *z = float4{0.0f, 0.0f, 0.0f, 0.0f};   // a valid draw follows; the step is abandoned after it
+        return false;
+      }
+      const __amdgpu_buffer_rsrc_t r = xrsrc(xopaque(src), bytes);
+      xw4 x[NK];
+#pragma unroll
+      for (int k = 0; k < NK; ++k)
+        if (pending >> k & 1u) x[k] = xpeek4(r, k * ps + lo);
+#pragma unroll
+      for (int k = 0; k < NK; ++k)
+        if ((pending >> k & 1u) && xok4(x[k], tag)) {
+          w[k] = x[k];
+          pending &= ~(1u << k);
+        }
+    }
+  }
+  float4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int k = 0; k < NK; ++k) {
+    float4& d = k < NHP ? s0 : s1;
+    d.x += xval(w[k].x);
+    d.y += xval(w[k].y);
+    d.z += xval(w[k].z);
+    d.w += xval(w[k].w);
+  }
+  z->x = s0.x + s1.x;
+  z->y = s0.y + s1.y;
+  z->z = s0.z + s1.z;
+  z->w = s0.w + s1.w;
+  return true;
+}
+
 // ------------------------------------------------------------------ head role
 // A head owns a slice of HR = 16 RT rows of O1 / O3 (RT row tiles; the 8
 // waves split them into RT row tiles x KC = 8 / RT column-tile chunks of KH
@@ -41,7 +101,10 @@
 // All 8 waves run the MFMA layers and gather the partial logits (two threads
 // per class); the gate threads of this head's slice of units publish it for
 // the unit workgroups.
-template <int KH, int RT, int GU, bool SPLIT>
+// MR (mirrors, dense GU = 1 only): a coarse gate's pre-activation is the
+// units' coarse-column word plus the mirrors' fine-column word, and the fine
+// rows' words and the fine partial logits are double-buffered by step parity.
+template <int KH, int RT, int GU, bool SPLIT, bool MR = false>
 __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned char* lds) {
   constexpr int KC = 8 / RT;                       // column-tile chunks
   constexpr int KT = KH * KC;                      // column tiles per half
@@ -149,22 +212,28 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   xw* YF = a.xc + P.x_yf;
   xw* PCo = a.xc + P.x_pc + (size_t)jk * P.x_ps;
   xw* PFo = a.xc + P.x_pf + (size_t)jk * P.x_ps;
+  const xw* HF = a.xc + P.x_hf;
   const xw* PC = a.xc + P.x_pc;
   const xw* PF = a.xc + P.x_pf;
   const int rt = wave % RT, kc = wave / RT;        // first layer: row tile, column-tile chunk
-  // GU = 1: pre-activation words of this thread's units, loaded ahead
-  xw pc[3] = {0, 0, 0}, pf[3] = {0, 0, 0};
+  // GU = 1: pre-activation words of this thread's units, loaded ahead (MR:
+  // the units' three, then the mirrors' three of the coarse half)
+  constexpr int NCW = MR ? 6 : 3;
+  xw pc[NCW] = {}, pf[3] = {0, 0, 0};
   float cbe_c = 0.0f, cbe_f = 0.0f;
   auto prefetch_coarse = [&](int64_t n) {
     if (!WIDE && gate && coarse) {
       pc[0] = xpeek(GA + u); pc[1] = xpeek(GA + Hh + u); pc[2] = xpeek(GA + 2 * Hh + u);
+      if (MR) { pc[3] = xpeek(HF + u); pc[4] = xpeek(HF + Hh + u); pc[5] = xpeek(HF + 2 * Hh + u); }
       cbe_c = cb_row(a, n)[2 * H + u];
     }
   };
-  auto prefetch_fine = [&](int64_t n) {
+  // the fine rows' words of launch step t (its buffer with MR)
+  auto prefetch_fine = [&](int64_t t) {
     if (!WIDE && gate && fine) {
-      pf[0] = xpeek(GF + u); pf[1] = xpeek(GF + Hh + u); pf[2] = xpeek(GF + 2 * Hh + u);
-      cbe_f = cb_row(a, n)[2 * H + Hh + u];
+      const xw* G = GF + wr_dbuf(t, P.x_gfs);
+      pf[0] = xpeek(G + u); pf[1] = xpeek(G + Hh + u); pf[2] = xpeek(G + 2 * Hh + u);
+      cbe_f = cb_row(a, a.t0 + t)[2 * H + Hh + u];
     }
   };
   // first layer on the 8 waves -> relu -> operand image of the second layer
@@ -221,61 +290,8 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (!sum_parts<NHP>(src, P.x_ps, hh ? NHP : 0, hh ? NK : NHP, v, tag, &s, a)) misc[0] = 1;
     else (hh ? zs2 : zs)[v] = s;
   };
-  // Without SPLIT the draw wave gathers alone: lane l reads classes 4 l ..
-  // 4 l + 3 of every slice with one 16-byte load (a wave's load covers whole
-  // cache lines) and sums slices [0, NHP), then [NHP, NK), then adds the two
-  // (the sums and order of the two-thread gather, so every head draws the
-  // same class); the logits stay in registers and no barrier separates
-  // gather and draw, while waves 0-6 go on to the next gate terms (measured
-  // at H = 896: 4.94 us per step, against 5.13 with the two-thread gather
-  // and its barriers).
   auto gather_wave = [&](const xw* src, uint32_t tag, float4* z) -> bool {
-    __builtin_amdgcn_s_sleep(6);
-    const uint32_t bytes = (uint32_t)(NK * P.x_ps * 4), lo = 16u * lane, ps = (uint32_t)P.x_ps * 4u;
-    xw4 w[NK];
-    uint32_t pending = 0;
-    {
-      const __amdgpu_buffer_rsrc_t r = xrsrc(xopaque(src), bytes);
-#pragma unroll
-      for (int k = 0; k < NK; ++k) w[k] = xpeek4(r, k * ps + lo);
-    }
-#pragma unroll
-    for (int k = 0; k < NK; ++k)
-      if (!xok4(w[k], tag)) pending |= 1u << k;
-    if (pending) {
-      WaitBudget wb{wr_clock(), 0};
-      while (pending) {
-        if (!wait_ok(wb, a.err, a.limit, a.err)) {
-          *z = float4{0.0f, 0.0f, 0.0f, 0.0f};   // a valid draw follows; the step is abandoned after it
-          return false;
-        }
-        const __amdgpu_buffer_rsrc_t r = xrsrc(xopaque(src), bytes);
-        xw4 x[NK];
-#pragma unroll
-        for (int k = 0; k < NK; ++k)
-          if (pending >> k & 1u) x[k] = xpeek4(r, k * ps + lo);
-#pragma unroll
-        for (int k = 0; k < NK; ++k)
-          if ((pending >> k & 1u) && xok4(x[k], tag)) {
-            w[k] = x[k];
-            pending &= ~(1u << k);
-          }
-      }
-    }
-    float4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int k = 0; k < NK; ++k) {
-      float4& d = k < NHP ? s0 : s1;
-      d.x += xval(w[k].x);
-      d.y += xval(w[k].y);
-      d.z += xval(w[k].z);
-      d.w += xval(w[k].w);
-    }
-    z->x = s0.x + s1.x;
-    z->y = s0.y + s1.y;
-    z->z = s0.z + s1.z;
-    z->w = s0.w + s1.w;
-    return true;
+    return gather_partials<NK>(a, src, tag, z);
   };
   // Philox blocks of steps t .. t+63 into batch buffer b, one step per lane of
   // the draw wave: the 64-bit multiplies cost the same for 64 lanes as for one
@@ -291,7 +307,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   if (wave == DW) fill_batch(0, 0);
   __syncthreads();
   prefetch_coarse(a.t0);
-  prefetch_fine(a.t0);
+  prefetch_fine(0);
   const bool trw = j == 0 && tid == WR_THREADS - 64;       // tracing thread (draw wave)
   // wide: the units publish a step's coarse and fine words together, so both
   // are read at once (one round trip) with the conditioning of the e gates:
@@ -355,18 +371,23 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     // end of the fine gather)
     __builtin_amdgcn_s_sleep(8);
     prefetch_coarse(n);
-    const xw* ps[3] = {GA + u, GA + Hh + u, GA + 2 * Hh + u};
-    float v[3];
-    if (!poll_pref<3>(ps, pc, tag, v, a)) {
+    const xw* ps[6] = {GA + u, GA + Hh + u, GA + 2 * Hh + u, HF + u, HF + Hh + u, HF + 2 * Hh + u};
+    float v[NCW];
+    if (!poll_pref<NCW>(ps, pc, tag, v, a)) {
       misc[0] = 1;
       return;
+    }
+    if (MR) {   // the units' coarse-column part plus the mirrors' fine-column part
+      v[0] = v[0] + v[3];
+      v[1] = v[1] + v[4];
+      v[2] = v[2] + v[5];
     }
     cu = v[0] + ic[0][0] * x0;
     cr = v[1] + ic[1][0] * x0;
     ce = v[2];
     cie = ic[2][0] * x0;
   };
-  auto fine_pre = [&](uint32_t tag, float x0, float x1, int64_t n) {
+  auto fine_pre = [&](int64_t t, float x0, float x1) {
     if (WIDE) {   // from the words read with the coarse ones (LDS only)
       if (!fine) return;
       for (int un = tid; un < Hh; un += 448) {
@@ -380,9 +401,10 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       return;
     }
     if (!gate || !fine) return;
-    const xw* ps[3] = {GF + u, GF + Hh + u, GF + 2 * Hh + u};
+    const xw* G = GF + wr_dbuf(t, P.x_gfs);
+    const xw* ps[3] = {G + u, G + Hh + u, G + 2 * Hh + u};
     float v[3];
-    if (!poll_pref<3>(ps, pf, tag, v, a)) {
+    if (!poll_pref<3>(ps, pf, wr_dtag(t, P.x_gfs), v, a)) {
       misc[0] = 1;
       return;
     }
@@ -450,7 +472,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       gather_logits(PC, tag);
       if (trw) trace_at(a, t, 15);
     }
-    if (t > 0) prefetch_fine(n);
+    if (t > 0) prefetch_fine(t);
     if (SPLIT) {
       __syncthreads();
       if (misc[0]) return;
@@ -479,7 +501,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
         }
       }
     } else {
-      fine_pre(tag, fscale(misc[2]), fscale(misc[3]), n);
+      fine_pre(t, fscale(misc[2]), fscale(misc[3]));
     }
     __syncthreads();
     if (misc[0]) return;
@@ -504,18 +526,18 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     if (fine) {
       if (SPLIT) {
         first_layer(W1, imf, b3r);
-        second_layer(W2, PFo, tag);
+        second_layer(W2, PFo + wr_dbuf(t, P.x_pfs), wr_dtag(t, P.x_pfs));
       } else {
         first_layer(W3, imf, b3r);
         if (trw) trace_at(a, t, 7);
-        second_layer(W4, PFo, tag);
+        second_layer(W4, PFo + wr_dbuf(t, P.x_pfs), wr_dtag(t, P.x_pfs));
         if (trw) trace_at(a, t, 8);
       }
     }
     if (j == NH - 1 && tid == WR_THREADS - 64) trace_at(a, t, 14);
     // (7) fine logits of all heads
     if (SPLIT) {
-      gather_logits(PF, tag);
+      gather_logits(PF + wr_dbuf(t, P.x_pfs), wr_dtag(t, P.x_pfs));
       if (trw) trace_at(a, t, 17);
       __syncthreads();
       if (misc[0]) return;
@@ -530,7 +552,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
         f = draw_wave(zs, zs2, b4l, uni[bs].y, forced, zk, a.nll_out ? &lse : nullptr);
       } else {
         float4 z;
-        if (!gather_wave(PF, tag, &z)) misc[0] = 1;
+        if (!gather_wave(PF + wr_dbuf(t, P.x_pfs), wr_dtag(t, P.x_pfs), &z)) misc[0] = 1;
         if (trw) trace_at(a, t, 17);
         f = draw_z(z, b4l, uni[bs].y, forced, zk, a.nll_out ? &lse : nullptr);
       }
@@ -571,13 +593,169 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
   }
 }
 
+// ------------------------------------------------------------------ mirror role
+// Mirror j draws c_t as every head does (the same partial logits summed in
+// the same order, the same uniform or target), evaluates the fine gates of
+// every unit (Eq. 2, with c_t) with a head's arithmetic, and forms the
+// products of the coarse rows with the new y_f for the next step: coarse row
+// tiles 12 j .. 12 j + 11 over the fine columns (wave w: row tiles
+// 3 (w % 4) .. +2 over the column tiles of half w / 4, the halves added in
+// LDS).  The heads add them to the units' coarse-column words.  y_f enters
+// the products as the exchange delivers values (lowest bit cleared), so the
+// teacher-forced scoring recurrence forms the same sums.  The mirror then
+// draws f_t as the heads do, for the next step's input terms.
+// Exchange order: the words of step t + 1 are published after c_t, and a head
+// publishes the partials of c_{t+1} only after reading them, so one buffer
+// holds them.  A mirror reads the fine partials of step t after publishing
+// those words: a head publishes fine partials of step t + 2 only after the
+// mirrors' words of step t + 2, which follow f_t, so two buffers by step
+// parity suffice; the fine rows' words likewise.
+template <int KH>
+__device__ __forceinline__ void mirror_role(const PersistArgs& a, int j, unsigned char* lds) {
+  constexpr int KT = 2 * KH;                       // column tiles per half
+  constexpr int MK = KT / 2;                       // column tiles per wave (half of the fine columns)
+  constexpr int NK = KH;                           // slices of the partial logits (Hh / 64 heads)
+  constexpr int DW = 7;                            // the draw wave
+  constexpr int Hh = 32 * KT;
+  constexpr int MRW = 16 * WR_MTILES;              // rows of a mirror
+  const PersistPlan& P = a.P;
+  const int H = P.H;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  unsigned char* imf = lds;                        // [KT] operand image of y_f
+  float* part = (float*)(imf + KT * WR_FRAG);      // [2][MRW] products of the two column halves
+  float* zk = part + 2 * MRW;                      // [256] logits of the last draw
+  int* misc = (int*)(zk + 256);                    // [0] abort [1] c_t [2] c_prev [3] f_prev
+  float2* uni = (float2*)(misc + 16);              // [2][64] (u_c, u_f) of a batch of 64 steps
+  int* tgt = (int*)(uni + 128);                    // [2][64] teacher-forcing targets of the batch
+  for (int i = tid; i < KT * WR_FRAG / 16; i += WR_THREADS) ((uint4*)imf)[i] = uint4{0, 0, 0, 0};
+  const int rq = wave & 3, kh = wave >> 2;         // row tiles 3 rq .. 3 rq + 2, column half kh
+  bf16x8 W[3 * MK];
+  {
+    const uint4* src = a.mw + ((size_t)(j * 8 + wave) * P.mw_frags) * 64 + lane;
+#pragma unroll
+    for (int i = 0; i < 3 * MK; ++i) W[i] = __builtin_bit_cast(bf16x8, src[(size_t)i * 64]);
+  }
+  // gate thread u < Hh: fine unit Hh + u, its I* coefficients (c_{t-1}, f_{t-1}, c_t) and state
+  const bool gate = tid < Hh;
+  const int u = tid;
+  float ifn[3][3];
+  float hf = 0.0f;
+  if (gate) {
+#pragma unroll
+    for (int g = 0; g < 3; ++g)
+#pragma unroll
+      for (int q = 0; q < 3; ++q) ifn[g][q] = a.Iw[3 * (g * H + Hh + u) + q];
+    if (a.h_in) hf = a.h_in[Hh + u];
+  }
+  const float4 b2l = wave == DW ? *(const float4*)(a.b2 + 4 * lane) : float4{0, 0, 0, 0};
+  const float4 b4l = wave == DW ? *(const float4*)(a.b4 + 4 * lane) : float4{0, 0, 0, 0};
+  if (tid == 0) {
+    misc[0] = 0;
+    misc[2] = a.c_in ? a.c_in[0] : 128;
+    misc[3] = a.f_in ? a.f_in[0] : 0;
+  }
+  const xw* GF = a.xc + P.x_gf;
+  const xw* PC = a.xc + P.x_pc;
+  const xw* PF = a.xc + P.x_pf;
+  xw* HF = a.xc + P.x_hf + (size_t)MRW * j;
+  // Philox blocks of steps t .. t+63 into batch buffer b (as the heads draw them)
+  auto fill_batch = [&](int64_t t, int b) {
+    const int64_t s = t + lane;
+    if (s < a.T) {
+      float uc, uf;
+      wr_uniforms(a.seed, a.stream_id, (uint64_t)(a.t0 + s), &uc, &uf);
+      uni[b * 64 + lane] = float2{uc, uf};
+      tgt[b * 64 + lane] = a.target ? a.target[s] : 0;
+    }
+  };
+  if (wave == DW) fill_batch(0, 0);
+  __syncthreads();
+  if (gate) aput(imf + (u >> 5) * WR_FRAG, u & 31, xround(hf));
+  // the coarse rows' products with y_f for step s, published for the heads
+  auto products = [&](int64_t s) {
+    f32x4 acc[3];
+#pragma unroll
+    for (int r = 0; r < 3; ++r) acc[r] = f32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < MK; ++i) {
+      const bf16x8 x = afrag(imf, kh * MK + i);
+#pragma unroll
+      for (int r = 0; r < 3; ++r) acc[r] = mfma(x, W[r * MK + i], acc[r]);
+    }
+    if (lane < 16) {
+#pragma unroll
+      for (int r = 0; r < 3; ++r) part[kh * MRW + 16 * (3 * rq + r) + lane] = mfma_row(acc[r]);
+    }
+    __syncthreads();
+    if (tid < MRW) xpub(HF + tid, (uint32_t)s + 1u, part[tid] + part[MRW + tid]);
+  };
+  __builtin_amdgcn_s_waitcnt(0);   // prologue loads in before the loop (see head_role)
+  __syncthreads();
+  products(0);
+  float fu = 0.0f, fr = 0.0f, fe = 0.0f, fie = 0.0f, cbe = 0.0f;
+  for (int64_t t = 0; t < a.T; ++t) {
+    const uint32_t tag = (uint32_t)(t + 1);
+    const int bs = (int)((t >> 6) & 1) * 64 + (int)(t & 63);
+    if (wave == DW && (t & 63) == 0) fill_batch(t + 64, (int)(((t >> 6) + 1) & 1));
+    // (1) c_t on the draw wave; the fine rows' words of step t on the gate threads
+    if (wave == DW) {
+      float4 z;
+      if (!gather_partials<NK>(a, PC, tag, &z)) misc[0] = 1;
+      const int c = draw_z(z, b2l, uni[bs].x, a.target ? (tgt[bs] >> 8) : -1, zk, nullptr);
+      if (lane == 0) misc[1] = c;
+    } else if (gate) {
+      const xw* G = GF + wr_dbuf(t, P.x_gfs);
+      const xw* ps[3] = {G + u, G + Hh + u, G + 2 * Hh + u};
+      const xw w0[3] = {xpeek(ps[0]), xpeek(ps[1]), xpeek(ps[2])};
+      cbe = cb_row(a, a.t0 + t)[2 * H + Hh + u];
+      float v[3];
+      if (!poll_pref<3>(ps, w0, wr_dtag(t, P.x_gfs), v, a)) {
+        misc[0] = 1;
+      } else {
+        const float x0 = fscale(misc[2]), x1 = fscale(misc[3]);
+        fu = v[0] + __builtin_fmaf(ifn[0][1], x1, ifn[0][0] * x0);
+        fr = v[1] + __builtin_fmaf(ifn[1][1], x1, ifn[1][0] * x0);
+        fe = v[2];
+        fie = __builtin_fmaf(ifn[2][1], x1, ifn[2][0] * x0);
+      }
+    }
+    __syncthreads();
+    if (misc[0]) return;
+    // (2) the fine gates with c_t, as a head evaluates them
+    if (gate) {
+      const float x2 = fscale(misc[1]);
+      const float uu = fsig(__builtin_fmaf(ifn[0][2], x2, fu)), rr = fsig(__builtin_fmaf(ifn[1][2], x2, fr));
+      const float e = ftanh(__builtin_fmaf(rr, fe, __builtin_fmaf(ifn[2][2], x2, fie) + cbe));
+      hf = __builtin_fmaf(uu, hf, (1.0f - uu) * e);
+      aput(imf + (u >> 5) * WR_FRAG, u & 31, xround(hf));
+    }
+    __syncthreads();
+    // (3) the coarse rows' products with y_f for step t + 1
+    if (t + 1 < a.T) products(t + 1);
+    if (j == 0 && tid == 0) trace_at(a, t, 23);
+    // (4) f_t on the draw wave
+    if (wave == DW) {
+      float4 z;
+      if (!gather_partials<NK>(a, PF + wr_dbuf(t, P.x_pfs), wr_dtag(t, P.x_pfs), &z)) misc[0] = 1;
+      const int f = draw_z(z, b4l, uni[bs].y, a.target ? (tgt[bs] & 255) : -1, zk, nullptr);
+      if (lane == 0) {
+        misc[2] = misc[1];
+        misc[3] = f;
+      }
+    }
+    __syncthreads();
+    if (misc[0]) return;
+  }
+}
+
 template <int KH>
 __global__ __launch_bounds__(WR_THREADS, 1) void wr_persist_kernel(PersistArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int r = wr_role(a.P, blockIdx.x);
   if (r < 0) return;
-  if (r < a.P.NH) head_role<KH, 4, 1, false>(a, r, lds);
-  else unit_role<KH, false>(a, r - a.P.NH, lds);
+  if (r < a.P.NH) head_role<KH, 4, 1, false, true>(a, r, lds);
+  else if (r < a.P.NH + a.P.NM) mirror_role<KH>(a, r - a.P.NH, lds);
+  else unit_role<KH, false, true>(a, r - a.P.NH - a.P.NM, lds);
 }
 
 // ------------------------------------------------------------ block-sparse unit role

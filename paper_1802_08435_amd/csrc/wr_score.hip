@@ -9,9 +9,13 @@
 // bytes and publish the new slice of h; waves 3-7 gather the next h from every
 // workgroup into the operand image (an all-gather: one hop per step).  The
 // products and the gate arithmetic are the sampling kernel's operation for
-// operation (even and odd column tiles in two accumulation chains, values as
-// the exchange delivers them, lowest bit cleared), so a scored trajectory
-// reproduces the sampler's state bit for bit.  The output layers run
+// operation, so a scored trajectory reproduces the sampler's state bit for
+// bit: a fine row's R h is one pass over all columns (even and odd column
+// tiles in two accumulation chains), a coarse row's is the sampling units'
+// coarse-column part (two chains, + bias and conditioning) plus the sampling
+// mirrors' fine-column part (one chain per half of the fine columns, the
+// halves added), each rounded as the exchange delivers it (lowest bit
+// cleared).  The output layers run
 // afterwards over all steps at once (wr_cnn_gemm), and the NLL per step in
 // wr_score_nll.
 //
@@ -28,6 +32,36 @@ __device__ __forceinline__ const float* score_cb(const ScoreArgs& a, int64_t n) 
   int64_t fr = n / a.frame_len;
   if (fr >= a.n_cb) fr = a.n_cb - 1;
   return a.cb + (size_t)fr * 3 * a.H;
+}
+
+// The products of a gate wave's 16 rows with h (operand image img, fragments
+// W over all KT2 column tiles).  Fine rows: even and odd column tiles in
+// acc0 and acc1 (the sampling units' fine rows).  Coarse rows: the coarse
+// column tiles in acc0 and acc1 (the units' coarse-column part), and the two
+// halves of the fine column tiles in one chain each, accA and accB (the
+// mirrors' waves, in column order).
+template <int KT2>
+__device__ __forceinline__ void score_products(const unsigned char* img, const bf16x8* W, bool fine, f32x4& acc0,
+                                               f32x4& acc1, f32x4& accA, f32x4& accB) {
+  constexpr int KT = KT2 / 2, MK = KT / 2;
+  if (fine) {
+#pragma unroll
+    for (int i = 0; i < KT2; i += 2) {
+      acc0 = mfma(afrag(img, i), W[i], acc0);
+      if (i + 1 < KT2) acc1 = mfma(afrag(img, i + 1), W[i + 1], acc1);
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < KT; i += 2) {
+    acc0 = mfma(afrag(img, i), W[i], acc0);
+    if (i + 1 < KT) acc1 = mfma(afrag(img, i + 1), W[i + 1], acc1);
+  }
+#pragma unroll
+  for (int i = 0; i < MK; ++i) {
+    accA = mfma(afrag(img, KT + i), W[KT + i], accA);
+    accB = mfma(afrag(img, KT + MK + i), W[KT + MK + i], accB);
+  }
 }
 
 }  // namespace
@@ -101,17 +135,13 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_score_kernel(ScoreArgs a) {
       if (misc[0]) return;
     }
     const int64_t n = a.t0 + s;
-    if (wave < 3) {   // gate `wave`: rows wave H + 16 k .. + 15 of R h, as the sampling units form them
-      f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-#pragma unroll
-      for (int i = 0; i < KT2; i += 2) {
-        acc0 = mfma(afrag(img, i), W[i], acc0);
-        if (i + 1 < KT2) acc1 = mfma(afrag(img, i + 1), W[i + 1], acc1);
-      }
+    if (wave < 3) {   // gate `wave`: rows wave H + 16 k .. + 15 of R h, as the sampling kernel forms them
+      f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0}, accA = {0, 0, 0, 0}, accB = {0, 0, 0, 0};
+      score_products<KT2>(img, W, fine, acc0, acc1, accA, accB);
       if (lane < 16) {
         float v = mfma_row(acc0) + mfma_row(acc1);
         if (wave < 2) v += score_cb(a, n)[wave * H + 16 * k + lane];   // bias + conditioning of u and r
-        pre[wave * 16 + lane] = xround(v);
+        pre[wave * 16 + lane] = fine ? xround(v) : xround(v) + xround(mfma_row(accA) + mfma_row(accB));
       }
     }
     __syncthreads();
@@ -238,12 +268,8 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_score_multi(ScoreArgs a) {
     int64_t fr = n / a.frame_len;
     if (fr >= a.n_cb) fr = a.n_cb - 1;
     if (wave < 3) {   // gate `wave`: rows wave H + 16 k .. + 15 of R h for every vector
-      f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-#pragma unroll
-      for (int i = 0; i < KT2; i += 2) {
-        acc0 = mfma(afrag(img, i), W[i], acc0);
-        if (i + 1 < KT2) acc1 = mfma(afrag(img, i + 1), W[i + 1], acc1);
-      }
+      f32x4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0}, accA = {0, 0, 0, 0}, accB = {0, 0, 0, 0};
+      score_products<KT2>(img, W, fine, acc0, acc1, accA, accB);
       const int b0 = 2 * (lane >> 4), row = lane & 15;
       if (b0 < nv) {
         float v0 = mfma_row(acc0) + mfma_row(acc1), v1 = mfma_row_hi(acc0) + mfma_row_hi(acc1);
@@ -251,8 +277,10 @@ __global__ __launch_bounds__(WR_THREADS, 1) void wr_score_multi(ScoreArgs a) {
           v0 += a.cb[((size_t)b0 * a.n_cb + fr) * 3 * H + wave * H + 16 * k + row];
           if (b0 + 1 < nv) v1 += a.cb[((size_t)(b0 + 1) * a.n_cb + fr) * 3 * H + wave * H + 16 * k + row];
         }
-        pre[(wave * LV + b0) * 16 + row] = xround(v0);
-        if (b0 + 1 < nv) pre[(wave * LV + b0 + 1) * 16 + row] = xround(v1);
+        const float f0 = fine ? 0.0f : xround(mfma_row(accA) + mfma_row(accB));
+        const float f1 = fine ? 0.0f : xround(mfma_row_hi(accA) + mfma_row_hi(accB));
+        pre[(wave * LV + b0) * 16 + row] = fine ? xround(v0) : xround(v0) + f0;
+        if (b0 + 1 < nv) pre[(wave * LV + b0 + 1) * 16 + row] = fine ? xround(v1) : xround(v1) + f1;
       }
     }
     __syncthreads();

@@ -30,7 +30,11 @@ __device__ __forceinline__ int64_t fused_sample(const PersistArgs& a, int s, int
 // k*UCT + q: coarse columns from LDS (used when y_c arrives), fine columns from
 // VGPRs (used when y_f arrives, so the part on the way to the heads reads no
 // weights from LDS); each publishes its 16 pre-activations once y_f is in.
-template <int KH, bool FUSED>
+// MR (mirrors form the coarse rows' fine-column products): a coarse wave
+// publishes its coarse columns' part (with bias + conditioning) as soon as
+// y_c is in and holds no fine columns; the fine rows' words go to the buffer
+// of their step's parity (wr_dbuf), since mirrors read them too.
+template <int KH, bool FUSED, bool MR = false>
 __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned char* lds) {
   constexpr int KT = 2 * KH;
   const PersistPlan& P = a.P;
@@ -41,6 +45,7 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   unsigned char* img = lds + P.u_lds_w;                          // [2KT] operand image of h
   int* misc = (int*)(img + 2 * KT * WR_FRAG);
   const bool cw = wave < UCT, fw = wave >= 4 && wave - 4 < UCT;
+  const bool fx = MR ? fw : (cw || fw);                           // waves with fine-column products
   const int q = cw ? wave : wave - 4;
   // this wave's tile: gate g, units i0 .. i0+15 of its half
   const int tile = k * UCT + q;
@@ -54,7 +59,7 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
     if (tid == 0) misc[0] = 0;
   }
   bf16x8 WR[KT];
-  if (cw || fw) {
+  if (fx) {
     const uint4* src = a.ur + ((size_t)(fw ? P.NU * UCT + tile : tile) * KT) * 64 + lane;
 #pragma unroll
     for (int i = 0; i < KT; ++i) WR[i] = __builtin_bit_cast(bf16x8, src[(size_t)i * 64]);
@@ -79,19 +84,28 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
       }
     }
   };
-  // columns [KT, 2KT): fine inputs; then publish with `tag`
-  auto phase_f = [&](uint32_t tag, float cbv) {
-    if (cw || fw) {
+  // MR: a coarse wave's words of step s (its coarse columns' part) once y_c is in
+  auto publish_c = [&](int64_t s, float cbv) {
+    if (MR && cw && lane < 16) {
+      float v = mfma_row(acc0) + mfma_row(acc1);
+      if (g < 2) v += cbv;                      // bias + conditioning of the u and r gates
+      xpub(dst, (uint32_t)s + 1u, v);
+    }
+  };
+  // columns [KT, 2KT): fine inputs; then publish the words of step s
+  auto phase_f = [&](int64_t s, float cbv) {
+    if (fx) {
 #pragma unroll
       for (int i = 0; i < KT; i += 2) {
         acc0 = mfma(afrag(img, KT + i), WR[i], acc0);
         if (i + 1 < KT) acc1 = mfma(afrag(img, KT + i + 1), WR[i + 1], acc1);
       }
     }
-    if ((cw || fw) && lane < 16) {
+    if (fx && lane < 16) {
       float v = mfma_row(acc0) + mfma_row(acc1);
       if (g < 2) v += cbv;                      // bias + conditioning of the u and r gates
-      xpub(dst, tag, v);
+      if (MR) xpub(dst + wr_dbuf(s, P.x_gfs), wr_dtag(s, P.x_gfs), v);
+      else xpub(dst, (uint32_t)s + 1u, v);
     }
   };
   __builtin_amdgcn_s_waitcnt(0);   // weights and operands are in before the loop (see head_role)
@@ -101,7 +115,11 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
   // quarter of sub-tensor s follows the sample its sub-tensor makes
   const int rs = (i0 + (lane & 15)) / (Hh / 2);
   auto cbs = [&](int64_t t) { return FUSED ? fused_sample(a, rs, t) : a.t0 + t; };
-  phase_f(1u, (cw || fw) && g < 2 ? cb_row(a, cbs(0))[row] : 0.0f);
+  {
+    const float cb0 = (cw || fw) && g < 2 ? cb_row(a, cbs(0))[row] : 0.0f;
+    publish_c(0, cb0);
+    phase_f(0, cb0);
+  }
   const xw* YC = a.xc + P.x_yc;
   const xw* YF = a.xc + P.x_yf;
   // Wait for a half of h.  Waves 3 and 7 own no row tile and never store, so
@@ -151,11 +169,12 @@ __device__ __forceinline__ void unit_role(const PersistArgs& a, int k, unsigned 
     if (misc[0]) return;
     if (k == 0 && tid == 0) trace_at(a, t, 20);
     phase_c();
+    publish_c(t + 1, cbv);
     if (k == 0 && tid == 0) trace_at(a, t, 21);
     gather_half(YF, tag, KT, false);   // y_f gates the next coarse step: no flag phase
     if (misc[0]) return;
     if (k == 0 && tid == 0) trace_at(a, t + 1, 11);
-    phase_f(tag + 1, cbv);
+    phase_f(t + 1, cbv);
     if (k == 0 && tid == 0) trace_at(a, t + 1, 12);
   }
 }
