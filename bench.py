@@ -177,6 +177,13 @@ PHASES["fused"] = [(1, "coarse gates (last f of both sub-tensors) done, own y_c 
                    (18, "4 fine nibbles drawn (draw wave)"), (10, "next step's coarse gate words received (end of step)")]
 
 
+# Stamps of other workgroups of the same step (µs from head 0's step start),
+# reported beside the chain above.
+SIDE = {"persistent": [(23, "mirror 0: its coarse rows' products with y_f published"),
+                       (11, "unit 0: y_f in, fine rows' products started"),
+                       (12, "unit 0: fine rows' words of the next step published")]}
+
+
 def phases(m, w, path: str, S: int, feat, n_steps: int) -> dict:
     """Median per-phase timestamps of one traced launch of n_steps steps (the
     first and last eighth left out)."""
@@ -201,7 +208,14 @@ def phases(m, w, path: str, S: int, feat, n_steps: int) -> dict:
         t = float(np.median(rel[:, slot]))
         out.append({"slot": slot, "phase": name, "end_ns": round(t), "took_ns": round(t - prev)})
         prev = t
-    return {"phases": out, "step_ns_median": round(float(np.median(step_ns))),
+    side = []
+    for slot, name in SIDE.get(path, []):
+        if (tr[:, slot] == 0).any():
+            continue
+        # unit stamps 11 and 12 are recorded under the step they serve (t + 1)
+        col = rel[1:, slot] + (tr[1:, 0] - tr[:-1, 0]) * 10.0 if slot in (11, 12) else rel[:, slot]
+        side.append({"slot": slot, "event": name, "at_ns": round(float(np.median(col)))})
+    return {"phases": out, "side": side, "step_ns_median": round(float(np.median(step_ns))),
             "step_ns_p10": round(float(np.percentile(step_ns, 10))),
             "step_ns_p90": round(float(np.percentile(step_ns, 90))), "traced_steps": int(len(step_ns))}
 
