@@ -43,21 +43,34 @@ KERNEL_OF = {"persistent": "wr_persist_kernel", "block-sparse": "wr_sparse_kerne
              "single-workgroup": "wr_small_kernel", "concurrent": "wr_persist_kernel", "fused": "wr_fused_kernel"}
 
 
-def kernel_source_digest() -> str:
-    """Digest of every kernel and host source of the library (any change voids old counters)."""
+# source file of each kernel (the digest covers it and the headers it includes)
+KERNEL_SOURCE = {"wr_persist_kernel": "wr_persist.hip", "wr_sparse_kernel": "wr_persist.hip",
+                 "wr_fused_kernel": "wr_fused.hip", "wr_batch_kernel": "wr_batch.hip", "wr_small_kernel": "wr_small.hip"}
+
+
+def kernel_source_digest(kernel: str) -> str:
+    """Digest of the device sources a kernel is compiled from: its .hip file and every header it
+    includes, directly or not (any change voids the counters taken on it)."""
     import hashlib
-    h = hashlib.sha256()
+    import re
     d = os.path.join(ROOT, "paper_1802_08435_amd", "csrc")
-    for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".h")):
-            with open(os.path.join(d, f), "rb") as fh:
-                h.update(f.encode() + fh.read())
+    todo, seen = [KERNEL_SOURCE[kernel]], set()
+    while todo:
+        f = todo.pop()
+        if f in seen or not os.path.exists(os.path.join(d, f)):
+            continue
+        seen.add(f)
+        todo += re.findall(r'#include "([^"]+)"', open(os.path.join(d, f)).read())
+    h = hashlib.sha256()
+    for f in sorted(seen):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per call (its launches of the kernel) from the committed rocprofv3 --pmc summary of
-    this kernel and workload, or None when the library sources changed since the counters were taken."""
+    this kernel and workload, or None when the kernel's sources changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -66,7 +79,7 @@ def measured_traffic(kernel: str, workload: str):
     if i < 0:
         return None
     d = json.loads(text[i + 7:text.index("```", i + 7)])
-    if d.get("kernel_source_sha256_16") != kernel_source_digest():
+    if d.get("kernel_source_sha256_16") != kernel_source_digest(kernel):
         return None
     return (d["fetch_bytes_per_launch"] + d["write_bytes_per_launch"]) * d.get("launches_per_call", 1)
 
