@@ -53,16 +53,12 @@ __device__ __forceinline__ bool gather_partials(const PersistArgs& a, const xw* 
         return false;
       }
       const __amdgpu_buffer_rsrc_t r = xrsrc(xopaque(src), bytes);
-      xw4 x[NK];
 #pragma unroll
       for (int k = 0; k < NK; ++k)
-        if (pending >> k & 1u) x[k] = xpeek4(r, k * ps + lo);
+        if (pending >> k & 1u) w[k] = xpeek4(r, k * ps + lo);
 #pragma unroll
       for (int k = 0; k < NK; ++k)
-        if ((pending >> k & 1u) && xok4(x[k], tag)) {
-          w[k] = x[k];
-          pending &= ~(1u << k);
-        }
+        if ((pending >> k & 1u) && xok4(w[k], tag)) pending &= ~(1u << k);
     }
   }
   float4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = {0.0f, 0.0f, 0.0f, 0.0f};
