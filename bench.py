@@ -195,6 +195,7 @@ PHASES["fused"] = [(1, "coarse gates (last f of both sub-tensors) done, own y_c 
 SIDE = {"persistent": [(23, "mirror 0: its coarse rows' products with y_f published"),
                        (11, "unit 0: y_f in, fine rows' products started"),
                        (12, "unit 0: fine rows' words of the next step published")]}
+SIDE["fused"] = SIDE["persistent"]
 
 
 def phases(m, w, path: str, S: int, feat, n_steps: int) -> dict:
