@@ -142,6 +142,7 @@ struct BatchArgs {
 
 // One GEMM of the conditioning CNN: dst[m][n] (epilogue) over
 // acc = sum_k A[m][k] W[n][k], n < N, on 128 x 128 tiles.
+#define WR_CNN_MAXB 64   // sub-tensors of a streamed CNN run at most
 struct CnnGemmArgs {
   const float* src;       // activations [M][kin]
   int kin;                // source row width (a multiple of 32)
@@ -164,6 +165,13 @@ struct CnnGemmArgs {
                           // workgroup (tile, q) writes g_q to part[q] and wr_cnn_reduce adds them in order
   float* part;            // [groups][M][N] (split > 1)
   int tiles_m, tiles, per_xcd;   // 128-row tiles, all tiles, tiles x split per XCD slot
+  // Streamed runs (rng = 1): block b of the run is (utterance b / B, sub-tensor out_s0 + b % B); its
+  // row k is utterance row lo[s] + k, and only rows below hi[s] are computed (the others are read as
+  // zero and not stored).  With src_abs (dst_abs) the source (destination) is a whole-utterance array
+  // [U][out_B][rows_utt][width] at that row (taps past rows_utt read zero); otherwise it is indexed by
+  // the run's row m.
+  int rng, src_abs, dst_abs;
+  int lo[WR_CNN_MAXB], hi[WR_CNN_MAXB];
 };
 #define CNN_TM 128
 #define CNN_TN 128
@@ -183,6 +191,8 @@ struct CnnInputArgs {
                           // (u, s - s0)
   int M, kin;
   float* x;               // [M][kin]
+  int rng;                // streamed run: block (u, s - s0)'s row k is utterance row lo[s] + k
+  int lo[WR_CNN_MAXB];
 };
 
 // Kernel entry points (taken by address in the launcher).

@@ -24,15 +24,34 @@
 
 namespace {
 
+// Streamed runs: the sub-tensor and the utterance row of run row m (see CnnGemmArgs).
+__device__ __forceinline__ int cnn_rng_row(const CnnGemmArgs& a, int m, int* s, int* blk) {
+  const int b = m / a.rows;
+  *s = a.out_s0 + b % a.B;
+  *blk = (b / a.B) * a.out_B + *s;                  // (utterance, sub-tensor) of the whole-utterance arrays
+  return a.lo[*s] + m % a.rows;
+}
+
 // A's piece of thread t for K-step kt: row t / 4 of the tile, inputs 8 (t % 4) .. +7 of the step.
 __device__ __forceinline__ void cnn_load(const CnnGemmArgs& a, int m0, int n0, int kt, float4* x, uint4* wv) {
   const int t = threadIdx.x, row = t >> 2, oct = t & 3;
   const int m = m0 + row;
   const int kbase = kt * 32, tap = kbase / a.kin, col = kbase % a.kin + 8 * oct;
-  const int kb = m % a.rows + tap * a.dil;           // row within the block of the tap
-  const int64_t q = a.row0 + (int64_t)((m / a.rows) % a.B) * a.row_step + kb;   // its utterance row
-  if (m < a.M && kb < a.rows && q < a.rows_utt) {
-    const float4* p = (const float4*)(a.src + (size_t)(m + tap * a.dil) * a.kin + col);
+  bool ok;
+  size_t sr;                                         // source row
+  if (a.rng) {
+    int s = 0, blk = 0;
+    const int q = m < a.M ? cnn_rng_row(a, m, &s, &blk) + tap * a.dil : 0;   // the tap's utterance row
+    ok = m < a.M && q < a.rows_utt;
+    sr = a.src_abs ? (size_t)blk * a.rows_utt + q : (size_t)m;
+  } else {
+    const int kb = m % a.rows + tap * a.dil;         // row within the block of the tap
+    const int64_t q = a.row0 + (int64_t)((m / a.rows) % a.B) * a.row_step + kb;   // its utterance row
+    ok = m < a.M && kb < a.rows && q < a.rows_utt;
+    sr = (size_t)(m + tap * a.dil);
+  }
+  if (ok) {
+    const float4* p = (const float4*)(a.src + sr * a.kin + col);
     x[0] = p[0];
     x[1] = p[1];
   } else {
@@ -89,8 +108,16 @@ __device__ __forceinline__ void cnn_store(const CnnGemmArgs& a, int m0, int n0, 
           part[(size_t)m * a.N + n] = v[i][j][r];
           continue;
         }
-        const int blk = m / a.rows;
-        const size_t dm = (size_t)((blk / a.B) * a.out_B + a.out_s0 + blk % a.B) * a.rows + m % a.rows;
+        size_t dm;
+        if (a.rng) {
+          int s, b2;
+          const int q = cnn_rng_row(a, m, &s, &b2);
+          if (q >= a.hi[s]) continue;                  // not a row of this run
+          dm = a.dst_abs ? (size_t)b2 * a.rows_utt + q : (size_t)m;
+        } else {
+          const int blk = m / a.rows;
+          dm = (size_t)((blk / a.B) * a.out_B + a.out_s0 + blk % a.B) * a.rows + m % a.rows;
+        }
         float* d = a.dst + dm * a.N + n;
         const float x = v[i][j][r] + bn;
         *d = a.epi == 0 ? x : a.epi == 1 ? wr_relu(x) : *d + x;
@@ -156,8 +183,16 @@ __global__ void wr_cnn_reduce(CnnGemmArgs a) {
   const int m = (int)(idx / a.N), n = (int)(idx % a.N);
   float v = a.part[idx];
   for (int q = 1; q < a.split; ++q) v = v + a.part[(size_t)q * a.M * a.N + idx];
-  const int blk = m / a.rows;
-  const size_t dm = (size_t)((blk / a.B) * a.out_B + a.out_s0 + blk % a.B) * a.rows + m % a.rows;
+  size_t dm;
+  if (a.rng) {
+    int s, b2;
+    const int q = cnn_rng_row(a, m, &s, &b2);
+    if (q >= a.hi[s]) return;                        // not a row of this run
+    dm = a.dst_abs ? (size_t)b2 * a.rows_utt + q : (size_t)m;
+  } else {
+    const int blk = m / a.rows;
+    dm = (size_t)((blk / a.B) * a.out_B + a.out_s0 + blk % a.B) * a.rows + m % a.rows;
+  }
   float* d = a.dst + dm * a.N + n;
   const float x = v + a.bias[n];
   *d = a.epi == 0 ? x : a.epi == 1 ? wr_relu(x) : *d + x;
@@ -175,7 +210,7 @@ __global__ void wr_cnn_input(CnnInputArgs a) {
   if (idx >= (int64_t)a.M * a.kin) return;
   const int m = (int)(idx / a.kin), ch = (int)(idx % a.kin);
   const int k = m % a.win, s = a.s0 + (m / a.win) % a.nsb, u = m / a.win / a.nsb, z = ch >> 1;
-  const int64_t q = a.row0 + (int64_t)s * a.row_step + k;
+  const int64_t q = a.rng ? (int64_t)a.lo[s] + k : a.row0 + (int64_t)s * a.row_step + k;
   float v = 0.0f;
   if (z < s && q >= 0 && q < a.rows && q <= a.front0 + (int64_t)z * a.front_step) {
     const int smp = a.seq[(size_t)u * a.n_samples + (size_t)a.B * q + z];

@@ -120,6 +120,8 @@ struct wavernn_model {
     int64_t cap = 0;                   // activation rows the buffers hold
     float* part = nullptr;             // per-group partial products of split GEMMs
     int64_t part_cap = 0;              // floats
+    float* rfull = nullptr;            // streamed sampling: residual activations [U][B][rows][Rc]
+    int64_t rfull_cap = 0;             // floats
   } cnn;
   bool has_cnn = false;
   int64_t cnn_chunk = 0, cnn_win = 0;   // sampling: steps per chunk, CNN window rows
@@ -872,10 +874,25 @@ int cnn_split(int M, int N, int K) {
   return tiles < 256 && groups > 1 ? groups : 1;
 }
 
+// A streamed run's rows (see CnnGemmArgs::rng): sub-tensor s's run rows are its utterance rows
+// lo[s] .. hi[s] - 1; whole-utterance source and destination arrays where src_abs / dst_abs.
+struct CnnRng {
+  const int* lo;
+  const int* hi;
+  int src_abs, dst_abs;
+};
+
 wavernn_status cnn_gemm(const float* src, int kin, int taps, int dil, int rows, const CnnRows& cr, int M,
                         const uint4* w, const float* bias, int N, float* dst, int epi, hipStream_t st,
-                        float* part = nullptr, int out_B = 0, int out_s0 = 0) {
+                        float* part = nullptr, int out_B = 0, int out_s0 = 0, const CnnRng* rng = nullptr) {
   CnnGemmArgs g;
+  memset(&g, 0, sizeof g);
+  if (rng) {
+    g.rng = 1;
+    g.src_abs = rng->src_abs;
+    g.dst_abs = rng->dst_abs;
+    for (int s = 0; s < WR_CNN_MAXB; ++s) g.lo[s] = rng->lo[s], g.hi[s] = rng->hi[s];
+  }
   g.src = src;
   g.kin = kin;
   g.taps = taps;
@@ -944,6 +961,7 @@ wavernn_status run_cnn(wavernn_model* m, int U, const uint16_t* seq, int64_t n_s
     }
   }
   CnnInputArgs in;
+  memset(&in, 0, sizeof in);
   in.seq = seq;
   in.n_samples = n_samples;
   in.B = B;
@@ -977,6 +995,129 @@ wavernn_status run_cnn(wavernn_model* m, int U, const uint16_t* seq, int64_t n_s
       return s;
   }
   return cnn_gemm(C.r, C.Rc, 1, 0, win, cr, M, C.w + C.woff[i], C.bias + C.boff[i], Dx, out, 0, st, C.part, B, s0);
+}
+
+// The conditioning CNN streamed over a sampling call (Sec. 4.2: the
+// conditioning runs ahead of the sampler).  Level 0 is the input layer,
+// levels 1 .. L the dilated layers, level L + 1 the output layer; before the
+// chunk that starts at step t0, level v of sub-tensor s is final below row
+// cnn_front(v, s, t0): the input rows of s hold the samples of the sub-tensors
+// z < s, made below row t0 - z (F + 1), and a level-v row reads input rows up
+// to its reach.  Each chunk computes every level's newly final rows once (from
+// lo[v][s], then lo[v][s] = the front), the dilated layers in place in a
+// whole-utterance residual array (a layer's convolution reads every row it
+// needs before its projection updates any), and writes the output rows into
+// the whole-utterance context table out [U][B][rows][Dx].  A row is computed
+// with the arithmetic of a windowed run, so the table, and the samples, do not
+// depend on the chunking.
+int64_t cnn_front(const int* reach, int v, int s, int64_t t0, int F, int64_t rows) {
+  int64_t f0 = t0 - (int64_t)(s - 1) * (F + 1);   // rows below f0: made by sub-tensor s - 1 (and so every z < s)
+  if (f0 >= rows) return rows;                      // (past the utterance the taps are zero: final too)
+  if (f0 < 0) f0 = 0;
+  const int64_t f = f0 - reach[v];
+  return f > 0 ? f : 0;
+}
+
+wavernn_status run_cnn_stream(wavernn_model* m, int U, const uint16_t* seq, int64_t n_samples, int64_t t0, int F,
+                              int (*lo)[WR_CNN_MAXB], float* out, hipStream_t st) {
+  auto& C = m->cnn;
+  const int B = m->cfg.subscale, Dx = m->cfg.ctx_dim, L = C.layers;
+  const int64_t rows = n_samples / B;
+  int reach[2 * 32 + 2];
+  reach[0] = 0;
+  for (int l = 1; l <= L; ++l) reach[l] = reach[l - 1] + (2 << ((l - 1) % 5));
+  reach[L + 1] = reach[L];
+  // the whole-utterance residual array (an allocation only when a call needs more rows than any before)
+  const int64_t rf = (int64_t)U * B * rows * C.Rc;
+  if (rf > C.rfull_cap) {
+    HIPOK(hipStreamSynchronize(st));
+    wavernn_status s;
+    if ((s = m->alloc(&C.rfull, (size_t)rf * 4)) != WAVERNN_OK) return s;
+    C.rfull_cap = rf;
+  }
+  for (int v = 0; v <= L + 1; ++v) {
+    int hi[WR_CNN_MAXB] = {}, a = -1, b = -1, n = 0;
+    for (int s = 0; s < B; ++s) {
+      hi[s] = (int)cnn_front(reach, v, s, t0, F, rows);
+      if (hi[s] < lo[v][s]) hi[s] = lo[v][s];
+      if (hi[s] > lo[v][s]) {
+        if (a < 0) a = s;
+        b = s;
+        n = std::max(n, hi[s] - lo[v][s]);
+      }
+    }
+    if (a < 0) continue;
+    const int nsb = b - a + 1;
+    const int64_t M64 = (int64_t)U * nsb * n;
+    if (M64 > (1 << 28)) return fail(WAVERNN_E_INVALID, "conditioning CNN: %lld rows, above 2^28", (long long)M64);
+    const int M = (int)M64;
+    if (M > C.cap) {   // the run's transient rows
+      HIPOK(hipStreamSynchronize(st));
+      wavernn_status s;
+      if ((s = m->alloc(&C.x, (size_t)M * C.kin * 4)) != WAVERNN_OK) return s;
+      if ((s = m->alloc(&C.r, (size_t)M * C.Rc * 4)) != WAVERNN_OK) return s;
+      if ((s = m->alloc(&C.act, (size_t)M * C.Cc * 4)) != WAVERNN_OK) return s;
+      C.cap = M;
+    }
+    {
+      int64_t need = 0;
+      const int KN[4][2] = {{C.kin, C.Rc}, {3 * C.Rc, C.Cc}, {C.Cc, C.Rc}, {C.Rc, Dx}};
+      for (auto& kn : KN) {
+        const int sp = cnn_split(M, kn[1], kn[0]);
+        if (sp > 1) need = std::max(need, (int64_t)sp * M * kn[1]);
+      }
+      if (need > C.part_cap) {
+        HIPOK(hipStreamSynchronize(st));
+        wavernn_status s;
+        if ((s = m->alloc(&C.part, (size_t)need * 4)) != WAVERNN_OK) return s;
+        C.part_cap = need;
+      }
+    }
+    const CnnRows cr{nsb, 0, 0, rows};
+    wavernn_status s;
+    if (v == 0) {   // input rows, then r = Win x + bin into the residual array
+      CnnInputArgs in;
+      memset(&in, 0, sizeof in);
+      in.seq = seq;
+      in.n_samples = n_samples;
+      in.B = B;
+      in.rows = rows;
+      in.win = n;
+      in.front0 = t0 - 1;
+      in.front_step = -(int64_t)(F + 1);
+      in.s0 = a;
+      in.nsb = nsb;
+      in.M = M;
+      in.kin = C.kin;
+      in.x = C.x;
+      in.rng = 1;
+      for (int z = 0; z < WR_CNN_MAXB; ++z) in.lo[z] = lo[0][z];
+      void* args[] = {&in};
+      const int64_t nx = (int64_t)M * C.kin;
+      HIPOK(hipLaunchKernel(wr_cnn_input_ptr(), dim3((unsigned)((nx + 255) / 256)), dim3(256), args, 0, st));
+      const CnnRng rg{lo[0], hi, 0, 1};
+      if ((s = cnn_gemm(C.x, C.kin, 1, 0, n, cr, M, C.w + C.woff[0], C.bias + C.boff[0], C.Rc, C.rfull, 0, st,
+                        C.part, B, a, &rg)) != WAVERNN_OK)
+        return s;
+    } else if (v <= L) {   // layer v: convolution from the residual array, projection added back into it
+      const size_t i = 1 + 2 * (size_t)(v - 1);
+      const CnnRng conv{lo[v], hi, 1, 0}, proj{lo[v], hi, 0, 1};
+      if ((s = cnn_gemm(C.rfull, C.Rc, 3, 1 << ((v - 1) % 5), n, cr, M, C.w + C.woff[i], C.bias + C.boff[i], C.Cc,
+                        C.act, 1, st, C.part, B, a, &conv)) != WAVERNN_OK)
+        return s;
+      if ((s = cnn_gemm(C.act, C.Cc, 1, 0, n, cr, M, C.w + C.woff[i + 1], C.bias + C.boff[i + 1], C.Rc, C.rfull, 2,
+                        st, C.part, B, a, &proj)) != WAVERNN_OK)
+        return s;
+    } else {   // output rows into the whole-utterance table
+      const size_t i = 1 + 2 * (size_t)L;
+      const CnnRng o{lo[v], hi, 1, 1};
+      if ((s = cnn_gemm(C.rfull, C.Rc, 1, 0, n, cr, M, C.w + C.woff[i], C.bias + C.boff[i], Dx, out, 0, st, C.part,
+                        B, a, &o)) != WAVERNN_OK)
+        return s;
+    }
+    for (int z = 0; z < B; ++z) lo[v][z] = hi[z];
+  }
+  return WAVERNN_OK;
 }
 
 // Bias + conditioning table cb[s][f][3H] for n_streams streams of n_frames frames.
@@ -1464,30 +1605,34 @@ wavernn_status run_batch(wavernn_model* m, const RunIO& io) {
     return launch(0, steps, io.init, io.fin);   // (scoring runs whole calls only)
   }
   // Sampling: chunks of LC = F - R + 1 steps (R the CNN's reach in rows).
-  // Before chunk [t0, t0 + LC) the CNN runs on windows of LC + R rows, lane s
-  // from its position t0 - s (F + 1) on: sub-tensor z < s has made its rows up
-  // to t0 - 1 - z (F + 1), which covers the window's first LC rows with their
-  // reach (Sec. 4.2: the conditioning runs ahead by a chosen number of
-  // samples; the lag between sub-tensors pays for it).
-  const int64_t LC = m->cnn_chunk, W = m->cnn_win;
+  // Before chunk [t0, t0 + LC) sub-tensor z < s has made its rows up to
+  // t0 - 1 - z (F + 1), which covers the next LC rows of sub-tensor s (from its
+  // position t0 - s (F + 1)) with their reach (Sec. 4.2: the conditioning runs
+  // ahead by a chosen number of samples; the lag between sub-tensors pays for
+  // it).  The CNN is streamed (run_cnn_stream): each chunk computes the rows
+  // of every layer that have become final, into a whole-utterance table.  The
+  // call's first chunk starts every level at the first position the call runs.
+  if (SB > WR_CNN_MAXB || m->cnn.layers + 2 > 2 * 32 + 2)
+    return fail(WAVERNN_E_UNSUPPORTED, "streamed CNN: at most %d sub-tensors and 64 layers", WR_CNN_MAXB);
+  const int64_t LC = m->cnn_chunk;
+  {
+    hipStream_t s0s = io.st;
+    if ((st = grow_ctab(m, (size_t)V * rows * m->cfg.ctx_dim, &s0s)) != WAVERNN_OK) return st;
+  }
   a.ctab = m->d_ctab;
-  a.ctab_rows = W;
-  a.ctab_step = -(int64_t)(F + 1);
+  a.ctab_rows = rows;
+  a.ctab_row0 = 0;
+  a.ctab_step = 0;
+  int lo[2 * 32 + 2][WR_CNN_MAXB];
+  for (int v = 0; v < m->cnn.layers + 2; ++v)
+    for (int s = 0; s < WR_CNN_MAXB; ++s) {
+      const int64_t p = s0 - (int64_t)s * (F + 1);
+      lo[v][s] = (int)(s < SB ? std::min<int64_t>(std::max<int64_t>(p, 0), rows) : 0);
+    }
   int cur = 0;
   for (int64_t t0 = s0; t0 < s1; t0 += LC) {
     const int64_t n = std::min(LC, s1 - t0);
-    // only the sub-tensors that make a position in this chunk (a contiguous
-    // range: the lag grows with s); an idle lane's table rows are never used
-    int s_lo = SB, s_hi = -1;
-    for (int s = 0; s < SB; ++s) {
-      const int64_t p0 = t0 - (int64_t)s * (F + 1);
-      if (p0 + n > 0 && p0 < a.rows) s_lo = std::min(s_lo, s), s_hi = s;
-    }
-    if (s_hi >= s_lo &&
-        (st = run_cnn(m, io.S, io.out, io.T, (int)W, t0, -(int64_t)(F + 1), t0 - 1, -(int64_t)(F + 1), m->d_ctab,
-                      io.st, s_lo, s_hi - s_lo + 1)) != WAVERNN_OK)
-      return st;
-    a.ctab_row0 = t0;
+    if ((st = run_cnn_stream(m, io.S, io.out, io.T, t0, F, lo, m->d_ctab, io.st)) != WAVERNN_OK) return st;
     const bool last = t0 + n >= s1;
     const wavernn_state* in = t0 == s0 ? io.init : &m->cnn_state[cur];
     const wavernn_state* out = last ? io.fin : &m->cnn_state[cur ^ 1];
