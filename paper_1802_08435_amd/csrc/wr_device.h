@@ -128,6 +128,15 @@ __device__ __forceinline__ xw xpeek(const xw* p) {
 }
 __device__ __forceinline__ bool xok(xw w, uint32_t tag) { return ((w ^ tag) & 1u) == 0; }
 __device__ __forceinline__ float xval(xw w) { return __uint_as_float(w & ~1u); }
+// A word that only workgroups on the writer's own XCD read (`local`, see
+// leads_share_xcd) is published with a plain store: it stays in that XCD's L2,
+// where the readers' coherent loads find it, a shorter hop than a store
+// written through to memory.  Otherwise as xpub.
+__device__ __forceinline__ void xpub_l(xw* p, uint32_t tag, float v, bool local) {
+  const xw w = (__float_as_uint(v) & ~1u) | (tag & 1u);
+  if (local) __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  else __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 // Two adjacent words (p 8-byte aligned) written and read as one 64-bit access.
 __device__ __forceinline__ void xpub2(xw* p, uint32_t tag, float v0, float v1) {
   const uint64_t w = (uint64_t)((__float_as_uint(v0) & ~1u) | (tag & 1u)) |

@@ -9,7 +9,9 @@
 // (the dense plan) each mirror waits for the coarse partials, publishes its
 // words of the coarse rows for the next step and waits for the fine partials;
 // the heads wait for those words at the start of a step, and the fine words
-// and fine partials sit in the sampling kernel's two buffers.  The time per
+// and fine partials sit in the sampling kernel's two buffers; the partials and
+// the mirrors' words stay in the L2 of the leads' XCD when all leads share
+// one, as in the sampling kernels.  The time per
 // step of this kernel is what the exchange pattern alone costs (Sec. 2.1 of
 // the paper counts such a synchronization cost per step).
 #include "wr_kern.h"
@@ -36,6 +38,8 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
   xw* PF = a.xc + P.x_pf;
   if (tid == 0) misc[0] = 0;
   __syncthreads();
+  const bool lx = WR_LOCAL_XCHG && P.x_xcc &&
+                  leads_share_xcd(a.xc + P.x_xcc, P.NH + P.NM, j, misc + 4, a);
   // with mirrors: wait for their words of the coarse rows (3 per unit)
   auto mirror_words = [&](uint32_t tag) {
     if (P.NM == 0 || tid >= Hh) return;
@@ -75,7 +79,7 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
     if (coarse) mirror_words(tag);
     if (coarse && wave == 7)
       for (int i = lane; i < HR; i += 64) xpub(YC + HR * jk + i, tag, 0.0f);
-    if (coarse && lane < 32) xpub(PC + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f);
+    if (coarse && lane < 32) xpub_l(PC + (size_t)jk * P.x_ps + 32 * wave + lane, tag, 0.0f, lx);
     if (coarse) gate_words(GA);   // (read while the partials are exchanged, as the sampling heads prefetch)
     gather(PC, tag);
     __syncthreads();
@@ -84,7 +88,7 @@ __device__ __forceinline__ void floor_head(const PersistArgs& a, int j, unsigned
       for (int i = lane; i < HR; i += 64) xpub(YF + HR * jk + i, tag, 0.0f);
     xw* PFt = PF + wr_dbuf(t, P.x_pfs);
     const uint32_t ftag = wr_dtag(t, P.x_pfs);
-    if (fine && lane < 32) xpub(PFt + (size_t)jk * P.x_ps + 32 * wave + lane, ftag, 0.0f);
+    if (fine && lane < 32) xpub_l(PFt + (size_t)jk * P.x_ps + 32 * wave + lane, ftag, 0.0f, lx);
     if (fine) gate_words(GF + wr_dbuf(t, P.x_gfs));
     gather(PFt, ftag);
     __syncthreads();
@@ -119,13 +123,14 @@ __device__ __forceinline__ void floor_mirror(const PersistArgs& a, int j, unsign
     if (!sum_parts<16>(src, P.x_ps, hh ? h0 : 0, hh ? NK : h0, v, tag, &s, a)) misc[0] = 1;
     else zs[hh * 256 + v] = s;
   };
-  if (tid < MRW) xpub(HF + tid, 1u, 0.0f);
+  const bool lx = WR_LOCAL_XCHG && leads_share_xcd(a.xc + P.x_xcc, P.NH + P.NM, P.NH + j, misc + 4, a);
+  if (tid < MRW) xpub_l(HF + tid, 1u, 0.0f, lx);
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
     gather(PC, tag);
     __syncthreads();
     if (misc[0]) return;
-    if (t + 1 < a.T && tid < MRW) xpub(HF + tid, tag + 1, 0.0f);
+    if (t + 1 < a.T && tid < MRW) xpub_l(HF + tid, tag + 1, 0.0f, lx);
     {   // the fine rows' words of step t (read without waiting, while the fine partials are exchanged)
       const xw* G = GF + wr_dbuf(t, P.x_gfs);
       float acc = 0.0f;

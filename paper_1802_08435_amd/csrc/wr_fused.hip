@@ -154,12 +154,13 @@ __device__ __forceinline__ void fused_head_role(const PersistArgs& a, int j, uns
     __syncthreads();
   };
   // second layer: class tile `wave` (< 4) over this head's HR columns -> 16 of the 64 partials
+  bool lx = false;   // all heads on one XCD: partials published into its L2
   auto second_layer = [&](const bf16x8* W, xw* dst, uint32_t tag) {
     if (wave >= 4) return;
     f32x4 A = {0, 0, 0, 0};
 #pragma unroll
     for (int kt = 0; kt < KO; ++kt) A = mfma(afrag(imo, kt), W[kt], A);
-    if (lane < 16) xpub(dst + 16 * wave + lane, tag, mfma_row(A));
+    if (lane < 16) xpub_l(dst + 16 * wave + lane, tag, mfma_row(A), lx);
   };
   // the draw wave: lane l sums partial l of every head (in head order, as
   // every head does) once all carry `tag`; the first probe waits a little
@@ -223,6 +224,7 @@ __device__ __forceinline__ void fused_head_role(const PersistArgs& a, int j, uns
     fe = v[2];
     fie = last4(2);
   };
+  if (WR_LOCAL_XCHG) lx = leads_share_xcd(a.xc + P.x_xcc, P.NH, j, misc + 8, a);
   coarse_pre(1u, fscale(misc[4]), fscale(misc[5]), 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();

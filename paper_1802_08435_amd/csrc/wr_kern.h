@@ -222,3 +222,37 @@ template <class A>
 __device__ __forceinline__ void trace_at(const A& a, int64_t t, int slot) {
   if (a.trace && t < a.trace_steps) a.trace[t * WR_TRACE_SLOTS + slot] = wr_clock();
 }
+
+// Words that only the lead workgroups read (partial logits, the mirrors'
+// words) are published into the L2 of their XCD when all leads share one
+// (build with WR_LOCAL_XCHG=0 to keep every word coherent across XCDs).
+#ifndef WR_LOCAL_XCHG
+#define WR_LOCAL_XCHG 1
+#endif
+// Do all n lead workgroups of a launch (the heads and mirrors of a batch-1
+// grid, placed on one XCD) run on one XCD?  Lead i publishes its XCD (the
+// XCC_ID hardware register) in words[i] and thread 0 reads every lead's; all
+// leads read the same words, so all get the same answer.  Called by every
+// thread of the workgroup (one barrier inside; flag: an LDS int).  A wait
+// that expires flags the launch's error word and answers no.
+template <class A>
+__device__ __forceinline__ bool leads_share_xcd(xw* words, int n, int i, int* flag, const A& a) {
+  if (threadIdx.x == 0) {
+    const unsigned x = __builtin_amdgcn_s_getreg((3 << 11) | 20) & 15u;   // XCC_ID, bits 3:0
+    __hip_atomic_store(words + i, 0x100u | x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int same = 1;
+    WaitBudget wb{wr_clock(), 0};
+    for (int k = 0; k < n && same; ++k) {
+      xw w;
+      while (!((w = xpeek(words + k)) & 0x100u))
+        if (!wait_ok(wb, a.err, a.limit, a.err)) {
+          same = 0;
+          break;
+        }
+      same = same && (w & 15u) == x;
+    }
+    *flag = same;
+  }
+  __syncthreads();
+  return *flag != 0;
+}

@@ -107,6 +107,7 @@ struct PersistPlan {
   int u_lds_w;            // unit LDS block: dense R tiles, or the block-sparse records
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_words;   // exchange regions (32-bit words)
   int x_hf;               // with mirrors: the coarse rows' products with y_f [3 Hh]
+  int x_xcc;              // the XCD of each head and mirror, published at the start
   int x_ps;               // words between the partial-logit blocks of consecutive heads
   int x_gfs, x_pfs;       // with mirrors the fine rows' words and the fine partial logits are
                           // double-buffered by step parity: words between the two buffers (0: one)
@@ -202,6 +203,7 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
   P->x_gfs = wr_rup(3 * P->Hh, WR_XALIGN);
   P->x_gf = take(2 * P->x_gfs);
   P->x_hf = take(3 * P->Hh);
+  P->x_xcc = take(P->NH + P->NM);
   P->x_ps = 256;
   P->x_pc = take(P->NH * P->x_ps);
   P->x_pfs = P->NH * P->x_ps;
@@ -220,7 +222,7 @@ WR_HD inline bool persist_plan(int H, PersistPlan* P) {
 WR_HD inline bool fused_plan(int H, PersistPlan* P) {
   if (!persist_plan(H, P)) return false;
   P->NM = P->mw_frags = P->lds_m = 0;             // no mirrors: single-buffered words
-  P->x_hf = P->x_gfs = P->x_pfs = 0;
+  P->x_hf = P->x_gfs = P->x_pfs = P->x_xcc = 0;
   wr_place(P, 0, 255);
   P->hw_frags = 2 * P->KH + 2 * P->KO;
   // head LDS: y_c and y_f operand images (KT fragments each), relu image (KO),
@@ -235,6 +237,7 @@ WR_HD inline bool fused_plan(int H, PersistPlan* P) {
   P->x_ps = 64;
   P->x_pc = take(P->NH * P->x_ps);
   P->x_pf = take(P->NH * P->x_ps);
+  P->x_xcc = take(P->NH);
   P->x_words = o;
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024;
@@ -293,7 +296,7 @@ WR_HD inline bool sparse_plan(int H, int SR, int BH, int BW, int NRC, int NRF, P
   P->NCT = 3 * P->Hh / 16;
   P->NU = 3 * H / SR;
   P->NM = P->mw_frags = P->lds_m = 0;             // no mirrors: single-buffered words
-  P->x_hf = P->x_gfs = P->x_pfs = 0;
+  P->x_hf = P->x_gfs = P->x_pfs = P->x_xcc = 0;
   P->hw_frags = P->KH + 2 * P->KO;
   // head LDS: operand image (KT + KO fragments), first-layer partials
   // [KC][HR], logit sums [2][256], logits [256], then y [Hh] (GU = 1) or
@@ -317,6 +320,7 @@ WR_HD inline bool sparse_plan(int H, int SR, int BH, int BW, int NRC, int NRF, P
   P->x_ps = 256;
   P->x_pc = take(P->NK * P->x_ps);
   P->x_pf = take(P->NK * P->x_ps);
+  P->x_xcc = take(P->NH);
   P->x_words = o;
   P->lds = P->lds_h > P->lds_u ? P->lds_h : P->lds_u;
   return P->lds <= 160 * 1024 && P->grid <= 256;

@@ -251,6 +251,7 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     __syncthreads();
   };
   // second layer: class tiles 2*wave, 2*wave+1 over this head's HR columns
+  bool lx = false;   // heads (and mirrors) share one XCD (leads_share_xcd)
   auto second_layer = [&](const bf16x8* W, xw* dst, uint32_t tag) {
     f32x4 A = {0, 0, 0, 0}, B = {0, 0, 0, 0};
 #pragma unroll
@@ -260,8 +261,8 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       B = mfma(x, W[KO + kt], B);
     }
     if (lane < 16) {
-      xpub(dst + 32 * wave + lane, tag, mfma_row(A));
-      xpub(dst + 32 * wave + 16 + lane, tag, mfma_row(B));
+      xpub_l(dst + 32 * wave + lane, tag, mfma_row(A), lx);
+      xpub_l(dst + 32 * wave + 16 + lane, tag, mfma_row(B), lx);
     }
   };
   // partial logits of all slices: thread (v, half) sums its half of the
@@ -426,6 +427,9 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
       if ((unsigned)(un - HR * jk) < (unsigned)HR) xpub(Y + un, tag, hn);   // this head's slice, for the units
     }
   };
+  // before step 0's coarse gates, which wait for the mirrors' first words:
+  // the mirrors check the XCDs before they publish those
+  if (WR_LOCAL_XCHG && P.x_xcc) lx = leads_share_xcd(a.xc + P.x_xcc, P.NH + P.NM, j, misc + 4, a);
   coarse_pre(1u, fscale(misc[2]), a.t0);
   // Every prologue load has landed: no wait inside the loop is left waiting on
   // them (a wait there would also wait for the wave's outstanding stores).
@@ -667,6 +671,7 @@ __device__ __forceinline__ void mirror_role(const PersistArgs& a, int j, unsigne
   if (wave == DW) fill_batch(0, 0);
   __syncthreads();
   if (gate) aput(imf + (u >> 5) * WR_FRAG, u & 31, xround(hf));
+  bool lx = false;   // heads and mirrors share one XCD (leads_share_xcd)
   // the coarse rows' products with y_f for step s, published for the heads
   auto products = [&](int64_t s) {
     f32x4 acc[3];
@@ -683,10 +688,11 @@ __device__ __forceinline__ void mirror_role(const PersistArgs& a, int j, unsigne
       for (int r = 0; r < 3; ++r) part[kh * MRW + 16 * (3 * rq + r) + lane] = mfma_row(acc[r]);
     }
     __syncthreads();
-    if (tid < MRW) xpub(HF + tid, (uint32_t)s + 1u, part[tid] + part[MRW + tid]);
+    if (tid < MRW) xpub_l(HF + tid, (uint32_t)s + 1u, part[tid] + part[MRW + tid], lx);
   };
   __builtin_amdgcn_s_waitcnt(0);   // prologue loads in before the loop (see head_role)
   __syncthreads();
+  if (WR_LOCAL_XCHG) lx = leads_share_xcd(a.xc + P.x_xcc, P.NH + P.NM, P.NH + j, misc + 4, a);
   products(0);
   float fu = 0.0f, fr = 0.0f, fe = 0.0f, fie = 0.0f, cbe = 0.0f;
   for (int64_t t = 0; t < a.T; ++t) {
