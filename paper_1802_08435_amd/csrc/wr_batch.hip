@@ -91,6 +91,7 @@ __device__ __forceinline__ T* opaque(T* p) {
 template <int N, class O, class F>
 __device__ __forceinline__ bool poll_put(const xw* base, O off, F put, uint32_t tag, const BatchArgs& a,
                                          uint32_t need = ~0u) {
+  static_assert(N <= 32, "one pending bit per word");
   uint32_t pending = (N >= 32 ? ~0u : (1u << N) - 1u) & need;
   WaitBudget wb{wr_clock(), 0};
   for (;;) {
@@ -113,7 +114,8 @@ __device__ __forceinline__ bool poll_put(const xw* base, O off, F put, uint32_t 
 // put(k, first, second) for pair k at base + off(k) (off even).
 template <int N, class O, class F>
 __device__ __forceinline__ bool poll_put2(const xw* base, O off, F put, uint32_t tag, const BatchArgs& a) {
-  uint32_t pending = (1u << N) - 1u;
+  static_assert(N <= 32, "one pending bit per pair");
+  uint32_t pending = N >= 32 ? ~0u : (1u << N) - 1u;   // (a 32-bit shift by 32 is undefined)
   WaitBudget wb{wr_clock(), 0};
   for (;;) {
     const xw* b = opaque(base);
@@ -277,6 +279,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     __syncthreads();
   };
   // class tiles 2*wave, 2*wave+1 over this head's 64 columns, for all vectors
+  bool lx = false;   // the group's heads share one XCD: partials and classes into its L2
   auto second_layer = [&](const bf16x8* W, xw* dst, uint32_t tag) {
     f32x4 A = {0, 0, 0, 0}, B = {0, 0, 0, 0};
     if (!FL) {
@@ -288,10 +291,10 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
     }
     const int c0 = 32 * wave + (lane & 15);
     if (bl0 < L) {
-      xpub(dst + bl0 * 256 + c0, tag, mfma_row(A));
-      xpub(dst + (bl0 + 1) * 256 + c0, tag, mfma_row_hi(A));
-      xpub(dst + bl0 * 256 + c0 + 16, tag, mfma_row(B));
-      xpub(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B));
+      xpub_l(dst + bl0 * 256 + c0, tag, mfma_row(A), lx);
+      xpub_l(dst + (bl0 + 1) * 256 + c0, tag, mfma_row_hi(A), lx);
+      xpub_l(dst + bl0 * 256 + c0 + 16, tag, mfma_row(B), lx);
+      xpub_l(dst + (bl0 + 1) * 256 + c0 + 16, tag, mfma_row_hi(B), lx);
     }
   };
   // Vector ownership.  With 8 vectors per group head j draws the vectors j,
@@ -495,6 +498,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
   const bool own = wave < nown;                     // this wave draws an owned vector
   const bool writer = own && (!ALL || bw % NH == j); // ... and writes its outputs (one head per vector)
   const bool live = writer && v0 + bw < a.S;       // ... of a vector in use
+  if (WR_LOCAL_XCHG) lx = leads_share_xcd(X + P.x_xcc, P.NH, j, misc + 1, a);
 
   for (int64_t t = 0; t < a.T; ++t) {
     const uint32_t tag = (uint32_t)(t + 1);
@@ -565,7 +569,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
         int cw = c;                                 // the class word: an idle lane's last class
         if (act) misc[8 + bw] = c;
         else cw = misc[8 + bw];
-        if (!ALL) xpub(CC + bw, tag, (float)cw);
+        if (!ALL) xpub_l(CC + bw, tag, (float)cw, lx);
         if (a.nll_out) {
           fmisc[wave] = lse;
           fmisc[8 + wave] = zk[wave * 256 + c];
@@ -630,7 +634,7 @@ __device__ __forceinline__ void bhead_role(const BatchArgs& a, int g, int j, uns
           if (act) misc[24 + bw] = f;
           else fw = misc[24 + bw];
         }
-        if (!ALL) xpub(CF + bw, tag, (float)fw);
+        if (!ALL) xpub_l(CF + bw, tag, (float)fw, lx);
         // for later contexts; an idle lane publishes a word too (value unused)
         if (a.ux && writer) spub(X + P.x_sp, L, P.SS, bw, tag, act ? 256 * c + f : 0);
         if (live && act) {

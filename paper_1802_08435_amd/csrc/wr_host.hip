@@ -2114,11 +2114,14 @@ wavernn_status wavernn_tune(wavernn_model* m, int64_t n_steps, int32_t rounds, f
     m->solo_uxm = P.uxm;
     if (chosen) *chosen = k;
   }
-  if (e0) hipEventDestroy(e0);
-  if (e1) hipEventDestroy(e1);
-  hipStreamSynchronize(st);
-  if (out) hipFree(out);
-  if (cond) hipFree(cond);
+  // clean-up: the first failure is the one reported
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  const hipError_t se = hipStreamSynchronize(st);
+  if (s == WAVERNN_OK && se != hipSuccess)
+    s = fail(WAVERNN_E_HIP, "hipStreamSynchronize: %s", hipGetErrorString(se));
+  if (out) (void)hipFree(out);
+  if (cond) (void)hipFree(cond);
   return s;
 }
 

@@ -347,6 +347,7 @@ struct BatchPlan {
   int L;                  // vectors per group (2, 4 or 8)
   int hw_frags;           // head fragments per wave (as the batch-1 plan)
   int u_lds_w;            // unit LDS weights: [UCT][KT] coarse tiles, then [UCT][KT] fine tiles
+  int x_xcc;              // per group: the XCD of each head, published at the start
   int x_yc, x_yf, x_ga, x_gf, x_pc, x_pf, x_sp, x_xc, x_xf, x_cc, x_cf, x_words;   // per group: y [L][Hh],
       // g [3][Hh][L], p [NH][L][256], drawn samples [2][L], e-gate context terms [Hh][L] x 2,
       // drawn coarse and fine classes [L] each
@@ -409,6 +410,7 @@ WR_HD inline bool batch_plan(int H, int n_vectors, BatchPlan* P, int ctx_dim = 0
   P->x_xf = take(P->L * P->Hh);
   P->x_cc = take(P->L);
   P->x_cf = take(P->L);
+  P->x_xcc = take(P->NH);
   P->x_words = o;
   // head: operand images (2 KT + 2 fragments), first-layer partials [2][L][64],
   // logit sums [L][256], logits [L][256], both halves of h and the staged
