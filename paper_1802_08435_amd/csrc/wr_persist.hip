@@ -33,7 +33,9 @@ template <int NK>
 __device__ __forceinline__ bool gather_partials(const PersistArgs& a, const xw* src, uint32_t tag, float4* z) {
   constexpr int NHP = (NK + 1) / 2;
   const int lane = threadIdx.x & 63;
-  __builtin_amdgcn_s_sleep(6);
+  // first probe after 4 x 64 clocks (measured at H = 896 with the partials in
+  // the leads' L2: 2 or 4 best, 6 1.6% slower, 0 or 1 6% slower)
+  __builtin_amdgcn_s_sleep(4);
   const uint32_t bytes = (uint32_t)(NK * a.P.x_ps * 4), lo = 16u * lane, ps = (uint32_t)a.P.x_ps * 4u;
   xw4 w[NK];
   uint32_t pending = 0;
