@@ -12,6 +12,7 @@ kernel's tags:
   coarse-column words, the mirrors' words) hold the parity of step + 1;
 * double-buffered words (the units' fine-row words and the fine partial
   logits) of step s sit in buffer s mod 2 and hold the parity of s / 2 + 1.
+* the leads' XCD words are written once, at the start.
 
 A reader accepts a word whose bit matches, and the model then checks that the
 word was written for the awaited step: a match on another step is a misread.
@@ -25,7 +26,7 @@ import random
 import pytest
 
 
-def run(NH=3, NU=4, T=14, seed=0, pf_double=True, gf_double=True, max_ticks=2_000_000):
+def run(NH=3, NU=4, T=14, seed=0, pf_double=True, gf_double=True, heads_check_first=True, max_ticks=2_000_000):
     rng = random.Random(seed)
     NM = NH
     mem = {}
@@ -66,8 +67,21 @@ def run(NH=3, NU=4, T=14, seed=0, pf_double=True, gf_double=True, max_ticks=2_00
     def coarse_words(s):
         return [wait(GA(k, s), s) for k in range(NU)] + [wait(HF(m, s), s) for m in range(NM)]
 
+    # The XCD check at the start: every lead (head or mirror) publishes its
+    # XCD word once and reads every lead's before it uses local stores.
+    XC = lambda i: (("XC", i), 1)
+
+    def xcd_check(i):
+        yield pub(XC(i), 0)
+        for ii in range(NH + NM):
+            yield wait(XC(ii), 0)
+
     def head(j):
+        if heads_check_first:           # the kernel's order: before step 0's coarse gates
+            yield from xcd_check(j)
         yield from coarse_words(0)
+        if not heads_check_first:
+            yield from xcd_check(j)
         for s in range(T):
             yield pub(YC(j, s), s)
             yield pub(PC(j, s), s)
@@ -80,6 +94,7 @@ def run(NH=3, NU=4, T=14, seed=0, pf_double=True, gf_double=True, max_ticks=2_00
             yield from mixed([wait(PF(jj, s), s) for jj in range(NH)], nxt)
 
     def mirror(m):
+        yield from xcd_check(NH + m)    # before the words of step 0
         yield pub(HF(m, 0), 0)
         for s in range(T):
             yield from mixed([wait(PC(jj, s), s) for jj in range(NH)], [wait(GF(k, s), s) for k in range(NU)])
@@ -141,3 +156,14 @@ def test_the_model_catches_single_buffered_fine_words():
     the units publish fine words a mirror may not have read yet)."""
     assert any(run(seed=sd, pf_double=False) for sd in range(200))
     assert any(run(seed=sd, gf_double=False) for sd in range(200))
+
+
+def test_the_xcd_check_comes_before_any_wait_on_another_lead():
+    """The leads' XCD check (every head and mirror publishes its XCD, then
+    reads all of them) sits before a head's step-0 coarse gates, which wait
+    for the mirrors' first words, and before a mirror publishes those: no
+    interleaving deadlocks.  With the heads' check after their step-0 gates,
+    every interleaving deadlocks (the mirrors wait for the heads' XCD words,
+    the heads for the mirrors' words)."""
+    assert not [sd for sd in range(40) if run(seed=sd, T=4)]
+    assert all((run(seed=sd, T=4, heads_check_first=False) or "").startswith("deadlock") for sd in range(10))
