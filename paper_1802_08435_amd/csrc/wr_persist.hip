@@ -367,8 +367,9 @@ __device__ __forceinline__ void head_role(const PersistArgs& a, int j, unsigned 
     // the units publish these words at about the time this head starts to
     // wait for them, so the first probe goes out a little later (measured at
     // H = 896: 5.12 us per step, against 5.22 with the probe issued at the
-    // end of the fine gather)
-    __builtin_amdgcn_s_sleep(8);
+    // end of the fine gather).  With mirrors, whose words stay in the leads'
+    // L2, 5 x 64 clocks (3 to 5 best, 8 1.4% slower, 0 or 1 5% slower)
+    __builtin_amdgcn_s_sleep(MR ? 5 : 8);
     prefetch_coarse(n);
     const xw* ps[6] = {GA + u, GA + Hh + u, GA + 2 * Hh + u, HF + u, HF + Hh + u, HF + 2 * Hh + u};
     float v[NCW];
