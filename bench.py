@@ -251,7 +251,7 @@ def main() -> int:
                     help="only time the phases of one traced launch (in-kernel timestamps) and print them")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the benchmark runs on one GPU; --gpus {args.gpus} is not supported "
               "(utterances are independent: more GPUs would each run their own).", file=sys.stderr)
         return 2
 

@@ -55,7 +55,7 @@ extern "C" {
 typedef enum {
   WAVERNN_OK = 0,
   WAVERNN_E_INVALID = 1,      /* bad argument: null pointer, shape, size, range */
-  WAVERNN_E_UNSUPPORTED = 2,  /* valid request this build cannot run (e.g. grid cannot be co-resident) */
+  WAVERNN_E_UNSUPPORTED = 2,  /* valid request the library cannot run (e.g. grid cannot be co-resident) */
   WAVERNN_E_OOM = 3,          /* device allocation failed */
   WAVERNN_E_HIP = 4,          /* a HIP runtime call failed */
   WAVERNN_E_DEVICE = 5        /* the kernel reported a failure (wavernn_device_status) */
@@ -171,7 +171,7 @@ typedef struct wavernn_model wavernn_model;
 
 /* Validate cfg, copy and pack the weights to the current HIP device.
  * *out receives the model handle.  Errors: E_INVALID (null pointer, odd or
- * unsupported H, bad config field), E_UNSUPPORTED (no kernel of this build
+ * unsupported H, bad config field), E_UNSUPPORTED (no kernel of the library
  * serves the configuration), E_OOM, E_HIP. */
 wavernn_status wavernn_create(const wavernn_config* cfg, const wavernn_weights* w, wavernn_model** out);
 
